@@ -1,0 +1,338 @@
+/*
+ * ckv_oracle.c -- plain, slow, fp64 CPU oracle (TEST INFRASTRUCTURE ONLY).
+ *
+ * Only the tests, the smoke check and the benchmark's CPU-baseline leg may
+ * load this library.  It shares no code with the HIP path.  Every function
+ * below names the passage of the paper it follows; no blocking, fusion or
+ * reordering is done beyond what the definition states.
+ */
+#include "ckv_oracle.h"
+
+#include <math.h>
+#include <pthread.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* bf16 is the upper half of an IEEE-754 binary32; widening is exact. */
+double ckvref_bf16_to_f64(uint16_t bits) {
+  uint32_t u = (uint32_t)bits << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* Sec. 2.2, Sec. 4.1: the retrieval score of a position is the query's inner
+ * product with that position's landmark; the landmark of a position is its
+ * own key here.  A KV head is shared by the G query heads of its group and
+ * carries a single index set, so a position's score is the largest scaled
+ * logit among those G heads. */
+void ckvref_unit_scores(int G, int d, int n, const uint16_t* q,
+                        const uint16_t* keys, int64_t key_row_stride,
+                        float scale, double* S) {
+  const double sc = (double)scale;
+  for (int j = 0; j < n; ++j) {
+    const uint16_t* kr = keys + (int64_t)j * key_row_stride;
+    double best = -INFINITY;
+    for (int g = 0; g < G; ++g) {
+      double dot = 0.0;
+      for (int c = 0; c < d; ++c)
+        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);
+      double s = sc * dot;
+      if (s > best) best = s;
+    }
+    S[j] = best;
+  }
+}
+
+static _Thread_local const double* g_sort_scores;
+
+/* Order of the critical set: larger score first; equal scores keep the lower
+ * position first. */
+static int by_score_desc(const void* a, const void* b) {
+  int32_t i = *(const int32_t*)a, j = *(const int32_t*)b;
+  double si = g_sort_scores[i], sj = g_sort_scores[j];
+  if (si > sj) return -1;
+  if (si < sj) return 1;
+  return (i > j) - (i < j);
+}
+
+static int by_position(const void* a, const void* b) {
+  int32_t i = *(const int32_t*)a, j = *(const int32_t*)b;
+  return (i > j) - (i < j);
+}
+
+/* Sec. 2.2: only the important entries are retrieved, within the sparse
+ * budget k.  Full sort of all positions by the order above, keep the first
+ * m = min(k, n), then list them by ascending position. */
+int ckvref_unit_select(int n, const double* S, int k, int32_t* idx) {
+  int m = n < k ? n : k;
+  if (m < 0) m = 0;
+  if (n > 0) {
+    int32_t* order = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
+    for (int j = 0; j < n; ++j) order[j] = j;
+    g_sort_scores = S;
+    qsort(order, (size_t)n, sizeof(int32_t), by_score_desc);
+    qsort(order, (size_t)m, sizeof(int32_t), by_position);
+    memcpy(idx, order, sizeof(int32_t) * (size_t)m);
+    free(order);
+  }
+  for (int i = m; i < k; ++i) idx[i] = -1;
+  return m;
+}
+
+/* Sec. 5.3 / Sec. 5.4: the attention of the decoding token runs over exactly
+ * the assembled sparse set.  Naive max-shifted softmax over the m logits,
+ * then the probability-weighted sum of the value rows. */
+void ckvref_unit_attn(int G, int d, int m, const uint16_t* q,
+                      const uint16_t* k_rows, const uint16_t* v_rows,
+                      float scale, double* out, double* p) {
+  const double sc = (double)scale;
+  double* logit = (double*)malloc(sizeof(double) * (size_t)(m > 0 ? m : 1));
+  for (int g = 0; g < G; ++g) {
+    double* o = out + (int64_t)g * d;
+    for (int c = 0; c < d; ++c) o[c] = 0.0;
+    if (m == 0) continue;
+    double mx = -INFINITY;
+    for (int i = 0; i < m; ++i) {
+      double dot = 0.0;
+      for (int c = 0; c < d; ++c)
+        dot += ckvref_bf16_to_f64(q[g * d + c]) *
+               ckvref_bf16_to_f64(k_rows[(int64_t)i * d + c]);
+      logit[i] = sc * dot;
+      if (logit[i] > mx) mx = logit[i];
+    }
+    double z = 0.0;
+    for (int i = 0; i < m; ++i) {
+      logit[i] = exp(logit[i] - mx);
+      z += logit[i];
+    }
+    for (int i = 0; i < m; ++i) {
+      double w = logit[i] / z;
+      if (p) p[(int64_t)g * m + i] = w;
+      for (int c = 0; c < d; ++c)
+        o[c] += w * ckvref_bf16_to_f64(v_rows[(int64_t)i * d + c]);
+    }
+  }
+  free(logit);
+}
+
+/* ------------------------------------------------------------------------ */
+/* whole-batch wrappers                                                      */
+
+static int shape_ok(const ckvref_shape* s) {
+  if (!s) return 0;
+  if (s->batch < 0 || s->num_q_heads < 1 || s->num_kv_heads < 1) return 0;
+  if (s->num_q_heads % s->num_kv_heads) return 0;
+  if (s->head_dim < 1 || s->max_ctx < 0) return 0;
+  if (s->key_row_stride < s->head_dim || s->kv_row_stride < s->head_dim)
+    return 0;
+  return 1;
+}
+
+static int clamp_len(int32_t n, int32_t max_ctx) {
+  if (n < 0) return 0;
+  return n > max_ctx ? max_ctx : n;
+}
+
+typedef struct {
+  const ckvref_shape* s;
+  int kind; /* 0 score, 1 select, 2 attn, 3 pipeline */
+  const uint16_t *q, *q2, *keys, *k_src, *v_src, *k_buf, *v_buf;
+  const int32_t* ctx_lens;
+  const int32_t* n_sel_in;
+  const double* scores_in;
+  double* scores;
+  int32_t* idx;
+  int32_t* n_sel;
+  double* out;
+  int k;
+  float scale;
+  int unit_begin, unit_end;
+} job;
+
+static void run_unit(const job* jb, int u) {
+  const ckvref_shape* s = jb->s;
+  const int Hkv = s->num_kv_heads, G = s->num_q_heads / s->num_kv_heads;
+  const int d = s->head_dim, nmax = s->max_ctx, k = jb->k;
+  const int b = u / Hkv, h = u % Hkv;
+  const int64_t qoff = ((int64_t)b * s->num_q_heads + (int64_t)h * G) * d;
+  if (jb->kind == 0) {
+    int n = clamp_len(jb->ctx_lens[b], nmax);
+    double* S = jb->scores + (int64_t)u * nmax;
+    ckvref_unit_scores(G, d, n, jb->q + qoff,
+                       jb->keys + (int64_t)u * nmax * s->key_row_stride,
+                       s->key_row_stride, jb->scale, S);
+    for (int j = n; j < nmax; ++j) S[j] = -INFINITY;
+  } else if (jb->kind == 1) {
+    int n = clamp_len(jb->ctx_lens[b], nmax);
+    jb->n_sel[u] = ckvref_unit_select(n, jb->scores_in + (int64_t)u * nmax, k,
+                                      jb->idx + (int64_t)u * k);
+  } else if (jb->kind == 2) {
+    int m = jb->n_sel_in[u];
+    if (m < 0) m = 0;
+    if (m > k) m = k;
+    ckvref_unit_attn(G, d, m, jb->q + qoff,
+                     jb->k_buf + (int64_t)u * k * d,
+                     jb->v_buf + (int64_t)u * k * d, jb->scale,
+                     jb->out + qoff, NULL);
+  } else {
+    /* Sec. 4.1 + Sec. 5.3: index from the selecting query, attention of
+     * the attending query over the rows of that index. */
+    int n = clamp_len(jb->ctx_lens[b], nmax);
+    double* S = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    ckvref_unit_scores(G, d, n, jb->q2 + qoff,
+                       jb->keys + (int64_t)u * nmax * s->key_row_stride,
+                       s->key_row_stride, jb->scale, S);
+    int32_t* idx = jb->idx + (int64_t)u * k;
+    int m = ckvref_unit_select(n, S, k, idx);
+    jb->n_sel[u] = m;
+    uint16_t* kr = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(m > 0 ? m : 1) * d);
+    uint16_t* vr = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(m > 0 ? m : 1) * d);
+    const int64_t base = (int64_t)u * nmax * s->kv_row_stride;
+    for (int i = 0; i < m; ++i) {
+      memcpy(kr + (int64_t)i * d,
+             jb->k_src + base + (int64_t)idx[i] * s->kv_row_stride,
+             sizeof(uint16_t) * d);
+      memcpy(vr + (int64_t)i * d,
+             jb->v_src + base + (int64_t)idx[i] * s->kv_row_stride,
+             sizeof(uint16_t) * d);
+    }
+    ckvref_unit_attn(G, d, m, jb->q + qoff, kr, vr, jb->scale, jb->out + qoff,
+                     NULL);
+    free(kr);
+    free(vr);
+    free(S);
+  }
+}
+
+static void* run_range(void* arg) {
+  const job* jb = (const job*)arg;
+  for (int u = jb->unit_begin; u < jb->unit_end; ++u) run_unit(jb, u);
+  return NULL;
+}
+
+/* Units are independent; threads only split the unit range. */
+static void run_units(job* base, int units, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > units) nthreads = units > 0 ? units : 1;
+  if (nthreads == 1) {
+    base->unit_begin = 0;
+    base->unit_end = units;
+    run_range(base);
+    return;
+  }
+  pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
+  job* jobs = (job*)malloc(sizeof(job) * (size_t)nthreads);
+  for (int t = 0; t < nthreads; ++t) {
+    jobs[t] = *base;
+    jobs[t].unit_begin = (int)((int64_t)units * t / nthreads);
+    jobs[t].unit_end = (int)((int64_t)units * (t + 1) / nthreads);
+    pthread_create(&th[t], NULL, run_range, &jobs[t]);
+  }
+  for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+  free(jobs);
+  free(th);
+}
+
+int ckvref_score_keys(const ckvref_shape* s, const uint16_t* q,
+                      const uint16_t* k_score, const int32_t* ctx_lens,
+                      float scale, double* scores, int nthreads) {
+  if (!shape_ok(s)) return -1;
+  job jb;
+  memset(&jb, 0, sizeof jb);
+  jb.s = s;
+  jb.kind = 0;
+  jb.q = q;
+  jb.keys = k_score;
+  jb.ctx_lens = ctx_lens;
+  jb.scale = scale;
+  jb.scores = scores;
+  run_units(&jb, s->batch * s->num_kv_heads, nthreads);
+  return 0;
+}
+
+int ckvref_select_topk(const ckvref_shape* s, const double* scores,
+                       const int32_t* ctx_lens, int k, int32_t* idx,
+                       int32_t* n_sel, int nthreads) {
+  if (!shape_ok(s) || k < 1) return -1;
+  job jb;
+  memset(&jb, 0, sizeof jb);
+  jb.s = s;
+  jb.kind = 1;
+  jb.scores_in = scores;
+  jb.ctx_lens = ctx_lens;
+  jb.k = k;
+  jb.idx = idx;
+  jb.n_sel = n_sel;
+  run_units(&jb, s->batch * s->num_kv_heads, nthreads);
+  return 0;
+}
+
+/* Sec. 5.4 (sparse KV assembly): each selected entry is placed, unchanged,
+ * at its slot of the attention layout.  Slots i >= n_sel are not written. */
+int ckvref_gather_kv(const ckvref_shape* s, const uint16_t* k_src,
+                     const uint16_t* v_src, const int32_t* idx,
+                     const int32_t* n_sel, int k, uint16_t* k_dst,
+                     uint16_t* v_dst) {
+  if (!shape_ok(s) || k < 1) return -1;
+  const int units = s->batch * s->num_kv_heads, d = s->head_dim;
+  for (int u = 0; u < units; ++u) {
+    int m = n_sel[u];
+    if (m > k) m = k;
+    const int64_t base = (int64_t)u * s->max_ctx * s->kv_row_stride;
+    for (int i = 0; i < m; ++i) {
+      int64_t row = idx[(int64_t)u * k + i];
+      memcpy(k_dst + ((int64_t)u * k + i) * d,
+             k_src + base + row * s->kv_row_stride, sizeof(uint16_t) * d);
+      memcpy(v_dst + ((int64_t)u * k + i) * d,
+             v_src + base + row * s->kv_row_stride, sizeof(uint16_t) * d);
+    }
+  }
+  return 0;
+}
+
+int ckvref_sparse_decode_attn(const ckvref_shape* s, const uint16_t* q_att,
+                              const uint16_t* k_buf, const uint16_t* v_buf,
+                              const int32_t* n_sel, int k, float scale,
+                              double* out, int nthreads) {
+  if (!shape_ok(s) || k < 1) return -1;
+  job jb;
+  memset(&jb, 0, sizeof jb);
+  jb.s = s;
+  jb.kind = 2;
+  jb.q = q_att;
+  jb.k_buf = k_buf;
+  jb.v_buf = v_buf;
+  jb.n_sel_in = n_sel;
+  jb.k = k;
+  jb.scale = scale;
+  jb.out = out;
+  run_units(&jb, s->batch * s->num_kv_heads, nthreads);
+  return 0;
+}
+
+int ckvref_critical_kv_attn(const ckvref_shape* s, const uint16_t* q_att,
+                            const uint16_t* q_sel, const uint16_t* k_score,
+                            const uint16_t* k_src, const uint16_t* v_src,
+                            const int32_t* ctx_lens, int k, float scale,
+                            int32_t* idx, int32_t* n_sel, double* out,
+                            int nthreads) {
+  if (!shape_ok(s) || k < 1) return -1;
+  job jb;
+  memset(&jb, 0, sizeof jb);
+  jb.s = s;
+  jb.kind = 3;
+  jb.q = q_att;
+  jb.q2 = q_sel ? q_sel : q_att;
+  jb.keys = k_score;
+  jb.k_src = k_src;
+  jb.v_src = v_src;
+  jb.ctx_lens = ctx_lens;
+  jb.k = k;
+  jb.scale = scale;
+  jb.idx = idx;
+  jb.n_sel = n_sel;
+  jb.out = out;
+  run_units(&jb, s->batch * s->num_kv_heads, nthreads);
+  return 0;
+}

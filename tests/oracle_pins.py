@@ -1,0 +1,358 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each ``pin_*`` takes an ``oracle.Oracle`` handle and raises AssertionError when
+the oracle disagrees with an independent fact: a closed form of a special
+case, brute force on tiny inputs, a library routine the special case reduces
+to, or an invariant of the method.  None retypes the oracle's own formula.
+The same pins run against deliberately broken copies of the oracle
+(``test_oracle_mutants.py``), each of which must fail at least one pin.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+
+import numpy as np
+import torch
+
+import synth
+
+SCALE = float(np.float32(1.0 / math.sqrt(128.0)))
+
+
+# --- bf16 helpers (host side, used only to build inputs) ----------------------
+def f2bf(x) -> np.ndarray:
+    """fp32 -> bf16 bits, round to nearest even (finite inputs)."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def bf2f(u) -> np.ndarray:
+    return (np.asarray(u, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def rand_bf(rng, shape, scale=1.0):
+    return f2bf(rng.standard_normal(shape) * scale)
+
+
+# --- bf16 decode --------------------------------------------------------------
+def pin_bf16_decode(orc):
+    cases = {0x3F80: 1.0, 0xC000: -2.0, 0x4049: 3.140625, 0x0001: 2.0 ** -133,
+             0x8000: -0.0, 0x7F80: math.inf, 0x3E00: 0.125, 0x4500: 2048.0}
+    for bits, val in cases.items():
+        got = orc.bf16_to_f64(bits)
+        assert got == val, (hex(bits), got, val)
+
+
+# --- scores -------------------------------------------------------------------
+def pin_scores_onehot(orc):
+    """Query heads that are one-hot on distinct channels: each head's logit is
+    scale * value * K[j, c_g], and the group's score is the largest of them."""
+    rng = np.random.default_rng(1)
+    G, d, n = 4, 128, 61
+    K = rand_bf(rng, (n, d))
+    chans, vals = [5, 77, 3, 127], [1.0, -2.0, 0.5, 3.0]
+    q = np.zeros((G, d), np.uint16)
+    for g in range(G):
+        q[g, chans[g]] = f2bf(vals[g])
+    S = orc.unit_scores(q, K, SCALE)
+    Kf = bf2f(K).astype(np.float64)
+    for j in range(n):
+        exp = max(SCALE * vals[g] * Kf[j, chans[g]] for g in range(G))
+        assert S[j] == exp, (j, S[j], exp)
+
+
+def pin_scores_integer(orc):
+    """Integer keys and constant queries: q_g = (g+1) * ones, so the logit of
+    head g is scale*(g+1)*rowsum(K_j); the max picks g=G-1 for positive row
+    sums and g=0 for negative ones."""
+    rng = np.random.default_rng(2)
+    G, d, n = 3, 32, 40
+    K = f2bf(rng.integers(-3, 4, size=(n, d)).astype(np.float32))
+    q = np.stack([f2bf(np.full(d, g + 1.0)) for g in range(G)])
+    S = orc.unit_scores(q, K, 0.5)
+    rs = bf2f(K).astype(np.float64).sum(axis=1)
+    for j in range(n):
+        mult = G if rs[j] > 0 else 1
+        assert S[j] == 0.5 * mult * rs[j], (j, S[j], rs[j])
+
+
+def pin_scores_batch_layout(orc):
+    """Batch layout: query head q belongs to KV head q // G, keys of (b, h)
+    start at ((b*Hkv + h)*max_ctx)*row_stride, padding columns of a strided row
+    are never read, positions >= n_b score -inf."""
+    rng = np.random.default_rng(3)
+    B, Hq, Hkv, d, nmax, stride = 2, 8, 2, 16, 12, 20
+    G = Hq // Hkv
+    lens = np.array([9, 5], np.int32)
+    keys = rand_bf(rng, (B, Hkv, nmax, stride))
+    keys[..., d:] = 0x7FC0                    # NaN in the padding columns
+    q = np.zeros((B, Hq, d), np.uint16)
+    val = {}
+    for b in range(B):
+        for hq in range(Hq):
+            c = (3 * hq + b) % d
+            v = float(1 + hq + 10 * b)
+            q[b, hq, c] = f2bf(v)
+            val[(b, hq)] = (c, v)
+    s = orc.shape(B, Hq, Hkv, d, nmax, key_row_stride=stride)
+    S = orc.score_keys(s, q, keys, lens, SCALE)
+    Kf = bf2f(keys).astype(np.float64)
+    for b in range(B):
+        for h in range(Hkv):
+            for j in range(nmax):
+                if j >= lens[b]:
+                    assert S[b, h, j] == -math.inf
+                    continue
+                exp = max(SCALE * val[(b, hq)][1] * Kf[b, h, j, val[(b, hq)][0]]
+                          for hq in range(h * G, h * G + G))
+                assert S[b, h, j] == exp, (b, h, j, S[b, h, j], exp)
+
+
+# --- selection ----------------------------------------------------------------
+def _dominates(S, sub, n):
+    """Definition of the critical set: every chosen position beats every
+    unchosen one, by larger score, or by lower position on equal scores."""
+    chosen = set(sub)
+    for i in chosen:
+        for u in range(n):
+            if u in chosen:
+                continue
+            if not (S[i] > S[u] or (S[i] == S[u] and i < u)):
+                return False
+    return True
+
+
+def pin_select_bruteforce(orc):
+    """Enumerate every subset of size min(k, n) for n <= 10; exactly one obeys
+    the definition and it is the oracle's, listed ascending, padded with -1."""
+    rng = np.random.default_rng(4)
+    levels = np.array([-1.5, 0.0, 0.25, 2.0, 7.0])
+    for trial in range(250):
+        n = int(rng.integers(0, 11))
+        k = int(rng.integers(1, 13))
+        if trial % 2:
+            S = rng.choice(levels, size=n)           # many exact ties
+        else:
+            S = rng.standard_normal(n)
+        idx, m = orc.unit_select(S, k)
+        m_exp = min(k, n)
+        assert m == m_exp, (n, k, m)
+        valid = [c for c in itertools.combinations(range(n), m_exp)
+                 if _dominates(S, c, n)]
+        assert len(valid) == 1, (S, k, valid)
+        assert list(idx[:m]) == list(valid[0]), (S, k, idx, valid)
+        assert all(idx[m:] == -1), idx
+
+
+def pin_select_reversal(orc):
+    """Reversing the positions of distinct scores reverses the chosen set."""
+    rng = np.random.default_rng(5)
+    S = rng.standard_normal(200)
+    idx, m = orc.unit_select(S, 37)
+    idx_r, m_r = orc.unit_select(S[::-1].copy(), 37)
+    assert m == m_r == 37
+    assert sorted(199 - idx[:m]) == list(idx_r[:m])
+
+
+def pin_select_small_contexts(orc):
+    """n <= k selects every position; n = 0 selects none."""
+    S = np.array([3.0, -1.0, 3.0, 0.5, 9.0])
+    idx, m = orc.unit_select(S, 8)
+    assert m == 5 and list(idx) == [0, 1, 2, 3, 4, -1, -1, -1]
+    idx, m = orc.unit_select(np.zeros(0), 4)
+    assert m == 0 and list(idx) == [-1] * 4
+
+
+def pin_select_planted(orc, seeds=range(20)):
+    """Tiny workload: the 16 keys planted at 4x the group's mean query
+    direction are always among the 256 selected per KV head."""
+    w = synth.WORKLOADS["tiny"]
+    for seed in seeds:
+        t = synth.make_layer(w, seed=seed)
+        s = orc.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
+        scores = orc.score_keys(s, synth.to_u16(t["q"]), synth.to_u16(t["k"]),
+                                t["ctx_lens"].numpy(), SCALE, nthreads=2)
+        idx, n_sel = orc.select_topk(s, scores, t["ctx_lens"].numpy(), w.k)
+        marked = t["marked"].numpy()
+        for b in range(w.batch):
+            for h in range(w.kv_heads):
+                planted = set(np.nonzero(marked[b, h])[0].tolist())
+                assert len(planted) == 16
+                assert planted <= set(idx[b, h, :n_sel[b, h]].tolist()), (seed, b, h)
+
+
+# --- attention ----------------------------------------------------------------
+def _sdpa(qf, kf, vf, scale):
+    """torch's scaled-dot-product attention in float64 on the CPU."""
+    q = torch.from_numpy(qf)[:, None, :]                    # [G][1][d]
+    k = torch.from_numpy(kf)[None].expand(qf.shape[0], -1, -1).contiguous()
+    v = torch.from_numpy(vf)[None].expand(qf.shape[0], -1, -1).contiguous()
+    o = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=scale)
+    return o[:, 0, :].numpy()
+
+
+def pin_attn_dense_library(orc):
+    """With every row selected, the result is ordinary dense softmax attention
+    (torch SDPA in float64)."""
+    rng = np.random.default_rng(6)
+    G, d, m = 4, 128, 300
+    q, K, V = rand_bf(rng, (G, d)), rand_bf(rng, (m, d)), rand_bf(rng, (m, d))
+    out, _ = orc.unit_attn(q, K, V, SCALE)
+    ref = _sdpa(bf2f(q).astype(np.float64), bf2f(K).astype(np.float64),
+                bf2f(V).astype(np.float64), SCALE)
+    assert np.max(np.abs(out - ref)) < 1e-12, np.max(np.abs(out - ref))
+
+
+def pin_attn_single_row(orc):
+    """One selected row: its weight is exactly 1, so out is that V row."""
+    rng = np.random.default_rng(7)
+    q, K, V = rand_bf(rng, (4, 128)), rand_bf(rng, (1, 128)), rand_bf(rng, (1, 128))
+    out, p = orc.unit_attn(q, K, V, SCALE)
+    assert np.all(p == 1.0)
+    assert np.array_equal(out, np.broadcast_to(bf2f(V[0]).astype(np.float64), out.shape))
+
+
+def pin_attn_zero_query(orc):
+    """A zero query gives equal logits: out is the mean of the V rows."""
+    rng = np.random.default_rng(8)
+    q = np.zeros((2, 128), np.uint16)
+    K, V = rand_bf(rng, (50, 128)), rand_bf(rng, (50, 128))
+    out, _ = orc.unit_attn(q, K, V, SCALE)
+    mean = bf2f(V).astype(np.float64).mean(axis=0)
+    assert np.max(np.abs(out - mean)) < 1e-13
+
+
+def pin_attn_two_rows(orc):
+    """Two rows with logits a and b: weights are the logistic function of the
+    logit difference."""
+    rng = np.random.default_rng(9)
+    d = 128
+    q = np.zeros((1, d), np.uint16)
+    q[0, 17] = f2bf(1.0)
+    K = rand_bf(rng, (2, d))
+    K[0, 17], K[1, 17] = f2bf(1.25), f2bf(-0.5)
+    V = rand_bf(rng, (2, d))
+    out, _ = orc.unit_attn(q, K, V, 1.0)
+    a, b = 1.25, -0.5
+    w0 = 1.0 / (1.0 + math.exp(b - a))
+    w1 = 1.0 / (1.0 + math.exp(a - b))
+    Vf = bf2f(V).astype(np.float64)
+    assert np.max(np.abs(out[0] - (w0 * Vf[0] + w1 * Vf[1]))) < 1e-14
+
+
+def pin_attn_weights_normalised(orc):
+    """Softmax weights are non-negative and sum to 1; V = 1 gives out = 1."""
+    rng = np.random.default_rng(10)
+    q, K = rand_bf(rng, (4, 128), 3.0), rand_bf(rng, (77, 128))
+    V = np.full((77, 128), f2bf(1.0), np.uint16)
+    out, p = orc.unit_attn(q, K, V, SCALE)
+    assert np.all(p >= 0)
+    assert np.max(np.abs(p.sum(axis=1) - 1.0)) < 1e-13
+    assert np.max(np.abs(out - 1.0)) < 1e-13
+
+
+def pin_attn_permutation(orc):
+    """The result does not depend on the order of the selected rows."""
+    rng = np.random.default_rng(11)
+    q, K, V = rand_bf(rng, (4, 128)), rand_bf(rng, (90, 128)), rand_bf(rng, (90, 128))
+    out, _ = orc.unit_attn(q, K, V, SCALE)
+    perm = rng.permutation(90)
+    out_p, _ = orc.unit_attn(q, K[perm], V[perm], SCALE)
+    assert np.max(np.abs(out - out_p)) < 1e-12
+
+
+def pin_attn_large_logits(orc):
+    """Logits 2048 and 2040 (exp overflows fp64 without a max shift): the
+    result is still the logistic mix of the two rows."""
+    rng = np.random.default_rng(12)
+    d = 128
+    q = np.zeros((1, d), np.uint16)
+    q[0, 3] = f2bf(1.0)
+    K = rand_bf(rng, (2, d))
+    K[0, 3], K[1, 3] = f2bf(2048.0), f2bf(2040.0)
+    V = rand_bf(rng, (2, d))
+    out, _ = orc.unit_attn(q, K, V, 1.0)
+    w0 = 1.0 / (1.0 + math.exp(-8.0))
+    Vf = bf2f(V).astype(np.float64)
+    ref = w0 * Vf[0] + (1 - w0) * Vf[1]
+    assert np.all(np.isfinite(out)) and np.max(np.abs(out[0] - ref)) < 1e-14
+
+
+# --- gather ---------------------------------------------------------------------
+def pin_gather_exact(orc):
+    """Gather is an exact copy of the indexed rows (K|V interleaved source,
+    row stride 2d); slots at or beyond n_sel are left untouched."""
+    rng = np.random.default_rng(13)
+    B, Hkv, nmax, d, k = 2, 3, 10, 8, 4
+    src = rng.integers(0, 65536, size=(B, Hkv, nmax, 2, d)).astype(np.uint16)
+    flat = src.reshape(-1)
+    idx = np.full((B, Hkv, k), -1, np.int32)
+    n_sel = rng.integers(0, k + 1, size=(B, Hkv)).astype(np.int32)
+    for b in range(B):
+        for h in range(Hkv):
+            idx[b, h, :n_sel[b, h]] = np.sort(rng.choice(nmax, n_sel[b, h], replace=False))
+    kd = np.full((B, Hkv, k, d), 0xABCD, np.uint16)
+    vd = np.full((B, Hkv, k, d), 0xABCD, np.uint16)
+    s = orc.shape(B, Hkv, Hkv, d, nmax, kv_row_stride=2 * d)
+    orc.gather_kv(s, flat, flat[d:], idx, n_sel, k, kd, vd)
+    for b in range(B):
+        for h in range(Hkv):
+            m = n_sel[b, h]
+            assert np.array_equal(kd[b, h, :m], src[b, h, idx[b, h, :m], 0])
+            assert np.array_equal(vd[b, h, :m], src[b, h, idx[b, h, :m], 1])
+            assert np.all(kd[b, h, m:] == 0xABCD) and np.all(vd[b, h, m:] == 0xABCD)
+
+
+# --- composition ------------------------------------------------------------------
+def pin_pipeline_composition(orc):
+    """The fused oracle equals score -> select -> gather -> attend, each part
+    pinned above; with a separate selecting query, selection follows q_sel
+    and attention follows q_att.  A budget >= n_b reduces to dense attention."""
+    rng = np.random.default_rng(14)
+    B, Hq, Hkv, d, nmax, k = 2, 8, 2, 128, 300, 40
+    G = Hq // Hkv
+    lens = np.array([300, 123], np.int32)
+    q1, q2 = rand_bf(rng, (B, Hq, d)), rand_bf(rng, (B, Hq, d))
+    K, V = rand_bf(rng, (B, Hkv, nmax, d)), rand_bf(rng, (B, Hkv, nmax, d))
+    s = orc.shape(B, Hq, Hkv, d, nmax)
+    for qs in (None, q2):
+        idx, n_sel, out = orc.critical_kv_attn(s, q1, qs, K, K, V, lens, k, SCALE)
+        sc = orc.score_keys(s, q1 if qs is None else qs, K, lens, SCALE)
+        idx2, n_sel2 = orc.select_topk(s, sc, lens, k)
+        assert np.array_equal(idx, idx2) and np.array_equal(n_sel, n_sel2)
+        kb = np.zeros((B, Hkv, k, d), np.uint16)
+        vb = np.zeros((B, Hkv, k, d), np.uint16)
+        orc.gather_kv(s, K, V, idx, n_sel, k, kb, vb)
+        out2 = orc.sparse_decode_attn(s, q1, kb, vb, n_sel, k, SCALE)
+        assert np.max(np.abs(out - out2)) < 1e-12
+    # q_sel != q_att really changes the set here (else the check above is void)
+    idx_a, _, _ = orc.critical_kv_attn(s, q1, None, K, K, V, lens, k, SCALE)
+    idx_b, _, _ = orc.critical_kv_attn(s, q1, q2, K, K, V, lens, k, SCALE)
+    assert not np.array_equal(idx_a, idx_b)
+    kbig = 512
+    idx, n_sel, out = orc.critical_kv_attn(s, q1, q2, K, K, V, lens, kbig, SCALE)
+    for b in range(B):
+        for h in range(Hkv):
+            n = lens[b]
+            assert n_sel[b, h] == n and list(idx[b, h, :n]) == list(range(n))
+            ref = _sdpa(bf2f(q1[b, h * G:(h + 1) * G]).astype(np.float64),
+                        bf2f(K[b, h, :n]).astype(np.float64),
+                        bf2f(V[b, h, :n]).astype(np.float64), SCALE)
+            assert np.max(np.abs(out[b, h * G:(h + 1) * G] - ref)) < 1e-12
+
+
+def pin_empty_context(orc):
+    """n_b = 0: nothing selected, idx all -1, output zero."""
+    rng = np.random.default_rng(15)
+    B, Hq, Hkv, d, nmax, k = 2, 4, 1, 128, 16, 8
+    lens = np.array([0, 5], np.int32)
+    q = rand_bf(rng, (B, Hq, d))
+    K, V = rand_bf(rng, (B, Hkv, nmax, d)), rand_bf(rng, (B, Hkv, nmax, d))
+    s = orc.shape(B, Hq, Hkv, d, nmax)
+    idx, n_sel, out = orc.critical_kv_attn(s, q, None, K, K, V, lens, k, SCALE)
+    assert n_sel[0, 0] == 0 and np.all(idx[0, 0] == -1) and np.all(out[0] == 0.0)
+    assert n_sel[1, 0] == 5 and list(idx[1, 0]) == [0, 1, 2, 3, 4, -1, -1, -1]
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
