@@ -1,0 +1,187 @@
+/*
+ * ckv.h -- C ABI of libckv: critical-KV selection and sparse decode attention
+ * for MI355X (gfx950).
+ *
+ * The operation is the decode-step hot path of DualDecoder (arXiv
+ * 2607.26475): for every (request, KV head) the positions of the context are
+ * scored against a query (Sec. 2.2 and Sec. 4.1: the retrieval index comes from
+ * a query and per-position key summaries; here the summary of a position is
+ * its own key), the top-k positions are selected once per KV head for all
+ * query heads of its GQA group, the selected K/V rows are gathered from HBM or
+ * host-pinned memory into a layer-scoped GPU buffer (Sec. 5.4, GPU-side sparse
+ * KV assembly), and softmax attention runs over only those rows (Sec. 5.3:
+ * the result must equal attention over the selected entries).  In DualDecoder
+ * the selecting query is the speculative token's (Sec. 4.1, retrieval index
+ * prediction) and the attending query is the current token's (Sec. 5.2).
+ *
+ * Conventions shared by every entry point
+ *   - Types: bf16 tensors are passed as uint16_t bit patterns; scores and
+ *     outputs are fp32; positions and counts are int32.
+ *   - Layouts (row-major, dense unless a stride says otherwise):
+ *       q, q_att, q_sel   [B][Hq][d]                     bf16, device
+ *       k_score           row j of (b,h) at element
+ *                         ((b*Hkv + h)*max_ctx + j) * key_row_stride  bf16, device
+ *       k_src, v_src      row j of (b,h) at element
+ *                         ((b*Hkv + h)*max_ctx + j) * kv_row_stride   bf16,
+ *                         device or host-pinned (src_kind); K and V may be
+ *                         interleaved per row (kv_row_stride = 2d, v_src =
+ *                         k_src + d)
+ *       ctx_lens          [B] int32, device; n_b, clamped to [0, max_ctx]
+ *       scores            [B][Hkv][max_ctx] fp32, device
+ *       idx               [B][Hkv][k] int32, device; ascending positions,
+ *                         then -1
+ *       n_sel             [B][Hkv] int32, device; m = min(k, n_b)
+ *       k_buf, v_buf      [B][Hkv][k][d] bf16, device (slot i = i-th selected)
+ *       out               [B][Hq][d] fp32, device
+ *     Query head q belongs to KV head q / (Hq/Hkv) (consecutive grouping).
+ *   - Supported shapes: head_dim == 128; Hq % Hkv == 0 with group size
+ *     G = Hq/Hkv in {1, 2, 4, 8, 16}; 1 <= max_ctx <= 2^30; 1 <= k <= 2^20;
+ *     row strides >= 128 and multiples of 8 elements; every tensor pointer
+ *     16-byte aligned.
+ *   - Ownership: every buffer belongs to the caller; the library never
+ *     allocates or frees caller memory.  Scratch memory is a caller-provided
+ *     workspace of at least ckv_workspace_bytes() bytes, 256-byte aligned; its
+ *     contents on entry do not matter and are undefined on return.
+ *   - Streams: every call only enqueues work on `stream` (a hipStream_t; NULL
+ *     is the legacy default stream) and returns without synchronising.  Calls
+ *     that share a workspace must be ordered on one stream.
+ *   - Errors: each call returns a ckv_status.  Argument errors are detected on
+ *     the host before anything is enqueued; CKV_EHIP reports a failed launch
+ *     (the HIP error code is in the detail text).  Faults during kernel
+ *     execution surface at the caller's next synchronisation.  No C++
+ *     exception crosses this interface.  ckv_last_error_detail() gives a
+ *     thread-local description of the last failure.
+ *   - Device-side preconditions (not checked, values are clamped so that no
+ *     access leaves the caller's buffers): 0 <= n_b <= max_ctx; gathered idx
+ *     entries lie in [0, max_ctx) (slots whose idx is outside are skipped).
+ *   - Scores are compared by their fp32 value (-0 equals +0); equal scores
+ *     rank the lower position first.  Inputs must be finite.
+ */
+#ifndef CKV_H
+#define CKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CKV_ABI_VERSION 1
+
+typedef enum ckv_status {
+  CKV_OK = 0,
+  CKV_EINVAL = 1,        /* null pointer, misaligned pointer or bad value   */
+  CKV_ESHAPE = 2,        /* Hq % Hkv != 0, k < 1, max_ctx < 1, bad stride    */
+  CKV_EUNSUPPORTED = 3,  /* head_dim != 128, group size not in {1,2,4,8,16}  */
+  CKV_EWORKSPACE = 4,    /* workspace NULL or smaller than required          */
+  CKV_EHIP = 5           /* a HIP runtime call or kernel launch failed       */
+} ckv_status;
+
+typedef enum ckv_src_kind {
+  CKV_SRC_DEVICE = 0,      /* K/V rows in device memory (HBM)                */
+  CKV_SRC_HOST_PINNED = 1  /* K/V rows in host memory from hipHostMalloc or   */
+                           /* torch pin_memory; read by the GPU over the host */
+                           /* link, no staging copy                           */
+} ckv_src_kind;
+
+typedef enum ckv_entry {
+  CKV_ENTRY_SELECT_TOPK = 1,
+  CKV_ENTRY_SPARSE_DECODE_ATTN = 2,
+  CKV_ENTRY_CRITICAL_KV_ATTN = 3
+} ckv_entry;
+
+typedef struct ckv_shape {
+  int32_t batch;          /* B: requests in the decode batch                  */
+  int32_t num_q_heads;    /* Hq                                               */
+  int32_t num_kv_heads;   /* Hkv                                              */
+  int32_t head_dim;       /* d (must be 128)                                  */
+  int32_t max_ctx;        /* rows stored per (request, KV head)               */
+  int32_t reserved;       /* must be 0                                        */
+  int64_t key_row_stride; /* elements between consecutive rows of k_score     */
+  int64_t kv_row_stride;  /* elements between consecutive rows of k_src/v_src */
+} ckv_shape;
+
+/* Version of this interface (CKV_ABI_VERSION of the built library). */
+int ckv_abi_version(void);
+
+/* Static text for a status code (never NULL). */
+const char* ckv_status_str(int status);
+
+/* Thread-local description of the last failed call on this thread ("" if
+ * none).  Valid until the next call on the same thread. */
+const char* ckv_last_error_detail(void);
+
+/* Workspace that `entry` needs for this shape and budget k, in bytes, stored
+ * in *bytes.  Entry points not listed in ckv_entry need none. */
+int ckv_workspace_bytes(const ckv_shape* shape, int32_t k, int entry,
+                        size_t* bytes);
+
+/* Sec. 2.2 / Sec. 4.1 -- retrieval scores.  For every request b, KV head h and
+ * position j < n_b:
+ *   scores[b][h][j] = max over the G query heads g of h's group of
+ *                     scale * sum_c q[b][h*G+g][c] * k_score(b,h,j)[c]
+ * computed from bf16 inputs with fp32 accumulation; positions
+ * n_b <= j < max_ctx get -inf.  scale > 0 (normally 1/sqrt(d)). */
+int ckv_score_keys(const ckv_shape* shape, const uint16_t* q,
+                   const uint16_t* k_score, const int32_t* ctx_lens,
+                   float scale, float* scores, void* stream);
+
+/* Sec. 2.2 -- critical-entry selection within the sparse budget.  For every
+ * (b, h) the m = min(k, n_b) largest scores[b][h][0..n_b), ties broken by lower
+ * position, are written to idx[b][h][0..m) in ascending position order, the
+ * remaining k - m slots get -1, and n_sel[b][h] = m.  One index set per KV
+ * head serves all G query heads of its group.  Workspace:
+ * CKV_ENTRY_SELECT_TOPK. */
+int ckv_select_topk(const ckv_shape* shape, const float* scores,
+                    const int32_t* ctx_lens, int32_t k, int32_t* idx,
+                    int32_t* n_sel, void* ws, size_t ws_bytes, void* stream);
+
+/* Sec. 5.4 -- GPU-side sparse KV assembly.  For i < n_sel[b][h]:
+ *   k_dst[b][h][i] = K row idx[b][h][i] of (b,h) in k_src,
+ *   v_dst[b][h][i] = V row idx[b][h][i] of (b,h) in v_src,
+ * copied bit-exactly; slots i >= n_sel (and slots whose idx is outside
+ * [0, max_ctx)) are not written.  src_kind says where k_src/v_src live; with
+ * CKV_SRC_HOST_PINNED the GPU reads the rows straight from pinned host memory.
+ * k_dst/v_dst are device buffers of [B][Hkv][k][d]. */
+int ckv_gather_kv(const ckv_shape* shape, const uint16_t* k_src,
+                  const uint16_t* v_src, int src_kind, const int32_t* idx,
+                  const int32_t* n_sel, int32_t k, uint16_t* k_dst,
+                  uint16_t* v_dst, void* stream);
+
+/* Sec. 5.3 / Sec. 5.4 -- attention over the assembled sparse set.  For every
+ * query head g of KV head h, with m = n_sel[b][h] (clamped to [0, k]):
+ *   l_i = scale * q_att[b][g] . k_buf[b][h][i],  p = softmax(l_0..l_{m-1}),
+ *   out[b][g] = sum_i p_i v_buf[b][h][i],
+ * fp32 logits, weights and accumulation; out = 0 when m = 0.  Workspace:
+ * CKV_ENTRY_SPARSE_DECODE_ATTN. */
+int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
+                           const uint16_t* k_buf, const uint16_t* v_buf,
+                           const int32_t* n_sel, int32_t k, float scale,
+                           float* out, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* Fused decode step of one layer (Sec. 4.1, Sec. 5.2-5.4).  The selecting
+ * query q_sel (the speculative token's; NULL means q_att) scores k_score and
+ * picks idx_out / n_sel_out exactly as ckv_score_keys + ckv_select_topk.
+ *   Same-step mode (k_buf == NULL): out = attention of q_att over the rows
+ *     idx_out of k_src / v_src (read in place, src_kind says where), i.e.
+ *     ckv_sparse_decode_attn applied to ckv_gather_kv(idx_out).
+ *   Pipelined mode (k_buf != NULL): out = attention of q_att over
+ *     k_buf/v_buf rows [0, n_sel_in) -- the set selected one step earlier
+ *     and already assembled -- and, in the same launch, idx_out/n_sel_out are
+ *     selected for the next step.  k_src/v_src are not read.
+ * Workspace: CKV_ENTRY_CRITICAL_KV_ATTN. */
+int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
+                         const uint16_t* q_sel, const uint16_t* k_score,
+                         const int32_t* ctx_lens, int32_t k, float scale,
+                         const uint16_t* k_src, const uint16_t* v_src,
+                         int src_kind, const uint16_t* k_buf,
+                         const uint16_t* v_buf, const int32_t* n_sel_in,
+                         int32_t* idx_out, int32_t* n_sel_out, float* out,
+                         void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CKV_H */

@@ -1,0 +1,170 @@
+"""Python binding of libckv (critical-KV selection and sparse decode attention
+on MI355X).
+
+Argument marshalling only: every function passes raw pointers, sizes and the
+current HIP stream to the C ABI declared in ``include/ckv.h`` and raises
+``CkvError`` on a non-zero status.  All computation happens in the HIP
+kernels of ``libckv.so``; there is no fallback.  torch is used for device
+memory, pinned host memory and streams.
+
+The library must have been built first (``python -m paper_2607_26475_amd.build``
+or ``__graft_entry__.build()``); importing this package without it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+__all__ = [
+    "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
+    "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
+    "critical_kv_attn", "abi_version", "status_str", "LIB_PATH",
+    "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
+    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "EXPORTS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
+
+SRC_DEVICE, SRC_HOST_PINNED = 0, 1
+ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
+EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
+           "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
+           "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn")
+
+
+class CkvError(RuntimeError):
+    def __init__(self, fn: str, status: int, detail: str):
+        super().__init__(f"{fn}: {status_str(status)} ({status}): {detail}")
+        self.status = status
+
+
+class Shape(ctypes.Structure):
+    """Mirror of ``ckv_shape``."""
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("max_ctx", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("key_row_stride", ctypes.c_int64),
+                ("kv_row_stride", ctypes.c_int64)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run "
+                          "`python -m paper_2607_26475_amd.build` first")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    sp = ctypes.POINTER(Shape)
+    sig = {
+        "ckv_abi_version": (ctypes.c_int, []),
+        "ckv_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+        "ckv_last_error_detail": (ctypes.c_char_p, []),
+        "ckv_workspace_bytes": (ctypes.c_int, [sp, i32, ctypes.c_int, ctypes.POINTER(sz)]),
+        "ckv_score_keys": (ctypes.c_int, [sp, vp, vp, vp, ctypes.c_float, vp, vp]),
+        "ckv_select_topk": (ctypes.c_int, [sp, vp, vp, i32, vp, vp, vp, sz, vp]),
+        "ckv_gather_kv": (ctypes.c_int, [sp, vp, vp, ctypes.c_int, vp, vp, i32, vp, vp, vp]),
+        "ckv_sparse_decode_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
+                                                  vp, vp, sz, vp]),
+        "ckv_critical_kv_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
+                                                vp, vp, ctypes.c_int, vp, vp, vp, vp, vp,
+                                                vp, vp, sz, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def abi_version() -> int:
+    return _lib.ckv_abi_version()
+
+
+def status_str(status: int) -> str:
+    return _lib.ckv_status_str(status).decode()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise CkvError(fn, status, _lib.ckv_last_error_detail().decode())
+
+
+def shape_for(batch: int, num_q_heads: int, num_kv_heads: int, max_ctx: int,
+              head_dim: int = 128, key_row_stride: Optional[int] = None,
+              kv_row_stride: Optional[int] = None) -> Shape:
+    return Shape(batch, num_q_heads, num_kv_heads, head_dim, max_ctx, 0,
+                 head_dim if key_row_stride is None else key_row_stride,
+                 head_dim if kv_row_stride is None else kv_row_stride)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def workspace_bytes(shape: Shape, k: int, entry: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check("ckv_workspace_bytes",
+           _lib.ckv_workspace_bytes(ctypes.byref(shape), k, entry, ctypes.byref(n)))
+    return n.value
+
+
+def workspace(shape: Shape, k: int, entry: int, device="cuda") -> torch.Tensor:
+    """A device byte tensor large enough for `entry` (torch allocations are
+    256-byte aligned)."""
+    return torch.empty(max(workspace_bytes(shape, k, entry), 1), dtype=torch.uint8,
+                       device=device)
+
+
+def score_keys(shape: Shape, q, k_score, ctx_lens, scale: float, scores,
+               stream=None) -> None:
+    _check("ckv_score_keys", _lib.ckv_score_keys(
+        ctypes.byref(shape), _ptr(q), _ptr(k_score), _ptr(ctx_lens), scale,
+        _ptr(scores), _stream(stream)))
+
+
+def select_topk(shape: Shape, scores, ctx_lens, k: int, idx, n_sel, ws,
+                stream=None) -> None:
+    _check("ckv_select_topk", _lib.ckv_select_topk(
+        ctypes.byref(shape), _ptr(scores), _ptr(ctx_lens), k, _ptr(idx), _ptr(n_sel),
+        _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def gather_kv(shape: Shape, k_src, v_src, src_kind: int, idx, n_sel, k: int,
+              k_dst, v_dst, stream=None) -> None:
+    _check("ckv_gather_kv", _lib.ckv_gather_kv(
+        ctypes.byref(shape), _ptr(k_src), _ptr(v_src), src_kind, _ptr(idx), _ptr(n_sel),
+        k, _ptr(k_dst), _ptr(v_dst), _stream(stream)))
+
+
+def sparse_decode_attn(shape: Shape, q_att, k_buf, v_buf, n_sel, k: int,
+                       scale: float, out, ws, stream=None) -> None:
+    _check("ckv_sparse_decode_attn", _lib.ckv_sparse_decode_attn(
+        ctypes.byref(shape), _ptr(q_att), _ptr(k_buf), _ptr(v_buf), _ptr(n_sel), k, scale,
+        _ptr(out), _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def critical_kv_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
+                     scale: float, k_src, v_src, src_kind: int, k_buf, v_buf,
+                     n_sel_in, idx_out, n_sel_out, out, ws, stream=None) -> None:
+    _check("ckv_critical_kv_attn", _lib.ckv_critical_kv_attn(
+        ctypes.byref(shape), _ptr(q_att), _ptr(q_sel), _ptr(k_score), _ptr(ctx_lens), k,
+        scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(k_buf), _ptr(v_buf),
+        _ptr(n_sel_in), _ptr(idx_out), _ptr(n_sel_out), _ptr(out), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))

@@ -1,0 +1,453 @@
+// ckv_api.cpp -- the C ABI of libckv: argument checks, workspace layout and
+// the launch sequences of each entry point.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <string>
+
+#include "ckv.h"
+#include "ckv_launch.hpp"
+
+namespace {
+
+using namespace ckv;
+
+thread_local std::string g_detail;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_detail = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(CKV_EHIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+#define CKV_TRY_HIP(expr, what)                 \
+  do {                                          \
+    hipError_t e_ = (expr);                     \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+struct Dims {
+  int B, Hq, Hkv, G, U, max_ctx;
+  int64_t key_stride, kv_stride;
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_shape(const ckv_shape* s, Dims* d) {
+  if (!s) return fail(CKV_EINVAL, "shape is NULL");
+  if (s->reserved != 0) return fail(CKV_EINVAL, "shape.reserved must be 0");
+  if (s->batch < 0 || s->num_q_heads < 1 || s->num_kv_heads < 1)
+    return fail(CKV_ESHAPE, "batch=%d num_q_heads=%d num_kv_heads=%d", s->batch,
+                s->num_q_heads, s->num_kv_heads);
+  if (s->num_q_heads % s->num_kv_heads)
+    return fail(CKV_ESHAPE, "num_q_heads %d not a multiple of num_kv_heads %d",
+                s->num_q_heads, s->num_kv_heads);
+  if (s->head_dim != kD)
+    return fail(CKV_EUNSUPPORTED, "head_dim %d (only %d is supported)", s->head_dim, kD);
+  const int G = s->num_q_heads / s->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
+    return fail(CKV_EUNSUPPORTED, "group size %d not in {1,2,4,8,16}", G);
+  if (s->max_ctx < 1 || s->max_ctx > (1 << 30))
+    return fail(CKV_ESHAPE, "max_ctx %d outside [1, 2^30]", s->max_ctx);
+  if (s->key_row_stride < kD || (s->key_row_stride & 7))
+    return fail(CKV_ESHAPE, "key_row_stride %lld (>= 128, multiple of 8)",
+                (long long)s->key_row_stride);
+  if (s->kv_row_stride < kD || (s->kv_row_stride & 7))
+    return fail(CKV_ESHAPE, "kv_row_stride %lld (>= 128, multiple of 8)",
+                (long long)s->kv_row_stride);
+  const int64_t units = (int64_t)s->batch * s->num_kv_heads;
+  if (units > (1 << 24)) return fail(CKV_EUNSUPPORTED, "batch*num_kv_heads too large");
+  d->B = s->batch;
+  d->Hq = s->num_q_heads;
+  d->Hkv = s->num_kv_heads;
+  d->G = G;
+  d->U = (int)units;
+  d->max_ctx = s->max_ctx;
+  d->key_stride = s->key_row_stride;
+  d->kv_stride = s->kv_row_stride;
+  return CKV_OK;
+}
+
+int check_k(int32_t k) {
+  if (k < 1 || k > (1 << 20)) return fail(CKV_ESHAPE, "k %d outside [1, 2^20]", k);
+  return CKV_OK;
+}
+
+int check_scale(float scale) {
+  if (!(scale > 0.f) || scale > 3.0e38f)
+    return fail(CKV_EINVAL, "scale must be a finite positive number");
+  return CKV_OK;
+}
+
+#define CKV_PTR(p)                                                          \
+  do {                                                                      \
+    if (!(p)) return fail(CKV_EINVAL, "%s is NULL", #p);                    \
+    if (!aligned16(p)) return fail(CKV_EINVAL, "%s is not 16-byte aligned", #p); \
+  } while (0)
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace regions, each 256-byte aligned.  [0, zero_end) is cleared at the
+// start of every selecting call.
+struct Layout {
+  size_t hist = 0, coarse = 0, ctrl = 0, zero_end = 0;
+  size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0, total = 0;
+  int64_t bm_words = 0;
+  int chunks = 0, score_tiles = 0, filter_tiles = 0;
+};
+
+Layout make_layout(const Dims& d, int32_t k, int entry) {
+  Layout L;
+  const size_t U = (size_t)d.U;
+  size_t off = 0;
+  L.score_tiles = (d.max_ctx + kScoreTile - 1) / kScoreTile;
+  L.filter_tiles = (d.max_ctx + kFilterTile - 1) / kFilterTile;
+  L.chunks = (k + kAttnRows - 1) / kAttnRows;
+  const bool select = entry == CKV_ENTRY_SELECT_TOPK || entry == CKV_ENTRY_CRITICAL_KV_ATTN;
+  const bool attn = entry == CKV_ENTRY_SPARSE_DECODE_ATTN || entry == CKV_ENTRY_CRITICAL_KV_ATTN;
+  if (select) {
+    L.hist = off;
+    off += U * kHistBins * 4;
+    L.coarse = off;
+    off += U * kCoarseBins * 4;
+    L.ctrl = off;
+    off += U * kCtrlWords * 4;
+    off = align256(off);
+    L.zero_end = off;
+    L.sel = off;
+    off = align256(off + U * (size_t)k * 4);
+    L.cand = off;
+    off = align256(off + U * (size_t)d.max_ctx * 8);
+    if (d.max_ctx > kBitmapLdsBits) {
+      L.bm_words = (d.max_ctx + 31) / 32;
+      L.bitmap = off;
+      off = align256(off + U * (size_t)L.bm_words * 4);
+    }
+  }
+  if (entry == CKV_ENTRY_CRITICAL_KV_ATTN) {
+    L.scores = off;
+    off = align256(off + U * (size_t)d.max_ctx * 4);
+  }
+  if (attn) {
+    L.part = off;
+    off = align256(off + U * (size_t)L.chunks * d.G * kPartStride * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+int check_grid(const Dims& d, const Layout& L) {
+  // work-items per dispatch must stay below 2^32
+  const int64_t limit = ((int64_t)1 << 32) / 1024 - 1;
+  if ((int64_t)d.U * L.score_tiles > limit || (int64_t)d.U * L.chunks > limit)
+    return fail(CKV_EUNSUPPORTED, "grid too large for this shape");
+  return CKV_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, const Layout& L) {
+  if (L.total == 0) return CKV_OK;
+  if (!ws) return fail(CKV_EWORKSPACE, "workspace is NULL (%zu bytes needed)", L.total);
+  if (reinterpret_cast<uintptr_t>(ws) & 255u)
+    return fail(CKV_EWORKSPACE, "workspace is not 256-byte aligned");
+  if (ws_bytes < L.total)
+    return fail(CKV_EWORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, L.total);
+  return CKV_OK;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Device address of a host-pinned buffer (hipHostMalloc / torch pin_memory).
+int host_to_device(const uint16_t* p, const uint16_t** out) {
+  void* dp = nullptr;
+  hipError_t e = hipHostGetDevicePointer(&dp, const_cast<uint16_t*>(p), 0);
+  if (e != hipSuccess || !dp)
+    return fail(CKV_EINVAL, "source is not host-pinned memory visible to the device (%s)",
+                hipGetErrorString(e));
+  *out = static_cast<const uint16_t*>(dp);
+  return CKV_OK;
+}
+
+int resolve_src(int src_kind, const uint16_t** k_src, const uint16_t** v_src) {
+  if (src_kind == CKV_SRC_DEVICE) return CKV_OK;
+  if (src_kind != CKV_SRC_HOST_PINNED) return fail(CKV_EINVAL, "bad src_kind %d", src_kind);
+  int rc = host_to_device(*k_src, k_src);
+  if (rc) return rc;
+  return host_to_device(*v_src, v_src);
+}
+
+int gather_blocks(int src_kind) {
+  const char* env = std::getenv("CKV_GATHER_BLOCKS");
+  if (env) {
+    int v = std::atoi(env);
+    if (v > 0) return v;
+  }
+  return src_kind == CKV_SRC_HOST_PINNED ? 256 : 4096;
+}
+
+SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* scores,
+                       const int32_t* ctx_lens, int32_t k, int32_t* idx, int32_t* n_sel) {
+  SelectArgs a;
+  a.scores = scores;
+  a.ctx_lens = ctx_lens;
+  a.hist = at<uint32_t>(ws, L.hist);
+  a.coarse = at<uint32_t>(ws, L.coarse);
+  a.ctrl = at<uint32_t>(ws, L.ctrl);
+  a.sel = at<int32_t>(ws, L.sel);
+  a.cand = at<uint2>(ws, L.cand);
+  a.bitmap = L.bm_words ? at<uint32_t>(ws, L.bitmap) : nullptr;
+  a.idx = idx;
+  a.n_sel = n_sel;
+  a.bm_words = L.bm_words;
+  a.Hkv = d.Hkv;
+  a.max_ctx = d.max_ctx;
+  a.k = k;
+  a.tiles = L.filter_tiles;
+  return a;
+}
+
+ScoreArgs score_args(const Dims& d, const Layout& L, const uint16_t* q,
+                     const uint16_t* keys, const int32_t* ctx_lens, float scale,
+                     float* scores, uint32_t* hist, uint32_t* coarse) {
+  ScoreArgs a;
+  a.q = q;
+  a.keys = keys;
+  a.ctx_lens = ctx_lens;
+  a.scores = scores;
+  a.hist = hist;
+  a.coarse = coarse;
+  a.key_stride = d.key_stride;
+  a.scale = scale;
+  a.Hq = d.Hq;
+  a.Hkv = d.Hkv;
+  a.max_ctx = d.max_ctx;
+  a.tiles = L.score_tiles;
+  return a;
+}
+
+AttnArgs attn_args(const Dims& d, const Layout& L, void* ws, const uint16_t* q,
+                   const uint16_t* k_rows, const uint16_t* v_rows, const int32_t* idx,
+                   const int32_t* n_sel, int64_t row_stride, int32_t k, float scale,
+                   float* out) {
+  AttnArgs a;
+  a.q = q;
+  a.k_rows = k_rows;
+  a.v_rows = v_rows;
+  a.idx = idx;
+  a.n_sel = n_sel;
+  a.part = at<float>(ws, L.part);
+  a.out = out;
+  a.row_stride = row_stride;
+  a.scale = scale;
+  a.Hq = d.Hq;
+  a.Hkv = d.Hkv;
+  a.max_ctx = d.max_ctx;
+  a.k = k;
+  a.chunks = L.chunks;
+  return a;
+}
+
+// zero -> filter -> finish, given scores and a filled first-digit histogram
+int run_select_tail(const SelectArgs& a, int units, hipStream_t s) {
+  CKV_TRY_HIP(launch_filter(a, units, s), "filter launch");
+  CKV_TRY_HIP(launch_finish(a, units, s), "finish launch");
+  return CKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ckv_abi_version(void) { return CKV_ABI_VERSION; }
+
+const char* ckv_status_str(int status) {
+  switch (status) {
+    case CKV_OK: return "ok";
+    case CKV_EINVAL: return "invalid argument";
+    case CKV_ESHAPE: return "invalid shape";
+    case CKV_EUNSUPPORTED: return "unsupported shape";
+    case CKV_EWORKSPACE: return "workspace missing or too small";
+    case CKV_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* ckv_last_error_detail(void) { return g_detail.c_str(); }
+
+int ckv_workspace_bytes(const ckv_shape* shape, int32_t k, int entry, size_t* bytes) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if (!bytes) return fail(CKV_EINVAL, "bytes is NULL");
+  if (entry != CKV_ENTRY_SELECT_TOPK && entry != CKV_ENTRY_SPARSE_DECODE_ATTN &&
+      entry != CKV_ENTRY_CRITICAL_KV_ATTN)
+    return fail(CKV_EINVAL, "unknown entry %d", entry);
+  *bytes = make_layout(d, k, entry).total;
+  return CKV_OK;
+}
+
+int ckv_score_keys(const ckv_shape* shape, const uint16_t* q, const uint16_t* k_score,
+                   const int32_t* ctx_lens, float scale, float* scores, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  CKV_PTR(q);
+  CKV_PTR(k_score);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(scores);
+  if (d.U == 0) return CKV_OK;
+  Layout L = make_layout(d, 1, 0);
+  if ((rc = check_grid(d, L))) return rc;
+  ScoreArgs a = score_args(d, L, q, k_score, ctx_lens, scale, scores, nullptr, nullptr);
+  CKV_TRY_HIP(launch_score(a, d.G, false, d.U, (hipStream_t)stream), "score launch");
+  return CKV_OK;
+}
+
+int ckv_select_topk(const ckv_shape* shape, const float* scores, const int32_t* ctx_lens,
+                    int32_t k, int32_t* idx, int32_t* n_sel, void* ws, size_t ws_bytes,
+                    void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  CKV_PTR(scores);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(idx);
+  CKV_PTR(n_sel);
+  Layout L = make_layout(d, k, CKV_ENTRY_SELECT_TOPK);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  SelectArgs a = select_args(d, L, ws, scores, ctx_lens, k, idx, n_sel);
+  CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
+  CKV_TRY_HIP(launch_hist(a, d.U, s), "hist launch");
+  return run_select_tail(a, d.U, s);
+}
+
+int ckv_gather_kv(const ckv_shape* shape, const uint16_t* k_src, const uint16_t* v_src,
+                  int src_kind, const int32_t* idx, const int32_t* n_sel, int32_t k,
+                  uint16_t* k_dst, uint16_t* v_dst, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  CKV_PTR(k_src);
+  CKV_PTR(v_src);
+  CKV_PTR(idx);
+  CKV_PTR(n_sel);
+  CKV_PTR(k_dst);
+  CKV_PTR(v_dst);
+  if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
+  if (d.U == 0) return CKV_OK;
+  GatherArgs a;
+  a.k_src = k_src;
+  a.v_src = v_src;
+  a.idx = idx;
+  a.n_sel = n_sel;
+  a.k_dst = k_dst;
+  a.v_dst = v_dst;
+  a.row_stride = d.kv_stride;
+  a.items = (int64_t)d.U * k * 32;
+  a.max_ctx = d.max_ctx;
+  a.k = k;
+  CKV_TRY_HIP(launch_gather(a, gather_blocks(src_kind), (hipStream_t)stream), "gather launch");
+  return CKV_OK;
+}
+
+int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
+                           const uint16_t* k_buf, const uint16_t* v_buf,
+                           const int32_t* n_sel, int32_t k, float scale, float* out,
+                           void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  CKV_PTR(q_att);
+  CKV_PTR(k_buf);
+  CKV_PTR(v_buf);
+  CKV_PTR(n_sel);
+  CKV_PTR(out);
+  Layout L = make_layout(d, k, CKV_ENTRY_SPARSE_DECODE_ATTN);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  AttnArgs a = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel, kD, k, scale, out);
+  CKV_TRY_HIP(launch_attn(a, d.G, false, d.U, s), "attention launch");
+  CKV_TRY_HIP(launch_combine(a, d.G, d.U, s), "combine launch");
+  return CKV_OK;
+}
+
+int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
+                         const uint16_t* q_sel, const uint16_t* k_score,
+                         const int32_t* ctx_lens, int32_t k, float scale,
+                         const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                         const uint16_t* k_buf, const uint16_t* v_buf,
+                         const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out,
+                         float* out, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  CKV_PTR(q_att);
+  if (!q_sel) q_sel = q_att;
+  CKV_PTR(q_sel);
+  CKV_PTR(k_score);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(idx_out);
+  CKV_PTR(n_sel_out);
+  CKV_PTR(out);
+  const bool pipelined = k_buf != nullptr;
+  if (pipelined) {
+    CKV_PTR(k_buf);
+    CKV_PTR(v_buf);
+    CKV_PTR(n_sel_in);
+  } else {
+    CKV_PTR(k_src);
+    CKV_PTR(v_src);
+    if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
+  }
+  Layout L = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  float* scores = at<float>(ws, L.scores);
+  SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
+  ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, sa.hist, sa.coarse);
+  CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
+  if (pipelined) {
+    AttnArgs at_ = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel_in, kD, k,
+                             scale, out);
+    CKV_TRY_HIP(launch_dual(at_, sc, d.G, d.U, s), "dual launch");
+    if ((rc = run_select_tail(sa, d.U, s))) return rc;
+    CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+  } else {
+    CKV_TRY_HIP(launch_score(sc, d.G, true, d.U, s), "score launch");
+    if ((rc = run_select_tail(sa, d.U, s))) return rc;
+    AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
+                             d.kv_stride, k, scale, out);
+    CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
+    CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+  }
+  return CKV_OK;
+}
+
+}  // extern "C"

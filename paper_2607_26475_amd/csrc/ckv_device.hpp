@@ -1,0 +1,195 @@
+// ckv_device.hpp -- device helpers and launch-argument structs shared by the
+// libckv kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ckv {
+
+constexpr int kD = 128;            // head_dim supported by the kernels
+constexpr int kWave = 64;
+
+// Scoring: one workgroup scores kScoreTile consecutive positions of one
+// (request, KV head) unit; each of its 4 waves covers a quarter of the tile
+// in MFMA blocks of 16 keys.
+constexpr int kScoreThreads = 256;
+constexpr int kScoreTile = 1024;
+constexpr int kScoreUnroll = 4;    // 16-key blocks loaded before any MFMA
+
+// Selection: the first radix digit is the top 12 bits of the order key; a
+// 64-bin coarse histogram (top 6 bits) finds its bin quickly.
+constexpr int kHistBits = 12;
+constexpr int kHistBins = 1 << kHistBits;
+constexpr int kCoarseBins = 64;
+constexpr int kCtrlWords = 4;      // per unit: above, cand, digit-1 bin, spare
+constexpr int kFilterThreads = 256;
+constexpr int kFilterTile = 4096;  // positions per filter workgroup
+constexpr int kFinishThreads = 1024;
+constexpr int kFinishLdsBytes = 128 * 1024;   // candidates or bitmap
+constexpr int kCandLds = kFinishLdsBytes / 8;  // (key, pos) pairs held in LDS
+constexpr int kBitmapLdsBits = kFinishLdsBytes * 8;
+
+// Attention: one workgroup reduces kAttnRows gathered rows of one unit into a
+// partial (running max, sum of weights, weighted V) per query head.
+constexpr int kAttnThreads = 256;
+constexpr int kAttnRows = 128;
+constexpr int kPartStride = 132;   // floats per (chunk, head): m, l, pad, pad, o[128]
+
+// Gather: one thread moves 16 bytes per item; items are (unit, slot, K|V, part).
+constexpr int kGatherThreads = 256;
+constexpr int kGatherUnroll = 4;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct ScoreArgs {
+  const uint16_t* q;        // [B][Hq][d]
+  const uint16_t* keys;     // unit rows at stride key_stride
+  const int32_t* ctx_lens;  // [B]
+  float* scores;            // [U][max_ctx]
+  uint32_t* hist;           // [U][kHistBins] or nullptr
+  uint32_t* coarse;         // [U][kCoarseBins]
+  int64_t key_stride;
+  float scale;
+  int Hq, Hkv, max_ctx, tiles;
+};
+
+struct SelectArgs {
+  const float* scores;      // [U][max_ctx]
+  const int32_t* ctx_lens;  // [B]
+  uint32_t* hist;           // [U][kHistBins]
+  uint32_t* coarse;         // [U][kCoarseBins]
+  uint32_t* ctrl;           // [U][kCtrlWords]
+  int32_t* sel;             // [U][k]   positions above the digit-1 bin, then
+                            //          the chosen candidates
+  uint2* cand;              // [U][max_ctx] (order key, position)
+  uint32_t* bitmap;         // [U][bm_words] when max_ctx > kBitmapLdsBits
+  int32_t* idx;             // [U][k]
+  int32_t* n_sel;           // [U]
+  int64_t bm_words;
+  int Hkv, max_ctx, k, tiles;
+};
+
+struct AttnArgs {
+  const uint16_t* q;        // [B][Hq][d]
+  const uint16_t* k_rows;   // buffer [U][k][d] or source rows (indexed)
+  const uint16_t* v_rows;
+  const int32_t* idx;       // indexed mode: [U][k] positions into the source
+  const int32_t* n_sel;     // [U]
+  float* part;              // [U][chunks][G][kPartStride]
+  float* out;               // [B][Hq][d]
+  int64_t row_stride;       // indexed mode: source row stride
+  float scale;
+  int Hq, Hkv, max_ctx, k, chunks;
+};
+
+struct GatherArgs {
+  const uint16_t* k_src;
+  const uint16_t* v_src;
+  const int32_t* idx;
+  const int32_t* n_sel;
+  uint16_t* k_dst;
+  uint16_t* v_dst;
+  int64_t row_stride;
+  int64_t items;            // U * k * 32
+  int max_ctx, k;
+};
+
+// ---- small device helpers ---------------------------------------------------
+
+__device__ __forceinline__ int clamp_len(int n, int hi) {
+  return n < 0 ? 0 : (n > hi ? hi : n);
+}
+
+// Monotone map from fp32 to uint32: a < b as floats <=> key(a) < key(b);
+// -0 is folded onto +0 so that equal values compare equal.
+__device__ __forceinline__ uint32_t order_key(float s) {
+  uint32_t u = __float_as_uint(s);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ uint4 ld16(const uint16_t* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming load (nontemporal hint: the line is not kept in the caches).
+__device__ __forceinline__ uint4 ld16_nt(const uint16_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Exact widening of the 8 bf16 values packed in v (lowest element first).
+__device__ __forceinline__ void unpack8(uint4 v, float* f) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Inclusive prefix sum over a workgroup of NW waves.  `tmp` is LDS scratch of
+// at least NW+1 words.  Ends with a barrier; returns the thread's inclusive
+// sum and writes the workgroup total to *total.
+template <int NW>
+__device__ __forceinline__ uint32_t block_incl_scan(uint32_t x, uint32_t* tmp,
+                                                    uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t s = wave_incl_scan(x);
+  if (lane == 63) tmp[wave] = s;
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t t = lane < NW ? tmp[lane] : 0u;
+    uint32_t ts = wave_incl_scan(t);
+    if (lane < NW) tmp[lane] = ts - t;  // exclusive wave offsets
+    if (lane == NW - 1) tmp[NW] = ts;
+  }
+  __syncthreads();
+  s += tmp[wave];
+  *total = tmp[NW];
+  __syncthreads();
+  return s;
+}
+
+}  // namespace ckv

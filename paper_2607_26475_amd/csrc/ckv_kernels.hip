@@ -1,0 +1,420 @@
+// ckv_kernels.hip -- gfx950 kernels of libckv and their host-side launchers.
+#include "ckv_attn.hpp"
+#include "ckv_launch.hpp"
+#include "ckv_score.hpp"
+#include "ckv_topk.hpp"
+
+namespace ckv {
+
+// ---- workspace clearing (a kernel, not hipMemsetAsync: safe to capture) ----
+__global__ __launch_bounds__(256) void k_zero(uint4* p, int64_t n16) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// ---- scoring -------------------------------------------------------------
+template <int G, bool HIST>
+__global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a) {
+  __shared__ uint32_t lds_hist[HIST ? kHistBins : 1];
+  const int unit = blockIdx.x / a.tiles;
+  const int tile = blockIdx.x - unit * a.tiles;
+  score_tile<G, HIST>(a, unit, tile, lds_hist);
+}
+
+// ---- selection -----------------------------------------------------------
+// First-digit histogram of given scores (standalone selection entry).
+__global__ __launch_bounds__(kScoreThreads) void k_hist(SelectArgs a) {
+  __shared__ uint32_t lds_hist[kHistBins];
+  const int unit = blockIdx.x / a.tiles;
+  const int tile = blockIdx.x - unit * a.tiles;
+  const int b = unit / a.Hkv;
+  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int j0 = tile * kFilterTile;
+  if (j0 >= n) return;
+  const int jend = min(j0 + kFilterTile, n);
+  for (int i = threadIdx.x; i < kHistBins; i += kScoreThreads) lds_hist[i] = 0u;
+  __syncthreads();
+  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
+  for (int j = j0 + threadIdx.x; j < jend; j += kScoreThreads)
+    atomicAdd(&lds_hist[order_key(srow[j]) >> (32 - kHistBits)], 1u);
+  __syncthreads();
+  flush_hist(lds_hist, a.hist + (int64_t)unit * kHistBins,
+             a.coarse + (int64_t)unit * kCoarseBins);
+}
+
+// Selects positions above the first-digit bin of the m-th largest key and
+// collects the positions inside that bin as candidates.
+__global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
+  constexpr int kPer = kFilterTile / kFilterThreads;  // 16 positions per thread
+  __shared__ uint32_t sh[4];
+  __shared__ uint32_t scan_tmp[kFilterThreads / 64 + 1];
+  const int unit = blockIdx.x / a.tiles;
+  const int tile = blockIdx.x - unit * a.tiles;
+  const int b = unit / a.Hkv;
+  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int m = min(a.k, n);
+  const int j0 = tile * kFilterTile;
+  if (m == 0 || m >= n || j0 >= n) return;  // uniform
+  if (threadIdx.x < 64)
+    find_first_bin(a.coarse + (int64_t)unit * kCoarseBins,
+                   a.hist + (int64_t)unit * kHistBins, (uint32_t)m, sh);
+  __syncthreads();
+  const uint32_t b1 = sh[0];
+  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
+  uint32_t keys[kPer];
+  uint32_t selmask = 0u, candmask = 0u;
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const int j = j0 + r * kFilterThreads + threadIdx.x;
+    keys[r] = 0u;
+    if (j < n) {
+      const uint32_t key = order_key(srow[j]);
+      const uint32_t d1 = key >> (32 - kHistBits);
+      keys[r] = key;
+      if (d1 > b1) selmask |= 1u << r;
+      else if (d1 == b1) candmask |= 1u << r;
+    }
+  }
+  const uint32_t cnt = (uint32_t)__popc(selmask) | ((uint32_t)__popc(candmask) << 16);
+  uint32_t total;
+  const uint32_t excl = block_incl_scan<kFilterThreads / 64>(cnt, scan_tmp, &total) - cnt;
+  if (threadIdx.x == 0) {
+    uint32_t* ctrl = a.ctrl + (int64_t)unit * kCtrlWords;
+    sh[2] = (total & 0xffffu) ? atomicAdd(&ctrl[0], total & 0xffffu) : 0u;
+    sh[3] = (total >> 16) ? atomicAdd(&ctrl[1], total >> 16) : 0u;
+    if (tile == 0) ctrl[2] = b1;
+  }
+  __syncthreads();
+  uint32_t os = sh[2] + (excl & 0xffffu), oc = sh[3] + (excl >> 16);
+  int32_t* sel = a.sel + (int64_t)unit * a.k;
+  uint2* cand = a.cand + (int64_t)unit * a.max_ctx;
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const int j = j0 + r * kFilterThreads + threadIdx.x;
+    if ((selmask >> r) & 1u) sel[os++] = j;
+    else if ((candmask >> r) & 1u) cand[oc++] = make_uint2(keys[r], (uint32_t)j);
+  }
+}
+
+// Writes set bits of bm[0, words) as ascending positions to out[], 16 waves
+// each owning a contiguous word range (reads are lane-consecutive).
+__device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
+                                            int32_t* out, uint32_t* tmp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kW = kFinishThreads / 64;
+  const int per = (((words + kW - 1) / kW) + 63) & ~63;
+  const int w0 = wave * per, w1 = min(w0 + per, words);
+  uint32_t cnt = 0;
+  for (int w = w0 + lane; w < w1; w += 64) cnt += (uint32_t)__popc(bm[w]);
+  cnt = wave_sum_u32(cnt);
+  if (lane == 0) tmp[wave] = cnt;
+  __syncthreads();
+  uint32_t base = 0;
+  for (int i = 0; i < wave; ++i) base += tmp[i];
+  for (int ws = w0; ws < w1; ws += 64) {
+    const int w = ws + lane;
+    uint32_t bits = w < w1 ? bm[w] : 0u;
+    const uint32_t c = (uint32_t)__popc(bits);
+    const uint32_t incl = wave_incl_scan(c);
+    uint32_t o = base + incl - c;
+    while (bits) {
+      const int bit = __ffs(bits) - 1;
+      out[o++] = w * 32 + bit;
+      bits &= bits - 1u;
+    }
+    base += __shfl(incl, 63);
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
+  __shared__ uint2 area[kCandLds];  // candidates, later the position bitmap
+  __shared__ uint32_t hist[1024];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  const int unit = blockIdx.x;
+  const int b = unit / a.Hkv;
+  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int m = min(a.k, n);
+  const int tid = threadIdx.x;
+  int32_t* idx = a.idx + (int64_t)unit * a.k;
+  if (m >= n) {  // uniform; every position (possibly none) is selected
+    for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
+    if (tid == 0) a.n_sel[unit] = m;
+    return;
+  }
+  const uint32_t* ctrl = a.ctrl + (int64_t)unit * kCtrlWords;
+  const uint32_t above = ctrl[0], nc = ctrl[1], b1 = ctrl[2];
+  const uint32_t need = (uint32_t)m - above;  // >= 1 and <= nc
+  const uint2* cg = a.cand + (int64_t)unit * a.max_ctx;
+  const bool in_lds = nc <= (uint32_t)kCandLds;
+  if (in_lds) {
+    for (uint32_t i = tid; i < nc; i += kFinishThreads) area[i] = cg[i];
+  }
+  const uint2* cs = in_lds ? area : cg;
+
+  // Second digit: bits 19..10 of the order key.
+  for (int i = tid; i < 1024; i += kFinishThreads) hist[i] = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < nc; i += kFinishThreads)
+    atomicAdd(&hist[(cs[i].x >> 10) & 1023u], 1u);
+  __syncthreads();
+  uint32_t need2;
+  const uint32_t b2 = find_bin_block<true>(hist, 1024, need, tmp, misc, &need2);
+  // Third digit: bits 9..0, among candidates whose second digit is b2.
+  for (int i = tid; i < 1024; i += kFinishThreads) hist[i] = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+    const uint32_t key = cs[i].x;
+    if (((key >> 10) & 1023u) == b2) atomicAdd(&hist[key & 1023u], 1u);
+  }
+  __syncthreads();
+  uint32_t need3;
+  const uint32_t b3 = find_bin_block<true>(hist, 1024, need2, tmp, misc, &need3);
+  const uint32_t T = (b1 << 20) | (b2 << 10) | b3;
+  const uint32_t eq = hist[b3];  // candidates with key == T
+  __syncthreads();
+
+  // Ties at T: keep the need3 lowest positions (radix select on position,
+  // ascending, 8 bits at a time).
+  uint32_t pmax = 0xffffffffu;
+  if (eq > need3) {
+    uint32_t prefix = 0u, want = need3;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < 256; i += kFinishThreads) hist[i] = 0u;
+      __syncthreads();
+      const uint32_t hi_mask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
+      for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+        const uint2 c = cs[i];
+        if (c.x == T && (c.y & hi_mask) == prefix) atomicAdd(&hist[(c.y >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      uint32_t rest;
+      const uint32_t bb = find_bin_block<false>(hist, 256, want, tmp, misc, &rest);
+      prefix |= bb << shift;
+      want = rest;
+    }
+    pmax = prefix;  // the need3-th smallest tied position
+  }
+
+  // Append the chosen candidates after the positions selected by the filter.
+  if (tid == 0) misc[4] = above;
+  __syncthreads();
+  int32_t* sel = a.sel + (int64_t)unit * a.k;
+  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+    const uint2 c = cs[i];
+    if (c.x > T || (c.x == T && c.y <= pmax)) sel[atomicAdd(&misc[4], 1u)] = (int32_t)c.y;
+  }
+  __syncthreads();
+
+  // Mark the m chosen positions in a bitmap and emit them in ascending order.
+  const int words = (n + 31) >> 5;
+  uint32_t* bm = n <= kBitmapLdsBits ? reinterpret_cast<uint32_t*>(area)
+                                     : a.bitmap + (int64_t)unit * a.bm_words;
+  for (int w = tid; w < words; w += kFinishThreads) bm[w] = 0u;
+  __syncthreads();
+  for (int i = tid; i < m; i += kFinishThreads) {
+    const int p = sel[i];
+    atomicOr(&bm[p >> 5], 1u << (p & 31));
+  }
+  __syncthreads();
+  emit_bitmap(bm, words, idx, tmp);
+  for (int i = m + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
+  if (tid == 0) a.n_sel[unit] = m;
+}
+
+// ---- attention -------------------------------------------------------------
+template <int G, bool INDEXED>
+__global__ __launch_bounds__(kAttnThreads) void k_attn(AttnArgs a) {
+  __shared__ float lds[AttnLds<G>::kFloats];
+  const int unit = blockIdx.x / a.chunks;
+  const int chunk = blockIdx.x - unit * a.chunks;
+  attn_chunk<G, INDEXED>(a, unit, chunk, lds);
+}
+
+// One launch, two roles (pipelined decode): the first attn_blocks workgroups
+// attend with q_att over the buffer assembled for this step, the rest score
+// the context with q_sel for the next step's selection.
+template <int G>
+__global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc,
+                                                      int attn_blocks) {
+  static_assert(kAttnThreads == kScoreThreads, "roles share the block size");
+  constexpr int kA = AttnLds<G>::kFloats;
+  constexpr int kS = kHistBins;
+  __shared__ float lds[kA > kS ? kA : kS];
+  if ((int)blockIdx.x < attn_blocks) {
+    const int unit = blockIdx.x / at.chunks;
+    attn_chunk<G, false>(at, unit, blockIdx.x - unit * at.chunks, lds);
+  } else {
+    const int bid = blockIdx.x - attn_blocks;
+    const int unit = bid / sc.tiles;
+    score_tile<G, true>(sc, unit, bid - unit * sc.tiles,
+                        reinterpret_cast<uint32_t*>(lds));
+  }
+}
+
+// Merges the chunk partials of every query head into the output.
+template <int G>
+__global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
+  const int unit = blockIdx.x;
+  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+  const float* pu = a.part + (int64_t)unit * a.chunks * G * kPartStride;
+  for (int o = threadIdx.x; o < G * kD; o += kAttnThreads) {
+    const int g = o / kD, c = o - g * kD;
+    float M = -INFINITY;
+    for (int ch = 0; ch < a.chunks; ++ch) M = fmaxf(M, pu[(ch * G + g) * kPartStride]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
+      for (int ch = 0; ch < a.chunks; ++ch) {
+        const float* p = pu + (ch * G + g) * kPartStride;
+        const float mc = p[0];
+        if (mc == -INFINITY) continue;
+        const float w = __expf(mc - M);
+        L = fmaf(w, p[1], L);
+        O = fmaf(w, p[4 + c], O);
+      }
+    }
+    a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = L > 0.f ? O / L : 0.f;
+  }
+}
+
+// ---- gather ----------------------------------------------------------------
+// Item it = ((unit*k + slot)*2 + kv)*16 + part moves 16 bytes; the 32 items of
+// one slot are its K row then its V row (contiguous for K|V interleaved rows).
+__global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
+  const int64_t step = (int64_t)gridDim.x * kGatherThreads * kGatherUnroll;
+  for (int64_t it0 = (int64_t)blockIdx.x * kGatherThreads * kGatherUnroll; it0 < a.items;
+       it0 += step) {
+    uint4 v[kGatherUnroll];
+    uint16_t* dst[kGatherUnroll];
+#pragma unroll
+    for (int u = 0; u < kGatherUnroll; ++u) {
+      const int64_t it = it0 + u * kGatherThreads + threadIdx.x;
+      dst[u] = nullptr;
+      if (it < a.items) {
+        const int part = (int)(it & 15);
+        const int kv = (int)((it >> 4) & 1);
+        const int64_t slot = it >> 5;
+        const int64_t unit = slot / a.k;
+        const int i = (int)(slot - unit * a.k);
+        if (i < a.n_sel[unit]) {
+          const int pos = a.idx[slot];
+          if (pos >= 0 && pos < a.max_ctx) {
+            const uint16_t* src = (kv ? a.v_src : a.k_src) +
+                                  (unit * a.max_ctx + pos) * a.row_stride + part * 8;
+            v[u] = ld16(src);
+            dst[u] = (kv ? a.v_dst : a.k_dst) + slot * kD + part * 8;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kGatherUnroll; ++u)
+      if (dst[u]) *reinterpret_cast<uint4*>(dst[u]) = v[u];
+  }
+}
+
+// ---- launchers ---------------------------------------------------------------
+static inline int blocks_for(int64_t n, int per, int cap) {
+  int64_t b = (n + per - 1) / per;
+  if (b < 1) b = 1;
+  return (int)(b > cap ? cap : b);
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero, dim3(blocks_for(n16, 256 * 4, 2048)), dim3(256), 0, s,
+                     reinterpret_cast<uint4*>(p), n16);
+  return hipGetLastError();
+}
+
+template <int G>
+static void launch_score_g(const ScoreArgs& a, bool hist, int units, hipStream_t s) {
+  const dim3 grid(units * a.tiles), block(kScoreThreads);
+  if (hist) hipLaunchKernelGGL((k_score<G, true>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((k_score<G, false>), grid, block, 0, s, a);
+}
+
+hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s) {
+  switch (G) {
+    case 1: launch_score_g<1>(a, hist, units, s); break;
+    case 2: launch_score_g<2>(a, hist, units, s); break;
+    case 4: launch_score_g<4>(a, hist, units, s); break;
+    case 8: launch_score_g<8>(a, hist, units, s); break;
+    case 16: launch_score_g<16>(a, hist, units, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s) {
+  hipLaunchKernelGGL(k_hist, dim3(units * a.tiles), dim3(kScoreThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s) {
+  hipLaunchKernelGGL(k_filter, dim3(units * a.tiles), dim3(kFilterThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(units), dim3(kFinishThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int G>
+static void launch_attn_g(const AttnArgs& a, bool indexed, int units, hipStream_t s) {
+  const dim3 grid(units * a.chunks), block(kAttnThreads);
+  if (indexed) hipLaunchKernelGGL((k_attn<G, true>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((k_attn<G, false>), grid, block, 0, s, a);
+}
+
+hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s) {
+  switch (G) {
+    case 1: launch_attn_g<1>(a, indexed, units, s); break;
+    case 2: launch_attn_g<2>(a, indexed, units, s); break;
+    case 4: launch_attn_g<4>(a, indexed, units, s); break;
+    case 8: launch_attn_g<8>(a, indexed, units, s); break;
+    case 16: launch_attn_g<16>(a, indexed, units, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
+  const dim3 grid(units), block(kAttnThreads);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(k_combine<1>, grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL(k_combine<2>, grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL(k_combine<4>, grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL(k_combine<8>, grid, block, 0, s, a); break;
+    case 16: hipLaunchKernelGGL(k_combine<16>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, int units,
+                       hipStream_t s) {
+  const int attn_blocks = units * at.chunks;
+  const dim3 grid(attn_blocks + units * sc.tiles), block(kAttnThreads);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(k_dual<1>, grid, block, 0, s, at, sc, attn_blocks); break;
+    case 2: hipLaunchKernelGGL(k_dual<2>, grid, block, 0, s, at, sc, attn_blocks); break;
+    case 4: hipLaunchKernelGGL(k_dual<4>, grid, block, 0, s, at, sc, attn_blocks); break;
+    case 8: hipLaunchKernelGGL(k_dual<8>, grid, block, 0, s, at, sc, attn_blocks); break;
+    case 16: hipLaunchKernelGGL(k_dual<16>, grid, block, 0, s, at, sc, attn_blocks); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s) {
+  const int blocks = blocks_for(a.items, kGatherThreads * kGatherUnroll, max_blocks);
+  hipLaunchKernelGGL(k_gather, dim3(blocks), dim3(kGatherThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ckv

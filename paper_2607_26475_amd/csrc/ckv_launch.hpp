@@ -1,0 +1,19 @@
+// ckv_launch.hpp -- host-side launchers of the libckv kernels.
+#pragma once
+
+#include "ckv_device.hpp"
+
+namespace ckv {
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s);
+hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s);
+hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s);
+hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s);
+hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
+hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, int units,
+                       hipStream_t s);
+hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s);
+
+}  // namespace ckv

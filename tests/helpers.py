@@ -1,0 +1,144 @@
+"""Shared pieces of the GPU parity tests: running the library, asking the
+oracle the same question, and the comparison rules.
+
+Comparison rules (the library's contract):
+  * index sets: identical to the oracle's, except for swaps among entries
+    whose oracle (fp64) scores differ by less than TIE_REL relative to the
+    oracle's m-th score; the GPU set must be duplicate-free, in range,
+    ascending and padded with -1;
+  * attention outputs: within ATOL_OUT max-abs of the oracle's attention over
+    the GPU's own index set (and of the oracle pipeline when the sets agree);
+  * gathers: bit-exact.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2607_26475_amd as ckv
+import synth
+
+SCALE = float(np.float32(1.0 / math.sqrt(128.0)))
+ATOL_OUT = 2e-3
+TIE_REL = 1e-5
+# fp32 dot product over 128 products plus the final scaling: |err| <= this
+# factor times scale * sum_c |q_c k_c| (sequential-sum worst case).
+SCORE_REL = 130 * 2.0 ** -24
+
+
+def device() -> torch.device:
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    return torch.device("cuda:0")
+
+
+def u16(t: torch.Tensor) -> np.ndarray:
+    return synth.to_u16(t)
+
+
+def bf2f(u: np.ndarray) -> np.ndarray:
+    return (np.asarray(u, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def orc() -> oracle.Oracle:
+    return oracle.get()
+
+
+def check_index_sets(gpu_idx, gpu_nsel, orc_idx, orc_nsel, S, lens, units=None):
+    """Compare GPU and oracle index sets unit by unit under the near-tie rule.
+
+    gpu_idx/orc_idx [B][Hkv][k], S the oracle's fp64 scores [B][Hkv][>=n].
+    Returns the number of units whose sets differ (by tolerated swaps)."""
+    B, Hkv, k = gpu_idx.shape
+    if units is None:
+        units = [(b, h) for b in range(B) for h in range(Hkv)]
+    swaps = 0
+    for b, h in units:
+        n = int(lens[b])
+        m = min(k, n)
+        assert gpu_nsel[b, h] == m, (b, h, gpu_nsel[b, h], m)
+        assert orc_nsel[b, h] == m
+        P = gpu_idx[b, h, :m].astype(np.int64)
+        assert np.all(gpu_idx[b, h, m:] == -1), (b, h)
+        if m:
+            assert P[0] >= 0 and P[-1] < n, (b, h, P[0], P[-1], n)
+            assert np.all(np.diff(P) > 0), (b, h, "not ascending / duplicates")
+        O = orc_idx[b, h, :m].astype(np.int64)
+        if np.array_equal(P, O):
+            continue
+        swaps += 1
+        Su = S[b, h]
+        missing = np.setdiff1d(O, P)
+        extra = np.setdiff1d(P, O)
+        assert len(missing) == len(extra)
+        tau = Su[O].min()
+        gap = Su[missing].max() - Su[extra].min()
+        assert gap <= TIE_REL * abs(tau), (b, h, len(missing), gap, tau)
+    return swaps
+
+
+def check_scores(gpu_scores, orc_scores, q_sel_u16, keys_u16, lens, G):
+    """GPU fp32 scores within the fp32 dot-product bound of the oracle's;
+    positions >= n_b exactly -inf."""
+    B, Hkv, nmax = gpu_scores.shape
+    qf = np.abs(bf2f(q_sel_u16).astype(np.float64))
+    for b in range(B):
+        for h in range(Hkv):
+            n = int(lens[b])
+            assert np.all(gpu_scores[b, h, n:] == -np.inf), (b, h)
+            if n == 0:
+                continue
+            kf = np.abs(bf2f(keys_u16[b, h, :n]).astype(np.float64))
+            mag = (qf[b, h * G:(h + 1) * G] @ kf.T).max(axis=0) * SCALE
+            err = np.abs(gpu_scores[b, h, :n].astype(np.float64) - orc_scores[b, h, :n])
+            assert np.all(err <= SCORE_REL * mag + 1e-30), (b, h, err.max())
+
+
+def oracle_attn_over(shape_o, q_att, k_src, v_src, idx, n_sel, k):
+    """Oracle attention of q_att over the rows idx of the given sources."""
+    B, Hkv = shape_o.batch, shape_o.num_kv_heads
+    d = shape_o.head_dim
+    kb = np.zeros((B, Hkv, k, d), np.uint16)
+    vb = np.zeros((B, Hkv, k, d), np.uint16)
+    o = orc()
+    o.gather_kv(shape_o, k_src.reshape(-1), v_src.reshape(-1), idx, n_sel, k, kb, vb)
+    return o.sparse_decode_attn(shape_o, q_att, kb, vb, n_sel, k, SCALE, nthreads=8)
+
+
+class Run:
+    """Device buffers and one call of the fused entry point."""
+
+    def __init__(self, w: synth.Workload, lens: torch.Tensor, dev):
+        self.w = w
+        B, Hq, Hkv, d, k = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k
+        self.idx = torch.full((B, Hkv, k), -9, dtype=torch.int32, device=dev)
+        self.n_sel = torch.full((B, Hkv), -9, dtype=torch.int32, device=dev)
+        self.out = torch.full((B, Hq, d), float("nan"), dtype=torch.float32, device=dev)
+        self.lens = lens
+
+    def same_step(self, q_att, q_sel, k_score, k_src, v_src, src_kind, key_stride=None,
+                  kv_stride=None):
+        w = self.w
+        s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx,
+                          key_row_stride=key_stride, kv_row_stride=kv_stride)
+        ws = ckv.workspace(s, w.k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        ckv.critical_kv_attn(s, q_att, q_sel, k_score, self.lens, w.k, SCALE, k_src, v_src,
+                             src_kind, None, None, None, self.idx, self.n_sel, self.out, ws)
+        torch.cuda.synchronize()
+        return s
+
+    def pipelined(self, q_att, q_sel, k_score, k_buf, v_buf, n_sel_in, key_stride=None):
+        w = self.w
+        s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx,
+                          key_row_stride=key_stride)
+        ws = ckv.workspace(s, w.k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        ckv.critical_kv_attn(s, q_att, q_sel, k_score, self.lens, w.k, SCALE, None, None,
+                             0, k_buf, v_buf, n_sel_in, self.idx, self.n_sel, self.out, ws)
+        torch.cuda.synchronize()
+        return s
+
+    def host(self):
+        return (self.idx.cpu().numpy(), self.n_sel.cpu().numpy(), self.out.cpu().numpy())

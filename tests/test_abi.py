@@ -1,0 +1,112 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments on the host before touching the device."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2607_26475_amd as ckv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ckv.h")
+FAKE = 0x100000          # 16-byte aligned, never dereferenced by these calls
+STATUS = {"OK": 0, "EINVAL": 1, "ESHAPE": 2, "EUNSUPPORTED": 3, "EWORKSPACE": 4,
+          "EHIP": 5}
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\w[\w\s\*]*?\b(ckv_\w+)\(", text, re.M)))
+
+
+def test_header_functions_are_exported():
+    declared = declared_functions()
+    assert set(declared) == set(ckv.EXPORTS), declared
+    out = subprocess.run(["nm", "-D", "--defined-only", ckv.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (ckv_\w+)$", out, re.M))
+    for name in declared:
+        assert name in exported, name
+        assert hasattr(ckv._lib, name)
+
+
+def test_abi_version_and_status_text():
+    assert ckv.abi_version() == 1
+    texts = {ckv.status_str(v) for v in STATUS.values()}
+    assert len(texts) == len(STATUS)
+    assert ckv.status_str(99) == "unknown status"
+
+
+def call_score(shape, q=FAKE, k=FAKE, lens=FAKE, scale=0.088, out=FAKE):
+    return ckv._lib.ckv_score_keys(ctypes.byref(shape), q, k, lens, scale, out, 0)
+
+
+def good_shape(**kw):
+    args = dict(batch=2, num_q_heads=8, num_kv_heads=2, max_ctx=64)
+    args.update(kw)
+    return ckv.shape_for(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_q_heads=6, num_kv_heads=4), "ESHAPE"),
+    (dict(head_dim=64), "EUNSUPPORTED"),
+    (dict(num_q_heads=6, num_kv_heads=2), "EUNSUPPORTED"),
+    (dict(num_q_heads=64, num_kv_heads=2), "EUNSUPPORTED"),
+    (dict(max_ctx=0), "ESHAPE"),
+    (dict(key_row_stride=100), "ESHAPE"),
+    (dict(kv_row_stride=132), "ESHAPE"),
+    (dict(num_kv_heads=0), "ESHAPE"),
+])
+def test_shape_validation(kw, status):
+    assert call_score(good_shape(**kw)) == STATUS[status]
+    assert ckv._lib.ckv_last_error_detail().decode() != ""
+
+
+def test_pointer_and_value_validation():
+    s = good_shape()
+    assert call_score(s, q=None) == STATUS["EINVAL"]
+    assert call_score(s, out=FAKE + 4) == STATUS["EINVAL"]        # misaligned
+    assert call_score(s, scale=0.0) == STATUS["EINVAL"]
+    assert call_score(s, scale=-1.0) == STATUS["EINVAL"]
+    assert call_score(s, scale=float("nan")) == STATUS["EINVAL"]
+    s.reserved = 1
+    assert call_score(s) == STATUS["EINVAL"]
+    assert ckv._lib.ckv_score_keys(None, FAKE, FAKE, FAKE, 0.1, FAKE, 0) == STATUS["EINVAL"]
+
+
+def test_budget_and_workspace_validation():
+    s = good_shape()
+    lib = ckv._lib
+    # k < 1
+    assert lib.ckv_select_topk(ctypes.byref(s), FAKE, FAKE, 0, FAKE, FAKE, FAKE, 1 << 20,
+                               0) == STATUS["ESHAPE"]
+    need = ckv.workspace_bytes(s, 16, ckv.ENTRY_SELECT_TOPK)
+    assert need > 0
+    # workspace missing / too small / misaligned
+    assert lib.ckv_select_topk(ctypes.byref(s), FAKE, FAKE, 16, FAKE, FAKE, None, need,
+                               0) == STATUS["EWORKSPACE"]
+    assert lib.ckv_select_topk(ctypes.byref(s), FAKE, FAKE, 16, FAKE, FAKE, FAKE, need - 1,
+                               0) == STATUS["EWORKSPACE"]
+    assert lib.ckv_select_topk(ctypes.byref(s), FAKE, FAKE, 16, FAKE, FAKE, FAKE + 16, need,
+                               0) == STATUS["EWORKSPACE"]
+    # bad src kind is rejected before any device call
+    assert lib.ckv_gather_kv(ctypes.byref(s), FAKE, FAKE, 7, FAKE, FAKE, 16, FAKE, FAKE,
+                             0) == STATUS["EINVAL"]
+    with pytest.raises(ckv.CkvError):
+        ckv.workspace_bytes(s, 16, 42)
+
+
+def test_workspace_sizes_grow_with_shape():
+    small = good_shape(max_ctx=1000)
+    big = good_shape(max_ctx=100000)
+    for e in (ckv.ENTRY_SELECT_TOPK, ckv.ENTRY_SPARSE_DECODE_ATTN,
+              ckv.ENTRY_CRITICAL_KV_ATTN):
+        a = ckv.workspace_bytes(small, 256, e)
+        assert a % 256 == 0 and a > 0
+        assert ckv.workspace_bytes(small, 1024, e) >= a
+        if e != ckv.ENTRY_SPARSE_DECODE_ATTN:
+            assert ckv.workspace_bytes(big, 256, e) > a
+    crit = ckv.workspace_bytes(small, 256, ckv.ENTRY_CRITICAL_KV_ATTN)
+    assert crit >= ckv.workspace_bytes(small, 256, ckv.ENTRY_SELECT_TOPK)
