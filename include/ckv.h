@@ -181,6 +181,46 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          int32_t* idx_out, int32_t* n_sel_out, float* out,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* ---- kernel timing -------------------------------------------------------
+ * For benchmarks and profiling, not for serving: between ckv_profile_begin()
+ * and ckv_profile_end(), every kernel the library launches carries a pair of
+ * HIP events stamped by the dispatch itself (start and end of that kernel on
+ * the caller's stream), so timing adds no packets to the stream.  The state
+ * is process-wide and guarded by a lock; calls on several threads are
+ * accumulated together. */
+typedef enum ckv_kernel_id {
+  CKV_K_ZERO = 0,     /* workspace clear                                    */
+  CKV_K_SCORE = 1,    /* scoring pass (with first-digit histogram if fused) */
+  CKV_K_HIST = 2,     /* first-digit histogram of given scores              */
+  CKV_K_FILTER = 3,   /* selection: above-bin positions and candidates      */
+  CKV_K_FINISH = 4,   /* selection: exact threshold, ordered output         */
+  CKV_K_ATTN = 5,     /* attention partials over selected rows              */
+  CKV_K_COMBINE = 6,  /* merge of attention partials                        */
+  CKV_K_DUAL = 7,     /* one launch: attention (buffer) + scoring           */
+  CKV_K_GATHER = 8,   /* sparse K/V assembly                                */
+  CKV_K_COUNT = 9
+} ckv_kernel_id;
+
+#define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)
+
+typedef struct ckv_kernel_stats {
+  int64_t launches;   /* dispatches of this kernel class                    */
+  double total_ms;    /* sum of their durations                             */
+  double max_ms;      /* longest single dispatch                            */
+} ckv_kernel_stats;
+
+/* Static name of a kernel class ("" for an unknown id). */
+const char* ckv_kernel_name(int id);
+
+/* Start recording the kernel classes whose bit (1 << ckv_kernel_id) is set
+ * in kernel_mask; other kernels launch unstamped.  Drops anything recorded
+ * before. */
+int ckv_profile_begin(uint32_t kernel_mask);
+
+/* Stop recording, wait for the recorded kernels to finish and write one
+ * entry per ckv_kernel_id into stats[0 .. CKV_K_COUNT). */
+int ckv_profile_end(ckv_kernel_stats* stats);
+
 #ifdef __cplusplus
 }
 #endif

@@ -7,7 +7,7 @@ current HIP stream to the C ABI declared in ``include/ckv.h`` and raises
 kernels of ``libckv.so``; there is no fallback.  torch is used for device
 memory, pinned host memory and streams.
 
-The library must have been built first (``python -m paper_2607_26475_amd.build``
+The library must have been built first (``python paper_2607_26475_amd/build.py``
 or ``__graft_entry__.build()``); importing this package without it raises.
 """
 from __future__ import annotations
@@ -21,7 +21,7 @@ import torch
 __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
-    "critical_kv_attn", "abi_version", "status_str", "LIB_PATH",
+    "critical_kv_attn", "profile_begin", "profile_end", "abi_version", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "EXPORTS",
 ]
@@ -32,13 +32,21 @@ SRC_DEVICE, SRC_HOST_PINNED = 0, 1
 ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
-           "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn")
+           "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
+           "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end")
+KERNEL_COUNT = 9
 
 
 class CkvError(RuntimeError):
     def __init__(self, fn: str, status: int, detail: str):
         super().__init__(f"{fn}: {status_str(status)} ({status}): {detail}")
         self.status = status
+
+
+class KernelStats(ctypes.Structure):
+    """Mirror of ``ckv_kernel_stats``."""
+    _fields_ = [("launches", ctypes.c_int64), ("total_ms", ctypes.c_double),
+                ("max_ms", ctypes.c_double)]
 
 
 class Shape(ctypes.Structure):
@@ -53,7 +61,7 @@ class Shape(ctypes.Structure):
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run "
-                          "`python -m paper_2607_26475_amd.build` first")
+                          "`python paper_2607_26475_amd/build.py` first")
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     sp = ctypes.POINTER(Shape)
@@ -70,6 +78,9 @@ def _load() -> ctypes.CDLL:
         "ckv_critical_kv_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                                 vp, vp, ctypes.c_int, vp, vp, vp, vp, vp,
                                                 vp, vp, sz, vp]),
+        "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
+        "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
+        "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -168,3 +179,27 @@ def critical_kv_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
         scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(k_buf), _ptr(v_buf),
         _ptr(n_sel_in), _ptr(idx_out), _ptr(n_sel_out), _ptr(out), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
+              "combine": 6, "dual": 7, "gather": 8}
+
+
+def profile_begin(kernels=None) -> None:
+    """Start stamping library kernels with dispatch start/end events: all of
+    them, or only the named kernel classes."""
+    mask = (1 << KERNEL_COUNT) - 1
+    if kernels is not None:
+        mask = 0
+        for name in kernels:
+            mask |= 1 << KERNEL_IDS[name]
+    _check("ckv_profile_begin", _lib.ckv_profile_begin(mask))
+
+
+def profile_end() -> dict:
+    """Stop recording; {kernel name: (launches, total_ms, max_ms)} for every
+    kernel class that ran (waits for the recorded kernels)."""
+    arr = (KernelStats * KERNEL_COUNT)()
+    _check("ckv_profile_end", _lib.ckv_profile_end(arr))
+    return {_lib.ckv_kernel_name(i).decode(): (arr[i].launches, arr[i].total_ms, arr[i].max_ms)
+            for i in range(KERNEL_COUNT) if arr[i].launches}

@@ -1,6 +1,6 @@
 """Build libckv.so (HIP, gfx950) in-tree.
 
-    python -m paper_2607_26475_amd.build
+    python paper_2607_26475_amd/build.py
 
 Every source is compiled for gfx950 only, with packed-fp32 VALU forms
 disabled.  Each translation unit is compiled to an object in parallel, then
@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libckv.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["ckv_kernels.hip", "ckv_api.cpp"]
+SOURCES = ["ckv_kernels.hip", "ckv_api.cpp", "ckv_profile.cpp"]
 
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

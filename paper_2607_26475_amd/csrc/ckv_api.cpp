@@ -103,14 +103,13 @@ struct Layout {
   size_t hist = 0, coarse = 0, ctrl = 0, zero_end = 0;
   size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0, total = 0;
   int64_t bm_words = 0;
-  int chunks = 0, score_tiles = 0, filter_tiles = 0;
+  int chunks = 0, filter_tiles = 0;
 };
 
 Layout make_layout(const Dims& d, int32_t k, int entry) {
   Layout L;
   const size_t U = (size_t)d.U;
   size_t off = 0;
-  L.score_tiles = (d.max_ctx + kScoreTile - 1) / kScoreTile;
   L.filter_tiles = (d.max_ctx + kFilterTile - 1) / kFilterTile;
   L.chunks = (k + kAttnRows - 1) / kAttnRows;
   const bool select = entry == CKV_ENTRY_SELECT_TOPK || entry == CKV_ENTRY_CRITICAL_KV_ATTN;
@@ -149,7 +148,7 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
 int check_grid(const Dims& d, const Layout& L) {
   // work-items per dispatch must stay below 2^32
   const int64_t limit = ((int64_t)1 << 32) / 1024 - 1;
-  if ((int64_t)d.U * L.score_tiles > limit || (int64_t)d.U * L.chunks > limit)
+  if ((int64_t)d.U * L.filter_tiles > limit || (int64_t)d.U * L.chunks > limit)
     return fail(CKV_EUNSUPPORTED, "grid too large for this shape");
   return CKV_OK;
 }
@@ -233,7 +232,7 @@ ScoreArgs score_args(const Dims& d, const Layout& L, const uint16_t* q,
   a.Hq = d.Hq;
   a.Hkv = d.Hkv;
   a.max_ctx = d.max_ctx;
-  a.tiles = L.score_tiles;
+  a.units = d.U;
   return a;
 }
 
@@ -259,8 +258,14 @@ AttnArgs attn_args(const Dims& d, const Layout& L, void* ws, const uint16_t* q,
   return a;
 }
 
-// zero -> filter -> finish, given scores and a filled first-digit histogram
+// Selection given scores and a filled first-digit histogram: one workgroup
+// per unit for contexts that fit its LDS, else the many-workgroup filter
+// followed by the per-unit finish.
 int run_select_tail(const SelectArgs& a, int units, hipStream_t s) {
+  if (a.max_ctx <= kFusedSelectMaxCtx) {
+    CKV_TRY_HIP(launch_select_fused(a, units, s), "select launch");
+    return CKV_OK;
+  }
   CKV_TRY_HIP(launch_filter(a, units, s), "filter launch");
   CKV_TRY_HIP(launch_finish(a, units, s), "finish launch");
   return CKV_OK;

@@ -18,17 +18,26 @@ namespace ckv {
 
 template <int G>
 struct AttnLds {
-  static constexpr int kFloats = G * kAttnRows + 4 * G * kD + 2 * G;
+  // K stage (4 waves x 32 rows, padded) | logits [G][rows] | partial sums
+  // [4 waves][G][kD] | per-head max and weight sum
+  static constexpr int kStage = 4 * kStageDwords;
+  static constexpr int kFloats = kStage + G * kAttnRows + 4 * G * kD + 2 * G;
 };
 
 // All kAttnThreads threads of the workgroup must call this.  INDEXED: rows are
 // source rows idx[unit][r] read in place; otherwise slot rows of a dense
 // [U][k][d] buffer.
+//
+// Loads: wave w owns rows [32w, 32w+32); every load instruction reads four
+// whole 256-byte rows (16 lanes x 16 bytes per row), K and V alike.  K goes
+// through a padded LDS stage into the MFMA operand placement; V stays in
+// registers in exactly the placement the weighted sum needs.
 template <int G, bool INDEXED>
 __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
                                            int chunk, float* lds) {
-  float* lg = lds;                        // [G][kAttnRows] logits, then weights
-  float* red = lds + G * kAttnRows;       // [4 waves][G][kD] partial sums
+  uint32_t* stage_all = reinterpret_cast<uint32_t*>(lds);
+  float* lg = lds + AttnLds<G>::kStage;   // [G][kAttnRows] logits, then weights
+  float* red = lg + G * kAttnRows;        // [4 waves][G][kD] partial sums
   float* stat = red + 4 * G * kD;         // [2][G] chunk max, weight sum
   const int b = unit / a.Hkv, h = unit - b * a.Hkv;
   const int nsel = clamp_len(a.n_sel[unit], a.k);
@@ -36,15 +45,15 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
   const int rows = min(kAttnRows, nsel - r0);
   float* part = a.part + ((int64_t)unit * a.chunks + chunk) * G * kPartStride;
   const int tid = threadIdx.x;
-  if (rows <= 0) {  // uniform: empty chunk
-    if (tid < G) {
-      part[tid * kPartStride] = -INFINITY;
-      part[tid * kPartStride + 1] = 0.f;
-    }
+  if (rows <= 0) {  // uniform: empty chunk (zero weight, zero sums)
+    for (int o = tid; o < G * kPartStride; o += kAttnThreads)
+      part[o] = (o % kPartStride) == 0 ? -INFINITY : 0.f;
     return;
   }
   const int lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
+  const int lrow = lane >> 4, lchunk = lane & 15;
+  uint32_t* stage = stage_all + wave * kStageDwords;
 
   auto row_off = [&](int i) -> int64_t {
     if (INDEXED) {
@@ -55,27 +64,17 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
     return ((int64_t)unit * a.k + r0 + i) * kD;
   };
 
-  // V rows for the weighted sum: wave w covers rows [32w, 32w+32), four rows
-  // per load (16 lanes x 16 bytes per 256-byte row).  Issued first so that
-  // they are in flight with the K loads.
-  uint4 vr[8];
+  // K and V of rows 32w + 4it + lrow, 16-byte chunk lchunk of each.
+  uint4 kr[8], vr[8];
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
-    const int i = wave * 32 + it * 4 + kg;
+    const int i = wave * 32 + it * 4 + lrow;
+    kr[it] = make_uint4(0u, 0u, 0u, 0u);
     vr[it] = make_uint4(0u, 0u, 0u, 0u);
-    if (i < rows) vr[it] = ld16(a.v_rows + row_off(i) + 8 * r16);
-  }
-  uint4 kk[2][4];
-#pragma unroll
-  for (int bk = 0; bk < 2; ++bk) {
-    const int i = wave * 32 + bk * 16 + r16;
     if (i < rows) {
-      const uint16_t* p = a.k_rows + row_off(i) + 8 * kg;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) kk[bk][t] = ld16(p + 32 * t);
-    } else {
-#pragma unroll
-      for (int t = 0; t < 4; ++t) kk[bk][t] = make_uint4(0u, 0u, 0u, 0u);
+      const int64_t off = row_off(i) + 8 * lchunk;
+      kr[it] = ld16(a.k_rows + off);
+      vr[it] = ld16(a.v_rows + off);
     }
   }
   bf16x8 qa[4];
@@ -90,10 +89,18 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
     }
   }
 #pragma unroll
+  for (int it = 0; it < 8; ++it)
+    *reinterpret_cast<uint4*>(stage + (4 * it + lrow) * kStageRowDwords + 4 * lchunk) = kr[it];
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
   for (int bk = 0; bk < 2; ++bk) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc = mfma_16x16x32(qa[t], as_bf16x8(kk[bk][t]), acc);
+    for (int t = 0; t < 4; ++t) {
+      const uint4 kv = *reinterpret_cast<const uint4*>(
+          stage + (16 * bk + r16) * kStageRowDwords + 4 * (4 * t + kg));
+      acc = mfma_16x16x32(qa[t], as_bf16x8(kv), acc);
+    }
     const int r = wave * 32 + bk * 16 + r16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -119,7 +126,7 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
   }
   __syncthreads();
 
-  // Weighted V sum: lane holds channels [8*r16, +8) of 8 rows.
+  // Weighted V sum: lane holds channels [8*lchunk, +8) of 8 rows.
   float acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g)
@@ -127,7 +134,7 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
-    const int i = wave * 32 + it * 4 + kg;
+    const int i = wave * 32 + it * 4 + lrow;
     float vf[8];
     unpack8(vr[it], vf);
 #pragma unroll
@@ -146,18 +153,18 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
       x += __shfl_xor(x, 32);
       acc[g][e] = x;
     }
-  if (kg == 0) {
+  if (lrow == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) red[(wave * G + g) * kD + 8 * r16 + e] = acc[g][e];
+      for (int e = 0; e < 8; ++e) red[(wave * G + g) * kD + 8 * lchunk + e] = acc[g][e];
   }
   __syncthreads();
   for (int o = tid; o < G * kD; o += kAttnThreads) {
     const int g = o / kD, c = o - g * kD;
-    const float s = red[(0 * G + g) * kD + c] + red[(1 * G + g) * kD + c] +
-                    red[(2 * G + g) * kD + c] + red[(3 * G + g) * kD + c];
-    part[g * kPartStride + 4 + c] = s;
+    const float sum = red[(0 * G + g) * kD + c] + red[(1 * G + g) * kD + c] +
+                      red[(2 * G + g) * kD + c] + red[(3 * G + g) * kD + c];
+    part[g * kPartStride + 4 + c] = sum;
   }
   if (tid < G) {
     part[tid * kPartStride] = stat[tid];

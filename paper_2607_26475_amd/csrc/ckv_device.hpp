@@ -10,16 +10,19 @@ namespace ckv {
 constexpr int kD = 128;            // head_dim supported by the kernels
 constexpr int kWave = 64;
 
-// Scoring: one workgroup scores kScoreTile consecutive positions of one
-// (request, KV head) unit; each of its 4 waves covers a quarter of the tile
-// in MFMA blocks of 16 keys.
+// Scoring: a persistent grid; each workgroup scores a balanced contiguous
+// range of kStageRows-key groups (4 waves, MFMA blocks of 16 keys).
 constexpr int kScoreThreads = 256;
-constexpr int kScoreTile = 1024;
-constexpr int kScoreUnroll = 4;    // 16-key blocks loaded before any MFMA
+constexpr int kStageRows = 32;     // key rows staged per wave per step
+constexpr int kStageRowDwords = 68;  // 256-byte row + 16-byte pad (bank spread)
+constexpr int kStageDwords = kStageRows * kStageRowDwords;
+constexpr int kFlushGroups = 64;   // groups of scores held per wave in LDS
+constexpr int kScoreLdsDwords = 4 * kStageDwords + 4 * kFlushGroups * kStageRows;
 
-// Selection: the first radix digit is the top 12 bits of the order key; a
-// 64-bin coarse histogram (top 6 bits) finds its bin quickly.
-constexpr int kHistBits = 12;
+// Selection: the first radix digit is the top 11 bits of the order key; a
+// 64-bin coarse histogram (top 6 bits) finds its bin quickly.  The remaining
+// 21 bits are resolved in two digits of 11 and 10 bits.
+constexpr int kHistBits = 11;
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kCoarseBins = 64;
 constexpr int kCtrlWords = 4;      // per unit: above, cand, digit-1 bin, spare
@@ -29,6 +32,9 @@ constexpr int kFinishThreads = 1024;
 constexpr int kFinishLdsBytes = 128 * 1024;   // candidates or bitmap
 constexpr int kCandLds = kFinishLdsBytes / 8;  // (key, pos) pairs held in LDS
 constexpr int kBitmapLdsBits = kFinishLdsBytes * 8;
+// Contexts up to this many positions are selected by one workgroup per unit
+// in a single kernel (scores read once, everything else in LDS).
+constexpr int kFusedSelectMaxCtx = 65536;
 
 // Attention: one workgroup reduces kAttnRows gathered rows of one unit into a
 // partial (running max, sum of weights, weighted V) per query head.
@@ -52,7 +58,7 @@ struct ScoreArgs {
   uint32_t* coarse;         // [U][kCoarseBins]
   int64_t key_stride;
   float scale;
-  int Hq, Hkv, max_ctx, tiles;
+  int Hq, Hkv, max_ctx, units;
 };
 
 struct SelectArgs {
@@ -156,6 +162,20 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
   return x;
+}
+
+// Wave-aggregated append: lanes with `flag` get consecutive slots from the
+// counter at *ctr (one atomic per wave); returns this lane's slot.
+__device__ __forceinline__ uint32_t wave_append(bool flag, uint32_t* ctr) {
+  const unsigned long long mask = __ballot(flag);
+  const uint32_t cnt = (uint32_t)__popcll(mask);
+  const uint32_t lo = (uint32_t)mask, hi = (uint32_t)(mask >> 32);
+  const uint32_t rank = __builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
+  const int leader = cnt ? __ffsll(mask) - 1 : 0;
+  uint32_t base = 0u;
+  if (cnt && (int)(threadIdx.x & 63) == leader) base = atomicAdd(ctr, cnt);
+  base = __shfl(base, leader);
+  return base + rank;
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave.

@@ -1,6 +1,7 @@
 // ckv_kernels.hip -- gfx950 kernels of libckv and their host-side launchers.
 #include "ckv_attn.hpp"
 #include "ckv_launch.hpp"
+#include "ckv_profile.hpp"
 #include "ckv_score.hpp"
 #include "ckv_topk.hpp"
 
@@ -17,9 +18,8 @@ __global__ __launch_bounds__(256) void k_zero(uint4* p, int64_t n16) {
 template <int G, bool HIST>
 __global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a) {
   __shared__ uint32_t lds_hist[HIST ? kHistBins : 1];
-  const int unit = blockIdx.x / a.tiles;
-  const int tile = blockIdx.x - unit * a.tiles;
-  score_tile<G, HIST>(a, unit, tile, lds_hist);
+  __shared__ __attribute__((aligned(16))) uint32_t lds_stage[kScoreLdsDwords];
+  score_range<G, HIST>(a, blockIdx.x, gridDim.x, lds_hist, lds_stage);
 }
 
 // ---- selection -----------------------------------------------------------
@@ -56,12 +56,19 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
   const int m = min(a.k, n);
   const int j0 = tile * kFilterTile;
   if (m == 0 || m >= n || j0 >= n) return;  // uniform
+  // issue the score loads first; the bin lookup below overlaps their latency
+  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
+  float sv[kPer];
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const int j = j0 + r * kFilterThreads + threadIdx.x;
+    sv[r] = j < n ? srow[j] : 0.f;
+  }
   if (threadIdx.x < 64)
     find_first_bin(a.coarse + (int64_t)unit * kCoarseBins,
                    a.hist + (int64_t)unit * kHistBins, (uint32_t)m, sh);
   __syncthreads();
   const uint32_t b1 = sh[0];
-  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
   uint32_t keys[kPer];
   uint32_t selmask = 0u, candmask = 0u;
 #pragma unroll
@@ -69,7 +76,7 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
     const int j = j0 + r * kFilterThreads + threadIdx.x;
     keys[r] = 0u;
     if (j < n) {
-      const uint32_t key = order_key(srow[j]);
+      const uint32_t key = order_key(sv[r]);
       const uint32_t d1 = key >> (32 - kHistBits);
       keys[r] = key;
       if (d1 > b1) selmask |= 1u << r;
@@ -128,9 +135,66 @@ __device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
   __syncthreads();
 }
 
+// Radix select among candidates (order key, position) that share the first
+// digit b1: the need largest by (key descending, position ascending).
+// Returns the threshold key T; candidates with key > T are all chosen, and of
+// those equal to T the ones with position <= *pmax.  All kFinishThreads
+// threads call this; hist needs 2048 words.
+__device__ __forceinline__ uint32_t refine_threshold(const uint2* cs, uint32_t nc,
+                                                     uint32_t need, uint32_t b1,
+                                                     uint32_t* hist, uint32_t* tmp,
+                                                     uint32_t* misc, uint32_t* pmax) {
+  const int tid = threadIdx.x;
+  // Second digit: bits 20..10 of the order key (11 bits).
+  static_assert(kHistBits == 11, "digits 11 + 11 + 10");
+  for (int i = tid; i < 2048; i += kFinishThreads) hist[i] = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < nc; i += kFinishThreads)
+    atomicAdd(&hist[(cs[i].x >> 10) & 2047u], 1u);
+  __syncthreads();
+  uint32_t need2;
+  const uint32_t b2 = find_bin_block<true>(hist, 2048, need, tmp, misc, &need2);
+  // Third digit: bits 9..0, among candidates whose second digit is b2.
+  for (int i = tid; i < 1024; i += kFinishThreads) hist[i] = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+    const uint32_t key = cs[i].x;
+    if (((key >> 10) & 2047u) == b2) atomicAdd(&hist[key & 1023u], 1u);
+  }
+  __syncthreads();
+  uint32_t need3;
+  const uint32_t b3 = find_bin_block<true>(hist, 1024, need2, tmp, misc, &need3);
+  const uint32_t T = (b1 << 21) | (b2 << 10) | b3;
+  const uint32_t eq = hist[b3];  // candidates with key == T
+  __syncthreads();
+
+  // Ties at T: keep the need3 lowest positions (radix select on position,
+  // ascending, 8 bits at a time).
+  *pmax = 0xffffffffu;
+  if (eq > need3) {
+    uint32_t prefix = 0u, want = need3;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < 256; i += kFinishThreads) hist[i] = 0u;
+      __syncthreads();
+      const uint32_t hi_mask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
+      for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+        const uint2 c = cs[i];
+        if (c.x == T && (c.y & hi_mask) == prefix) atomicAdd(&hist[(c.y >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      uint32_t rest;
+      const uint32_t bb = find_bin_block<false>(hist, 256, want, tmp, misc, &rest);
+      prefix |= bb << shift;
+      want = rest;
+    }
+    *pmax = prefix;  // the need3-th smallest tied position
+  }
+  return T;
+}
+
 __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
   __shared__ uint2 area[kCandLds];  // candidates, later the position bitmap
-  __shared__ uint32_t hist[1024];
+  __shared__ uint32_t hist[2048];
   __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
   __shared__ uint32_t misc[8];
   const int unit = blockIdx.x;
@@ -153,58 +217,23 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
     for (uint32_t i = tid; i < nc; i += kFinishThreads) area[i] = cg[i];
   }
   const uint2* cs = in_lds ? area : cg;
-
-  // Second digit: bits 19..10 of the order key.
-  for (int i = tid; i < 1024; i += kFinishThreads) hist[i] = 0u;
-  __syncthreads();
-  for (uint32_t i = tid; i < nc; i += kFinishThreads)
-    atomicAdd(&hist[(cs[i].x >> 10) & 1023u], 1u);
-  __syncthreads();
-  uint32_t need2;
-  const uint32_t b2 = find_bin_block<true>(hist, 1024, need, tmp, misc, &need2);
-  // Third digit: bits 9..0, among candidates whose second digit is b2.
-  for (int i = tid; i < 1024; i += kFinishThreads) hist[i] = 0u;
-  __syncthreads();
-  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
-    const uint32_t key = cs[i].x;
-    if (((key >> 10) & 1023u) == b2) atomicAdd(&hist[key & 1023u], 1u);
-  }
-  __syncthreads();
-  uint32_t need3;
-  const uint32_t b3 = find_bin_block<true>(hist, 1024, need2, tmp, misc, &need3);
-  const uint32_t T = (b1 << 20) | (b2 << 10) | b3;
-  const uint32_t eq = hist[b3];  // candidates with key == T
-  __syncthreads();
-
-  // Ties at T: keep the need3 lowest positions (radix select on position,
-  // ascending, 8 bits at a time).
-  uint32_t pmax = 0xffffffffu;
-  if (eq > need3) {
-    uint32_t prefix = 0u, want = need3;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += kFinishThreads) hist[i] = 0u;
-      __syncthreads();
-      const uint32_t hi_mask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
-      for (uint32_t i = tid; i < nc; i += kFinishThreads) {
-        const uint2 c = cs[i];
-        if (c.x == T && (c.y & hi_mask) == prefix) atomicAdd(&hist[(c.y >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      uint32_t rest;
-      const uint32_t bb = find_bin_block<false>(hist, 256, want, tmp, misc, &rest);
-      prefix |= bb << shift;
-      want = rest;
-    }
-    pmax = prefix;  // the need3-th smallest tied position
-  }
+  uint32_t pmax;
+  const uint32_t T = refine_threshold(cs, nc, need, b1, hist, tmp, misc, &pmax);
 
   // Append the chosen candidates after the positions selected by the filter.
   if (tid == 0) misc[4] = above;
   __syncthreads();
   int32_t* sel = a.sel + (int64_t)unit * a.k;
-  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
-    const uint2 c = cs[i];
-    if (c.x > T || (c.x == T && c.y <= pmax)) sel[atomicAdd(&misc[4], 1u)] = (int32_t)c.y;
+  for (uint32_t i0 = 0; i0 < nc; i0 += kFinishThreads) {
+    const uint32_t i = i0 + tid;
+    bool take = false;
+    uint2 c = make_uint2(0u, 0u);
+    if (i < nc) {
+      c = cs[i];
+      take = c.x > T || (c.x == T && c.y <= pmax);
+    }
+    const uint32_t slot = wave_append(take, &misc[4]);
+    if (take) sel[slot] = (int32_t)c.y;
   }
   __syncthreads();
 
@@ -217,6 +246,73 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
   for (int i = tid; i < m; i += kFinishThreads) {
     const int p = sel[i];
     atomicOr(&bm[p >> 5], 1u << (p & 31));
+  }
+  __syncthreads();
+  emit_bitmap(bm, words, idx, tmp);
+  for (int i = m + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
+  if (tid == 0) a.n_sel[unit] = m;
+}
+
+// Whole selection of one unit in one workgroup, for n_b <= kFusedSelectMaxCtx:
+// reads the unit's scores once, marks positions above the first-digit bin in
+// an LDS bitmap, collects the bin's candidates, resolves the threshold and
+// emits the chosen positions in ascending order.
+__global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
+  __shared__ uint2 cand[kCandLds];
+  __shared__ uint32_t bm[kFusedSelectMaxCtx / 32];
+  __shared__ uint32_t hist[2048];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  const int unit = blockIdx.x;
+  const int b = unit / a.Hkv;
+  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int m = min(a.k, n);
+  const int tid = threadIdx.x;
+  int32_t* idx = a.idx + (int64_t)unit * a.k;
+  if (m >= n) {  // uniform; every position (possibly none) is selected
+    for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
+    if (tid == 0) a.n_sel[unit] = m;
+    return;
+  }
+  if (tid < 64)
+    find_first_bin(a.coarse + (int64_t)unit * kCoarseBins,
+                   a.hist + (int64_t)unit * kHistBins, (uint32_t)m, misc + 4);
+  const int words = (n + 31) >> 5;
+  for (int w = tid; w < words; w += kFinishThreads) bm[w] = 0u;
+  if (tid == 0) misc[6] = 0u;
+  __syncthreads();
+  const uint32_t b1 = misc[4], above = misc[5];
+  const uint32_t need = (uint32_t)m - above;
+  const uint32_t nc_expect = a.hist[(int64_t)unit * kHistBins + b1];
+  uint2* cs = nc_expect <= (uint32_t)kCandLds ? cand : a.cand + (int64_t)unit * a.max_ctx;
+  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
+  constexpr int kUnroll = 8;
+  for (int j0 = 0; j0 < n; j0 += kFinishThreads * kUnroll) {
+    float sv[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int j = j0 + u * kFinishThreads + tid;
+      sv[u] = j < n ? srow[j] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int j = j0 + u * kFinishThreads + tid;
+      const uint32_t key = order_key(sv[u]);
+      const uint32_t d1 = key >> (32 - kHistBits);
+      const bool valid = j < n;
+      if (valid && d1 > b1) atomicOr(&bm[j >> 5], 1u << (j & 31));
+      const bool is_cand = valid && d1 == b1;
+      const uint32_t slot = wave_append(is_cand, &misc[6]);
+      if (is_cand) cs[slot] = make_uint2(key, (uint32_t)j);
+    }
+  }
+  __syncthreads();
+  const uint32_t nc = misc[6];
+  uint32_t pmax;
+  const uint32_t T = refine_threshold(cs, nc, need, b1, hist, tmp, misc, &pmax);
+  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+    const uint2 c = cs[i];
+    if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
   }
   __syncthreads();
   emit_bitmap(bm, words, idx, tmp);
@@ -241,26 +337,62 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
                                                       int attn_blocks) {
   static_assert(kAttnThreads == kScoreThreads, "roles share the block size");
   constexpr int kA = AttnLds<G>::kFloats;
-  constexpr int kS = kHistBins;
-  __shared__ float lds[kA > kS ? kA : kS];
+  constexpr int kS = kHistBins + kScoreLdsDwords;
+  __shared__ __attribute__((aligned(16))) float lds[kA > kS ? kA : kS];
   if ((int)blockIdx.x < attn_blocks) {
     const int unit = blockIdx.x / at.chunks;
     attn_chunk<G, false>(at, unit, blockIdx.x - unit * at.chunks, lds);
   } else {
-    const int bid = blockIdx.x - attn_blocks;
-    const int unit = bid / sc.tiles;
-    score_tile<G, true>(sc, unit, bid - unit * sc.tiles,
-                        reinterpret_cast<uint32_t*>(lds));
+    uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
+    score_range<G, true>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks,
+                         l32 + kScoreLdsDwords, l32);
   }
 }
 
-// Merges the chunk partials of every query head into the output.
+// Merges the chunk partials of every query head into the output.  The
+// per-chunk (max, weight sum) pairs go through LDS first so that each thread's
+// loads of the weighted sums are independent of one another.
 template <int G>
 __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
+  constexpr int kMaxChunks = 64;
+  __shared__ float s_m[G][kMaxChunks], s_w[G][kMaxChunks], s_inv[G];
   const int unit = blockIdx.x;
   const int b = unit / a.Hkv, h = unit - b * a.Hkv;
   const float* pu = a.part + (int64_t)unit * a.chunks * G * kPartStride;
-  for (int o = threadIdx.x; o < G * kD; o += kAttnThreads) {
+  const int tid = threadIdx.x;
+  if (a.chunks <= kMaxChunks) {
+    const int nc = a.chunks;
+    for (int i = tid; i < nc * G; i += kAttnThreads) {
+      const int ch = i / G, g = i - ch * G;
+      s_m[g][ch] = pu[(ch * G + g) * kPartStride];
+      s_w[g][ch] = pu[(ch * G + g) * kPartStride + 1];
+    }
+    __syncthreads();
+    if (tid < G) {  // per head: global max, chunk weights exp(m_c - M), 1/L
+      const int g = tid;
+      float M = -INFINITY;
+      for (int ch = 0; ch < nc; ++ch) M = fmaxf(M, s_m[g][ch]);
+      float L = 0.f;
+      for (int ch = 0; ch < nc; ++ch) {
+        const float w = s_m[g][ch] == -INFINITY ? 0.f : __expf(s_m[g][ch] - M);
+        L = fmaf(w, s_w[g][ch], L);
+        s_m[g][ch] = w;
+      }
+      s_inv[g] = L > 0.f ? 1.f / L : 0.f;
+    }
+    __syncthreads();
+    for (int o = tid; o < G * kD; o += kAttnThreads) {
+      const int g = o / kD, c = o - g * kD;
+      float O = 0.f;  // empty chunks carry weight 0 and zero sums
+#pragma unroll 8
+      for (int ch = 0; ch < nc; ++ch)
+        O = fmaf(s_m[g][ch], pu[(ch * G + g) * kPartStride + 4 + c], O);
+      a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = O * s_inv[g];
+    }
+    return;
+  }
+  // More chunks than fit in LDS: straightforward per-output loop.
+  for (int o = tid; o < G * kD; o += kAttnThreads) {
     const int g = o / kD, c = o - g * kD;
     float M = -INFINITY;
     for (int ch = 0; ch < a.chunks; ++ch) M = fmaxf(M, pu[(ch * G + g) * kPartStride]);
@@ -268,9 +400,8 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
     if (M != -INFINITY) {
       for (int ch = 0; ch < a.chunks; ++ch) {
         const float* p = pu + (ch * G + g) * kPartStride;
-        const float mc = p[0];
-        if (mc == -INFINITY) continue;
-        const float w = __expf(mc - M);
+        if (p[0] == -INFINITY) continue;
+        const float w = __expf(p[0] - M);
         L = fmaf(w, p[1], L);
         O = fmaf(w, p[4 + c], O);
       }
@@ -325,50 +456,82 @@ static inline int blocks_for(int64_t n, int per, int cap) {
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   const int64_t n16 = (int64_t)(bytes / 16);
   if (n16 == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_zero, dim3(blocks_for(n16, 256 * 4, 2048)), dim3(256), 0, s,
-                     reinterpret_cast<uint4*>(p), n16);
+  launch_kernel(CKV_K_ZERO, k_zero, dim3(blocks_for(n16, 256 * 4, 2048)), dim3(256), s,
+                reinterpret_cast<uint4*>(p), n16);
   return hipGetLastError();
 }
 
+// Workgroups that fit on the device at once for a 256-thread kernel; the
+// persistent scoring grid is this many workgroups (or fewer if less work).
+static int resident_blocks(const void* fn) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 1024;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus < 1)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kScoreThreads, 0) !=
+          hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  return cus * per_cu;
+}
+
+static int score_grid(const ScoreArgs& a, const void* fn) {
+  const int64_t groups = (int64_t)a.units * ((a.max_ctx + kStageRows - 1) / kStageRows);
+  const int64_t slots = resident_blocks(fn);
+  return (int)(groups < slots ? groups : slots);
+}
+
 template <int G>
-static void launch_score_g(const ScoreArgs& a, bool hist, int units, hipStream_t s) {
-  const dim3 grid(units * a.tiles), block(kScoreThreads);
-  if (hist) hipLaunchKernelGGL((k_score<G, true>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((k_score<G, false>), grid, block, 0, s, a);
+static void launch_score_g(const ScoreArgs& a, bool hist, hipStream_t s) {
+  const dim3 block(kScoreThreads);
+  if (hist) {
+    auto fn = k_score<G, true>;
+    launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
+  } else {
+    auto fn = k_score<G, false>;
+    launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
+  }
 }
 
 hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s) {
+  (void)units;
   switch (G) {
-    case 1: launch_score_g<1>(a, hist, units, s); break;
-    case 2: launch_score_g<2>(a, hist, units, s); break;
-    case 4: launch_score_g<4>(a, hist, units, s); break;
-    case 8: launch_score_g<8>(a, hist, units, s); break;
-    case 16: launch_score_g<16>(a, hist, units, s); break;
+    case 1: launch_score_g<1>(a, hist, s); break;
+    case 2: launch_score_g<2>(a, hist, s); break;
+    case 4: launch_score_g<4>(a, hist, s); break;
+    case 8: launch_score_g<8>(a, hist, s); break;
+    case 16: launch_score_g<16>(a, hist, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s) {
-  hipLaunchKernelGGL(k_hist, dim3(units * a.tiles), dim3(kScoreThreads), 0, s, a);
+  launch_kernel(CKV_K_HIST, k_hist, dim3(units * a.tiles), dim3(kScoreThreads), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s) {
-  hipLaunchKernelGGL(k_filter, dim3(units * a.tiles), dim3(kFilterThreads), 0, s, a);
+  launch_kernel(CKV_K_FILTER, k_filter, dim3(units * a.tiles), dim3(kFilterThreads), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s) {
-  hipLaunchKernelGGL(k_finish, dim3(units), dim3(kFinishThreads), 0, s, a);
+  launch_kernel(CKV_K_FINISH, k_finish, dim3(units), dim3(kFinishThreads), s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_fused(const SelectArgs& a, int units, hipStream_t s) {
+  launch_kernel(CKV_K_FINISH, k_select_fused, dim3(units), dim3(kFinishThreads), s, a);
   return hipGetLastError();
 }
 
 template <int G>
 static void launch_attn_g(const AttnArgs& a, bool indexed, int units, hipStream_t s) {
   const dim3 grid(units * a.chunks), block(kAttnThreads);
-  if (indexed) hipLaunchKernelGGL((k_attn<G, true>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((k_attn<G, false>), grid, block, 0, s, a);
+  if (indexed) launch_kernel(CKV_K_ATTN, k_attn<G, true>, grid, block, s, a);
+  else launch_kernel(CKV_K_ATTN, k_attn<G, false>, grid, block, s, a);
 }
 
 hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s) {
@@ -386,26 +549,34 @@ hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStr
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
   const dim3 grid(units), block(kAttnThreads);
   switch (G) {
-    case 1: hipLaunchKernelGGL(k_combine<1>, grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL(k_combine<2>, grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL(k_combine<4>, grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL(k_combine<8>, grid, block, 0, s, a); break;
-    case 16: hipLaunchKernelGGL(k_combine<16>, grid, block, 0, s, a); break;
+    case 1: launch_kernel(CKV_K_COMBINE, k_combine<1>, grid, block, s, a); break;
+    case 2: launch_kernel(CKV_K_COMBINE, k_combine<2>, grid, block, s, a); break;
+    case 4: launch_kernel(CKV_K_COMBINE, k_combine<4>, grid, block, s, a); break;
+    case 8: launch_kernel(CKV_K_COMBINE, k_combine<8>, grid, block, s, a); break;
+    case 16: launch_kernel(CKV_K_COMBINE, k_combine<16>, grid, block, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+template <int G>
+static void launch_dual_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks,
+                          hipStream_t s) {
+  auto fn = k_dual<G>;
+  const int score_blocks = score_grid(sc, (const void*)fn);
+  launch_kernel(CKV_K_DUAL, fn, dim3(attn_blocks + score_blocks), dim3(kAttnThreads), s, at,
+                sc, attn_blocks);
+}
+
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, int units,
                        hipStream_t s) {
   const int attn_blocks = units * at.chunks;
-  const dim3 grid(attn_blocks + units * sc.tiles), block(kAttnThreads);
   switch (G) {
-    case 1: hipLaunchKernelGGL(k_dual<1>, grid, block, 0, s, at, sc, attn_blocks); break;
-    case 2: hipLaunchKernelGGL(k_dual<2>, grid, block, 0, s, at, sc, attn_blocks); break;
-    case 4: hipLaunchKernelGGL(k_dual<4>, grid, block, 0, s, at, sc, attn_blocks); break;
-    case 8: hipLaunchKernelGGL(k_dual<8>, grid, block, 0, s, at, sc, attn_blocks); break;
-    case 16: hipLaunchKernelGGL(k_dual<16>, grid, block, 0, s, at, sc, attn_blocks); break;
+    case 1: launch_dual_g<1>(at, sc, attn_blocks, s); break;
+    case 2: launch_dual_g<2>(at, sc, attn_blocks, s); break;
+    case 4: launch_dual_g<4>(at, sc, attn_blocks, s); break;
+    case 8: launch_dual_g<8>(at, sc, attn_blocks, s); break;
+    case 16: launch_dual_g<16>(at, sc, attn_blocks, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -413,7 +584,7 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, int units
 
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s) {
   const int blocks = blocks_for(a.items, kGatherThreads * kGatherUnroll, max_blocks);
-  hipLaunchKernelGGL(k_gather, dim3(blocks), dim3(kGatherThreads), 0, s, a);
+  launch_kernel(CKV_K_GATHER, k_gather, dim3(blocks), dim3(kGatherThreads), s, a);
   return hipGetLastError();
 }
 

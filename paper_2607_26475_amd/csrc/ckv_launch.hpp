@@ -10,6 +10,7 @@ hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStre
 hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s);
+hipError_t launch_select_fused(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, int units,

@@ -1,0 +1,100 @@
+// ckv_profile.cpp -- event pool and aggregation behind ckv_profile_*().
+#include <atomic>
+#include <mutex>
+#include <vector>
+
+#include "ckv_profile.hpp"
+
+namespace ckv {
+namespace {
+
+struct Record {
+  int id;
+  hipEvent_t start, stop;
+};
+
+std::atomic<bool> g_on{false};
+std::atomic<uint32_t> g_mask{0};
+std::mutex g_mu;
+std::vector<Record> g_records;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t take_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void recycle_all() {
+  for (const Record& r : g_records) {
+    g_pool.push_back(r.start);
+    g_pool.push_back(r.stop);
+  }
+  g_records.clear();
+}
+
+}  // namespace
+
+bool profile_events(int id, hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_on.load(std::memory_order_relaxed)) return false;
+  if (!((g_mask.load(std::memory_order_relaxed) >> id) & 1u)) return false;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_on.load(std::memory_order_relaxed)) return false;
+  hipEvent_t a = take_event(), b = take_event();
+  if (!a || !b) {
+    if (a) g_pool.push_back(a);
+    if (b) g_pool.push_back(b);
+    return false;
+  }
+  g_records.push_back({id, a, b});
+  *start = a;
+  *stop = b;
+  return true;
+}
+
+}  // namespace ckv
+
+extern "C" {
+
+const char* ckv_kernel_name(int id) {
+  static const char* names[CKV_K_COUNT] = {"zero", "score", "hist", "filter", "finish",
+                                           "attn", "combine", "dual", "gather"};
+  return (id >= 0 && id < CKV_K_COUNT) ? names[id] : "";
+}
+
+int ckv_profile_begin(uint32_t kernel_mask) {
+  std::lock_guard<std::mutex> lk(ckv::g_mu);
+  ckv::recycle_all();
+  ckv::g_mask.store(kernel_mask & CKV_K_ALL);
+  ckv::g_on.store(true);
+  return CKV_OK;
+}
+
+int ckv_profile_end(ckv_kernel_stats* stats) {
+  if (!stats) return CKV_EINVAL;
+  std::lock_guard<std::mutex> lk(ckv::g_mu);
+  ckv::g_on.store(false);
+  for (int i = 0; i < CKV_K_COUNT; ++i) stats[i] = ckv_kernel_stats{0, 0.0, 0.0};
+  int rc = CKV_OK;
+  for (const ckv::Record& r : ckv::g_records) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.stop) != hipSuccess ||
+        hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+      rc = CKV_EHIP;
+      continue;
+    }
+    ckv_kernel_stats& s = stats[r.id];
+    s.launches += 1;
+    s.total_ms += ms;
+    if (ms > s.max_ms) s.max_ms = ms;
+  }
+  ckv::recycle_all();
+  return rc;
+}
+
+}  // extern "C"

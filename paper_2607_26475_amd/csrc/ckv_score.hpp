@@ -9,8 +9,7 @@
 //
 // Operand placement (wave64): lane l holds key (l % 16) of the block as the B
 // operand and query head (l % 16) as the A operand; lane group kg = l / 16
-// supplies channels [32t + 8kg, 32t + 8kg + 8) of step t, so each load
-// instruction reads 64 contiguous bytes of 16 key rows.  The accumulator of
+// supplies channels [32t + 8kg, 32t + 8kg + 8) of step t.  The accumulator of
 // lane l then holds heads 4kg..4kg+3 of key (l % 16).
 #pragma once
 
@@ -19,19 +18,20 @@
 namespace ckv {
 
 // Adds the workgroup's LDS histogram into the unit's global fine and coarse
-// histograms (kScoreThreads threads, kHistBins bins).
+// histograms (kScoreThreads threads, kHistBins bins, kBinsPerThread each).
 __device__ __forceinline__ void flush_hist(const uint32_t* lds_hist,
                                            uint32_t* g_hist,
                                            uint32_t* g_coarse) {
-  static_assert(kHistBins == 16 * kScoreThreads, "16 bins per thread");
-  static_assert(kHistBins / kCoarseBins == 64, "4 threads per coarse bin");
+  constexpr int kBinsPerThread = kHistBins / kScoreThreads;
+  constexpr int kThreadsPerCoarse = kHistBins / kCoarseBins / kBinsPerThread;
+  static_assert(kThreadsPerCoarse == 4, "4 threads per coarse bin");
   const int t = threadIdx.x;
   uint32_t csum = 0;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const uint32_t v = lds_hist[16 * t + i];
+  for (int i = 0; i < kBinsPerThread; ++i) {
+    const uint32_t v = lds_hist[kBinsPerThread * t + i];
     if (v) {
-      atomicAdd(&g_hist[16 * t + i], v);
+      atomicAdd(&g_hist[kBinsPerThread * t + i], v);
       csum += v;
     }
   }
@@ -40,86 +40,169 @@ __device__ __forceinline__ void flush_hist(const uint32_t* lds_hist,
   if ((t & 3) == 0 && csum) atomicAdd(&g_coarse[t >> 2], csum);
 }
 
-// Scores positions [tile*kScoreTile, +kScoreTile) of `unit` into a.scores
-// (fp32, -inf at and beyond n_b) and, if HIST, counts their first radix digit.
-// Must be called by all kScoreThreads threads of the workgroup.
+// Scores a balanced share of the whole batch: the positions of every unit are
+// cut into groups of kStageRows keys, the groups of all units are numbered
+// unit-major, and workgroup `wg` of `nwg` takes the contiguous range
+// [wg*T/nwg, (wg+1)*T/nwg) of the T groups.  A range spans few units; for each
+// unit it touches the workgroup loads that unit's G query rows once and, if
+// HIST, counts the first radix digit of its scores in LDS and adds the counts
+// to the unit's histogram when it leaves the unit.  Groups at or beyond n_b
+// only write -inf.  Must be called by all kScoreThreads threads.
+//
+// Memory path: each wave takes a contiguous quarter of the range's groups,
+// reads each group with fully coalesced 16-byte loads (one instruction = 4 whole 256-byte rows),
+// writes it to a private, padded LDS stage and reads it back in the MFMA
+// operand placement while the loads of its next group are in flight.  Loading
+// the operand placement straight from HBM (16 rows x 64 bytes per
+// instruction) costs about a tenth of the achievable bandwidth.
+//
+// Scores are collected in a per-wave LDS buffer and written out every
+// kFlushGroups groups as one contiguous run (for a Llama-8B-sized batch that
+// is once, at the end of the range).  A global store pending in the loop
+// would make every wait for the current group also wait for the prefetched
+// one (loads and stores share one counter), and score writes interleaved
+// with the key stream cost bandwidth even in large batches: about 10 % at
+// every 16 groups against 2 % when written once.
 template <int G, bool HIST>
-__device__ __forceinline__ void score_tile(const ScoreArgs& a, int unit,
-                                           int tile, uint32_t* lds_hist) {
-  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
-  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
-  const int j0 = tile * kScoreTile;
-  const int jend = min(j0 + kScoreTile, a.max_ctx);
-  float* srow = a.scores + (int64_t)unit * a.max_ctx;
+__device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
+                                            uint32_t* lds_hist,
+                                            uint32_t* lds_stage) {
   const int tid = threadIdx.x;
-  if (j0 >= n) {  // uniform over the workgroup
-    for (int j = j0 + tid; j < jend; j += kScoreThreads) srow[j] = -INFINITY;
-    return;
-  }
-  if (HIST) {
-    for (int i = tid; i < kHistBins; i += kScoreThreads) lds_hist[i] = 0u;
-    __syncthreads();
-  }
   const int lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
+  const int lrow = lane >> 4, lchunk = lane & 15;
+  constexpr int kLoads = kStageRows / 4;  // 4 rows per load instruction
+  const int64_t gpu_groups = (a.max_ctx + kStageRows - 1) / kStageRows;  // per unit
+  const int64_t total = (int64_t)a.units * gpu_groups;
+  const int64_t g0 = total * wg / nwg, g1 = total * (wg + 1) / nwg;
+  uint32_t* stage = lds_stage + wave * kStageDwords;
+  float* sbuf = reinterpret_cast<float*>(lds_stage + 4 * kStageDwords) +
+                wave * kFlushGroups * kStageRows;
 
-  bf16x8 qa[4];
-  {
-    const uint16_t* qrow =
-        a.q + ((int64_t)b * a.Hq + (int64_t)h * G + r16) * kD + 8 * kg;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (r16 < G) v = ld16(qrow + 32 * t);
-      qa[t] = as_bf16x8(v);
+  for (int64_t seg = g0; seg < g1;) {
+    const int unit = (int)(seg / gpu_groups);
+    const int64_t ubase = (int64_t)unit * gpu_groups;
+    const int64_t seg_end = min(g1, ubase + gpu_groups);
+    const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+    const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+    float* srow = a.scores + (int64_t)unit * a.max_ctx;
+    // groups [ubase + first_empty, ...) hold no position below n_b
+    const int64_t valid_end = min(seg_end, ubase + (n + kStageRows - 1) / kStageRows);
+    for (int64_t gg = max(seg, valid_end); gg < seg_end; ++gg) {
+      const int j = (int)(gg - ubase) * kStageRows + (tid & (kStageRows - 1));
+      if (tid < kStageRows && j < a.max_ctx) srow[j] = -INFINITY;
     }
-  }
-  const uint16_t* kbase =
-      a.keys + (int64_t)unit * a.max_ctx * a.key_stride + 8 * kg;
-  const int wj0 = j0 + wave * (kScoreTile / 4);
-  constexpr int kBlocks = kScoreTile / 4 / 16;
-
-  for (int blk = 0; blk < kBlocks; blk += kScoreUnroll) {
-    uint4 kv[kScoreUnroll][4];
-#pragma unroll
-    for (int u = 0; u < kScoreUnroll; ++u) {
-      const int j = wj0 + (blk + u) * 16 + r16;
-      if (j < n) {
-        const uint16_t* p = kbase + (int64_t)j * a.key_stride;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) kv[u][t] = ld16_nt(p + 32 * t);
-      } else {
-#pragma unroll
-        for (int t = 0; t < 4; ++t) kv[u][t] = make_uint4(0u, 0u, 0u, 0u);
+    if (seg < valid_end) {  // uniform over the workgroup
+      if (HIST) {
+        for (int i = tid; i < kHistBins; i += kScoreThreads) lds_hist[i] = 0u;
+        __syncthreads();
       }
-    }
+      bf16x8 qa[4];
+      {
+        const uint16_t* qrow =
+            a.q + ((int64_t)b * a.Hq + (int64_t)h * G + r16) * kD + 8 * kg;
 #pragma unroll
-    for (int u = 0; u < kScoreUnroll; ++u) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int t = 0; t < 4; ++t) acc = mfma_16x16x32(qa[t], as_bf16x8(kv[u][t]), acc);
-      float s = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (4 * kg + i < G) s = fmaxf(s, acc[i]);
-      if (G > 4) s = fmaxf(s, __shfl_xor(s, 16));
-      if (G > 8) s = fmaxf(s, __shfl_xor(s, 32));
-      s *= a.scale;
-      const int j = wj0 + (blk + u) * 16 + lane;
-      if (lane < 16) {
-        if (j < n) {
-          srow[j] = s;
-          if (HIST) atomicAdd(&lds_hist[order_key(s) >> (32 - kHistBits)], 1u);
-        } else if (j < jend) {
-          srow[j] = -INFINITY;
+        for (int t = 0; t < 4; ++t) {
+          uint4 v = make_uint4(0u, 0u, 0u, 0u);
+          if (r16 < G) v = ld16(qrow + 32 * t);
+          qa[t] = as_bf16x8(v);
         }
       }
+      const uint16_t* kunit = a.keys + (int64_t)unit * a.max_ctx * a.key_stride;
+      auto load_group = [&](int64_t gg, uint4* v) {
+        const int jb = (int)(gg - ubase) * kStageRows;
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) {
+          const int j = jb + 4 * i + lrow;
+          v[i] = j < n ? ld16_nt(kunit + (int64_t)j * a.key_stride + 8 * lchunk)
+                       : make_uint4(0u, 0u, 0u, 0u);
+        }
+      };
+      // writes the scores of the nb buffered groups [first, first + nb): one
+      // contiguous run, 16 bytes per lane when rows are 16-byte aligned
+      auto flush = [&](int64_t first, int nb) {
+        __builtin_amdgcn_wave_barrier();
+        const int jb = (int)(first - ubase) * kStageRows;
+        const int count = nb * kStageRows;
+        if ((a.max_ctx & 3) == 0) {
+          for (int c = 4 * lane; c < count; c += 256) {
+            const float4 v = *reinterpret_cast<const float4*>(sbuf + c);
+            const int j = jb + c;
+            if (j + 3 < a.max_ctx) {
+              *reinterpret_cast<float4*>(srow + j) = v;
+            } else {
+              if (j < a.max_ctx) srow[j] = v.x;
+              if (j + 1 < a.max_ctx) srow[j + 1] = v.y;
+              if (j + 2 < a.max_ctx) srow[j + 2] = v.z;
+            }
+          }
+        } else {
+          for (int c = lane; c < count; c += 64)
+            if (jb + c < a.max_ctx) srow[jb + c] = sbuf[c];
+        }
+        __builtin_amdgcn_wave_barrier();
+      };
+      // this wave's contiguous share of the segment's groups below n_b
+      const int64_t span = valid_end - seg;
+      const int64_t w0 = seg + span * wave / 4, w1 = seg + span * (wave + 1) / 4;
+      uint4 cur[kLoads], nxt[kLoads];
+      int64_t gg = w0;
+      int64_t first = gg;
+      int nb = 0;
+      if (gg < w1) load_group(gg, cur);
+#pragma unroll 1
+      for (; gg < w1; ++gg) {
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i)
+          *reinterpret_cast<uint4*>(stage + (4 * i + lrow) * kStageRowDwords + 4 * lchunk) =
+              cur[i];
+        if (gg + 1 < w1) load_group(gg + 1, nxt);
+        __builtin_amdgcn_wave_barrier();
+        const int jb = (int)(gg - ubase) * kStageRows;
+#pragma unroll
+        for (int u = 0; u < kStageRows / 16; ++u) {
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const uint4 kv = *reinterpret_cast<const uint4*>(
+                stage + (16 * u + r16) * kStageRowDwords + 4 * (4 * t + kg));
+            acc = mfma_16x16x32(qa[t], as_bf16x8(kv), acc);
+          }
+          float sc = -INFINITY;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (4 * kg + i < G) sc = fmaxf(sc, acc[i]);
+          if (G > 4) sc = fmaxf(sc, __shfl_xor(sc, 16));
+          if (G > 8) sc = fmaxf(sc, __shfl_xor(sc, 32));
+          sc *= a.scale;
+          const int j = jb + 16 * u + lane;
+          if (lane < 16) {
+            if (j < n) {
+              if (HIST) atomicAdd(&lds_hist[order_key(sc) >> (32 - kHistBits)], 1u);
+            } else {
+              sc = -INFINITY;
+            }
+            sbuf[nb * kStageRows + 16 * u + lane] = sc;
+          }
+        }
+        if (++nb == kFlushGroups) {
+          flush(first, nb);
+          first = gg + 1;
+          nb = 0;
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) cur[i] = nxt[i];
+      }
+      if (nb) flush(first, nb);
+      if (HIST) {
+        __syncthreads();
+        flush_hist(lds_hist, a.hist + (int64_t)unit * kHistBins,
+                   a.coarse + (int64_t)unit * kCoarseBins);
+        __syncthreads();
+      }
     }
-  }
-  if (HIST) {
-    __syncthreads();
-    flush_hist(lds_hist, a.hist + (int64_t)unit * kHistBins,
-               a.coarse + (int64_t)unit * kCoarseBins);
+    seg = seg_end;
   }
 }
 

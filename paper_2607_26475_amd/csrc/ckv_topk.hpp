@@ -3,13 +3,13 @@
 // retrieved; one index set per KV head).
 //
 // Three passes, all exact:
-//   1. histogram of the first digit (top 12 bits of the order key), fused
+//   1. histogram of the first digit (top 11 bits of the order key), fused
 //      into the scoring pass or run over given scores;
 //   2. filter (many workgroups per unit): positions whose first digit is
 //      above the bin holding the m-th largest key are selected outright;
 //      positions in that bin become candidates (order key, position);
 //   3. finish (one workgroup per unit): radix select over the candidates on
-//      the remaining 20 bits finds the exact threshold key T; ties at T are
+//      the remaining 21 bits finds the exact threshold key T; ties at T are
 //      resolved by lower position; the chosen positions are marked in a
 //      bitmap and written out in ascending order.
 #pragma once
@@ -23,6 +23,8 @@ namespace ckv {
 __device__ __forceinline__ void find_first_bin(const uint32_t* coarse,
                                                const uint32_t* hist,
                                                uint32_t m, uint32_t* out) {
+  constexpr int kFine = kHistBins / kCoarseBins;  // fine bins per coarse bin
+  static_assert(kCoarseBins == 64 && kFine <= 64, "one lane per bin");
   const int lane = threadIdx.x & 63;
   const uint32_t c = coarse[kCoarseBins - 1 - lane];  // descending bins
   const uint32_t s = wave_incl_scan(c);
@@ -30,21 +32,22 @@ __device__ __forceinline__ void find_first_bin(const uint32_t* coarse,
   if (L < 0) L = kCoarseBins - 1;  // only if the histogram were inconsistent
   const uint32_t above_c = __shfl(s - c, L);
   const int sb = kCoarseBins - 1 - L;
-  const uint32_t f = hist[sb * 64 + 63 - lane];
+  const uint32_t f = lane < kFine ? hist[sb * kFine + kFine - 1 - lane] : 0u;
   const uint32_t s2 = wave_incl_scan(f) + above_c;
-  int L2 = __ffsll((unsigned long long)__ballot(s2 >= m)) - 1;
-  if (L2 < 0) L2 = 63;
+  int L2 = __ffsll((unsigned long long)__ballot(lane < kFine && s2 >= m)) - 1;
+  if (L2 < 0) L2 = kFine - 1;
   const uint32_t above = __shfl(s2 - f, L2);
   if (lane == 0) {
-    out[0] = (uint32_t)(sb * 64 + 63 - L2);
+    out[0] = (uint32_t)(sb * kFine + kFine - 1 - L2);
     out[1] = above;
   }
 }
 
-// All threads of a kFinishThreads workgroup: given a histogram of nb <= 1024
-// bins in LDS, find the bin where the running count (from the top bin down
-// when desc, else from bin 0 up) first reaches `need`.  Returns the bin and
-// sets *rest to the number still needed inside that bin.
+// All threads of a kFinishThreads workgroup: given a histogram of nb bins in
+// LDS (nb a multiple of kFinishThreads or at most kFinishThreads), find the
+// bin where the running count (from the top bin down when DESC, else from
+// bin 0 up) first reaches `need`.  Returns the bin and sets *rest to the
+// number still needed inside that bin.
 template <bool DESC>
 __device__ __forceinline__ uint32_t find_bin_block(const uint32_t* hist, int nb,
                                                    uint32_t need, uint32_t* tmp,
@@ -55,13 +58,26 @@ __device__ __forceinline__ uint32_t find_bin_block(const uint32_t* hist, int nb,
     misc[0] = 0u;
     misc[1] = 0u;
   }
-  const int bin = DESC ? nb - 1 - t : t;
-  const uint32_t v = t < nb ? hist[bin] : 0u;
+  const int per = nb > kFinishThreads ? nb / kFinishThreads : 1;
+  // thread t owns scan positions [t*per, t*per + per)
+  auto bin_at = [&](int pos) { return DESC ? nb - 1 - pos : pos; };
+  uint32_t v = 0u;
+  if (t * per < nb)
+    for (int i = 0; i < per; ++i) v += hist[bin_at(t * per + i)];
   uint32_t total;
   const uint32_t incl = block_incl_scan<kFinishThreads / 64>(v, tmp, &total);
-  if (t < nb && incl >= need && incl - v < need) {
-    misc[0] = (uint32_t)bin;
-    misc[1] = need - (incl - v);
+  if (t * per < nb && incl >= need && incl - v < need) {
+    uint32_t run = incl - v;
+    for (int i = 0; i < per; ++i) {
+      const int bin = bin_at(t * per + i);
+      const uint32_t c = hist[bin];
+      if (run + c >= need) {
+        misc[0] = (uint32_t)bin;
+        misc[1] = need - run;
+        break;
+      }
+      run += c;
+    }
   }
   __syncthreads();
   const uint32_t b = misc[0];

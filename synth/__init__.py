@@ -34,7 +34,8 @@ from typing import Dict, Optional
 import numpy as np
 import torch
 
-__all__ = ["Workload", "WORKLOADS", "make_layer", "to_u16", "generator"]
+__all__ = ["Workload", "WORKLOADS", "make_layer", "to_u16", "generator",
+           "interleave_kv", "host_kv"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -173,6 +174,21 @@ def make_layer(w: Workload, seed: int = 0, layer: int = 0,
                     k[b, h, pos] = rows.to(torch.bfloat16)
     return {"q": q, "q_sel": q_sel, "k": k, "v": v, "ctx_lens": lens,
             "marked": marked}
+
+
+def interleave_kv(k: torch.Tensor, v: torch.Tensor) -> torch.Tensor:
+    """K and V interleaved per row on k's device: [B][Hkv][n][2][d].
+
+    Row j of (b, h) holds its key then its value (2*d contiguous bf16), so a
+    selected position is one 512-byte read; keys are rows at stride 2*d from
+    the start, values the same from element d.
+    """
+    B, Hkv, n, d = k.shape
+    out = torch.empty((B, Hkv, n, 2, d), dtype=torch.bfloat16, device=k.device)
+    for b in range(B):
+        out[b, :, :, 0].copy_(k[b])
+        out[b, :, :, 1].copy_(v[b])
+    return out
 
 
 def host_kv(k: torch.Tensor, v: torch.Tensor) -> torch.Tensor:
