@@ -181,6 +181,60 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          int32_t* idx_out, int32_t* n_sel_out, float* out,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* ---- layer pipeline --------------------------------------------------------
+ * The decode loop of Sec. 5.3 (layer-aware transfer overlap) and Sec. 5.4
+ * (two-layer ping-pong buffer): the set selected for a layer at step t-1 is
+ * gathered into one of two layer-scoped buffers on a copy stream while the
+ * compute stream works on the previous layer; the gather for layer l+2 starts
+ * as soon as the attention of layer l has released its buffer.  The compute
+ * stream waits for a buffer's fill event before attending over it (no
+ * read-after-write hazard) and the copy stream waits for its release event
+ * before refilling it (no write-after-read hazard).  Layer g of the decode
+ * (counting layers across steps) uses buffer g % 2.
+ *
+ * Per layer the caller provides: */
+typedef struct ckv_layer {
+  const uint16_t* q_att;      /* [B][Hq][d] query of the current token         */
+  const uint16_t* q_sel;      /* [B][Hq][d] query of the speculative token,    */
+                              /* NULL => q_att                                 */
+  const uint16_t* k_score;    /* scoring keys (device, key_row_stride)          */
+  const uint16_t* k_src;      /* K rows gathered into the buffer (src_kind,     */
+  const uint16_t* v_src;      /* kv_row_stride); V rows likewise                */
+  const int32_t* idx_prev;    /* [B][Hkv][k] set selected at the previous step  */
+  const int32_t* n_sel_prev;  /* [B][Hkv]                                       */
+  int32_t* idx_next;          /* [B][Hkv][k] written: selected at this step     */
+  int32_t* n_sel_next;        /* [B][Hkv] written                               */
+  float* out;                 /* [B][Hq][d] written: attention output           */
+} ckv_layer;
+
+typedef struct ckv_pipeline ckv_pipeline; /* events of one decode loop */
+
+/* Creates the events of one decode loop on the current device. */
+int ckv_pipeline_create(ckv_pipeline** pipe);
+int ckv_pipeline_destroy(ckv_pipeline* pipe);
+
+/* Starts a decode loop: gathers layer 0 (into buffer 0) and layer 1 (into
+ * buffer 1) from their idx_prev/n_sel_prev on copy_stream.  Buffers are
+ * k_buf[i], v_buf[i], each [B][Hkv][k][d] bf16 on the device. */
+int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
+                       const ckv_layer* layers, int num_layers, int src_kind,
+                       uint16_t* const k_buf[2], uint16_t* const v_buf[2],
+                       void* copy_stream);
+
+/* One decode step over num_layers >= 2 layers.  For each layer l, on
+ * compute_stream: ckv_critical_kv_attn in pipelined mode (attention of q_att
+ * over the buffer holding idx_prev's rows, selection from q_sel into
+ * idx_next); on copy_stream: the refill of the released buffer with layer
+ * l+2, or, for the last two layers, with the next step's layers 0 and 1 from
+ * this step's idx_next.  Before the next step the caller swaps idx_prev and
+ * idx_next.  ws is the workspace of CKV_ENTRY_CRITICAL_KV_ATTN, used on the
+ * compute stream only. */
+int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
+                    const ckv_layer* layers, const int32_t* ctx_lens, int32_t k,
+                    float scale, int src_kind, uint16_t* const k_buf[2],
+                    uint16_t* const v_buf[2], void* ws, size_t ws_bytes,
+                    void* compute_stream, void* copy_stream);
+
 /* ---- kernel timing -------------------------------------------------------
  * For benchmarks and profiling, not for serving: between ckv_profile_begin()
  * and ckv_profile_end(), every kernel the library launches carries a pair of

@@ -21,7 +21,8 @@ import torch
 __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
-    "critical_kv_attn", "profile_begin", "profile_end", "abi_version", "status_str", "LIB_PATH",
+    "critical_kv_attn", "profile_begin", "profile_end", "abi_version", "Layer",
+    "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "EXPORTS",
 ]
@@ -33,7 +34,9 @@ ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
-           "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end")
+           "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
+           "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_prime",
+           "ckv_decode_step")
 KERNEL_COUNT = 9
 
 
@@ -47,6 +50,13 @@ class KernelStats(ctypes.Structure):
     """Mirror of ``ckv_kernel_stats``."""
     _fields_ = [("launches", ctypes.c_int64), ("total_ms", ctypes.c_double),
                 ("max_ms", ctypes.c_double)]
+
+
+class Layer(ctypes.Structure):
+    """Mirror of ``ckv_layer``."""
+    _fields_ = [(name, ctypes.c_void_p) for name in (
+        "q_att", "q_sel", "k_score", "k_src", "v_src", "idx_prev", "n_sel_prev",
+        "idx_next", "n_sel_next", "out")]
 
 
 class Shape(ctypes.Structure):
@@ -81,6 +91,15 @@ def _load() -> ctypes.CDLL:
         "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
+        "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
+        "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
+        "ckv_pipeline_prime": (ctypes.c_int, [vp, sp, i32, ctypes.POINTER(Layer), ctypes.c_int,
+                                              ctypes.c_int, ctypes.POINTER(vp),
+                                              ctypes.POINTER(vp), vp]),
+        "ckv_decode_step": (ctypes.c_int, [vp, sp, ctypes.c_int, ctypes.POINTER(Layer), vp,
+                                           i32, ctypes.c_float, ctypes.c_int,
+                                           ctypes.POINTER(vp), ctypes.POINTER(vp), vp, sz, vp,
+                                           vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -203,3 +222,55 @@ def profile_end() -> dict:
     _check("ckv_profile_end", _lib.ckv_profile_end(arr))
     return {_lib.ckv_kernel_name(i).decode(): (arr[i].launches, arr[i].total_ms, arr[i].max_ms)
             for i in range(KERNEL_COUNT) if arr[i].launches}
+
+
+def _layers(layers) -> "ctypes.Array":
+    """dicts with the ckv_layer field names (tensors, ints or None) -> array."""
+    arr = (Layer * len(layers))()
+    for i, d in enumerate(layers):
+        for name, _ in Layer._fields_:
+            setattr(arr[i], name, _ptr(d.get(name)))
+    return arr
+
+
+class Pipeline:
+    """The two-buffer decode loop of ``ckv_decode_step`` (owns its events)."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check("ckv_pipeline_create", _lib.ckv_pipeline_create(ctypes.byref(h)))
+        self._h = h
+
+    def close(self) -> None:
+        if self._h:
+            _lib.ckv_pipeline_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @staticmethod
+    def _bufs(k_buf, v_buf):
+        kb = (ctypes.c_void_p * 2)(_ptr(k_buf[0]), _ptr(k_buf[1]))
+        vb = (ctypes.c_void_p * 2)(_ptr(v_buf[0]), _ptr(v_buf[1]))
+        return kb, vb
+
+    def prime(self, shape: Shape, k: int, layers, src_kind: int, k_buf, v_buf,
+              copy_stream) -> None:
+        arr = _layers(layers)
+        kb, vb = self._bufs(k_buf, v_buf)
+        _check("ckv_pipeline_prime", _lib.ckv_pipeline_prime(
+            self._h, ctypes.byref(shape), k, arr, len(layers), src_kind, kb, vb,
+            _stream(copy_stream)))
+
+    def step(self, shape: Shape, layers, ctx_lens, k: int, scale: float, src_kind: int,
+             k_buf, v_buf, ws, compute_stream, copy_stream) -> None:
+        arr = _layers(layers)
+        kb, vb = self._bufs(k_buf, v_buf)
+        _check("ckv_decode_step", _lib.ckv_decode_step(
+            self._h, ctypes.byref(shape), len(layers), arr, _ptr(ctx_lens), k, scale,
+            src_kind, kb, vb, _ptr(ws), ws.numel(), _stream(compute_stream),
+            _stream(copy_stream)))

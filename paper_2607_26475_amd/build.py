@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libckv.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["ckv_kernels.hip", "ckv_api.cpp", "ckv_profile.cpp"]
+SOURCES = ["ckv_kernels.hip", "ckv_api.cpp", "ckv_profile.cpp", "ckv_pipeline.cpp"]
 
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

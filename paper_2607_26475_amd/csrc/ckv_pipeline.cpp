@@ -1,0 +1,105 @@
+// ckv_pipeline.cpp -- the two-buffer decode loop: compute stream and copy
+// stream ordered by fill and release events.
+#include <hip/hip_runtime.h>
+
+#include <new>
+
+#include "ckv.h"
+
+struct ckv_pipeline {
+  hipEvent_t filled[2];  // buffer i holds the rows of the layer about to use it
+  hipEvent_t freed[2];   // the attention that read buffer i has been enqueued before this
+  int parity;            // buffer of the next layer to compute
+};
+
+namespace {
+
+int gather_layer(const ckv_shape* shape, int32_t k, const ckv_layer& L, const int32_t* idx,
+                 const int32_t* n_sel, int src_kind, uint16_t* kb, uint16_t* vb,
+                 void* stream) {
+  return ckv_gather_kv(shape, L.k_src, L.v_src, src_kind, idx, n_sel, k, kb, vb, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+int ckv_pipeline_create(ckv_pipeline** pipe) {
+  if (!pipe) return CKV_EINVAL;
+  ckv_pipeline* p = new (std::nothrow) ckv_pipeline();
+  if (!p) return CKV_EINVAL;
+  for (int i = 0; i < 2; ++i) {
+    if (hipEventCreateWithFlags(&p->filled[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&p->freed[i], hipEventDisableTiming) != hipSuccess) {
+      delete p;
+      return CKV_EHIP;
+    }
+  }
+  p->parity = 0;
+  *pipe = p;
+  return CKV_OK;
+}
+
+int ckv_pipeline_destroy(ckv_pipeline* pipe) {
+  if (!pipe) return CKV_OK;
+  for (int i = 0; i < 2; ++i) {
+    (void)hipEventDestroy(pipe->filled[i]);
+    (void)hipEventDestroy(pipe->freed[i]);
+  }
+  delete pipe;
+  return CKV_OK;
+}
+
+int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
+                       const ckv_layer* layers, int num_layers, int src_kind,
+                       uint16_t* const k_buf[2], uint16_t* const v_buf[2],
+                       void* copy_stream) {
+  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf) return CKV_EINVAL;
+  pipe->parity = 0;
+  for (int l = 0; l < 2; ++l) {
+    int rc = gather_layer(shape, k, layers[l], layers[l].idx_prev, layers[l].n_sel_prev,
+                          src_kind, k_buf[l], v_buf[l], copy_stream);
+    if (rc) return rc;
+    if (hipEventRecord(pipe->filled[l], (hipStream_t)copy_stream) != hipSuccess)
+      return CKV_EHIP;
+  }
+  return CKV_OK;
+}
+
+int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
+                    const ckv_layer* layers, const int32_t* ctx_lens, int32_t k,
+                    float scale, int src_kind, uint16_t* const k_buf[2],
+                    uint16_t* const v_buf[2], void* ws, size_t ws_bytes,
+                    void* compute_stream, void* copy_stream) {
+  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf) return CKV_EINVAL;
+  hipStream_t cs = (hipStream_t)compute_stream, xs = (hipStream_t)copy_stream;
+  for (int l = 0; l < num_layers; ++l) {
+    const int p = pipe->parity;
+    const ckv_layer& L = layers[l];
+    // attention over buffer p once its gather has landed
+    if (hipStreamWaitEvent(cs, pipe->filled[p], 0) != hipSuccess) return CKV_EHIP;
+    int rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
+                                  nullptr, nullptr, src_kind, k_buf[p], v_buf[p],
+                                  L.n_sel_prev, L.idx_next, L.n_sel_next, L.out, ws,
+                                  ws_bytes, compute_stream);
+    if (rc) return rc;
+    if (hipEventRecord(pipe->freed[p], cs) != hipSuccess) return CKV_EHIP;
+    // refill buffer p with the layer two ahead (into the next step at the end)
+    if (hipStreamWaitEvent(xs, pipe->freed[p], 0) != hipSuccess) return CKV_EHIP;
+    const int j = l + 2;
+    if (j < num_layers) {
+      rc = gather_layer(shape, k, layers[j], layers[j].idx_prev, layers[j].n_sel_prev,
+                        src_kind, k_buf[p], v_buf[p], copy_stream);
+    } else {
+      const ckv_layer& N = layers[j - num_layers];
+      rc = gather_layer(shape, k, N, N.idx_next, N.n_sel_next, src_kind, k_buf[p], v_buf[p],
+                        copy_stream);
+    }
+    if (rc) return rc;
+    if (hipEventRecord(pipe->filled[p], xs) != hipSuccess) return CKV_EHIP;
+    pipe->parity ^= 1;
+  }
+  return CKV_OK;
+}
+
+}  // extern "C"

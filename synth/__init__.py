@@ -136,7 +136,8 @@ def make_layer(w: Workload, seed: int = 0, layer: int = 0,
     if ctx_override is not None:
         lens = torch.full((B,), int(ctx_override), dtype=torch.int32)
     elif w.ctx_min < n:
-        gl = generator(w.name, seed, layer, "len", "cpu")
+        # a request's context length is the same in every layer
+        gl = generator(w.name, seed, 0, "len", "cpu")
         lens = torch.randint(w.ctx_min, n + 1, (B,), generator=gl,
                              dtype=torch.int64).to(torch.int32)
     else:

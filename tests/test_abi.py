@@ -110,3 +110,16 @@ def test_workspace_sizes_grow_with_shape():
             assert ckv.workspace_bytes(big, 256, e) > a
     crit = ckv.workspace_bytes(small, 256, ckv.ENTRY_CRITICAL_KV_ATTN)
     assert crit >= ckv.workspace_bytes(small, 256, ckv.ENTRY_SELECT_TOPK)
+
+
+def test_pipeline_argument_checks():
+    lib = ckv._lib
+    s = good_shape()
+    bufs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    assert lib.ckv_pipeline_create(None) == STATUS["EINVAL"]
+    assert lib.ckv_pipeline_destroy(None) == STATUS["OK"]
+    layers = (ckv.Layer * 2)()
+    assert lib.ckv_pipeline_prime(None, ctypes.byref(s), 16, layers, 2, 0, bufs, bufs,
+                                  None) == STATUS["EINVAL"]
+    assert lib.ckv_decode_step(None, ctypes.byref(s), 2, layers, FAKE, 16, 0.1, 0, bufs,
+                               bufs, FAKE, 1 << 20, None, None) == STATUS["EINVAL"]

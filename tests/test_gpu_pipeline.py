@@ -1,0 +1,176 @@
+"""The two-buffer decode loop (ckv_decode_step) against the oracle, and its
+stream ordering under injected delays (MI355X only).
+
+Semantics checked, per layer l and step t (Sec. 4.1, Sec. 5.3, Sec. 5.4):
+  out_t[l]  = attention of q_att_t[l] over the rows selected at step t-1
+  idx_t[l]  = top-k of the scores of q_sel_t[l]
+with the selection before the first step made from a bootstrap query (the
+pre-decoding step).  Queries change from step to step, so a buffer holding
+the wrong layer's or the wrong step's rows shows up in the outputs.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_26475_amd as ckv
+import synth
+from helpers import (ATOL_OUT, SCALE, check_index_sets, device, oracle_attn_over, orc, u16)
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(*a):
+    print(*a, flush=True)
+
+
+class Loop:
+    """Inputs and state of a pipelined decode over L layers of one workload."""
+
+    def __init__(self, w, layers, steps, seed, dev):
+        self.w, self.L, self.dev = w, layers, dev
+        d = w.head_dim
+        B, Hq, Hkv, k = w.batch, w.q_heads, w.kv_heads, w.k
+        self.t = [synth.make_layer(w, seed=seed, layer=l, device=dev) for l in range(layers)]
+        self.lens = self.t[0]["ctx_lens"]
+        for t in self.t:
+            assert torch.equal(t["ctx_lens"], self.lens)
+        self.kv_host = [synth.host_kv(t["k"], t["v"]) for t in self.t]
+        # per step (0 = bootstrap selection) the attending and selecting queries
+        self.q_att, self.q_sel = [], []
+        for s in range(steps + 1):
+            qa, qs = [], []
+            for l in range(layers):
+                g = synth.generator(w.name, seed, l, f"step{s}", dev)
+                a = torch.randn((B, Hq, d), generator=g, device=dev).to(torch.bfloat16)
+                b = (0.8 * a.float() + 0.6 * torch.randn((B, Hq, d), generator=g, device=dev)
+                     ).to(torch.bfloat16)
+                qa.append(a)
+                qs.append(b)
+            self.q_att.append(qa)
+            self.q_sel.append(qs)
+        mk = lambda: [torch.full((B, Hkv, k), -9, dtype=torch.int32, device=dev)
+                      for _ in range(layers)]
+        mn = lambda: [torch.full((B, Hkv), -9, dtype=torch.int32, device=dev)
+                      for _ in range(layers)]
+        self.idx = [mk(), mk()]
+        self.nsel = [mn(), mn()]
+        self.out = [torch.full((B, Hq, d), float("nan"), device=dev) for _ in range(layers)]
+        self.k_buf = [torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev)
+                      for _ in range(2)]
+        self.v_buf = [torch.empty_like(self.k_buf[0]) for _ in range(2)]
+        self.shape = ckv.shape_for(B, Hq, Hkv, w.max_ctx, kv_row_stride=2 * d)
+        self.ws = ckv.workspace(self.shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        self.copy = torch.cuda.Stream(device=dev)
+        self.compute = torch.cuda.current_stream(dev)
+
+    def layer_io(self, step, cur):
+        d = self.w.head_dim
+        nxt = 1 - cur
+        return [{"q_att": self.q_att[step][l], "q_sel": self.q_sel[step][l],
+                 "k_score": self.t[l]["k"], "k_src": self.kv_host[l].data_ptr(),
+                 "v_src": self.kv_host[l].data_ptr() + 2 * d,
+                 "idx_prev": self.idx[cur][l], "n_sel_prev": self.nsel[cur][l],
+                 "idx_next": self.idx[nxt][l], "n_sel_next": self.nsel[nxt][l],
+                 "out": self.out[l]} for l in range(self.L)]
+
+    def bootstrap(self):
+        """Selection before the first step (the pre-decoding step), into set 0."""
+        w = self.w
+        s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
+        scores = torch.empty((w.batch, w.kv_heads, w.max_ctx), device=self.dev)
+        ws = ckv.workspace(s, w.k, ckv.ENTRY_SELECT_TOPK)
+        for l in range(self.L):
+            ckv.score_keys(s, self.q_sel[0][l], self.t[l]["k"], self.lens, SCALE, scores)
+            ckv.select_topk(s, scores, self.lens, w.k, self.idx[0][l], self.nsel[0][l], ws)
+        torch.cuda.synchronize()
+
+    def run(self, steps, pipe, delay=None):
+        """steps decode steps; returns host copies of (idx, nsel, out) per step."""
+        self.copy.wait_stream(self.compute)
+        pipe.prime(self.shape, self.w.k, self.layer_io(1, 0), ckv.SRC_HOST_PINNED,
+                   self.k_buf, self.v_buf, self.copy)
+        cur, hist = 0, []
+        for st in range(1, steps + 1):
+            if delay is not None:
+                delay(self.copy if delay.stream == "copy" else self.compute)
+            pipe.step(self.shape, self.layer_io(st, cur), self.lens, self.w.k, SCALE,
+                      ckv.SRC_HOST_PINNED, self.k_buf, self.v_buf, self.ws, self.compute,
+                      self.copy)
+            self.compute.wait_stream(self.copy)
+            torch.cuda.synchronize()
+            nxt = 1 - cur
+            hist.append(([i.cpu().numpy() for i in self.idx[nxt]],
+                         [n.cpu().numpy() for n in self.nsel[nxt]],
+                         [o.cpu().numpy() for o in self.out]))
+            cur = nxt
+        return hist
+
+
+@pytest.mark.parametrize("wl,layers", [("long128k_s", 3), ("dual64_s", 2)])
+def test_pipeline_matches_oracle(wl, layers):
+    _log("pipeline", wl, layers)
+    dev = device()
+    w = synth.WORKLOADS[wl]
+    lp = Loop(w, layers, steps=2, seed=5, dev=dev)
+    lp.bootstrap()
+    boot = ([i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]])
+    pipe = ckv.Pipeline()
+    hist = lp.run(2, pipe)
+    pipe.close()
+    o = orc()
+    lens = lp.lens.cpu().numpy()
+    so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
+    prev_sets = boot
+    for st in range(1, 3):
+        g_idx, g_nsel, g_out = hist[st - 1]
+        for l in range(layers):
+            K, V = u16(lp.t[l]["k"]), u16(lp.t[l]["v"])
+            # selection at this step from this step's speculative query
+            S = o.score_keys(so, u16(lp.q_sel[st][l]), K, lens, SCALE, nthreads=8)
+            r_idx, r_nsel = o.select_topk(so, S, lens, w.k, nthreads=8)
+            swaps = check_index_sets(g_idx[l], g_nsel[l], r_idx, r_nsel, S, lens)
+            # attention of this step's query over the set selected one step earlier
+            ref = oracle_attn_over(so, u16(lp.q_att[st][l]), K, V, prev_sets[0][l],
+                                   prev_sets[1][l], w.k)
+            err = np.abs(g_out[l] - ref).max()
+            _log(f"  step {st} layer {l}: swaps {swaps}, max abs err {err:.2e}")
+            assert err <= ATOL_OUT
+        prev_sets = (g_idx, g_nsel)
+
+
+class _Delay:
+    """Keeps one stream busy (device copies) before each step."""
+
+    def __init__(self, stream_name, dev):
+        self.stream = stream_name
+        self.a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        self.b = torch.empty_like(self.a)
+
+    def __call__(self, stream):
+        with torch.cuda.stream(stream):
+            for _ in range(40):
+                self.b.copy_(self.a)
+
+
+@pytest.mark.parametrize("stream_name", ["copy", "compute"])
+def test_pipeline_ordering_under_delay(stream_name):
+    """A busy copy stream (gathers land late: read-after-write) or a busy
+    compute stream (buffers released late: write-after-read) must not change
+    a single output bit."""
+    _log("pipeline delay", stream_name)
+    dev = device()
+    w = synth.WORKLOADS["long128k_s"]
+    lp = Loop(w, 3, steps=2, seed=7, dev=dev)
+    lp.bootstrap()
+    pipe = ckv.Pipeline()
+    ref = lp.run(2, pipe)
+    lp.bootstrap()
+    got = lp.run(2, pipe, delay=_Delay(stream_name, dev))
+    pipe.close()
+    for (ri, rn, ro), (gi, gn, go) in zip(ref, got):
+        for l in range(3):
+            np.testing.assert_array_equal(ri[l], gi[l])
+            np.testing.assert_array_equal(rn[l], gn[l])
+            np.testing.assert_array_equal(ro[l], go[l])
