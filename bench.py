@@ -14,7 +14,6 @@ Prints ONE JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
-import glob
 import hashlib
 import json
 import math
@@ -37,13 +36,16 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+SCORE_SOURCES = ("ckv_score.hpp", "ckv_device.hpp")
+
+
 def source_digest() -> str:
-    """sha256 over the library's kernel and host sources (counters taken on
-    other sources are stale)."""
+    """sha256 over the sources of the scoring kernel (counters taken on other
+    sources are stale)."""
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2607_26475_amd", "csrc", "*"))):
-        with open(p, "rb") as f:
-            h.update(os.path.basename(p).encode())
+    for name in SCORE_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_26475_amd", "csrc", name), "rb") as f:
+            h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()
 
@@ -83,6 +85,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-host-link", action="store_true")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the pipelined long-context measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (known bytes) before timing, so "
                          "that counter runs can scale FETCH_SIZE/WRITE_SIZE")
@@ -204,6 +208,12 @@ def main() -> int:
     if not args.no_host_link:
         host_link = measure_host_link(torch, ckv, dev)
         log(f"host link: {host_link}")
+    pipeline = None
+    if not args.no_pipeline:
+        del layers[1:]  # keep layer 0 for the CPU baseline, free 62 GiB
+        torch.cuda.empty_cache()
+        pipeline = measure_pipeline(torch, ckv, synth, dev, np, host_link)
+        log(f"pipeline: {pipeline}")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(layers, w, scale, np)
@@ -235,6 +245,7 @@ def main() -> int:
         "kernels": per_kernel,
         "roofline": roofline,
         "host_link": host_link,
+        "pipeline": pipeline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
@@ -290,6 +301,98 @@ def measure_host_link(torch, ckv, dev):
     return {"gather_GBps": gather_gbps, "h2d_copy_GBps": copy_gbps,
             "frac_of_copy": gather_gbps / copy_gbps, "bytes_per_gather": gbytes,
             "workload": "B8, 8 KV heads, n 131072, k 4096, 512-byte K|V rows, pinned host"}
+
+
+def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
+    """The two-buffer decode loop on the long-context workload: B8, 32 q / 8 KV
+    heads, n 131072, k 4096, 32 layers; K|V rows in pinned host memory,
+    scoring keys in HBM.  Layer inputs cycle over 4 distinct HBM and 2 distinct
+    host layers (each far larger than any cache); queries are distinct per
+    layer and step.  Step time from events on the compute stream after it has
+    joined the copy stream."""
+    w = synth.WORKLOADS["long128k"]
+    B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
+                              w.layers)
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    n_hbm, n_host = 4, 2
+    kscore, hosts = [], []
+    for i in range(n_hbm):
+        t = synth.make_layer(w, seed=0, layer=i, device=dev)
+        if i < n_host:
+            hosts.append(synth.host_kv(t["k"], t["v"]))
+        kscore.append(t["k"])
+        lens = t["ctx_lens"]
+        del t
+    torch.cuda.empty_cache()
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    q = [[torch.randn((B, Hq, d), generator=g, device=dev).to(torch.bfloat16)
+          for _ in range(L)] for _ in range(steps + 2)]
+    idx = [[torch.empty((B, Hkv, k), dtype=torch.int32, device=dev) for _ in range(L)]
+           for _ in range(2)]
+    nsel = [[torch.empty((B, Hkv), dtype=torch.int32, device=dev) for _ in range(L)]
+            for _ in range(2)]
+    out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
+    k_buf = [torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    v_buf = [torch.empty_like(k_buf[0]) for _ in range(2)]
+    shape = ckv.shape_for(B, Hq, Hkv, n, kv_row_stride=2 * d)
+    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+
+    def io(step, cur):
+        return [{"q_att": q[step][l], "q_sel": q[step + 1][l], "k_score": kscore[l % n_hbm],
+                 "k_src": hosts[l % n_host].data_ptr(),
+                 "v_src": hosts[l % n_host].data_ptr() + 2 * d,
+                 "idx_prev": idx[cur][l], "n_sel_prev": nsel[cur][l],
+                 "idx_next": idx[1 - cur][l], "n_sel_next": nsel[1 - cur][l],
+                 "out": out[l]} for l in range(L)]
+
+    # bootstrap selection (the pre-decoding step) into set 0
+    s1 = ckv.shape_for(B, Hq, Hkv, n)
+    sc = torch.empty((B, Hkv, n), device=dev)
+    wsel = ckv.workspace(s1, k, ckv.ENTRY_SELECT_TOPK)
+    for l in range(L):
+        ckv.score_keys(s1, q[0][l], kscore[l % n_hbm], lens, scale, sc)
+        ckv.select_topk(s1, sc, lens, k, idx[0][l], nsel[0][l], wsel)
+    torch.cuda.synchronize()
+    pipe = ckv.Pipeline()
+    copy.wait_stream(compute)
+    pipe.prime(shape, k, io(0, 0), ckv.SRC_HOST_PINNED, k_buf, v_buf, copy)
+    cur = 0
+    pipe.step(shape, io(0, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf, ws,
+              compute, copy)  # warm-up step
+    cur = 1 - cur
+    compute.wait_stream(copy)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ckv.profile_begin()
+    e0.record(compute)
+    for st in range(1, steps + 1):
+        pipe.step(shape, io(st, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf, ws,
+                  compute, copy)
+        cur = 1 - cur
+    compute.wait_stream(copy)
+    e1.record(compute)
+    torch.cuda.synchronize()
+    stats = ckv.profile_end()
+    pipe.close()
+    ms = e0.elapsed_time(e1) / steps
+    host_bytes = L * B * Hkv * k * 2 * d * 2
+    gather_ms = stats.get("gather", (0, 0.0, 0.0))[1] / steps
+    compute_ms = sum(v[1] for kname, v in stats.items() if kname != "gather") / steps
+    res = {"workload": "long-context decode, 32 layers: B8, 32 q / 8 KV heads, head_dim 128, "
+                       "context 131072, k 4096; K|V rows host-pinned, scoring keys in HBM; "
+                       "4 HBM and 2 host layers cycled",
+           "ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3),
+           "host_bytes_per_step": host_bytes,
+           "host_GBps_step": host_bytes / (ms * 1e-3) / 1e9,
+           "gather_ms_per_step": gather_ms, "compute_kernels_ms_per_step": compute_ms,
+           "overlap": (gather_ms + compute_ms) / ms}
+    if host_link:
+        res["frac_of_h2d_copy"] = res["host_GBps_step"] / host_link["h2d_copy_GBps"]
+    del hosts
+    return res
 
 
 def cpu_baseline(layers, w, scale, np):
