@@ -9,7 +9,8 @@
 // Logits: Q[G x d] . K_chunk^T on MFMA (bf16 products are exact, fp32
 // accumulation), same operand placement as the scoring pass.  Weights and the
 // weighted V sum stay in fp32 on the VALU: rounding the weights to bf16 for an
-// MFMA would cost up to 2^-9 relative per weight.
+// MFMA would cost up to 2^-9 relative per weight.  An empty chunk (all rows
+// past n_sel) yields m = -inf and zero sums, which the combine ignores.
 #pragma once
 
 #include "ckv_device.hpp"
@@ -18,65 +19,85 @@ namespace ckv {
 
 template <int G>
 struct AttnLds {
-  // K stage (4 waves x 32 rows, padded) | logits [G][rows] | partial sums
-  // [4 waves][G][kD] | per-head max and weight sum
-  static constexpr int kStage = 4 * kStageDwords;
-  static constexpr int kFloats = kStage + G * kAttnRows + 4 * G * kD + 2 * G;
+  // K stage (4 waves x 16 rows, padded) | per-wave weight table
+  // [4][16 rows x G + G rescale] | per-wave partials [4][G][kD + 2]
+  static constexpr int kStage = 4 * 16 * kStageRowDwords;
+  static constexpr int kPTab = 16 * G + G + (G < 4 ? 4 - G : 0);
+  static constexpr int kP = 4 * kPTab;
+  static constexpr int kMerge = 4 * G * (kD + 2);
+  static constexpr int kFloats = kStage + kP + kMerge;
 };
 
-// All kAttnThreads threads of the workgroup must call this.  INDEXED: rows are
-// source rows idx[unit][r] read in place; otherwise slot rows of a dense
-// [U][k][d] buffer.
+// All kAttnThreads threads of the workgroup must call this.  The workgroup
+// covers selected rows [chunk*kAttnRows, +kAttnRows) of `unit`; wave w owns
+// the kWaveRows rows starting at w*kWaveRows and streams them in blocks of 16
+// with an online softmax (running max m, weight sum l and weighted V sum o
+// per query head), keeping the next block's loads in flight.  The four
+// waves' states are merged through LDS into the chunk's partial.  INDEXED:
+// rows are source rows idx[unit][r] read in place; otherwise slot rows of a
+// dense [U][k][d] buffer.
 //
-// Loads: wave w owns rows [32w, 32w+32); every load instruction reads four
-// whole 256-byte rows (16 lanes x 16 bytes per row), K and V alike.  K goes
-// through a padded LDS stage into the MFMA operand placement; V stays in
+// Loads: every instruction reads four whole 256-byte rows (16 lanes x 16
+// bytes per row), K and V alike.  K goes through a padded per-wave LDS stage
+// into the MFMA operand placement (logits Q[G x d] . K^T on MFMA); V stays in
 // registers in exactly the placement the weighted sum needs.
 template <int G, bool INDEXED>
 __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
                                            int chunk, float* lds) {
-  uint32_t* stage_all = reinterpret_cast<uint32_t*>(lds);
-  float* lg = lds + AttnLds<G>::kStage;   // [G][kAttnRows] logits, then weights
-  float* red = lg + G * kAttnRows;        // [4 waves][G][kD] partial sums
-  float* stat = red + 4 * G * kD;         // [2][G] chunk max, weight sum
-  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
-  const int nsel = clamp_len(a.n_sel[unit], a.k);
-  const int r0 = chunk * kAttnRows;
-  const int rows = min(kAttnRows, nsel - r0);
-  float* part = a.part + ((int64_t)unit * a.chunks + chunk) * G * kPartStride;
+  static_assert(kWaveRows % 16 == 0 && 4 * kWaveRows == kAttnRows, "4 waves per chunk");
+  constexpr int kBlocks = kWaveRows / 16;
   const int tid = threadIdx.x;
-  if (rows <= 0) {  // uniform: empty chunk (zero weight, zero sums)
-    for (int o = tid; o < G * kPartStride; o += kAttnThreads)
-      part[o] = (o % kPartStride) == 0 ? -INFINITY : 0.f;
-    return;
-  }
   const int lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
   const int lrow = lane >> 4, lchunk = lane & 15;
-  uint32_t* stage = stage_all + wave * kStageDwords;
+  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+  const int nsel = clamp_len(a.n_sel[unit], a.k);
+  const int w0 = chunk * kAttnRows + wave * kWaveRows;  // first row of this wave
+  const int wrows = max(0, min(kWaveRows, nsel - w0));
+  uint32_t* stage = reinterpret_cast<uint32_t*>(lds) + wave * 16 * kStageRowDwords;
+  float* ptab = lds + AttnLds<G>::kStage + wave * AttnLds<G>::kPTab;  // [16][G], [G]
+  float* merge = lds + AttnLds<G>::kStage + AttnLds<G>::kP;
+  float* part = a.part + ((int64_t)unit * a.chunks + chunk) * G * kPartStride;
 
-  auto row_off = [&](int i) -> int64_t {
-    if (INDEXED) {
-      int pos = a.idx[(int64_t)unit * a.k + r0 + i];
-      pos = pos < 0 ? 0 : (pos >= a.max_ctx ? a.max_ctx - 1 : pos);
-      return ((int64_t)unit * a.max_ctx + pos) * a.row_stride;
-    }
-    return ((int64_t)unit * a.k + r0 + i) * kD;
-  };
-
-  // K and V of rows 32w + 4it + lrow, 16-byte chunk lchunk of each.
-  uint4 kr[8], vr[8];
+  // Source offsets of the rows this lane loads (block blk, load it -> row
+  // 16*blk + 4*it + lrow of the wave).  Rows past wrows load the wave's last
+  // row instead: every load is unconditional (lane-conditional loads make the
+  // compiler wait for all outstanding loads at each use), and those rows are
+  // masked out of the softmax.
+  const int nblk = (wrows + 15) / 16;
+  int64_t off[kBlocks][4];
+  if (wrows > 0) {
+    int pos[kBlocks][4];
 #pragma unroll
-  for (int it = 0; it < 8; ++it) {
-    const int i = wave * 32 + it * 4 + lrow;
-    kr[it] = make_uint4(0u, 0u, 0u, 0u);
-    vr[it] = make_uint4(0u, 0u, 0u, 0u);
-    if (i < rows) {
-      const int64_t off = row_off(i) + 8 * lchunk;
-      kr[it] = ld16(a.k_rows + off);
-      vr[it] = ld16(a.v_rows + off);
-    }
+    for (int blk = 0; blk < kBlocks; ++blk)
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        const int i = min(16 * blk + 4 * it + lrow, wrows - 1);
+        pos[blk][it] = INDEXED ? a.idx[(int64_t)unit * a.k + w0 + i] : w0 + i;
+      }
+#pragma unroll
+    for (int blk = 0; blk < kBlocks; ++blk)
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        int ps = pos[blk][it];
+        if (INDEXED) {
+          ps = ps < 0 ? 0 : (ps >= a.max_ctx ? a.max_ctx - 1 : ps);
+          off[blk][it] = ((int64_t)unit * a.max_ctx + ps) * a.row_stride + 8 * lchunk;
+        } else {
+          off[blk][it] = ((int64_t)unit * a.k + ps) * kD + 8 * lchunk;
+        }
+      }
   }
+  auto load_blk = [&](int blk, uint4* kv) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      kv[it] = ld16(a.k_rows + off[blk][it]);
+      kv[4 + it] = ld16(a.v_rows + off[blk][it]);
+    }
+  };
+  uint4 cur[8], nxt[8];
+  if (nblk > 0) load_blk(0, cur);
+
   bf16x8 qa[4];
   {
     const uint16_t* qrow =
@@ -88,87 +109,140 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
       qa[t] = as_bf16x8(v);
     }
   }
+  // online state: register i of lane group kg is head 4*kg + i
+  float m_i[4], l_i[4];
 #pragma unroll
-  for (int it = 0; it < 8; ++it)
-    *reinterpret_cast<uint4*>(stage + (4 * it + lrow) * kStageRowDwords + 4 * lchunk) = kr[it];
-  __builtin_amdgcn_wave_barrier();
+  for (int i = 0; i < 4; ++i) {
+    m_i[i] = -INFINITY;
+    l_i[i] = 0.f;
+  }
+  float o[G][8];
 #pragma unroll
-  for (int bk = 0; bk < 2; ++bk) {
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+
+#pragma unroll
+  for (int blk = 0; blk < kBlocks; ++blk) {
+    if (blk >= nblk) break;  // uniform over the wave
+    if (blk + 1 < nblk) load_blk(blk + 1, nxt);
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+      *reinterpret_cast<uint4*>(stage + (4 * it + lrow) * kStageRowDwords + 4 * lchunk) =
+          cur[it];
+    __builtin_amdgcn_wave_barrier();
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const uint4 kv = *reinterpret_cast<const uint4*>(
-          stage + (16 * bk + r16) * kStageRowDwords + 4 * (4 * t + kg));
+          stage + r16 * kStageRowDwords + 4 * (4 * t + kg));
       acc = mfma_16x16x32(qa[t], as_bf16x8(kv), acc);
     }
-    const int r = wave * 32 + bk * 16 + r16;
+    __builtin_amdgcn_wave_barrier();
+    // logits of key r16 of the block for heads 4kg..4kg+3, block max and sum
+    // (reductions over the 16 keys of a lane row stay in the row: DPP)
+    const bool valid = 16 * blk + r16 < wrows;
+    float p[4], al[4];
+    bool moved = false;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int g = 4 * kg + i;
-      if (g < G) lg[g * kAttnRows + r] = r < rows ? acc[i] * a.scale : -INFINITY;
+      const float lg = (4 * kg + i < G && valid) ? acc[i] * a.scale : -INFINITY;
+      const float mn = fmaxf(m_i[i], row16_max(lg));
+      moved |= mn != m_i[i];
+      al[i] = m_i[i] == -INFINITY ? 0.f : __expf(m_i[i] - mn);
+      p[i] = lg == -INFINITY ? 0.f : __expf(lg - mn);
+      l_i[i] = l_i[i] * al[i] + row16_sum(p[i]);
+      m_i[i] = mn;
     }
-  }
-  __syncthreads();
-
-  // Per-head softmax over the chunk (one wave per head, two rows per lane).
-  for (int g = wave; g < G; g += 4) {
-    const float x0 = lg[g * kAttnRows + lane];
-    const float x1 = lg[g * kAttnRows + 64 + lane];
-    const float mx = wave_max(fmaxf(x0, x1));  // finite: rows >= 1
-    const float p0 = __expf(x0 - mx), p1 = __expf(x1 - mx);
-    const float l = wave_sum(p0 + p1);
-    lg[g * kAttnRows + lane] = p0;
-    lg[g * kAttnRows + 64 + lane] = p1;
-    if (lane == 0) {
-      stat[g] = mx;
-      stat[G + g] = l;
+    // weights of the block's rows and the rescale factors -> per-wave table
+    if (4 * kg < G) {
+      if (G >= 4) {
+        *reinterpret_cast<float4*>(ptab + r16 * G + 4 * kg) = make_float4(p[0], p[1], p[2], p[3]);
+        if (r16 == 0)
+          *reinterpret_cast<float4*>(ptab + 16 * G + 4 * kg) =
+              make_float4(al[0], al[1], al[2], al[3]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+          ptab[r16 * G + i] = p[i];
+          if (r16 == 0) ptab[16 * G + i] = al[i];
+        }
+      }
     }
-  }
-  __syncthreads();
-
-  // Weighted V sum: lane holds channels [8*lchunk, +8) of 8 rows.
-  float acc[G][8];
+    const bool rescale = __any(moved);  // running max moved for some head
+    __builtin_amdgcn_wave_barrier();
+    // weighted V sum: lane holds channels [8*lchunk, +8) of rows 4*it + lrow
+    if (rescale) {
 #pragma unroll
-  for (int g = 0; g < G; ++g)
+      for (int g = 0; g < G; ++g) {
+        const float alpha = ptab[16 * G + g];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
-#pragma unroll
-  for (int it = 0; it < 8; ++it) {
-    const int i = wave * 32 + it * 4 + lrow;
-    float vf[8];
-    unpack8(vr[it], vf);
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float p = lg[g * kAttnRows + i];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+        for (int e = 0; e < 8; ++e) o[g][e] *= alpha;
+      }
     }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      float vf[8];
+      unpack8(cur[4 + it], vf);
+      const float* pr = ptab + (4 * it + lrow) * G;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float pg = pr[g];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pg, vf[e], o[g][e]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
   }
+  // sum the four row phases (lrow) of each channel chunk
 #pragma unroll
   for (int g = 0; g < G; ++g)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float x = acc[g][e];
+      float x = o[g][e];
       x += __shfl_xor(x, 16);
       x += __shfl_xor(x, 32);
-      acc[g][e] = x;
+      o[g][e] = x;
     }
+  float* mw = merge + wave * G * (kD + 2);
   if (lrow == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) red[(wave * G + g) * kD + 8 * lchunk + e] = acc[g][e];
+      for (int e = 0; e < 8; ++e) mw[g * (kD + 2) + 8 * lchunk + e] = o[g][e];
+  }
+  if (lchunk == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = 4 * lrow + i;
+      if (g < G) {
+        mw[g * (kD + 2) + kD] = m_i[i];
+        mw[g * (kD + 2) + kD + 1] = l_i[i];
+      }
+    }
   }
   __syncthreads();
-  for (int o = tid; o < G * kD; o += kAttnThreads) {
-    const int g = o / kD, c = o - g * kD;
-    const float sum = red[(0 * G + g) * kD + c] + red[(1 * G + g) * kD + c] +
-                      red[(2 * G + g) * kD + c] + red[(3 * G + g) * kD + c];
-    part[g * kPartStride + 4 + c] = sum;
-  }
-  if (tid < G) {
-    part[tid * kPartStride] = stat[tid];
-    part[tid * kPartStride + 1] = stat[G + tid];
+  // merge the four waves into the chunk's partial
+  for (int oi = tid; oi < G * kD; oi += kAttnThreads) {
+    const int g = oi / kD, c = oi - g * kD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, merge[(w * G + g) * (kD + 2) + kD]);
+    float O = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float* mg = merge + (w * G + g) * (kD + 2);
+      const float wt = mg[kD] == -INFINITY ? 0.f : __expf(mg[kD] - M);
+      O = fmaf(wt, mg[c], O);
+      L = fmaf(wt, mg[kD + 1], L);
+    }
+    part[g * kPartStride + 4 + c] = O;
+    if (c == 0) {
+      part[g * kPartStride] = M;
+      part[g * kPartStride + 1] = L;
+    }
   }
 }
 

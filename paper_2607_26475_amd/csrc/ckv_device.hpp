@@ -37,9 +37,11 @@ constexpr int kBitmapLdsBits = kFinishLdsBytes * 8;
 constexpr int kFusedSelectMaxCtx = 65536;
 
 // Attention: one workgroup reduces kAttnRows gathered rows of one unit into a
-// partial (running max, sum of weights, weighted V) per query head.
+// partial (running max, sum of weights, weighted V) per query head; each of
+// its 4 waves streams kWaveRows of them.
 constexpr int kAttnThreads = 256;
-constexpr int kAttnRows = 128;
+constexpr int kWaveRows = 64;
+constexpr int kAttnRows = 4 * kWaveRows;
 constexpr int kPartStride = 132;   // floats per (chunk, head): m, l, pad, pad, o[128]
 
 // Gather: one thread moves 16 bytes per item; items are (unit, slot, K|V, part).
@@ -144,6 +146,30 @@ __device__ __forceinline__ void unpack8(uint4 v, float* f) {
     f[2 * i] = __uint_as_float(w[i] << 16);
     f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
+}
+
+// DPP lane exchange within rows of 16 lanes (no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// Max / sum over the 16 lanes of each row; every lane of the row gets it.
+// quad_perm [1,0,3,2] and [2,3,0,1] reduce a quad, row_half_mirror pairs the
+// two quads of each half row, row_mirror the two half rows.
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_f32<0xB1>(x));
+  x = fmaxf(x, dpp_f32<0x4E>(x));
+  x = fmaxf(x, dpp_f32<0x141>(x));
+  return fmaxf(x, dpp_f32<0x140>(x));
+}
+
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_f32<0xB1>(x);
+  x += dpp_f32<0x4E>(x);
+  x += dpp_f32<0x141>(x);
+  return x + dpp_f32<0x140>(x);
 }
 
 __device__ __forceinline__ float wave_max(float x) {

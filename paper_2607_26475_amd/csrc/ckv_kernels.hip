@@ -60,10 +60,8 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
   const float* srow = a.scores + (int64_t)unit * a.max_ctx;
   float sv[kPer];
 #pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    const int j = j0 + r * kFilterThreads + threadIdx.x;
-    sv[r] = j < n ? srow[j] : 0.f;
-  }
+  for (int r = 0; r < kPer; ++r)  // unconditional loads (clamped position)
+    sv[r] = srow[min(j0 + r * kFilterThreads + (int)threadIdx.x, n - 1)];
   if (threadIdx.x < 64)
     find_first_bin(a.coarse + (int64_t)unit * kCoarseBins,
                    a.hist + (int64_t)unit * kHistBins, (uint32_t)m, sh);
@@ -290,10 +288,8 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   for (int j0 = 0; j0 < n; j0 += kFinishThreads * kUnroll) {
     float sv[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int j = j0 + u * kFinishThreads + tid;
-      sv[u] = j < n ? srow[j] : 0.f;
-    }
+    for (int u = 0; u < kUnroll; ++u)  // unconditional loads (clamped position)
+      sv[u] = srow[min(j0 + u * kFinishThreads + tid, n - 1)];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int j = j0 + u * kFinishThreads + tid;

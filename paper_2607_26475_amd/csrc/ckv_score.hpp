@@ -109,13 +109,15 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
         }
       }
       const uint16_t* kunit = a.keys + (int64_t)unit * a.max_ctx * a.key_stride;
+      // Rows at or past n_b load row n_b - 1 instead (their scores are
+      // replaced by -inf): lane-conditional loads would make the compiler
+      // wait for every outstanding load at each use.
       auto load_group = [&](int64_t gg, uint4* v) {
         const int jb = (int)(gg - ubase) * kStageRows;
 #pragma unroll
         for (int i = 0; i < kLoads; ++i) {
-          const int j = jb + 4 * i + lrow;
-          v[i] = j < n ? ld16_nt(kunit + (int64_t)j * a.key_stride + 8 * lchunk)
-                       : make_uint4(0u, 0u, 0u, 0u);
+          const int j = min(jb + 4 * i + lrow, n - 1);
+          v[i] = ld16_nt(kunit + (int64_t)j * a.key_stride + 8 * lchunk);
         }
       };
       // writes the scores of the nb buffered groups [first, first + nb): one
