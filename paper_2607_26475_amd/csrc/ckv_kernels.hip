@@ -138,7 +138,8 @@ __device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
 // Returns the threshold key T; candidates with key > T are all chosen, and of
 // those equal to T the ones with position <= *pmax.  All kFinishThreads
 // threads call this; hist needs 2048 words.
-__device__ __forceinline__ uint32_t refine_threshold(const uint2* cs, uint32_t nc,
+template <class Cands>
+__device__ __forceinline__ uint32_t refine_threshold(const Cands& cs, uint32_t nc,
                                                      uint32_t need, uint32_t b1,
                                                      uint32_t* hist, uint32_t* tmp,
                                                      uint32_t* misc, uint32_t* pmax) {
@@ -251,14 +252,90 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
   if (tid == 0) a.n_sel[unit] = m;
 }
 
-// Whole selection of one unit in one workgroup, for n_b <= kFusedSelectMaxCtx:
-// reads the unit's scores once, marks positions above the first-digit bin in
-// an LDS bitmap, collects the bin's candidates, resolves the threshold and
-// emits the chosen positions in ascending order.
+// Whole selection of one unit in one workgroup, for n_b <= kFusedSelectMaxCtx.
+// The unit's scores are read once, kSelPer per thread per batch of
+// kSelBatch positions, all loads of a batch in flight together.  Positions
+// above the first-digit bin go straight into an LDS bitmap (one ballot per
+// 64 positions, no atomics); positions inside the bin become candidates
+// (order key, position), whose slots are reserved with one atomic per wave.
+// The threshold inside the bin is then resolved exactly, the chosen
+// candidates marked, and the bitmap written out in ascending order.
+constexpr int kSelPer = 32;
+constexpr int kSelBatch = kSelPer * kFinishThreads;
+static_assert(kFusedSelectMaxCtx % kSelBatch == 0, "whole batches");
+
+__device__ __forceinline__ void load_score_batch(const float* srow, int j0, int n,
+                                                 float (&sv)[kSelPer]) {
+  // unconditional loads (clamped position); 32-bit byte offsets from the
+  // row base let every load share one scalar base address
+  const char* base = reinterpret_cast<const char*>(srow);
+#pragma unroll
+  for (int u = 0; u < kSelPer; ++u) {
+    const uint32_t off = 4u * (uint32_t)min(j0 + u * kFinishThreads + (int)threadIdx.x, n - 1);
+    sv[u] = *reinterpret_cast<const float*>(base + off);
+  }
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// One batch of kSelBatch positions starting at j0: bitmap words of the
+// positions above the bin b1, candidates inside it appended at *ctr.
+template <class Cands>
+__device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j0, int n,
+                                               uint32_t b1, uint32_t* bm, const Cands& cs,
+                                               uint32_t* ctr) {
+  static_assert(2 * kSelPer == 64, "one bitmap word per lane and batch");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The wave's positions j0 + u * kFinishThreads + wave * 64 + [0, 64) form
+  // bitmap words 2u and 2u + 1 of its share; lane 2u + h keeps word h of u.
+  uint32_t word = 0u, wc = 0u;
+#pragma unroll
+  for (int u = 0; u < kSelPer; ++u) {
+    const int jw = j0 + u * kFinishThreads + wave * 64;
+    const uint32_t d1 = order_key(sv[u]) >> (32 - kHistBits);
+    const bool valid = jw + lane < n;
+    const uint64_t hi = __ballot(valid && d1 > b1);
+    const uint32_t half = (lane & 1) ? (uint32_t)(hi >> 32) : (uint32_t)hi;
+    word = (lane >> 1) == u ? half : word;
+    wc += (uint32_t)__popcll(__ballot(valid && d1 == b1));
+  }
+  bm[((j0 + (lane >> 1) * kFinishThreads + wave * 64) >> 5) + (lane & 1)] = word;
+  uint32_t base = 0u;
+  if (lane == 0 && wc) base = atomicAdd(ctr, wc);
+  base = __builtin_amdgcn_readfirstlane(base);
+#pragma unroll
+  for (int u = 0; u < kSelPer; ++u) {
+    const int j = j0 + u * kFinishThreads + tid;
+    const uint32_t key = order_key(sv[u]);
+    const bool is_cand = j < n && (key >> (32 - kHistBits)) == b1;
+    const uint64_t cm = __ballot(is_cand);
+    const uint32_t o = base + lanes_below(cm);
+    if (is_cand) cs.put(o, make_uint2(key, (uint32_t)j));
+    base += (uint32_t)__popcll(cm);
+  }
+}
+
+// Candidate slots of the fused selection: the first kCandLds in LDS, any
+// beyond (heavy ties) in the unit's global candidate area.
+struct SplitCands {
+  uint2* lds;
+  uint2* glob;
+  __device__ __forceinline__ uint2 operator[](uint32_t i) const {
+    return i < (uint32_t)kCandLds ? lds[i] : glob[i];
+  }
+  __device__ __forceinline__ void put(uint32_t i, uint2 v) const {
+    if (i < (uint32_t)kCandLds) lds[i] = v;
+    else glob[i] = v;
+  }
+};
+
 __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __shared__ uint2 cand[kCandLds];
   __shared__ uint32_t bm[kFusedSelectMaxCtx / 32];
-  __shared__ uint32_t hist[2048];
+  __shared__ uint32_t lhist[2048];
   __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
   __shared__ uint32_t misc[8];
   const int unit = blockIdx.x;
@@ -272,46 +349,33 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
     if (tid == 0) a.n_sel[unit] = m;
     return;
   }
-  if (tid < 64)
-    find_first_bin(a.coarse + (int64_t)unit * kCoarseBins,
-                   a.hist + (int64_t)unit * kHistBins, (uint32_t)m, misc + 4);
-  const int words = (n + 31) >> 5;
-  for (int w = tid; w < words; w += kFinishThreads) bm[w] = 0u;
-  if (tid == 0) misc[6] = 0u;
-  __syncthreads();
-  const uint32_t b1 = misc[4], above = misc[5];
-  const uint32_t need = (uint32_t)m - above;
-  const uint32_t nc_expect = a.hist[(int64_t)unit * kHistBins + b1];
-  uint2* cs = nc_expect <= (uint32_t)kCandLds ? cand : a.cand + (int64_t)unit * a.max_ctx;
+  // the first batch of scores is in flight while wave 0 finds the bin
   const float* srow = a.scores + (int64_t)unit * a.max_ctx;
-  constexpr int kUnroll = 8;
-  for (int j0 = 0; j0 < n; j0 += kFinishThreads * kUnroll) {
-    float sv[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)  // unconditional loads (clamped position)
-      sv[u] = srow[min(j0 + u * kFinishThreads + tid, n - 1)];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int j = j0 + u * kFinishThreads + tid;
-      const uint32_t key = order_key(sv[u]);
-      const uint32_t d1 = key >> (32 - kHistBits);
-      const bool valid = j < n;
-      if (valid && d1 > b1) atomicOr(&bm[j >> 5], 1u << (j & 31));
-      const bool is_cand = valid && d1 == b1;
-      const uint32_t slot = wave_append(is_cand, &misc[6]);
-      if (is_cand) cs[slot] = make_uint2(key, (uint32_t)j);
-    }
+  float sv0[kSelPer];
+  load_score_batch(srow, 0, n, sv0);
+  if (tid < 64)
+    find_first_bin_fine(a.hist + (int64_t)unit * kHistBins, (uint32_t)m, lhist, misc + 4);
+  if (tid == 64) misc[7] = 0u;
+  __syncthreads();
+  const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
+  const uint32_t b1 = misc[4], above = misc[5];
+  classify_batch(sv0, 0, n, b1, bm, cs, &misc[7]);
+  for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {  // a fresh array per batch
+    float sv[kSelPer];
+    load_score_batch(srow, j0, n, sv);
+    classify_batch(sv, j0, n, b1, bm, cs, &misc[7]);
   }
   __syncthreads();
-  const uint32_t nc = misc[6];
+  const uint32_t nc = misc[7];
+  const uint32_t need = (uint32_t)m - above;
   uint32_t pmax;
-  const uint32_t T = refine_threshold(cs, nc, need, b1, hist, tmp, misc, &pmax);
+  const uint32_t T = refine_threshold(cs, nc, need, b1, lhist, tmp, misc, &pmax);
   for (uint32_t i = tid; i < nc; i += kFinishThreads) {
     const uint2 c = cs[i];
     if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
   }
   __syncthreads();
-  emit_bitmap(bm, words, idx, tmp);
+  emit_bitmap(bm, (n + 31) >> 5, idx, tmp);
   for (int i = m + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
   if (tid == 0) a.n_sel[unit] = m;
 }

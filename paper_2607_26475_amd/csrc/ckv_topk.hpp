@@ -43,6 +43,40 @@ __device__ __forceinline__ void find_first_bin(const uint32_t* coarse,
   }
 }
 
+// Wave 0 only, from the fine histogram alone in one round trip: lane l reads
+// the 32 bins of coarse range 63 - l (ranges in descending order) and copies
+// them to stage[] (2048 words of LDS); the lane whose range holds the m-th
+// largest key then walks its bins downwards from there.
+// out[0] = bin, out[1] = keys in higher bins, out[2] = keys in the bin.
+__device__ __forceinline__ void find_first_bin_fine(const uint32_t* hist, uint32_t m,
+                                                    uint32_t* stage, uint32_t* out) {
+  constexpr int kFine = kHistBins / 64;
+  static_assert(kFine % 4 == 0, "16-byte loads");
+  const int lane = threadIdx.x & 63;
+  const int cb = 63 - lane;
+  const uint4* src = reinterpret_cast<const uint4*>(hist + cb * kFine);
+  uint4* dst = reinterpret_cast<uint4*>(stage + cb * kFine);
+  uint32_t c = 0u;
+#pragma unroll
+  for (int i = 0; i < kFine / 4; ++i) {
+    const uint4 v = src[i];
+    c += v.x + v.y + v.z + v.w;
+    dst[i] = v;
+  }
+  const uint32_t s = wave_incl_scan(c);
+  int L = __ffsll((unsigned long long)__ballot(s >= m)) - 1;
+  if (L < 0) L = 63;  // only if the histogram were inconsistent
+  if (lane == L) {
+    const uint32_t* f = stage + cb * kFine;
+    uint32_t run = s - c;
+    int i = kFine - 1;
+    while (i > 0 && run + f[i] < m) run += f[i--];
+    out[0] = (uint32_t)(cb * kFine + i);
+    out[1] = run;
+    out[2] = f[i];
+  }
+}
+
 // All threads of a kFinishThreads workgroup: given a histogram of nb bins in
 // LDS (nb a multiple of kFinishThreads or at most kFinishThreads), find the
 // bin where the running count (from the top bin down when DESC, else from
