@@ -83,6 +83,8 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--layout", choices=("separate", "interleaved"), default="separate",
+                    help="K and V caches as two arrays, or K|V interleaved per position")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-host-link", action="store_true")
     ap.add_argument("--no-pipeline", action="store_true",
@@ -115,22 +117,27 @@ def main() -> int:
     layers = []
     for l in range(L):
         t = synth.make_layer(w, seed=0, layer=l, device=dev)
-        # K|V interleaved per position: the scoring pass reads the K half of
-        # each 512-byte row, attention reads a selected row in one piece
-        t["kv"] = synth.interleave_kv(t.pop("k"), t.pop("v"))
+        if args.layout == "interleaved":
+            # the scoring pass reads the K half of each 512-byte row,
+            # attention reads a selected row in one piece
+            t["kv"] = synth.interleave_kv(t.pop("k"), t.pop("v"))
         del t["marked"]
         layers.append(t)
     torch.cuda.synchronize()
     log(f"  {time.time() - t0:.1f} s; {torch.cuda.memory_allocated() / 2**30:.1f} GiB resident")
 
-    s = ckv.shape_for(B, Hq, Hkv, n, key_row_stride=2 * d, kv_row_stride=2 * d)
+    row = 2 * d if args.layout == "interleaved" else d
+    s = ckv.shape_for(B, Hq, Hkv, n, key_row_stride=row, kv_row_stride=row)
     ws = ckv.workspace(s, k, ckv.ENTRY_CRITICAL_KV_ATTN)
     idx = [torch.empty((B, Hkv, k), dtype=torch.int32, device=dev) for _ in range(L)]
     nsel = [torch.empty((B, Hkv), dtype=torch.int32, device=dev) for _ in range(L)]
     out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
     stream = torch.cuda.current_stream()
 
-    kv_ptrs = [(t["kv"].data_ptr(), t["kv"].data_ptr() + 2 * d) for t in layers]
+    if args.layout == "interleaved":
+        kv_ptrs = [(t["kv"].data_ptr(), t["kv"].data_ptr() + 2 * d) for t in layers]
+    else:
+        kv_ptrs = [(t["k"].data_ptr(), t["v"].data_ptr()) for t in layers]
 
     def step():
         for l, t in enumerate(layers):
@@ -236,7 +243,9 @@ def main() -> int:
         "config": {
             "workload": "Llama-3-8B-shaped decode, 32 layers: B16, 32 q / 8 KV heads, "
                         "head_dim 128, context 32768, k 2048 per KV head, K/V in HBM "
-                        "(K|V interleaved per position)",
+                        + ("(K|V interleaved per position)" if args.layout == "interleaved"
+                           else "(separate K and V caches)"),
+            "layout": args.layout,
             "batch": B, "context": n, "k": k, "layers": L, "q_heads": Hq,
             "kv_heads": Hkv, "head_dim": d, "placement": "hbm",
         },
@@ -408,18 +417,27 @@ def cpu_baseline(layers, w, scale, np):
     cores = max(1, min(cores, 16))
     t = layers[0]
     q = synth.to_u16(t["q"])
-    K = synth.to_u16(t["kv"][:, :, :, 0].contiguous())
-    V = synth.to_u16(t["kv"][:, :, :, 1].contiguous())
+    if "kv" in t:
+        K = synth.to_u16(t["kv"][:, :, :, 0].contiguous())
+        V = synth.to_u16(t["kv"][:, :, :, 1].contiguous())
+    else:
+        K, V = synth.to_u16(t["k"]), synth.to_u16(t["v"])
     lens = t["ctx_lens"].cpu().numpy()
     so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
-    t0 = time.perf_counter()
-    o.critical_kv_attn(so, q, None, K, K, V, lens, w.k, scale, nthreads=cores)
-    sec_layer = time.perf_counter() - t0
+    # repeated until about 10 s of wall time: a bounded sample of the step
+    runs, elapsed = 0, 0.0
+    while elapsed < 10.0:
+        t0 = time.perf_counter()
+        o.critical_kv_attn(so, q, None, K, K, V, lens, w.k, scale, nthreads=cores)
+        elapsed += time.perf_counter() - t0
+        runs += 1
+    sec_layer = elapsed / runs
     sec_step = sec_layer * w.layers
     return {"value": w.batch / sec_step, "unit": "tokens/s", "cores": cores,
             "kind": "oracle", "cpu": cpu_name(), "seconds_per_step": sec_step,
             "sample": f"layer 0 of {w.layers}, all {w.units} (request, KV head) units, "
-                      f"timed once ({sec_layer:.2f} s) and scaled x{w.layers} layers"}
+                      f"run {runs} times ({elapsed:.1f} s, {sec_layer:.2f} s each) and "
+                      f"scaled x{w.layers} layers"}
 
 
 if __name__ == "__main__":

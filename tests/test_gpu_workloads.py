@@ -143,19 +143,25 @@ def _check_units(w, t, g_idx, g_nsel, g_out, units, k_rows, v_rows):
     _log("  checked units:", units)
 
 
-def test_full_llama8b_layer_sampled():
+@pytest.mark.parametrize("layout", ["separate", "interleaved"])
+def test_full_llama8b_layer_sampled(layout):
     """One full-size Llama-8B-shaped layer (B16, 32/8 heads, n 32768, k 2048)
-    through the fused same-step entry, K|V interleaved in HBM, as the
-    benchmark runs it."""
-    _log("full llama8b layer")
+    through the fused same-step entry with K/V in HBM, in either layout the
+    benchmark runs (separate K and V caches, or K|V interleaved per position)."""
+    _log("full llama8b layer", layout)
     dev = device()
     w = synth.WORKLOADS["llama8b"]
     t = synth.make_layer(w, seed=0, layer=0, device=dev)
-    kv = synth.interleave_kv(t["k"], t["v"])  # the benchmark's HBM layout
     d = w.head_dim
     run = Run(w, t["ctx_lens"], dev)
-    run.same_step(t["q"], t["q_sel"], kv.data_ptr(), kv.data_ptr(), kv.data_ptr() + 2 * d,
-                  ckv.SRC_DEVICE, key_stride=2 * d, kv_stride=2 * d)
+    if layout == "interleaved":
+        kv = synth.interleave_kv(t["k"], t["v"])
+        run.same_step(t["q"], t["q_sel"], kv.data_ptr(), kv.data_ptr(),
+                      kv.data_ptr() + 2 * d, ckv.SRC_DEVICE, key_stride=2 * d,
+                      kv_stride=2 * d)
+        del kv
+    else:
+        run.same_step(t["q"], t["q_sel"], t["k"], t["k"], t["v"], ckv.SRC_DEVICE)
     g_idx, g_nsel, g_out = run.host()
     assert np.all(np.isfinite(g_out))
     units = _sampled_units(w, 8, seed=0)
