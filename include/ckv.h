@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 1
+#define CKV_ABI_VERSION 2
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -88,7 +88,8 @@ typedef enum ckv_src_kind {
 typedef enum ckv_entry {
   CKV_ENTRY_SELECT_TOPK = 1,
   CKV_ENTRY_SPARSE_DECODE_ATTN = 2,
-  CKV_ENTRY_CRITICAL_KV_ATTN = 3
+  CKV_ENTRY_CRITICAL_KV_ATTN = 3,
+  CKV_ENTRY_CORRECTED_ATTN = 4
 } ckv_entry;
 
 typedef struct ckv_shape {
@@ -181,6 +182,38 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          int32_t* idx_out, int32_t* n_sel_out, float* out,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* Sec. 5.3 (prioritized missing KV transfer) and Sec. 5.4 (GPU-side sparse KV
+ * assembly with deferred reordering) -- one layer of a pipelined decode step
+ * whose attention uses the current token's own selection, not the
+ * prediction.  On entry k_buf/v_buf hold, in slot order, the rows of the
+ * predicted set idx_pred/n_pred: the selection made one step earlier from the
+ * speculative query and gathered ahead of time.  The call
+ *   1. selects idx_true/n_true from q_att exactly as ckv_score_keys +
+ *      ckv_select_topk;
+ *   2. gathers every row of idx_true that is missing from idx_pred from
+ *      k_src/v_src (src_kind says where) into a buffer slot whose predicted
+ *      row is not in idx_true, or a slot past n_pred: the buffer then holds
+ *      every row of idx_true.  hits[b][h] = |idx_true ∩ idx_pred|;
+ *   3. computes out = attention of q_att over exactly the rows of idx_true,
+ *      the same-step result of ckv_critical_kv_attn with q_sel = q_att;
+ *   4. in the same launch as that attention, selects idx_next/n_next from
+ *      q_sel (the speculative query; NULL means q_att): the prediction for
+ *      the next step.
+ * idx_pred must be ascending in [0, max_ctx) and -1 padded, as
+ * ckv_select_topk writes it; n_pred is clamped to [0, k].  k_buf/v_buf are
+ * modified: slots of mispredicted rows are overwritten.  All streams run at
+ * the default priority; the misses are fetched on `stream` ahead of the
+ * attention that needs them.  Workspace: CKV_ENTRY_CORRECTED_ATTN. */
+int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att,
+                       const uint16_t* q_sel, const uint16_t* k_score,
+                       const int32_t* ctx_lens, int32_t k, float scale,
+                       const uint16_t* k_src, const uint16_t* v_src,
+                       int src_kind, const int32_t* idx_pred,
+                       const int32_t* n_pred, uint16_t* k_buf, uint16_t* v_buf,
+                       int32_t* idx_true, int32_t* n_true, int32_t* hits,
+                       int32_t* idx_next, int32_t* n_next, float* out,
+                       void* ws, size_t ws_bytes, void* stream);
+
 /* ---- layer pipeline --------------------------------------------------------
  * The decode loop of Sec. 5.3 (layer-aware transfer overlap) and Sec. 5.4
  * (two-layer ping-pong buffer): the set selected for a layer at step t-1 is
@@ -205,6 +238,9 @@ typedef struct ckv_layer {
   int32_t* idx_next;          /* [B][Hkv][k] written: selected at this step     */
   int32_t* n_sel_next;        /* [B][Hkv] written                               */
   float* out;                 /* [B][Hq][d] written: attention output           */
+  int32_t* idx_true;          /* NULL: attention over the predicted set.  Else  */
+  int32_t* n_true;            /* the layer runs ckv_corrected_attn: [B][Hkv][k], */
+  int32_t* hits;              /* [B][Hkv] and [B][Hkv] written                   */
 } ckv_layer;
 
 typedef struct ckv_pipeline ckv_pipeline; /* events of one decode loop */
@@ -224,11 +260,14 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
 /* One decode step over num_layers >= 2 layers.  For each layer l, on
  * compute_stream: ckv_critical_kv_attn in pipelined mode (attention of q_att
  * over the buffer holding idx_prev's rows, selection from q_sel into
- * idx_next); on copy_stream: the refill of the released buffer with layer
- * l+2, or, for the last two layers, with the next step's layers 0 and 1 from
- * this step's idx_next.  Before the next step the caller swaps idx_prev and
- * idx_next.  ws is the workspace of CKV_ENTRY_CRITICAL_KV_ATTN, used on the
- * compute stream only. */
+ * idx_next), or, for a layer with idx_true set, ckv_corrected_attn (misses
+ * of idx_prev against q_att's own selection fetched into the buffer first,
+ * src_kind and the layer's k_src/v_src); on copy_stream: the refill of the
+ * released buffer with layer l+2, or, for the last two layers, with the next
+ * step's layers 0 and 1 from this step's idx_next.  Before the next step the
+ * caller swaps idx_prev and idx_next.  ws is the workspace of
+ * CKV_ENTRY_CRITICAL_KV_ATTN, or of CKV_ENTRY_CORRECTED_ATTN if any layer
+ * has idx_true set, used on the compute stream only. */
 int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                     const ckv_layer* layers, const int32_t* ctx_lens, int32_t k,
                     float scale, int src_kind, uint16_t* const k_buf[2],
@@ -252,7 +291,8 @@ typedef enum ckv_kernel_id {
   CKV_K_COMBINE = 6,  /* merge of attention partials                        */
   CKV_K_DUAL = 7,     /* one launch: attention (buffer) + scoring           */
   CKV_K_GATHER = 8,   /* sparse K/V assembly                                */
-  CKV_K_COUNT = 9
+  CKV_K_MISS = 9,     /* predicted vs selected set: hits, misses, slots     */
+  CKV_K_COUNT = 10
 } ckv_kernel_id;
 
 #define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)

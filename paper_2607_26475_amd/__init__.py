@@ -21,23 +21,25 @@ import torch
 __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
-    "critical_kv_attn", "profile_begin", "profile_end", "abi_version", "Layer",
-    "Pipeline", "status_str", "LIB_PATH",
+    "critical_kv_attn", "corrected_attn", "profile_begin", "profile_end", "abi_version",
+    "Layer", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
-    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "EXPORTS",
+    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "EXPORTS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
 
 SRC_DEVICE, SRC_HOST_PINNED = 0, 1
 ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
+ENTRY_CORRECTED_ATTN = 4
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
+           "ckv_corrected_attn",
            "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_prime",
            "ckv_decode_step")
-KERNEL_COUNT = 9
+KERNEL_COUNT = 10
 
 
 class CkvError(RuntimeError):
@@ -56,7 +58,7 @@ class Layer(ctypes.Structure):
     """Mirror of ``ckv_layer``."""
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "q_att", "q_sel", "k_score", "k_src", "v_src", "idx_prev", "n_sel_prev",
-        "idx_next", "n_sel_next", "out")]
+        "idx_next", "n_sel_next", "out", "idx_true", "n_true", "hits")]
 
 
 class Shape(ctypes.Structure):
@@ -88,6 +90,9 @@ def _load() -> ctypes.CDLL:
         "ckv_critical_kv_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                                 vp, vp, ctypes.c_int, vp, vp, vp, vp, vp,
                                                 vp, vp, sz, vp]),
+        "ckv_corrected_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
+                                              vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp,
+                                              vp, vp, vp, vp, vp, sz, vp]),
         "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
@@ -200,8 +205,19 @@ def critical_kv_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
         ws.numel() if ws is not None else 0, _stream(stream)))
 
 
+def corrected_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int, scale: float,
+                   k_src, v_src, src_kind: int, idx_pred, n_pred, k_buf, v_buf, idx_true,
+                   n_true, hits, idx_next, n_next, out, ws, stream=None) -> None:
+    _check("ckv_corrected_attn", _lib.ckv_corrected_attn(
+        ctypes.byref(shape), _ptr(q_att), _ptr(q_sel), _ptr(k_score), _ptr(ctx_lens), k,
+        scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(idx_pred), _ptr(n_pred),
+        _ptr(k_buf), _ptr(v_buf), _ptr(idx_true), _ptr(n_true), _ptr(hits), _ptr(idx_next),
+        _ptr(n_next), _ptr(out), _ptr(ws), ws.numel() if ws is not None else 0,
+        _stream(stream)))
+
+
 KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
-              "combine": 6, "dual": 7, "gather": 8}
+              "combine": 6, "dual": 7, "gather": 8, "miss": 9}
 
 
 def profile_begin(kernels=None) -> None:

@@ -100,8 +100,9 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Workspace regions, each 256-byte aligned.  [0, zero_end) is cleared at the
 // start of every selecting call.
 struct Layout {
-  size_t hist = 0, coarse = 0, ctrl = 0, zero_end = 0;
-  size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0, total = 0;
+  size_t hist = 0, coarse = 0, ctrl = 0, hist2 = 0, coarse2 = 0, ctrl2 = 0, zero_end = 0;
+  size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0;
+  size_t slot_of = 0, miss_pos = 0, miss_slot = 0, n_miss = 0, free_slot = 0, total = 0;
   int64_t bm_words = 0;
   int chunks = 0, filter_tiles = 0;
 };
@@ -112,8 +113,11 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
   size_t off = 0;
   L.filter_tiles = (d.max_ctx + kFilterTile - 1) / kFilterTile;
   L.chunks = (k + kAttnRows - 1) / kAttnRows;
-  const bool select = entry == CKV_ENTRY_SELECT_TOPK || entry == CKV_ENTRY_CRITICAL_KV_ATTN;
-  const bool attn = entry == CKV_ENTRY_SPARSE_DECODE_ATTN || entry == CKV_ENTRY_CRITICAL_KV_ATTN;
+  const bool corrected = entry == CKV_ENTRY_CORRECTED_ATTN;
+  const bool select = entry == CKV_ENTRY_SELECT_TOPK || entry == CKV_ENTRY_CRITICAL_KV_ATTN ||
+                      corrected;
+  const bool attn = entry == CKV_ENTRY_SPARSE_DECODE_ATTN ||
+                    entry == CKV_ENTRY_CRITICAL_KV_ATTN || corrected;
   if (select) {
     L.hist = off;
     off += U * kHistBins * 4;
@@ -121,6 +125,14 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
     off += U * kCoarseBins * 4;
     L.ctrl = off;
     off += U * kCtrlWords * 4;
+    if (corrected) {  // the second selection of the call starts from zero too
+      L.hist2 = off;
+      off += U * kHistBins * 4;
+      L.coarse2 = off;
+      off += U * kCoarseBins * 4;
+      L.ctrl2 = off;
+      off += U * kCtrlWords * 4;
+    }
     off = align256(off);
     L.zero_end = off;
     L.sel = off;
@@ -133,13 +145,28 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
       off = align256(off + U * (size_t)L.bm_words * 4);
     }
   }
-  if (entry == CKV_ENTRY_CRITICAL_KV_ATTN) {
+  if (entry == CKV_ENTRY_CRITICAL_KV_ATTN || corrected) {
     L.scores = off;
     off = align256(off + U * (size_t)d.max_ctx * 4);
   }
   if (attn) {
     L.part = off;
     off = align256(off + U * (size_t)L.chunks * d.G * kPartStride * 4);
+  }
+  if (corrected) {
+    const size_t list = align256(U * (size_t)k * 4);
+    L.slot_of = off;
+    off += list;
+    L.miss_pos = off;
+    off += list;
+    L.miss_slot = off;
+    off += list;
+    L.n_miss = off;
+    off = align256(off + U * 4);
+    if (k > kMissLds) {
+      L.free_slot = off;
+      off += list;
+    }
   }
   L.total = off;
   return L;
@@ -298,7 +325,7 @@ int ckv_workspace_bytes(const ckv_shape* shape, int32_t k, int entry, size_t* by
   if ((rc = check_k(k))) return rc;
   if (!bytes) return fail(CKV_EINVAL, "bytes is NULL");
   if (entry != CKV_ENTRY_SELECT_TOPK && entry != CKV_ENTRY_SPARSE_DECODE_ATTN &&
-      entry != CKV_ENTRY_CRITICAL_KV_ATTN)
+      entry != CKV_ENTRY_CRITICAL_KV_ATTN && entry != CKV_ENTRY_CORRECTED_ATTN)
     return fail(CKV_EINVAL, "unknown entry %d", entry);
   *bytes = make_layout(d, k, entry).total;
   return CKV_OK;
@@ -364,6 +391,7 @@ int ckv_gather_kv(const ckv_shape* shape, const uint16_t* k_src, const uint16_t*
   a.v_src = v_src;
   a.idx = idx;
   a.n_sel = n_sel;
+  a.slots = nullptr;
   a.k_dst = k_dst;
   a.v_dst = v_dst;
   a.row_stride = d.kv_stride;
@@ -441,7 +469,7 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   if (pipelined) {
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel_in, kD, k,
                              scale, out);
-    CKV_TRY_HIP(launch_dual(at_, sc, d.G, d.U, s), "dual launch");
+    CKV_TRY_HIP(launch_dual(at_, sc, d.G, false, d.U, s), "dual launch");
     if ((rc = run_select_tail(sa, d.U, s))) return rc;
     CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   } else {
@@ -452,6 +480,93 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
     CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
     CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   }
+  return CKV_OK;
+}
+
+int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                       const uint16_t* k_score, const int32_t* ctx_lens, int32_t k,
+                       float scale, const uint16_t* k_src, const uint16_t* v_src,
+                       int src_kind, const int32_t* idx_pred, const int32_t* n_pred,
+                       uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
+                       int32_t* n_true, int32_t* hits, int32_t* idx_next, int32_t* n_next,
+                       float* out, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  CKV_PTR(q_att);
+  if (!q_sel) q_sel = q_att;
+  CKV_PTR(q_sel);
+  CKV_PTR(k_score);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(k_src);
+  CKV_PTR(v_src);
+  CKV_PTR(idx_pred);
+  CKV_PTR(n_pred);
+  CKV_PTR(k_buf);
+  CKV_PTR(v_buf);
+  CKV_PTR(idx_true);
+  CKV_PTR(n_true);
+  CKV_PTR(hits);
+  CKV_PTR(idx_next);
+  CKV_PTR(n_next);
+  CKV_PTR(out);
+  if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
+  Layout L = make_layout(d, k, CKV_ENTRY_CORRECTED_ATTN);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  float* scores = at<float>(ws, L.scores);
+  CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
+  // 1. the current token's own selection
+  SelectArgs s1 = select_args(d, L, ws, scores, ctx_lens, k, idx_true, n_true);
+  ScoreArgs c1 = score_args(d, L, q_att, k_score, ctx_lens, scale, scores, s1.hist, s1.coarse);
+  CKV_TRY_HIP(launch_score(c1, d.G, true, d.U, s), "score launch");
+  if ((rc = run_select_tail(s1, d.U, s))) return rc;
+  // 2. hits and misses against the predicted set; misses into free slots
+  MissArgs m;
+  m.idx_true = idx_true;
+  m.n_true = n_true;
+  m.idx_pred = idx_pred;
+  m.n_pred = n_pred;
+  m.slot_of = at<int32_t>(ws, L.slot_of);
+  m.miss_pos = at<int32_t>(ws, L.miss_pos);
+  m.miss_slot = at<int32_t>(ws, L.miss_slot);
+  m.n_miss = at<int32_t>(ws, L.n_miss);
+  m.hits = hits;
+  m.free_slot = L.free_slot ? at<int32_t>(ws, L.free_slot) : nullptr;
+  m.k = k;
+  CKV_TRY_HIP(launch_miss(m, d.U, s), "miss launch");
+  GatherArgs g;
+  g.k_src = k_src;
+  g.v_src = v_src;
+  g.idx = m.miss_pos;
+  g.n_sel = m.n_miss;
+  g.slots = m.miss_slot;
+  g.k_dst = k_buf;
+  g.v_dst = v_buf;
+  g.row_stride = d.kv_stride;
+  g.items = (int64_t)d.U * k * 32;
+  g.max_ctx = d.max_ctx;
+  g.k = k;
+  CKV_TRY_HIP(launch_gather(g, gather_blocks(src_kind), s), "miss gather launch");
+  // 3. attention over exactly the selected rows, now all in the buffer (read
+  //    through the slot list), in one launch with 4. the next step's scoring
+  SelectArgs s2 = select_args(d, L, ws, scores, ctx_lens, k, idx_next, n_next);
+  s2.hist = at<uint32_t>(ws, L.hist2);
+  s2.coarse = at<uint32_t>(ws, L.coarse2);
+  s2.ctrl = at<uint32_t>(ws, L.ctrl2);
+  ScoreArgs c2 = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, s2.hist, s2.coarse);
+  // the buffer as an indexed source: unit u's slot r is row r of [U][k][d]
+  Dims db = d;
+  db.max_ctx = k;
+  AttnArgs at_ = attn_args(db, L, ws, q_att, k_buf, v_buf, m.slot_of, n_true, kD, k, scale,
+                           out);
+  CKV_TRY_HIP(launch_dual(at_, c2, d.G, true, d.U, s), "dual launch");
+  if ((rc = run_select_tail(s2, d.U, s))) return rc;
+  CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   return CKV_OK;
 }
 

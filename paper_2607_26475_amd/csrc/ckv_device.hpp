@@ -97,11 +97,30 @@ struct GatherArgs {
   const uint16_t* v_src;
   const int32_t* idx;
   const int32_t* n_sel;
+  const int32_t* slots;     // [U][k] destination slot of entry i; NULL: slot i
   uint16_t* k_dst;
   uint16_t* v_dst;
   int64_t row_stride;
   int64_t items;            // U * k * 32
   int max_ctx, k;
+};
+
+// Miss detection: the selected set against the predicted set in the buffer.
+constexpr int kMissThreads = 1024;
+constexpr int kMissLds = 8192;  // budgets up to this keep both sets in LDS
+
+struct MissArgs {
+  const int32_t* idx_true;  // [U][k] ascending, -1 padded
+  const int32_t* n_true;    // [U]
+  const int32_t* idx_pred;  // [U][k] ascending, -1 padded
+  const int32_t* n_pred;    // [U]
+  int32_t* slot_of;         // [U][k] written: buffer slot of idx_true[i]
+  int32_t* miss_pos;        // [U][k] written: positions to fetch
+  int32_t* miss_slot;       // [U][k] written: their slots
+  int32_t* n_miss;          // [U] written
+  int32_t* hits;            // [U] written
+  int32_t* free_slot;       // [U][k] scratch when k > kMissLds
+  int k;
 };
 
 // ---- small device helpers ---------------------------------------------------

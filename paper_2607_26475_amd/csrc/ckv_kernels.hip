@@ -392,7 +392,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(AttnArgs a) {
 // One launch, two roles (pipelined decode): the first attn_blocks workgroups
 // attend with q_att over the buffer assembled for this step, the rest score
 // the context with q_sel for the next step's selection.
-template <int G>
+template <int G, bool INDEXED>
 __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc,
                                                       int attn_blocks) {
   static_assert(kAttnThreads == kScoreThreads, "roles share the block size");
@@ -401,7 +401,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
   __shared__ __attribute__((aligned(16))) float lds[kA > kS ? kA : kS];
   if ((int)blockIdx.x < attn_blocks) {
     const int unit = blockIdx.x / at.chunks;
-    attn_chunk<G, false>(at, unit, blockIdx.x - unit * at.chunks, lds);
+    attn_chunk<G, INDEXED>(at, unit, blockIdx.x - unit * at.chunks, lds);
   } else {
     uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
     score_range<G, true>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks,
@@ -470,9 +470,99 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
   }
 }
 
+// ---- miss detection -----------------------------------------------------------
+// First index i in [0, n) with a[i] >= v (a ascending).
+template <class P>
+__device__ __forceinline__ int lower_bound_i32(P a, int n, int v) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a[mid] < v) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// One unit: which rows of the selected set (T, nt) the buffer already holds
+// (the predicted set P, np, in slot order), and where the others go.  Free
+// slots are those whose predicted row is not selected, then slots np..nt-1;
+// there are at least as many as misses.  Miss r (in set order) takes the r-th
+// free slot.  T/P/F are LDS arrays or the global sets, per IN_LDS.
+template <bool IN_LDS>
+__device__ __forceinline__ void miss_unit(const MissArgs& a, int unit, const int32_t* T,
+                                          const int32_t* P, int32_t* F, int nt, int np,
+                                          uint32_t* tmp) {
+  const int k = a.k, tid = threadIdx.x;
+  const int64_t base = (int64_t)unit * k;
+  const int ns = max(np, nt);
+  uint32_t nfree = 0;
+  for (int s0 = 0; s0 < ns; s0 += kMissThreads) {
+    const int sl = s0 + tid;
+    bool fr = false;
+    if (sl < ns) {
+      if (sl < np) {
+        const int pos = P[sl];
+        const int j = lower_bound_i32(T, nt, pos);
+        fr = !(j < nt && T[j] == pos);
+      } else {
+        fr = true;
+      }
+    }
+    uint32_t total;
+    const uint32_t incl = block_incl_scan<kMissThreads / 64>(fr ? 1u : 0u, tmp, &total);
+    if (fr) F[nfree + incl - 1] = sl;
+    nfree += total;
+  }
+  __syncthreads();  // the free list is complete
+  uint32_t nmiss = 0;
+  for (int i0 = 0; i0 < nt; i0 += kMissThreads) {
+    const int i = i0 + tid;
+    bool miss = false;
+    int slot = -1, pos = 0;
+    if (i < nt) {
+      pos = T[i];
+      const int j = lower_bound_i32(P, np, pos);
+      if (j < np && P[j] == pos) slot = j;
+      else miss = true;
+    }
+    uint32_t total;
+    const uint32_t incl = block_incl_scan<kMissThreads / 64>(miss ? 1u : 0u, tmp, &total);
+    if (miss) {
+      const uint32_t r = nmiss + incl - 1;  // < nfree
+      slot = F[r];
+      a.miss_pos[base + r] = pos;
+      a.miss_slot[base + r] = slot;
+    }
+    if (i < nt) a.slot_of[base + i] = slot;
+    nmiss += total;
+  }
+  if (tid == 0) {
+    a.n_miss[unit] = (int32_t)nmiss;
+    a.hits[unit] = nt - (int32_t)nmiss;
+  }
+}
+
+__global__ __launch_bounds__(kMissThreads) void k_miss(MissArgs a) {
+  __shared__ int32_t l_true[kMissLds], l_pred[kMissLds], l_free[kMissLds];
+  __shared__ uint32_t tmp[kMissThreads / 64 + 1];
+  const int unit = blockIdx.x, k = a.k;
+  const int nt = clamp_len(a.n_true[unit], k), np = clamp_len(a.n_pred[unit], k);
+  const int32_t* gt = a.idx_true + (int64_t)unit * k;
+  const int32_t* gp = a.idx_pred + (int64_t)unit * k;
+  if (k <= kMissLds) {  // uniform
+    for (int i = threadIdx.x; i < nt; i += kMissThreads) l_true[i] = gt[i];
+    for (int i = threadIdx.x; i < np; i += kMissThreads) l_pred[i] = gp[i];
+    __syncthreads();
+    miss_unit<true>(a, unit, l_true, l_pred, l_free, nt, np, tmp);
+  } else {
+    miss_unit<false>(a, unit, gt, gp, a.free_slot + (int64_t)unit * k, nt, np, tmp);
+  }
+}
+
 // ---- gather ----------------------------------------------------------------
 // Item it = ((unit*k + slot)*2 + kv)*16 + part moves 16 bytes; the 32 items of
 // one slot are its K row then its V row (contiguous for K|V interleaved rows).
+// With a slot list, entry slot of the unit lands in slot slots[unit][slot].
 __global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
   const int64_t step = (int64_t)gridDim.x * kGatherThreads * kGatherUnroll;
   for (int64_t it0 = (int64_t)blockIdx.x * kGatherThreads * kGatherUnroll; it0 < a.items;
@@ -491,11 +581,12 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
         const int i = (int)(slot - unit * a.k);
         if (i < a.n_sel[unit]) {
           const int pos = a.idx[slot];
-          if (pos >= 0 && pos < a.max_ctx) {
+          const int di = a.slots ? a.slots[slot] : i;
+          if (pos >= 0 && pos < a.max_ctx && di >= 0 && di < a.k) {
             const uint16_t* src = (kv ? a.v_src : a.k_src) +
                                   (unit * a.max_ctx + pos) * a.row_stride + part * 8;
             v[u] = ld16(src);
-            dst[u] = (kv ? a.v_dst : a.k_dst) + slot * kD + part * 8;
+            dst[u] = (kv ? a.v_dst : a.k_dst) + (unit * a.k + di) * kD + part * 8;
           }
         }
       }
@@ -619,26 +710,38 @@ hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int G>
+template <int G, bool INDEXED>
 static void launch_dual_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks,
                           hipStream_t s) {
-  auto fn = k_dual<G>;
+  auto fn = k_dual<G, INDEXED>;
   const int score_blocks = score_grid(sc, (const void*)fn);
   launch_kernel(CKV_K_DUAL, fn, dim3(attn_blocks + score_blocks), dim3(kAttnThreads), s, at,
                 sc, attn_blocks);
 }
 
-hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, int units,
-                       hipStream_t s) {
-  const int attn_blocks = units * at.chunks;
+template <bool INDEXED>
+static hipError_t launch_dual_i(const AttnArgs& at, const ScoreArgs& sc, int G,
+                                int attn_blocks, hipStream_t s) {
   switch (G) {
-    case 1: launch_dual_g<1>(at, sc, attn_blocks, s); break;
-    case 2: launch_dual_g<2>(at, sc, attn_blocks, s); break;
-    case 4: launch_dual_g<4>(at, sc, attn_blocks, s); break;
-    case 8: launch_dual_g<8>(at, sc, attn_blocks, s); break;
-    case 16: launch_dual_g<16>(at, sc, attn_blocks, s); break;
+    case 1: launch_dual_g<1, INDEXED>(at, sc, attn_blocks, s); break;
+    case 2: launch_dual_g<2, INDEXED>(at, sc, attn_blocks, s); break;
+    case 4: launch_dual_g<4, INDEXED>(at, sc, attn_blocks, s); break;
+    case 8: launch_dual_g<8, INDEXED>(at, sc, attn_blocks, s); break;
+    case 16: launch_dual_g<16, INDEXED>(at, sc, attn_blocks, s); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
+                       int units, hipStream_t s) {
+  const int attn_blocks = units * at.chunks;
+  return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, s)
+                 : launch_dual_i<false>(at, sc, G, attn_blocks, s);
+}
+
+hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s) {
+  launch_kernel(CKV_K_MISS, k_miss, dim3(units), dim3(kMissThreads), s, a);
   return hipGetLastError();
 }
 

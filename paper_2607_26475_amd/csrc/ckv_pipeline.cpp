@@ -78,10 +78,18 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     const ckv_layer& L = layers[l];
     // attention over buffer p once its gather has landed
     if (hipStreamWaitEvent(cs, pipe->filled[p], 0) != hipSuccess) return CKV_EHIP;
-    int rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
-                                  nullptr, nullptr, src_kind, k_buf[p], v_buf[p],
-                                  L.n_sel_prev, L.idx_next, L.n_sel_next, L.out, ws,
-                                  ws_bytes, compute_stream);
+    int rc;
+    if (L.idx_true) {  // the current query's own set: misses fetched into buffer p first
+      rc = ckv_corrected_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale, L.k_src,
+                              L.v_src, src_kind, L.idx_prev, L.n_sel_prev, k_buf[p],
+                              v_buf[p], L.idx_true, L.n_true, L.hits, L.idx_next,
+                              L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
+    } else {
+      rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
+                                nullptr, nullptr, src_kind, k_buf[p], v_buf[p], L.n_sel_prev,
+                                L.idx_next, L.n_sel_next, L.out, ws, ws_bytes,
+                                compute_stream);
+    }
     if (rc) return rc;
     if (hipEventRecord(pipe->freed[p], cs) != hipSuccess) return CKV_EHIP;
     // refill buffer p with the layer two ahead (into the next step at the end)

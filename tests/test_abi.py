@@ -33,7 +33,7 @@ def test_header_functions_are_exported():
 
 
 def test_abi_version_and_status_text():
-    assert ckv.abi_version() == 1
+    assert ckv.abi_version() == 2
     texts = {ckv.status_str(v) for v in STATUS.values()}
     assert len(texts) == len(STATUS)
     assert ckv.status_str(99) == "unknown status"
@@ -123,3 +123,29 @@ def test_pipeline_argument_checks():
                                   None) == STATUS["EINVAL"]
     assert lib.ckv_decode_step(None, ctypes.byref(s), 2, layers, FAKE, 16, 0.1, 0, bufs,
                                bufs, FAKE, 1 << 20, None, None) == STATUS["EINVAL"]
+
+
+def test_corrected_attn_argument_checks():
+    lib = ckv._lib
+    s = good_shape()
+    need = ckv.workspace_bytes(s, 16, ckv.ENTRY_CORRECTED_ATTN)
+    assert need >= ckv.workspace_bytes(s, 16, ckv.ENTRY_CRITICAL_KV_ATTN)
+    # larger budgets than the LDS miss lists hold need a free-slot list too
+    assert (ckv.workspace_bytes(good_shape(max_ctx=20000), 9000, ckv.ENTRY_CORRECTED_ATTN) >
+            ckv.workspace_bytes(good_shape(max_ctx=20000), 9000, ckv.ENTRY_CRITICAL_KV_ATTN))
+
+    def call(**kw):
+        args = dict(q_att=FAKE, q_sel=None, k_score=FAKE, lens=FAKE, k=16, scale=0.1,
+                    k_src=FAKE, v_src=FAKE, kind=0, idx_pred=FAKE, n_pred=FAKE, k_buf=FAKE,
+                    v_buf=FAKE, idx_true=FAKE, n_true=FAKE, hits=FAKE, idx_next=FAKE,
+                    n_next=FAKE, out=FAKE, ws=FAKE, ws_bytes=need)
+        args.update(kw)
+        return lib.ckv_corrected_attn(ctypes.byref(s), *args.values(), None)
+
+    assert call(idx_pred=None) == STATUS["EINVAL"]
+    assert call(hits=None) == STATUS["EINVAL"]
+    assert call(k_buf=FAKE + 8) == STATUS["EINVAL"]
+    assert call(kind=5) == STATUS["EINVAL"]
+    assert call(k=0) == STATUS["ESHAPE"]
+    assert call(ws_bytes=need - 1) == STATUS["EWORKSPACE"]
+    assert call(ws=None) == STATUS["EWORKSPACE"]

@@ -57,11 +57,15 @@ class Loop:
         self.idx = [mk(), mk()]
         self.nsel = [mn(), mn()]
         self.out = [torch.full((B, Hq, d), float("nan"), device=dev) for _ in range(layers)]
+        self.corrected = False
+        self.idx_true = mk()
+        self.n_true = mn()
+        self.hits = mn()
         self.k_buf = [torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev)
                       for _ in range(2)]
         self.v_buf = [torch.empty_like(self.k_buf[0]) for _ in range(2)]
         self.shape = ckv.shape_for(B, Hq, Hkv, w.max_ctx, kv_row_stride=2 * d)
-        self.ws = ckv.workspace(self.shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        self.ws = ckv.workspace(self.shape, k, ckv.ENTRY_CORRECTED_ATTN)
         self.copy = torch.cuda.Stream(device=dev)
         self.compute = torch.cuda.current_stream(dev)
 
@@ -73,7 +77,10 @@ class Loop:
                  "v_src": self.kv_host[l].data_ptr() + 2 * d,
                  "idx_prev": self.idx[cur][l], "n_sel_prev": self.nsel[cur][l],
                  "idx_next": self.idx[nxt][l], "n_sel_next": self.nsel[nxt][l],
-                 "out": self.out[l]} for l in range(self.L)]
+                 "out": self.out[l],
+                 "idx_true": self.idx_true[l] if self.corrected else None,
+                 "n_true": self.n_true[l] if self.corrected else None,
+                 "hits": self.hits[l] if self.corrected else None} for l in range(self.L)]
 
     def bootstrap(self):
         """Selection before the first step (the pre-decoding step), into set 0."""
@@ -103,7 +110,10 @@ class Loop:
             nxt = 1 - cur
             hist.append(([i.cpu().numpy() for i in self.idx[nxt]],
                          [n.cpu().numpy() for n in self.nsel[nxt]],
-                         [o.cpu().numpy() for o in self.out]))
+                         [o.cpu().numpy() for o in self.out],
+                         [i.cpu().numpy() for i in self.idx_true],
+                         [n.cpu().numpy() for n in self.n_true],
+                         [h.cpu().numpy() for h in self.hits]))
             cur = nxt
         return hist
 
@@ -124,7 +134,7 @@ def test_pipeline_matches_oracle(wl, layers):
     so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
     prev_sets = boot
     for st in range(1, 3):
-        g_idx, g_nsel, g_out = hist[st - 1]
+        g_idx, g_nsel, g_out = hist[st - 1][:3]
         for l in range(layers):
             K, V = u16(lp.t[l]["k"]), u16(lp.t[l]["v"])
             # selection at this step from this step's speculative query
@@ -169,8 +179,57 @@ def test_pipeline_ordering_under_delay(stream_name):
     lp.bootstrap()
     got = lp.run(2, pipe, delay=_Delay(stream_name, dev))
     pipe.close()
-    for (ri, rn, ro), (gi, gn, go) in zip(ref, got):
+    for (ri, rn, ro, *_), (gi, gn, go, *_) in zip(ref, got):
         for l in range(3):
             np.testing.assert_array_equal(ri[l], gi[l])
             np.testing.assert_array_equal(rn[l], gn[l])
             np.testing.assert_array_equal(ro[l], go[l])
+
+
+@pytest.mark.parametrize("wl,layers", [("dual64_s", 3), ("long128k_s", 2)])
+def test_pipeline_corrected_matches_oracle(wl, layers):
+    """Corrected layers in the decode loop: whatever was prefetched from the
+    previous step's speculative selection, each layer's output is the current
+    query's attention over its own top-k (the same-step result), the misses
+    against the prefetched set are counted in hits, and the speculative
+    selection for the next step is made as before."""
+    _log("pipeline corrected", wl, layers)
+    dev = device()
+    w = synth.WORKLOADS[wl]
+    lp = Loop(w, layers, steps=2, seed=11, dev=dev)
+    lp.corrected = True
+    lp.bootstrap()
+    boot = [i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]]
+    pipe = ckv.Pipeline()
+    hist = lp.run(2, pipe)
+    pipe.close()
+    o = orc()
+    lens = lp.lens.cpu().numpy()
+    so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
+    prev_pred = boot
+    for st in range(1, 3):
+        g_idx, g_nsel, g_out, g_true, g_ntrue, g_hits = hist[st - 1]
+        for l in range(layers):
+            K, V = u16(lp.t[l]["k"]), u16(lp.t[l]["v"])
+            q_att = u16(lp.q_att[st][l])
+            S = o.score_keys(so, q_att, K, lens, SCALE, nthreads=8)
+            r_true, r_nt = o.select_topk(so, S, lens, w.k, nthreads=8)
+            check_index_sets(g_true[l], g_ntrue[l], r_true, r_nt, S, lens)
+            S2 = o.score_keys(so, u16(lp.q_sel[st][l]), K, lens, SCALE, nthreads=8)
+            r_next, r_nn = o.select_topk(so, S2, lens, w.k, nthreads=8)
+            check_index_sets(g_idx[l], g_nsel[l], r_next, r_nn, S2, lens)
+            total = found = 0
+            for b in range(w.batch):
+                for h in range(w.kv_heads):
+                    t_ = g_true[l][b, h, :g_ntrue[l][b, h]]
+                    p_ = prev_pred[0][l][b, h, :prev_pred[1][l][b, h]]
+                    want = len(np.intersect1d(t_, p_))
+                    assert g_hits[l][b, h] == want, (st, l, b, h)
+                    total += len(t_)
+                    found += want
+            ref = oracle_attn_over(so, q_att, K, V, g_true[l], g_ntrue[l], w.k)
+            err = np.abs(g_out[l] - ref).max()
+            _log(f"  step {st} layer {l}: hit rate {found / max(total, 1):.3f}, "
+                 f"max abs err {err:.2e}")
+            assert err <= ATOL_OUT
+        prev_pred = (g_idx, g_nsel)
