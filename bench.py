@@ -317,8 +317,12 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
     heads, n 131072, k 4096, 32 layers; K|V rows in pinned host memory,
     scoring keys in HBM.  Layer inputs cycle over 4 distinct HBM and 2 distinct
     host layers (each far larger than any cache); queries are distinct per
-    layer and step.  Step time from events on the compute stream after it has
-    joined the copy stream."""
+    layer and step.  The speculative query of step t is 0.8 x the query of step
+    t+1 plus 0.6 x noise (the dual workload's recipe).  Two runs over the same
+    inputs: attention over the prefetched prediction, and with miss correction
+    (each layer attends over its own query's set, misses fetched on the compute
+    stream).  Step time from events on the compute stream after it has joined
+    the copy stream."""
     w = synth.WORKLOADS["long128k"]
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
@@ -336,70 +340,90 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
     g = torch.Generator(device=dev)
     g.manual_seed(1234)
     q = [[torch.randn((B, Hq, d), generator=g, device=dev).to(torch.bfloat16)
-          for _ in range(L)] for _ in range(steps + 2)]
-    idx = [[torch.empty((B, Hkv, k), dtype=torch.int32, device=dev) for _ in range(L)]
-           for _ in range(2)]
-    nsel = [[torch.empty((B, Hkv), dtype=torch.int32, device=dev) for _ in range(L)]
-            for _ in range(2)]
+          for _ in range(L)] for _ in range(steps + 3)]
+    qs = [[(0.8 * q[st + 1][l].float() + 0.6 * torch.randn((B, Hq, d), generator=g,
+                                                           device=dev)).to(torch.bfloat16)
+           for l in range(L)] for st in range(steps + 2)]
+    i32 = dict(dtype=torch.int32, device=dev)
+    idx = [[torch.empty((B, Hkv, k), **i32) for _ in range(L)] for _ in range(2)]
+    nsel = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(2)]
+    idx_true = [torch.empty((B, Hkv, k), **i32) for _ in range(L)]
+    n_true = [torch.empty((B, Hkv), **i32) for _ in range(L)]
+    hits = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(steps + 1)]
     out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
     k_buf = [torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev) for _ in range(2)]
     v_buf = [torch.empty_like(k_buf[0]) for _ in range(2)]
     shape = ckv.shape_for(B, Hq, Hkv, n, kv_row_stride=2 * d)
-    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    ws = ckv.workspace(shape, k, ckv.ENTRY_CORRECTED_ATTN)
     compute = torch.cuda.current_stream()
     copy = torch.cuda.Stream()
-
-    def io(step, cur):
-        return [{"q_att": q[step][l], "q_sel": q[step + 1][l], "k_score": kscore[l % n_hbm],
-                 "k_src": hosts[l % n_host].data_ptr(),
-                 "v_src": hosts[l % n_host].data_ptr() + 2 * d,
-                 "idx_prev": idx[cur][l], "n_sel_prev": nsel[cur][l],
-                 "idx_next": idx[1 - cur][l], "n_sel_next": nsel[1 - cur][l],
-                 "out": out[l]} for l in range(L)]
-
-    # bootstrap selection (the pre-decoding step) into set 0
     s1 = ckv.shape_for(B, Hq, Hkv, n)
     sc = torch.empty((B, Hkv, n), device=dev)
     wsel = ckv.workspace(s1, k, ckv.ENTRY_SELECT_TOPK)
-    for l in range(L):
-        ckv.score_keys(s1, q[0][l], kscore[l % n_hbm], lens, scale, sc)
-        ckv.select_topk(s1, sc, lens, k, idx[0][l], nsel[0][l], wsel)
-    torch.cuda.synchronize()
-    pipe = ckv.Pipeline()
-    copy.wait_stream(compute)
-    pipe.prime(shape, k, io(0, 0), ckv.SRC_HOST_PINNED, k_buf, v_buf, copy)
-    cur = 0
-    pipe.step(shape, io(0, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf, ws,
-              compute, copy)  # warm-up step
-    cur = 1 - cur
-    compute.wait_stream(copy)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ckv.profile_begin()
-    e0.record(compute)
-    for st in range(1, steps + 1):
-        pipe.step(shape, io(st, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf, ws,
-                  compute, copy)
+
+    def run(corrected):
+        def io(step, cur):
+            return [{"q_att": q[step][l], "q_sel": qs[step][l], "k_score": kscore[l % n_hbm],
+                     "k_src": hosts[l % n_host].data_ptr(),
+                     "v_src": hosts[l % n_host].data_ptr() + 2 * d,
+                     "idx_prev": idx[cur][l], "n_sel_prev": nsel[cur][l],
+                     "idx_next": idx[1 - cur][l], "n_sel_next": nsel[1 - cur][l],
+                     "out": out[l],
+                     "idx_true": idx_true[l] if corrected else None,
+                     "n_true": n_true[l] if corrected else None,
+                     "hits": hits[step][l] if corrected else None} for l in range(L)]
+
+        # bootstrap selection (the pre-decoding step) into set 0
+        for l in range(L):
+            ckv.score_keys(s1, q[0][l], kscore[l % n_hbm], lens, scale, sc)
+            ckv.select_topk(s1, sc, lens, k, idx[0][l], nsel[0][l], wsel)
+        torch.cuda.synchronize()
+        pipe = ckv.Pipeline()
+        copy.wait_stream(compute)
+        pipe.prime(shape, k, io(0, 0), ckv.SRC_HOST_PINNED, k_buf, v_buf, copy)
+        cur = 0
+        pipe.step(shape, io(0, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf, ws,
+                  compute, copy)  # warm-up step
         cur = 1 - cur
-    compute.wait_stream(copy)
-    e1.record(compute)
-    torch.cuda.synchronize()
-    stats = ckv.profile_end()
-    pipe.close()
-    ms = e0.elapsed_time(e1) / steps
-    host_bytes = L * B * Hkv * k * 2 * d * 2
-    gather_ms = stats.get("gather", (0, 0.0, 0.0))[1] / steps
-    compute_ms = sum(v[1] for kname, v in stats.items() if kname != "gather") / steps
-    res = {"workload": "long-context decode, 32 layers: B8, 32 q / 8 KV heads, head_dim 128, "
+        compute.wait_stream(copy)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ckv.profile_begin()
+        e0.record(compute)
+        for st in range(1, steps + 1):
+            pipe.step(shape, io(st, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf,
+                      ws, compute, copy)
+            cur = 1 - cur
+        compute.wait_stream(copy)
+        e1.record(compute)
+        torch.cuda.synchronize()
+        stats = ckv.profile_end()
+        pipe.close()
+        ms = e0.elapsed_time(e1) / steps
+        host_bytes = L * B * Hkv * k * 2 * d * 2
+        gather_ms = stats.get("gather", (0, 0.0, 0.0))[1] / steps
+        compute_ms = sum(v[1] for kname, v in stats.items() if kname != "gather") / steps
+        res = {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3),
+               "host_bytes_per_step": host_bytes,
+               "host_GBps_step": host_bytes / (ms * 1e-3) / 1e9,
+               "gather_ms_per_step": gather_ms, "compute_kernels_ms_per_step": compute_ms,
+               "overlap": (gather_ms + compute_ms) / ms}
+        if corrected:  # the misses cross the link too, on the compute stream
+            found = sum(int(hits[st][l].sum()) for st in range(1, steps + 1) for l in range(L))
+            total = steps * L * B * Hkv * min(k, n)
+            res["hit_rate"] = found / total
+            res["miss_bytes_per_step"] = (total - found) / steps * 2 * d * 2
+            res["host_bytes_per_step"] = host_bytes + res["miss_bytes_per_step"]
+            res["host_GBps_step"] = res["host_bytes_per_step"] / (ms * 1e-3) / 1e9
+        if host_link:
+            res["frac_of_h2d_copy"] = res["host_GBps_step"] / host_link["h2d_copy_GBps"]
+        return res
+
+    res = run(False)
+    res["workload"] = ("long-context decode, 32 layers: B8, 32 q / 8 KV heads, head_dim 128, "
                        "context 131072, k 4096; K|V rows host-pinned, scoring keys in HBM; "
-                       "4 HBM and 2 host layers cycled",
-           "ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3),
-           "host_bytes_per_step": host_bytes,
-           "host_GBps_step": host_bytes / (ms * 1e-3) / 1e9,
-           "gather_ms_per_step": gather_ms, "compute_kernels_ms_per_step": compute_ms,
-           "overlap": (gather_ms + compute_ms) / ms}
-    if host_link:
-        res["frac_of_h2d_copy"] = res["host_GBps_step"] / host_link["h2d_copy_GBps"]
+                       "4 HBM and 2 host layers cycled")
+    res["corrected"] = run(True)
     del hosts
     return res
 
