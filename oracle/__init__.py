@@ -78,8 +78,15 @@ class Oracle:
         lib.ckvref_sparse_decode_attn.argtypes = [sp, vp, vp, vp, vp, i32, f32, vp, i32]
         lib.ckvref_critical_kv_attn.argtypes = [sp, vp, vp, vp, vp, vp, vp, i32, f32,
                                                 vp, vp, vp, i32]
+        lib.ckvref_f64_to_bf16.restype = ctypes.c_uint16
+        lib.ckvref_f64_to_bf16.argtypes = [ctypes.c_double]
+        lib.ckvref_chunk_landmarks.argtypes = [sp, i32, vp, vp, vp]
+        lib.ckvref_expand_chunks.argtypes = [i32, i32, vp, i32, i32, vp]
+        lib.ckvref_select_chunks.argtypes = [sp, i32, vp, vp, vp, i32, f32, vp, vp, vp, vp,
+                                             i32]
         for f in ("ckvref_score_keys", "ckvref_select_topk", "ckvref_gather_kv",
-                  "ckvref_sparse_decode_attn", "ckvref_critical_kv_attn"):
+                  "ckvref_sparse_decode_attn", "ckvref_critical_kv_attn",
+                  "ckvref_chunk_landmarks", "ckvref_expand_chunks", "ckvref_select_chunks"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
 
@@ -173,6 +180,42 @@ class Oracle:
                                               _p(out), nthreads)
         assert rc == 0
         return idx, n_sel, out
+
+
+    # ---- chunk landmarks --------------------------------------------------
+    def f64_to_bf16(self, x: float) -> int:
+        return self.lib.ckvref_f64_to_bf16(float(x))
+
+    def chunk_landmarks(self, s: _Shape, chunk: int, keys, ctx_lens, fill=0xFFFF):
+        """[B][Hkv][ceil(max_ctx/chunk)][d] uint16; unwritten rows keep `fill`."""
+        keys, lens = _u16(keys), _i32(ctx_lens)
+        cmax = (s.max_ctx + chunk - 1) // chunk
+        out = np.full((s.batch, s.num_kv_heads, cmax, s.head_dim), fill, dtype=np.uint16)
+        rc = self.lib.ckvref_chunk_landmarks(ctypes.byref(s), chunk, _p(keys), _p(lens),
+                                             _p(out))
+        assert rc == 0
+        return out
+
+    def expand_chunks(self, chunk: int, chunk_idx, n: int, k: int) -> Tuple[np.ndarray, int]:
+        ci = _i32(chunk_idx)
+        rows = np.full(k, -7, dtype=np.int32)
+        r = self.lib.ckvref_expand_chunks(chunk, len(ci), _p(ci), n, k, _p(rows))
+        return rows, r
+
+    def select_chunks(self, s: _Shape, chunk: int, q_sel, landmarks, ctx_lens, k, scale,
+                      nthreads=1):
+        q_sel, lm, lens = _u16(q_sel), _u16(landmarks), _i32(ctx_lens)
+        kc = k // chunk
+        U = (s.batch, s.num_kv_heads)
+        cidx = np.full(U + (kc,), -7, dtype=np.int32)
+        nch = np.full(U, -7, dtype=np.int32)
+        rows = np.full(U + (k,), -7, dtype=np.int32)
+        nrows = np.full(U, -7, dtype=np.int32)
+        rc = self.lib.ckvref_select_chunks(ctypes.byref(s), chunk, _p(q_sel), _p(lm), _p(lens),
+                                           k, scale, _p(cidx), _p(nch), _p(rows), _p(nrows),
+                                           nthreads)
+        assert rc == 0
+        return cidx, nch, rows, nrows
 
 
 _default: Optional[Oracle] = None

@@ -336,3 +336,89 @@ int ckvref_critical_kv_attn(const ckvref_shape* s, const uint16_t* q_att,
   run_units(&jb, s->batch * s->num_kv_heads, nthreads);
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* chunk landmarks                                                           */
+
+/* Round to 8 significant bits (bf16), ties to even: |x| = m * 2^e with m in
+ * [0.5, 1) has quantum 2^(e-8); below the smallest normal bf16 (2^-126) the
+ * quantum stays 2^-133.  nearbyint rounds ties to even in the default mode. */
+uint16_t ckvref_f64_to_bf16(double x) {
+  const uint16_t sign = signbit(x) ? 0x8000u : 0u;
+  const double a = fabs(x);
+  if (a == 0.0) return sign;
+  int e;
+  (void)frexp(a, &e);
+  int q = e - 8;
+  if (q < -133) q = -133;
+  const double y = ldexp(nearbyint(ldexp(a, -q)), q);
+  const float f = (float)y; /* exact: at most 8 significant bits */
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  return (uint16_t)(sign | (u >> 16));
+}
+
+/* Sec. 2.2: one landmark per chunk of adjacent entries, here their mean key;
+ * Sec. 4.1: computed once, before decoding.  Only rows below n_b count. */
+int ckvref_chunk_landmarks(const ckvref_shape* s, int chunk, const uint16_t* keys,
+                           const int32_t* ctx_lens, uint16_t* landmarks) {
+  if (!shape_ok(s) || chunk < 1) return -1;
+  const int units = s->batch * s->num_kv_heads, d = s->head_dim;
+  const int nmax = s->max_ctx, cmax = (nmax + chunk - 1) / chunk;
+  for (int u = 0; u < units; ++u) {
+    const int n = clamp_len(ctx_lens[u / s->num_kv_heads], nmax);
+    const int nc = (n + chunk - 1) / chunk;
+    const uint16_t* ku = keys + (int64_t)u * nmax * s->key_row_stride;
+    for (int c = 0; c < nc; ++c) {
+      const int j0 = c * chunk, j1 = j0 + chunk < n ? j0 + chunk : n;
+      for (int ch = 0; ch < d; ++ch) {
+        double sum = 0.0;
+        for (int j = j0; j < j1; ++j)
+          sum += ckvref_bf16_to_f64(ku[(int64_t)j * s->key_row_stride + ch]);
+        landmarks[((int64_t)u * cmax + c) * d + ch] = ckvref_f64_to_bf16(sum / (j1 - j0));
+      }
+    }
+  }
+  return 0;
+}
+
+/* Sec. 2.2: a selected chunk brings all of its (valid) entries. */
+int ckvref_expand_chunks(int chunk, int m, const int32_t* chunk_idx, int n, int k,
+                         int32_t* rows) {
+  int r = 0;
+  for (int i = 0; i < m; ++i)
+    for (int t = 0; t < chunk; ++t) {
+      const int row = chunk_idx[i] * chunk + t;
+      if (row < n && r < k) rows[r++] = row;
+    }
+  for (int i = r; i < k; ++i) rows[i] = -1;
+  return r;
+}
+
+int ckvref_select_chunks(const ckvref_shape* s, int chunk, const uint16_t* q_sel,
+                         const uint16_t* landmarks, const int32_t* ctx_lens, int k,
+                         float scale, int32_t* chunk_idx, int32_t* n_chunks,
+                         int32_t* rows, int32_t* n_rows, int nthreads) {
+  if (!shape_ok(s) || chunk < 1 || k < chunk || k % chunk) return -1;
+  const int units = s->batch * s->num_kv_heads, kc = k / chunk;
+  const int cmax = (s->max_ctx + chunk - 1) / chunk;
+  /* the landmarks as a batch of rows: one per chunk, ceil(n_b/chunk) valid */
+  ckvref_shape sc = *s;
+  sc.max_ctx = cmax;
+  sc.key_row_stride = s->head_dim;
+  sc.kv_row_stride = s->head_dim;
+  int32_t* clens = (int32_t*)malloc(sizeof(int32_t) * (size_t)(s->batch > 0 ? s->batch : 1));
+  for (int b = 0; b < s->batch; ++b)
+    clens[b] = (clamp_len(ctx_lens[b], s->max_ctx) + chunk - 1) / chunk;
+  double* S = (double*)malloc(sizeof(double) * (size_t)units * (size_t)(cmax > 0 ? cmax : 1));
+  ckvref_score_keys(&sc, q_sel, landmarks, clens, scale, S, nthreads);
+  ckvref_select_topk(&sc, S, clens, kc, chunk_idx, n_chunks, nthreads);
+  for (int u = 0; u < units; ++u) {
+    const int n = clamp_len(ctx_lens[u / s->num_kv_heads], s->max_ctx);
+    n_rows[u] = ckvref_expand_chunks(chunk, n_chunks[u], chunk_idx + (int64_t)u * kc, n, k,
+                                     rows + (int64_t)u * k);
+  }
+  free(S);
+  free(clens);
+  return 0;
+}

@@ -107,6 +107,39 @@ int ckvref_critical_kv_attn(const ckvref_shape* s, const uint16_t* q_att,
                             int32_t* idx, int32_t* n_sel, double* out,
                             int nthreads);
 
+/* ---- chunk landmarks ---------------------------------------------------
+ * Sec. 2.2 (adjacent KV entries segmented into chunks, one compressed
+ * landmark per chunk, chunks selected by the query) and Sec. 4.1 (the
+ * landmarks are fixed before decoding).  The landmark of a chunk is the mean
+ * of its keys, rounded once to bf16. */
+
+/* Nearest bf16 to x, ties to the even significand; the bit pattern. */
+uint16_t ckvref_f64_to_bf16(double x);
+
+/* For every (b, h) and chunk c < ceil(n_b / chunk): landmark row c =
+ * bf16(mean of key rows [c*chunk, min(c*chunk + chunk, n_b))), the mean
+ * summed in fp64 in row order and divided by the row count.  Chunks at or
+ * past ceil(n_b / chunk) are not written.  keys use s->key_row_stride;
+ * landmarks are dense [B][Hkv][ceil(max_ctx / chunk)][d]. */
+int ckvref_chunk_landmarks(const ckvref_shape* s, int chunk, const uint16_t* keys,
+                           const int32_t* ctx_lens, uint16_t* landmarks);
+
+/* The rows of m selected chunks (ascending chunk indices): rows[i] =
+ * chunk_idx[i / chunk] * chunk + i % chunk for the rows below n, in that
+ * order; -1 after, up to k.  Returns the row count. */
+int ckvref_expand_chunks(int chunk, int m, const int32_t* chunk_idx, int n, int k,
+                         int32_t* rows);
+
+/* Chunk selection: every landmark scored against q_sel (ckvref_score_keys on
+ * the landmarks, ceil(n_b / chunk) chunks per unit), the k / chunk best
+ * chunks selected (ckvref_select_topk) and expanded to rows.  chunk_idx
+ * [B][Hkv][k/chunk], n_chunks [B][Hkv], rows [B][Hkv][k], n_rows [B][Hkv].
+ * k must be a multiple of chunk. */
+int ckvref_select_chunks(const ckvref_shape* s, int chunk, const uint16_t* q_sel,
+                         const uint16_t* landmarks, const int32_t* ctx_lens, int k,
+                         float scale, int32_t* chunk_idx, int32_t* n_chunks,
+                         int32_t* rows, int32_t* n_rows, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

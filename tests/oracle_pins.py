@@ -355,4 +355,126 @@ def pin_empty_context(orc):
     assert n_sel[1, 0] == 5 and list(idx[1, 0]) == [0, 1, 2, 3, 4, -1, -1, -1]
 
 
+# --- chunk landmarks ------------------------------------------------------------
+def pin_bf16_rounding(orc):
+    """fp64 -> bf16: torch's fp32 -> bf16 conversion (round to nearest even) on
+    fp32-representable values, closed-form midpoints, a value that rounding via
+    fp32 would get wrong, and every finite bf16 pattern mapping to itself."""
+    rng = np.random.default_rng(21)
+    xs = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-30, 30, 4000),
+                         [0.0, -0.0, 1.0, -1.0, 3.0e38, 1e-40, -7e-39]]).astype(np.float32)
+    want = torch.from_numpy(xs).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    for x, w in zip(xs, want):
+        assert orc.f64_to_bf16(float(x)) == int(w), (float(x), hex(int(w)))
+    # 1 + 2^-8 lies halfway between 1 (even) and 1 + 2^-7: even wins; just above
+    # it rounds up, which an intermediate fp32 rounding (to 1 + 2^-8) would lose
+    assert orc.f64_to_bf16(1.0 + 2.0 ** -8) == 0x3F80
+    assert orc.f64_to_bf16(1.0 + 2.0 ** -8 + 2.0 ** -40) == 0x3F81
+    assert orc.f64_to_bf16(1.0 + 3 * 2.0 ** -8) == 0x3F82  # between 0x3F81 and 0x3F82
+    assert orc.f64_to_bf16(-(1.0 + 3 * 2.0 ** -8)) == 0xBF82
+    for b in range(0x10000):
+        if (b & 0x7F80) == 0x7F80:  # inf / nan
+            continue
+        assert orc.f64_to_bf16(orc.bf16_to_f64(b)) == (b if b != 0x8000 else 0x8000), hex(b)
+
+
+def pin_landmarks_unit_chunk(orc):
+    """Chunks of one row: the landmarks are the keys, bit for bit (strided
+    rows, ragged contexts; rows past n_b are not written)."""
+    rng = np.random.default_rng(22)
+    B, Hkv, n, d, stride = 2, 3, 13, 128, 136
+    keys = rand_bf(rng, (B, Hkv, n, stride))
+    lens = np.array([13, 9], np.int32)
+    s = orc.shape(B, 2 * Hkv, Hkv, d, n, key_row_stride=stride)
+    lm = orc.chunk_landmarks(s, 1, keys, lens, fill=0x7777)
+    for b in range(B):
+        nb = lens[b]
+        assert np.array_equal(lm[b, :, :nb], keys[b, :, :nb, :d])
+        assert np.all(lm[b, :, nb:] == 0x7777)
+
+
+def pin_landmarks_closed_form(orc):
+    """Means that bf16 holds exactly, and a partial last chunk that averages
+    only the rows below n_b (the rows past it are huge, so counting them
+    shows)."""
+    d, C = 128, 4
+    rows = np.zeros((1, 1, 12, d), np.float32)
+    rows[0, 0, 0:4] = np.array([1.0, 2.0, 3.0, 4.0])[:, None]      # mean 2.5
+    rows[0, 0, 4:8] = np.array([0.5, 0.25, -0.5, -0.25])[:, None]  # mean 0
+    rows[0, 0, 4:8, 7] = [0.5, 0.25, 0.5, 0.25]                    # channel 7: 0.375
+    rows[0, 0, 8:10] = np.array([-6.0, 2.0])[:, None]              # partial: -2
+    rows[0, 0, 10:12] = 1e30
+    keys = f2bf(rows)
+    s = orc.shape(1, 1, 1, d, 12)
+    lm = bf2f(orc.chunk_landmarks(s, C, keys, np.array([10], np.int32)))
+    assert np.all(lm[0, 0, 0] == 2.5)
+    assert lm[0, 0, 1, 7] == 0.375 and np.all(np.delete(lm[0, 0, 1], 7) == 0.0)
+    assert np.all(lm[0, 0, 2] == -2.0)
+
+
+def pin_landmarks_rounding(orc):
+    """Means on a bf16 midpoint round to the even neighbour."""
+    d = 128
+    a, b, c = 1.0, 1.0 + 2.0 ** -7, 1.0 + 2.0 ** -6
+    keys = f2bf(np.array([a, b, b, c], np.float32)[None, None, :, None] *
+                np.ones((1, 1, 4, d), np.float32))
+    lm = orc.chunk_landmarks(orc.shape(1, 1, 1, d, 4), 2, keys, np.array([4], np.int32))
+    assert np.all(lm[0, 0, 0] == 0x3F80)  # (1 + (1+2^-7)) / 2: tie, even is 1.0
+    assert np.all(lm[0, 0, 1] == 0x3F82)  # ((1+2^-7) + (1+2^-6)) / 2: tie, even up
+
+
+def pin_expand_chunks(orc):
+    rows, r = orc.expand_chunks(4, [0, 2], 10, 16)
+    assert r == 6 and list(rows) == [0, 1, 2, 3, 8, 9] + [-1] * 10
+    rows, r = orc.expand_chunks(3, [1, 2, 4], 100, 9)
+    assert r == 9 and list(rows) == [3, 4, 5, 6, 7, 8, 12, 13, 14]
+    rows, r = orc.expand_chunks(5, [], 7, 5)
+    assert r == 0 and list(rows) == [-1] * 5
+
+
+def pin_select_chunks_unit_chunk(orc):
+    """Chunk size 1 is the per-position selection."""
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, n, d, k = 2, 8, 2, 300, 128, 32
+    keys = rand_bf(rng, (B, Hkv, n, d))
+    q = rand_bf(rng, (B, Hq, d))
+    lens = np.array([300, 77], np.int32)
+    s = orc.shape(B, Hq, Hkv, d, n)
+    lm = orc.chunk_landmarks(s, 1, keys, lens)
+    cidx, nch, rows, nrows = orc.select_chunks(s, 1, q, lm, lens, k, SCALE)
+    idx, nsel = orc.select_topk(s, orc.score_keys(s, q, keys, lens, SCALE), lens, k)
+    assert np.array_equal(cidx, idx) and np.array_equal(rows, idx)
+    assert np.array_equal(nch, nsel) and np.array_equal(nrows, nsel)
+
+
+def pin_select_chunks_bruteforce(orc):
+    """Tiny contexts: the chosen chunks are the unique subset of size kc whose
+    scores (numpy dot products with the landmarks, max over the group) all beat
+    the others, ties to the lower chunk; rows are those chunks' rows below n."""
+    rng = np.random.default_rng(24)
+    d, G, C, k = 128, 2, 3, 6
+    for trial in range(30):
+        n = int(rng.integers(4, 13))
+        keys = rand_bf(rng, (1, 1, 12, d))
+        if trial % 3 == 0:  # exact ties between chunks
+            keys[0, 0, 3:6] = keys[0, 0, 0:3]
+        q = rand_bf(rng, (1, G, d))
+        s = orc.shape(1, G, 1, d, 12)
+        lm = orc.chunk_landmarks(s, C, keys, np.array([n], np.int32))
+        nc = (n + C - 1) // C
+        L = bf2f(lm[0, 0, :nc]).astype(np.float64)
+        S = (bf2f(q[0]).astype(np.float64) @ L.T).max(axis=0) * SCALE
+        kc = min(k // C, nc)
+        best = None
+        for sub in itertools.combinations(range(nc), kc):
+            if _dominates(S, sub, nc):
+                best = sub
+                break
+        cidx, nch, rows, nrows = orc.select_chunks(s, C, q, lm, np.array([n], np.int32), k,
+                                                   SCALE)
+        assert nch[0, 0] == kc and tuple(cidx[0, 0, :kc]) == best, (trial, best, cidx)
+        want = [c * C + t for c in best for t in range(C) if c * C + t < n]
+        assert nrows[0, 0] == len(want) and list(rows[0, 0, :len(want)]) == want
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -45,6 +45,18 @@ MUTANTS = {
     "bf16_shift": ("uint32_t u = (uint32_t)bits << 16;", "uint32_t u = (uint32_t)bits << 15;"),
     "select_with_att_query": ("ckvref_unit_scores(G, d, n, jb->q2 + qoff,",
                               "ckvref_unit_scores(G, d, n, jb->q + qoff,"),
+    "landmark_sum_not_mean": ("ckvref_f64_to_bf16(sum / (j1 - j0));",
+                              "ckvref_f64_to_bf16(sum);"),
+    "landmark_drop_partial_chunk": ("const int nc = (n + chunk - 1) / chunk;",
+                                    "const int nc = n / chunk;"),
+    "bf16_ties_away": ("ldexp(nearbyint(ldexp(a, -q)), q);", "ldexp(round(ldexp(a, -q)), q);"),
+    "bf16_truncate": ("ldexp(nearbyint(ldexp(a, -q)), q);", "ldexp(trunc(ldexp(a, -q)), q);"),
+    "expand_no_chunk_scale": ("const int row = chunk_idx[i] * chunk + t;",
+                              "const int row = chunk_idx[i] + t;"),
+    "expand_past_context": ("if (row < n && r < k) rows[r++] = row;",
+                            "if (r < k) rows[r++] = row;"),
+    "chunk_lens_floor": ("clens[b] = (clamp_len(ctx_lens[b], s->max_ctx) + chunk - 1) / chunk;",
+                         "clens[b] = clamp_len(ctx_lens[b], s->max_ctx) / chunk;"),
     "scores_skip_last_channel": ("for (int c = 0; c < d; ++c)\n        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);",
                                  "for (int c = 0; c < d - 1; ++c)\n        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);"),
 }
