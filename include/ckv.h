@@ -214,6 +214,51 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att,
                        int32_t* idx_next, int32_t* n_next, float* out,
                        void* ws, size_t ws_bytes, void* stream);
 
+/* ---- chunk landmarks --------------------------------------------------------
+ * Sec. 2.2: adjacent KV entries are segmented into chunks, each with a small
+ * GPU-resident landmark; the query selects chunks by their landmarks and the
+ * selected chunks' entries are retrieved.  Sec. 4.1: the landmarks are built
+ * before decoding and stay fixed.  A chunk holds `chunk` consecutive rows
+ * (chunk >= 1; chunk 1 is the per-position path above); a unit with n_b rows
+ * has ceil(n_b / chunk) chunks, the last possibly partial.
+ *   landmarks   [B][Hkv][ceil(max_ctx / chunk)][d] bf16, device
+ *   chunk_idx   [B][Hkv][k / chunk] int32: ascending chunk numbers, -1 padded
+ *   n_chunks    [B][Hkv] int32
+ *   rows        [B][Hkv][k] int32: the selected chunks' rows below n_b in
+ *               ascending order, -1 padded (the idx of the other entries)
+ *   n_rows      [B][Hkv] int32 */
+
+/* Landmark c of every (b, h), for c < ceil(n_b / chunk): the mean of key rows
+ * [c*chunk, min(c*chunk + chunk, n_b)) of `keys` (key_row_stride), summed in
+ * fp64 in row order, divided by the row count and rounded once to bf16
+ * (nearest, ties to even).  Later landmarks are not written. */
+int ckv_chunk_landmarks(const ckv_shape* shape, int32_t chunk, const uint16_t* keys,
+                        const int32_t* ctx_lens, uint16_t* landmarks, void* stream);
+
+/* Chunk selection: every landmark is scored against q_sel exactly as
+ * ckv_score_keys scores a key (max over the group's heads), the k / chunk
+ * best chunks are selected as ckv_select_topk selects positions (ties to the
+ * lower chunk; all chunks if there are fewer), and expanded to rows.  k must
+ * be a multiple of chunk.  Workspace: CKV_ENTRY_CRITICAL_KV_ATTN for this
+ * shape and k. */
+int ckv_select_chunks(const ckv_shape* shape, int32_t chunk, const uint16_t* q_sel,
+                      const uint16_t* landmarks, const int32_t* ctx_lens, int32_t k,
+                      float scale, int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
+                      int32_t* n_rows, void* ws, size_t ws_bytes, void* stream);
+
+/* Same-step decode of one layer over chunks: ckv_select_chunks with q_sel
+ * (NULL means q_att), then out = attention of q_att over the rows `rows` of
+ * k_src/v_src read in place (src_kind says where), i.e.
+ * ckv_sparse_decode_attn over ckv_gather_kv(rows, n_rows).  Workspace:
+ * CKV_ENTRY_CRITICAL_KV_ATTN for this shape and k. */
+int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q_att,
+                        const uint16_t* q_sel, const uint16_t* landmarks,
+                        const int32_t* ctx_lens, int32_t k, float scale,
+                        const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                        int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
+                        int32_t* n_rows, float* out, void* ws, size_t ws_bytes,
+                        void* stream);
+
 /* ---- layer pipeline --------------------------------------------------------
  * The decode loop of Sec. 5.3 (layer-aware transfer overlap) and Sec. 5.4
  * (two-layer ping-pong buffer): the set selected for a layer at step t-1 is
@@ -292,7 +337,9 @@ typedef enum ckv_kernel_id {
   CKV_K_DUAL = 7,     /* one launch: attention (buffer) + scoring           */
   CKV_K_GATHER = 8,   /* sparse K/V assembly                                */
   CKV_K_MISS = 9,     /* predicted vs selected set: hits, misses, slots     */
-  CKV_K_COUNT = 10
+  CKV_K_LANDMARKS = 10, /* chunk landmarks (mean keys)                      */
+  CKV_K_EXPAND = 11,  /* selected chunks -> their rows                      */
+  CKV_K_COUNT = 12
 } ckv_kernel_id;
 
 #define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)

@@ -21,7 +21,8 @@ import torch
 __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
-    "critical_kv_attn", "corrected_attn", "profile_begin", "profile_end", "abi_version",
+    "critical_kv_attn", "corrected_attn", "chunk_landmarks", "select_chunks",
+    "chunked_kv_attn", "profile_begin", "profile_end", "abi_version",
     "Layer", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "EXPORTS",
@@ -35,11 +36,12 @@ ENTRY_CORRECTED_ATTN = 4
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
-           "ckv_corrected_attn",
+           "ckv_corrected_attn", "ckv_chunk_landmarks", "ckv_select_chunks",
+           "ckv_chunked_kv_attn",
            "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_prime",
            "ckv_decode_step")
-KERNEL_COUNT = 10
+KERNEL_COUNT = 12
 
 
 class CkvError(RuntimeError):
@@ -93,6 +95,12 @@ def _load() -> ctypes.CDLL:
         "ckv_corrected_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                               vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp,
                                               vp, vp, vp, vp, vp, sz, vp]),
+        "ckv_chunk_landmarks": (ctypes.c_int, [sp, i32, vp, vp, vp, vp]),
+        "ckv_select_chunks": (ctypes.c_int, [sp, i32, vp, vp, vp, i32, ctypes.c_float, vp, vp,
+                                             vp, vp, vp, sz, vp]),
+        "ckv_chunked_kv_attn": (ctypes.c_int, [sp, i32, vp, vp, vp, vp, i32, ctypes.c_float,
+                                               vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp,
+                                               sz, vp]),
         "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
@@ -216,8 +224,34 @@ def corrected_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int, scale:
         _stream(stream)))
 
 
+def chunk_landmarks(shape: Shape, chunk: int, keys, ctx_lens, landmarks,
+                    stream=None) -> None:
+    _check("ckv_chunk_landmarks", _lib.ckv_chunk_landmarks(
+        ctypes.byref(shape), chunk, _ptr(keys), _ptr(ctx_lens), _ptr(landmarks),
+        _stream(stream)))
+
+
+def select_chunks(shape: Shape, chunk: int, q_sel, landmarks, ctx_lens, k: int,
+                  scale: float, chunk_idx, n_chunks, rows, n_rows, ws, stream=None) -> None:
+    _check("ckv_select_chunks", _lib.ckv_select_chunks(
+        ctypes.byref(shape), chunk, _ptr(q_sel), _ptr(landmarks), _ptr(ctx_lens), k, scale,
+        _ptr(chunk_idx), _ptr(n_chunks), _ptr(rows), _ptr(n_rows), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def chunked_kv_attn(shape: Shape, chunk: int, q_att, q_sel, landmarks, ctx_lens, k: int,
+                    scale: float, k_src, v_src, src_kind: int, chunk_idx, n_chunks, rows,
+                    n_rows, out, ws, stream=None) -> None:
+    _check("ckv_chunked_kv_attn", _lib.ckv_chunked_kv_attn(
+        ctypes.byref(shape), chunk, _ptr(q_att), _ptr(q_sel), _ptr(landmarks),
+        _ptr(ctx_lens), k, scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(chunk_idx),
+        _ptr(n_chunks), _ptr(rows), _ptr(n_rows), _ptr(out), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))
+
+
 KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
-              "combine": 6, "dual": 7, "gather": 8, "miss": 9}
+              "combine": 6, "dual": 7, "gather": 8, "miss": 9, "landmarks": 10,
+              "expand": 11}
 
 
 def profile_begin(kernels=None) -> None:

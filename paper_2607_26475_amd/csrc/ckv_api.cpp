@@ -241,6 +241,7 @@ SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* sc
   a.max_ctx = d.max_ctx;
   a.k = k;
   a.tiles = L.filter_tiles;
+  a.chunk = 1;
   return a;
 }
 
@@ -260,6 +261,7 @@ ScoreArgs score_args(const Dims& d, const Layout& L, const uint16_t* q,
   a.Hkv = d.Hkv;
   a.max_ctx = d.max_ctx;
   a.units = d.U;
+  a.chunk = 1;
   return a;
 }
 
@@ -295,6 +297,50 @@ int run_select_tail(const SelectArgs& a, int units, hipStream_t s) {
   }
   CKV_TRY_HIP(launch_filter(a, units, s), "filter launch");
   CKV_TRY_HIP(launch_finish(a, units, s), "finish launch");
+  return CKV_OK;
+}
+
+int check_chunk(int32_t chunk, int32_t k) {
+  if (chunk < 1 || chunk > (1 << 20)) return fail(CKV_ESHAPE, "chunk %d outside [1, 2^20]", chunk);
+  if (k % chunk) return fail(CKV_ESHAPE, "k %d is not a multiple of chunk %d", k, chunk);
+  return CKV_OK;
+}
+
+// Chunk selection into caller arrays; `Lc` is the layout of the chunk problem
+// (one entry per chunk, budget k / chunk), which fits inside the layout of
+// the row problem that the caller's workspace was sized for.
+int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
+                      const uint16_t* landmarks, const int32_t* ctx_lens, int32_t k,
+                      float scale, int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
+                      int32_t* n_rows, void* ws, hipStream_t s) {
+  Dims dc = d;
+  dc.max_ctx = (d.max_ctx + chunk - 1) / chunk;
+  dc.key_stride = kD;
+  const int32_t kc = k / chunk;
+  Layout Lc = make_layout(dc, kc, CKV_ENTRY_CRITICAL_KV_ATTN);
+  int rc;
+  if ((rc = check_grid(dc, Lc))) return rc;
+  float* scores = at<float>(ws, Lc.scores);
+  SelectArgs sa = select_args(dc, Lc, ws, scores, ctx_lens, kc, chunk_idx, n_chunks);
+  sa.chunk = chunk;
+  ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, sa.hist,
+                            sa.coarse);
+  sc.chunk = chunk;
+  CKV_TRY_HIP(launch_zero(ws, Lc.zero_end, s), "zero launch");
+  CKV_TRY_HIP(launch_score(sc, d.G, true, d.U, s), "score launch");
+  if ((rc = run_select_tail(sa, d.U, s))) return rc;
+  ExpandArgs e;
+  e.chunk_idx = chunk_idx;
+  e.n_chunks = n_chunks;
+  e.ctx_lens = ctx_lens;
+  e.rows = rows;
+  e.n_rows = n_rows;
+  e.Hkv = d.Hkv;
+  e.max_ctx = d.max_ctx;
+  e.chunk = chunk;
+  e.kc = kc;
+  e.k = k;
+  CKV_TRY_HIP(launch_expand(e, d.U, s), "expand launch");
   return CKV_OK;
 }
 
@@ -480,6 +526,96 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
     CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
     CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   }
+  return CKV_OK;
+}
+
+int ckv_chunk_landmarks(const ckv_shape* shape, int32_t chunk, const uint16_t* keys,
+                        const int32_t* ctx_lens, uint16_t* landmarks, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_chunk(chunk, chunk))) return rc;
+  CKV_PTR(keys);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(landmarks);
+  if (d.U == 0) return CKV_OK;
+  LandmarkArgs a;
+  a.keys = keys;
+  a.ctx_lens = ctx_lens;
+  a.landmarks = landmarks;
+  a.key_stride = d.key_stride;
+  a.Hkv = d.Hkv;
+  a.max_ctx = d.max_ctx;
+  a.chunk = chunk;
+  a.cmax = (d.max_ctx + chunk - 1) / chunk;
+  a.items = (int64_t)d.U * a.cmax * 16;
+  CKV_TRY_HIP(launch_landmarks(a, (hipStream_t)stream), "landmarks launch");
+  return CKV_OK;
+}
+
+int ckv_select_chunks(const ckv_shape* shape, int32_t chunk, const uint16_t* q_sel,
+                      const uint16_t* landmarks, const int32_t* ctx_lens, int32_t k,
+                      float scale, int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
+                      int32_t* n_rows, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_chunk(chunk, k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  CKV_PTR(q_sel);
+  CKV_PTR(landmarks);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(chunk_idx);
+  CKV_PTR(n_chunks);
+  CKV_PTR(rows);
+  CKV_PTR(n_rows);
+  Layout L = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN);
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  return run_select_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx,
+                           n_chunks, rows, n_rows, ws, (hipStream_t)stream);
+}
+
+int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q_att,
+                        const uint16_t* q_sel, const uint16_t* landmarks,
+                        const int32_t* ctx_lens, int32_t k, float scale,
+                        const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                        int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
+                        int32_t* n_rows, float* out, void* ws, size_t ws_bytes,
+                        void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_chunk(chunk, k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  CKV_PTR(q_att);
+  if (!q_sel) q_sel = q_att;
+  CKV_PTR(q_sel);
+  CKV_PTR(landmarks);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(k_src);
+  CKV_PTR(v_src);
+  CKV_PTR(chunk_idx);
+  CKV_PTR(n_chunks);
+  CKV_PTR(rows);
+  CKV_PTR(n_rows);
+  CKV_PTR(out);
+  if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
+  Layout L = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  if ((rc = run_select_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx,
+                              n_chunks, rows, n_rows, ws, s)))
+    return rc;
+  // the partials live past everything the chunk selection used
+  AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, rows, n_rows, d.kv_stride, k, scale,
+                           out);
+  CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
+  CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   return CKV_OK;
 }
 

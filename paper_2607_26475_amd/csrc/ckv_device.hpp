@@ -61,6 +61,7 @@ struct ScoreArgs {
   int64_t key_stride;
   float scale;
   int Hq, Hkv, max_ctx, units;
+  int chunk;                // rows per scored entry: n_b rows give ceil(n_b/chunk) entries
 };
 
 struct SelectArgs {
@@ -77,6 +78,7 @@ struct SelectArgs {
   int32_t* n_sel;           // [U]
   int64_t bm_words;
   int Hkv, max_ctx, k, tiles;
+  int chunk;                // as in ScoreArgs
 };
 
 struct AttnArgs {
@@ -105,6 +107,26 @@ struct GatherArgs {
   int max_ctx, k;
 };
 
+// Chunk landmarks: the mean key of every chunk of `chunk` rows.
+struct LandmarkArgs {
+  const uint16_t* keys;     // unit rows at stride key_stride
+  const int32_t* ctx_lens;  // [B]
+  uint16_t* landmarks;      // [U][cmax][d]
+  int64_t key_stride;
+  int64_t items;            // U * cmax * 16 (16 bytes of a landmark each)
+  int Hkv, max_ctx, chunk, cmax;
+};
+
+// Rows of the selected chunks.
+struct ExpandArgs {
+  const int32_t* chunk_idx; // [U][kc] ascending
+  const int32_t* n_chunks;  // [U]
+  const int32_t* ctx_lens;  // [B]
+  int32_t* rows;            // [U][k] written
+  int32_t* n_rows;          // [U] written
+  int Hkv, max_ctx, chunk, kc, k;
+};
+
 // Miss detection: the selected set against the predicted set in the buffer.
 constexpr int kMissThreads = 1024;
 constexpr int kMissLds = 8192;  // budgets up to this keep both sets in LDS
@@ -124,6 +146,13 @@ struct MissArgs {
 };
 
 // ---- small device helpers ---------------------------------------------------
+
+// Entries of a unit with n_b context rows when one entry covers `chunk` rows:
+// ceil(n_b / chunk), clamped to [0, hi].
+__device__ __forceinline__ int unit_len(int n_rows, int hi, int chunk) {
+  const int n = max(n_rows, 0);
+  return min(n / chunk + (n % chunk != 0 ? 1 : 0), hi);
+}
 
 __device__ __forceinline__ int clamp_len(int n, int hi) {
   return n < 0 ? 0 : (n > hi ? hi : n);

@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_hist(SelectArgs a) {
   const int unit = blockIdx.x / a.tiles;
   const int tile = blockIdx.x - unit * a.tiles;
   const int b = unit / a.Hkv;
-  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
   const int j0 = tile * kFilterTile;
   if (j0 >= n) return;
   const int jend = min(j0 + kFilterTile, n);
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
   const int unit = blockIdx.x / a.tiles;
   const int tile = blockIdx.x - unit * a.tiles;
   const int b = unit / a.Hkv;
-  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   const int j0 = tile * kFilterTile;
   if (m == 0 || m >= n || j0 >= n) return;  // uniform
@@ -198,7 +198,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
   __shared__ uint32_t misc[8];
   const int unit = blockIdx.x;
   const int b = unit / a.Hkv;
-  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   const int tid = threadIdx.x;
   int32_t* idx = a.idx + (int64_t)unit * a.k;
@@ -340,7 +340,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __shared__ uint32_t misc[8];
   const int unit = blockIdx.x;
   const int b = unit / a.Hkv;
-  const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+  const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   const int tid = threadIdx.x;
   int32_t* idx = a.idx + (int64_t)unit * a.k;
@@ -468,6 +468,80 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
     }
     a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = L > 0.f ? O / L : 0.f;
   }
+}
+
+// ---- chunk landmarks -----------------------------------------------------------
+// Nearest bf16 to x, ties to the even significand, from the binary64 fields:
+// normal results keep 7 of the 52 stored significand bits; below the
+// smallest normal bf16 (2^-126) the quantum is 2^-133.
+__device__ __forceinline__ uint16_t f64_to_bf16_rne(double x) {
+  uint64_t b = (uint64_t)__double_as_longlong(x);
+  const uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
+  b &= 0x7fffffffffffffffull;
+  if (b == 0) return sign;
+  if ((int)(b >> 52) < 1023 - 126) {
+    const double r = rint(__longlong_as_double((long long)b) * 0x1p133);
+    return (uint16_t)(sign | (uint16_t)r);  // r = 128 is the smallest normal
+  }
+  b += 0x00000fffffffffffull + ((b >> 45) & 1u);  // 2^44 - 1 + kept lsb
+  const uint32_t e = (uint32_t)(b >> 52) - 1023u + 127u;
+  return (uint16_t)(sign | (e << 7) | (uint32_t)((b >> 45) & 0x7fu));
+}
+
+// One item = 8 channels of one landmark: the fp64 sum of the chunk's rows
+// below n_b in row order, divided by their count, rounded once to bf16.
+__global__ __launch_bounds__(kGatherThreads) void k_landmarks(LandmarkArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * kGatherThreads;
+  for (int64_t it = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x; it < a.items;
+       it += stride) {
+    const int part = (int)(it & 15);
+    const int64_t uc = it >> 4;
+    const int64_t unit = uc / a.cmax;
+    const int c = (int)(uc - unit * a.cmax);
+    const int n = clamp_len(a.ctx_lens[unit / a.Hkv], a.max_ctx);
+    const int j0 = c * a.chunk;
+    if (j0 >= n) continue;
+    const int j1 = min(j0 + a.chunk, n);
+    const uint16_t* src = a.keys + (unit * a.max_ctx + j0) * a.key_stride + 8 * part;
+    double sum[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int j = j0; j < j1; ++j, src += a.key_stride) {
+      float f[8];
+      unpack8(ld16(src), f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum[e] += (double)f[e];
+    }
+    const double cnt = (double)(j1 - j0);
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = (uint32_t)f64_to_bf16_rne(sum[2 * e] / cnt) |
+             ((uint32_t)f64_to_bf16_rne(sum[2 * e + 1] / cnt) << 16);
+    *reinterpret_cast<uint4*>(a.landmarks + uc * kD + 8 * part) =
+        make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Row i of a unit's expanded set is row t = i % chunk of its (i / chunk)-th
+// selected chunk; chunks are ascending, so only the last one can run past n_b
+// and the valid rows form a prefix.
+__global__ __launch_bounds__(kGatherThreads) void k_expand(ExpandArgs a) {
+  const int unit = blockIdx.y;
+  const int i = blockIdx.x * kGatherThreads + threadIdx.x;
+  const int n = clamp_len(a.ctx_lens[unit / a.Hkv], a.max_ctx);
+  const int m = clamp_len(a.n_chunks[unit], a.kc);
+  const int32_t* ci = a.chunk_idx + (int64_t)unit * a.kc;
+  if (i < a.k) {
+    const int c = i / a.chunk;
+    int row = -1;
+    if (c < m) {
+      row = ci[c] * a.chunk + (i - c * a.chunk);
+      if (row >= n) row = -1;
+    }
+    a.rows[(int64_t)unit * a.k + i] = row;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    a.n_rows[unit] =
+        m == 0 ? 0 : (m - 1) * a.chunk + max(0, min(a.chunk, n - ci[m - 1] * a.chunk));
 }
 
 // ---- miss detection -----------------------------------------------------------
@@ -738,6 +812,18 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
   const int attn_blocks = units * at.chunks;
   return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, s)
                  : launch_dual_i<false>(at, sc, G, attn_blocks, s);
+}
+
+hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s) {
+  const int blocks = blocks_for(a.items, kGatherThreads, 8192);
+  launch_kernel(CKV_K_LANDMARKS, k_landmarks, dim3(blocks), dim3(kGatherThreads), s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_expand(const ExpandArgs& a, int units, hipStream_t s) {
+  const dim3 grid((a.k + kGatherThreads - 1) / kGatherThreads, units);
+  launch_kernel(CKV_K_EXPAND, k_expand, grid, dim3(kGatherThreads), s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s) {

@@ -16,6 +16,8 @@ hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
                        int units, hipStream_t s);
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s);
+hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s);
+hipError_t launch_expand(const ExpandArgs& a, int units, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s);
 
 }  // namespace ckv

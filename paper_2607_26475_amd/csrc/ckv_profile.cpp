@@ -63,7 +63,8 @@ extern "C" {
 
 const char* ckv_kernel_name(int id) {
   static const char* names[CKV_K_COUNT] = {"zero", "score", "hist", "filter", "finish",
-                                           "attn", "combine", "dual", "gather", "miss"};
+                                           "attn", "combine", "dual", "gather", "miss",
+                                           "landmarks", "expand"};
   return (id >= 0 && id < CKV_K_COUNT) ? names[id] : "";
 }
 

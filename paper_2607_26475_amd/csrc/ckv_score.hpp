@@ -84,7 +84,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
     const int64_t ubase = (int64_t)unit * gpu_groups;
     const int64_t seg_end = min(g1, ubase + gpu_groups);
     const int b = unit / a.Hkv, h = unit - b * a.Hkv;
-    const int n = clamp_len(a.ctx_lens[b], a.max_ctx);
+    const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
     float* srow = a.scores + (int64_t)unit * a.max_ctx;
     // groups [ubase + first_empty, ...) hold no position below n_b
     const int64_t valid_end = min(seg_end, ubase + (n + kStageRows - 1) / kStageRows);

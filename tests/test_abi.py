@@ -149,3 +149,23 @@ def test_corrected_attn_argument_checks():
     assert call(k=0) == STATUS["ESHAPE"]
     assert call(ws_bytes=need - 1) == STATUS["EWORKSPACE"]
     assert call(ws=None) == STATUS["EWORKSPACE"]
+
+
+def test_chunk_entries_argument_checks():
+    lib = ckv._lib
+    s = good_shape()
+    need = ckv.workspace_bytes(s, 16, ckv.ENTRY_CRITICAL_KV_ATTN)
+    assert lib.ckv_chunk_landmarks(ctypes.byref(s), 0, FAKE, FAKE, FAKE, None) == STATUS["ESHAPE"]
+    assert lib.ckv_chunk_landmarks(ctypes.byref(s), 4, None, FAKE, FAKE, None) == STATUS["EINVAL"]
+
+    def sel(chunk=4, k=16, ws=FAKE, ws_bytes=need, rows=FAKE):
+        return lib.ckv_select_chunks(ctypes.byref(s), chunk, FAKE, FAKE, FAKE, k, 0.1, FAKE,
+                                     FAKE, rows, FAKE, ws, ws_bytes, None)
+
+    assert sel(k=18) == STATUS["ESHAPE"]       # k not a multiple of the chunk
+    assert sel(chunk=0) == STATUS["ESHAPE"]
+    assert sel(rows=None) == STATUS["EINVAL"]
+    assert sel(ws_bytes=need - 1) == STATUS["EWORKSPACE"]
+    assert lib.ckv_chunked_kv_attn(ctypes.byref(s), 4, FAKE, None, FAKE, FAKE, 16, 0.1, FAKE,
+                                   FAKE, 3, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need,
+                                   None) == STATUS["EINVAL"]  # bad src kind
