@@ -211,6 +211,10 @@ def main() -> int:
     log(f"dominant kernel {dominant}: {avg_s * 1e6:.1f} us/launch, "
         f"{achieved:.0f} GB/s algorithmic")
 
+    chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
+    log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} ms/step, "
+        f"{chunked['tokens_per_s']:.0f} tokens/s")
+
     host_link = None
     if not args.no_host_link:
         host_link = measure_host_link(torch, ckv, dev)
@@ -253,6 +257,7 @@ def main() -> int:
         "ms_per_step_unstamped": ms_plain,
         "kernels": per_kernel,
         "roofline": roofline,
+        "chunked": chunked,
         "host_link": host_link,
         "pipeline": pipeline,
         "cpu_baseline": cpu,
@@ -310,6 +315,56 @@ def measure_host_link(torch, ckv, dev):
     return {"gather_GBps": gather_gbps, "h2d_copy_GBps": copy_gbps,
             "frac_of_copy": gather_gbps / copy_gbps, "bytes_per_gather": gbytes,
             "workload": "B8, 8 KV heads, n 131072, k 4096, 512-byte K|V rows, pinned host"}
+
+
+def measure_chunked(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream,
+                    chunk=8):
+    """The same Llama-8B step with chunk landmarks (the paper's index source):
+    every layer scores the mean keys of 8-row chunks, selects k/8 chunks and
+    attends over their rows in place.  Landmarks are built once beforehand (at
+    prefill time, not timed): 1/8 of the keys' size."""
+    B, Hq, Hkv, d, n, k = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k
+    dev = torch.device("cuda:0")
+    cmax = (n + chunk - 1) // chunk
+    lms = []
+    for l, t in enumerate(layers):
+        lm = torch.empty((B, Hkv, cmax, d), dtype=torch.bfloat16, device=dev)
+        ckv.chunk_landmarks(shape, chunk, kv_ptrs[l][0], t["ctx_lens"], lm, stream)
+        lms.append(lm)
+    i32 = dict(dtype=torch.int32, device=dev)
+    cidx = torch.empty((B, Hkv, k // chunk), **i32)
+    nch = torch.empty((B, Hkv), **i32)
+    rows = [torch.empty((B, Hkv, k), **i32) for _ in layers]
+    nrows = [torch.empty((B, Hkv), **i32) for _ in layers]
+    out = [torch.empty((B, Hq, d), device=dev) for _ in layers]
+    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+
+    def step():
+        for l, t in enumerate(layers):
+            kp, vp = kv_ptrs[l]
+            ckv.chunked_kv_attn(shape, chunk, t["q"], None, lms[l], t["ctx_lens"], k, scale,
+                                kp, vp, ckv.SRC_DEVICE, cidx, nch, rows[l], nrows[l], out[l],
+                                ws, stream)
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    ckv.profile_begin()
+    step()
+    torch.cuda.synchronize()
+    per = {kname: round(1e3 * tot / c, 1) for kname, (c, tot, _) in ckv.profile_end().items()}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    del lms
+    return {"chunk": chunk, "ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3),
+            "per_layer_us": per, "landmark_bytes_per_layer": B * Hkv * cmax * d * 2,
+            "workload": "the Llama-8B step above, chunk landmarks of 8 rows, k 2048 rows "
+                        "(256 chunks) per KV head"}
 
 
 def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
