@@ -84,7 +84,10 @@ class Oracle:
         lib.ckvref_expand_chunks.argtypes = [i32, i32, vp, i32, i32, vp]
         lib.ckvref_select_chunks.argtypes = [sp, i32, vp, vp, vp, i32, f32, vp, vp, vp, vp,
                                              i32]
-        for f in ("ckvref_score_keys", "ckvref_select_topk", "ckvref_gather_kv",
+        lib.ckvref_dual_token_attn.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, f32, vp,
+                                               vp, i32]
+        for f in ("ckvref_dual_token_attn", "ckvref_score_keys", "ckvref_select_topk",
+                  "ckvref_gather_kv",
                   "ckvref_sparse_decode_attn", "ckvref_critical_kv_attn",
                   "ckvref_chunk_landmarks", "ckvref_expand_chunks", "ckvref_select_chunks"):
             getattr(lib, f).restype = ctypes.c_int
@@ -216,6 +219,20 @@ class Oracle:
                                            nthreads)
         assert rc == 0
         return cidx, nch, rows, nrows
+
+
+    # ---- dual-token attention ------------------------------------------------
+    def dual_token_attn(self, s: _Shape, q_cur, q_spec, k_buf, v_buf, n_sel, k_local,
+                        v_local, k, scale, nthreads=1):
+        q_cur, q_spec, k_buf, v_buf = _u16(q_cur), _u16(q_spec), _u16(k_buf), _u16(v_buf)
+        k_local, v_local, n_sel = _u16(k_local), _u16(v_local), _i32(n_sel)
+        shp = (s.batch, s.num_q_heads, s.head_dim)
+        out_cur, out_spec = np.full(shp, np.nan), np.full(shp, np.nan)
+        rc = self.lib.ckvref_dual_token_attn(ctypes.byref(s), _p(q_cur), _p(q_spec), _p(k_buf),
+                                             _p(v_buf), _p(n_sel), _p(k_local), _p(v_local), k,
+                                             scale, _p(out_cur), _p(out_spec), nthreads)
+        assert rc == 0
+        return out_cur, out_spec
 
 
 _default: Optional[Oracle] = None

@@ -136,8 +136,9 @@ static int clamp_len(int32_t n, int32_t max_ctx) {
 
 typedef struct {
   const ckvref_shape* s;
-  int kind; /* 0 score, 1 select, 2 attn, 3 pipeline */
-  const uint16_t *q, *q2, *keys, *k_src, *v_src, *k_buf, *v_buf;
+  int kind; /* 0 score, 1 select, 2 attn, 3 pipeline, 4 dual-token attn */
+  const uint16_t *q, *q2, *keys, *k_src, *v_src, *k_buf, *v_buf, *k_local, *v_local;
+  double* out2;
   const int32_t* ctx_lens;
   const int32_t* n_sel_in;
   const double* scores_in;
@@ -175,6 +176,23 @@ static void run_unit(const job* jb, int u) {
                      jb->k_buf + (int64_t)u * k * d,
                      jb->v_buf + (int64_t)u * k * d, jb->scale,
                      jb->out + qoff, NULL);
+  } else if (jb->kind == 4) {
+    /* Sec. 5.2: the two tokens as consecutive positions after the selected
+     * rows; the causal mask hides the speculative token from the current
+     * one.  Rows: the m buffer rows, then the local rows each token sees. */
+    int m = jb->n_sel_in[u];
+    if (m < 0) m = 0;
+    if (m > k) m = k;
+    uint16_t* kr = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(m + 2) * d);
+    uint16_t* vr = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(m + 2) * d);
+    memcpy(kr, jb->k_buf + (int64_t)u * k * d, sizeof(uint16_t) * (size_t)m * d);
+    memcpy(vr, jb->v_buf + (int64_t)u * k * d, sizeof(uint16_t) * (size_t)m * d);
+    memcpy(kr + (int64_t)m * d, jb->k_local + (int64_t)u * 2 * d, sizeof(uint16_t) * 2 * d);
+    memcpy(vr + (int64_t)m * d, jb->v_local + (int64_t)u * 2 * d, sizeof(uint16_t) * 2 * d);
+    ckvref_unit_attn(G, d, m + 1, jb->q + qoff, kr, vr, jb->scale, jb->out + qoff, NULL);
+    ckvref_unit_attn(G, d, m + 2, jb->q2 + qoff, kr, vr, jb->scale, jb->out2 + qoff, NULL);
+    free(kr);
+    free(vr);
   } else {
     /* Sec. 4.1 + Sec. 5.3: index from the selecting query, attention of
      * the attending query over the rows of that index. */
@@ -420,5 +438,30 @@ int ckvref_select_chunks(const ckvref_shape* s, int chunk, const uint16_t* q_sel
   }
   free(S);
   free(clens);
+  return 0;
+}
+
+int ckvref_dual_token_attn(const ckvref_shape* s, const uint16_t* q_cur,
+                           const uint16_t* q_spec, const uint16_t* k_buf,
+                           const uint16_t* v_buf, const int32_t* n_sel,
+                           const uint16_t* k_local, const uint16_t* v_local, int k,
+                           float scale, double* out_cur, double* out_spec, int nthreads) {
+  if (!shape_ok(s) || k < 1) return -1;
+  job jb;
+  memset(&jb, 0, sizeof jb);
+  jb.s = s;
+  jb.kind = 4;
+  jb.q = q_cur;
+  jb.q2 = q_spec;
+  jb.k_buf = k_buf;
+  jb.v_buf = v_buf;
+  jb.n_sel_in = n_sel;
+  jb.k_local = k_local;
+  jb.v_local = v_local;
+  jb.k = k;
+  jb.scale = scale;
+  jb.out = out_cur;
+  jb.out2 = out_spec;
+  run_units(&jb, s->batch * s->num_kv_heads, nthreads);
   return 0;
 }

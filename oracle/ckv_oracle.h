@@ -140,6 +140,21 @@ int ckvref_select_chunks(const ckvref_shape* s, int chunk, const uint16_t* q_sel
                          float scale, int32_t* chunk_idx, int32_t* n_chunks,
                          int32_t* rows, int32_t* n_rows, int nthreads);
 
+/* ---- dual-token attention ----------------------------------------------
+ * Sec. 5.2 (dual-token decoding): the current token T_i and the speculative
+ * token T'_{i+1} of a request run as two consecutive positions of one
+ * sequence, causally masked: T_i never sees T'_{i+1}.  Over the sparse set
+ * both tokens attend to the same selected rows; the tokens' own new rows
+ * (k_local/v_local [B][Hkv][2][d]: row 0 = T_i, row 1 = T'_{i+1}) follow
+ * them.  Per unit with m = n_sel (clamped to [0, k]):
+ *   out_cur[b][g]  = attention of q_cur[b][g]  over buffer rows [0, m) + local row 0
+ *   out_spec[b][g] = attention of q_spec[b][g] over buffer rows [0, m) + local rows 0, 1 */
+int ckvref_dual_token_attn(const ckvref_shape* s, const uint16_t* q_cur,
+                           const uint16_t* q_spec, const uint16_t* k_buf,
+                           const uint16_t* v_buf, const int32_t* n_sel,
+                           const uint16_t* k_local, const uint16_t* v_local, int k,
+                           float scale, double* out_cur, double* out_spec, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -477,4 +477,78 @@ def pin_select_chunks_bruteforce(orc):
         assert nrows[0, 0] == len(want) and list(rows[0, 0, :len(want)]) == want
 
 
+# --- dual-token attention ---------------------------------------------------------
+def _dual_case(rng, B=2, Hq=8, Hkv=2, k=24, m=(17, 0), d=128):
+    s_shape = dict(B=B, Hq=Hq, Hkv=Hkv, d=d, k=k)
+    kb = rand_bf(rng, (B, Hkv, k, d))
+    vb = rand_bf(rng, (B, Hkv, k, d))
+    kl = rand_bf(rng, (B, Hkv, 2, d))
+    vl = rand_bf(rng, (B, Hkv, 2, d))
+    qc = rand_bf(rng, (B, Hq, d))
+    qs = rand_bf(rng, (B, Hq, d))
+    n_sel = np.array([[m[b % len(m)]] * Hkv for b in range(B)], np.int32)
+    return s_shape, qc, qs, kb, vb, n_sel, kl, vl
+
+
+def pin_dual_token_causal_sdpa(orc):
+    """Both tokens against torch's scaled_dot_product_attention in fp64 on the
+    dense sequence [selected rows, T_i, T'_{i+1}] with the causal mask on the
+    two new positions."""
+    rng = np.random.default_rng(31)
+    sh, qc, qs, kb, vb, n_sel, kl, vl = _dual_case(rng)
+    B, Hq, Hkv, d, k = sh["B"], sh["Hq"], sh["Hkv"], sh["d"], sh["k"]
+    s = orc.shape(B, Hq, Hkv, d, 64)
+    oc, os_ = orc.dual_token_attn(s, qc, qs, kb, vb, n_sel, kl, vl, k, SCALE)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hkv):
+            m = int(n_sel[b, h])
+            K = torch.from_numpy(np.concatenate([bf2f(kb[b, h, :m]), bf2f(kl[b, h])]).astype(np.float64))
+            V = torch.from_numpy(np.concatenate([bf2f(vb[b, h, :m]), bf2f(vl[b, h])]).astype(np.float64))
+            Q = torch.from_numpy(np.stack([bf2f(qc[b, h * G:(h + 1) * G]),
+                                           bf2f(qs[b, h * G:(h + 1) * G])]).astype(np.float64))
+            mask = torch.ones(2, 1, m + 2, dtype=torch.bool)
+            mask[0, 0, m + 1] = False  # the current token does not see the speculative one
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                Q, K[None].expand(2, -1, -1), V[None].expand(2, -1, -1), attn_mask=mask,
+                scale=SCALE).numpy()
+            assert np.abs(oc[b, h * G:(h + 1) * G] - ref[0]).max() < 1e-12
+            assert np.abs(os_[b, h * G:(h + 1) * G] - ref[1]).max() < 1e-12
+
+
+def pin_dual_token_empty_set(orc):
+    """No selected rows: the current token sees only itself (its V row,
+    exactly); the speculative token sees the two new rows (logistic weights)."""
+    rng = np.random.default_rng(32)
+    sh, qc, qs, kb, vb, n_sel, kl, vl = _dual_case(rng, B=1, m=(0,))
+    B, Hq, Hkv, d, k = sh["B"], sh["Hq"], sh["Hkv"], sh["d"], sh["k"]
+    oc, os_ = orc.dual_token_attn(orc.shape(B, Hq, Hkv, d, 64), qc, qs, kb, vb, n_sel, kl, vl,
+                                  k, SCALE)
+    G = Hq // Hkv
+    for h in range(Hkv):
+        v0, v1 = bf2f(vl[0, h, 0]).astype(np.float64), bf2f(vl[0, h, 1]).astype(np.float64)
+        k0, k1 = bf2f(kl[0, h, 0]).astype(np.float64), bf2f(kl[0, h, 1]).astype(np.float64)
+        for g in range(G):
+            assert np.array_equal(oc[0, h * G + g], v0)
+            q = bf2f(qs[0, h * G + g]).astype(np.float64)
+            p1 = 1.0 / (1.0 + math.exp(SCALE * (q @ k0 - q @ k1)))
+            assert np.abs(os_[0, h * G + g] - ((1 - p1) * v0 + p1 * v1)).max() < 1e-12
+
+
+def pin_dual_token_mask_invariance(orc):
+    """Changing the speculative token's row never changes the current token's
+    output, and does change the speculative token's."""
+    rng = np.random.default_rng(33)
+    sh, qc, qs, kb, vb, n_sel, kl, vl = _dual_case(rng)
+    B, Hq, Hkv, d, k = sh["B"], sh["Hq"], sh["Hkv"], sh["d"], sh["k"]
+    s = orc.shape(B, Hq, Hkv, d, 64)
+    oc1, os1 = orc.dual_token_attn(s, qc, qs, kb, vb, n_sel, kl, vl, k, SCALE)
+    kl2, vl2 = kl.copy(), vl.copy()
+    kl2[:, :, 1] = rand_bf(rng, kl2[:, :, 1].shape, scale=8.0)
+    vl2[:, :, 1] = rand_bf(rng, vl2[:, :, 1].shape, scale=8.0)
+    oc2, os2 = orc.dual_token_attn(s, qc, qs, kb, vb, n_sel, kl2, vl2, k, SCALE)
+    assert np.array_equal(oc1, oc2)
+    assert np.abs(os1 - os2).max() > 1e-3
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

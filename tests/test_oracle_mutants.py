@@ -57,6 +57,12 @@ MUTANTS = {
                             "if (r < k) rows[r++] = row;"),
     "chunk_lens_floor": ("clens[b] = (clamp_len(ctx_lens[b], s->max_ctx) + chunk - 1) / chunk;",
                          "clens[b] = clamp_len(ctx_lens[b], s->max_ctx) / chunk;"),
+    "dual_cur_sees_spec": ("ckvref_unit_attn(G, d, m + 1, jb->q + qoff, kr, vr, jb->scale, jb->out + qoff, NULL);",
+                           "ckvref_unit_attn(G, d, m + 2, jb->q + qoff, kr, vr, jb->scale, jb->out + qoff, NULL);"),
+    "dual_spec_blind_to_itself": ("ckvref_unit_attn(G, d, m + 2, jb->q2 + qoff,",
+                                  "ckvref_unit_attn(G, d, m + 1, jb->q2 + qoff,"),
+    "dual_spec_with_cur_query": ("ckvref_unit_attn(G, d, m + 2, jb->q2 + qoff,",
+                                 "ckvref_unit_attn(G, d, m + 2, jb->q + qoff,"),
     "scores_skip_last_channel": ("for (int c = 0; c < d; ++c)\n        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);",
                                  "for (int c = 0; c < d - 1; ++c)\n        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);"),
 }
