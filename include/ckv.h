@@ -89,7 +89,8 @@ typedef enum ckv_entry {
   CKV_ENTRY_SELECT_TOPK = 1,
   CKV_ENTRY_SPARSE_DECODE_ATTN = 2,
   CKV_ENTRY_CRITICAL_KV_ATTN = 3,
-  CKV_ENTRY_CORRECTED_ATTN = 4
+  CKV_ENTRY_CORRECTED_ATTN = 4,
+  CKV_ENTRY_DUAL_TOKEN_ATTN = 5
 } ckv_entry;
 
 typedef struct ckv_shape {
@@ -213,6 +214,26 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att,
                        int32_t* idx_true, int32_t* n_true, int32_t* hits,
                        int32_t* idx_next, int32_t* n_next, float* out,
                        void* ws, size_t ws_bytes, void* stream);
+
+/* Sec. 5.2 (dual-token decoding, co-batched attention) -- the current token
+ * T_i and the speculative token T'_{i+1} of every request attend together,
+ * as two consecutive positions after the selected rows, with the causal mask
+ * that hides T'_{i+1} from T_i.  k_local/v_local [B][Hkv][2][d] bf16 hold
+ * the two tokens' own rows (row 0: T_i, row 1: T'_{i+1}).  With m = n_sel
+ * (clamped to [0, k]):
+ *   out_cur[b][g]  = attention of q_cur[b][g]  over k_buf/v_buf rows [0, m)
+ *                    and local row 0,
+ *   out_spec[b][g] = attention of q_spec[b][g] over the same m rows and
+ *                    local rows 0 and 1,
+ * fp32 as in ckv_sparse_decode_attn.  One launch reads each selected row
+ * once for both tokens' 2G head rows, so G <= 8 (CKV_EUNSUPPORTED else).
+ * Workspace: CKV_ENTRY_DUAL_TOKEN_ATTN. */
+int ckv_dual_token_attn(const ckv_shape* shape, const uint16_t* q_cur,
+                        const uint16_t* q_spec, const uint16_t* k_buf,
+                        const uint16_t* v_buf, const int32_t* n_sel,
+                        const uint16_t* k_local, const uint16_t* v_local, int32_t k,
+                        float scale, float* out_cur, float* out_spec, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /* ---- chunk landmarks --------------------------------------------------------
  * Sec. 2.2: adjacent KV entries are segmented into chunks, each with a small

@@ -22,22 +22,22 @@ __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
     "critical_kv_attn", "corrected_attn", "chunk_landmarks", "select_chunks",
-    "chunked_kv_attn", "profile_begin", "profile_end", "abi_version",
+    "chunked_kv_attn", "dual_token_attn", "profile_begin", "profile_end", "abi_version",
     "Layer", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
-    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "EXPORTS",
+    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "EXPORTS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
 
 SRC_DEVICE, SRC_HOST_PINNED = 0, 1
 ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
-ENTRY_CORRECTED_ATTN = 4
+ENTRY_CORRECTED_ATTN, ENTRY_DUAL_TOKEN_ATTN = 4, 5
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
            "ckv_corrected_attn", "ckv_chunk_landmarks", "ckv_select_chunks",
-           "ckv_chunked_kv_attn",
+           "ckv_chunked_kv_attn", "ckv_dual_token_attn",
            "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_prime",
            "ckv_decode_step")
@@ -101,6 +101,8 @@ def _load() -> ctypes.CDLL:
         "ckv_chunked_kv_attn": (ctypes.c_int, [sp, i32, vp, vp, vp, vp, i32, ctypes.c_float,
                                                vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp,
                                                sz, vp]),
+        "ckv_dual_token_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, vp, vp, vp, i32,
+                                               ctypes.c_float, vp, vp, vp, sz, vp]),
         "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
@@ -222,6 +224,14 @@ def corrected_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int, scale:
         _ptr(k_buf), _ptr(v_buf), _ptr(idx_true), _ptr(n_true), _ptr(hits), _ptr(idx_next),
         _ptr(n_next), _ptr(out), _ptr(ws), ws.numel() if ws is not None else 0,
         _stream(stream)))
+
+
+def dual_token_attn(shape: Shape, q_cur, q_spec, k_buf, v_buf, n_sel, k_local, v_local,
+                    k: int, scale: float, out_cur, out_spec, ws, stream=None) -> None:
+    _check("ckv_dual_token_attn", _lib.ckv_dual_token_attn(
+        ctypes.byref(shape), _ptr(q_cur), _ptr(q_spec), _ptr(k_buf), _ptr(v_buf), _ptr(n_sel),
+        _ptr(k_local), _ptr(v_local), k, scale, _ptr(out_cur), _ptr(out_spec), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def chunk_landmarks(shape: Shape, chunk: int, keys, ctx_lens, landmarks,

@@ -116,8 +116,9 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
   const bool corrected = entry == CKV_ENTRY_CORRECTED_ATTN;
   const bool select = entry == CKV_ENTRY_SELECT_TOPK || entry == CKV_ENTRY_CRITICAL_KV_ATTN ||
                       corrected;
+  const bool two_tokens = entry == CKV_ENTRY_DUAL_TOKEN_ATTN;
   const bool attn = entry == CKV_ENTRY_SPARSE_DECODE_ATTN ||
-                    entry == CKV_ENTRY_CRITICAL_KV_ATTN || corrected;
+                    entry == CKV_ENTRY_CRITICAL_KV_ATTN || corrected || two_tokens;
   if (select) {
     L.hist = off;
     off += U * kHistBins * 4;
@@ -151,7 +152,7 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
   }
   if (attn) {
     L.part = off;
-    off = align256(off + U * (size_t)L.chunks * d.G * kPartStride * 4);
+    off = align256(off + U * (size_t)L.chunks * (two_tokens ? 2 : 1) * d.G * kPartStride * 4);
   }
   if (corrected) {
     const size_t list = align256(U * (size_t)k * 4);
@@ -277,6 +278,10 @@ AttnArgs attn_args(const Dims& d, const Layout& L, void* ws, const uint16_t* q,
   a.n_sel = n_sel;
   a.part = at<float>(ws, L.part);
   a.out = out;
+  a.q2 = nullptr;
+  a.out2 = nullptr;
+  a.k_local = nullptr;
+  a.v_local = nullptr;
   a.row_stride = row_stride;
   a.scale = scale;
   a.Hq = d.Hq;
@@ -371,7 +376,8 @@ int ckv_workspace_bytes(const ckv_shape* shape, int32_t k, int entry, size_t* by
   if ((rc = check_k(k))) return rc;
   if (!bytes) return fail(CKV_EINVAL, "bytes is NULL");
   if (entry != CKV_ENTRY_SELECT_TOPK && entry != CKV_ENTRY_SPARSE_DECODE_ATTN &&
-      entry != CKV_ENTRY_CRITICAL_KV_ATTN && entry != CKV_ENTRY_CORRECTED_ATTN)
+      entry != CKV_ENTRY_CRITICAL_KV_ATTN && entry != CKV_ENTRY_CORRECTED_ATTN &&
+      entry != CKV_ENTRY_DUAL_TOKEN_ATTN)
     return fail(CKV_EINVAL, "unknown entry %d", entry);
   *bytes = make_layout(d, k, entry).total;
   return CKV_OK;
@@ -526,6 +532,43 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
     CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
     CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   }
+  return CKV_OK;
+}
+
+int ckv_dual_token_attn(const ckv_shape* shape, const uint16_t* q_cur, const uint16_t* q_spec,
+                        const uint16_t* k_buf, const uint16_t* v_buf, const int32_t* n_sel,
+                        const uint16_t* k_local, const uint16_t* v_local, int32_t k,
+                        float scale, float* out_cur, float* out_spec, void* ws, size_t ws_bytes,
+                        void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  if (d.G > 8)
+    return fail(CKV_EUNSUPPORTED, "two tokens need 2G <= 16 head rows (G = %d)", d.G);
+  CKV_PTR(q_cur);
+  CKV_PTR(q_spec);
+  CKV_PTR(k_buf);
+  CKV_PTR(v_buf);
+  CKV_PTR(n_sel);
+  CKV_PTR(k_local);
+  CKV_PTR(v_local);
+  CKV_PTR(out_cur);
+  CKV_PTR(out_spec);
+  Layout L = make_layout(d, k, CKV_ENTRY_DUAL_TOKEN_ATTN);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  AttnArgs a = attn_args(d, L, ws, q_cur, k_buf, v_buf, nullptr, n_sel, kD, k, scale, out_cur);
+  a.q2 = q_spec;
+  a.out2 = out_spec;
+  a.k_local = k_local;
+  a.v_local = v_local;
+  // one launch reads each selected row once for the 2G head rows of both tokens
+  CKV_TRY_HIP(launch_attn(a, 2 * d.G, false, d.U, s), "attention launch");
+  CKV_TRY_HIP(launch_combine(a, 2 * d.G, d.U, s), "combine launch");
   return CKV_OK;
 }
 

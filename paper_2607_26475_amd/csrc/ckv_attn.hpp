@@ -100,8 +100,13 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
 
   bf16x8 qa[4];
   {
-    const uint16_t* qrow =
-        a.q + ((int64_t)b * a.Hq + (int64_t)h * G + r16) * kD + 8 * kg;
+    // two tokens: rows [0, G/2) are the current token's heads, the rest the
+    // speculative token's (same KV head)
+    const int Gq = a.q2 ? G / 2 : G;
+    const bool second = a.q2 && r16 >= Gq;
+    const uint16_t* qrow = (second ? a.q2 : a.q) +
+                           ((int64_t)b * a.Hq + (int64_t)h * Gq + (second ? r16 - Gq : r16)) *
+                               kD + 8 * kg;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       uint4 v = make_uint4(0u, 0u, 0u, 0u);

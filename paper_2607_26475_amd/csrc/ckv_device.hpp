@@ -89,6 +89,14 @@ struct AttnArgs {
   const int32_t* n_sel;     // [U]
   float* part;              // [U][chunks][G][kPartStride]
   float* out;               // [B][Hq][d]
+  // Two tokens (q2 != NULL): the G head rows of a unit are the current
+  // token's G/2 heads (q, out) then the speculative token's (q2, out2); the
+  // merge adds the tokens' own rows k_local/v_local [U][2][d] under the
+  // causal mask (current: row 0; speculative: rows 0 and 1).
+  const uint16_t* q2;
+  float* out2;
+  const uint16_t* k_local;
+  const uint16_t* v_local;
   int64_t row_stride;       // indexed mode: source row stride
   float scale;
   int Hq, Hkv, max_ctx, k, chunks;

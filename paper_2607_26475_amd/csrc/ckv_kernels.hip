@@ -411,15 +411,44 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
 
 // Merges the chunk partials of every query head into the output.  The
 // per-chunk (max, weight sum) pairs go through LDS first so that each thread's
-// loads of the weighted sums are independent of one another.
+// loads of the weighted sums are independent of one another.  With two tokens
+// the tokens' own rows join the merge as one more partial each (Sec. 5.2:
+// the current token sees its own row, the speculative token both rows).
 template <int G>
 __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
   constexpr int kMaxChunks = 64;
-  __shared__ float s_m[G][kMaxChunks], s_w[G][kMaxChunks], s_inv[G];
+  __shared__ float s_m[G][kMaxChunks], s_w[G][kMaxChunks], s_inv[G], s_loc[G][2];
   const int unit = blockIdx.x;
   const int b = unit / a.Hkv, h = unit - b * a.Hkv;
   const float* pu = a.part + (int64_t)unit * a.chunks * G * kPartStride;
   const int tid = threadIdx.x;
+  const bool dual = a.q2 != nullptr;
+  const int Gq = dual ? G / 2 : G;
+  auto out_row = [&](int g) {
+    if (!dual) return a.out + ((int64_t)b * a.Hq + (int64_t)h * G + g) * kD;
+    return g < Gq ? a.out + ((int64_t)b * a.Hq + (int64_t)h * Gq + g) * kD
+                  : a.out2 + ((int64_t)b * a.Hq + (int64_t)h * Gq + g - Gq) * kD;
+  };
+  // logits of the local rows each head row sees (-inf where masked)
+  if (tid < 2 * G) {
+    const int g = tid >> 1, j = tid & 1;
+    float lg = -INFINITY;
+    if (dual && (j == 0 || g >= Gq)) {
+      const uint16_t* q = (g < Gq ? a.q : a.q2) +
+                          ((int64_t)b * a.Hq + (int64_t)h * Gq + (g < Gq ? g : g - Gq)) * kD;
+      const uint16_t* kr = a.k_local + ((int64_t)unit * 2 + j) * kD;
+      float dot = 0.f;
+      for (int c = 0; c < kD; c += 8) {
+        float qf[8], kf[8];
+        unpack8(ld16(q + c), qf);
+        unpack8(ld16(kr + c), kf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dot = fmaf(qf[e], kf[e], dot);
+      }
+      lg = dot * a.scale;
+    }
+    s_loc[g][j] = lg;
+  }
   if (a.chunks <= kMaxChunks) {
     const int nc = a.chunks;
     for (int i = tid; i < nc * G; i += kAttnThreads) {
@@ -428,15 +457,21 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
       s_w[g][ch] = pu[(ch * G + g) * kPartStride + 1];
     }
     __syncthreads();
-    if (tid < G) {  // per head: global max, chunk weights exp(m_c - M), 1/L
+    if (tid < G) {  // per head: global max, chunk and local weights, 1/L
       const int g = tid;
-      float M = -INFINITY;
+      float M = fmaxf(s_loc[g][0], s_loc[g][1]);
       for (int ch = 0; ch < nc; ++ch) M = fmaxf(M, s_m[g][ch]);
       float L = 0.f;
       for (int ch = 0; ch < nc; ++ch) {
         const float w = s_m[g][ch] == -INFINITY ? 0.f : __expf(s_m[g][ch] - M);
         L = fmaf(w, s_w[g][ch], L);
         s_m[g][ch] = w;
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const float w = s_loc[g][j] == -INFINITY ? 0.f : __expf(s_loc[g][j] - M);
+        L += w;
+        s_loc[g][j] = w;
       }
       s_inv[g] = L > 0.f ? 1.f / L : 0.f;
     }
@@ -447,14 +482,21 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
 #pragma unroll 8
       for (int ch = 0; ch < nc; ++ch)
         O = fmaf(s_m[g][ch], pu[(ch * G + g) * kPartStride + 4 + c], O);
-      a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = O * s_inv[g];
+      if (dual)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          O = fmaf(s_loc[g][j],
+                   __uint_as_float((uint32_t)a.v_local[((int64_t)unit * 2 + j) * kD + c] << 16),
+                   O);
+      out_row(g)[c] = O * s_inv[g];
     }
     return;
   }
   // More chunks than fit in LDS: straightforward per-output loop.
+  __syncthreads();
   for (int o = tid; o < G * kD; o += kAttnThreads) {
     const int g = o / kD, c = o - g * kD;
-    float M = -INFINITY;
+    float M = fmaxf(s_loc[g][0], s_loc[g][1]);
     for (int ch = 0; ch < a.chunks; ++ch) M = fmaxf(M, pu[(ch * G + g) * kPartStride]);
     float L = 0.f, O = 0.f;
     if (M != -INFINITY) {
@@ -465,8 +507,16 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
         L = fmaf(w, p[1], L);
         O = fmaf(w, p[4 + c], O);
       }
+      for (int j = 0; j < 2; ++j) {
+        if (s_loc[g][j] == -INFINITY) continue;
+        const float w = __expf(s_loc[g][j] - M);
+        L += w;
+        O = fmaf(w,
+                 __uint_as_float((uint32_t)a.v_local[((int64_t)unit * 2 + j) * kD + c] << 16),
+                 O);
+      }
     }
-    a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = L > 0.f ? O / L : 0.f;
+    out_row(g)[c] = L > 0.f ? O / L : 0.f;
   }
 }
 

@@ -169,3 +169,18 @@ def test_chunk_entries_argument_checks():
     assert lib.ckv_chunked_kv_attn(ctypes.byref(s), 4, FAKE, None, FAKE, FAKE, 16, 0.1, FAKE,
                                    FAKE, 3, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need,
                                    None) == STATUS["EINVAL"]  # bad src kind
+
+
+def test_dual_token_argument_checks():
+    lib = ckv._lib
+    s = good_shape()
+    need = ckv.workspace_bytes(s, 16, ckv.ENTRY_DUAL_TOKEN_ATTN)
+    assert need > ckv.workspace_bytes(s, 16, ckv.ENTRY_SPARSE_DECODE_ATTN)  # 2G head rows
+
+    def call(shape=s, q_spec=FAKE, ws_bytes=need):
+        return lib.ckv_dual_token_attn(ctypes.byref(shape), FAKE, q_spec, FAKE, FAKE, FAKE,
+                                       FAKE, FAKE, 16, 0.1, FAKE, FAKE, FAKE, ws_bytes, None)
+
+    assert call(q_spec=None) == STATUS["EINVAL"]
+    assert call(ws_bytes=need - 1) == STATUS["EWORKSPACE"]
+    assert call(shape=good_shape(num_q_heads=32, num_kv_heads=2)) == STATUS["EUNSUPPORTED"]
