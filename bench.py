@@ -211,6 +211,9 @@ def main() -> int:
     log(f"dominant kernel {dominant}: {avg_s * 1e6:.1f} us/launch, "
         f"{achieved:.0f} GB/s algorithmic")
 
+    dual_token = measure_dual_token(torch, ckv, w, scale, stream)
+    log(f"dual-token attention: co-batched {dual_token['co_batched_us']:.1f} us, two launches "
+        f"{dual_token['two_launches_us']:.1f} us per layer")
     chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
     log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} ms/step, "
         f"{chunked['tokens_per_s']:.0f} tokens/s")
@@ -258,6 +261,7 @@ def main() -> int:
         "kernels": per_kernel,
         "roofline": roofline,
         "chunked": chunked,
+        "dual_token": dual_token,
         "host_link": host_link,
         "pipeline": pipeline,
         "cpu_baseline": cpu,
@@ -315,6 +319,53 @@ def measure_host_link(torch, ckv, dev):
     return {"gather_GBps": gather_gbps, "h2d_copy_GBps": copy_gbps,
             "frac_of_copy": gather_gbps / copy_gbps, "bytes_per_gather": gbytes,
             "workload": "B8, 8 KV heads, n 131072, k 4096, 512-byte K|V rows, pinned host"}
+
+
+def measure_dual_token(torch, ckv, w, scale, stream, reps=50):
+    """Sec. 5.2's co-batched attention at the Llama-8B shape (B16, 32 q / 8 KV
+    heads, k 2048 gathered rows): the current and the speculative token in one
+    launch against two attention calls, one per token.  Times per layer from
+    events around `reps` repetitions, each layer on its own buffers (32 sets,
+    so no repetition finds its rows in a cache)."""
+    B, Hq, Hkv, d, k, L = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k, w.layers
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(77)
+    bf = lambda *shape: torch.randn(shape, generator=g, device=dev).to(torch.bfloat16)
+    bufs = [(bf(B, Hkv, k, d), bf(B, Hkv, k, d)) for _ in range(L)]
+    q1, q2 = bf(B, Hq, d), bf(B, Hq, d)
+    kl, vl = bf(B, Hkv, 2, d), bf(B, Hkv, 2, d)
+    n_sel = torch.full((B, Hkv), k, dtype=torch.int32, device=dev)
+    o1, o2 = torch.empty((B, Hq, d), device=dev), torch.empty((B, Hq, d), device=dev)
+    s = ckv.shape_for(B, Hq, Hkv, w.max_ctx)
+    ws2 = ckv.workspace(s, k, ckv.ENTRY_DUAL_TOKEN_ATTN)
+    ws1 = ckv.workspace(s, k, ckv.ENTRY_SPARSE_DECODE_ATTN)
+
+    def co(l):
+        ckv.dual_token_attn(s, q1, q2, bufs[l][0], bufs[l][1], n_sel, kl, vl, k, scale, o1, o2,
+                            ws2, stream)
+
+    def two(l):
+        ckv.sparse_decode_attn(s, q1, bufs[l][0], bufs[l][1], n_sel, k, scale, o1, ws1, stream)
+        ckv.sparse_decode_attn(s, q2, bufs[l][0], bufs[l][1], n_sel, k, scale, o2, ws1, stream)
+
+    res = {}
+    for name, fn in (("co_batched_us", co), ("two_launches_us", two)):
+        for l in range(L):
+            fn(l)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for r in range(reps):
+            fn(r % L)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res[name] = 1e3 * e0.elapsed_time(e1) / reps
+    res["saving"] = 1.0 - res["co_batched_us"] / res["two_launches_us"]
+    res["workload"] = ("B16, 32 q / 8 KV heads, k 2048 gathered rows per KV head; the two "
+                       "tokens' own rows under the causal mask (co-batched only)")
+    del bufs
+    return res
 
 
 def measure_chunked(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream,
