@@ -22,6 +22,15 @@ __global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a) {
   score_range<G, HIST>(a, blockIdx.x, gridDim.x, lds_hist, lds_stage);
 }
 
+// The same pass over chunk landmarks (a kernel of its own only so that
+// traces and profiles keep the two workloads apart).
+template <int G>
+__global__ __launch_bounds__(kScoreThreads) void k_score_chunks(ScoreArgs a) {
+  __shared__ uint32_t lds_hist[kHistBins];
+  __shared__ __attribute__((aligned(16))) uint32_t lds_stage[kScoreLdsDwords];
+  score_range<G, true>(a, blockIdx.x, gridDim.x, lds_hist, lds_stage);
+}
+
 // ---- selection -----------------------------------------------------------
 // First-digit histogram of given scores (standalone selection entry).
 __global__ __launch_bounds__(kScoreThreads) void k_hist(SelectArgs a) {
@@ -760,7 +769,10 @@ static int score_grid(const ScoreArgs& a, const void* fn) {
 template <int G>
 static void launch_score_g(const ScoreArgs& a, bool hist, hipStream_t s) {
   const dim3 block(kScoreThreads);
-  if (hist) {
+  if (a.chunk > 1) {
+    auto fn = k_score_chunks<G>;
+    launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
+  } else if (hist) {
     auto fn = k_score<G, true>;
     launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
   } else {
