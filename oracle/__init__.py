@@ -84,6 +84,8 @@ class Oracle:
         lib.ckvref_expand_chunks.argtypes = [i32, i32, vp, i32, i32, vp]
         lib.ckvref_select_chunks.argtypes = [sp, i32, vp, vp, vp, i32, f32, vp, vp, vp, vp,
                                              i32]
+        lib.ckvref_reconstruct_keys.argtypes = [sp, i32, vp, vp, vp, vp, i32, vp]
+        lib.ckvref_reconstruct_keys.restype = ctypes.c_int
         lib.ckvref_dual_token_attn.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, f32, vp,
                                                vp, i32]
         for f in ("ckvref_dual_token_attn", "ckvref_score_keys", "ckvref_select_topk",
@@ -233,6 +235,17 @@ class Oracle:
                                              scale, _p(out_cur), _p(out_spec), nthreads)
         assert rc == 0
         return out_cur, out_spec
+
+
+    # ---- low-rank key reconstruction ----------------------------------------
+    def reconstruct_keys(self, s: _Shape, rank: int, u_fac, w_fac, idx, n_sel, k,
+                         fill=0x7777):
+        u_fac, w_fac, idx, n_sel = _u16(u_fac), _u16(w_fac), _i32(idx), _i32(n_sel)
+        out = np.full((s.batch, s.num_kv_heads, k, s.head_dim), fill, dtype=np.uint16)
+        rc = self.lib.ckvref_reconstruct_keys(ctypes.byref(s), rank, _p(u_fac), _p(w_fac),
+                                              _p(idx), _p(n_sel), k, _p(out))
+        assert rc == 0
+        return out
 
 
 _default: Optional[Oracle] = None

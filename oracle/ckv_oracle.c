@@ -465,3 +465,30 @@ int ckvref_dual_token_attn(const ckvref_shape* s, const uint16_t* q_cur,
   run_units(&jb, s->batch * s->num_kv_heads, nthreads);
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* low-rank key reconstruction                                               */
+
+/* Sec. 5.3: a selected key is rebuilt from the unit's low-rank factors. */
+int ckvref_reconstruct_keys(const ckvref_shape* s, int rank, const uint16_t* u_fac,
+                            const uint16_t* w_fac, const int32_t* idx, const int32_t* n_sel,
+                            int k, uint16_t* k_dst) {
+  if (!shape_ok(s) || rank < 1 || k < 1) return -1;
+  const int units = s->batch * s->num_kv_heads, d = s->head_dim;
+  for (int u = 0; u < units; ++u) {
+    int m = n_sel[u];
+    if (m < 0) m = 0;
+    if (m > k) m = k;
+    const uint16_t* W = w_fac + (int64_t)u * rank * d;
+    for (int i = 0; i < m; ++i) {
+      const uint16_t* U = u_fac + ((int64_t)u * s->max_ctx + idx[(int64_t)u * k + i]) * rank;
+      for (int c = 0; c < d; ++c) {
+        double acc = 0.0;
+        for (int j = 0; j < rank; ++j)
+          acc += ckvref_bf16_to_f64(U[j]) * ckvref_bf16_to_f64(W[(int64_t)j * d + c]);
+        k_dst[((int64_t)u * k + i) * d + c] = ckvref_f64_to_bf16(acc);
+      }
+    }
+  }
+  return 0;
+}

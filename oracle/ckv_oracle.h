@@ -155,6 +155,19 @@ int ckvref_dual_token_attn(const ckvref_shape* s, const uint16_t* q_cur,
                            const uint16_t* k_local, const uint16_t* v_local, int k,
                            float scale, double* out_cur, double* out_spec, int nthreads);
 
+/* ---- low-rank key reconstruction --------------------------------------
+ * Sec. 5.3 (adaptive key reconstruction, after ShadowKV): for layers whose
+ * prediction misses often, selected keys are rebuilt on the GPU from a
+ * low-rank key cache instead of being fetched; values are still fetched.
+ * The cache of a unit is K ~ U . W with U [max_ctx][rank] and W [rank][d]
+ * (bf16).  For i < n_sel (clamped to [0, k]):
+ *   k_dst[b][h][i][c] = bf16(sum over j < rank, ascending, of
+ *                            U[idx_i][j] * W[j][c])   (fp64 sum, rounded once)
+ * Slots i >= n_sel are not written. */
+int ckvref_reconstruct_keys(const ckvref_shape* s, int rank, const uint16_t* u_fac,
+                            const uint16_t* w_fac, const int32_t* idx, const int32_t* n_sel,
+                            int k, uint16_t* k_dst);
+
 #ifdef __cplusplus
 }
 #endif

@@ -551,4 +551,53 @@ def pin_dual_token_mask_invariance(orc):
     assert np.abs(os1 - os2).max() > 1e-3
 
 
+# --- low-rank key reconstruction ---------------------------------------------------
+def pin_reconstruct_identity(orc):
+    """rank = d and W = I: the reconstruction is the U row itself, bit for bit
+    (slots past n_sel untouched)."""
+    rng = np.random.default_rng(41)
+    B, Hkv, n, d, k = 2, 2, 40, 128, 8
+    U = rand_bf(rng, (B, Hkv, n, d))
+    W = np.tile(f2bf(np.eye(d, dtype=np.float32)), (B, Hkv, 1, 1))
+    idx = rng.integers(0, n, size=(B, Hkv, k)).astype(np.int32)
+    nsel = np.array([[8, 3], [0, 5]], np.int32)
+    out = orc.reconstruct_keys(orc.shape(B, 2 * Hkv, Hkv, d, n), d, U, W, idx, nsel, k)
+    for b in range(B):
+        for h in range(Hkv):
+            m = nsel[b, h]
+            assert np.array_equal(out[b, h, :m], U[b, h, idx[b, h, :m]])
+            assert np.all(out[b, h, m:] == 0x7777)
+
+
+def pin_reconstruct_library(orc):
+    """Small exact factors (values in multiples of 1/8, rank 4): the products
+    and sums are exact in fp64 and fit bf16, so the result equals numpy's
+    matrix product, rounded by torch to bf16 (a no-op here)."""
+    rng = np.random.default_rng(42)
+    B, Hkv, n, d, r, k = 1, 3, 20, 128, 4, 6
+    U = f2bf(rng.integers(-8, 9, size=(B, Hkv, n, r)).astype(np.float32) / 8)
+    W = f2bf(rng.integers(-4, 5, size=(B, Hkv, r, d)).astype(np.float32) / 4)
+    idx = np.stack([[rng.permutation(n)[:k] for _ in range(Hkv)]]).astype(np.int32)
+    nsel = np.full((B, Hkv), k, np.int32)
+    out = orc.reconstruct_keys(orc.shape(B, Hkv, Hkv, d, n), r, U, W, idx, nsel, k)
+    for h in range(Hkv):
+        ref = bf2f(U[0, h, idx[0, h]]).astype(np.float64) @ bf2f(W[0, h]).astype(np.float64)
+        want = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16).view(torch.int16)
+        assert np.array_equal(out[0, h].view(np.int16), want.numpy())
+
+
+def pin_reconstruct_rounding(orc):
+    """A sum landing on a bf16 midpoint rounds to even: 1 + 2^-8 from two
+    rank terms (1 and 2^-8) gives 1.0; 1 + 2^-8 + 2^-16 gives 1 + 2^-7."""
+    d = 128
+    U = f2bf(np.array([[[[1.0, 2.0 ** -8, 2.0 ** -16]]]], np.float32))
+    W1 = f2bf(np.concatenate([np.ones((1, 1, 2, d)), np.zeros((1, 1, 1, d))], axis=2)
+              .astype(np.float32))
+    W2 = f2bf(np.ones((1, 1, 3, d), np.float32))
+    s = orc.shape(1, 1, 1, d, 1)
+    idx, nsel = np.zeros((1, 1, 1), np.int32), np.ones((1, 1), np.int32)
+    assert np.all(orc.reconstruct_keys(s, 3, U, W1, idx, nsel, 1) == 0x3F80)
+    assert np.all(orc.reconstruct_keys(s, 3, U, W2, idx, nsel, 1) == 0x3F81)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -63,6 +63,12 @@ MUTANTS = {
                                   "ckvref_unit_attn(G, d, m + 1, jb->q2 + qoff,"),
     "dual_spec_with_cur_query": ("ckvref_unit_attn(G, d, m + 2, jb->q2 + qoff,",
                                  "ckvref_unit_attn(G, d, m + 2, jb->q + qoff,"),
+    "recon_transposed_w": ("ckvref_bf16_to_f64(W[(int64_t)j * d + c]);",
+                           "ckvref_bf16_to_f64(W[(int64_t)c * rank + j]);"),
+    "recon_drop_last_rank": ("for (int j = 0; j < rank; ++j)\n          acc +=",
+                             "for (int j = 0; j < rank - 1; ++j)\n          acc +="),
+    "recon_slot_not_row": ("const uint16_t* U = u_fac + ((int64_t)u * s->max_ctx + idx[(int64_t)u * k + i]) * rank;",
+                           "const uint16_t* U = u_fac + ((int64_t)u * s->max_ctx + i) * rank;"),
     "scores_skip_last_channel": ("for (int c = 0; c < d; ++c)\n        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);",
                                  "for (int c = 0; c < d - 1; ++c)\n        dot += ckvref_bf16_to_f64(q[g * d + c]) * ckvref_bf16_to_f64(kr[c]);"),
 }
