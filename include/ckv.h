@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 2
+#define CKV_ABI_VERSION 3
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -215,6 +215,43 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att,
                        int32_t* idx_next, int32_t* n_next, float* out,
                        void* ws, size_t ws_bytes, void* stream);
 
+/* ---- adaptive key reconstruction -------------------------------------------
+ * Sec. 5.3 (adaptive key reconstruction): for layers where the prediction
+ * misses many rows, the keys of the missing rows are rebuilt on the GPU from
+ * a low-rank key cache, and only their values come from k_src/v_src's
+ * memory.  Factors per (b, h), bf16 on the device:
+ *   u_fac [B][Hkv][max_ctx][rank]   w_fac [B][Hkv][rank][d]
+ * Key row p of (b, h) is rebuilt as
+ *   K'[p][c] = sum_{j < rank} u_fac[b][h][p][j] * w_fac[b][h][j][c],
+ * summed in fp64 in ascending j (each product is exact) and rounded once to
+ * bf16, nearest, ties to even.  rank is in [1, CKV_MAX_RANK]. */
+#define CKV_MAX_RANK 4096
+
+/* For i < n_sel[b][h] (clamped to [0, k]) writes K'[idx[b][h][i]] to
+ * k_dst[b][h][i] ([B][Hkv][k][d]).  Entries whose idx is outside
+ * [0, max_ctx), and slots i >= n_sel, are not written. */
+int ckv_reconstruct_keys(const ckv_shape* shape, int32_t rank, const uint16_t* u_fac,
+                         const uint16_t* w_fac, const int32_t* idx, const int32_t* n_sel,
+                         int32_t k, uint16_t* k_dst, void* stream);
+
+/* ckv_corrected_attn for a layer with key reconstruction: the same, except
+ * that the key of every row of idx_true missing from idx_pred is rebuilt into
+ * its slot as ckv_reconstruct_keys rebuilds it, in the same launch that
+ * fetches its value from v_src (k_src is not read and may be NULL).  out is
+ * the attention of q_att over the rows of idx_true, with the prefetched keys
+ * for hits and the rebuilt keys for misses.  Workspace:
+ * CKV_ENTRY_CORRECTED_ATTN. */
+int ckv_corrected_attn_lowrank(const ckv_shape* shape, const uint16_t* q_att,
+                               const uint16_t* q_sel, const uint16_t* k_score,
+                               const int32_t* ctx_lens, int32_t k, float scale,
+                               const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                               int32_t rank, const uint16_t* u_fac, const uint16_t* w_fac,
+                               const int32_t* idx_pred, const int32_t* n_pred,
+                               uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
+                               int32_t* n_true, int32_t* hits, int32_t* idx_next,
+                               int32_t* n_next, float* out, void* ws, size_t ws_bytes,
+                               void* stream);
+
 /* Sec. 5.2 (dual-token decoding, co-batched attention) -- the current token
  * T_i and the speculative token T'_{i+1} of every request attend together,
  * as two consecutive positions after the selected rows, with the causal mask
@@ -307,6 +344,9 @@ typedef struct ckv_layer {
   int32_t* idx_true;          /* NULL: attention over the predicted set.  Else  */
   int32_t* n_true;            /* the layer runs ckv_corrected_attn: [B][Hkv][k], */
   int32_t* hits;              /* [B][Hkv] and [B][Hkv] written                   */
+  int32_t lr_rank;            /* > 0 (with idx_true set): misses' keys rebuilt  */
+  const uint16_t* lr_u;       /* from these factors, ckv_corrected_attn_lowrank */
+  const uint16_t* lr_w;       /* (u_fac, w_fac); 0/NULL otherwise               */
 } ckv_layer;
 
 typedef struct ckv_pipeline ckv_pipeline; /* events of one decode loop */
@@ -328,7 +368,8 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
  * over the buffer holding idx_prev's rows, selection from q_sel into
  * idx_next), or, for a layer with idx_true set, ckv_corrected_attn (misses
  * of idx_prev against q_att's own selection fetched into the buffer first,
- * src_kind and the layer's k_src/v_src); on copy_stream: the refill of the
+ * src_kind and the layer's k_src/v_src), ckv_corrected_attn_lowrank if its
+ * lr_rank is also > 0; on copy_stream: the refill of the
  * released buffer with layer l+2, or, for the last two layers, with the next
  * step's layers 0 and 1 from this step's idx_next.  Before the next step the
  * caller swaps idx_prev and idx_next.  ws is the workspace of
@@ -360,7 +401,8 @@ typedef enum ckv_kernel_id {
   CKV_K_MISS = 9,     /* predicted vs selected set: hits, misses, slots     */
   CKV_K_LANDMARKS = 10, /* chunk landmarks (mean keys)                      */
   CKV_K_EXPAND = 11,  /* selected chunks -> their rows                      */
-  CKV_K_COUNT = 12
+  CKV_K_RECONSTRUCT = 12, /* low-rank key rebuild (with the misses' V fetch)  */
+  CKV_K_COUNT = 13
 } ckv_kernel_id;
 
 #define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)

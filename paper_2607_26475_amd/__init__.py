@@ -22,7 +22,8 @@ __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
     "critical_kv_attn", "corrected_attn", "chunk_landmarks", "select_chunks",
-    "chunked_kv_attn", "dual_token_attn", "profile_begin", "profile_end", "abi_version",
+    "chunked_kv_attn", "dual_token_attn", "reconstruct_keys", "corrected_attn_lowrank",
+    "MAX_RANK", "profile_begin", "profile_end", "abi_version",
     "Layer", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "EXPORTS",
@@ -37,11 +38,13 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
            "ckv_corrected_attn", "ckv_chunk_landmarks", "ckv_select_chunks",
-           "ckv_chunked_kv_attn", "ckv_dual_token_attn",
+           "ckv_chunked_kv_attn", "ckv_dual_token_attn", "ckv_reconstruct_keys",
+           "ckv_corrected_attn_lowrank",
            "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_prime",
            "ckv_decode_step")
-KERNEL_COUNT = 12
+KERNEL_COUNT = 13
+MAX_RANK = 4096
 
 
 class CkvError(RuntimeError):
@@ -60,7 +63,8 @@ class Layer(ctypes.Structure):
     """Mirror of ``ckv_layer``."""
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "q_att", "q_sel", "k_score", "k_src", "v_src", "idx_prev", "n_sel_prev",
-        "idx_next", "n_sel_next", "out", "idx_true", "n_true", "hits")]
+        "idx_next", "n_sel_next", "out", "idx_true", "n_true", "hits")] + [
+        ("lr_rank", ctypes.c_int32), ("lr_u", ctypes.c_void_p), ("lr_w", ctypes.c_void_p)]
 
 
 class Shape(ctypes.Structure):
@@ -103,6 +107,11 @@ def _load() -> ctypes.CDLL:
                                                sz, vp]),
         "ckv_dual_token_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, vp, vp, vp, i32,
                                                ctypes.c_float, vp, vp, vp, sz, vp]),
+        "ckv_reconstruct_keys": (ctypes.c_int, [sp, i32, vp, vp, vp, vp, i32, vp, vp]),
+        "ckv_corrected_attn_lowrank": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
+                                                      vp, vp, ctypes.c_int, i32, vp, vp, vp,
+                                                      vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                      vp, sz, vp]),
         "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
@@ -226,6 +235,25 @@ def corrected_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int, scale:
         _stream(stream)))
 
 
+def corrected_attn_lowrank(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
+                           scale: float, k_src, v_src, src_kind: int, rank: int, u_fac, w_fac,
+                           idx_pred, n_pred, k_buf, v_buf, idx_true, n_true, hits, idx_next,
+                           n_next, out, ws, stream=None) -> None:
+    _check("ckv_corrected_attn_lowrank", _lib.ckv_corrected_attn_lowrank(
+        ctypes.byref(shape), _ptr(q_att), _ptr(q_sel), _ptr(k_score), _ptr(ctx_lens), k,
+        scale, _ptr(k_src), _ptr(v_src), src_kind, rank, _ptr(u_fac), _ptr(w_fac),
+        _ptr(idx_pred), _ptr(n_pred), _ptr(k_buf), _ptr(v_buf), _ptr(idx_true), _ptr(n_true),
+        _ptr(hits), _ptr(idx_next), _ptr(n_next), _ptr(out), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def reconstruct_keys(shape: Shape, rank: int, u_fac, w_fac, idx, n_sel, k: int, k_dst,
+                     stream=None) -> None:
+    _check("ckv_reconstruct_keys", _lib.ckv_reconstruct_keys(
+        ctypes.byref(shape), rank, _ptr(u_fac), _ptr(w_fac), _ptr(idx), _ptr(n_sel), k,
+        _ptr(k_dst), _stream(stream)))
+
+
 def dual_token_attn(shape: Shape, q_cur, q_spec, k_buf, v_buf, n_sel, k_local, v_local,
                     k: int, scale: float, out_cur, out_spec, ws, stream=None) -> None:
     _check("ckv_dual_token_attn", _lib.ckv_dual_token_attn(
@@ -261,7 +289,7 @@ def chunked_kv_attn(shape: Shape, chunk: int, q_att, q_sel, landmarks, ctx_lens,
 
 KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
               "combine": 6, "dual": 7, "gather": 8, "miss": 9, "landmarks": 10,
-              "expand": 11}
+              "expand": 11, "reconstruct": 12}
 
 
 def profile_begin(kernels=None) -> None:
@@ -288,8 +316,11 @@ def _layers(layers) -> "ctypes.Array":
     """dicts with the ckv_layer field names (tensors, ints or None) -> array."""
     arr = (Layer * len(layers))()
     for i, d in enumerate(layers):
-        for name, _ in Layer._fields_:
-            setattr(arr[i], name, _ptr(d.get(name)))
+        for name, typ in Layer._fields_:
+            if typ is ctypes.c_int32:
+                setattr(arr[i], name, int(d.get(name) or 0))
+            else:
+                setattr(arr[i], name, _ptr(d.get(name)))
     return arr
 
 

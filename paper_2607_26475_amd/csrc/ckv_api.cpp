@@ -83,6 +83,12 @@ int check_k(int32_t k) {
   return CKV_OK;
 }
 
+int check_rank(int32_t rank) {
+  if (rank < 1 || rank > CKV_MAX_RANK)
+    return fail(CKV_ESHAPE, "rank %d outside [1, %d]", rank, CKV_MAX_RANK);
+  return CKV_OK;
+}
+
 int check_scale(float scale) {
   if (!(scale > 0.f) || scale > 3.0e38f)
     return fail(CKV_EINVAL, "scale must be a finite positive number");
@@ -213,6 +219,23 @@ int resolve_src(int src_kind, const uint16_t** k_src, const uint16_t** v_src) {
   int rc = host_to_device(*k_src, k_src);
   if (rc) return rc;
   return host_to_device(*v_src, v_src);
+}
+
+ReconArgs recon_args(const Dims& d, int32_t rank, const uint16_t* u_fac, const uint16_t* w_fac,
+                     const int32_t* idx, const int32_t* n_sel, const int32_t* slots, int32_t k,
+                     uint16_t* k_dst) {
+  ReconArgs r;
+  r.u_fac = u_fac;
+  r.w_fac = w_fac;
+  r.idx = idx;
+  r.n_sel = n_sel;
+  r.slots = slots;
+  r.k_dst = k_dst;
+  r.items = (int64_t)d.U * k * 16;
+  r.max_ctx = d.max_ctx;
+  r.k = k;
+  r.rank = rank;
+  return r;
 }
 
 int gather_blocks(int src_kind) {
@@ -662,13 +685,18 @@ int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q
   return CKV_OK;
 }
 
-int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
-                       const uint16_t* k_score, const int32_t* ctx_lens, int32_t k,
-                       float scale, const uint16_t* k_src, const uint16_t* v_src,
-                       int src_kind, const int32_t* idx_pred, const int32_t* n_pred,
-                       uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
-                       int32_t* n_true, int32_t* hits, int32_t* idx_next, int32_t* n_next,
-                       float* out, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// rank == 0: misses fetched whole; else their keys rebuilt from u_fac/w_fac
+int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                   const uint16_t* k_score, const int32_t* ctx_lens, int32_t k, float scale,
+                   const uint16_t* k_src, const uint16_t* v_src, int src_kind, int32_t rank,
+                   const uint16_t* u_fac, const uint16_t* w_fac, const int32_t* idx_pred,
+                   const int32_t* n_pred, uint16_t* k_buf, uint16_t* v_buf,
+                   int32_t* idx_true, int32_t* n_true, int32_t* hits, int32_t* idx_next,
+                   int32_t* n_next, float* out, void* ws, size_t ws_bytes, void* stream) {
   Dims d;
   int rc = check_shape(shape, &d);
   if (rc) return rc;
@@ -679,6 +707,12 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint
   CKV_PTR(q_sel);
   CKV_PTR(k_score);
   CKV_PTR(ctx_lens);
+  if (rank > 0) {
+    if ((rc = check_rank(rank))) return rc;
+    CKV_PTR(u_fac);
+    CKV_PTR(w_fac);
+    if (!k_src) k_src = v_src;  // not read
+  }
   CKV_PTR(k_src);
   CKV_PTR(v_src);
   CKV_PTR(idx_pred);
@@ -724,13 +758,19 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint
   g.idx = m.miss_pos;
   g.n_sel = m.n_miss;
   g.slots = m.miss_slot;
-  g.k_dst = k_buf;
+  g.k_dst = rank > 0 ? nullptr : k_buf;
   g.v_dst = v_buf;
   g.row_stride = d.kv_stride;
   g.items = (int64_t)d.U * k * 32;
   g.max_ctx = d.max_ctx;
   g.k = k;
-  CKV_TRY_HIP(launch_gather(g, gather_blocks(src_kind), s), "miss gather launch");
+  if (rank > 0) {
+    ReconArgs r = recon_args(d, rank, u_fac, w_fac, m.miss_pos, m.n_miss, m.miss_slot, k,
+                             k_buf);
+    CKV_TRY_HIP(launch_miss_fill(g, gather_blocks(src_kind), r, s), "miss fill launch");
+  } else {
+    CKV_TRY_HIP(launch_gather(g, gather_blocks(src_kind), s), "miss gather launch");
+  }
   // 3. attention over exactly the selected rows, now all in the buffer (read
   //    through the slot list), in one launch with 4. the next step's scoring
   SelectArgs s2 = select_args(d, L, ws, scores, ctx_lens, k, idx_next, n_next);
@@ -746,6 +786,58 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint
   CKV_TRY_HIP(launch_dual(at_, c2, d.G, true, d.U, s), "dual launch");
   if ((rc = run_select_tail(s2, d.U, s))) return rc;
   CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+  return CKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                       const uint16_t* k_score, const int32_t* ctx_lens, int32_t k,
+                       float scale, const uint16_t* k_src, const uint16_t* v_src,
+                       int src_kind, const int32_t* idx_pred, const int32_t* n_pred,
+                       uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
+                       int32_t* n_true, int32_t* hits, int32_t* idx_next, int32_t* n_next,
+                       float* out, void* ws, size_t ws_bytes, void* stream) {
+  return corrected_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
+                        src_kind, 0, nullptr, nullptr, idx_pred, n_pred, k_buf, v_buf,
+                        idx_true, n_true, hits, idx_next, n_next, out, ws, ws_bytes, stream);
+}
+
+int ckv_corrected_attn_lowrank(const ckv_shape* shape, const uint16_t* q_att,
+                               const uint16_t* q_sel, const uint16_t* k_score,
+                               const int32_t* ctx_lens, int32_t k, float scale,
+                               const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                               int32_t rank, const uint16_t* u_fac, const uint16_t* w_fac,
+                               const int32_t* idx_pred, const int32_t* n_pred,
+                               uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
+                               int32_t* n_true, int32_t* hits, int32_t* idx_next,
+                               int32_t* n_next, float* out, void* ws, size_t ws_bytes,
+                               void* stream) {
+  int rc = check_rank(rank);
+  if (rc) return rc;
+  return corrected_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
+                        src_kind, rank, u_fac, w_fac, idx_pred, n_pred, k_buf, v_buf,
+                        idx_true, n_true, hits, idx_next, n_next, out, ws, ws_bytes, stream);
+}
+
+int ckv_reconstruct_keys(const ckv_shape* shape, int32_t rank, const uint16_t* u_fac,
+                         const uint16_t* w_fac, const int32_t* idx, const int32_t* n_sel,
+                         int32_t k, uint16_t* k_dst, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_rank(rank))) return rc;
+  CKV_PTR(u_fac);
+  CKV_PTR(w_fac);
+  CKV_PTR(idx);
+  CKV_PTR(n_sel);
+  CKV_PTR(k_dst);
+  if (d.U == 0) return CKV_OK;
+  ReconArgs r = recon_args(d, rank, u_fac, w_fac, idx, n_sel, nullptr, k, k_dst);
+  CKV_TRY_HIP(launch_reconstruct(r, (hipStream_t)stream), "reconstruct launch");
   return CKV_OK;
 }
 

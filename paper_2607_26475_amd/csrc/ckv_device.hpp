@@ -125,6 +125,18 @@ struct LandmarkArgs {
   int Hkv, max_ctx, chunk, cmax;
 };
 
+// Low-rank key reconstruction: K row = U row . W, rounded once to bf16.
+struct ReconArgs {
+  const uint16_t* u_fac;    // [U][max_ctx][rank]
+  const uint16_t* w_fac;    // [U][rank][d]
+  const int32_t* idx;       // [U][k] rows to rebuild
+  const int32_t* n_sel;     // [U]
+  const int32_t* slots;     // [U][k] destination slot of entry i; NULL: slot i
+  uint16_t* k_dst;          // [U][k][d]
+  int64_t items;            // U * k * 16
+  int max_ctx, k, rank;
+};
+
 // Rows of the selected chunks.
 struct ExpandArgs {
   const int32_t* chunk_idx; // [U][kc] ascending

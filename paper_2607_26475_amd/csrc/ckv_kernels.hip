@@ -603,6 +603,45 @@ __global__ __launch_bounds__(kGatherThreads) void k_expand(ExpandArgs a) {
         m == 0 ? 0 : (m - 1) * a.chunk + max(0, min(a.chunk, n - ci[m - 1] * a.chunk));
 }
 
+// ---- low-rank key reconstruction -------------------------------------------------
+// One item = 8 channels of one rebuilt key: the fp64 sum over the rank in
+// ascending order (bf16 products are exact in fp64), rounded once to bf16.
+__device__ __forceinline__ void reconstruct_range(const ReconArgs& a, int blk, int nblk) {
+  const int64_t stride = (int64_t)nblk * kGatherThreads;
+  for (int64_t it = (int64_t)blk * kGatherThreads + threadIdx.x; it < a.items;
+       it += stride) {
+    const int part = (int)(it & 15);
+    const int64_t slot = it >> 4;
+    const int64_t unit = slot / a.k;
+    const int i = (int)(slot - unit * a.k);
+    if (i >= clamp_len(a.n_sel[unit], a.k)) continue;
+    const int row = a.idx[slot];
+    const int di = a.slots ? a.slots[slot] : i;
+    if (row < 0 || row >= a.max_ctx || di < 0 || di >= a.k) continue;
+    const uint16_t* u = a.u_fac + (unit * a.max_ctx + row) * a.rank;
+    const uint16_t* w = a.w_fac + unit * a.rank * kD + 8 * part;
+    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int j = 0; j < a.rank; ++j) {
+      const double uj = (double)__uint_as_float((uint32_t)u[j] << 16);
+      float wf[8];
+      unpack8(ld16(w + (int64_t)j * kD), wf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += uj * (double)wf[e];
+    }
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      o[e] = (uint32_t)f64_to_bf16_rne(acc[2 * e]) |
+             ((uint32_t)f64_to_bf16_rne(acc[2 * e + 1]) << 16);
+    *reinterpret_cast<uint4*>(a.k_dst + (unit * a.k + di) * kD + 8 * part) =
+        make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+__global__ __launch_bounds__(kGatherThreads) void k_reconstruct(ReconArgs a) {
+  reconstruct_range(a, blockIdx.x, gridDim.x);
+}
+
 // ---- miss detection -----------------------------------------------------------
 // First index i in [0, n) with a[i] >= v (a ascending).
 template <class P>
@@ -696,9 +735,10 @@ __global__ __launch_bounds__(kMissThreads) void k_miss(MissArgs a) {
 // Item it = ((unit*k + slot)*2 + kv)*16 + part moves 16 bytes; the 32 items of
 // one slot are its K row then its V row (contiguous for K|V interleaved rows).
 // With a slot list, entry slot of the unit lands in slot slots[unit][slot].
-__global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
-  const int64_t step = (int64_t)gridDim.x * kGatherThreads * kGatherUnroll;
-  for (int64_t it0 = (int64_t)blockIdx.x * kGatherThreads * kGatherUnroll; it0 < a.items;
+// K items are skipped when k_dst is NULL.
+__device__ __forceinline__ void gather_range(const GatherArgs& a, int blk, int nblk) {
+  const int64_t step = (int64_t)nblk * kGatherThreads * kGatherUnroll;
+  for (int64_t it0 = (int64_t)blk * kGatherThreads * kGatherUnroll; it0 < a.items;
        it0 += step) {
     uint4 v[kGatherUnroll];
     uint16_t* dst[kGatherUnroll];
@@ -715,7 +755,7 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
         if (i < a.n_sel[unit]) {
           const int pos = a.idx[slot];
           const int di = a.slots ? a.slots[slot] : i;
-          if (pos >= 0 && pos < a.max_ctx && di >= 0 && di < a.k) {
+          if (pos >= 0 && pos < a.max_ctx && di >= 0 && di < a.k && (kv || a.k_dst)) {
             const uint16_t* src = (kv ? a.v_src : a.k_src) +
                                   (unit * a.max_ctx + pos) * a.row_stride + part * 8;
             v[u] = ld16(src);
@@ -728,6 +768,21 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
     for (int u = 0; u < kGatherUnroll; ++u)
       if (dst[u]) *reinterpret_cast<uint4*>(dst[u]) = v[u];
   }
+}
+
+__global__ __launch_bounds__(kGatherThreads) void k_gather(GatherArgs a) {
+  gather_range(a, blockIdx.x, gridDim.x);
+}
+
+// Misses of a layer with key reconstruction: the first `nfetch` workgroups
+// fetch the missing values while the others rebuild the missing keys, so the
+// transfer and the arithmetic overlap in one launch.
+__global__ __launch_bounds__(kGatherThreads) void k_miss_fill(GatherArgs g, ReconArgs r,
+                                                              int nfetch) {
+  if ((int)blockIdx.x < nfetch)
+    gather_range(g, blockIdx.x, nfetch);
+  else
+    reconstruct_range(r, blockIdx.x - nfetch, gridDim.x - nfetch);
 }
 
 // ---- launchers ---------------------------------------------------------------
@@ -879,6 +934,21 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s) {
   const int blocks = blocks_for(a.items, kGatherThreads, 8192);
   launch_kernel(CKV_K_LANDMARKS, k_landmarks, dim3(blocks), dim3(kGatherThreads), s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_reconstruct(const ReconArgs& a, hipStream_t s) {
+  const int blocks = blocks_for(a.items, kGatherThreads, 8192);
+  launch_kernel(CKV_K_RECONSTRUCT, k_reconstruct, dim3(blocks), dim3(kGatherThreads), s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconArgs& r,
+                            hipStream_t s) {
+  const int nf = blocks_for(g.items, kGatherThreads * kGatherUnroll, fetch_blocks);
+  const int nr = blocks_for(r.items, kGatherThreads, 8192);
+  launch_kernel(CKV_K_RECONSTRUCT, k_miss_fill, dim3(nf + nr), dim3(kGatherThreads), s, g, r,
+                nf);
   return hipGetLastError();
 }
 

@@ -18,6 +18,10 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s);
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s);
 hipError_t launch_expand(const ExpandArgs& a, int units, hipStream_t s);
+hipError_t launch_reconstruct(const ReconArgs& a, hipStream_t s);
+// value fetch (gather with k_dst NULL) and key rebuild of the misses in one launch
+hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconArgs& r,
+                            hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s);
 
 }  // namespace ckv

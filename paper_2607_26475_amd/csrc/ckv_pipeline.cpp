@@ -79,7 +79,13 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     // attention over buffer p once its gather has landed
     if (hipStreamWaitEvent(cs, pipe->filled[p], 0) != hipSuccess) return CKV_EHIP;
     int rc;
-    if (L.idx_true) {  // the current query's own set: misses fetched into buffer p first
+    if (L.idx_true && L.lr_rank > 0) {  // misses: keys rebuilt, values fetched
+      rc = ckv_corrected_attn_lowrank(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
+                                      L.k_src, L.v_src, src_kind, L.lr_rank, L.lr_u, L.lr_w,
+                                      L.idx_prev, L.n_sel_prev, k_buf[p], v_buf[p],
+                                      L.idx_true, L.n_true, L.hits, L.idx_next,
+                                      L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
+    } else if (L.idx_true) {  // the current query's own set: misses fetched into buffer p first
       rc = ckv_corrected_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale, L.k_src,
                               L.v_src, src_kind, L.idx_prev, L.n_sel_prev, k_buf[p],
                               v_buf[p], L.idx_true, L.n_true, L.hits, L.idx_next,

@@ -35,7 +35,7 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "make_layer", "to_u16", "generator",
-           "interleave_kv", "host_kv"]
+           "interleave_kv", "host_kv", "low_rank_factors"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -175,6 +175,24 @@ def make_layer(w: Workload, seed: int = 0, layer: int = 0,
                     k[b, h, pos] = rows.to(torch.bfloat16)
     return {"q": q, "q_sel": q_sel, "k": k, "v": v, "ctx_lens": lens,
             "marked": marked}
+
+
+def low_rank_factors(w: Workload, rank: int, seed: int = 0, layer: int = 0,
+                     device: str | torch.device = "cpu"):
+    """Low-rank key-cache factors of one layer: ``u`` [B][Hkv][max_ctx][rank]
+    with bf16(N(0,1)) entries and ``w`` [B][Hkv][rank][d] with
+    bf16(N(0,1) / sqrt(rank)) entries, so that a rebuilt key entry has about
+    unit variance like the drawn keys.  The factors are drawn independently of
+    the layer's keys: the rebuilt keys are not approximations of them, which
+    keeps a key that was rebuilt apart from one that was fetched."""
+    dev = torch.device(device)
+    B, Hkv, n, d = w.batch, w.kv_heads, w.max_ctx, w.head_dim
+    u = torch.empty((B, Hkv, n, rank), dtype=torch.bfloat16, device=dev)
+    wf = torch.empty((B, Hkv, rank, d), dtype=torch.bfloat16, device=dev)
+    _fill_normal_bf16(u, generator(w.name, seed, layer, f"lr_u{rank}", dev))
+    _fill_normal_bf16(wf, generator(w.name, seed, layer, f"lr_w{rank}", dev),
+                      1.0 / math.sqrt(rank))
+    return u, wf
 
 
 def interleave_kv(k: torch.Tensor, v: torch.Tensor) -> torch.Tensor:

@@ -108,6 +108,61 @@ def oracle_attn_over(shape_o, q_att, k_src, v_src, idx, n_sel, k):
     return o.sparse_decode_attn(shape_o, q_att, kb, vb, n_sel, k, SCALE, nthreads=8)
 
 
+def make_prediction(kind, S_att, S_sel, lens, k, max_ctx, rng):
+    """Host-made predicted sets [B][Hkv][k] (ascending, -1 padded) and counts."""
+    B, Hkv = S_att.shape[:2]
+    idx = np.full((B, Hkv, k), -1, np.int32)
+    cnt = np.zeros((B, Hkv), np.int32)
+    o = orc()
+    for b in range(B):
+        n = int(lens[b])
+        m = min(k, n)
+        for h in range(Hkv):
+            if kind == "speculative":
+                sel, mm = o.unit_select(S_sel[b, h, :n], k)
+                p = sel[:mm]
+            elif kind == "exact":
+                sel, mm = o.unit_select(S_att[b, h, :n], k)
+                p = sel[:mm]
+            elif kind == "disjoint":  # the lowest-scoring positions
+                p = np.sort(np.argsort(S_att[b, h, :n], kind="stable")[:m])
+            elif kind == "half":  # every other selected row replaced by an unselected one
+                sel, mm = o.unit_select(S_att[b, h, :n], k)
+                keep = sel[:mm][::2]
+                others = np.setdiff1d(np.arange(n), sel[:mm])
+                extra = rng.choice(others, size=min(mm - len(keep), len(others)), replace=False)
+                p = np.sort(np.concatenate([keep, extra]))
+            elif kind == "empty":
+                p = np.zeros(0, np.int64)
+            elif kind == "beyond":  # k distinct positions anywhere in the stored rows
+                p = np.sort(rng.choice(max_ctx, size=k, replace=False))
+            else:
+                raise KeyError(kind)
+            idx[b, h, :len(p)] = p
+            cnt[b, h] = len(p)
+    return idx, cnt
+
+
+def oracle_lowrank_buffers(shape_o, K, V, rank, u_fac, w_fac, idx_true, n_true, idx_pred,
+                           n_pred, k):
+    """The rows a layer with key reconstruction attends over, in idx_true
+    order: for a row of idx_true also in idx_pred (a hit) its stored key, for
+    a miss the key the oracle rebuilds from the factors; the stored value
+    either way.  Returns bf16 bit buffers kb, vb [B][Hkv][k][d]."""
+    B, Hkv, d = shape_o.batch, shape_o.num_kv_heads, shape_o.head_dim
+    rec = orc().reconstruct_keys(shape_o, rank, u_fac, w_fac, idx_true, n_true, k, fill=0)
+    kb = np.zeros((B, Hkv, k, d), np.uint16)
+    vb = np.zeros((B, Hkv, k, d), np.uint16)
+    for b in range(B):
+        for h in range(Hkv):
+            m = int(n_true[b, h])
+            rows = idx_true[b, h, :m]
+            hit = np.isin(rows, idx_pred[b, h, :max(0, min(int(n_pred[b, h]), k))])
+            kb[b, h, :m] = np.where(hit[:, None], K[b, h, rows], rec[b, h, :m])
+            vb[b, h, :m] = V[b, h, rows]
+    return kb, vb
+
+
 class Run:
     """Device buffers and one call of the fused entry point."""
 

@@ -33,7 +33,7 @@ def test_header_functions_are_exported():
 
 
 def test_abi_version_and_status_text():
-    assert ckv.abi_version() == 2
+    assert ckv.abi_version() == 3
     texts = {ckv.status_str(v) for v in STATUS.values()}
     assert len(texts) == len(STATUS)
     assert ckv.status_str(99) == "unknown status"
@@ -184,3 +184,49 @@ def test_dual_token_argument_checks():
     assert call(q_spec=None) == STATUS["EINVAL"]
     assert call(ws_bytes=need - 1) == STATUS["EWORKSPACE"]
     assert call(shape=good_shape(num_q_heads=32, num_kv_heads=2)) == STATUS["EUNSUPPORTED"]
+
+
+def test_reconstruct_argument_checks():
+    lib = ckv._lib
+    s = good_shape()
+
+    def rec(rank=8, u=FAKE, w=FAKE, k=16, dst=FAKE):
+        return lib.ckv_reconstruct_keys(ctypes.byref(s), rank, u, w, FAKE, FAKE, k, dst, None)
+
+    assert rec(rank=0) == STATUS["ESHAPE"]
+    assert rec(rank=ckv.MAX_RANK + 1) == STATUS["ESHAPE"]
+    assert rec(u=None) == STATUS["EINVAL"]
+    assert rec(w=FAKE + 2) == STATUS["EINVAL"]
+    assert rec(dst=None) == STATUS["EINVAL"]
+    assert rec(k=0) == STATUS["ESHAPE"]
+    need = ckv.workspace_bytes(s, 16, ckv.ENTRY_CORRECTED_ATTN)
+
+    def call(**kw):
+        args = dict(q_att=FAKE, q_sel=None, k_score=FAKE, lens=FAKE, k=16, scale=0.1,
+                    k_src=FAKE, v_src=FAKE, kind=0, rank=8, u=FAKE, w=FAKE, idx_pred=FAKE,
+                    n_pred=FAKE, k_buf=FAKE, v_buf=FAKE, idx_true=FAKE, n_true=FAKE,
+                    hits=FAKE, idx_next=FAKE, n_next=FAKE, out=FAKE, ws=FAKE, ws_bytes=need)
+        args.update(kw)
+        return lib.ckv_corrected_attn_lowrank(ctypes.byref(s), *args.values(), None)
+
+    assert call(rank=0) == STATUS["ESHAPE"]
+    assert call(u=None) == STATUS["EINVAL"]
+    assert call(w=None) == STATUS["EINVAL"]
+    assert call(v_src=None) == STATUS["EINVAL"]
+    # keys are rebuilt, so k_src may be NULL: the call gets as far as the workspace check
+    assert call(k_src=None, ws_bytes=need - 1) == STATUS["EWORKSPACE"]
+
+
+def test_layer_struct_layout(tmp_path):
+    """The ctypes mirror of ckv_layer has the C compiler's offsets."""
+    names = [n for n, _ in ckv.Layer._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stddef.h>\n#include <stdio.h>\n#include "ckv.h"\n'
+                   "int main(void) {\n" +
+                   "".join(f'  printf("%zu\\n", offsetof(ckv_layer, {n}));\n' for n in names) +
+                   '  printf("%zu\\n", sizeof(ckv_layer));\n  return 0;\n}\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    assert got == [getattr(ckv.Layer, n).offset for n in names] + [ctypes.sizeof(ckv.Layer)]

@@ -16,48 +16,14 @@ import torch
 
 import paper_2607_26475_amd as ckv
 import synth
-from helpers import (ATOL_OUT, SCALE, check_index_sets, device, oracle_attn_over, orc, u16)
+from helpers import (ATOL_OUT, SCALE, check_index_sets, device, make_prediction,
+                     oracle_attn_over, orc, u16)
 
 pytestmark = pytest.mark.gpu
 
 
 def _log(*a):
     print(*a, flush=True)
-
-
-def _prediction(kind, S_att, S_sel, lens, k, max_ctx, rng):
-    """Host-made predicted sets [B][Hkv][k] (ascending, -1 padded) and counts."""
-    B, Hkv = S_att.shape[:2]
-    idx = np.full((B, Hkv, k), -1, np.int32)
-    cnt = np.zeros((B, Hkv), np.int32)
-    o = orc()
-    for b in range(B):
-        n = int(lens[b])
-        m = min(k, n)
-        for h in range(Hkv):
-            if kind == "speculative":
-                sel, mm = o.unit_select(S_sel[b, h, :n], k)
-                p = sel[:mm]
-            elif kind == "exact":
-                sel, mm = o.unit_select(S_att[b, h, :n], k)
-                p = sel[:mm]
-            elif kind == "disjoint":  # the lowest-scoring positions
-                p = np.sort(np.argsort(S_att[b, h, :n], kind="stable")[:m])
-            elif kind == "half":  # every other selected row replaced by an unselected one
-                sel, mm = o.unit_select(S_att[b, h, :n], k)
-                keep = sel[:mm][::2]
-                others = np.setdiff1d(np.arange(n), sel[:mm])
-                extra = rng.choice(others, size=min(mm - len(keep), len(others)), replace=False)
-                p = np.sort(np.concatenate([keep, extra]))
-            elif kind == "empty":
-                p = np.zeros(0, np.int64)
-            elif kind == "beyond":  # k distinct positions anywhere in the stored rows
-                p = np.sort(rng.choice(max_ctx, size=k, replace=False))
-            else:
-                raise KeyError(kind)
-            idx[b, h, :len(p)] = p
-            cnt[b, h] = len(p)
-    return idx, cnt
 
 
 CASES = [
@@ -84,7 +50,7 @@ def test_corrected_attn(wl, kind, src_kind):
     so = o.shape(B, Hq, Hkv, d, n)
     S_att = o.score_keys(so, q_att, K, lens_h, SCALE, nthreads=8)
     S_sel = o.score_keys(so, q_sel, K, lens_h, SCALE, nthreads=8)
-    pred, npred = _prediction(kind, S_att, S_sel, lens_h, k, n, np.random.default_rng(7))
+    pred, npred = make_prediction(kind, S_att, S_sel, lens_h, k, n, np.random.default_rng(7))
 
     if src_kind == ckv.SRC_HOST_PINNED:
         kv = synth.host_kv(t["k"], t["v"])

@@ -16,7 +16,8 @@ import torch
 
 import paper_2607_26475_amd as ckv
 import synth
-from helpers import (ATOL_OUT, SCALE, check_index_sets, device, oracle_attn_over, orc, u16)
+from helpers import (ATOL_OUT, SCALE, check_index_sets, device, oracle_attn_over,
+                     oracle_lowrank_buffers, orc, u16)
 
 pytestmark = pytest.mark.gpu
 
@@ -58,6 +59,7 @@ class Loop:
         self.nsel = [mn(), mn()]
         self.out = [torch.full((B, Hq, d), float("nan"), device=dev) for _ in range(layers)]
         self.corrected = False
+        self.lowrank = {}  # layer -> (rank, u_fac, w_fac): misses' keys rebuilt
         self.idx_true = mk()
         self.n_true = mn()
         self.hits = mn()
@@ -80,7 +82,11 @@ class Loop:
                  "out": self.out[l],
                  "idx_true": self.idx_true[l] if self.corrected else None,
                  "n_true": self.n_true[l] if self.corrected else None,
-                 "hits": self.hits[l] if self.corrected else None} for l in range(self.L)]
+                 "hits": self.hits[l] if self.corrected else None,
+                 "lr_rank": self.lowrank[l][0] if l in self.lowrank else 0,
+                 "lr_u": self.lowrank[l][1] if l in self.lowrank else None,
+                 "lr_w": self.lowrank[l][2] if l in self.lowrank else None}
+                for l in range(self.L)]
 
     def bootstrap(self):
         """Selection before the first step (the pre-decoding step), into set 0."""
@@ -186,18 +192,25 @@ def test_pipeline_ordering_under_delay(stream_name):
             np.testing.assert_array_equal(ro[l], go[l])
 
 
-@pytest.mark.parametrize("wl,layers", [("dual64_s", 3), ("long128k_s", 2)])
-def test_pipeline_corrected_matches_oracle(wl, layers):
+@pytest.mark.parametrize("wl,layers,lowrank", [("dual64_s", 3, ()), ("long128k_s", 2, ()),
+                                               ("dual64_s", 3, (1,))])
+def test_pipeline_corrected_matches_oracle(wl, layers, lowrank):
     """Corrected layers in the decode loop: whatever was prefetched from the
     previous step's speculative selection, each layer's output is the current
     query's attention over its own top-k (the same-step result), the misses
     against the prefetched set are counted in hits, and the speculative
-    selection for the next step is made as before."""
-    _log("pipeline corrected", wl, layers)
+    selection for the next step is made as before.  Layers in `lowrank`
+    rebuild their misses' keys (Sec. 5.3, adaptive key reconstruction): they
+    attend over the prefetched keys of the hits and the rebuilt keys of the
+    misses."""
+    _log("pipeline corrected", wl, layers, lowrank)
     dev = device()
     w = synth.WORKLOADS[wl]
     lp = Loop(w, layers, steps=2, seed=11, dev=dev)
     lp.corrected = True
+    rank = 32
+    for l in lowrank:
+        lp.lowrank[l] = (rank,) + synth.low_rank_factors(w, rank, seed=11, layer=l, device=dev)
     lp.bootstrap()
     boot = [i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]]
     pipe = ckv.Pipeline()
@@ -227,7 +240,14 @@ def test_pipeline_corrected_matches_oracle(wl, layers):
                     assert g_hits[l][b, h] == want, (st, l, b, h)
                     total += len(t_)
                     found += want
-            ref = oracle_attn_over(so, q_att, K, V, g_true[l], g_ntrue[l], w.k)
+            if l in lp.lowrank:
+                kb, vb = oracle_lowrank_buffers(so, K, V, rank, u16(lp.lowrank[l][1]),
+                                                u16(lp.lowrank[l][2]), g_true[l], g_ntrue[l],
+                                                prev_pred[0][l], prev_pred[1][l], w.k)
+                ref = o.sparse_decode_attn(so, q_att, kb, vb, g_ntrue[l], w.k, SCALE,
+                                           nthreads=8)
+            else:
+                ref = oracle_attn_over(so, q_att, K, V, g_true[l], g_ntrue[l], w.k)
             err = np.abs(g_out[l] - ref).max()
             _log(f"  step {st} layer {l}: hit rate {found / max(total, 1):.3f}, "
                  f"max abs err {err:.2e}")
