@@ -427,8 +427,10 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
     t+1 plus 0.6 x noise (the dual workload's recipe).  Two runs over the same
     inputs: attention over the prefetched prediction, and with miss correction
     (each layer attends over its own query's set, misses fetched on the compute
-    stream).  Step time from events on the compute stream after it has joined
-    the copy stream."""
+    stream); a third run rebuilds the misses' keys in every layer from rank-32
+    factors (per (request, KV head), one set per host layer) and fetches only
+    their values.  Step time from events on the compute stream after it has
+    joined the copy stream."""
     w = synth.WORKLOADS["long128k"]
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
@@ -467,7 +469,10 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
     sc = torch.empty((B, Hkv, n), device=dev)
     wsel = ckv.workspace(s1, k, ckv.ENTRY_SELECT_TOPK)
 
-    def run(corrected):
+    lr_rank = 32
+    lr = []
+
+    def run(corrected, lowrank=False):
         def io(step, cur):
             return [{"q_att": q[step][l], "q_sel": qs[step][l], "k_score": kscore[l % n_hbm],
                      "k_src": hosts[l % n_host].data_ptr(),
@@ -477,7 +482,10 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
                      "out": out[l],
                      "idx_true": idx_true[l] if corrected else None,
                      "n_true": n_true[l] if corrected else None,
-                     "hits": hits[step][l] if corrected else None} for l in range(L)]
+                     "hits": hits[step][l] if corrected else None,
+                     "lr_rank": lr_rank if lowrank else 0,
+                     "lr_u": lr[l % n_host][0] if lowrank else None,
+                     "lr_w": lr[l % n_host][1] if lowrank else None} for l in range(L)]
 
         # bootstrap selection (the pre-decoding step) into set 0
         for l in range(L):
@@ -513,12 +521,15 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
                "host_bytes_per_step": host_bytes,
                "host_GBps_step": host_bytes / (ms * 1e-3) / 1e9,
                "gather_ms_per_step": gather_ms, "compute_kernels_ms_per_step": compute_ms,
+               "kernels_ms_per_step": {kname: round(v[1] / steps, 4)
+                                       for kname, v in stats.items()},
                "overlap": (gather_ms + compute_ms) / ms}
         if corrected:  # the misses cross the link too, on the compute stream
             found = sum(int(hits[st][l].sum()) for st in range(1, steps + 1) for l in range(L))
             total = steps * L * B * Hkv * min(k, n)
             res["hit_rate"] = found / total
-            res["miss_bytes_per_step"] = (total - found) / steps * 2 * d * 2
+            # a rebuilt miss fetches its value only
+            res["miss_bytes_per_step"] = (total - found) / steps * (1 if lowrank else 2) * d * 2
             res["host_bytes_per_step"] = host_bytes + res["miss_bytes_per_step"]
             res["host_GBps_step"] = res["host_bytes_per_step"] / (ms * 1e-3) / 1e9
         if host_link:
@@ -530,7 +541,11 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
                        "context 131072, k 4096; K|V rows host-pinned, scoring keys in HBM; "
                        "4 HBM and 2 host layers cycled")
     res["corrected"] = run(True)
-    del hosts
+    for i in range(n_host):
+        lr.append(synth.low_rank_factors(w, lr_rank, seed=0, layer=i, device=dev))
+    res["corrected_lowrank"] = run(True, lowrank=True)
+    res["corrected_lowrank"]["rank"] = lr_rank
+    del hosts, lr
     return res
 
 
