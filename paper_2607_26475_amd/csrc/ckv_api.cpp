@@ -2,6 +2,7 @@
 // the launch sequences of each entry point.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -107,7 +108,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // start of every selecting call.
 struct Layout {
   size_t hist = 0, coarse = 0, ctrl = 0, hist2 = 0, coarse2 = 0, ctrl2 = 0, zero_end = 0;
-  size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0;
+  size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0, hist_part = 0, hist_part_bytes = 0;
   size_t slot_of = 0, miss_pos = 0, miss_slot = 0, n_miss = 0, free_slot = 0, total = 0;
   int64_t bm_words = 0;
   int chunks = 0, filter_tiles = 0;
@@ -155,6 +156,11 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
   if (entry == CKV_ENTRY_CRITICAL_KV_ATTN || corrected) {
     L.scores = off;
     off = align256(off + U * (size_t)d.max_ctx * 4);
+    // per-workgroup histograms of the scoring pass (slots unit + workgroup)
+    const int64_t groups = (int64_t)U * ((d.max_ctx + kStageRows - 1) / kStageRows);
+    L.hist_part = off;
+    L.hist_part_bytes = (U + (size_t)std::min<int64_t>(groups, kMaxScoreWgs)) * kHistBins * 4;
+    off = align256(off + L.hist_part_bytes);
   }
   if (attn) {
     L.part = off;
@@ -266,6 +272,9 @@ SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* sc
   a.k = k;
   a.tiles = L.filter_tiles;
   a.chunk = 1;
+  a.hist_part = nullptr;
+  a.score_nwg = 0;
+  a.units = d.U;
   return a;
 }
 
@@ -286,6 +295,7 @@ ScoreArgs score_args(const Dims& d, const Layout& L, const uint16_t* q,
   a.max_ctx = d.max_ctx;
   a.units = d.U;
   a.chunk = 1;
+  a.hist_part = nullptr;
   return a;
 }
 
@@ -318,6 +328,24 @@ AttnArgs attn_args(const Dims& d, const Layout& L, void* ws, const uint16_t* q,
 // Selection given scores and a filled first-digit histogram: one workgroup
 // per unit for contexts that fit its LDS, else the many-workgroup filter
 // followed by the per-unit finish.
+// The scoring pass leaves per-workgroup histograms (stored, so no clearing
+// and no atomics) when the fused selection reads them and no unit needs more
+// than kMaxPartials of them; then the call has nothing to clear.  Otherwise
+// the histograms are added into cleared per-unit counts.
+bool use_partials(const Dims& d, const Layout& L, int nwg) {
+  if (!L.hist_part_bytes || d.max_ctx > kFusedSelectMaxCtx || nwg < 1) return false;
+  // a unit's gu groups meet at most ceil(gu / shortest range) + 1 ranges
+  const int64_t gu = (d.max_ctx + kStageRows - 1) / kStageRows;
+  const int64_t shortest = gu * d.U / nwg;
+  return shortest >= 1 && (gu + shortest - 1) / shortest + 1 <= kMaxPartials;
+}
+
+void set_partials(void* ws, const Layout& L, int nwg, ScoreArgs* sc, SelectArgs* sa) {
+  sc->hist_part = at<uint32_t>(ws, L.hist_part);
+  sa->hist_part = sc->hist_part;
+  sa->score_nwg = nwg;
+}
+
 int run_select_tail(const SelectArgs& a, int units, hipStream_t s) {
   if (a.max_ctx <= kFusedSelectMaxCtx) {
     CKV_TRY_HIP(launch_select_fused(a, units, s), "select launch");
@@ -354,7 +382,11 @@ int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
   ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, sa.hist,
                             sa.coarse);
   sc.chunk = chunk;
-  CKV_TRY_HIP(launch_zero(ws, Lc.zero_end, s), "zero launch");
+  const int nwg = score_blocks(sc, d.G, false, false);
+  if (use_partials(dc, Lc, nwg))
+    set_partials(ws, Lc, nwg, &sc, &sa);
+  else
+    CKV_TRY_HIP(launch_zero(ws, Lc.zero_end, s), "zero launch");
   CKV_TRY_HIP(launch_score(sc, d.G, true, d.U, s), "score launch");
   if ((rc = run_select_tail(sa, d.U, s))) return rc;
   ExpandArgs e;
@@ -540,7 +572,11 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   float* scores = at<float>(ws, L.scores);
   SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
   ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, sa.hist, sa.coarse);
-  CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
+  const int nwg = score_blocks(sc, d.G, pipelined, false);
+  if (use_partials(d, L, nwg))
+    set_partials(ws, L, nwg, &sc, &sa);
+  else
+    CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
   if (pipelined) {
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel_in, kD, k,
                              scale, out);
@@ -732,10 +768,25 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   if (d.U == 0) return CKV_OK;
   hipStream_t s = (hipStream_t)stream;
   float* scores = at<float>(ws, L.scores);
-  CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
   // 1. the current token's own selection
   SelectArgs s1 = select_args(d, L, ws, scores, ctx_lens, k, idx_true, n_true);
   ScoreArgs c1 = score_args(d, L, q_att, k_score, ctx_lens, scale, scores, s1.hist, s1.coarse);
+  // the next step's selection (4. below) is scored by the dual kernel
+  SelectArgs s2 = select_args(d, L, ws, scores, ctx_lens, k, idx_next, n_next);
+  s2.hist = at<uint32_t>(ws, L.hist2);
+  s2.coarse = at<uint32_t>(ws, L.coarse2);
+  s2.ctrl = at<uint32_t>(ws, L.ctrl2);
+  ScoreArgs c2 = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, s2.hist, s2.coarse);
+  const int nwg1 = score_blocks(c1, d.G, false, false);
+  const int nwg2 = score_blocks(c2, d.G, true, true);
+  if (use_partials(d, L, nwg1) && use_partials(d, L, nwg2)) {
+    // both selections use the slots in turn: the first reads them before the
+    // dual launch writes them again
+    set_partials(ws, L, nwg1, &c1, &s1);
+    set_partials(ws, L, nwg2, &c2, &s2);
+  } else {
+    CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
+  }
   CKV_TRY_HIP(launch_score(c1, d.G, true, d.U, s), "score launch");
   if ((rc = run_select_tail(s1, d.U, s))) return rc;
   // 2. hits and misses against the predicted set; misses into free slots
@@ -773,11 +824,6 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   }
   // 3. attention over exactly the selected rows, now all in the buffer (read
   //    through the slot list), in one launch with 4. the next step's scoring
-  SelectArgs s2 = select_args(d, L, ws, scores, ctx_lens, k, idx_next, n_next);
-  s2.hist = at<uint32_t>(ws, L.hist2);
-  s2.coarse = at<uint32_t>(ws, L.coarse2);
-  s2.ctrl = at<uint32_t>(ws, L.ctrl2);
-  ScoreArgs c2 = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, s2.hist, s2.coarse);
   // the buffer as an indexed source: unit u's slot r is row r of [U][k][d]
   Dims db = d;
   db.max_ctx = k;

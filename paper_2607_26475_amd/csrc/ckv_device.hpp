@@ -35,6 +35,14 @@ constexpr int kBitmapLdsBits = kFinishLdsBytes * 8;
 // Contexts up to this many positions are selected by one workgroup per unit
 // in a single kernel (scores read once, everything else in LDS).
 constexpr int kFusedSelectMaxCtx = 65536;
+// Scoring grids are capped at kMaxScoreWgs workgroups.  With per-workgroup
+// histograms (ScoreArgs::hist_part) the histogram of unit u is the sum of the
+// slots u + wg over the workgroups wg whose range meets the unit; slot u + wg
+// is unique because ranges and units are both in group order.  The selection
+// reads at most kMaxPartials slots per unit, else the histograms are added
+// with atomics.
+constexpr int kMaxScoreWgs = 1024;
+constexpr int kMaxPartials = 8;
 
 // Attention: one workgroup reduces kAttnRows gathered rows of one unit into a
 // partial (running max, sum of weights, weighted V) per query head; each of
@@ -58,6 +66,8 @@ struct ScoreArgs {
   float* scores;            // [U][max_ctx]
   uint32_t* hist;           // [U][kHistBins] or nullptr
   uint32_t* coarse;         // [U][kCoarseBins]
+  uint32_t* hist_part;      // non-null: per-workgroup histograms instead,
+                            //   [U + kMaxScoreWgs][kHistBins], stored not added
   int64_t key_stride;
   float scale;
   int Hq, Hkv, max_ctx, units;
@@ -70,6 +80,9 @@ struct SelectArgs {
   uint32_t* hist;           // [U][kHistBins]
   uint32_t* coarse;         // [U][kCoarseBins]
   uint32_t* ctrl;           // [U][kCtrlWords]
+  const uint32_t* hist_part;  // non-null: the scoring pass wrote per-workgroup
+  int score_nwg;            //   histograms with a grid of score_nwg workgroups
+  int units;
   int32_t* sel;             // [U][k]   positions above the digit-1 bin, then
                             //          the chosen candidates
   uint2* cand;              // [U][max_ctx] (order key, position)
@@ -176,6 +189,12 @@ __device__ __forceinline__ int unit_len(int n_rows, int hi, int chunk) {
 
 __device__ __forceinline__ int clamp_len(int n, int hi) {
   return n < 0 ? 0 : (n > hi ? hi : n);
+}
+
+// Workgroup of the balanced split of T groups over nwg workgroups (range
+// [wg*T/nwg, (wg+1)*T/nwg)) that holds group g.
+__host__ __device__ __forceinline__ int64_t range_owner(int64_t g, int64_t T, int64_t nwg) {
+  return ((g + 1) * nwg - 1) / T;
 }
 
 // Monotone map from fp32 to uint32: a < b as floats <=> key(a) < key(b);

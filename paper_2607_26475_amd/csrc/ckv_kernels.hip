@@ -358,13 +358,31 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
     if (tid == 0) a.n_sel[unit] = m;
     return;
   }
-  // the first batch of scores is in flight while wave 0 finds the bin
   const float* srow = a.scores + (int64_t)unit * a.max_ctx;
   float sv0[kSelPer];
-  load_score_batch(srow, 0, n, sv0);
-  if (tid < 64)
-    find_first_bin_fine(a.hist + (int64_t)unit * kHistBins, (uint32_t)m, lhist, misc + 4);
-  if (tid == 64) misc[7] = 0u;
+  if (a.hist_part) {
+    // the slots unit + wg of the workgroups that scored the unit's groups:
+    // every thread sums two bins of them into LDS, the histogram loads
+    // issued before the first batch of scores
+    const int64_t gu = (a.max_ctx + kStageRows - 1) / kStageRows;
+    const int64_t T = gu * a.units, g0 = (int64_t)unit * gu;
+    const int64_t lo = range_owner(g0, T, a.score_nwg);
+    const int64_t hi = range_owner(g0 + (n + kStageRows - 1) / kStageRows - 1, T, a.score_nwg);
+    const int nslots = (int)min<int64_t>(hi - lo + 1, kMaxPartials);  // the host keeps it below
+    uint2 hv[kMaxPartials];
+    load_hist_slots(a.hist_part + (unit + lo) * kHistBins, nslots, hv);
+    load_score_batch(srow, 0, n, sv0);
+    store_hist_sum(hv, nslots, lhist);
+    if (tid == 64) misc[7] = 0u;
+    __syncthreads();
+    if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
+  } else {
+    // the first batch of scores is in flight while wave 0 finds the bin
+    load_score_batch(srow, 0, n, sv0);
+    if (tid < 64)
+      find_first_bin_fine(a.hist + (int64_t)unit * kHistBins, (uint32_t)m, lhist, misc + 4);
+    if (tid == 64) misc[7] = 0u;
+  }
   __syncthreads();
   const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
   const uint32_t b1 = misc[4], above = misc[5];
@@ -817,8 +835,28 @@ static int resident_blocks(const void* fn) {
 
 static int score_grid(const ScoreArgs& a, const void* fn) {
   const int64_t groups = (int64_t)a.units * ((a.max_ctx + kStageRows - 1) / kStageRows);
-  const int64_t slots = resident_blocks(fn);
+  int64_t slots = resident_blocks(fn);
+  if (slots > kMaxScoreWgs) slots = kMaxScoreWgs;
   return (int)(groups < slots ? groups : slots);
+}
+
+template <int G>
+static int score_blocks_g(const ScoreArgs& a, bool dual, bool indexed) {
+  const void* fn = dual ? (indexed ? (const void*)k_dual<G, true> : (const void*)k_dual<G, false>)
+                        : (a.chunk > 1 ? (const void*)k_score_chunks<G>
+                                       : (const void*)k_score<G, true>);
+  return score_grid(a, fn);
+}
+
+int score_blocks(const ScoreArgs& a, int G, bool dual, bool indexed) {
+  switch (G) {
+    case 1: return score_blocks_g<1>(a, dual, indexed);
+    case 2: return score_blocks_g<2>(a, dual, indexed);
+    case 4: return score_blocks_g<4>(a, dual, indexed);
+    case 8: return score_blocks_g<8>(a, dual, indexed);
+    case 16: return score_blocks_g<16>(a, dual, indexed);
+    default: return 0;
+  }
 }
 
 template <int G>

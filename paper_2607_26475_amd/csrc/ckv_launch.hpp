@@ -7,6 +7,9 @@ namespace ckv {
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s);
+// workgroups of the scoring pass (with a histogram) or of the dual kernel's
+// scoring role for these arguments: the grid the launchers use
+int score_blocks(const ScoreArgs& a, int G, bool dual, bool indexed);
 hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s);

@@ -40,13 +40,25 @@ __device__ __forceinline__ void flush_hist(const uint32_t* lds_hist,
   if ((t & 3) == 0 && csum) atomicAdd(&g_coarse[t >> 2], csum);
 }
 
+// Stores the workgroup's LDS histogram as its slot (kScoreThreads threads).
+__device__ __forceinline__ void store_hist(const uint32_t* lds_hist, uint32_t* slot) {
+  constexpr int kPer = kHistBins / kScoreThreads;
+  static_assert(kPer % 4 == 0, "16-byte stores");
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < kPer; i += 4)
+    *reinterpret_cast<uint4*>(slot + kPer * t + i) =
+        *reinterpret_cast<const uint4*>(lds_hist + kPer * t + i);
+}
+
 // Scores a balanced share of the whole batch: the positions of every unit are
 // cut into groups of kStageRows keys, the groups of all units are numbered
 // unit-major, and workgroup `wg` of `nwg` takes the contiguous range
 // [wg*T/nwg, (wg+1)*T/nwg) of the T groups.  A range spans few units; for each
 // unit it touches the workgroup loads that unit's G query rows once and, if
-// HIST, counts the first radix digit of its scores in LDS and adds the counts
-// to the unit's histogram when it leaves the unit.  Groups at or beyond n_b
+// HIST, counts the first radix digit of its scores in LDS and, when it leaves
+// the unit, adds the counts to the unit's histogram or stores them as its own
+// slot (hist_part).  Groups at or beyond n_b
 // only write -inf.  Must be called by all kScoreThreads threads.
 //
 // Memory path: the four waves take the range's groups round-robin (wave w
@@ -203,8 +215,11 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
       if (nb) flush(first, nb);
       if (HIST) {
         __syncthreads();
-        flush_hist(lds_hist, a.hist + (int64_t)unit * kHistBins,
-                   a.coarse + (int64_t)unit * kCoarseBins);
+        if (a.hist_part)
+          store_hist(lds_hist, a.hist_part + ((int64_t)unit + wg) * kHistBins);
+        else
+          flush_hist(lds_hist, a.hist + (int64_t)unit * kHistBins,
+                     a.coarse + (int64_t)unit * kCoarseBins);
         __syncthreads();
       }
     }

@@ -43,6 +43,55 @@ __device__ __forceinline__ void find_first_bin(const uint32_t* coarse,
   }
 }
 
+// Wave 0: lane l holds the count c of coarse range cb = 63 - l, whose 32 fine
+// bins are at stage[cb*32 ..]; finds the bin holding the m-th largest key.
+// out[0] = bin, out[1] = keys in higher bins, out[2] = keys in the bin.
+__device__ __forceinline__ void walk_first_bin(const uint32_t* stage, int cb, uint32_t c,
+                                               uint32_t m, uint32_t* out) {
+  constexpr int kFine = kHistBins / 64;
+  const int lane = threadIdx.x & 63;
+  const uint32_t s = wave_incl_scan(c);
+  int L = __ffsll((unsigned long long)__ballot(s >= m)) - 1;
+  if (L < 0) L = 63;  // only if the histogram were inconsistent
+  if (lane == L) {
+    const uint32_t* f = stage + cb * kFine;
+    uint32_t run = s - c;
+    int i = kFine - 1;
+    while (i > 0 && run + f[i] < m) run += f[i--];
+    out[0] = (uint32_t)(cb * kFine + i);
+    out[1] = run;
+    out[2] = f[i];
+  }
+}
+
+// All kFinishThreads threads: the first-digit histogram is the sum of nslots
+// (1 .. kMaxPartials) consecutive slots of kHistBins counts.  Every thread
+// loads its two bins of every slot at once (one round trip; slots past nslots
+// repeat slot 0 and are not added) ...
+__device__ __forceinline__ void load_hist_slots(const uint32_t* hist, int nslots,
+                                                uint2 (&v)[kMaxPartials]) {
+  static_assert(2 * kFinishThreads == kHistBins, "two bins per thread");
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int p = 0; p < kMaxPartials; ++p)
+    v[p] = *reinterpret_cast<const uint2*>(hist + (int64_t)(p < nslots ? p : 0) * kHistBins +
+                                           2 * t);
+}
+
+// ... and stores the sums to lhist (LDS); the caller synchronises before
+// reading it.
+__device__ __forceinline__ void store_hist_sum(const uint2 (&v)[kMaxPartials], int nslots,
+                                               uint32_t* lhist) {
+  uint2 acc = make_uint2(0u, 0u);
+#pragma unroll
+  for (int p = 0; p < kMaxPartials; ++p)
+    if (p < nslots) {
+      acc.x += v[p].x;
+      acc.y += v[p].y;
+    }
+  *reinterpret_cast<uint2*>(lhist + 2 * threadIdx.x) = acc;
+}
+
 // Wave 0 only, from the fine histogram alone in one round trip: lane l reads
 // the 32 bins of coarse range 63 - l (ranges in descending order) and copies
 // them to stage[] (2048 words of LDS); the lane whose range holds the m-th
@@ -63,18 +112,21 @@ __device__ __forceinline__ void find_first_bin_fine(const uint32_t* hist, uint32
     c += v.x + v.y + v.z + v.w;
     dst[i] = v;
   }
-  const uint32_t s = wave_incl_scan(c);
-  int L = __ffsll((unsigned long long)__ballot(s >= m)) - 1;
-  if (L < 0) L = 63;  // only if the histogram were inconsistent
-  if (lane == L) {
-    const uint32_t* f = stage + cb * kFine;
-    uint32_t run = s - c;
-    int i = kFine - 1;
-    while (i > 0 && run + f[i] < m) run += f[i--];
-    out[0] = (uint32_t)(cb * kFine + i);
-    out[1] = run;
-    out[2] = f[i];
+  walk_first_bin(stage, cb, c, m, out);
+}
+
+// The same from a histogram already in LDS (lhist).
+__device__ __forceinline__ void find_first_bin_lds(const uint32_t* lhist, uint32_t m,
+                                                   uint32_t* out) {
+  constexpr int kFine = kHistBins / 64;
+  const int cb = 63 - (threadIdx.x & 63);
+  uint32_t c = 0u;
+#pragma unroll
+  for (int i = 0; i < kFine / 4; ++i) {
+    const uint4 v = reinterpret_cast<const uint4*>(lhist + cb * kFine)[i];
+    c += v.x + v.y + v.z + v.w;
   }
+  walk_first_bin(lhist, cb, c, m, out);
 }
 
 // All threads of a kFinishThreads workgroup: given a histogram of nb bins in
