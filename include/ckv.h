@@ -374,7 +374,16 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
  * step's layers 0 and 1 from this step's idx_next.  Before the next step the
  * caller swaps idx_prev and idx_next.  ws is the workspace of
  * CKV_ENTRY_CRITICAL_KV_ATTN, or of CKV_ENTRY_CORRECTED_ATTN if any layer
- * has idx_true set, used on the compute stream only. */
+ * has idx_true set, used on the compute stream only.
+ *
+ * Steps can be captured into a HIP graph on compute_stream (whole steps: the
+ * copy stream joins the capture at its first wait and the caller joins it
+ * back before the capture ends).  A fill recorded outside the capture (by
+ * the prime or an eager step) is not waited for inside it, so the caller
+ * orders each launch of the graph after the copy stream's earlier work
+ * (e.g. compute_stream waits for copy_stream before the first launch); a
+ * graph of an even number of layers leaves the buffers as it found them
+ * for its next launch. */
 int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                     const ckv_layer* layers, const int32_t* ctx_lens, int32_t k,
                     float scale, int src_kind, uint16_t* const k_buf[2],

@@ -9,10 +9,19 @@
 struct ckv_pipeline {
   hipEvent_t filled[2];  // buffer i holds the rows of the layer about to use it
   hipEvent_t freed[2];   // the attention that read buffer i has been enqueued before this
+  unsigned long long filled_capture[2];  // capture filled[i] was last recorded in (0: none)
   int parity;            // buffer of the next layer to compute
 };
 
 namespace {
+
+// Id of the stream capture s takes part in, 0 if it is not capturing.
+unsigned long long capture_id(hipStream_t s) {
+  hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+  unsigned long long id = 0;
+  if (hipStreamGetCaptureInfo(s, &st, &id) != hipSuccess) return 0;
+  return st == hipStreamCaptureStatusActive ? id : 0;
+}
 
 int gather_layer(const ckv_shape* shape, int32_t k, const ckv_layer& L, const int32_t* idx,
                  const int32_t* n_sel, int src_kind, uint16_t* kb, uint16_t* vb,
@@ -36,6 +45,7 @@ int ckv_pipeline_create(ckv_pipeline** pipe) {
     }
   }
   p->parity = 0;
+  p->filled_capture[0] = p->filled_capture[1] = 0;
   *pipe = p;
   return CKV_OK;
 }
@@ -62,6 +72,7 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
     if (rc) return rc;
     if (hipEventRecord(pipe->filled[l], (hipStream_t)copy_stream) != hipSuccess)
       return CKV_EHIP;
+    pipe->filled_capture[l] = capture_id((hipStream_t)copy_stream);
   }
   return CKV_OK;
 }
@@ -73,11 +84,15 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                     void* compute_stream, void* copy_stream) {
   if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf) return CKV_EINVAL;
   hipStream_t cs = (hipStream_t)compute_stream, xs = (hipStream_t)copy_stream;
+  const unsigned long long capture = capture_id(cs);
   for (int l = 0; l < num_layers; ++l) {
     const int p = pipe->parity;
     const ckv_layer& L = layers[l];
-    // attention over buffer p once its gather has landed
-    if (hipStreamWaitEvent(cs, pipe->filled[p], 0) != hipSuccess) return CKV_EHIP;
+    // attention over buffer p once its gather has landed.  Under stream
+    // capture a fill recorded outside this capture cannot be waited for;
+    // the graph is then ordered after it by its launch.
+    if (!capture || pipe->filled_capture[p] == capture)
+      if (hipStreamWaitEvent(cs, pipe->filled[p], 0) != hipSuccess) return CKV_EHIP;
     int rc;
     if (L.idx_true && L.lr_rank > 0) {  // misses: keys rebuilt, values fetched
       rc = ckv_corrected_attn_lowrank(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
@@ -111,6 +126,7 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     }
     if (rc) return rc;
     if (hipEventRecord(pipe->filled[p], xs) != hipSuccess) return CKV_EHIP;
+    pipe->filled_capture[p] = capture;
     pipe->parity ^= 1;
   }
   return CKV_OK;
