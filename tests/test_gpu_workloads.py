@@ -205,3 +205,90 @@ def test_full_million_layer_sampled():
     _check_units(w, t, g_idx, g_nsel, g_out, units,
                  lambda b, h, s_: kv_host[b, h, torch.from_numpy(s_), 0],
                  lambda b, h, s_: kv_host[b, h, torch.from_numpy(s_), 1])
+
+
+def test_full_dual64_pipelined_sampled():
+    """The full-size dual-token workload (B64, n_b ~ U{16384..65536}, k 2048,
+    K|V host-pinned) through the pipelined fused entry, as a serving step
+    runs it: the set selected from q2 one step earlier is gathered over the
+    host link, then one launch attends with q1 over it while scoring q2 for
+    the next step.  Sampled units against the oracle."""
+    _log("full dual64 pipelined")
+    dev = device()
+    w = synth.WORKLOADS["dual64"]
+    t = synth.make_layer(w, seed=0, layer=0, device=dev)
+    kv_host = synth.host_kv(t["k"], t["v"])
+    del t["v"]
+    torch.cuda.empty_cache()
+    d = w.head_dim
+    lens = t["ctx_lens"]
+    s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
+    # step t-1: the selection from q2
+    prev = Run(w, lens, dev)
+    scores = torch.empty((w.batch, w.kv_heads, w.max_ctx), device=dev)
+    ckv.score_keys(s, t["q_sel"], t["k"], lens, SCALE, scores)
+    ws = ckv.workspace(s, w.k, ckv.ENTRY_SELECT_TOPK)
+    ckv.select_topk(s, scores, lens, w.k, prev.idx, prev.n_sel, ws)
+    del scores, ws
+    s_kv = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx, kv_row_stride=2 * d)
+    k_buf = torch.empty((w.batch, w.kv_heads, w.k, d), dtype=torch.bfloat16, device=dev)
+    v_buf = torch.empty_like(k_buf)
+    ckv.gather_kv(s_kv, kv_host.data_ptr(), kv_host.data_ptr() + 2 * d, ckv.SRC_HOST_PINNED,
+                  prev.idx, prev.n_sel, w.k, k_buf, v_buf)
+    # step t: attention (q1) over the buffer and scoring (q2) in one launch
+    cur = Run(w, lens, dev)
+    cur.pipelined(t["q"], t["q_sel"], t["k"], k_buf, v_buf, prev.n_sel)
+    p_idx, p_nsel, _ = prev.host()
+    c_idx, c_nsel, c_out = cur.host()
+    np.testing.assert_array_equal(c_idx, p_idx)  # step-invariant queries
+    np.testing.assert_array_equal(c_nsel, p_nsel)
+    assert np.all(np.isfinite(c_out))
+    units = _sampled_units(w, 6, seed=3)
+    _check_units(w, t, c_idx, c_nsel, c_out, units,
+                 lambda b, h, s_: kv_host[b, h, torch.from_numpy(s_), 0],
+                 lambda b, h, s_: kv_host[b, h, torch.from_numpy(s_), 1])
+
+
+def test_full_long128k_decode_step_sampled():
+    """The full-size long-context workload (B8, n 131072, k 4096, K|V
+    host-pinned) through the two-buffer decode loop over two layers, the
+    launch configuration of the benchmark's pipeline: each layer attends with
+    this step's query over the set its speculative query selected a step
+    earlier, gathered on the copy stream.  Sampled units against the oracle."""
+    from test_gpu_pipeline import Loop
+
+    _log("full long128k decode step")
+    dev = device()
+    w = synth.WORKLOADS["long128k"]
+    lp = Loop(w, 2, steps=1, seed=4, dev=dev)
+    lp.bootstrap()
+    boot = [i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]]
+    pipe = ckv.Pipeline()
+    hist = lp.run(1, pipe)
+    pipe.close()
+    g_idx, g_nsel, g_out = hist[0][:3]
+    o = orc()
+    G = w.group
+    lens = lp.lens.cpu().numpy()
+    for l in range(2):
+        q_att = u16(lp.q_att[1][l])
+        q_sel = u16(lp.q_sel[1][l])
+        for b, h in _sampled_units(w, 3, seed=5 + l):
+            n = int(lens[b])
+            keys = u16(lp.t[l]["k"][b, h, :n])
+            # this step's selection, from its speculative query
+            S = o.unit_scores(q_sel[b, h * G:(h + 1) * G], keys, SCALE)
+            r_idx, m = o.unit_select(S, w.k)
+            Sfull = np.full((1, 1, n), np.nan)
+            Sfull[0, 0] = S
+            check_index_sets(g_idx[l][b:b + 1, h:h + 1], g_nsel[l][b:b + 1, h:h + 1],
+                             r_idx[None, None], np.array([[m]]), Sfull, np.array([n]))
+            # this step's attention, over the set selected before it
+            mp = int(boot[1][l][b, h])
+            rows = torch.from_numpy(boot[0][l][b, h, :mp].astype(np.int64))
+            kv = lp.kv_host[l]
+            ref, _ = o.unit_attn(q_att[b, h * G:(h + 1) * G], u16(kv[b, h, rows, 0]),
+                                 u16(kv[b, h, rows, 1]), SCALE)
+            err = np.abs(g_out[l][b, h * G:(h + 1) * G] - ref).max()
+            assert err <= ATOL_OUT, (l, b, h, err)
+    _log("  checked 3 units in each of 2 layers")
