@@ -244,14 +244,9 @@ ReconArgs recon_args(const Dims& d, int32_t rank, const uint16_t* u_fac, const u
   return r;
 }
 
-int gather_blocks(int src_kind) {
-  const char* env = std::getenv("CKV_GATHER_BLOCKS");
-  if (env) {
-    int v = std::atoi(env);
-    if (v > 0) return v;
-  }
-  return src_kind == CKV_SRC_HOST_PINNED ? 256 : 4096;
-}
+// Workgroups of a gather: a pinned source is read over the host link, which
+// 256 workgroups keep at its copy rate; device sources take a full grid.
+int gather_blocks(int src_kind) { return src_kind == CKV_SRC_HOST_PINNED ? 256 : 4096; }
 
 SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* scores,
                        const int32_t* ctx_lens, int32_t k, int32_t* idx, int32_t* n_sel) {
