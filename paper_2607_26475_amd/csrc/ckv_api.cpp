@@ -5,17 +5,16 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
-#include <cstdlib>
 #include <string>
 
 #include "ckv.h"
 #include "ckv_launch.hpp"
 
+namespace ckv {
+
 namespace {
-
-using namespace ckv;
-
 thread_local std::string g_detail;
+}  // namespace
 
 int fail(int code, const char* fmt, ...) {
   char buf[512];
@@ -30,6 +29,14 @@ int fail(int code, const char* fmt, ...) {
 int hip_fail(hipError_t e, const char* what) {
   return fail(CKV_EHIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }
+
+const char* last_detail() { return g_detail.c_str(); }
+
+}  // namespace ckv
+
+namespace {
+
+using namespace ckv;
 
 #define CKV_TRY_HIP(expr, what)                 \
   do {                                          \
@@ -417,7 +424,7 @@ const char* ckv_status_str(int status) {
   }
 }
 
-const char* ckv_last_error_detail(void) { return g_detail.c_str(); }
+const char* ckv_last_error_detail(void) { return last_detail(); }
 
 int ckv_workspace_bytes(const ckv_shape* shape, int32_t k, int entry, size_t* bytes) {
   Dims d;

@@ -5,6 +5,12 @@
 
 namespace ckv {
 
+// Sets the thread-local detail text of ckv_last_error_detail() and returns
+// code; hip_fail reports a failed HIP call as CKV_EHIP.
+int fail(int code, const char* fmt, ...);
+int hip_fail(hipError_t e, const char* what);
+const char* last_detail();
+
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s);
 // workgroups of the scoring pass (with a histogram) or of the dual kernel's

@@ -5,6 +5,7 @@
 #include <new>
 
 #include "ckv.h"
+#include "ckv_launch.hpp"
 
 struct ckv_pipeline {
   hipEvent_t filled[2];  // buffer i holds the rows of the layer about to use it
@@ -34,14 +35,15 @@ int gather_layer(const ckv_shape* shape, int32_t k, const ckv_layer& L, const in
 extern "C" {
 
 int ckv_pipeline_create(ckv_pipeline** pipe) {
-  if (!pipe) return CKV_EINVAL;
+  if (!pipe) return ckv::fail(CKV_EINVAL, "pipe is NULL");
   ckv_pipeline* p = new (std::nothrow) ckv_pipeline();
-  if (!p) return CKV_EINVAL;
+  if (!p) return ckv::fail(CKV_EINVAL, "out of host memory");
   for (int i = 0; i < 2; ++i) {
-    if (hipEventCreateWithFlags(&p->filled[i], hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&p->freed[i], hipEventDisableTiming) != hipSuccess) {
+    hipError_t e = hipEventCreateWithFlags(&p->filled[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&p->freed[i], hipEventDisableTiming);
+    if (e != hipSuccess) {
       delete p;
-      return CKV_EHIP;
+      return ckv::hip_fail(e, "pipeline event creation");
     }
   }
   p->parity = 0;
@@ -64,14 +66,15 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
                        const ckv_layer* layers, int num_layers, int src_kind,
                        uint16_t* const k_buf[2], uint16_t* const v_buf[2],
                        void* copy_stream) {
-  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf) return CKV_EINVAL;
+  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf)
+    return ckv::fail(CKV_EINVAL, "pipe, layers (at least 2) and both buffers are required");
   pipe->parity = 0;
   for (int l = 0; l < 2; ++l) {
     int rc = gather_layer(shape, k, layers[l], layers[l].idx_prev, layers[l].n_sel_prev,
                           src_kind, k_buf[l], v_buf[l], copy_stream);
     if (rc) return rc;
-    if (hipEventRecord(pipe->filled[l], (hipStream_t)copy_stream) != hipSuccess)
-      return CKV_EHIP;
+    hipError_t e = hipEventRecord(pipe->filled[l], (hipStream_t)copy_stream);
+    if (e != hipSuccess) return ckv::hip_fail(e, "fill event record");
     pipe->filled_capture[l] = capture_id((hipStream_t)copy_stream);
   }
   return CKV_OK;
@@ -82,7 +85,8 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                     float scale, int src_kind, uint16_t* const k_buf[2],
                     uint16_t* const v_buf[2], void* ws, size_t ws_bytes,
                     void* compute_stream, void* copy_stream) {
-  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf) return CKV_EINVAL;
+  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf)
+    return ckv::fail(CKV_EINVAL, "pipe, layers (at least 2) and both buffers are required");
   hipStream_t cs = (hipStream_t)compute_stream, xs = (hipStream_t)copy_stream;
   const unsigned long long capture = capture_id(cs);
   for (int l = 0; l < num_layers; ++l) {
@@ -92,7 +96,8 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     // capture a fill recorded outside this capture cannot be waited for;
     // the graph is then ordered after it by its launch.
     if (!capture || pipe->filled_capture[p] == capture)
-      if (hipStreamWaitEvent(cs, pipe->filled[p], 0) != hipSuccess) return CKV_EHIP;
+      if (hipError_t e = hipStreamWaitEvent(cs, pipe->filled[p], 0))
+        return ckv::hip_fail(e, "wait for a buffer fill");
     int rc;
     if (L.idx_true && L.lr_rank > 0) {  // misses: keys rebuilt, values fetched
       rc = ckv_corrected_attn_lowrank(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
@@ -112,9 +117,11 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                                 compute_stream);
     }
     if (rc) return rc;
-    if (hipEventRecord(pipe->freed[p], cs) != hipSuccess) return CKV_EHIP;
+    if (hipError_t e = hipEventRecord(pipe->freed[p], cs))
+      return ckv::hip_fail(e, "release event record");
     // refill buffer p with the layer two ahead (into the next step at the end)
-    if (hipStreamWaitEvent(xs, pipe->freed[p], 0) != hipSuccess) return CKV_EHIP;
+    if (hipError_t e = hipStreamWaitEvent(xs, pipe->freed[p], 0))
+      return ckv::hip_fail(e, "wait for a buffer release");
     const int j = l + 2;
     if (j < num_layers) {
       rc = gather_layer(shape, k, layers[j], layers[j].idx_prev, layers[j].n_sel_prev,
@@ -125,7 +132,8 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                         copy_stream);
     }
     if (rc) return rc;
-    if (hipEventRecord(pipe->filled[p], xs) != hipSuccess) return CKV_EHIP;
+    if (hipError_t e = hipEventRecord(pipe->filled[p], xs))
+      return ckv::hip_fail(e, "fill event record");
     pipe->filled_capture[p] = capture;
     pipe->parity ^= 1;
   }

@@ -3,6 +3,7 @@
 #include <mutex>
 #include <vector>
 
+#include "ckv_launch.hpp"
 #include "ckv_profile.hpp"
 
 namespace ckv {
@@ -77,16 +78,17 @@ int ckv_profile_begin(uint32_t kernel_mask) {
 }
 
 int ckv_profile_end(ckv_kernel_stats* stats) {
-  if (!stats) return CKV_EINVAL;
+  if (!stats) return ckv::fail(CKV_EINVAL, "stats is NULL");
   std::lock_guard<std::mutex> lk(ckv::g_mu);
   ckv::g_on.store(false);
   for (int i = 0; i < CKV_K_COUNT; ++i) stats[i] = ckv_kernel_stats{0, 0.0, 0.0};
   int rc = CKV_OK;
   for (const ckv::Record& r : ckv::g_records) {
     float ms = 0.f;
-    if (hipEventSynchronize(r.stop) != hipSuccess ||
-        hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
-      rc = CKV_EHIP;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) {
+      rc = ckv::hip_fail(e, "kernel timing event");
       continue;
     }
     ckv_kernel_stats& s = stats[r.id];
