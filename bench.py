@@ -228,6 +228,11 @@ def main() -> int:
         torch.cuda.empty_cache()
         pipeline = measure_pipeline(torch, ckv, synth, dev, np, host_link)
         log(f"pipeline: {pipeline}")
+        torch.cuda.empty_cache()
+        # the dual-token serving workload: 64 requests of ragged contexts
+        pipeline["dual64"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "dual64",
+                                              n_hbm=2, n_host=1, steps=3, runs=("plain",))
+        log(f"pipeline dual64: {pipeline['dual64']}")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(layers, w, scale, np)
@@ -418,12 +423,14 @@ def measure_chunked(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream,
                         "(256 chunks) per KV head"}
 
 
-def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
-    """The two-buffer decode loop on the long-context workload: B8, 32 q / 8 KV
-    heads, n 131072, k 4096, 32 layers; K|V rows in pinned host memory,
-    scoring keys in HBM.  Layer inputs cycle over 4 distinct HBM and 2 distinct
-    host layers (each far larger than any cache); queries are distinct per
-    layer and step.  The speculative query of step t is 0.8 x the query of step
+def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm=4, n_host=2,
+                     steps=4, runs=("plain", "corrected", "lowrank")):
+    """The two-buffer decode loop of 32 layers on a host-pinned workload: the
+    long-context one (B8, 32 q / 8 KV heads, n 131072, k 4096) or the
+    dual-token one (B64, n_b ~ U{16384..65536}, k 2048); K|V rows in pinned
+    host memory, scoring keys in HBM.  Layer inputs cycle over n_hbm distinct
+    HBM and n_host distinct host layers (each far larger than any cache);
+    queries are distinct per layer and step.  The speculative query of step t is 0.8 x the query of step
     t+1 plus 0.6 x noise (the dual workload's recipe).  Two runs over the same
     inputs: attention over the prefetched prediction, and with miss correction
     (each layer attends over its own query's set, misses fetched on the compute
@@ -431,11 +438,10 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
     factors (per (request, KV head), one set per host layer) and fetches only
     their values.  Step time from events on the compute stream after it has
     joined the copy stream."""
-    w = synth.WORKLOADS["long128k"]
+    w = synth.WORKLOADS[wl]
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
     scale = float(np.float32(1.0 / math.sqrt(d)))
-    n_hbm, n_host = 4, 2
     kscore, hosts = [], []
     for i in range(n_hbm):
         t = synth.make_layer(w, seed=0, layer=i, device=dev)
@@ -537,14 +543,17 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, steps=4):
         return res
 
     res = run(False)
-    res["workload"] = ("long-context decode, 32 layers: B8, 32 q / 8 KV heads, head_dim 128, "
-                       "context 131072, k 4096; K|V rows host-pinned, scoring keys in HBM; "
-                       "4 HBM and 2 host layers cycled")
-    res["corrected"] = run(True)
-    for i in range(n_host):
-        lr.append(synth.low_rank_factors(w, lr_rank, seed=0, layer=i, device=dev))
-    res["corrected_lowrank"] = run(True, lowrank=True)
-    res["corrected_lowrank"]["rank"] = lr_rank
+    ctx = (f"context {n}" if w.ctx_min == n else f"contexts U{{{w.ctx_min}..{n}}}")
+    res["workload"] = (f"{wl} decode, {L} layers: B{B}, {Hq} q / {Hkv} KV heads, head_dim {d}, "
+                       f"{ctx}, k {k}; K|V rows host-pinned, scoring keys in HBM; "
+                       f"{n_hbm} HBM and {n_host} host layers cycled")
+    if "corrected" in runs:
+        res["corrected"] = run(True)
+    if "lowrank" in runs:
+        for i in range(n_host):
+            lr.append(synth.low_rank_factors(w, lr_rank, seed=0, layer=i, device=dev))
+        res["corrected_lowrank"] = run(True, lowrank=True)
+        res["corrected_lowrank"]["rank"] = lr_rank
     del hosts, lr
     return res
 
