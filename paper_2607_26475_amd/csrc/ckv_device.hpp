@@ -37,8 +37,10 @@ constexpr int kBitmapLdsBits = kFinishLdsBytes * 8;
 constexpr int kFusedSelectMaxCtx = 65536;
 // Scoring grids are capped at kMaxScoreWgs workgroups.  With per-workgroup
 // histograms (ScoreArgs::hist_part) the histogram of unit u is the sum of the
-// slots u + wg over the workgroups wg whose range meets the unit; slot u + wg
-// is unique because ranges and units are both in group order.  The selection
+// slots u + wg over the workgroups wg whose range meets the unit's groups
+// (all of them, below n_b or not: a range past n_b stores zeros, so the
+// slots to read follow from the shape alone); slot u + wg is unique because
+// ranges and units are both in group order.  The selection
 // reads at most kMaxPartials slots per unit, else the histograms are added
 // with atomics.
 constexpr int kMaxScoreWgs = 1024;
@@ -205,6 +207,16 @@ __device__ __forceinline__ uint32_t order_key(float s) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// The key test key(x) > km1 as one fp32 compare, x > float(bits): exact for
+// every finite x when km1 >= 0x007fffff (the key of -inf).  Non-negative
+// keys map back to the float they encode; for km1 = 0x7fffffff, which no
+// float has (-0 is folded), x >= -0 is written x > -denorm_min.
+__host__ __device__ __forceinline__ uint32_t key_bound_bits(uint32_t km1) {
+  if (km1 >= 0x80000000u) return km1 ^ 0x80000000u;
+  const uint32_t g = ~km1;
+  return g == 0x80000000u ? 0x80000001u : g;
+}
+
 __device__ __forceinline__ uint4 ld16(const uint16_t* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
@@ -271,11 +283,6 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
-}
 
 // Wave-aggregated append: lanes with `flag` get consecutive slots from the
 // counter at *ctr (one atomic per wave); returns this lane's slot.
@@ -287,19 +294,33 @@ __device__ __forceinline__ uint32_t wave_append(bool flag, uint32_t* ctr) {
   const int leader = cnt ? __ffsll(mask) - 1 : 0;
   uint32_t base = 0u;
   if (cnt && (int)(threadIdx.x & 63) == leader) base = atomicAdd(ctr, cnt);
-  base = __shfl(base, leader);
+  base = __builtin_amdgcn_readlane(base, leader);
   return base + rank;
 }
 
-// Inclusive prefix sum over the 64 lanes of a wave.
+template <int CTRL, int ROW_MASK, bool ZERO_FILL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xF, ZERO_FILL);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave, in DPP moves only: a
+// Hillis-Steele scan inside each row of 16 lanes (row_shr 1, 2, 4, 8, lanes
+// shifted in from outside the row read 0), then the total of row 0 added to
+// row 1 and of row 2 to row 3 (row_bcast:15), then the total of rows 0-1 to
+// rows 2-3 (row_bcast:31).
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  x += dpp_u32<0x111, 0xF, true>(x);
+  x += dpp_u32<0x112, 0xF, true>(x);
+  x += dpp_u32<0x114, 0xF, true>(x);
+  x += dpp_u32<0x118, 0xF, true>(x);
+  x += dpp_u32<0x142, 0xA, false>(x);
+  x += dpp_u32<0x143, 0xC, false>(x);
   return x;
+}
+
+// Sum over the 64 lanes of a wave, the same in every lane.
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
+  return __builtin_amdgcn_readlane(wave_incl_scan(x), 63);
 }
 
 // Inclusive prefix sum over a workgroup of NW waves.  `tmp` is LDS scratch of

@@ -137,7 +137,7 @@ __device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
       out[o++] = w * 32 + bit;
       bits &= bits - 1u;
     }
-    base += __shfl(incl, 63);
+    base += __builtin_amdgcn_readlane(incl, 63);
   }
   __syncthreads();
 }
@@ -266,7 +266,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
 // kSelBatch positions, all loads of a batch in flight together.  Positions
 // above the first-digit bin go straight into an LDS bitmap (one ballot per
 // 64 positions, no atomics); positions inside the bin become candidates
-// (order key, position), whose slots are reserved with one atomic per wave.
+// (fp32 bits, position), whose slots are reserved with one atomic per wave.
 // The threshold inside the bin is then resolved exactly, the chosen
 // candidates marked, and the bitmap written out in ascending order.
 constexpr int kSelPer = 32;
@@ -291,7 +291,8 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 }
 
 // One batch of kSelBatch positions starting at j0: bitmap words of the
-// positions above the bin b1, candidates inside it appended at *ctr.
+// positions above the bin b1, candidates inside it appended at *ctr as
+// (fp32 bits, position).
 template <class Cands>
 __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j0, int n,
                                                uint32_t b1, uint32_t* bm, const Cands& cs,
@@ -322,7 +323,7 @@ __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j
     const bool is_cand = j < n && (key >> (32 - kHistBits)) == b1;
     const uint64_t cm = __ballot(is_cand);
     const uint32_t o = base + lanes_below(cm);
-    if (is_cand) cs.put(o, make_uint2(key, (uint32_t)j));
+    if (is_cand) cs.put(o, make_uint2(__float_as_uint(sv[u]), (uint32_t)j));
     base += (uint32_t)__popcll(cm);
   }
 }
@@ -341,6 +342,72 @@ struct SplitCands {
   }
 };
 
+// The same classification with two fp32 compares per position, for bins
+// b1 >= 4 (every finite threshold): x > f_hi <=> key(x) is above the bin,
+// x > f_lo <=> key(x) is at or above its lower edge.  FULL batches lie
+// wholly below n.
+template <bool FULL>
+__device__ __forceinline__ void classify_batch_f(const float (&sv)[kSelPer], int j0, int n,
+                                                 float f_lo, float f_hi, uint32_t* bm,
+                                                 const SplitCands& cs, uint32_t* ctr) {
+  static_assert(2 * kSelPer == 64, "one bitmap word per lane and batch");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  auto valid = [&](int u) -> uint64_t {  // the wave's positions below n
+    if (FULL) return ~0ull;
+    const int rem = n - (j0 + u * kFinishThreads + wave * 64);
+    return rem >= 64 ? ~0ull : rem <= 0 ? 0ull : (1ull << rem) - 1ull;
+  };
+  uint32_t word = 0u, wc = 0u;
+#pragma unroll
+  for (int u = 0; u < kSelPer; ++u) {
+    const uint64_t v = valid(u);
+    const uint64_t hi = __builtin_amdgcn_ballot_w64(sv[u] > f_hi) & v;
+    const uint64_t ge = __builtin_amdgcn_ballot_w64(sv[u] > f_lo) & v;
+    // lane 2u + h keeps word h of the wave's 64 positions
+    asm("v_writelane_b32 %0, %1, %2" : "+v"(word) : "s"((uint32_t)hi), "n"(2 * u));
+    asm("v_writelane_b32 %0, %1, %2" : "+v"(word) : "s"((uint32_t)(hi >> 32)), "n"(2 * u + 1));
+    wc += (uint32_t)__popcll(ge & ~hi);
+  }
+  bm[((j0 + (lane >> 1) * kFinishThreads + wave * 64) >> 5) + (lane & 1)] = word;
+  uint32_t base = 0u;
+  if (lane == 0 && wc) base = atomicAdd(ctr, wc);
+  base = __builtin_amdgcn_readfirstlane(base);
+  if (base + wc <= (uint32_t)kCandLds) {  // the wave's candidates all fit in LDS
+#pragma unroll
+    for (int u = 0; u < kSelPer; ++u) {
+      // compare again rather than keep 2 x kSelPer lane masks live
+      float x = sv[u];
+      asm volatile("" : "+v"(x));
+      const int j = j0 + u * kFinishThreads + tid;
+      const uint64_t cm = (__builtin_amdgcn_ballot_w64(x > f_lo) &
+                           ~__builtin_amdgcn_ballot_w64(x > f_hi)) & valid(u);
+      if (x > f_lo && !(x > f_hi) && (FULL || j < n))
+        cs.lds[base + lanes_below(cm)] = make_uint2(__float_as_uint(x), (uint32_t)j);
+      base += (uint32_t)__popcll(cm);
+    }
+  } else {
+    for (int u = 0; u < kSelPer; ++u) {
+      const int j = j0 + u * kFinishThreads + tid;
+      const bool in = sv[u] > f_lo && !(sv[u] > f_hi) && j < n;
+      const uint64_t cm = __builtin_amdgcn_ballot_w64(in);
+      if (in) cs.put(base + lanes_below(cm), make_uint2(__float_as_uint(sv[u]), (uint32_t)j));
+      base += (uint32_t)__popcll(cm);
+    }
+  }
+}
+
+
+// The candidates as (order key, position): the fused selection stores the
+// scores' fp32 bits and converts on every read.
+struct KeyedCands {
+  SplitCands c;
+  __device__ __forceinline__ uint2 operator[](uint32_t i) const {
+    const uint2 v = c[i];
+    return make_uint2(order_key(__uint_as_float(v.x)), v.y);
+  }
+};
+
 __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __shared__ uint2 cand[kCandLds];
   __shared__ uint32_t bm[kFusedSelectMaxCtx / 32];
@@ -348,57 +415,67 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
   __shared__ uint32_t misc[8];
   const int unit = blockIdx.x;
+  const int tid = threadIdx.x;
+  // Every read the workgroup needs first is issued before anything waits:
+  // the histogram, and the first batch of scores (clamped to the row, not
+  // to n_b, which is not known yet; positions at or past n_b are masked).
+  // The histogram is the sum of the slots unit + wg of the workgroups that
+  // scored the unit's groups (every such workgroup stores one, zeros where
+  // its groups lie past n_b), or one slot already summed.
+  const uint32_t* slots = a.hist + (int64_t)unit * kHistBins;
+  int nslots = 1;
+  if (a.hist_part) {
+    const int64_t gu = (a.max_ctx + kStageRows - 1) / kStageRows;
+    const int64_t T = gu * a.units, g0 = (int64_t)unit * gu;
+    const int64_t lo = range_owner(g0, T, a.score_nwg);
+    const int64_t hi = range_owner(g0 + gu - 1, T, a.score_nwg);
+    slots = a.hist_part + (unit + lo) * kHistBins;
+    nslots = (int)min<int64_t>(hi - lo + 1, kMaxPartials);  // the host keeps it below
+  }
+  uint2 hv[kMaxPartials];
+  load_hist_slots(slots, nslots, hv);
+  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
+  float sv0[kSelPer];
+  load_score_batch(srow, 0, a.max_ctx, sv0);
   const int b = unit / a.Hkv;
   const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
   const int m = min(a.k, n);
-  const int tid = threadIdx.x;
   int32_t* idx = a.idx + (int64_t)unit * a.k;
   if (m >= n) {  // uniform; every position (possibly none) is selected
     for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
     if (tid == 0) a.n_sel[unit] = m;
     return;
   }
-  const float* srow = a.scores + (int64_t)unit * a.max_ctx;
-  float sv0[kSelPer];
-  if (a.hist_part) {
-    // the slots unit + wg of the workgroups that scored the unit's groups:
-    // every thread sums two bins of them into LDS, the histogram loads
-    // issued before the first batch of scores
-    const int64_t gu = (a.max_ctx + kStageRows - 1) / kStageRows;
-    const int64_t T = gu * a.units, g0 = (int64_t)unit * gu;
-    const int64_t lo = range_owner(g0, T, a.score_nwg);
-    const int64_t hi = range_owner(g0 + (n + kStageRows - 1) / kStageRows - 1, T, a.score_nwg);
-    const int nslots = (int)min<int64_t>(hi - lo + 1, kMaxPartials);  // the host keeps it below
-    uint2 hv[kMaxPartials];
-    load_hist_slots(a.hist_part + (unit + lo) * kHistBins, nslots, hv);
-    load_score_batch(srow, 0, n, sv0);
-    store_hist_sum(hv, nslots, lhist);
-    if (tid == 64) misc[7] = 0u;
-    __syncthreads();
-    if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
-  } else {
-    // the first batch of scores is in flight while wave 0 finds the bin
-    load_score_batch(srow, 0, n, sv0);
-    if (tid < 64)
-      find_first_bin_fine(a.hist + (int64_t)unit * kHistBins, (uint32_t)m, lhist, misc + 4);
-    if (tid == 64) misc[7] = 0u;
-  }
+  store_hist_sum(hv, nslots, lhist);
+  if (tid == 64) misc[7] = 0u;
+  __syncthreads();
+  if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
   __syncthreads();
   const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
   const uint32_t b1 = misc[4], above = misc[5];
-  classify_batch(sv0, 0, n, b1, bm, cs, &misc[7]);
-  for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {  // a fresh array per batch
-    float sv[kSelPer];
-    load_score_batch(srow, j0, n, sv);
-    classify_batch(sv, j0, n, b1, bm, cs, &misc[7]);
+  if (b1 >= 4u) {  // a finite threshold: fp32 compares against the bin's edges
+    const float f_lo = __uint_as_float(key_bound_bits((b1 << (32 - kHistBits)) - 1u));
+    const float f_hi = __uint_as_float(key_bound_bits(((b1 + 1u) << (32 - kHistBits)) - 1u));
+    for (int j0 = 0; j0 < n; j0 += kSelBatch) {
+      if (j0) load_score_batch(srow, j0, n, sv0);
+      if (j0 + kSelBatch <= n) classify_batch_f<true>(sv0, j0, n, f_lo, f_hi, bm, cs, &misc[7]);
+      else classify_batch_f<false>(sv0, j0, n, f_lo, f_hi, bm, cs, &misc[7]);
+    }
+  } else {  // a non-finite threshold: order keys, the scores read again
+    for (int j0 = 0; j0 < n; j0 += kSelBatch) {
+      float sv[kSelPer];
+      load_score_batch(srow, j0, n, sv);
+      classify_batch(sv, j0, n, b1, bm, cs, &misc[7]);
+    }
   }
   __syncthreads();
   const uint32_t nc = misc[7];
   const uint32_t need = (uint32_t)m - above;
+  const KeyedCands kc{cs};
   uint32_t pmax;
-  const uint32_t T = refine_threshold(cs, nc, need, b1, lhist, tmp, misc, &pmax);
+  const uint32_t T = refine_threshold(kc, nc, need, b1, lhist, tmp, misc, &pmax);
   for (uint32_t i = tid; i < nc; i += kFinishThreads) {
-    const uint2 c = cs[i];
+    const uint2 c = kc[i];
     if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
   }
   __syncthreads();

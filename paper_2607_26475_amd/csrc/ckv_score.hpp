@@ -51,6 +51,12 @@ __device__ __forceinline__ void store_hist(const uint32_t* lds_hist, uint32_t* s
         *reinterpret_cast<const uint4*>(lds_hist + kPer * t + i);
 }
 
+// An empty slot, for a workgroup whose groups of the unit all lie past n_b.
+__device__ __forceinline__ void store_zero_hist(uint32_t* slot) {
+  for (int i = 4 * (int)threadIdx.x; i < kHistBins; i += 4 * kScoreThreads)
+    *reinterpret_cast<uint4*>(slot + i) = make_uint4(0u, 0u, 0u, 0u);
+}
+
 // Scores a balanced share of the whole batch: the positions of every unit are
 // cut into groups of kStageRows keys, the groups of all units are numbered
 // unit-major, and workgroup `wg` of `nwg` takes the contiguous range
@@ -58,8 +64,9 @@ __device__ __forceinline__ void store_hist(const uint32_t* lds_hist, uint32_t* s
 // unit it touches the workgroup loads that unit's G query rows once and, if
 // HIST, counts the first radix digit of its scores in LDS and, when it leaves
 // the unit, adds the counts to the unit's histogram or stores them as its own
-// slot (hist_part).  Groups at or beyond n_b
-// only write -inf.  Must be called by all kScoreThreads threads.
+// slot (hist_part; an all-zero slot when its groups of the unit all lie at or
+// past n_b).  Groups at or beyond n_b only write -inf.  Must be called by all
+// kScoreThreads threads.
 //
 // Memory path: the four waves take the range's groups round-robin (wave w
 // the groups w, w + 4, ...), so that the workgroup streams one region at a
@@ -222,6 +229,8 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
                      a.coarse + (int64_t)unit * kCoarseBins);
         __syncthreads();
       }
+    } else if (HIST && a.hist_part) {  // the unit's histogram sums this slot too
+      store_zero_hist(a.hist_part + ((int64_t)unit + wg) * kHistBins);
     }
     seg = seg_end;
   }

@@ -30,13 +30,13 @@ __device__ __forceinline__ void find_first_bin(const uint32_t* coarse,
   const uint32_t s = wave_incl_scan(c);
   int L = __ffsll((unsigned long long)__ballot(s >= m)) - 1;
   if (L < 0) L = kCoarseBins - 1;  // only if the histogram were inconsistent
-  const uint32_t above_c = __shfl(s - c, L);
+  const uint32_t above_c = __builtin_amdgcn_readlane(s - c, L);
   const int sb = kCoarseBins - 1 - L;
   const uint32_t f = lane < kFine ? hist[sb * kFine + kFine - 1 - lane] : 0u;
   const uint32_t s2 = wave_incl_scan(f) + above_c;
   int L2 = __ffsll((unsigned long long)__ballot(lane < kFine && s2 >= m)) - 1;
   if (L2 < 0) L2 = kFine - 1;
-  const uint32_t above = __shfl(s2 - f, L2);
+  const uint32_t above = __builtin_amdgcn_readlane(s2 - f, L2);
   if (lane == 0) {
     out[0] = (uint32_t)(sb * kFine + kFine - 1 - L2);
     out[1] = above;
@@ -44,23 +44,29 @@ __device__ __forceinline__ void find_first_bin(const uint32_t* coarse,
 }
 
 // Wave 0: lane l holds the count c of coarse range cb = 63 - l, whose 32 fine
-// bins are at stage[cb*32 ..]; finds the bin holding the m-th largest key.
+// bins are at stage[cb*32 ..]; finds the bin holding the m-th largest key by
+// two wave scans (ranges, then the chosen range's bins, both descending).
 // out[0] = bin, out[1] = keys in higher bins, out[2] = keys in the bin.
-__device__ __forceinline__ void walk_first_bin(const uint32_t* stage, int cb, uint32_t c,
-                                               uint32_t m, uint32_t* out) {
+__device__ __forceinline__ void walk_first_bin(const uint32_t* stage, uint32_t c, uint32_t m,
+                                               uint32_t* out) {
   constexpr int kFine = kHistBins / 64;
+  static_assert(kFine <= 64, "one lane per fine bin");
   const int lane = threadIdx.x & 63;
   const uint32_t s = wave_incl_scan(c);
   int L = __ffsll((unsigned long long)__ballot(s >= m)) - 1;
   if (L < 0) L = 63;  // only if the histogram were inconsistent
-  if (lane == L) {
-    const uint32_t* f = stage + cb * kFine;
-    uint32_t run = s - c;
-    int i = kFine - 1;
-    while (i > 0 && run + f[i] < m) run += f[i--];
-    out[0] = (uint32_t)(cb * kFine + i);
-    out[1] = run;
-    out[2] = f[i];
+  const uint32_t above_c = __builtin_amdgcn_readlane(s - c, L);
+  const int cb = 63 - L;
+  const uint32_t f = lane < kFine ? stage[cb * kFine + kFine - 1 - lane] : 0u;
+  const uint32_t s2 = wave_incl_scan(f) + above_c;
+  int L2 = __ffsll((unsigned long long)__ballot(lane < kFine && s2 >= m)) - 1;
+  if (L2 < 0) L2 = kFine - 1;  // the range's lowest bin
+  const uint32_t above = __builtin_amdgcn_readlane(s2 - f, L2);
+  const uint32_t in_bin = __builtin_amdgcn_readlane(f, L2);
+  if (lane == 0) {
+    out[0] = (uint32_t)(cb * kFine + kFine - 1 - L2);
+    out[1] = above;
+    out[2] = in_bin;
   }
 }
 
@@ -92,30 +98,9 @@ __device__ __forceinline__ void store_hist_sum(const uint2 (&v)[kMaxPartials], i
   *reinterpret_cast<uint2*>(lhist + 2 * threadIdx.x) = acc;
 }
 
-// Wave 0 only, from the fine histogram alone in one round trip: lane l reads
-// the 32 bins of coarse range 63 - l (ranges in descending order) and copies
-// them to stage[] (2048 words of LDS); the lane whose range holds the m-th
-// largest key then walks its bins downwards from there.
-// out[0] = bin, out[1] = keys in higher bins, out[2] = keys in the bin.
-__device__ __forceinline__ void find_first_bin_fine(const uint32_t* hist, uint32_t m,
-                                                    uint32_t* stage, uint32_t* out) {
-  constexpr int kFine = kHistBins / 64;
-  static_assert(kFine % 4 == 0, "16-byte loads");
-  const int lane = threadIdx.x & 63;
-  const int cb = 63 - lane;
-  const uint4* src = reinterpret_cast<const uint4*>(hist + cb * kFine);
-  uint4* dst = reinterpret_cast<uint4*>(stage + cb * kFine);
-  uint32_t c = 0u;
-#pragma unroll
-  for (int i = 0; i < kFine / 4; ++i) {
-    const uint4 v = src[i];
-    c += v.x + v.y + v.z + v.w;
-    dst[i] = v;
-  }
-  walk_first_bin(stage, cb, c, m, out);
-}
-
-// The same from a histogram already in LDS (lhist).
+// Wave 0 only: the bin holding the m-th largest key, from the histogram in
+// LDS (lhist).  out[0] = bin, out[1] = keys in higher bins, out[2] = keys in
+// the bin.
 __device__ __forceinline__ void find_first_bin_lds(const uint32_t* lhist, uint32_t m,
                                                    uint32_t* out) {
   constexpr int kFine = kHistBins / 64;
@@ -126,7 +111,7 @@ __device__ __forceinline__ void find_first_bin_lds(const uint32_t* lhist, uint32
     const uint4 v = reinterpret_cast<const uint4*>(lhist + cb * kFine)[i];
     c += v.x + v.y + v.z + v.w;
   }
-  walk_first_bin(lhist, cb, c, m, out);
+  walk_first_bin(lhist, c, m, out);
 }
 
 // All threads of a kFinishThreads workgroup: given a histogram of nb bins in

@@ -79,6 +79,27 @@ def _select_case(name):
         B, Hkv, n, k, lens = 1, 1, 3000, 100, [3000]
         S = np.where(g.random((B, Hkv, n)) < 0.5, -0.0, 0.0).astype(np.float32)
         S[0, 0, ::97] = -1.0
+    elif name == "negative":
+        B, Hkv, n, k, lens = 2, 2, 6000, 500, [6000, 4321]
+        S = (-np.abs(g.standard_normal((B, Hkv, n))) - 1e-3).astype(np.float32)
+    elif name == "bin_edges":
+        # every unit's scores sit within a few order-key steps of the lower
+        # edge of one first-digit bin (11 bits of the monotone key, both
+        # signs, zeros and subnormals included), so that the bin and
+        # above-bin decisions meet exact edge values and heavy ties
+        bins = [5, 6, 100, 1000, 1023, 1024, 1025, 1026, 1900, 2043]
+        B, Hkv, n, k = len(bins), 1, 5000, 1500
+        lens = [5000, 4999, 3001, 5000, 2000, 5000, 4097, 5000, 1501, 5000]
+        S = np.empty((B, Hkv, n), np.float32)
+        for b, c in enumerate(bins):
+            keys = np.arange((c << 21) - 3, (c << 21) + 4, dtype=np.int64)
+            keys = keys[keys != 0x7FFFFFFF]  # no float has this key (-0 is +0)
+            bits = np.where(keys >= 0x80000000, keys ^ 0x80000000, ~keys & 0xFFFFFFFF)
+            vals = bits.astype(np.uint32).view(np.float32)
+            if c == 1024:
+                vals = np.append(vals, np.float32(-0.0))
+            assert np.all(np.isfinite(vals))
+            S[b, 0] = g.choice(vals, size=n)
     elif name == "budget_ge_context":
         B, Hkv, n, k, lens = 3, 2, 100, 128, [100, 64, 1]
         S = g.standard_normal((B, Hkv, n)).astype(np.float32)
@@ -102,8 +123,8 @@ def _select_case(name):
 
 
 @pytest.mark.parametrize("name", ["continuous", "ragged", "ties", "all_equal",
-                                  "signed_zero", "budget_ge_context", "dense_cluster",
-                                  "over_bitmap"])
+                                  "signed_zero", "negative", "bin_edges",
+                                  "budget_ge_context", "dense_cluster", "over_bitmap"])
 def test_select_topk_exact(name):
     """Same fp32 scores on both sides: the index sets must be identical."""
     _log("select_topk", name)

@@ -2,9 +2,11 @@
 
 The scoring pass splits T = units x groups-per-unit groups of keys into nwg
 contiguous ranges, [wg*T/nwg, (wg+1)*T/nwg).  A workgroup stores the
-histogram of each unit it meets as slot unit + wg, and the selection of a
-unit sums the slots of the workgroups that own its first and last valid
-group and every one between.  These checks enumerate the ranges directly.
+histogram of each unit it meets as slot unit + wg (zeros when its groups of
+the unit all lie past n_b), and the selection of a unit sums the slots of the
+workgroups that own its first and last group and every one between.  These
+checks enumerate the ranges directly; the selection's reading is the case
+where every group of the unit counts.
 Slots must be unique.  The owner of a group, computed as
 ((g + 1) * nwg - 1) // T, must be the range that holds it.  The workgroups
 between the two owners must be exactly those whose range meets the unit's
