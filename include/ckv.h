@@ -55,7 +55,10 @@
  *     access leaves the caller's buffers): 0 <= n_b <= max_ctx; gathered idx
  *     entries lie in [0, max_ctx) (slots whose idx is outside are skipped).
  *   - Scores are compared by their fp32 value (-0 equals +0); equal scores
- *     rank the lower position first.  Inputs must be finite.
+ *     rank the lower position first.  Inputs must be finite; scores may be
+ *     -inf or +inf but not NaN (a NaN score, which finite inputs can only
+ *     give through fp32 overflow, leaves the selected set unspecified while
+ *     every write stays inside the caller's buffers).
  */
 #ifndef CKV_H
 #define CKV_H

@@ -207,14 +207,18 @@ __device__ __forceinline__ uint32_t order_key(float s) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// The key test key(x) > km1 as one fp32 compare, x > float(bits): exact for
-// every finite x when km1 >= 0x007fffff (the key of -inf).  Non-negative
-// keys map back to the float they encode; for km1 = 0x7fffffff, which no
-// float has (-0 is folded), x >= -0 is written x > -denorm_min.
-__host__ __device__ __forceinline__ uint32_t key_bound_bits(uint32_t km1) {
-  if (km1 >= 0x80000000u) return km1 ^ 0x80000000u;
-  const uint32_t g = ~km1;
-  return g == 0x80000000u ? 0x80000001u : g;
+// The key test key(x) >= K as one fp32 compare, x >= float(bits), exact for
+// every x that is not NaN; K ranges over [0, 2^32] (2^32: no key).  A key at
+// or above 0x80000000 maps back to the non-negative float it encodes (+inf
+// and beyond: NaN bits, which no x reaches); one at or below that of -inf
+// admits every non-NaN x; others map to the negative float with that key
+// (0x7fffffff, which no float has, gives -0: x >= -0 <=> key(x) >= +0's).
+__host__ __device__ __forceinline__ uint32_t key_floor_bits(uint64_t K) {
+  if (K >= (1ull << 32)) return 0x7fc00000u;
+  const uint32_t k = (uint32_t)K;
+  if (k >= 0x80000000u) return k ^ 0x80000000u;
+  if (k <= 0x007fffffu) return 0xff800000u;
+  return ~k;
 }
 
 __device__ __forceinline__ uint4 ld16(const uint16_t* p) {

@@ -111,10 +111,13 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
   }
 }
 
-// Writes set bits of bm[0, words) as ascending positions to out[], 16 waves
-// each owning a contiguous word range (reads are lane-consecutive).
-__device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
-                                            int32_t* out, uint32_t* tmp) {
+// Writes set bits of bm[0, words) as ascending positions to out[0, limit),
+// 16 waves each owning a contiguous word range (reads are lane-consecutive),
+// and returns the number of set bits.  The bitmap holds exactly m <= limit
+// bits for scores as specified; the limit only keeps other input (NaN
+// scores) inside the row.
+__device__ __forceinline__ uint32_t emit_bitmap(const uint32_t* bm, int words, int32_t* out,
+                                                uint32_t limit, uint32_t* tmp) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr int kW = kFinishThreads / 64;
   const int per = (((words + kW - 1) / kW) + 63) & ~63;
@@ -124,8 +127,12 @@ __device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
   cnt = wave_sum_u32(cnt);
   if (lane == 0) tmp[wave] = cnt;
   __syncthreads();
-  uint32_t base = 0;
-  for (int i = 0; i < wave; ++i) base += tmp[i];
+  uint32_t base = 0, total = 0;
+  for (int i = 0; i < kW; ++i) {
+    const uint32_t t = tmp[i];
+    base += i < wave ? t : 0u;
+    total += t;
+  }
   for (int ws = w0; ws < w1; ws += 64) {
     const int w = ws + lane;
     uint32_t bits = w < w1 ? bm[w] : 0u;
@@ -134,12 +141,14 @@ __device__ __forceinline__ void emit_bitmap(const uint32_t* bm, int words,
     uint32_t o = base + incl - c;
     while (bits) {
       const int bit = __ffs(bits) - 1;
-      out[o++] = w * 32 + bit;
+      if (o < limit) out[o] = w * 32 + bit;
+      ++o;
       bits &= bits - 1u;
     }
     base += __builtin_amdgcn_readlane(incl, 63);
   }
   __syncthreads();
+  return total;
 }
 
 // Radix select among candidates (order key, position) that share the first
@@ -256,7 +265,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
     atomicOr(&bm[p >> 5], 1u << (p & 31));
   }
   __syncthreads();
-  emit_bitmap(bm, words, idx, tmp);
+  emit_bitmap(bm, words, idx, (uint32_t)a.k, tmp);
   for (int i = m + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
   if (tid == 0) a.n_sel[unit] = m;
 }
@@ -290,44 +299,6 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// One batch of kSelBatch positions starting at j0: bitmap words of the
-// positions above the bin b1, candidates inside it appended at *ctr as
-// (fp32 bits, position).
-template <class Cands>
-__device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j0, int n,
-                                               uint32_t b1, uint32_t* bm, const Cands& cs,
-                                               uint32_t* ctr) {
-  static_assert(2 * kSelPer == 64, "one bitmap word per lane and batch");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // The wave's positions j0 + u * kFinishThreads + wave * 64 + [0, 64) form
-  // bitmap words 2u and 2u + 1 of its share; lane 2u + h keeps word h of u.
-  uint32_t word = 0u, wc = 0u;
-#pragma unroll
-  for (int u = 0; u < kSelPer; ++u) {
-    const int jw = j0 + u * kFinishThreads + wave * 64;
-    const uint32_t d1 = order_key(sv[u]) >> (32 - kHistBits);
-    const bool valid = jw + lane < n;
-    const uint64_t hi = __ballot(valid && d1 > b1);
-    const uint32_t half = (lane & 1) ? (uint32_t)(hi >> 32) : (uint32_t)hi;
-    word = (lane >> 1) == u ? half : word;
-    wc += (uint32_t)__popcll(__ballot(valid && d1 == b1));
-  }
-  bm[((j0 + (lane >> 1) * kFinishThreads + wave * 64) >> 5) + (lane & 1)] = word;
-  uint32_t base = 0u;
-  if (lane == 0 && wc) base = atomicAdd(ctr, wc);
-  base = __builtin_amdgcn_readfirstlane(base);
-#pragma unroll
-  for (int u = 0; u < kSelPer; ++u) {
-    const int j = j0 + u * kFinishThreads + tid;
-    const uint32_t key = order_key(sv[u]);
-    const bool is_cand = j < n && (key >> (32 - kHistBits)) == b1;
-    const uint64_t cm = __ballot(is_cand);
-    const uint32_t o = base + lanes_below(cm);
-    if (is_cand) cs.put(o, make_uint2(__float_as_uint(sv[u]), (uint32_t)j));
-    base += (uint32_t)__popcll(cm);
-  }
-}
-
 // Candidate slots of the fused selection: the first kCandLds in LDS, any
 // beyond (heavy ties) in the unit's global candidate area.
 struct SplitCands {
@@ -342,31 +313,28 @@ struct SplitCands {
   }
 };
 
-// The same classification with two fp32 compares per position, for bins
-// b1 >= 4 (every finite threshold): x > f_hi <=> key(x) is above the bin,
-// x > f_lo <=> key(x) is at or above its lower edge.  FULL batches lie
-// wholly below n.
-template <bool FULL>
-__device__ __forceinline__ void classify_batch_f(const float (&sv)[kSelPer], int j0, int n,
-                                                 float f_lo, float f_hi, uint32_t* bm,
-                                                 const SplitCands& cs, uint32_t* ctr) {
+// One batch of kSelBatch positions starting at j0, with two fp32 compares
+// per position: x >= g_hi <=> key(x) is above the first-digit bin b1 (set in
+// the LDS bitmap, one ballot per 64 positions), g_lo <= x < g_hi <=> key(x)
+// lies in it (a candidate (fp32 bits, position) appended at *ctr, one atomic
+// per wave).  Positions at or past n_b must hold NaN (then neither holds).
+__device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j0, float g_lo,
+                                               float g_hi, uint32_t* bm, const SplitCands& cs,
+                                               uint32_t* ctr) {
   static_assert(2 * kSelPer == 64, "one bitmap word per lane and batch");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  auto valid = [&](int u) -> uint64_t {  // the wave's positions below n
-    if (FULL) return ~0ull;
-    const int rem = n - (j0 + u * kFinishThreads + wave * 64);
-    return rem >= 64 ? ~0ull : rem <= 0 ? 0ull : (1ull << rem) - 1ull;
-  };
   uint32_t word = 0u, wc = 0u;
 #pragma unroll
   for (int u = 0; u < kSelPer; ++u) {
-    const uint64_t v = valid(u);
-    const uint64_t hi = __builtin_amdgcn_ballot_w64(sv[u] > f_hi) & v;
-    const uint64_t ge = __builtin_amdgcn_ballot_w64(sv[u] > f_lo) & v;
-    // lane 2u + h keeps word h of the wave's 64 positions
-    asm("v_writelane_b32 %0, %1, %2" : "+v"(word) : "s"((uint32_t)hi), "n"(2 * u));
-    asm("v_writelane_b32 %0, %1, %2" : "+v"(word) : "s"((uint32_t)(hi >> 32)), "n"(2 * u + 1));
+    const uint64_t hi = __builtin_amdgcn_ballot_w64(sv[u] >= g_hi);
+    const uint64_t ge = __builtin_amdgcn_ballot_w64(sv[u] >= g_lo);
+    // lane 2u + h keeps word h of the wave's 64 positions.  The compare that
+    // wrote `hi` is a VALU write of SGPRs, which a VALU read right after may
+    // miss: the nop keeps the wait states the compiler cannot see inside asm.
+    asm("s_nop 4\n\tv_writelane_b32 %0, %1, %2\n\tv_writelane_b32 %0, %3, %4"
+        : "+v"(word)
+        : "s"((uint32_t)hi), "n"(2 * u), "s"((uint32_t)(hi >> 32)), "n"(2 * u + 1));
     wc += (uint32_t)__popcll(ge & ~hi);
   }
   bm[((j0 + (lane >> 1) * kFinishThreads + wave * 64) >> 5) + (lane & 1)] = word;
@@ -380,23 +348,22 @@ __device__ __forceinline__ void classify_batch_f(const float (&sv)[kSelPer], int
       float x = sv[u];
       asm volatile("" : "+v"(x));
       const int j = j0 + u * kFinishThreads + tid;
-      const uint64_t cm = (__builtin_amdgcn_ballot_w64(x > f_lo) &
-                           ~__builtin_amdgcn_ballot_w64(x > f_hi)) & valid(u);
-      if (x > f_lo && !(x > f_hi) && (FULL || j < n))
+      const uint64_t cm = __builtin_amdgcn_ballot_w64(x >= g_lo) &
+                          ~__builtin_amdgcn_ballot_w64(x >= g_hi);
+      if (x >= g_lo && !(x >= g_hi))
         cs.lds[base + lanes_below(cm)] = make_uint2(__float_as_uint(x), (uint32_t)j);
       base += (uint32_t)__popcll(cm);
     }
   } else {
     for (int u = 0; u < kSelPer; ++u) {
       const int j = j0 + u * kFinishThreads + tid;
-      const bool in = sv[u] > f_lo && !(sv[u] > f_hi) && j < n;
+      const bool in = sv[u] >= g_lo && !(sv[u] >= g_hi);
       const uint64_t cm = __builtin_amdgcn_ballot_w64(in);
       if (in) cs.put(base + lanes_below(cm), make_uint2(__float_as_uint(sv[u]), (uint32_t)j));
       base += (uint32_t)__popcll(cm);
     }
   }
 }
-
 
 // The candidates as (order key, position): the fused selection stores the
 // scores' fp32 bits and converts on every read.
@@ -432,13 +399,18 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
     slots = a.hist_part + (unit + lo) * kHistBins;
     nslots = (int)min<int64_t>(hi - lo + 1, kMaxPartials);  // the host keeps it below
   }
+  const int len_b = a.ctx_lens[unit / a.Hkv];
   uint2 hv[kMaxPartials];
   load_hist_slots(slots, nslots, hv);
+  // every wave's histogram loads queue ahead of all score loads (a bare
+  // barrier: no wait for the loads themselves)
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
   const float* srow = a.scores + (int64_t)unit * a.max_ctx;
   float sv0[kSelPer];
   load_score_batch(srow, 0, a.max_ctx, sv0);
-  const int b = unit / a.Hkv;
-  const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
+  __builtin_amdgcn_sched_barrier(0);  // n_b is waited for only here
+  const int n = unit_len(len_b, a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   int32_t* idx = a.idx + (int64_t)unit * a.k;
   if (m >= n) {  // uniform; every position (possibly none) is selected
@@ -453,20 +425,16 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __syncthreads();
   const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
   const uint32_t b1 = misc[4], above = misc[5];
-  if (b1 >= 4u) {  // a finite threshold: fp32 compares against the bin's edges
-    const float f_lo = __uint_as_float(key_bound_bits((b1 << (32 - kHistBits)) - 1u));
-    const float f_hi = __uint_as_float(key_bound_bits(((b1 + 1u) << (32 - kHistBits)) - 1u));
-    for (int j0 = 0; j0 < n; j0 += kSelBatch) {
-      if (j0) load_score_batch(srow, j0, n, sv0);
-      if (j0 + kSelBatch <= n) classify_batch_f<true>(sv0, j0, n, f_lo, f_hi, bm, cs, &misc[7]);
-      else classify_batch_f<false>(sv0, j0, n, f_lo, f_hi, bm, cs, &misc[7]);
+  const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
+  const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
+  for (int j0 = 0; j0 < n; j0 += kSelBatch) {
+    if (j0) load_score_batch(srow, j0, n, sv0);
+    if (j0 + kSelBatch > n) {  // the last, partial batch: NaN past n_b
+#pragma unroll
+      for (int u = 0; u < kSelPer; ++u)
+        if (j0 + u * kFinishThreads + tid >= n) sv0[u] = __builtin_nanf("");
     }
-  } else {  // a non-finite threshold: order keys, the scores read again
-    for (int j0 = 0; j0 < n; j0 += kSelBatch) {
-      float sv[kSelPer];
-      load_score_batch(srow, j0, n, sv);
-      classify_batch(sv, j0, n, b1, bm, cs, &misc[7]);
-    }
+    classify_batch(sv0, j0, g_lo, g_hi, bm, cs, &misc[7]);
   }
   __syncthreads();
   const uint32_t nc = misc[7];
@@ -479,9 +447,10 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
     if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
   }
   __syncthreads();
-  emit_bitmap(bm, (n + 31) >> 5, idx, tmp);
-  for (int i = m + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
-  if (tid == 0) a.n_sel[unit] = m;
+  // m positions for scores as specified (fewer only with NaN scores)
+  const int got = (int)min(emit_bitmap(bm, (n + 31) >> 5, idx, (uint32_t)a.k, tmp), (uint32_t)m);
+  for (int i = got + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
+  if (tid == 0) a.n_sel[unit] = got;
 }
 
 // ---- attention -------------------------------------------------------------

@@ -100,6 +100,18 @@ def _select_case(name):
                 vals = np.append(vals, np.float32(-0.0))
             assert np.all(np.isfinite(vals))
             S[b, 0] = g.choice(vals, size=n)
+    elif name == "infinities":
+        # -inf scores (fp32 overflow of finite inputs) and +inf ones; in two
+        # units the k-th largest score is -inf itself
+        B, Hkv, n, k, lens = 2, 2, 5000, 1500, [5000, 3000]
+        S = np.full((B, Hkv, n), -np.inf, np.float32)
+        fin = g.permutation(n)[:1000]
+        S[0, 0, fin] = g.standard_normal(1000)
+        S[0, 1] = g.standard_normal(n)
+        S[0, 1, g.permutation(n)[:20]] = np.inf
+        mix = g.permutation(3000)
+        S[1, 1, mix[:700]] = g.standard_normal(700)
+        S[1, 1, mix[700:800]] = np.inf
     elif name == "budget_ge_context":
         B, Hkv, n, k, lens = 3, 2, 100, 128, [100, 64, 1]
         S = g.standard_normal((B, Hkv, n)).astype(np.float32)
@@ -123,7 +135,7 @@ def _select_case(name):
 
 
 @pytest.mark.parametrize("name", ["continuous", "ragged", "ties", "all_equal",
-                                  "signed_zero", "negative", "bin_edges",
+                                  "signed_zero", "negative", "bin_edges", "infinities",
                                   "budget_ge_context", "dense_cluster", "over_bitmap"])
 def test_select_topk_exact(name):
     """Same fp32 scores on both sides: the index sets must be identical."""
@@ -143,6 +155,40 @@ def test_select_topk_exact(name):
     ref_idx, ref_n = o.select_topk(so, S.astype(np.float64), lens, k, nthreads=8)
     np.testing.assert_array_equal(n_sel.cpu().numpy(), ref_n)
     np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+
+
+def test_select_topk_nan_stays_in_bounds():
+    """NaN scores are outside the contract (the set is then unspecified), but
+    the selection must still write only inside its rows: n_sel <= m,
+    ascending in-range positions before it, -1 after, nothing past idx."""
+    _log("select_topk NaN scores")
+    dev = device()
+    g = np.random.default_rng(77)
+    B, Hkv, n, k = 2, 2, 20000, 1000
+    lens = np.array([20000, 7000], np.int32)
+    S = g.standard_normal((B, Hkv, n)).astype(np.float32)
+    S[g.random(S.shape) < 0.1] = np.nan
+    S[1, 1, :] = np.nan  # a unit of NaN only
+    s = ckv.shape_for(B, Hkv, Hkv, n)
+    ws = ckv.workspace(s, k, ckv.ENTRY_SELECT_TOPK)
+    canary = 4096
+    flat = torch.full((B * Hkv * k + canary,), -7, dtype=torch.int32, device=dev)
+    idx = flat[: B * Hkv * k].view(B, Hkv, k)
+    n_sel = torch.full((B, Hkv), -9, dtype=torch.int32, device=dev)
+    ckv.select_topk(s, torch.from_numpy(S).to(dev), torch.from_numpy(lens).to(dev), k, idx,
+                    n_sel, ws)
+    torch.cuda.synchronize()
+    f = flat.cpu().numpy()
+    assert np.all(f[B * Hkv * k:] == -7)
+    I, N = idx.cpu().numpy(), n_sel.cpu().numpy()
+    for b in range(B):
+        for h in range(Hkv):
+            m = min(k, int(lens[b]))
+            ns = int(N[b, h])
+            assert 0 <= ns <= m, (b, h, ns)
+            row = I[b, h]
+            assert np.all(np.diff(row[:ns]) > 0) and np.all(row[:ns] >= 0)
+            assert np.all(row[:ns] < lens[b]) and np.all(row[ns:] == -1)
 
 
 # ---- gather_kv ---------------------------------------------------------------------
