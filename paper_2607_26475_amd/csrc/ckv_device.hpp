@@ -307,6 +307,15 @@ __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xF, ZERO_FILL);
 }
 
+// Workgroup barrier for LDS traffic only: waits for the wave's own LDS (and
+// scalar) operations, not for its outstanding global loads, which
+// __syncthreads would drain as well.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave, in DPP moves only: a
 // Hillis-Steele scan inside each row of 16 lanes (row_shr 1, 2, 4, 8, lanes
 // shifted in from outside the row read 0), then the total of row 0 added to

@@ -348,10 +348,10 @@ __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j
       float x = sv[u];
       asm volatile("" : "+v"(x));
       const int j = j0 + u * kFinishThreads + tid;
-      const uint64_t cm = __builtin_amdgcn_ballot_w64(x >= g_lo) &
-                          ~__builtin_amdgcn_ballot_w64(x >= g_hi);
-      if (x >= g_lo && !(x >= g_hi))
-        cs.lds[base + lanes_below(cm)] = make_uint2(__float_as_uint(x), (uint32_t)j);
+      // g_lo <= g_hi, so "in the bin" is the exclusive or of the two tests
+      const bool ge = x >= g_lo, hi = x >= g_hi;
+      const uint64_t cm = __builtin_amdgcn_ballot_w64(ge) & ~__builtin_amdgcn_ballot_w64(hi);
+      if (ge != hi) cs.lds[base + lanes_below(cm)] = make_uint2(__float_as_uint(x), (uint32_t)j);
       base += (uint32_t)__popcll(cm);
     }
   } else {
@@ -420,21 +420,30 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   }
   store_hist_sum(hv, nslots, lhist);
   if (tid == 64) misc[7] = 0u;
-  __syncthreads();
+  // the scores may still be in flight across both barriers
+  lds_barrier();
   if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
-  __syncthreads();
+  lds_barrier();
   const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
   const uint32_t b1 = misc[4], above = misc[5];
   const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
   const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
-  for (int j0 = 0; j0 < n; j0 += kSelBatch) {
-    if (j0) load_score_batch(srow, j0, n, sv0);
-    if (j0 + kSelBatch > n) {  // the last, partial batch: NaN past n_b
+  // the last, partial batch holds NaN past n_b
+  auto pad = [&](float (&sv)[kSelPer], int j0) {
+    if (j0 + kSelBatch > n) {
 #pragma unroll
       for (int u = 0; u < kSelPer; ++u)
-        if (j0 + u * kFinishThreads + tid >= n) sv0[u] = __builtin_nanf("");
+        if (j0 + u * kFinishThreads + tid >= n) sv[u] = __builtin_nanf("");
     }
-    classify_batch(sv0, j0, g_lo, g_hi, bm, cs, &misc[7]);
+  };
+  // the first batch apart, so that its compares start as its loads land
+  pad(sv0, 0);
+  classify_batch(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
+  for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {
+    float sv[kSelPer];
+    load_score_batch(srow, j0, n, sv);
+    pad(sv, j0);
+    classify_batch(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
   }
   __syncthreads();
   const uint32_t nc = misc[7];
