@@ -20,12 +20,14 @@ namespace ckv {
 template <int G>
 struct AttnLds {
   // K stage (4 waves x 16 rows, padded) | per-wave weight table
-  // [4][16 rows x G + G rescale] | per-wave partials [4][G][kD + 2]
+  // [4][16 rows x G + G rescale] | per-wave partials [4][G][kD + 2] |
+  // query rows in the MFMA A placement [16][kD] bf16 (rows past G zero)
   static constexpr int kStage = 4 * 16 * kStageRowDwords;
   static constexpr int kPTab = 16 * G + G + (G < 4 ? 4 - G : 0);
   static constexpr int kP = 4 * kPTab;
   static constexpr int kMerge = 4 * G * (kD + 2);
-  static constexpr int kFloats = kStage + kP + kMerge;
+  static constexpr int kQ = 16 * kStageRowDwords;
+  static constexpr int kFloats = kStage + kP + kMerge + kQ;
 };
 
 // All kAttnThreads threads of the workgroup must call this.  The workgroup
@@ -59,60 +61,60 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
   float* merge = lds + AttnLds<G>::kStage + AttnLds<G>::kP;
   float* part = a.part + ((int64_t)unit * a.chunks + chunk) * G * kPartStride;
 
-  // Source offsets of the rows this lane loads (block blk, load it -> row
-  // 16*blk + 4*it + lrow of the wave).  Rows past wrows load the wave's last
-  // row instead: every load is unconditional (lane-conditional loads make the
-  // compiler wait for all outstanding loads at each use), and those rows are
-  // masked out of the softmax.
+  // Rows this lane loads (block blk, load it -> row 16*blk + 4*it + lrow of
+  // the wave), as row numbers from the unit's base; the addresses are formed
+  // at each load, so only 32-bit row numbers stay live.  Rows past wrows load
+  // the wave's last row instead: every load is unconditional (lane-conditional
+  // loads make the compiler wait for all outstanding loads at each use), and
+  // those rows are masked out of the softmax.
   const int nblk = (wrows + 15) / 16;
-  int64_t off[kBlocks][4];
+  const int64_t stride = INDEXED ? a.row_stride : kD;
+  const int64_t ubase = (INDEXED ? (int64_t)unit * a.max_ctx : (int64_t)unit * a.k) * stride +
+                        8 * lchunk;
+  int row[kBlocks][4];
   if (wrows > 0) {
-    int pos[kBlocks][4];
 #pragma unroll
     for (int blk = 0; blk < kBlocks; ++blk)
 #pragma unroll
       for (int it = 0; it < 4; ++it) {
         const int i = min(16 * blk + 4 * it + lrow, wrows - 1);
-        pos[blk][it] = INDEXED ? a.idx[(int64_t)unit * a.k + w0 + i] : w0 + i;
-      }
-#pragma unroll
-    for (int blk = 0; blk < kBlocks; ++blk)
-#pragma unroll
-      for (int it = 0; it < 4; ++it) {
-        int ps = pos[blk][it];
-        if (INDEXED) {
-          ps = ps < 0 ? 0 : (ps >= a.max_ctx ? a.max_ctx - 1 : ps);
-          off[blk][it] = ((int64_t)unit * a.max_ctx + ps) * a.row_stride + 8 * lchunk;
-        } else {
-          off[blk][it] = ((int64_t)unit * a.k + ps) * kD + 8 * lchunk;
-        }
+        int ps = INDEXED ? a.idx[(int64_t)unit * a.k + w0 + i] : w0 + i;
+        if (INDEXED) ps = ps < 0 ? 0 : (ps >= a.max_ctx ? a.max_ctx - 1 : ps);
+        row[blk][it] = ps;
       }
   }
-  auto load_blk = [&](int blk, uint4* kv) {
+  auto load_rows = [&](const uint16_t* base, int blk, uint4* dst) {
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      kv[it] = ld16(a.k_rows + off[blk][it]);
-      kv[4 + it] = ld16(a.v_rows + off[blk][it]);
-    }
+    for (int it = 0; it < 4; ++it) dst[it] = ld16(base + ubase + (int64_t)row[blk][it] * stride);
   };
-  uint4 cur[8], nxt[8];
-  if (nblk > 0) load_blk(0, cur);
+  // K and V of one block each: the next block's K is requested once the
+  // current K is staged, its V once the current V is consumed (loads return
+  // in order, so each wait covers exactly the block it needs)
+  uint4 kr[4], vr[4];
+  if (nblk > 0) {
+    load_rows(a.k_rows, 0, kr);
+    load_rows(a.v_rows, 0, vr);
+  }
 
-  bf16x8 qa[4];
+  // the query rows go to LDS once, in the MFMA A placement, and are read
+  // back at every block rather than held in registers
+  uint32_t* qlds = reinterpret_cast<uint32_t*>(lds + AttnLds<G>::kStage + AttnLds<G>::kP +
+                                               AttnLds<G>::kMerge);
   {
     // two tokens: rows [0, G/2) are the current token's heads, the rest the
     // speculative token's (same KV head)
     const int Gq = a.q2 ? G / 2 : G;
-    const bool second = a.q2 && r16 >= Gq;
-    const uint16_t* qrow = (second ? a.q2 : a.q) +
-                           ((int64_t)b * a.Hq + (int64_t)h * Gq + (second ? r16 - Gq : r16)) *
-                               kD + 8 * kg;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int e = tid; e < 16 * (kD / 8); e += kAttnThreads) {
+      const int r = e / (kD / 8), c = e - r * (kD / 8);
       uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (r16 < G) v = ld16(qrow + 32 * t);
-      qa[t] = as_bf16x8(v);
+      if (r < G) {
+        const bool second = a.q2 && r >= Gq;
+        v = ld16((second ? a.q2 : a.q) +
+                 ((int64_t)b * a.Hq + (int64_t)h * Gq + (second ? r - Gq : r)) * kD + 8 * c);
+      }
+      *reinterpret_cast<uint4*>(qlds + r * kStageRowDwords + 4 * c) = v;
     }
+    __syncthreads();
   }
   // online state: register i of lane group kg is head 4*kg + i
   float m_i[4], l_i[4];
@@ -130,18 +132,25 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
 #pragma unroll
   for (int blk = 0; blk < kBlocks; ++blk) {
     if (blk >= nblk) break;  // uniform over the wave
-    if (blk + 1 < nblk) load_blk(blk + 1, nxt);
 #pragma unroll
     for (int it = 0; it < 4; ++it)
       *reinterpret_cast<uint4*>(stage + (4 * it + lrow) * kStageRowDwords + 4 * lchunk) =
-          cur[it];
+          kr[it];
     __builtin_amdgcn_wave_barrier();
+    // the scheduler would otherwise hoist the next block's loads above this
+    // block's work and hold both blocks in registers
+    __builtin_amdgcn_sched_barrier(0);
+    // unconditional (rows of blocks past nblk are the wave's last row): a
+    // conditional load would become a branch that the compiler hoists
+    if (blk + 1 < kBlocks) load_rows(a.k_rows, blk + 1, kr);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const uint4 kv = *reinterpret_cast<const uint4*>(
           stage + r16 * kStageRowDwords + 4 * (4 * t + kg));
-      acc = mfma_16x16x32(qa[t], as_bf16x8(kv), acc);
+      const uint4 qv = *reinterpret_cast<const uint4*>(
+          qlds + r16 * kStageRowDwords + 4 * (4 * t + kg));
+      acc = mfma_16x16x32(as_bf16x8(qv), as_bf16x8(kv), acc);
     }
     __builtin_amdgcn_wave_barrier();
     // logits of key r16 of the block for heads 4kg..4kg+3, block max and sum
@@ -188,7 +197,7 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
       float vf[8];
-      unpack8(cur[4 + it], vf);
+      unpack8(vr[it], vf);
       const float* pr = ptab + (4 * it + lrow) * G;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
@@ -196,10 +205,11 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
 #pragma unroll
         for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pg, vf[e], o[g][e]);
       }
+      __builtin_amdgcn_sched_barrier(0);  // one row's unpacked V live at a time
     }
     __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
+    __builtin_amdgcn_sched_barrier(0);
+    if (blk + 1 < kBlocks) load_rows(a.v_rows, blk + 1, vr);
   }
   // sum the four row phases (lrow) of each channel chunk
 #pragma unroll
