@@ -23,7 +23,7 @@ __all__ = [
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
     "critical_kv_attn", "corrected_attn", "chunk_landmarks", "select_chunks",
     "chunked_kv_attn", "dual_token_attn", "reconstruct_keys", "corrected_attn_lowrank",
-    "MAX_RANK", "profile_begin", "profile_end", "abi_version",
+    "MAX_RANK", "ABI_VERSION", "profile_begin", "profile_end", "abi_version",
     "Layer", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "EXPORTS",
@@ -45,6 +45,7 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_decode_step")
 KERNEL_COUNT = 13
 MAX_RANK = 4096
+ABI_VERSION = 3  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -133,6 +134,9 @@ def _load() -> ctypes.CDLL:
 
 
 _lib = _load()
+if _lib.ckv_abi_version() != ABI_VERSION:
+    raise ImportError(f"{LIB_PATH} has ABI {_lib.ckv_abi_version()}, the binding expects "
+                      f"{ABI_VERSION}; rebuild it")
 
 
 def abi_version() -> int:
