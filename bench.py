@@ -217,6 +217,10 @@ def main() -> int:
     chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
     log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} ms/step, "
         f"{chunked['tokens_per_s']:.0f} tokens/s")
+    pipelined_hbm = measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps,
+                                          stream)
+    log(f"pipelined, HBM: {pipelined_hbm['ms_per_step']:.3f} ms/step, "
+        f"{pipelined_hbm['tokens_per_s']:.0f} tokens/s, per layer {pipelined_hbm['per_layer_us']}")
 
     host_link = None
     if not args.no_host_link:
@@ -233,6 +237,12 @@ def main() -> int:
         pipeline["dual64"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "dual64",
                                               n_hbm=2, n_host=1, steps=3, runs=("plain",))
         log(f"pipeline dual64: {pipeline['dual64']}")
+        torch.cuda.empty_cache()
+        # the million-token single request
+        pipeline["million"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "million",
+                                               n_hbm=2, n_host=2, steps=4, runs=("plain",),
+                                               layer_queries=True)
+        log(f"pipeline million: {pipeline['million']}")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(layers, w, scale, np)
@@ -266,6 +276,7 @@ def main() -> int:
         "kernels": per_kernel,
         "roofline": roofline,
         "chunked": chunked,
+        "pipelined_hbm": pipelined_hbm,
         "dual_token": dual_token,
         "host_link": host_link,
         "pipeline": pipeline,
@@ -423,8 +434,73 @@ def measure_chunked(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream,
                         "(256 chunks) per KV head"}
 
 
+def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream):
+    """The Llama-8B step in the paper's pipelined form with the caches in HBM
+    (Sec. 4.1: the set a layer attends over at step t was selected at step
+    t-1 from the speculative token's query): one launch per layer attends
+    with the current query over last step's set, read in place through its
+    indices, and scores the keys with the speculative query; the selection
+    then picks next step's set.  Index sets alternate between two arrays per
+    layer by step parity.  Queries are step-invariant: the current one is the
+    layer's, the speculative one bf16(0.8 q + 0.6 noise)."""
+    B, Hq, Hkv, d, k, L = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k, w.layers
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(4321)
+    qs = [(0.8 * t["q"].float() + 0.6 * torch.randn(t["q"].shape, generator=g, device=dev))
+          .to(torch.bfloat16) for t in layers]
+    i32 = dict(dtype=torch.int32, device=dev)
+    idx = [[torch.empty((B, Hkv, k), **i32) for _ in range(L)] for _ in range(2)]
+    nsel = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(2)]
+    out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
+    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    cur = [0]
+
+    def step():
+        c = cur[0]
+        for l, t in enumerate(layers):
+            kp, vp = kv_ptrs[l]
+            ckv.critical_kv_attn(shape, t["q"], qs[l], kp, t["ctx_lens"], k, scale, kp, vp,
+                                 ckv.SRC_DEVICE, None, None, nsel[c][l], idx[1 - c][l],
+                                 nsel[1 - c][l], out[l], ws, stream, idx_in=idx[c][l])
+        cur[0] = 1 - c
+
+    # bootstrap (the pre-decoding step): same-step selection into set 0
+    for l, t in enumerate(layers):
+        kp, vp = kv_ptrs[l]
+        ckv.critical_kv_attn(shape, t["q"], qs[l], kp, t["ctx_lens"], k, scale, kp, vp,
+                             ckv.SRC_DEVICE, None, None, None, idx[0][l], nsel[0][l], out[l],
+                             ws, stream)
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    ckv.profile_begin()
+    step()
+    torch.cuda.synchronize()
+    per = {kname: round(1e3 * tot / c, 1) for kname, (c, tot, _) in ckv.profile_end().items()}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    assert all(torch.isfinite(o).all().item() for o in out[:2])
+    dual_bytes = B * Hkv * (w.max_ctx * d * 2 + k * 2 * d * 2)
+    res = {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3), "per_layer_us": per,
+           "workload": "the Llama-8B step above, pipelined: attention over last step's set "
+                       "read in place from HBM and scoring with the speculative query in "
+                       "one launch per layer"}
+    if "dual" in per:
+        res["dual_bytes_per_launch"] = dual_bytes
+        res["dual_GBps"] = dual_bytes / (per["dual"] * 1e-6) / 1e9
+    del qs, idx, nsel, out, ws
+    return res
+
+
 def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm=4, n_host=2,
-                     steps=4, runs=("plain", "corrected", "lowrank")):
+                     steps=4, runs=("plain", "corrected", "lowrank"), layer_queries=False,
+                     gather_width=0):
     """The two-buffer decode loop of 32 layers on a host-pinned workload: the
     long-context one (B8, 32 q / 8 KV heads, n 131072, k 4096) or the
     dual-token one (B64, n_b ~ U{16384..65536}, k 2048); K|V rows in pinned
@@ -437,24 +513,30 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
     stream); a third run rebuilds the misses' keys in every layer from rank-32
     factors (per (request, KV head), one set per host layer) and fetches only
     their values.  Step time from events on the compute stream after it has
-    joined the copy stream."""
+    joined the copy stream.  layer_queries: every step's query of a layer is
+    the workload's own query of that layer (the million-token keys cluster
+    along it), instead of fresh draws per step."""
     w = synth.WORKLOADS[wl]
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
     scale = float(np.float32(1.0 / math.sqrt(d)))
-    kscore, hosts = [], []
+    kscore, hosts, lq = [], [], []
     for i in range(n_hbm):
         t = synth.make_layer(w, seed=0, layer=i, device=dev)
         if i < n_host:
             hosts.append(synth.host_kv(t["k"], t["v"]))
         kscore.append(t["k"])
+        lq.append(t["q"])
         lens = t["ctx_lens"]
         del t
     torch.cuda.empty_cache()
     g = torch.Generator(device=dev)
     g.manual_seed(1234)
-    q = [[torch.randn((B, Hq, d), generator=g, device=dev).to(torch.bfloat16)
-          for _ in range(L)] for _ in range(steps + 3)]
+    if layer_queries:
+        q = [[lq[l % n_hbm] for l in range(L)] for _ in range(steps + 3)]
+    else:
+        q = [[torch.randn((B, Hq, d), generator=g, device=dev).to(torch.bfloat16)
+              for _ in range(L)] for _ in range(steps + 3)]
     qs = [[(0.8 * q[st + 1][l].float() + 0.6 * torch.randn((B, Hq, d), generator=g,
                                                            device=dev)).to(torch.bfloat16)
            for l in range(L)] for st in range(steps + 2)]
@@ -499,6 +581,8 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
             ckv.select_topk(s1, sc, lens, k, idx[0][l], nsel[0][l], wsel)
         torch.cuda.synchronize()
         pipe = ckv.Pipeline()
+        if gather_width:
+            pipe.set_gather_width(gather_width)
         copy.wait_stream(compute)
         pipe.prime(shape, k, io(0, 0), ckv.SRC_HOST_PINNED, k_buf, v_buf, copy)
         cur = 0
@@ -529,7 +613,8 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
                "gather_ms_per_step": gather_ms, "compute_kernels_ms_per_step": compute_ms,
                "kernels_ms_per_step": {kname: round(v[1] / steps, 4)
                                        for kname, v in stats.items()},
-               "overlap": (gather_ms + compute_ms) / ms}
+               "overlap": (gather_ms + compute_ms) / ms,
+               "gather_workgroups": gather_width or 256}
         if corrected:  # the misses cross the link too, on the compute stream
             found = sum(int(hits[st][l].sum()) for st in range(1, steps + 1) for l in range(L))
             total = steps * L * B * Hkv * min(k, n)

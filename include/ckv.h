@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 3
+#define CKV_ABI_VERSION 4
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -169,22 +169,30 @@ int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
 /* Fused decode step of one layer (Sec. 4.1, Sec. 5.2-5.4).  The selecting
  * query q_sel (the speculative token's; NULL means q_att) scores k_score and
  * picks idx_out / n_sel_out exactly as ckv_score_keys + ckv_select_topk.
- *   Same-step mode (k_buf == NULL): out = attention of q_att over the rows
- *     idx_out of k_src / v_src (read in place, src_kind says where), i.e.
- *     ckv_sparse_decode_attn applied to ckv_gather_kv(idx_out).
- *   Pipelined mode (k_buf != NULL): out = attention of q_att over
- *     k_buf/v_buf rows [0, n_sel_in) -- the set selected one step earlier
- *     and already assembled -- and, in the same launch, idx_out/n_sel_out are
- *     selected for the next step.  k_src/v_src are not read.
+ *   Same-step mode (idx_in == NULL, k_buf == NULL): out = attention of q_att
+ *     over the rows idx_out of k_src / v_src (read in place, src_kind says
+ *     where), i.e. ckv_sparse_decode_attn applied to ckv_gather_kv(idx_out).
+ *   Pipelined modes (Sec. 4.1: the set attended at step t was selected at
+ *   step t-1 from the speculative token's query): out = attention of q_att
+ *   over the set selected one step earlier, and in the same launch the
+ *   context is scored with q_sel for the next step's idx_out / n_sel_out.
+ *   The earlier set is either
+ *     assembled (k_buf != NULL): k_buf/v_buf rows [0, n_sel_in), as
+ *       ckv_gather_kv left them; k_src/v_src and idx_in are not read; or
+ *     in place (idx_in != NULL): rows idx_in[b][h][0..n_sel_in[b][h]) of
+ *       k_src / v_src, read where they are (the HBM-resident cache needs no
+ *       buffer); idx_in must not alias idx_out.
+ *   idx_in and k_buf together are CKV_EINVAL.
  * Workspace: CKV_ENTRY_CRITICAL_KV_ATTN. */
 int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          const uint16_t* q_sel, const uint16_t* k_score,
                          const int32_t* ctx_lens, int32_t k, float scale,
                          const uint16_t* k_src, const uint16_t* v_src,
-                         int src_kind, const uint16_t* k_buf,
-                         const uint16_t* v_buf, const int32_t* n_sel_in,
-                         int32_t* idx_out, int32_t* n_sel_out, float* out,
-                         void* ws, size_t ws_bytes, void* stream);
+                         int src_kind, const int32_t* idx_in,
+                         const uint16_t* k_buf, const uint16_t* v_buf,
+                         const int32_t* n_sel_in, int32_t* idx_out,
+                         int32_t* n_sel_out, float* out, void* ws,
+                         size_t ws_bytes, void* stream);
 
 /* Sec. 5.3 (prioritized missing KV transfer) and Sec. 5.4 (GPU-side sparse KV
  * assembly with deferred reordering) -- one layer of a pipelined decode step
@@ -357,6 +365,14 @@ typedef struct ckv_pipeline ckv_pipeline; /* events of one decode loop */
 /* Creates the events of one decode loop on the current device. */
 int ckv_pipeline_create(ckv_pipeline** pipe);
 int ckv_pipeline_destroy(ckv_pipeline* pipe);
+
+/* Workgroups of every refill this loop launches on its copy stream (0, the
+ * default: the width ckv_gather_kv uses, 256 for pinned host sources).  A
+ * gather that reads pinned host memory slows kernels on other streams while
+ * it runs: a narrower one (64 workgroups still carry the link's rate) leaves
+ * the compute stream its speed, for loops where that stream, not the link,
+ * sets the step time.  0 <= workgroups <= 4096, else CKV_EINVAL. */
+int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups);
 
 /* Starts a decode loop: gathers layer 0 (into buffer 0) and layer 1 (into
  * buffer 1) from their idx_prev/n_sel_prev on copy_stream.  Buffers are

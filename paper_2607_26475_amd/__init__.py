@@ -41,11 +41,12 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_chunked_kv_attn", "ckv_dual_token_attn", "ckv_reconstruct_keys",
            "ckv_corrected_attn_lowrank",
            "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
-           "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_prime",
+           "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
+           "ckv_pipeline_prime",
            "ckv_decode_step")
 KERNEL_COUNT = 13
 MAX_RANK = 4096
-ABI_VERSION = 3  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
+ABI_VERSION = 4  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -96,7 +97,7 @@ def _load() -> ctypes.CDLL:
                                                   vp, vp, sz, vp]),
         "ckv_critical_kv_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                                 vp, vp, ctypes.c_int, vp, vp, vp, vp, vp,
-                                                vp, vp, sz, vp]),
+                                                vp, vp, vp, sz, vp]),
         "ckv_corrected_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                               vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp,
                                               vp, vp, vp, vp, vp, sz, vp]),
@@ -118,6 +119,7 @@ def _load() -> ctypes.CDLL:
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
         "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
         "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
+        "ckv_pipeline_set_gather_width": (ctypes.c_int, [vp, ctypes.c_int]),
         "ckv_pipeline_prime": (ctypes.c_int, [vp, sp, i32, ctypes.POINTER(Layer), ctypes.c_int,
                                               ctypes.c_int, ctypes.POINTER(vp),
                                               ctypes.POINTER(vp), vp]),
@@ -220,10 +222,13 @@ def sparse_decode_attn(shape: Shape, q_att, k_buf, v_buf, n_sel, k: int,
 
 def critical_kv_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
                      scale: float, k_src, v_src, src_kind: int, k_buf, v_buf,
-                     n_sel_in, idx_out, n_sel_out, out, ws, stream=None) -> None:
+                     n_sel_in, idx_out, n_sel_out, out, ws, stream=None,
+                     idx_in=None) -> None:
+    """Same-step (k_buf and idx_in None), pipelined over an assembled buffer
+    (k_buf), or pipelined over the rows idx_in read in place."""
     _check("ckv_critical_kv_attn", _lib.ckv_critical_kv_attn(
         ctypes.byref(shape), _ptr(q_att), _ptr(q_sel), _ptr(k_score), _ptr(ctx_lens), k,
-        scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(k_buf), _ptr(v_buf),
+        scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(idx_in), _ptr(k_buf), _ptr(v_buf),
         _ptr(n_sel_in), _ptr(idx_out), _ptr(n_sel_out), _ptr(out), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
 
@@ -346,6 +351,10 @@ class Pipeline:
             self.close()
         except Exception:
             pass
+
+    def set_gather_width(self, workgroups: int) -> None:
+        _check("ckv_pipeline_set_gather_width",
+               _lib.ckv_pipeline_set_gather_width(self._h, workgroups))
 
     @staticmethod
     def _bufs(k_buf, v_buf):

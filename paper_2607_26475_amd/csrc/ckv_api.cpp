@@ -255,6 +255,7 @@ ReconArgs recon_args(const Dims& d, int32_t rank, const uint16_t* u_fac, const u
 // 256 workgroups keep at its copy rate; device sources take a full grid.
 int gather_blocks(int src_kind) { return src_kind == CKV_SRC_HOST_PINNED ? 256 : 4096; }
 
+
 SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* scores,
                        const int32_t* ctx_lens, int32_t k, int32_t* idx, int32_t* n_sel) {
   SelectArgs a;
@@ -408,6 +409,41 @@ int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
 
 }  // namespace
 
+int ckv::gather_kv_width(const ckv_shape* shape, const uint16_t* k_src, const uint16_t* v_src,
+                    int src_kind, const int32_t* idx, const int32_t* n_sel, int32_t k,
+                    uint16_t* k_dst, uint16_t* v_dst, int workgroups, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  CKV_PTR(k_src);
+  CKV_PTR(v_src);
+  CKV_PTR(idx);
+  CKV_PTR(n_sel);
+  CKV_PTR(k_dst);
+  CKV_PTR(v_dst);
+  if (workgroups < 0 || workgroups > kMaxGatherWgs)
+    return fail(CKV_EINVAL, "gather width %d outside [0, %d]", workgroups, kMaxGatherWgs);
+  if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
+  if (d.U == 0) return CKV_OK;
+  GatherArgs a;
+  a.k_src = k_src;
+  a.v_src = v_src;
+  a.idx = idx;
+  a.n_sel = n_sel;
+  a.slots = nullptr;
+  a.k_dst = k_dst;
+  a.v_dst = v_dst;
+  a.row_stride = d.kv_stride;
+  a.items = (int64_t)d.U * k * 32;
+  a.max_ctx = d.max_ctx;
+  a.k = k;
+  CKV_TRY_HIP(launch_gather(a, workgroups ? workgroups : gather_blocks(src_kind),
+                            (hipStream_t)stream),
+              "gather launch");
+  return CKV_OK;
+}
+
 extern "C" {
 
 int ckv_abi_version(void) { return CKV_ABI_VERSION; }
@@ -483,32 +519,8 @@ int ckv_select_topk(const ckv_shape* shape, const float* scores, const int32_t* 
 int ckv_gather_kv(const ckv_shape* shape, const uint16_t* k_src, const uint16_t* v_src,
                   int src_kind, const int32_t* idx, const int32_t* n_sel, int32_t k,
                   uint16_t* k_dst, uint16_t* v_dst, void* stream) {
-  Dims d;
-  int rc = check_shape(shape, &d);
-  if (rc) return rc;
-  if ((rc = check_k(k))) return rc;
-  CKV_PTR(k_src);
-  CKV_PTR(v_src);
-  CKV_PTR(idx);
-  CKV_PTR(n_sel);
-  CKV_PTR(k_dst);
-  CKV_PTR(v_dst);
-  if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
-  if (d.U == 0) return CKV_OK;
-  GatherArgs a;
-  a.k_src = k_src;
-  a.v_src = v_src;
-  a.idx = idx;
-  a.n_sel = n_sel;
-  a.slots = nullptr;
-  a.k_dst = k_dst;
-  a.v_dst = v_dst;
-  a.row_stride = d.kv_stride;
-  a.items = (int64_t)d.U * k * 32;
-  a.max_ctx = d.max_ctx;
-  a.k = k;
-  CKV_TRY_HIP(launch_gather(a, gather_blocks(src_kind), (hipStream_t)stream), "gather launch");
-  return CKV_OK;
+  return ckv::gather_kv_width(shape, k_src, v_src, src_kind, idx, n_sel, k, k_dst, v_dst, 0,
+                              stream);
 }
 
 int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
@@ -540,7 +552,7 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          const uint16_t* q_sel, const uint16_t* k_score,
                          const int32_t* ctx_lens, int32_t k, float scale,
                          const uint16_t* k_src, const uint16_t* v_src, int src_kind,
-                         const uint16_t* k_buf, const uint16_t* v_buf,
+                         const int32_t* idx_in, const uint16_t* k_buf, const uint16_t* v_buf,
                          const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out,
                          float* out, void* ws, size_t ws_bytes, void* stream) {
   Dims d;
@@ -556,14 +568,19 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   CKV_PTR(idx_out);
   CKV_PTR(n_sel_out);
   CKV_PTR(out);
-  const bool pipelined = k_buf != nullptr;
-  if (pipelined) {
+  if (idx_in && k_buf)
+    return fail(CKV_EINVAL, "idx_in and k_buf are exclusive (rows in place or assembled)");
+  // pipelined: the attended set was selected one step earlier, either
+  // assembled in k_buf/v_buf or read in place through idx_in
+  const bool assembled = k_buf != nullptr, in_place = idx_in != nullptr;
+  if (assembled) {
     CKV_PTR(k_buf);
     CKV_PTR(v_buf);
     CKV_PTR(n_sel_in);
   } else {
     CKV_PTR(k_src);
     CKV_PTR(v_src);
+    if (in_place) CKV_PTR(n_sel_in);
     if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
   }
   Layout L = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN);
@@ -574,15 +591,18 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   float* scores = at<float>(ws, L.scores);
   SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
   ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, sa.hist, sa.coarse);
-  const int nwg = score_blocks(sc, d.G, pipelined, false);
+  const bool pipelined = assembled || in_place;
+  const int nwg = score_blocks(sc, d.G, pipelined, in_place);
   if (use_partials(d, L, nwg))
     set_partials(ws, L, nwg, &sc, &sa);
   else
     CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
   if (pipelined) {
-    AttnArgs at_ = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel_in, kD, k,
-                             scale, out);
-    CKV_TRY_HIP(launch_dual(at_, sc, d.G, false, d.U, s), "dual launch");
+    AttnArgs at_ = assembled ? attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel_in, kD,
+                                         k, scale, out)
+                             : attn_args(d, L, ws, q_att, k_src, v_src, idx_in, n_sel_in,
+                                         d.kv_stride, k, scale, out);
+    CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, s), "dual launch");
     if ((rc = run_select_tail(sa, d.U, s))) return rc;
     CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
   } else {

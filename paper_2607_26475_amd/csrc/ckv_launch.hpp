@@ -1,6 +1,7 @@
 // ckv_launch.hpp -- host-side launchers of the libckv kernels.
 #pragma once
 
+#include "ckv.h"
 #include "ckv_device.hpp"
 
 namespace ckv {
@@ -32,5 +33,13 @@ hipError_t launch_reconstruct(const ReconArgs& a, hipStream_t s);
 hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconArgs& r,
                             hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s);
+
+// Largest gather grid a caller may ask for.
+constexpr int kMaxGatherWgs = 4096;
+// ckv_gather_kv with an explicit grid: `workgroups` (0: the default for
+// src_kind) bounds the workgroups that stream the rows.
+int gather_kv_width(const ckv_shape* shape, const uint16_t* k_src, const uint16_t* v_src,
+                    int src_kind, const int32_t* idx, const int32_t* n_sel, int32_t k,
+                    uint16_t* k_dst, uint16_t* v_dst, int workgroups, void* stream);
 
 }  // namespace ckv

@@ -12,6 +12,7 @@ struct ckv_pipeline {
   hipEvent_t freed[2];   // the attention that read buffer i has been enqueued before this
   unsigned long long filled_capture[2];  // capture filled[i] was last recorded in (0: none)
   int parity;            // buffer of the next layer to compute
+  int gather_wgs;        // workgroups of each refill (0: the gather's default)
 };
 
 namespace {
@@ -24,10 +25,11 @@ unsigned long long capture_id(hipStream_t s) {
   return st == hipStreamCaptureStatusActive ? id : 0;
 }
 
-int gather_layer(const ckv_shape* shape, int32_t k, const ckv_layer& L, const int32_t* idx,
-                 const int32_t* n_sel, int src_kind, uint16_t* kb, uint16_t* vb,
-                 void* stream) {
-  return ckv_gather_kv(shape, L.k_src, L.v_src, src_kind, idx, n_sel, k, kb, vb, stream);
+int gather_layer(const ckv_pipeline* p, const ckv_shape* shape, int32_t k, const ckv_layer& L,
+                 const int32_t* idx, const int32_t* n_sel, int src_kind, uint16_t* kb,
+                 uint16_t* vb, void* stream) {
+  return ckv::gather_kv_width(shape, L.k_src, L.v_src, src_kind, idx, n_sel, k, kb, vb,
+                              p->gather_wgs, stream);
 }
 
 }  // namespace
@@ -47,8 +49,18 @@ int ckv_pipeline_create(ckv_pipeline** pipe) {
     }
   }
   p->parity = 0;
+  p->gather_wgs = 0;
   p->filled_capture[0] = p->filled_capture[1] = 0;
   *pipe = p;
+  return CKV_OK;
+}
+
+int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups) {
+  if (!pipe) return ckv::fail(CKV_EINVAL, "pipe is NULL");
+  if (workgroups < 0 || workgroups > ckv::kMaxGatherWgs)
+    return ckv::fail(CKV_EINVAL, "gather width %d outside [0, %d]", workgroups,
+                     ckv::kMaxGatherWgs);
+  pipe->gather_wgs = workgroups;
   return CKV_OK;
 }
 
@@ -70,7 +82,7 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
     return ckv::fail(CKV_EINVAL, "pipe, layers (at least 2) and both buffers are required");
   pipe->parity = 0;
   for (int l = 0; l < 2; ++l) {
-    int rc = gather_layer(shape, k, layers[l], layers[l].idx_prev, layers[l].n_sel_prev,
+    int rc = gather_layer(pipe, shape, k, layers[l], layers[l].idx_prev, layers[l].n_sel_prev,
                           src_kind, k_buf[l], v_buf[l], copy_stream);
     if (rc) return rc;
     hipError_t e = hipEventRecord(pipe->filled[l], (hipStream_t)copy_stream);
@@ -112,7 +124,8 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                               L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
     } else {
       rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
-                                nullptr, nullptr, src_kind, k_buf[p], v_buf[p], L.n_sel_prev,
+                                nullptr, nullptr, src_kind, nullptr, k_buf[p], v_buf[p],
+                                L.n_sel_prev,
                                 L.idx_next, L.n_sel_next, L.out, ws, ws_bytes,
                                 compute_stream);
     }
@@ -124,11 +137,11 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
       return ckv::hip_fail(e, "wait for a buffer release");
     const int j = l + 2;
     if (j < num_layers) {
-      rc = gather_layer(shape, k, layers[j], layers[j].idx_prev, layers[j].n_sel_prev,
+      rc = gather_layer(pipe, shape, k, layers[j], layers[j].idx_prev, layers[j].n_sel_prev,
                         src_kind, k_buf[p], v_buf[p], copy_stream);
     } else {
       const ckv_layer& N = layers[j - num_layers];
-      rc = gather_layer(shape, k, N, N.idx_next, N.n_sel_next, src_kind, k_buf[p], v_buf[p],
+      rc = gather_layer(pipe, shape, k, N, N.idx_next, N.n_sel_next, src_kind, k_buf[p], v_buf[p],
                         copy_stream);
     }
     if (rc) return rc;

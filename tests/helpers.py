@@ -195,5 +195,17 @@ class Run:
         torch.cuda.synchronize()
         return s
 
+    def in_place(self, q_att, q_sel, k_score, k_src, v_src, src_kind, idx_in, n_sel_in,
+                 kv_stride=None):
+        """Pipelined over the rows idx_in of k_src/v_src, read where they are."""
+        w = self.w
+        s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx, kv_row_stride=kv_stride)
+        ws = ckv.workspace(s, w.k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        ckv.critical_kv_attn(s, q_att, q_sel, k_score, self.lens, w.k, SCALE, k_src, v_src,
+                             src_kind, None, None, n_sel_in, self.idx, self.n_sel, self.out,
+                             ws, idx_in=idx_in)
+        torch.cuda.synchronize()
+        return s
+
     def host(self):
         return (self.idx.cpu().numpy(), self.n_sel.cpu().numpy(), self.out.cpu().numpy())

@@ -33,7 +33,7 @@ def test_header_functions_are_exported():
 
 
 def test_abi_version_and_status_text():
-    assert ckv.abi_version() == 3
+    assert ckv.abi_version() == ckv.ABI_VERSION == 4
     texts = {ckv.status_str(v) for v in STATUS.values()}
     assert len(texts) == len(STATUS)
     assert ckv.status_str(99) == "unknown status"
@@ -118,6 +118,7 @@ def test_pipeline_argument_checks():
     bufs = (ctypes.c_void_p * 2)(FAKE, FAKE)
     assert lib.ckv_pipeline_create(None) == STATUS["EINVAL"]
     assert lib.ckv_pipeline_destroy(None) == STATUS["OK"]
+    assert lib.ckv_pipeline_set_gather_width(None, 64) == STATUS["EINVAL"]
     layers = (ckv.Layer * 2)()
     assert lib.ckv_pipeline_prime(None, ctypes.byref(s), 16, layers, 2, 0, bufs, bufs,
                                   None) == STATUS["EINVAL"]
@@ -230,3 +231,24 @@ def test_layer_struct_layout(tmp_path):
     got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
                                           check=True).stdout.split()]
     assert got == [getattr(ckv.Layer, n).offset for n in names] + [ctypes.sizeof(ckv.Layer)]
+
+
+def test_critical_kv_attn_mode_checks():
+    """idx_in (rows in place) and k_buf (assembled rows) are exclusive; each
+    pipelined mode needs n_sel_in."""
+    lib = ckv._lib
+    s = good_shape()
+    need = ckv.workspace_bytes(s, 16, ckv.ENTRY_CRITICAL_KV_ATTN)
+
+    def call(idx_in=None, k_buf=None, v_buf=None, n_in=None, k_src=FAKE, v_src=FAKE):
+        return lib.ckv_critical_kv_attn(ctypes.byref(s), FAKE, None, FAKE, FAKE, 16, 0.1,
+                                        k_src, v_src, 0, idx_in, k_buf, v_buf, n_in, FAKE,
+                                        FAKE, FAKE, FAKE, need, 0)
+
+    assert call(idx_in=FAKE, k_buf=FAKE, v_buf=FAKE, n_in=FAKE) == STATUS["EINVAL"]
+    assert call(idx_in=FAKE) == STATUS["EINVAL"]             # no n_sel_in
+    assert call(idx_in=FAKE, n_in=FAKE, k_src=None) == STATUS["EINVAL"]
+    assert call(k_buf=FAKE, v_buf=FAKE) == STATUS["EINVAL"]  # no n_sel_in
+    assert "exclusive" in (lib.ckv_critical_kv_attn(
+        ctypes.byref(s), FAKE, None, FAKE, FAKE, 16, 0.1, FAKE, FAKE, 0, FAKE, FAKE, FAKE,
+        FAKE, FAKE, FAKE, FAKE, FAKE, need, 0), ckv._lib.ckv_last_error_detail().decode())[1]

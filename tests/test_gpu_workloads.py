@@ -12,8 +12,8 @@ import torch
 
 import paper_2607_26475_amd as ckv
 import synth
-from helpers import (ATOL_OUT, SCALE, Run, check_index_sets, device, oracle_attn_over, orc,
-                     u16)
+from helpers import (ATOL_OUT, SCALE, Run, check_index_sets, device, make_prediction,
+                     oracle_attn_over, orc, u16)
 
 pytestmark = pytest.mark.gpu
 
@@ -109,6 +109,67 @@ def test_pipelined_host_pinned(wl):
             rows = torch.from_numpy(p_idx[b, h, :m].astype(np.int64))
             assert torch.equal(kb[b, h, :m].view(torch.int16),
                                t["k"][b, h].cpu()[rows].view(torch.int16))
+
+
+IN_PLACE_CASES = [
+    ("tiny", "speculative", "separate"),
+    ("llama8b_s", "half", "interleaved"),
+    ("dual64_s", "beyond", "separate"),
+    ("dual64_s", "empty", "interleaved"),
+    ("long128k_s", "speculative", "host"),
+]
+
+
+@pytest.mark.parametrize("wl,kind,layout", IN_PLACE_CASES)
+def test_pipelined_in_place(wl, kind, layout):
+    """Pipelined entry over a set selected one step earlier and read in place
+    through idx_in (no assembled buffer): out is the attention of q_att over
+    exactly the rows idx_in, idx_out the selection of q_sel for the next
+    step.  The earlier sets are forced from the host: the speculative query's
+    own selection, half of the current query's set replaced, distinct
+    positions anywhere in the stored rows (past short contexts too), none."""
+    _log("pipelined in place", wl, kind, layout)
+    dev = device()
+    w = synth.WORKLOADS[wl]
+    B, Hq, Hkv, d, k, n = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k, w.max_ctx
+    t = synth.make_layer(w, seed=4, device=dev)
+    lens = t["ctx_lens"]
+    lens_h = lens.cpu().numpy()
+    q_att, q_sel, K, V = u16(t["q"]), u16(t["q_sel"]), u16(t["k"]), u16(t["v"])
+    o = orc()
+    so = o.shape(B, Hq, Hkv, d, n)
+    S_att = o.score_keys(so, q_att, K, lens_h, SCALE, nthreads=8)
+    S_sel = o.score_keys(so, q_sel, K, lens_h, SCALE, nthreads=8)
+    pred, npred = make_prediction(kind, S_att, S_sel, lens_h, k, n, np.random.default_rng(11))
+    keep = None
+    if layout == "host":
+        keep = synth.host_kv(t["k"], t["v"])
+        k_src, v_src, stride, kind_src = keep.data_ptr(), keep.data_ptr() + 2 * d, 2 * d, \
+            ckv.SRC_HOST_PINNED
+    elif layout == "interleaved":
+        keep = synth.interleave_kv(t["k"], t["v"])
+        k_src, v_src, stride, kind_src = keep.data_ptr(), keep.data_ptr() + 2 * d, 2 * d, \
+            ckv.SRC_DEVICE
+    else:
+        k_src, v_src, stride, kind_src = t["k"], t["v"], None, ckv.SRC_DEVICE
+    idx_in = torch.from_numpy(pred).to(dev)
+    n_in = torch.from_numpy(npred).to(dev)
+    run = Run(w, lens, dev)
+    run.in_place(t["q"], t["q_sel"], t["k"], k_src, v_src, kind_src, idx_in, n_in,
+                 kv_stride=stride)
+    g_idx, g_nsel, g_out = run.host()
+    r_idx, r_nsel = o.select_topk(so, S_sel, lens_h, k, nthreads=8)
+    swaps = check_index_sets(g_idx, g_nsel, r_idx, r_nsel, S_sel, lens_h)
+    _log("  units with tolerated swaps:", swaps)
+    ref = oracle_attn_over(so, q_att, K, V, pred, npred, k)
+    err = np.abs(g_out - ref).max()
+    _log("  max abs err vs oracle over idx_in:", err)
+    assert err <= ATOL_OUT
+    if kind == "empty":
+        assert not g_out.any()
+    # the earlier set was read, not written
+    np.testing.assert_array_equal(idx_in.cpu().numpy(), pred)
+    del keep
 
 
 def _sampled_units(w, count, seed):
