@@ -498,6 +498,19 @@ def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, s
     return res
 
 
+_STREAMS = []
+
+
+def _pipeline_streams(torch):
+    """The compute and copy streams of every decode loop, created once and in
+    succession: streams share the device's few hardware queues round-robin,
+    and a copy stream that landed on the compute stream's queue would
+    serialise the loop."""
+    if not _STREAMS:
+        _STREAMS.extend([torch.cuda.Stream(), torch.cuda.Stream()])
+    return _STREAMS[0], _STREAMS[1]
+
+
 def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm=4, n_host=2,
                      steps=4, runs=("plain", "corrected", "lowrank"), layer_queries=False,
                      gather_width=0):
@@ -551,8 +564,7 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
     v_buf = [torch.empty_like(k_buf[0]) for _ in range(2)]
     shape = ckv.shape_for(B, Hq, Hkv, n, kv_row_stride=2 * d)
     ws = ckv.workspace(shape, k, ckv.ENTRY_CORRECTED_ATTN)
-    compute = torch.cuda.current_stream()
-    copy = torch.cuda.Stream()
+    compute, copy = _pipeline_streams(torch)
     s1 = ckv.shape_for(B, Hq, Hkv, n)
     sc = torch.empty((B, Hkv, n), device=dev)
     wsel = ckv.workspace(s1, k, ckv.ENTRY_SELECT_TOPK)
@@ -614,7 +626,7 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
                "kernels_ms_per_step": {kname: round(v[1] / steps, 4)
                                        for kname, v in stats.items()},
                "overlap": (gather_ms + compute_ms) / ms,
-               "gather_workgroups": gather_width or 256}
+               "gather_workgroups": gather_width or ("auto: 64" if n >= 64 * k else "auto: 256")}
         if corrected:  # the misses cross the link too, on the compute stream
             found = sum(int(hits[st][l].sum()) for st in range(1, steps + 1) for l in range(L))
             total = steps * L * B * Hkv * min(k, n)

@@ -366,12 +366,14 @@ typedef struct ckv_pipeline ckv_pipeline; /* events of one decode loop */
 int ckv_pipeline_create(ckv_pipeline** pipe);
 int ckv_pipeline_destroy(ckv_pipeline* pipe);
 
-/* Workgroups of every refill this loop launches on its copy stream (0, the
- * default: the width ckv_gather_kv uses, 256 for pinned host sources).  A
+/* Workgroups of every refill this loop launches on its copy stream.  A
  * gather that reads pinned host memory slows kernels on other streams while
- * it runs: a narrower one (64 workgroups still carry the link's rate) leaves
+ * it runs; a narrower one (64 workgroups still carry the link's rate) leaves
  * the compute stream its speed, for loops where that stream, not the link,
- * sets the step time.  0 <= workgroups <= 4096, else CKV_EINVAL. */
+ * sets the step time.  0 (the default) chooses by shape: 64 workgroups for
+ * pinned sources when max_ctx >= 64 k (the scoring pass then reads at least
+ * 32 times the bytes the link carries per layer), else what ckv_gather_kv
+ * uses (256 for pinned sources).  0 <= workgroups <= 4096, else CKV_EINVAL. */
 int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups);
 
 /* Starts a decode loop: gathers layer 0 (into buffer 0) and layer 1 (into

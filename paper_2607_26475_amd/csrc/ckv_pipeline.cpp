@@ -25,11 +25,23 @@ unsigned long long capture_id(hipStream_t s) {
   return st == hipStreamCaptureStatusActive ? id : 0;
 }
 
+// Refill grid when the caller set none.  A gather reading pinned host memory
+// with one workgroup per CU slows the compute stream's kernels several-fold
+// while it runs; 64 workgroups still carry the link's rate and leave them
+// their speed, but lose a few percent of it beside them.  The compute stream
+// reads about max_ctx/(2k) times the bytes the link carries per layer (the
+// scoring pass's keys against the selected K|V rows); from a ratio of 32 on,
+// its slowed kernels, not the link, would set the step time.
+int refill_width(const ckv_pipeline* p, const ckv_shape* shape, int32_t k, int src_kind) {
+  if (p->gather_wgs || src_kind != CKV_SRC_HOST_PINNED || !shape || k < 1) return p->gather_wgs;
+  return (int64_t)shape->max_ctx >= 64 * (int64_t)k ? 64 : 0;
+}
+
 int gather_layer(const ckv_pipeline* p, const ckv_shape* shape, int32_t k, const ckv_layer& L,
                  const int32_t* idx, const int32_t* n_sel, int src_kind, uint16_t* kb,
                  uint16_t* vb, void* stream) {
   return ckv::gather_kv_width(shape, L.k_src, L.v_src, src_kind, idx, n_sel, k, kb, vb,
-                              p->gather_wgs, stream);
+                              refill_width(p, shape, k, src_kind), stream);
 }
 
 }  // namespace
