@@ -87,6 +87,9 @@ def main() -> int:
                     help="K and V caches as two arrays, or K|V interleaved per position")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-host-link", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the dual-token, chunked, graph and pipelined-HBM sections "
+                         "(the main step alone, e.g. for its kernel profile)")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the pipelined long-context measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -211,16 +214,22 @@ def main() -> int:
     log(f"dominant kernel {dominant}: {avg_s * 1e6:.1f} us/launch, "
         f"{achieved:.0f} GB/s algorithmic")
 
-    dual_token = measure_dual_token(torch, ckv, w, scale, stream)
-    log(f"dual-token attention: co-batched {dual_token['co_batched_us']:.1f} us, two launches "
-        f"{dual_token['two_launches_us']:.1f} us per layer")
-    chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
-    log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} ms/step, "
-        f"{chunked['tokens_per_s']:.0f} tokens/s")
-    pipelined_hbm = measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps,
-                                          stream)
-    log(f"pipelined, HBM: {pipelined_hbm['ms_per_step']:.3f} ms/step, "
-        f"{pipelined_hbm['tokens_per_s']:.0f} tokens/s, per layer {pipelined_hbm['per_layer_us']}")
+    dual_token = chunked = graph = pipelined_hbm = None
+    if not args.no_extras:
+        dual_token = measure_dual_token(torch, ckv, w, scale, stream)
+        log(f"dual-token attention: co-batched {dual_token['co_batched_us']:.1f} us, two "
+            f"launches {dual_token['two_launches_us']:.1f} us per layer")
+        chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
+        log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} "
+            f"ms/step, {chunked['tokens_per_s']:.0f} tokens/s")
+        graph = measure_graph(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, idx, out)
+        log(f"graph replay: {graph['ms_per_step']:.3f} ms/step, {graph['tokens_per_s']:.0f} "
+            f"tokens/s, bit-identical {graph['bit_identical_to_eager']}")
+        pipelined_hbm = measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, s, w, scale,
+                                              args.steps, stream)
+        log(f"pipelined, HBM: {pipelined_hbm['ms_per_step']:.3f} ms/step, "
+            f"{pipelined_hbm['tokens_per_s']:.0f} tokens/s, per layer "
+            f"{pipelined_hbm['per_layer_us']}")
 
     host_link = None
     if not args.no_host_link:
@@ -277,6 +286,7 @@ def main() -> int:
         "roofline": roofline,
         "chunked": chunked,
         "pipelined_hbm": pipelined_hbm,
+        "graph": graph,
         "dual_token": dual_token,
         "host_link": host_link,
         "pipeline": pipeline,
@@ -432,6 +442,59 @@ def measure_chunked(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream,
             "per_layer_us": per, "landmark_bytes_per_layer": B * Hkv * cmax * d * 2,
             "workload": "the Llama-8B step above, chunk landmarks of 8 rows, k 2048 rows "
                         "(256 chunks) per KV head"}
+
+
+def measure_graph(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, ref_idx, ref_out):
+    """The same Llama-8B step captured once into a HIP graph and replayed, as
+    a serving loop would run it: the 128 launches of a step go to the device
+    as one graph launch.  Every replay recomputes everything from the inputs;
+    the first replay's index sets and outputs are checked bit for bit against
+    the eager step's."""
+    B, Hq, Hkv, d, k, L = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k, w.layers
+    dev = torch.device("cuda:0")
+    i32 = dict(dtype=torch.int32, device=dev)
+    idx = [torch.empty((B, Hkv, k), **i32) for _ in range(L)]
+    nsel = [torch.empty((B, Hkv), **i32) for _ in range(L)]
+    out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
+    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+
+    def step():  # on the current stream: the capture stream inside the capture
+        for l, t in enumerate(layers):
+            kp, vp = kv_ptrs[l]
+            ckv.critical_kv_attn(shape, t["q"], None, kp, t["ctx_lens"], k, scale, kp, vp,
+                                 ckv.SRC_DEVICE, None, None, None, idx[l], nsel[l], out[l], ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for o in out:
+        o.fill_(float("nan"))
+    graph.replay()
+    torch.cuda.synchronize()
+    same = all(torch.equal(idx[l], ref_idx[l]) and torch.equal(out[l], ref_out[l])
+               for l in range(L))
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    del graph, idx, nsel, out, ws
+    return {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3), "bit_identical_to_eager": same,
+            "workload": "the Llama-8B step above (same-step, K/V in HBM), one graph launch "
+                        "per step"}
 
 
 def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream):
