@@ -7,10 +7,15 @@
 // combine kernel merges chunks.
 //
 // Logits: Q[G x d] . K_chunk^T on MFMA (bf16 products are exact, fp32
-// accumulation), same operand placement as the scoring pass.  Weights and the
-// weighted V sum stay in fp32 on the VALU: rounding the weights to bf16 for an
-// MFMA would cost up to 2^-9 relative per weight.  An empty chunk (all rows
-// past n_sel) yields m = -inf and zero sums, which the combine ignores.
+// accumulation), same operand placement as the scoring pass.  Softmax weights
+// are fp32.  The weighted V sum also runs on MFMA: each fp32 weight p is split
+// into two bf16 parts, hi = bf16(p) and lo = bf16(p - hi) (p - hi is exact in
+// fp32), and one 16x16x32 product takes both parts against the same V entry,
+// so hi*v + lo*v is accumulated in fp32 with exact products.  |p - hi - lo| <=
+// 2^-18 p, so the sum carries at most 2^-18 of sum_i p_i |v_i| beyond fp32
+// accumulation (a bf16 weight alone would cost up to 2^-9).  An empty chunk
+// (all rows past n_sel) yields m = -inf and zero sums, which the combine
+// ignores.
 #pragma once
 
 #include "ckv_device.hpp"
@@ -41,8 +46,13 @@ struct AttnLds {
 //
 // Loads: every instruction reads four whole 256-byte rows (16 lanes x 16
 // bytes per row), K and V alike.  K goes through a padded per-wave LDS stage
-// into the MFMA operand placement (logits Q[G x d] . K^T on MFMA); V stays in
-// registers in exactly the placement the weighted sum needs.
+// into the MFMA operand placement (logits Q[G x d] . K^T on MFMA).  V stays in
+// registers: lane (r, c) of the wave (r = lane / 16, c = lane % 16) holds
+// channels [8c, 8c + 8) of block rows r, r + 4, r + 8, r + 12, which is the
+// B placement of a 16x16x32 product over those four rows (each twice, for
+// the hi and lo weight parts) for one channel of each 8-channel group.  Eight
+// products per block, one per channel offset e, accumulate
+// O[head][8n + e] in lane (head / 4, n), register head % 4.
 template <int G, bool INDEXED>
 __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
                                            int chunk, float* lds) {
@@ -123,11 +133,11 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
     m_i[i] = -INFINITY;
     l_i[i] = 0.f;
   }
-  float o[G][8];
+  // weighted V sums: oacc[e][j] = O[head 4*kg + j][8*r16 + e]
+  static_assert(G <= 16, "the heads fill at most the 16 rows of a product");
+  f32x4 oacc[8];
 #pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+  for (int e = 0; e < 8; ++e) oacc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int blk = 0; blk < kBlocks; ++blk) {
@@ -185,48 +195,56 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
     }
     const bool rescale = __any(moved);  // running max moved for some head
     __builtin_amdgcn_wave_barrier();
-    // weighted V sum: lane holds channels [8*lchunk, +8) of rows 4*it + lrow
+    // rescale factors are lane-local: register j of lane group kg is head 4kg+j
     if (rescale) {
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float alpha = ptab[16 * G + g];
+      for (int e = 0; e < 8; ++e)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[g][e] *= alpha;
-      }
+        for (int j = 0; j < 4; ++j) oacc[e][j] *= al[j];
     }
+    // A operand: weights of head r16 at rows lrow + 4i (k = 8*lrow + 2i + s,
+    // s = 0 hi part, 1 lo part), read back transposed from the table
+    uint4 aw;
+    {
+      uint32_t w[4];
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      float vf[8];
-      unpack8(vr[it], vf);
-      const float* pr = ptab + (4 * it + lrow) * G;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float pg = pr[g];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pg, vf[e], o[g][e]);
+      for (int i = 0; i < 4; ++i) {
+        const float pv = r16 < G ? ptab[(4 * i + lrow) * G + r16] : 0.f;
+        const uint32_t hi = bf16_rne_bits(pv);
+        const uint32_t lo = bf16_rne_bits(pv - __uint_as_float(hi << 16));
+        w[i] = hi | (lo << 16);
       }
-      __builtin_amdgcn_sched_barrier(0);  // one row's unpacked V live at a time
+      aw = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    // B operand of product e: V[row lrow + 4i][8*lchunk + e], each entry twice
+    const uint32_t* vw = reinterpret_cast<const uint32_t*>(vr);  // [row i][4 dwords]
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t x = vw[4 * i + (e >> 1)];
+        b[i] = (e & 1) ? ((x >> 16) | (x & 0xffff0000u)) : ((x & 0xffffu) | (x << 16));
+      }
+      oacc[e] = mfma_16x16x32(as_bf16x8(aw), as_bf16x8(make_uint4(b[0], b[1], b[2], b[3])),
+                              oacc[e]);
+      __builtin_amdgcn_sched_barrier(0);  // one product's B operand live at a time
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if (blk + 1 < kBlocks) load_rows(a.v_rows, blk + 1, vr);
   }
-  // sum the four row phases (lrow) of each channel chunk
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float x = o[g][e];
-      x += __shfl_xor(x, 16);
-      x += __shfl_xor(x, 32);
-      o[g][e] = x;
-    }
+  // lane (kg, r16) holds O[4kg + j][8*r16 + e] in oacc[e][j]
   float* mw = merge + wave * G * (kD + 2);
-  if (lrow == 0) {
+  if (4 * kg < G) {
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+    for (int j = 0; j < 4; ++j) {
+      const int g = 4 * kg + j;
+      if (g < G) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) mw[g * (kD + 2) + 8 * lchunk + e] = o[g][e];
+        for (int e = 0; e < 8; ++e) mw[g * (kD + 2) + 8 * r16 + e] = oacc[e][j];
+      }
+    }
   }
   if (lchunk == 0) {
 #pragma unroll
