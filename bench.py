@@ -110,6 +110,7 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     dev = torch.device("cuda:0")
+    _pipeline_streams(torch)  # first, so that the decode loops' streams get queues of their own
     w = synth.WORKLOADS["llama8b"]
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
@@ -565,12 +566,20 @@ _STREAMS = []
 
 
 def _pipeline_streams(torch):
-    """The compute and copy streams of every decode loop, created once and in
-    succession: streams share the device's few hardware queues round-robin,
-    and a copy stream that landed on the compute stream's queue would
-    serialise the loop."""
+    """The compute and copy streams of every decode loop.  The runtime gives
+    a stream its hardware queue at the stream's first use, a fresh one while
+    fewer than its maximum exist (4 by default), else a shared one; a copy
+    stream sharing the compute stream's queue would serialise the loop.  So
+    the first call, made before anything else runs, puts one small kernel on
+    the default stream, then on each of the two (three fresh queues)."""
     if not _STREAMS:
-        _STREAMS.extend([torch.cuda.Stream(), torch.cuda.Stream()])
+        cs, xs = torch.cuda.Stream(), torch.cuda.Stream()
+        torch.zeros(1, device="cuda")
+        for st in (cs, xs):
+            with torch.cuda.stream(st):
+                torch.zeros(1, device="cuda")
+        torch.cuda.synchronize()
+        _STREAMS.extend([cs, xs])
     return _STREAMS[0], _STREAMS[1]
 
 
