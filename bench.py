@@ -211,6 +211,14 @@ def main() -> int:
         "kernel": dominant, "algorithmic_bytes_per_launch": algo_bytes,
         "avg_launch_us": avg_s * 1e6,
     }
+    # every kernel of the step against the same peak, from the breakdown's
+    # stamped durations (algorithmic bytes: keys for scoring, selected rows for
+    # attention; the selection and the merge move implementation bytes only)
+    for kname, v in per_kernel.items():
+        if kname in algo:
+            v["algorithmic_bytes"] = algo[kname]
+            v["achieved_GBps"] = algo[kname] / (v["avg_us"] * 1e-6) / 1e9
+            v["frac_of_peak"] = v["achieved_GBps"] / HBM_PEAK_GBPS
     step_bytes = L * (algo["score"] + algo["attn"])
     log(f"dominant kernel {dominant}: {avg_s * 1e6:.1f} us/launch, "
         f"{achieved:.0f} GB/s algorithmic")
