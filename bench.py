@@ -509,12 +509,13 @@ def measure_graph(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, ref_idx, 
 def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, stream):
     """The Llama-8B step in the paper's pipelined form with the caches in HBM
     (Sec. 4.1: the set a layer attends over at step t was selected at step
-    t-1 from the speculative token's query): one launch per layer attends
-    with the current query over last step's set, read in place through its
-    indices, and scores the keys with the speculative query; the selection
-    then picks next step's set.  Index sets alternate between two arrays per
-    layer by step parity.  Queries are step-invariant: the current one is the
-    layer's, the speculative one bf16(0.8 q + 0.6 noise)."""
+    t-1 from the speculative token's query), run by the library's decode loop
+    without buffers: per layer one launch attends with the current query over
+    last step's set, read in place through its indices, and scores the keys
+    with the speculative query; the selection then picks next step's set.
+    Index sets alternate between two arrays per layer by step parity.  Queries
+    are step-invariant: the current one is the layer's, the speculative one
+    bf16(0.8 q + 0.6 noise)."""
     B, Hq, Hkv, d, k, L = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k, w.layers
     dev = torch.device("cuda:0")
     g = torch.Generator(device=dev)
@@ -526,16 +527,21 @@ def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, s
     nsel = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(2)]
     out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
     ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    io = [ckv.layer_array([{"q_att": t["q"], "q_sel": qs[l], "k_score": kv_ptrs[l][0],
+                            "k_src": kv_ptrs[l][0], "v_src": kv_ptrs[l][1],
+                            "idx_prev": idx[c][l], "n_sel_prev": nsel[c][l],
+                            "idx_next": idx[1 - c][l], "n_sel_next": nsel[1 - c][l],
+                            "out": out[l]} for l, t in enumerate(layers)])
+          for c in range(2)]
+    lens = layers[0]["ctx_lens"]
+    assert all(torch.equal(t["ctx_lens"], lens) for t in layers)
+    pipe = ckv.Pipeline()
     cur = [0]
 
     def step():
-        c = cur[0]
-        for l, t in enumerate(layers):
-            kp, vp = kv_ptrs[l]
-            ckv.critical_kv_attn(shape, t["q"], qs[l], kp, t["ctx_lens"], k, scale, kp, vp,
-                                 ckv.SRC_DEVICE, None, None, nsel[c][l], idx[1 - c][l],
-                                 nsel[1 - c][l], out[l], ws, stream, idx_in=idx[c][l])
-        cur[0] = 1 - c
+        pipe.step(shape, io[cur[0]], lens, k, scale, ckv.SRC_DEVICE, None, None, ws, stream,
+                  None)
+        cur[0] ^= 1
 
     # bootstrap (the pre-decoding step): same-step selection into set 0
     for l, t in enumerate(layers):
@@ -556,17 +562,18 @@ def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, s
         step()
     e1.record(stream)
     torch.cuda.synchronize()
+    pipe.close()
     ms = e0.elapsed_time(e1) / steps
     assert all(torch.isfinite(o).all().item() for o in out[:2])
     dual_bytes = B * Hkv * (w.max_ctx * d * 2 + k * 2 * d * 2)
     res = {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3), "per_layer_us": per,
-           "workload": "the Llama-8B step above, pipelined: attention over last step's set "
-                       "read in place from HBM and scoring with the speculative query in "
-                       "one launch per layer"}
+           "workload": "the Llama-8B step above, pipelined through the decode loop without "
+                       "buffers: attention over last step's set read in place from HBM and "
+                       "scoring with the speculative query in one launch per layer"}
     if "dual" in per:
         res["dual_bytes_per_launch"] = dual_bytes
         res["dual_GBps"] = dual_bytes / (per["dual"] * 1e-6) / 1e9
-    del qs, idx, nsel, out, ws
+    del qs, idx, nsel, out, ws, io
     return res
 
 

@@ -384,7 +384,14 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
                        uint16_t* const k_buf[2], uint16_t* const v_buf[2],
                        void* copy_stream);
 
-/* One decode step over num_layers >= 2 layers.  For each layer l, on
+/* One decode step.  With k_buf and v_buf both NULL (a cache resident in
+ * device memory), each of num_layers >= 1 layers runs ckv_critical_kv_attn in
+ * place on compute_stream: attention of q_att over rows idx_prev/n_sel_prev
+ * of the layer's k_src/v_src, selection from q_sel into idx_next; nothing
+ * runs on copy_stream (it may be NULL), no prime is needed, and a layer with
+ * idx_true set is CKV_EINVAL.  Otherwise the two-buffer loop below.
+ *
+ * The two-buffer loop, over num_layers >= 2 layers.  For each layer l, on
  * compute_stream: ckv_critical_kv_attn in pipelined mode (attention of q_att
  * over the buffer holding idx_prev's rows, selection from q_sel into
  * idx_next), or, for a layer with idx_true set, ckv_corrected_attn (misses

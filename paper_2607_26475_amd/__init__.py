@@ -24,7 +24,7 @@ __all__ = [
     "critical_kv_attn", "corrected_attn", "chunk_landmarks", "select_chunks",
     "chunked_kv_attn", "dual_token_attn", "reconstruct_keys", "corrected_attn_lowrank",
     "MAX_RANK", "ABI_VERSION", "profile_begin", "profile_end", "abi_version",
-    "Layer", "Pipeline", "status_str", "LIB_PATH",
+    "Layer", "layer_array", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "EXPORTS",
 ]
@@ -321,8 +321,12 @@ def profile_end() -> dict:
             for i in range(KERNEL_COUNT) if arr[i].launches}
 
 
-def _layers(layers) -> "ctypes.Array":
-    """dicts with the ckv_layer field names (tensors, ints or None) -> array."""
+def layer_array(layers) -> "ctypes.Array":
+    """dicts with the ckv_layer field names (tensors, ints or None) -> the
+    ckv_layer array the decode loop takes; an array is returned as it is, so
+    a loop can build its per-parity arrays once."""
+    if isinstance(layers, ctypes.Array):
+        return layers
     arr = (Layer * len(layers))()
     for i, d in enumerate(layers):
         for name, typ in Layer._fields_:
@@ -358,13 +362,16 @@ class Pipeline:
 
     @staticmethod
     def _bufs(k_buf, v_buf):
+        """ctypes arrays of the two buffers; (None, None) for the in-place loop."""
+        if k_buf is None and v_buf is None:
+            return None, None
         kb = (ctypes.c_void_p * 2)(_ptr(k_buf[0]), _ptr(k_buf[1]))
         vb = (ctypes.c_void_p * 2)(_ptr(v_buf[0]), _ptr(v_buf[1]))
         return kb, vb
 
     def prime(self, shape: Shape, k: int, layers, src_kind: int, k_buf, v_buf,
               copy_stream) -> None:
-        arr = _layers(layers)
+        arr = layer_array(layers)
         kb, vb = self._bufs(k_buf, v_buf)
         _check("ckv_pipeline_prime", _lib.ckv_pipeline_prime(
             self._h, ctypes.byref(shape), k, arr, len(layers), src_kind, kb, vb,
@@ -372,7 +379,7 @@ class Pipeline:
 
     def step(self, shape: Shape, layers, ctx_lens, k: int, scale: float, src_kind: int,
              k_buf, v_buf, ws, compute_stream, copy_stream) -> None:
-        arr = _layers(layers)
+        arr = layer_array(layers)
         kb, vb = self._bufs(k_buf, v_buf)
         _check("ckv_decode_step", _lib.ckv_decode_step(
             self._h, ctypes.byref(shape), len(layers), arr, _ptr(ctx_lens), k, scale,

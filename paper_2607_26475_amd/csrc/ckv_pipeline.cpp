@@ -109,8 +109,25 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                     float scale, int src_kind, uint16_t* const k_buf[2],
                     uint16_t* const v_buf[2], void* ws, size_t ws_bytes,
                     void* compute_stream, void* copy_stream) {
-  if (!pipe || !layers || num_layers < 2 || !k_buf || !v_buf)
-    return ckv::fail(CKV_EINVAL, "pipe, layers (at least 2) and both buffers are required");
+  if (!pipe || !layers || num_layers < 1)
+    return ckv::fail(CKV_EINVAL, "pipe and layers are required");
+  if (!k_buf && !v_buf) {
+    // rows read in place through last step's index sets: no buffers, no refills
+    for (int l = 0; l < num_layers; ++l)
+      if (layers[l].idx_true)
+        return ckv::fail(CKV_EINVAL, "layer %d: miss correction needs the two buffers", l);
+    for (int l = 0; l < num_layers; ++l) {
+      const ckv_layer& L = layers[l];
+      int rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
+                                    L.k_src, L.v_src, src_kind, L.idx_prev, nullptr, nullptr,
+                                    L.n_sel_prev, L.idx_next, L.n_sel_next, L.out, ws,
+                                    ws_bytes, compute_stream);
+      if (rc) return rc;
+    }
+    return CKV_OK;
+  }
+  if (num_layers < 2 || !k_buf || !v_buf)
+    return ckv::fail(CKV_EINVAL, "the two-buffer loop needs at least 2 layers and both buffers");
   hipStream_t cs = (hipStream_t)compute_stream, xs = (hipStream_t)copy_stream;
   const unsigned long long capture = capture_id(cs);
   for (int l = 0; l < num_layers; ++l) {

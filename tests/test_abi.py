@@ -122,6 +122,12 @@ def test_pipeline_argument_checks():
     layers = (ckv.Layer * 2)()
     assert lib.ckv_pipeline_prime(None, ctypes.byref(s), 16, layers, 2, 0, bufs, bufs,
                                   None) == STATUS["EINVAL"]
+    # the in-place loop (no buffers) has no room for misses: refused before any launch
+    lay = (ckv.Layer * 1)()
+    lay[0].idx_true = FAKE
+    assert lib.ckv_decode_step(FAKE, ctypes.byref(s), 1, lay, FAKE, 16, 0.1, 0, None, None,
+                               FAKE, 1 << 20, None, None) == STATUS["EINVAL"]
+    assert "buffers" in lib.ckv_last_error_detail().decode()
     assert lib.ckv_decode_step(None, ctypes.byref(s), 2, layers, FAKE, 16, 0.1, 0, bufs,
                                bufs, FAKE, 1 << 20, None, None) == STATUS["EINVAL"]
 

@@ -156,6 +156,52 @@ def test_pipeline_matches_oracle(wl, layers):
         prev_sets = (g_idx, g_nsel)
 
 
+@pytest.mark.parametrize("wl,layers", [("llama8b_s", 2), ("dual64_s", 3)])
+def test_pipeline_in_place_matches_oracle(wl, layers):
+    """The loop without buffers (cache in device memory): every layer attends
+    over the rows of last step's set read in place and selects the next set."""
+    _log("pipeline in place", wl, layers)
+    dev = device()
+    w = synth.WORKLOADS[wl]
+    lp = Loop(w, layers, steps=2, seed=6, dev=dev)
+    lp.bootstrap()
+    boot = ([i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]])
+    shape = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
+    ws = ckv.workspace(shape, w.k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    pipe = ckv.Pipeline()
+    cur, hist = 0, []
+    for st in range(1, 3):
+        io = lp.layer_io(st, cur)
+        for l in range(layers):
+            io[l]["k_src"], io[l]["v_src"] = lp.t[l]["k"], lp.t[l]["v"]
+        pipe.step(shape, io, lp.lens, w.k, SCALE, ckv.SRC_DEVICE, None, None, ws, lp.compute,
+                  None)
+        torch.cuda.synchronize()
+        nxt = 1 - cur
+        hist.append(([i.cpu().numpy() for i in lp.idx[nxt]],
+                     [n.cpu().numpy() for n in lp.nsel[nxt]],
+                     [o.cpu().numpy() for o in lp.out]))
+        cur = nxt
+    pipe.close()
+    o = orc()
+    lens = lp.lens.cpu().numpy()
+    so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
+    prev_sets = boot
+    for st in range(1, 3):
+        g_idx, g_nsel, g_out = hist[st - 1]
+        for l in range(layers):
+            K, V = u16(lp.t[l]["k"]), u16(lp.t[l]["v"])
+            S = o.score_keys(so, u16(lp.q_sel[st][l]), K, lens, SCALE, nthreads=8)
+            r_idx, r_nsel = o.select_topk(so, S, lens, w.k, nthreads=8)
+            swaps = check_index_sets(g_idx[l], g_nsel[l], r_idx, r_nsel, S, lens)
+            ref = oracle_attn_over(so, u16(lp.q_att[st][l]), K, V, prev_sets[0][l],
+                                   prev_sets[1][l], w.k)
+            err = np.abs(g_out[l] - ref).max()
+            _log(f"  step {st} layer {l}: swaps {swaps}, max abs err {err:.2e}")
+            assert err <= ATOL_OUT
+        prev_sets = (g_idx, g_nsel)
+
+
 class _Delay:
     """Keeps one stream busy (device copies) before each step."""
 
