@@ -231,6 +231,50 @@ def test_full_llama8b_layer_sampled(layout):
                  lambda b, h, s: t["v"][b, h][torch.from_numpy(s).to(dev)])
 
 
+def test_full_llama8b_pipelined_in_place_sampled():
+    """One full-size Llama-8B-shaped layer in the pipelined form the benchmark
+    also times: step t-1 selects from a speculative query (same-step call),
+    step t attends with the current query over that set read in place from
+    HBM while selecting again from the next speculative query.  Sampled units:
+    the new set against the oracle's selection, the output against the
+    oracle's attention over the earlier set."""
+    _log("full llama8b pipelined in place")
+    dev = device()
+    w = synth.WORKLOADS["llama8b"]
+    t = synth.make_layer(w, seed=0, layer=1, device=dev)
+    G, d = w.group, w.head_dim
+    g = synth.generator(w.name, 0, 1, "spec", dev)
+    spec = [(0.8 * t["q"].float() + 0.6 * torch.randn(t["q"].shape, generator=g, device=dev))
+            .to(torch.bfloat16) for _ in range(2)]
+    prev = Run(w, t["ctx_lens"], dev)
+    prev.same_step(t["q"], spec[0], t["k"], t["k"], t["v"], ckv.SRC_DEVICE)
+    cur = Run(w, t["ctx_lens"], dev)
+    cur.in_place(t["q"], spec[1], t["k"], t["k"], t["v"], ckv.SRC_DEVICE, prev.idx, prev.n_sel)
+    p_idx, p_nsel, _ = prev.host()
+    g_idx, g_nsel, g_out = cur.host()
+    assert np.all(np.isfinite(g_out))
+    o = orc()
+    lens = t["ctx_lens"].cpu().numpy()
+    q_att, q_sel = u16(t["q"]), u16(spec[1])
+    units = _sampled_units(w, 8, seed=1)
+    for b, h in units:
+        n = int(lens[b])
+        keys = u16(t["k"][b, h, :n])
+        S = o.unit_scores(q_sel[b, h * G:(h + 1) * G], keys, SCALE)
+        r_idx, m = o.unit_select(S, w.k)
+        Sfull = np.full((1, 1, n), np.nan)
+        Sfull[0, 0] = S
+        check_index_sets(g_idx[b:b + 1, h:h + 1], g_nsel[b:b + 1, h:h + 1],
+                         r_idx[None, None], np.array([[m]]), Sfull, np.array([n]))
+        mp = int(p_nsel[b, h])
+        rows = torch.from_numpy(p_idx[b, h, :mp].astype(np.int64)).to(dev)
+        ref, _ = o.unit_attn(q_att[b, h * G:(h + 1) * G], u16(t["k"][b, h][rows]),
+                             u16(t["v"][b, h][rows]), SCALE)
+        err = np.abs(g_out[b, h * G:(h + 1) * G] - ref).max()
+        assert err <= ATOL_OUT, (b, h, err)
+    _log("  checked units:", units)
+
+
 def test_full_million_layer_sampled():
     """One full-size million-token layer (B1, n 1048576, k 8192) with K/V in
     pinned host memory: select, gather over the host link, attend."""
