@@ -573,6 +573,7 @@ def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, s
     if "dual" in per:
         res["dual_bytes_per_launch"] = dual_bytes
         res["dual_GBps"] = dual_bytes / (per["dual"] * 1e-6) / 1e9
+        res["dual_frac_of_peak"] = res["dual_GBps"] / HBM_PEAK_GBPS
     del qs, idx, nsel, out, ws, io
     return res
 
