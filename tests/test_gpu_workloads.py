@@ -172,6 +172,43 @@ def test_pipelined_in_place(wl, kind, layout):
     del keep
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (16, 8), (64, 8), (32, 2)])
+def test_fused_modes_group_sizes(Hq, Hkv):
+    """The fused entry for group sizes 1, 2, 8 and 16 in both modes: same-step
+    (selection then attention over the rows read in place) and pipelined in
+    place (attention over the same-step call's set, selection from a second
+    query).  Ragged contexts, some shorter than k."""
+    _log("fused modes", Hq, Hkv)
+    dev = device()
+    w = synth.Workload(f"groups_{Hq}_{Hkv}", 3, Hq, Hkv, 128, 3000, 200, 512, 1, "hbm",
+                       True, "normal")
+    t = synth.make_layer(w, seed=7, device=dev)
+    lens = torch.tensor([300, 3000, 1777], dtype=torch.int32, device=dev)  # one below k
+    lens_h = lens.cpu().numpy()
+    q_att, q_sel, K, V = u16(t["q"]), u16(t["q_sel"]), u16(t["k"]), u16(t["v"])
+    o = orc()
+    so = o.shape(w.batch, Hq, Hkv, w.head_dim, w.max_ctx)
+    S_att = o.score_keys(so, q_att, K, lens_h, SCALE, nthreads=8)
+    S_sel = o.score_keys(so, q_sel, K, lens_h, SCALE, nthreads=8)
+    first = Run(w, lens, dev)  # selects with q_att
+    first.same_step(t["q"], t["q"], t["k"], t["k"], t["v"], ckv.SRC_DEVICE)
+    f_idx, f_nsel, f_out = first.host()
+    r_idx, r_nsel = o.select_topk(so, S_att, lens_h, w.k, nthreads=8)
+    check_index_sets(f_idx, f_nsel, r_idx, r_nsel, S_att, lens_h)
+    err = np.abs(f_out - oracle_attn_over(so, q_att, K, V, f_idx, f_nsel, w.k)).max()
+    _log("  same-step max abs err:", err)
+    assert err <= ATOL_OUT
+    second = Run(w, lens, dev)  # attends over the first set, selects with q_sel
+    second.in_place(t["q"], t["q_sel"], t["k"], t["k"], t["v"], ckv.SRC_DEVICE, first.idx,
+                    first.n_sel)
+    s_idx, s_nsel, s_out = second.host()
+    r_idx, r_nsel = o.select_topk(so, S_sel, lens_h, w.k, nthreads=8)
+    check_index_sets(s_idx, s_nsel, r_idx, r_nsel, S_sel, lens_h)
+    err = np.abs(s_out - oracle_attn_over(so, q_att, K, V, f_idx, f_nsel, w.k)).max()
+    _log("  pipelined in place max abs err:", err)
+    assert err <= ATOL_OUT
+
+
 def _sampled_units(w, count, seed):
     rng = np.random.default_rng(seed)
     units = [(b, h) for b in range(w.batch) for h in range(w.kv_heads)]
