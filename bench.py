@@ -772,11 +772,25 @@ def cpu_baseline(layers, w, scale, np):
         runs += 1
     sec_layer = elapsed / runs
     sec_step = sec_layer * w.layers
+    # the tiny workload's layer (B1, 8/2 heads, n 4096, k 256) on one thread
+    wt = synth.WORKLOADS["tiny"]
+    tt = synth.make_layer(wt, seed=0)
+    st = o.shape(wt.batch, wt.q_heads, wt.kv_heads, wt.head_dim, wt.max_ctx)
+    qt, Kt, Vt = synth.to_u16(tt["q"]), synth.to_u16(tt["k"]), synth.to_u16(tt["v"])
+    lt = tt["ctx_lens"].numpy()
+    tiny_runs, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < 1.0:
+        o.critical_kv_attn(st, qt, None, Kt, Kt, Vt, lt, wt.k, scale, nthreads=1)
+        tiny_runs += 1
+    tiny_s = (time.perf_counter() - t0) / tiny_runs
     return {"value": w.batch / sec_step, "unit": "tokens/s", "cores": cores,
             "kind": "oracle", "cpu": cpu_name(), "seconds_per_step": sec_step,
             "sample": f"layer 0 of {w.layers}, all {w.units} (request, KV head) units, "
                       f"run {runs} times ({elapsed:.1f} s, {sec_layer:.2f} s each) and "
-                      f"scaled x{w.layers} layers"}
+                      f"scaled x{w.layers} layers",
+            "tiny_layer_one_thread_s": tiny_s,
+            "tiny_sample": f"the tiny workload's layer (B1, 8/2 heads, n 4096, k 256) on one "
+                           f"thread, {tiny_runs} runs"}
 
 
 if __name__ == "__main__":
