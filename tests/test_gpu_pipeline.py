@@ -156,6 +156,30 @@ def test_pipeline_matches_oracle(wl, layers):
         prev_sets = (g_idx, g_nsel)
 
 
+def test_pipeline_gather_width_bit_identical():
+    """The refill grid changes how many workgroups move the rows, not which:
+    the loop at 16 and 4096 workgroups and at the width it picks by shape
+    gives the same index sets and outputs bit for bit."""
+    _log("pipeline gather widths")
+    dev = device()
+    w = synth.WORKLOADS["long128k_s"]
+    results = []
+    for width in (0, 16, 4096):
+        lp = Loop(w, 2, steps=2, seed=8, dev=dev)
+        lp.bootstrap()
+        pipe = ckv.Pipeline()
+        pipe.set_gather_width(width)
+        results.append(lp.run(2, pipe))
+        pipe.close()
+    with pytest.raises(ckv.CkvError):
+        ckv.Pipeline().set_gather_width(4097)
+    for other in results[1:]:
+        for st in range(2):
+            for a, b in zip(results[0][st][:3], other[st][:3]):
+                for x, y in zip(a, b):
+                    np.testing.assert_array_equal(x, y)
+
+
 @pytest.mark.parametrize("wl,layers", [("llama8b_s", 2), ("dual64_s", 3)])
 def test_pipeline_in_place_matches_oracle(wl, layers):
     """The loop without buffers (cache in device memory): every layer attends
