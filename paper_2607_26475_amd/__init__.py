@@ -338,7 +338,9 @@ def layer_array(layers) -> "ctypes.Array":
 
 
 class Pipeline:
-    """The two-buffer decode loop of ``ckv_decode_step`` (owns its events)."""
+    """The decode loop of ``ckv_decode_step`` (owns its events): two buffers
+    refilled on a copy stream, or, with ``k_buf`` and ``v_buf`` None, rows
+    read in place from a cache in device memory."""
 
     def __init__(self):
         h = ctypes.c_void_p()
@@ -379,6 +381,7 @@ class Pipeline:
 
     def step(self, shape: Shape, layers, ctx_lens, k: int, scale: float, src_kind: int,
              k_buf, v_buf, ws, compute_stream, copy_stream) -> None:
+        """One decode step over ``layers`` (dicts or a ``layer_array``)."""
         arr = layer_array(layers)
         kb, vb = self._bufs(k_buf, v_buf)
         _check("ckv_decode_step", _lib.ckv_decode_step(
