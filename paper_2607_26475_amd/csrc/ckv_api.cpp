@@ -278,6 +278,9 @@ SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* sc
   a.hist_part = nullptr;
   a.score_nwg = 0;
   a.units = d.U;
+  a.mpart = nullptr;
+  a.mout = nullptr;
+  a.mchunks = a.mG = a.mHq = 0;
   return a;
 }
 
@@ -356,6 +359,26 @@ int run_select_tail(const SelectArgs& a, int units, hipStream_t s) {
   }
   CKV_TRY_HIP(launch_filter(a, units, s), "filter launch");
   CKV_TRY_HIP(launch_finish(a, units, s), "finish launch");
+  return CKV_OK;
+}
+
+// The next step's selection after a pipelined attend-and-score launch, and
+// the merge of that launch's attention partials: inside the fused selection
+// when it runs (one workgroup per unit, which loads the unit's partials while
+// it selects), else by the merge kernel.
+int select_and_merge(SelectArgs sa, const AttnArgs& at, const Dims& d, hipStream_t s) {
+  if (sa.max_ctx <= kFusedSelectMaxCtx && at.chunks <= kMergeChunks &&
+      d.G * kD <= kFinishThreads && !at.q2) {
+    sa.mpart = at.part;
+    sa.mout = at.out;
+    sa.mchunks = at.chunks;
+    sa.mG = d.G;
+    sa.mHq = d.Hq;
+    return run_select_tail(sa, d.U, s);
+  }
+  int rc = run_select_tail(sa, d.U, s);
+  if (rc) return rc;
+  CKV_TRY_HIP(launch_combine(at, d.G, d.U, s), "combine launch");
   return CKV_OK;
 }
 
@@ -603,8 +626,7 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                              : attn_args(d, L, ws, q_att, k_src, v_src, idx_in, n_sel_in,
                                          d.kv_stride, k, scale, out);
     CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, s), "dual launch");
-    if ((rc = run_select_tail(sa, d.U, s))) return rc;
-    CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+    if ((rc = select_and_merge(sa, at_, d, s))) return rc;
   } else {
     CKV_TRY_HIP(launch_score(sc, d.G, true, d.U, s), "score launch");
     if ((rc = run_select_tail(sa, d.U, s))) return rc;
@@ -852,9 +874,7 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   AttnArgs at_ = attn_args(db, L, ws, q_att, k_buf, v_buf, m.slot_of, n_true, kD, k, scale,
                            out);
   CKV_TRY_HIP(launch_dual(at_, c2, d.G, true, d.U, s), "dual launch");
-  if ((rc = run_select_tail(s2, d.U, s))) return rc;
-  CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
-  return CKV_OK;
+  return select_and_merge(s2, at_, d, s);
 }
 
 }  // namespace

@@ -53,6 +53,7 @@ constexpr int kAttnThreads = 256;
 constexpr int kWaveRows = 64;
 constexpr int kAttnRows = 4 * kWaveRows;
 constexpr int kPartStride = 132;   // floats per (chunk, head): m, l, pad, pad, o[128]
+constexpr int kMergeChunks = 8;    // partials per unit the fused selection merges
 
 // Gather: one thread moves 16 bytes per item; items are (unit, slot, K|V, part).
 constexpr int kGatherThreads = 256;
@@ -94,6 +95,12 @@ struct SelectArgs {
   int64_t bm_words;
   int Hkv, max_ctx, k, tiles;
   int chunk;                // as in ScoreArgs
+  // Pipelined calls: the fused selection also merges the attention partials
+  // of the launch before it (NULL mpart: a merge kernel runs instead).
+  // mchunks <= kMergeChunks and mG * kD <= kFinishThreads.
+  const float* mpart;       // [U][mchunks][mG][kPartStride]
+  float* mout;              // [B][mHq][d]
+  int mchunks, mG, mHq;
 };
 
 struct AttnArgs {

@@ -375,6 +375,62 @@ struct KeyedCands {
   }
 };
 
+// Pipelined calls: merges the attention partials of the launch before the
+// selection for one unit into the output, as the merge kernel does and in
+// its order of operations: out[b][h*G + g] = sum over chunks of
+// exp(m_c - M) o_c / sum over chunks of exp(m_c - M) l_c.  Thread t < mG * kD
+// owns channel t % kD of head t / kD; thread t < mchunks * mG reads the
+// (max, weight sum) of chunk t / mG, head t % mG.  lds: 16 * (2 *
+// kMergeChunks + 1) floats, free on entry.  All kFinishThreads threads call
+// it, from one place of the kernel (an inlined second copy kept more of the
+// selection's registers live).
+__device__ __forceinline__ void merge_partials(const SelectArgs& a, int unit, uint32_t* lds) {
+  const int tid = threadIdx.x;
+  const int G = a.mG, nc = a.mchunks;
+  const float* pu = a.mpart + (int64_t)unit * nc * G * kPartStride;
+  // unconditional (clamped) loads
+  float mo[kMergeChunks];
+  const int og = min(tid / kD, G - 1), oc = tid % kD;
+#pragma unroll
+  for (int ch = 0; ch < kMergeChunks; ++ch)
+    mo[ch] = pu[(min(ch, nc - 1) * G + og) * kPartStride + 4 + oc];
+  const int pc = min(tid, nc * G - 1);
+  const float mmax = pu[pc * kPartStride], msum = pu[pc * kPartStride + 1];
+  float* s_w = reinterpret_cast<float*>(lds);  // [16][kMergeChunks] weights
+  float* s_l = s_w + 16 * kMergeChunks;        // [16][kMergeChunks] weight sums
+  float* s_inv = s_l + 16 * kMergeChunks;      // [16]
+  __syncthreads();
+  if (tid < nc * G) {
+    const int ch = tid / G, g = tid - ch * G;
+    s_w[g * kMergeChunks + ch] = mmax;
+    s_l[g * kMergeChunks + ch] = msum;
+  }
+  __syncthreads();
+  if (tid < G) {
+    const int g = tid;
+    float M = -INFINITY;
+    for (int ch = 0; ch < nc; ++ch) M = fmaxf(M, s_w[g * kMergeChunks + ch]);
+    float L = 0.f;
+    for (int ch = 0; ch < nc; ++ch) {
+      const float mc = s_w[g * kMergeChunks + ch];
+      const float w = mc == -INFINITY ? 0.f : __expf(mc - M);
+      L = fmaf(w, s_l[g * kMergeChunks + ch], L);
+      s_w[g * kMergeChunks + ch] = w;
+    }
+    s_inv[g] = L > 0.f ? 1.f / L : 0.f;
+  }
+  __syncthreads();
+  if (tid < G * kD) {
+    const int g = tid / kD, c = tid - g * kD;
+    float O = 0.f;
+#pragma unroll
+    for (int ch = 0; ch < kMergeChunks; ++ch)
+      if (ch < nc) O = fmaf(s_w[g * kMergeChunks + ch], mo[ch], O);
+    const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+    a.mout[((int64_t)b * a.mHq + (int64_t)h * G + g) * kD + c] = O * s_inv[g];
+  }
+}
+
 __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __shared__ uint2 cand[kCandLds];
   __shared__ uint32_t bm[kFusedSelectMaxCtx / 32];
@@ -413,53 +469,56 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   const int n = unit_len(len_b, a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   int32_t* idx = a.idx + (int64_t)unit * a.k;
-  if (m >= n) {  // uniform; every position (possibly none) is selected
-    for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
-    if (tid == 0) a.n_sel[unit] = m;
-    return;
-  }
-  store_hist_sum(hv, nslots, lhist);
-  if (tid == 64) misc[7] = 0u;
-  // the scores may still be in flight across both barriers
-  lds_barrier();
-  if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
-  lds_barrier();
-  const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
-  const uint32_t b1 = misc[4], above = misc[5];
-  const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
-  const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
-  // the last, partial batch holds NaN past n_b
-  auto pad = [&](float (&sv)[kSelPer], int j0) {
-    if (j0 + kSelBatch > n) {
-#pragma unroll
-      for (int u = 0; u < kSelPer; ++u)
-        if (j0 + u * kFinishThreads + tid >= n) sv[u] = __builtin_nanf("");
+  do {  // one exit, so that the merge below appears once
+    if (m >= n) {  // uniform; every position (possibly none) is selected
+      for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
+      if (tid == 0) a.n_sel[unit] = m;
+      break;
     }
-  };
-  // the first batch apart, so that its compares start as its loads land
-  pad(sv0, 0);
-  classify_batch(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
-  for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {
-    float sv[kSelPer];
-    load_score_batch(srow, j0, n, sv);
-    pad(sv, j0);
-    classify_batch(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
-  }
-  __syncthreads();
-  const uint32_t nc = misc[7];
-  const uint32_t need = (uint32_t)m - above;
-  const KeyedCands kc{cs};
-  uint32_t pmax;
-  const uint32_t T = refine_threshold(kc, nc, need, b1, lhist, tmp, misc, &pmax);
-  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
-    const uint2 c = kc[i];
-    if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
-  }
-  __syncthreads();
-  // m positions for scores as specified (fewer only with NaN scores)
-  const int got = (int)min(emit_bitmap(bm, (n + 31) >> 5, idx, (uint32_t)a.k, tmp), (uint32_t)m);
-  for (int i = got + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
-  if (tid == 0) a.n_sel[unit] = got;
+    store_hist_sum(hv, nslots, lhist);
+    if (tid == 64) misc[7] = 0u;
+    // the scores may still be in flight across both barriers
+    lds_barrier();
+    if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
+    lds_barrier();
+    const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
+    const uint32_t b1 = misc[4], above = misc[5];
+    const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
+    const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
+    // the last, partial batch holds NaN past n_b
+    auto pad = [&](float (&sv)[kSelPer], int j0) {
+      if (j0 + kSelBatch > n) {
+#pragma unroll
+        for (int u = 0; u < kSelPer; ++u)
+          if (j0 + u * kFinishThreads + tid >= n) sv[u] = __builtin_nanf("");
+      }
+    };
+    // the first batch apart, so that its compares start as its loads land
+    pad(sv0, 0);
+    classify_batch(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
+    for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {
+      float sv[kSelPer];
+      load_score_batch(srow, j0, n, sv);
+      pad(sv, j0);
+      classify_batch(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
+    }
+    __syncthreads();
+    const uint32_t nc = misc[7];
+    const uint32_t need = (uint32_t)m - above;
+    const KeyedCands kc{cs};
+    uint32_t pmax;
+    const uint32_t T = refine_threshold(kc, nc, need, b1, lhist, tmp, misc, &pmax);
+    for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+      const uint2 c = kc[i];
+      if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
+    }
+    __syncthreads();
+    // m positions for scores as specified (fewer only with NaN scores)
+    const int got = (int)min(emit_bitmap(bm, (n + 31) >> 5, idx, (uint32_t)a.k, tmp), (uint32_t)m);
+    for (int i = got + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
+    if (tid == 0) a.n_sel[unit] = got;
+  } while (0);
+  if (a.mpart) merge_partials(a, unit, lhist);
 }
 
 // ---- attention -------------------------------------------------------------
