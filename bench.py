@@ -714,7 +714,7 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
                "kernels_ms_per_step": {kname: round(v[1] / steps, 4)
                                        for kname, v in stats.items()},
                "overlap": (gather_ms + compute_ms) / ms,
-               "gather_workgroups": gather_width or ("auto: 64" if n >= 64 * k else "auto: 256")}
+               "gather_workgroups": gather_width or ("auto: 80" if n >= 64 * k else "auto: 256")}
         if corrected:  # the misses cross the link too, on the compute stream
             found = sum(int(hits[st][l].sum()) for st in range(1, steps + 1) for l in range(L))
             total = steps * L * B * Hkv * min(k, n)

@@ -368,12 +368,13 @@ int ckv_pipeline_destroy(ckv_pipeline* pipe);
 
 /* Workgroups of every refill this loop launches on its copy stream.  A
  * gather that reads pinned host memory slows kernels on other streams while
- * it runs; a narrower one (64 workgroups still carry the link's rate) leaves
- * the compute stream its speed, for loops where that stream, not the link,
- * sets the step time.  0 (the default) chooses by shape: 64 workgroups for
- * pinned sources when max_ctx >= 64 k (the scoring pass then reads at least
- * 32 times the bytes the link carries per layer), else what ckv_gather_kv
- * uses (256 for pinned sources).  0 <= workgroups <= 4096, else CKV_EINVAL. */
+ * it runs; a narrower one (80 workgroups carry most of the link's rate)
+ * leaves the compute stream most of its speed, for loops where that stream,
+ * not the link, sets the step time.  0 (the default) chooses by shape: 80
+ * workgroups for pinned sources when max_ctx >= 64 k (the scoring pass then
+ * reads at least 32 times the bytes the link carries per layer), else what
+ * ckv_gather_kv uses (256 for pinned sources).  0 <= workgroups <= 4096,
+ * else CKV_EINVAL. */
 int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups);
 
 /* Starts a decode loop: gathers layer 0 (into buffer 0) and layer 1 (into

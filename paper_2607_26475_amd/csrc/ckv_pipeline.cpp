@@ -27,14 +27,16 @@ unsigned long long capture_id(hipStream_t s) {
 
 // Refill grid when the caller set none.  A gather reading pinned host memory
 // with one workgroup per CU slows the compute stream's kernels several-fold
-// while it runs; 64 workgroups still carry the link's rate and leave them
-// their speed, but lose a few percent of it beside them.  The compute stream
-// reads about max_ctx/(2k) times the bytes the link carries per layer (the
-// scoring pass's keys against the selected K|V rows); from a ratio of 32 on,
-// its slowed kernels, not the link, would set the step time.
+// while it runs; a narrow one (80 workgroups carry most of the link's rate)
+// leaves them most of their speed.  The compute stream reads about
+// max_ctx/(2k) times the bytes the link carries per layer (the scoring
+// pass's keys against the selected K|V rows); from a ratio of 32 on, its
+// slowed kernels, not the link, would set the step time.
+constexpr int kNarrowRefillWgs = 80;
+
 int refill_width(const ckv_pipeline* p, const ckv_shape* shape, int32_t k, int src_kind) {
   if (p->gather_wgs || src_kind != CKV_SRC_HOST_PINNED || !shape || k < 1) return p->gather_wgs;
-  return (int64_t)shape->max_ctx >= 64 * (int64_t)k ? 64 : 0;
+  return (int64_t)shape->max_ctx >= 64 * (int64_t)k ? kNarrowRefillWgs : 0;
 }
 
 int gather_layer(const ckv_pipeline* p, const ckv_shape* shape, int32_t k, const ckv_layer& L,
