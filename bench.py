@@ -32,8 +32,17 @@ HBM_PEAK_GBPS = 8000.0
 COUNTERS = os.path.join(ROOT, "profiles", "score_llama8b_counters.txt")
 
 
+SECTIONS = ("main", "extras", "host_link", "long128k", "dual64", "million", "cpu")
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def median(xs):
+    xs = sorted(xs)
+    n = len(xs)
+    return xs[n // 2] if n % 2 else 0.5 * (xs[n // 2 - 1] + xs[n // 2])
 
 
 SCORE_SOURCES = ("ckv_score.hpp", "ckv_device.hpp")
@@ -95,12 +104,28 @@ def main() -> int:
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (known bytes) before timing, so "
                          "that counter runs can scale FETCH_SIZE/WRITE_SIZE")
+    ap.add_argument("--sections", default=",".join(SECTIONS),
+                    help="comma-separated sections to run (default: all of "
+                         f"{','.join(SECTIONS)}); a kernel profile of one section "
+                         "names it alone, e.g. --sections host_link")
+    ap.add_argument("--loop-steps", type=int, default=20,
+                    help="timed steps of each host-pinned decode loop (median reported)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
         return 2
+    sections = [x for x in args.sections.split(",") if x]
+    bad = [x for x in sections if x not in SECTIONS]
+    if bad:
+        print(f"unknown sections {bad}; choose from {SECTIONS}", file=sys.stderr)
+        return 2
+    for flag, names in ((args.no_cpu_baseline, ("cpu",)), (args.no_host_link, ("host_link",)),
+                        (args.no_extras, ("extras",)),
+                        (args.no_pipeline, ("long128k", "dual64", "million"))):
+        if flag:
+            sections = [x for x in sections if x not in names]
 
     import numpy as np
     import torch
@@ -115,11 +140,13 @@ def main() -> int:
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
     scale = float(np.float32(1.0 / math.sqrt(d)))
+    need_llama = [x for x in sections if x in ("main", "extras", "cpu")]
+    n_layers = L if ("main" in sections or "extras" in sections) else (1 if need_llama else 0)
 
-    log(f"generating {L} layers of {w.name} inputs on {torch.cuda.get_device_name(0)}")
+    log(f"generating {n_layers} layers of {w.name} inputs on {torch.cuda.get_device_name(0)}")
     t0 = time.time()
     layers = []
-    for l in range(L):
+    for l in range(n_layers):
         t = synth.make_layer(w, seed=0, layer=l, device=dev)
         if args.layout == "interleaved":
             # the scoring pass reads the K half of each 512-byte row,
@@ -132,16 +159,118 @@ def main() -> int:
 
     row = 2 * d if args.layout == "interleaved" else d
     s = ckv.shape_for(B, Hq, Hkv, n, key_row_stride=row, kv_row_stride=row)
-    ws = ckv.workspace(s, k, ckv.ENTRY_CRITICAL_KV_ATTN)
-    idx = [torch.empty((B, Hkv, k), dtype=torch.int32, device=dev) for _ in range(L)]
-    nsel = [torch.empty((B, Hkv), dtype=torch.int32, device=dev) for _ in range(L)]
-    out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
     stream = torch.cuda.current_stream()
-
     if args.layout == "interleaved":
         kv_ptrs = [(t["kv"].data_ptr(), t["kv"].data_ptr() + 2 * d) for t in layers]
     else:
         kv_ptrs = [(t["k"].data_ptr(), t["v"].data_ptr()) for t in layers]
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    result = {
+        "metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": None,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "accumulate": "f32", "data": "synthetic",
+        "config": {
+            "workload": "Llama-3-8B-shaped decode, 32 layers: B16, 32 q / 8 KV heads, "
+                        "head_dim 128, context 32768, k 2048 per KV head, K/V in HBM "
+                        + ("(K|V interleaved per position)" if args.layout == "interleaved"
+                           else "(separate K and V caches)"),
+            "layout": args.layout,
+            "batch": B, "context": n, "k": k, "layers": L, "q_heads": Hq,
+            "kv_heads": Hkv, "head_dim": d, "placement": "hbm",
+        },
+        "sections": sections,
+    }
+    if "main" in sections:
+        result.update(measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream))
+    if "extras" in sections:
+        ws = ckv.workspace(s, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        dual_token = measure_dual_token(torch, ckv, w, scale, stream)
+        log(f"dual-token attention: co-batched {dual_token['co_batched_us']:.1f} us, two "
+            f"launches {dual_token['two_launches_us']:.1f} us per layer")
+        chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
+        log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} "
+            f"ms/step, {chunked['tokens_per_s']:.0f} tokens/s")
+        idx = [torch.empty((B, Hkv, k), dtype=torch.int32, device=dev) for _ in range(L)]
+        nsel = [torch.empty((B, Hkv), dtype=torch.int32, device=dev) for _ in range(L)]
+        out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
+        for l, t in enumerate(layers):  # the eager reference of the graph's first replay
+            kp, vp = kv_ptrs[l]
+            ckv.critical_kv_attn(s, t["q"], None, kp, t["ctx_lens"], k, scale, kp, vp,
+                                 ckv.SRC_DEVICE, None, None, None, idx[l], nsel[l], out[l],
+                                 ws, stream)
+        torch.cuda.synchronize()
+        graph = measure_graph(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, idx, out)
+        log(f"graph replay: {graph['ms_per_step']:.3f} ms/step, {graph['tokens_per_s']:.0f} "
+            f"tokens/s, bit-identical {graph['bit_identical_to_eager']}")
+        del idx, nsel, out, ws
+        pipelined_hbm = measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, s, w, scale,
+                                              args.steps, stream)
+        log(f"pipelined, HBM: {pipelined_hbm['ms_per_step']:.3f} ms/step, "
+            f"{pipelined_hbm['tokens_per_s']:.0f} tokens/s, per layer "
+            f"{pipelined_hbm['per_layer_us']}")
+        result.update(chunked=chunked, pipelined_hbm=pipelined_hbm, graph=graph,
+                      dual_token=dual_token)
+
+    host_link = None
+    if "host_link" in sections:
+        host_link = measure_host_link(torch, ckv, dev)
+        log(f"host link: {host_link}")
+        result["host_link"] = host_link
+    del layers[1:]  # keep layer 0 for the CPU baseline
+    torch.cuda.empty_cache()
+    pipeline = {}
+    if "long128k" in sections:
+        pipeline.update(measure_pipeline(torch, ckv, synth, dev, np, host_link,
+                                         steps=args.loop_steps))
+        log(f"pipeline long128k: {pipeline}")
+        torch.cuda.empty_cache()
+    if "dual64" in sections:
+        # the dual-token serving workload: 64 requests of ragged contexts
+        pipeline["dual64"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "dual64",
+                                              n_hbm=2, n_host=1, steps=args.loop_steps,
+                                              runs=("plain",))
+        log(f"pipeline dual64: {pipeline['dual64']}")
+        torch.cuda.empty_cache()
+    if "million" in sections:
+        # the million-token single request
+        pipeline["million"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "million",
+                                               n_hbm=2, n_host=2, steps=args.loop_steps,
+                                               runs=("plain",), layer_queries=True)
+        log(f"pipeline million: {pipeline['million']}")
+    if pipeline:
+        result["pipeline"] = pipeline
+    if "cpu" in sections:
+        cpu = cpu_baseline(layers, w, scale, np)
+        log(f"cpu baseline: {cpu}")
+        result["cpu_baseline"] = cpu
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_every=8):
+    """The headline: the Llama-8B same-step decode step, K steps timed by
+    events on the compute stream (one more event after each step gives the
+    per-step times and their median).  Inside the timed steps one launch in
+    `stamp_every` of the dominant kernel carries dispatch-stamped events: its
+    average duration there gives the roofline.  A stamped dispatch costs a few
+    microseconds more than a plain one, so only a sample is stamped; the same
+    steps are timed once more with no stamp at all."""
+    B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
+                              w.layers)
+    dev = torch.device("cuda:0")
+    ws = ckv.workspace(s, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    idx = [torch.empty((B, Hkv, k), dtype=torch.int32, device=dev) for _ in range(L)]
+    nsel = [torch.empty((B, Hkv), dtype=torch.int32, device=dev) for _ in range(L)]
+    out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
 
     def step():
         for l, t in enumerate(layers):
@@ -152,22 +281,15 @@ def main() -> int:
 
     def timed(steps):
         torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record(stream)
+        for i in range(steps):
             step()
-        e1.record(stream)
+            ev[i + 1].record(stream)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / steps
+        per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+        return ev[0].elapsed_time(ev[steps]) / steps, per
 
-    if args.calibrate_copy:
-        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
         step()
@@ -181,13 +303,14 @@ def main() -> int:
                          "ms_per_step": tot / nb}
                   for name, (c, tot, mx) in kstats.items()}
     dominant = max(kstats, key=lambda kname: kstats[kname][1])
-    # Timed region: only the dominant kernel carries dispatch-stamped start/end
-    # events on `stream`; its duration below comes from these very steps.
-    ckv.profile_begin([dominant])
-    ms_step = timed(args.steps)
+    # Timed region: one launch in stamp_every of the dominant kernel carries
+    # dispatch-stamped start/end events on `stream`.
+    ckv.profile_begin([dominant], every=stamp_every)
+    ms_step, per_step = timed(args.steps)
     dstats = ckv.profile_end()
-    ms_plain = timed(args.steps)  # same steps with no stamps at all (overhead check)
-    log(f"  {ms_step:.3f} ms/step ({ms_plain:.3f} ms/step unstamped)")
+    ms_plain, _ = timed(args.steps)  # same steps with no stamps at all (overhead check)
+    log(f"  {ms_step:.3f} ms/step, median {median(per_step):.3f} ({ms_plain:.3f} ms/step "
+        f"unstamped)")
     log("  per layer: " + ", ".join(f"{kname} {v['avg_us']:.1f} us"
                                    for kname, v in per_kernel.items()))
     assert all(torch.isfinite(o).all().item() for o in out[:2])
@@ -209,7 +332,8 @@ def main() -> int:
         "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
         "frac": achieved / HBM_PEAK_GBPS if achieved else None, "traffic": traffic,
         "kernel": dominant, "algorithmic_bytes_per_launch": algo_bytes,
-        "avg_launch_us": avg_s * 1e6,
+        "avg_launch_us": avg_s * 1e6, "stamped_launches": launches,
+        "stamped": f"one launch in {stamp_every} inside the timed steps",
     }
     # every kernel of the step against the same peak, from the breakdown's
     # stamped durations (algorithmic bytes: keys for scoring, selected rows for
@@ -222,87 +346,11 @@ def main() -> int:
     step_bytes = L * (algo["score"] + algo["attn"])
     log(f"dominant kernel {dominant}: {avg_s * 1e6:.1f} us/launch, "
         f"{achieved:.0f} GB/s algorithmic")
-
-    dual_token = chunked = graph = pipelined_hbm = None
-    if not args.no_extras:
-        dual_token = measure_dual_token(torch, ckv, w, scale, stream)
-        log(f"dual-token attention: co-batched {dual_token['co_batched_us']:.1f} us, two "
-            f"launches {dual_token['two_launches_us']:.1f} us per layer")
-        chunked = measure_chunked(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, stream)
-        log(f"chunked (landmarks per {chunked['chunk']} rows): {chunked['ms_per_step']:.3f} "
-            f"ms/step, {chunked['tokens_per_s']:.0f} tokens/s")
-        graph = measure_graph(torch, ckv, layers, kv_ptrs, s, w, scale, args.steps, idx, out)
-        log(f"graph replay: {graph['ms_per_step']:.3f} ms/step, {graph['tokens_per_s']:.0f} "
-            f"tokens/s, bit-identical {graph['bit_identical_to_eager']}")
-        pipelined_hbm = measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, s, w, scale,
-                                              args.steps, stream)
-        log(f"pipelined, HBM: {pipelined_hbm['ms_per_step']:.3f} ms/step, "
-            f"{pipelined_hbm['tokens_per_s']:.0f} tokens/s, per layer "
-            f"{pipelined_hbm['per_layer_us']}")
-
-    host_link = None
-    if not args.no_host_link:
-        host_link = measure_host_link(torch, ckv, dev)
-        log(f"host link: {host_link}")
-    pipeline = None
-    if not args.no_pipeline:
-        del layers[1:]  # keep layer 0 for the CPU baseline, free 62 GiB
-        torch.cuda.empty_cache()
-        pipeline = measure_pipeline(torch, ckv, synth, dev, np, host_link)
-        log(f"pipeline: {pipeline}")
-        torch.cuda.empty_cache()
-        # the dual-token serving workload: 64 requests of ragged contexts
-        pipeline["dual64"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "dual64",
-                                              n_hbm=2, n_host=1, steps=3, runs=("plain",))
-        log(f"pipeline dual64: {pipeline['dual64']}")
-        torch.cuda.empty_cache()
-        # the million-token single request
-        pipeline["million"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "million",
-                                               n_hbm=2, n_host=2, steps=4, runs=("plain",),
-                                               layer_queries=True)
-        log(f"pipeline million: {pipeline['million']}")
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(layers, w, scale, np)
-        log(f"cpu baseline: {cpu}")
-
-    result = {
-        "metric": METRIC,
-        "value": tokens_per_s,
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "accumulate": "f32",
-        "data": "synthetic",
-        "config": {
-            "workload": "Llama-3-8B-shaped decode, 32 layers: B16, 32 q / 8 KV heads, "
-                        "head_dim 128, context 32768, k 2048 per KV head, K/V in HBM "
-                        + ("(K|V interleaved per position)" if args.layout == "interleaved"
-                           else "(separate K and V caches)"),
-            "layout": args.layout,
-            "batch": B, "context": n, "k": k, "layers": L, "q_heads": Hq,
-            "kv_heads": Hkv, "head_dim": d, "placement": "hbm",
-        },
-        "hbm_algorithmic_gbps_step": step_bytes / (ms_step * 1e-3) / 1e9,
-        "ms_per_step_unstamped": ms_plain,
-        "kernels": per_kernel,
-        "roofline": roofline,
-        "chunked": chunked,
-        "pipelined_hbm": pipelined_hbm,
-        "graph": graph,
-        "dual_token": dual_token,
-        "host_link": host_link,
-        "pipeline": pipeline,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(result), flush=True)
-    return 0
+    del idx, nsel, out, ws
+    return {"value": tokens_per_s, "ms_per_step": ms_step,
+            "ms_per_step_median": median(per_step), "ms_per_step_unstamped": ms_plain,
+            "hbm_algorithmic_gbps_step": step_bytes / (ms_step * 1e-3) / 1e9,
+            "kernels": per_kernel, "roofline": roofline}
 
 
 def measure_host_link(torch, ckv, dev):
@@ -343,17 +391,20 @@ def measure_host_link(torch, ckv, dev):
         gather()
     torch.cuda.synchronize()
     ckv.profile_begin()
-    reps = 5
+    reps = 20
     for _ in range(reps):
         gather()
     st = ckv.profile_end()
-    c, tot, _ = st["gather"]
+    c, tot, mx = st["gather"]
     gbytes = B * Hkv * k * 2 * d * 2
     gather_gbps = gbytes / (tot / c * 1e-3) / 1e9
     del kv
     return {"gather_GBps": gather_gbps, "h2d_copy_GBps": copy_gbps,
             "frac_of_copy": gather_gbps / copy_gbps, "bytes_per_gather": gbytes,
-            "workload": "B8, 8 KV heads, n 131072, k 4096, 512-byte K|V rows, pinned host"}
+            "gathers": c, "avg_gather_us": 1e3 * tot / c, "max_gather_us": 1e3 * mx,
+            "workload": "B8, 8 KV heads, n 131072, k 4096, 512-byte K|V rows, pinned host; "
+                        "2 untimed and 20 timed gathers (the only gathers of "
+                        "`bench.py --sections host_link`)"}
 
 
 def measure_dual_token(torch, ckv, w, scale, stream, reps=50):
@@ -600,8 +651,8 @@ def _pipeline_streams(torch):
 
 
 def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm=4, n_host=2,
-                     steps=4, runs=("plain", "corrected", "lowrank"), layer_queries=False,
-                     gather_width=0):
+                     steps=20, runs=("plain", "corrected", "lowrank"), layer_queries=False,
+                     gather_width=0, warm=2, stamped=3):
     """The two-buffer decode loop of 32 layers on a host-pinned workload: the
     long-context one (B8, 32 q / 8 KV heads, n 131072, k 4096) or the
     dual-token one (B64, n_b ~ U{16384..65536}, k 2048); K|V rows in pinned
@@ -614,7 +665,10 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
     stream); a third run rebuilds the misses' keys in every layer from rank-32
     factors (per (request, KV head), one set per host layer) and fetches only
     their values.  Step time from events on the compute stream after it has
-    joined the copy stream.  layer_queries: every step's query of a layer is
+    joined the copy stream: the median over `steps` unstamped steady-state
+    steps (events after every step), after `warm` untimed steps; a further
+    `stamped` steps with every kernel stamped give the per-kernel times.
+    layer_queries: every step's query of a layer is
     the workload's own query of that layer (the million-token keys cluster
     along it), instead of fresh draws per step."""
     w = synth.WORKLOADS[wl]
@@ -633,20 +687,21 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
     torch.cuda.empty_cache()
     g = torch.Generator(device=dev)
     g.manual_seed(1234)
+    total_steps = warm + steps + stamped
     if layer_queries:
-        q = [[lq[l % n_hbm] for l in range(L)] for _ in range(steps + 3)]
+        q = [[lq[l % n_hbm] for l in range(L)] for _ in range(total_steps + 1)]
     else:
         q = [[torch.randn((B, Hq, d), generator=g, device=dev).to(torch.bfloat16)
-              for _ in range(L)] for _ in range(steps + 3)]
+              for _ in range(L)] for _ in range(total_steps + 1)]
     qs = [[(0.8 * q[st + 1][l].float() + 0.6 * torch.randn((B, Hq, d), generator=g,
                                                            device=dev)).to(torch.bfloat16)
-           for l in range(L)] for st in range(steps + 2)]
+           for l in range(L)] for st in range(total_steps)]
     i32 = dict(dtype=torch.int32, device=dev)
     idx = [[torch.empty((B, Hkv, k), **i32) for _ in range(L)] for _ in range(2)]
     nsel = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(2)]
     idx_true = [torch.empty((B, Hkv, k), **i32) for _ in range(L)]
     n_true = [torch.empty((B, Hkv), **i32) for _ in range(L)]
-    hits = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(steps + 1)]
+    hits = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(total_steps)]
     out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
     k_buf = [torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev) for _ in range(2)]
     v_buf = [torch.empty_like(k_buf[0]) for _ in range(2)]
@@ -685,38 +740,58 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
             pipe.set_gather_width(gather_width)
         copy.wait_stream(compute)
         pipe.prime(shape, k, io(0, 0), ckv.SRC_HOST_PINNED, k_buf, v_buf, copy)
-        cur = 0
-        pipe.step(shape, io(0, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf, ws,
-                  compute, copy)  # warm-up step
-        cur = 1 - cur
-        compute.wait_stream(copy)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ckv.profile_begin()
-        e0.record(compute)
-        for st in range(1, steps + 1):
+        cur, st = 0, 0
+
+        def one_step():
+            nonlocal cur, st
             pipe.step(shape, io(st, cur), lens, k, scale, ckv.SRC_HOST_PINNED, k_buf, v_buf,
                       ws, compute, copy)
-            cur = 1 - cur
+            cur, st = 1 - cur, st + 1
+
+        for _ in range(warm):
+            one_step()
         compute.wait_stream(copy)
-        e1.record(compute)
+        torch.cuda.synchronize()
+        # timed, unstamped: an event on the compute stream after each step
+        # (the copy stream keeps prefetching across step boundaries, as in
+        # serving); the last event follows the compute stream's join with it
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 2)]
+        first = st
+        ev[0].record(compute)
+        for i in range(steps):
+            one_step()
+            ev[i + 1].record(compute)
+        compute.wait_stream(copy)
+        ev[steps + 1].record(compute)
+        torch.cuda.synchronize()
+        per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+        ms_mean = ev[0].elapsed_time(ev[steps + 1]) / steps
+        ms = median(per)
+        # breakdown (separate, untimed): every kernel stamped for a few steps
+        ckv.profile_begin()
+        for _ in range(stamped):
+            one_step()
+        compute.wait_stream(copy)
         torch.cuda.synchronize()
         stats = ckv.profile_end()
         pipe.close()
-        ms = e0.elapsed_time(e1) / steps
         host_bytes = L * B * Hkv * k * 2 * d * 2
-        gather_ms = stats.get("gather", (0, 0.0, 0.0))[1] / steps
-        compute_ms = sum(v[1] for kname, v in stats.items() if kname != "gather") / steps
-        res = {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3),
+        gather_ms = stats.get("gather", (0, 0.0, 0.0))[1] / stamped
+        compute_ms = sum(v[1] for kname, v in stats.items() if kname != "gather") / stamped
+        res = {"ms_per_step": ms, "ms_per_step_mean": ms_mean,
+               "ms_per_step_min": min(per), "ms_per_step_max": max(per),
+               "timed_steps": steps, "tokens_per_s": B / (ms * 1e-3),
                "host_bytes_per_step": host_bytes,
                "host_GBps_step": host_bytes / (ms * 1e-3) / 1e9,
+               "stamped_steps": stamped,
                "gather_ms_per_step": gather_ms, "compute_kernels_ms_per_step": compute_ms,
-               "kernels_ms_per_step": {kname: round(v[1] / steps, 4)
+               "kernels_ms_per_step": {kname: round(v[1] / stamped, 4)
                                        for kname, v in stats.items()},
                "overlap": (gather_ms + compute_ms) / ms,
                "gather_workgroups": gather_width or ("auto: 80" if n >= 64 * k else "auto: 256")}
         if corrected:  # the misses cross the link too, on the compute stream
-            found = sum(int(hits[st][l].sum()) for st in range(1, steps + 1) for l in range(L))
+            found = sum(int(hits[t][l].sum()) for t in range(first, first + steps)
+                        for l in range(L))
             total = steps * L * B * Hkv * min(k, n)
             res["hit_rate"] = found / total
             # a rebuilt miss fetches its value only

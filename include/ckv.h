@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 4
+#define CKV_ABI_VERSION 5
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -410,9 +410,10 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
  * back before the capture ends).  A fill recorded outside the capture (by
  * the prime or an eager step) is not waited for inside it, so the caller
  * orders each launch of the graph after the copy stream's earlier work
- * (e.g. compute_stream waits for copy_stream before the first launch); a
- * graph of an even number of layers leaves the buffers as it found them
- * for its next launch. */
+ * (e.g. compute_stream waits for copy_stream before the first launch).  A
+ * captured two-buffer step must have an even number of layers, so that the
+ * graph leaves the buffers as it found them for its next launch; an odd
+ * number under capture is CKV_EINVAL. */
 int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
                     const ckv_layer* layers, const int32_t* ctx_lens, int32_t k,
                     float scale, int src_kind, uint16_t* const k_buf[2],
@@ -458,6 +459,12 @@ const char* ckv_kernel_name(int id);
  * in kernel_mask; other kernels launch unstamped.  Drops anything recorded
  * before. */
 int ckv_profile_begin(uint32_t kernel_mask);
+
+/* ckv_profile_begin, stamping only launches 0, every, 2*every, ... of each
+ * recorded class (every >= 1, else CKV_EINVAL).  A stamped dispatch costs a
+ * few microseconds of stream time more than a plain one, so a timed loop
+ * that also measures one kernel's duration stamps a sample of its launches. */
+int ckv_profile_begin_sampled(uint32_t kernel_mask, uint32_t every);
 
 /* Stop recording, wait for the recorded kernels to finish and write one
  * entry per ckv_kernel_id into stats[0 .. CKV_K_COUNT). */

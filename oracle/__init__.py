@@ -21,12 +21,15 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "ckv_oracle.c")
-LIB = os.path.join(HERE, "libckv_oracle.so")
+# CKV_ORACLE_LIB names another build of the same source (the sanitizer run
+# of the pin suite loads one built with -fsanitize=address,undefined)
+DEFAULT_LIB = os.path.join(HERE, "libckv_oracle.so")
+LIB = os.environ.get("CKV_ORACLE_LIB") or DEFAULT_LIB
 
 
-def build(src: str = SRC, out: str = LIB) -> str:
+def build(src: str = SRC, out: str = DEFAULT_LIB, extra=()) -> str:
     """Compile the oracle with gcc (-O2, C11) into a shared library."""
-    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-shared", "-fPIC",
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-shared", "-fPIC", *extra,
            f"-I{HERE}", "-o", out, src, "-lm", "-lpthread"]
     subprocess.run(cmd, check=True)
     return out
@@ -58,7 +61,7 @@ class Oracle:
     """ctypes handle on one build of the oracle library."""
 
     def __init__(self, path: str = LIB):
-        if path == LIB and not os.path.exists(LIB):
+        if path == DEFAULT_LIB and not os.path.exists(DEFAULT_LIB):
             build()
         self.path = path
         lib = ctypes.CDLL(path)

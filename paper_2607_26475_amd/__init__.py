@@ -40,13 +40,14 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_corrected_attn", "ckv_chunk_landmarks", "ckv_select_chunks",
            "ckv_chunked_kv_attn", "ckv_dual_token_attn", "ckv_reconstruct_keys",
            "ckv_corrected_attn_lowrank",
-           "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_end",
+           "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_begin_sampled",
+           "ckv_profile_end",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
            "ckv_pipeline_prime",
            "ckv_decode_step")
 KERNEL_COUNT = 13
 MAX_RANK = 4096
-ABI_VERSION = 4  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
+ABI_VERSION = 5  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -116,6 +117,7 @@ def _load() -> ctypes.CDLL:
                                                       vp, sz, vp]),
         "ckv_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
+        "ckv_profile_begin_sampled": (ctypes.c_int, [ctypes.c_uint32, ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
         "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
         "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
@@ -301,15 +303,16 @@ KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn"
               "expand": 11, "reconstruct": 12}
 
 
-def profile_begin(kernels=None) -> None:
+def profile_begin(kernels=None, every: int = 1) -> None:
     """Start stamping library kernels with dispatch start/end events: all of
-    them, or only the named kernel classes."""
+    them, or only the named kernel classes; with every > 1 only launches 0,
+    every, 2*every, ... of each class."""
     mask = (1 << KERNEL_COUNT) - 1
     if kernels is not None:
         mask = 0
         for name in kernels:
             mask |= 1 << KERNEL_IDS[name]
-    _check("ckv_profile_begin", _lib.ckv_profile_begin(mask))
+    _check("ckv_profile_begin_sampled", _lib.ckv_profile_begin_sampled(mask, every))
 
 
 def profile_end() -> dict:

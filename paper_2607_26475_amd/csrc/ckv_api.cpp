@@ -408,12 +408,12 @@ int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
   ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, sa.hist,
                             sa.coarse);
   sc.chunk = chunk;
-  const int nwg = score_blocks(sc, d.G, false, false);
+  const int nwg = score_blocks(sc, d.G, ScoreKind::kHist);
   if (use_partials(dc, Lc, nwg))
     set_partials(ws, Lc, nwg, &sc, &sa);
   else
     CKV_TRY_HIP(launch_zero(ws, Lc.zero_end, s), "zero launch");
-  CKV_TRY_HIP(launch_score(sc, d.G, true, d.U, s), "score launch");
+  CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
   if ((rc = run_select_tail(sa, d.U, s))) return rc;
   ExpandArgs e;
   e.chunk_idx = chunk_idx;
@@ -513,7 +513,9 @@ int ckv_score_keys(const ckv_shape* shape, const uint16_t* q, const uint16_t* k_
   Layout L = make_layout(d, 1, 0);
   if ((rc = check_grid(d, L))) return rc;
   ScoreArgs a = score_args(d, L, q, k_score, ctx_lens, scale, scores, nullptr, nullptr);
-  CKV_TRY_HIP(launch_score(a, d.G, false, d.U, (hipStream_t)stream), "score launch");
+  CKV_TRY_HIP(launch_score(a, d.G, false, score_blocks(a, d.G, ScoreKind::kPlain),
+                           (hipStream_t)stream),
+              "score launch");
   return CKV_OK;
 }
 
@@ -615,7 +617,8 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
   ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, sa.hist, sa.coarse);
   const bool pipelined = assembled || in_place;
-  const int nwg = score_blocks(sc, d.G, pipelined, in_place);
+  const int nwg = score_blocks(
+      sc, d.G, !pipelined ? ScoreKind::kHist : in_place ? ScoreKind::kDualIndexed : ScoreKind::kDual);
   if (use_partials(d, L, nwg))
     set_partials(ws, L, nwg, &sc, &sa);
   else
@@ -625,10 +628,10 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                                          k, scale, out)
                              : attn_args(d, L, ws, q_att, k_src, v_src, idx_in, n_sel_in,
                                          d.kv_stride, k, scale, out);
-    CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, s), "dual launch");
+    CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
     if ((rc = select_and_merge(sa, at_, d, s))) return rc;
   } else {
-    CKV_TRY_HIP(launch_score(sc, d.G, true, d.U, s), "score launch");
+    CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
     if ((rc = run_select_tail(sa, d.U, s))) return rc;
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
                              d.kv_stride, k, scale, out);
@@ -821,8 +824,8 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   s2.coarse = at<uint32_t>(ws, L.coarse2);
   s2.ctrl = at<uint32_t>(ws, L.ctrl2);
   ScoreArgs c2 = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, s2.hist, s2.coarse);
-  const int nwg1 = score_blocks(c1, d.G, false, false);
-  const int nwg2 = score_blocks(c2, d.G, true, true);
+  const int nwg1 = score_blocks(c1, d.G, ScoreKind::kHist);
+  const int nwg2 = score_blocks(c2, d.G, ScoreKind::kDualIndexed);
   if (use_partials(d, L, nwg1) && use_partials(d, L, nwg2)) {
     // both selections use the slots in turn: the first reads them before the
     // dual launch writes them again
@@ -831,7 +834,7 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   } else {
     CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
   }
-  CKV_TRY_HIP(launch_score(c1, d.G, true, d.U, s), "score launch");
+  CKV_TRY_HIP(launch_score(c1, d.G, true, nwg1, s), "score launch");
   if ((rc = run_select_tail(s1, d.U, s))) return rc;
   // 2. hits and misses against the predicted set; misses into free slots
   MissArgs m;
@@ -873,7 +876,7 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   db.max_ctx = k;
   AttnArgs at_ = attn_args(db, L, ws, q_att, k_buf, v_buf, m.slot_of, n_true, kD, k, scale,
                            out);
-  CKV_TRY_HIP(launch_dual(at_, c2, d.G, true, d.U, s), "dual launch");
+  CKV_TRY_HIP(launch_dual(at_, c2, d.G, true, d.U, nwg2, s), "dual launch");
   return select_and_merge(s2, at_, d, s);
 }
 

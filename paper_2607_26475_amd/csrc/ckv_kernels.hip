@@ -5,6 +5,10 @@
 #include "ckv_score.hpp"
 #include "ckv_topk.hpp"
 
+#include <map>
+#include <mutex>
+#include <utility>
+
 namespace ckv {
 
 // ---- workspace clearing (a kernel, not hipMemsetAsync: safe to capture) ----
@@ -932,11 +936,21 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Workgroups that fit on the device at once for a 256-thread kernel; the
-// persistent scoring grid is this many workgroups (or fewer if less work).
+// Workgroups of a kScoreThreads kernel that fit on the device at once, per
+// (kernel, device): queried once and cached, so a call makes no occupancy
+// query.  The persistent scoring grid is this many workgroups (or fewer if
+// there is less work).
 static int resident_blocks(const void* fn) {
-  int dev = 0, cus = 0, per_cu = 0;
+  int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 1024;
+  static std::mutex mu;
+  static std::map<std::pair<const void*, int>, int> cache;
+  {
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = cache.find({fn, dev});
+    if (it != cache.end()) return it->second;
+  }
+  int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus < 1)
     cus = 256;
@@ -944,10 +958,33 @@ static int resident_blocks(const void* fn) {
           hipSuccess ||
       per_cu < 1)
     per_cu = 1;
+  std::lock_guard<std::mutex> lk(mu);
+  cache[{fn, dev}] = cus * per_cu;
   return cus * per_cu;
 }
 
-static int score_grid(const ScoreArgs& a, const void* fn) {
+template <int G>
+static const void* score_kernel(ScoreKind kind, int chunk) {
+  switch (kind) {
+    case ScoreKind::kPlain: return (const void*)k_score<G, false>;
+    case ScoreKind::kHist:
+      return chunk > 1 ? (const void*)k_score_chunks<G> : (const void*)k_score<G, true>;
+    case ScoreKind::kDual: return (const void*)k_dual<G, false>;
+    case ScoreKind::kDualIndexed: return (const void*)k_dual<G, true>;
+  }
+  return nullptr;
+}
+
+int score_blocks(const ScoreArgs& a, int G, ScoreKind kind) {
+  const void* fn = nullptr;
+  switch (G) {
+    case 1: fn = score_kernel<1>(kind, a.chunk); break;
+    case 2: fn = score_kernel<2>(kind, a.chunk); break;
+    case 4: fn = score_kernel<4>(kind, a.chunk); break;
+    case 8: fn = score_kernel<8>(kind, a.chunk); break;
+    case 16: fn = score_kernel<16>(kind, a.chunk); break;
+    default: return 0;
+  }
   const int64_t groups = (int64_t)a.units * ((a.max_ctx + kStageRows - 1) / kStageRows);
   int64_t slots = resident_blocks(fn);
   if (slots > kMaxScoreWgs) slots = kMaxScoreWgs;
@@ -955,47 +992,21 @@ static int score_grid(const ScoreArgs& a, const void* fn) {
 }
 
 template <int G>
-static int score_blocks_g(const ScoreArgs& a, bool dual, bool indexed) {
-  const void* fn = dual ? (indexed ? (const void*)k_dual<G, true> : (const void*)k_dual<G, false>)
-                        : (a.chunk > 1 ? (const void*)k_score_chunks<G>
-                                       : (const void*)k_score<G, true>);
-  return score_grid(a, fn);
+static void launch_score_g(const ScoreArgs& a, bool hist, int nwg, hipStream_t s) {
+  const dim3 grid(nwg), block(kScoreThreads);
+  if (a.chunk > 1) launch_kernel(CKV_K_SCORE, k_score_chunks<G>, grid, block, s, a);
+  else if (hist) launch_kernel(CKV_K_SCORE, k_score<G, true>, grid, block, s, a);
+  else launch_kernel(CKV_K_SCORE, k_score<G, false>, grid, block, s, a);
 }
 
-int score_blocks(const ScoreArgs& a, int G, bool dual, bool indexed) {
+hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int nwg, hipStream_t s) {
+  if (nwg < 1 || nwg > kMaxScoreWgs) return hipErrorInvalidValue;
   switch (G) {
-    case 1: return score_blocks_g<1>(a, dual, indexed);
-    case 2: return score_blocks_g<2>(a, dual, indexed);
-    case 4: return score_blocks_g<4>(a, dual, indexed);
-    case 8: return score_blocks_g<8>(a, dual, indexed);
-    case 16: return score_blocks_g<16>(a, dual, indexed);
-    default: return 0;
-  }
-}
-
-template <int G>
-static void launch_score_g(const ScoreArgs& a, bool hist, hipStream_t s) {
-  const dim3 block(kScoreThreads);
-  if (a.chunk > 1) {
-    auto fn = k_score_chunks<G>;
-    launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
-  } else if (hist) {
-    auto fn = k_score<G, true>;
-    launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
-  } else {
-    auto fn = k_score<G, false>;
-    launch_kernel(CKV_K_SCORE, fn, dim3(score_grid(a, (const void*)fn)), block, s, a);
-  }
-}
-
-hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s) {
-  (void)units;
-  switch (G) {
-    case 1: launch_score_g<1>(a, hist, s); break;
-    case 2: launch_score_g<2>(a, hist, s); break;
-    case 4: launch_score_g<4>(a, hist, s); break;
-    case 8: launch_score_g<8>(a, hist, s); break;
-    case 16: launch_score_g<16>(a, hist, s); break;
+    case 1: launch_score_g<1>(a, hist, nwg, s); break;
+    case 2: launch_score_g<2>(a, hist, nwg, s); break;
+    case 4: launch_score_g<4>(a, hist, nwg, s); break;
+    case 8: launch_score_g<8>(a, hist, nwg, s); break;
+    case 16: launch_score_g<16>(a, hist, nwg, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1054,33 +1065,32 @@ hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
 }
 
 template <int G, bool INDEXED>
-static void launch_dual_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks,
+static void launch_dual_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks, int nwg,
                           hipStream_t s) {
-  auto fn = k_dual<G, INDEXED>;
-  const int score_blocks = score_grid(sc, (const void*)fn);
-  launch_kernel(CKV_K_DUAL, fn, dim3(attn_blocks + score_blocks), dim3(kAttnThreads), s, at,
-                sc, attn_blocks);
+  launch_kernel(CKV_K_DUAL, k_dual<G, INDEXED>, dim3(attn_blocks + nwg), dim3(kAttnThreads), s,
+                at, sc, attn_blocks);
 }
 
 template <bool INDEXED>
 static hipError_t launch_dual_i(const AttnArgs& at, const ScoreArgs& sc, int G,
-                                int attn_blocks, hipStream_t s) {
+                                int attn_blocks, int nwg, hipStream_t s) {
   switch (G) {
-    case 1: launch_dual_g<1, INDEXED>(at, sc, attn_blocks, s); break;
-    case 2: launch_dual_g<2, INDEXED>(at, sc, attn_blocks, s); break;
-    case 4: launch_dual_g<4, INDEXED>(at, sc, attn_blocks, s); break;
-    case 8: launch_dual_g<8, INDEXED>(at, sc, attn_blocks, s); break;
-    case 16: launch_dual_g<16, INDEXED>(at, sc, attn_blocks, s); break;
+    case 1: launch_dual_g<1, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 2: launch_dual_g<2, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 4: launch_dual_g<4, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 8: launch_dual_g<8, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 16: launch_dual_g<16, INDEXED>(at, sc, attn_blocks, nwg, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
-                       int units, hipStream_t s) {
+                       int units, int nwg, hipStream_t s) {
+  if (nwg < 1 || nwg > kMaxScoreWgs) return hipErrorInvalidValue;
   const int attn_blocks = units * at.chunks;
-  return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, s)
-                 : launch_dual_i<false>(at, sc, G, attn_blocks, s);
+  return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, nwg, s)
+                 : launch_dual_i<false>(at, sc, G, attn_blocks, nwg, s);
 }
 
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s) {

@@ -13,10 +13,15 @@ int hip_fail(hipError_t e, const char* what);
 const char* last_detail();
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
-hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int units, hipStream_t s);
-// workgroups of the scoring pass (with a histogram) or of the dual kernel's
-// scoring role for these arguments: the grid the launchers use
-int score_blocks(const ScoreArgs& a, int G, bool dual, bool indexed);
+// The kernel that runs a scoring pass: scores only, scores with the
+// first-digit histogram (chunk landmarks when a.chunk > 1), or the scoring
+// role of the one-launch attend-and-score kernel (buffer or rows in place).
+enum class ScoreKind { kPlain, kHist, kDual, kDualIndexed };
+// Workgroups of that scoring pass for these arguments.  A call computes it
+// once and passes the same value to the launcher and to the selection, whose
+// histogram slots depend on it.
+int score_blocks(const ScoreArgs& a, int G, ScoreKind kind);
+hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int nwg, hipStream_t s);
 hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s);
@@ -24,7 +29,7 @@ hipError_t launch_select_fused(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
-                       int units, hipStream_t s);
+                       int units, int nwg, hipStream_t s);
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s);
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s);
 hipError_t launch_expand(const ExpandArgs& a, int units, hipStream_t s);

@@ -132,6 +132,13 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     return ckv::fail(CKV_EINVAL, "the two-buffer loop needs at least 2 layers and both buffers");
   hipStream_t cs = (hipStream_t)compute_stream, xs = (hipStream_t)copy_stream;
   const unsigned long long capture = capture_id(cs);
+  // A graph fixes each layer's buffer at capture time.  Over an odd number of
+  // layers the last refills land in the buffers of the other parity, so a
+  // second launch of the graph would attend over another layer's rows.
+  if (capture && (num_layers & 1))
+    return ckv::fail(CKV_EINVAL,
+                     "a captured two-buffer step needs an even number of layers (got %d)",
+                     num_layers);
   for (int l = 0; l < num_layers; ++l) {
     const int p = pipe->parity;
     const ckv_layer& L = layers[l];

@@ -16,6 +16,8 @@ struct Record {
 
 std::atomic<bool> g_on{false};
 std::atomic<uint32_t> g_mask{0};
+uint32_t g_every = 1;                 // stamp one launch in g_every per class
+uint64_t g_seen[CKV_K_COUNT] = {};    // launches of each class since begin
 std::mutex g_mu;
 std::vector<Record> g_records;
 std::vector<hipEvent_t> g_pool;
@@ -46,6 +48,7 @@ bool profile_events(int id, hipEvent_t* start, hipEvent_t* stop) {
   if (!((g_mask.load(std::memory_order_relaxed) >> id) & 1u)) return false;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on.load(std::memory_order_relaxed)) return false;
+  if (g_seen[id]++ % g_every) return false;
   hipEvent_t a = take_event(), b = take_event();
   if (!a || !b) {
     if (a) g_pool.push_back(a);
@@ -69,13 +72,18 @@ const char* ckv_kernel_name(int id) {
   return (id >= 0 && id < CKV_K_COUNT) ? names[id] : "";
 }
 
-int ckv_profile_begin(uint32_t kernel_mask) {
+int ckv_profile_begin_sampled(uint32_t kernel_mask, uint32_t every) {
+  if (every < 1) return ckv::fail(CKV_EINVAL, "every must be at least 1");
   std::lock_guard<std::mutex> lk(ckv::g_mu);
   ckv::recycle_all();
+  ckv::g_every = every;
+  for (uint64_t& c : ckv::g_seen) c = 0;
   ckv::g_mask.store(kernel_mask & CKV_K_ALL);
   ckv::g_on.store(true);
   return CKV_OK;
 }
+
+int ckv_profile_begin(uint32_t kernel_mask) { return ckv_profile_begin_sampled(kernel_mask, 1); }
 
 int ckv_profile_end(ckv_kernel_stats* stats) {
   if (!stats) return ckv::fail(CKV_EINVAL, "stats is NULL");

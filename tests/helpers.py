@@ -47,6 +47,13 @@ def orc() -> oracle.Oracle:
     return oracle.get()
 
 
+# Running totals of the index-set comparisons of this test session, printed
+# in pytest's terminal summary (tests/conftest.py): units compared, units
+# whose sets differ by tolerated near-tie swaps, the most entries swapped in
+# one unit and the largest gap found, relative to |tau|.
+SWAP_STATS = {"units": 0, "swapped_units": 0, "max_entries": 0, "max_gap_rel": 0.0}
+
+
 def check_index_sets(gpu_idx, gpu_nsel, orc_idx, orc_nsel, S, lens, units=None):
     """Compare GPU and oracle index sets unit by unit under the near-tie rule.
 
@@ -67,6 +74,7 @@ def check_index_sets(gpu_idx, gpu_nsel, orc_idx, orc_nsel, S, lens, units=None):
             assert P[0] >= 0 and P[-1] < n, (b, h, P[0], P[-1], n)
             assert np.all(np.diff(P) > 0), (b, h, "not ascending / duplicates")
         O = orc_idx[b, h, :m].astype(np.int64)
+        SWAP_STATS["units"] += 1
         if np.array_equal(P, O):
             continue
         swaps += 1
@@ -77,6 +85,10 @@ def check_index_sets(gpu_idx, gpu_nsel, orc_idx, orc_nsel, S, lens, units=None):
         tau = Su[O].min()
         gap = Su[missing].max() - Su[extra].min()
         assert gap <= TIE_REL * abs(tau), (b, h, len(missing), gap, tau)
+        SWAP_STATS["swapped_units"] += 1
+        SWAP_STATS["max_entries"] = max(SWAP_STATS["max_entries"], len(missing))
+        if tau != 0:
+            SWAP_STATS["max_gap_rel"] = max(SWAP_STATS["max_gap_rel"], float(gap / abs(tau)))
     return swaps
 
 

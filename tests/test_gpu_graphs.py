@@ -179,7 +179,7 @@ def test_decode_loop_graph():
     _log("graph decode loop")
     dev = device()
     w = synth.WORKLOADS["long128k_s"]
-    layers = 3
+    layers = 4  # a captured two-buffer step needs an even number of layers
     lg = Loop(w, layers, steps=2, seed=12, dev=dev)
     le = Loop(w, layers, steps=2, seed=12, dev=dev)
     pipes = {}
@@ -218,3 +218,37 @@ def test_decode_loop_graph():
     for p in pipes.values():
         p.close()
     _log("  3 replays of two steps identical to eager steps")
+
+
+def test_decode_loop_graph_refuses_odd_layers():
+    """A graph fixes each layer's buffer at capture time, so a captured
+    two-buffer step over an odd number of layers would attend over another
+    layer's rows at its next launch: the call is refused (CKV_EINVAL) and
+    enqueues nothing."""
+    from test_gpu_pipeline import Loop
+
+    _log("graph decode loop, odd layer count")
+    dev = device()
+    w = synth.WORKLOADS["long128k_s"]
+    lp = Loop(w, 3, steps=1, seed=13, dev=dev)
+    lp.bootstrap()
+    pipe = ckv.Pipeline()
+    lp.copy.wait_stream(lp.compute)
+    pipe.prime(lp.shape, w.k, lp.layer_io(1, 0), ckv.SRC_HOST_PINNED, lp.k_buf, lp.v_buf,
+               lp.copy)
+    torch.cuda.synchronize()
+    raised = []
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cs = torch.cuda.current_stream()
+        lp.copy.wait_stream(cs)
+        try:
+            pipe.step(lp.shape, lp.layer_io(1, 0), lp.lens, w.k, SCALE, ckv.SRC_HOST_PINNED,
+                      lp.k_buf, lp.v_buf, lp.ws, cs, lp.copy)
+        except ckv.CkvError as e:
+            raised.append(e)
+        cs.wait_stream(lp.copy)
+    torch.cuda.synchronize()
+    pipe.close()
+    assert raised and raised[0].status == 1, raised
+    assert "even number of layers" in str(raised[0])
