@@ -194,6 +194,32 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          int32_t* n_sel_out, float* out, void* ws,
                          size_t ws_bytes, void* stream);
 
+/* ---- the fused step for callers that cannot allocate -----------------------
+ * For callers that cannot allocate device memory or hold a workspace: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  ckv_critical_kv_attn, with the same arguments and results,
+ * whose workspace is a fixed array of CKV_NOALLOC_SCRATCH_BYTES bytes of
+ * device memory, one per device, that the library holds from its load until
+ * the process ends.  The call allocates and frees nothing; the caller still
+ * passes every input and output.  A shape whose workspace
+ * (ckv_workspace_bytes, CKV_ENTRY_CRITICAL_KV_ATTN) is larger than
+ * CKV_NOALLOC_SCRATCH_BYTES is CKV_EWORKSPACE, before anything is enqueued.
+ * All calls on a device share that device's array, which keeps the last
+ * call's contents (each call clears what it needs cleared): calls on one
+ * device that may overlap in time (on different streams, or from threads
+ * without ordering) race on it, so the caller orders them, e.g. on one
+ * stream. */
+#define CKV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+int ckv_critical_kv_attn_noalloc(const ckv_shape* shape, const uint16_t* q_att,
+                                 const uint16_t* q_sel, const uint16_t* k_score,
+                                 const int32_t* ctx_lens, int32_t k, float scale,
+                                 const uint16_t* k_src, const uint16_t* v_src,
+                                 int src_kind, const int32_t* idx_in,
+                                 const uint16_t* k_buf, const uint16_t* v_buf,
+                                 const int32_t* n_sel_in, int32_t* idx_out,
+                                 int32_t* n_sel_out, float* out, void* stream);
+
 /* Sec. 5.3 (prioritized missing KV transfer) and Sec. 5.4 (GPU-side sparse KV
  * assembly with deferred reordering) -- one layer of a pipelined decode step
  * whose attention uses the current token's own selection, not the

@@ -21,7 +21,7 @@ import torch
 __all__ = [
     "CkvError", "Shape", "shape_for", "workspace_bytes", "workspace",
     "score_keys", "select_topk", "gather_kv", "sparse_decode_attn",
-    "critical_kv_attn", "corrected_attn", "chunk_landmarks", "select_chunks",
+    "critical_kv_attn", "critical_kv_attn_noalloc", "NOALLOC_SCRATCH_BYTES", "corrected_attn", "chunk_landmarks", "select_chunks",
     "chunked_kv_attn", "dual_token_attn", "reconstruct_keys", "corrected_attn_lowrank",
     "MAX_RANK", "ABI_VERSION", "profile_begin", "profile_end", "abi_version",
     "Layer", "layer_array", "Pipeline", "status_str", "LIB_PATH",
@@ -37,6 +37,7 @@ ENTRY_CORRECTED_ATTN, ENTRY_DUAL_TOKEN_ATTN = 4, 5
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
+           "ckv_critical_kv_attn_noalloc",
            "ckv_corrected_attn", "ckv_chunk_landmarks", "ckv_select_chunks",
            "ckv_chunked_kv_attn", "ckv_dual_token_attn", "ckv_reconstruct_keys",
            "ckv_corrected_attn_lowrank",
@@ -99,6 +100,9 @@ def _load() -> ctypes.CDLL:
         "ckv_critical_kv_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                                 vp, vp, ctypes.c_int, vp, vp, vp, vp, vp,
                                                 vp, vp, vp, sz, vp]),
+        "ckv_critical_kv_attn_noalloc": (ctypes.c_int, [sp, vp, vp, vp, vp, i32,
+                                                        ctypes.c_float, vp, vp, ctypes.c_int,
+                                                        vp, vp, vp, vp, vp, vp, vp, vp]),
         "ckv_corrected_attn": (ctypes.c_int, [sp, vp, vp, vp, vp, i32, ctypes.c_float,
                                               vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp,
                                               vp, vp, vp, vp, vp, sz, vp]),
@@ -233,6 +237,21 @@ def critical_kv_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
         scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(idx_in), _ptr(k_buf), _ptr(v_buf),
         _ptr(n_sel_in), _ptr(idx_out), _ptr(n_sel_out), _ptr(out), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # CKV_NOALLOC_SCRATCH_BYTES
+
+
+def critical_kv_attn_noalloc(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int,
+                             scale: float, k_src, v_src, src_kind: int, k_buf, v_buf,
+                             n_sel_in, idx_out, n_sel_out, out, stream=None,
+                             idx_in=None) -> None:
+    """critical_kv_attn with the library's fixed per-device scratch instead of
+    a workspace (the call allocates nothing)."""
+    _check("ckv_critical_kv_attn_noalloc", _lib.ckv_critical_kv_attn_noalloc(
+        ctypes.byref(shape), _ptr(q_att), _ptr(q_sel), _ptr(k_score), _ptr(ctx_lens), k,
+        scale, _ptr(k_src), _ptr(v_src), src_kind, _ptr(idx_in), _ptr(k_buf), _ptr(v_buf),
+        _ptr(n_sel_in), _ptr(idx_out), _ptr(n_sel_out), _ptr(out), _stream(stream)))
 
 
 def corrected_attn(shape: Shape, q_att, q_sel, k_score, ctx_lens, k: int, scale: float,

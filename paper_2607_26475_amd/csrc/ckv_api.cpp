@@ -641,6 +641,32 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   return CKV_OK;
 }
 
+int ckv_critical_kv_attn_noalloc(const ckv_shape* shape, const uint16_t* q_att,
+                                 const uint16_t* q_sel, const uint16_t* k_score,
+                                 const int32_t* ctx_lens, int32_t k, float scale,
+                                 const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                                 const int32_t* idx_in, const uint16_t* k_buf,
+                                 const uint16_t* v_buf, const int32_t* n_sel_in,
+                                 int32_t* idx_out, int32_t* n_sel_out, float* out,
+                                 void* stream) {
+  // the size check first: an oversized shape is refused before any runtime call
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  const size_t need = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN).total;
+  if (need > CKV_NOALLOC_SCRATCH_BYTES)
+    return fail(CKV_EWORKSPACE,
+                "this shape needs %zu bytes of workspace; the fixed scratch holds %zu "
+                "(use ckv_critical_kv_attn with a workspace)",
+                need, (size_t)CKV_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((rc = noalloc_scratch(&ws))) return rc;
+  return ckv_critical_kv_attn(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
+                              src_kind, idx_in, k_buf, v_buf, n_sel_in, idx_out, n_sel_out, out,
+                              ws, CKV_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 int ckv_dual_token_attn(const ckv_shape* shape, const uint16_t* q_cur, const uint16_t* q_spec,
                         const uint16_t* k_buf, const uint16_t* v_buf, const int32_t* n_sel,
                         const uint16_t* k_local, const uint16_t* v_local, int32_t k,

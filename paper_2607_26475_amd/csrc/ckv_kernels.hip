@@ -5,9 +5,7 @@
 #include "ckv_score.hpp"
 #include "ckv_topk.hpp"
 
-#include <map>
 #include <mutex>
-#include <utility>
 
 namespace ckv {
 
@@ -921,6 +919,37 @@ __global__ __launch_bounds__(kGatherThreads) void k_miss_fill(GatherArgs g, Reco
     reconstruct_range(r, blockIdx.x - nfetch, gridDim.x - nfetch);
 }
 
+// ---- fixed scratch for callers that cannot allocate -------------------------
+// The workspace of ckv_critical_kv_attn_noalloc: one array per device, held
+// for the life of the process.  Its name is a host-side stand-in in host
+// code, never an address: the device address of each device's copy is asked
+// of the runtime once, with that device current, and only that address is
+// passed to kernels.
+static __device__ __align__(256) uint8_t scratch[CKV_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 256;
+
+int noalloc_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "current device");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(CKV_EUNSUPPORTED, "device %d (the fixed scratch serves devices below %d)", dev,
+                kMaxDevices);
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "device address of the fixed scratch");
+    if (!p) return fail(CKV_EHIP, "device address of the fixed scratch is NULL");
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return CKV_OK;
+}
+
 // ---- launchers ---------------------------------------------------------------
 static inline int blocks_for(int64_t n, int per, int cap) {
   int64_t b = (n + per - 1) / per;
@@ -937,18 +966,24 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
 }
 
 // Workgroups of a kScoreThreads kernel that fit on the device at once, per
-// (kernel, device): queried once and cached, so a call makes no occupancy
-// query.  The persistent scoring grid is this many workgroups (or fewer if
-// there is less work).
+// (kernel, device): queried once and kept in a fixed table (no allocation on
+// the call path), so a call makes no occupancy query.  The persistent
+// scoring grid is this many workgroups (or fewer if there is less work).
 static int resident_blocks(const void* fn) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 1024;
+  struct Entry {
+    const void* fn;
+    int dev, blocks;
+  };
+  constexpr int kEntries = 512;
+  static Entry table[kEntries];
+  static int used = 0;
   static std::mutex mu;
-  static std::map<std::pair<const void*, int>, int> cache;
   {
     std::lock_guard<std::mutex> lk(mu);
-    auto it = cache.find({fn, dev});
-    if (it != cache.end()) return it->second;
+    for (int i = 0; i < used; ++i)
+      if (table[i].fn == fn && table[i].dev == dev) return table[i].blocks;
   }
   int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -959,7 +994,7 @@ static int resident_blocks(const void* fn) {
       per_cu < 1)
     per_cu = 1;
   std::lock_guard<std::mutex> lk(mu);
-  cache[{fn, dev}] = cus * per_cu;
+  if (used < kEntries) table[used++] = Entry{fn, dev, cus * per_cu};
   return cus * per_cu;
 }
 

@@ -39,6 +39,11 @@ hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconAr
                             hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s);
 
+// Device address of the current device's fixed scratch array
+// (CKV_NOALLOC_SCRATCH_BYTES), asked of the runtime on the first call per
+// device.
+int noalloc_scratch(void** ptr);
+
 // Largest gather grid a caller may ask for.
 constexpr int kMaxGatherWgs = 4096;
 // ckv_gather_kv with an explicit grid: `workgroups` (0: the default for

@@ -223,6 +223,20 @@ int main() {
            CKV_EUNSUPPORTED);
   }
 
+  // the fixed-scratch entry refuses a shape whose workspace does not fit,
+  // before any runtime call
+  {
+    const ckv_shape s = shape(8, 32, 8, 131072);
+    EXPECT(ckv_critical_kv_attn_noalloc(&s, F16, nullptr, F16, FI, 4096, 0.1f, F16, F16,
+                                        CKV_SRC_DEVICE, nullptr, nullptr, nullptr, nullptr, FI,
+                                        FI, FF, nullptr),
+           CKV_EWORKSPACE);
+    EXPECT(ckv_critical_kv_attn_noalloc(&s, F16, nullptr, F16, FI, 0, 0.1f, F16, F16,
+                                        CKV_SRC_DEVICE, nullptr, nullptr, nullptr, nullptr, FI,
+                                        FI, FF, nullptr),
+           CKV_ESHAPE);
+  }
+
   // pipeline object: creation needs the device (events); argument checks do not
   {
     const ckv_shape s = shape(2, 8, 2, 64);

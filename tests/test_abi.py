@@ -258,3 +258,24 @@ def test_critical_kv_attn_mode_checks():
     assert "exclusive" in (lib.ckv_critical_kv_attn(
         ctypes.byref(s), FAKE, None, FAKE, FAKE, 16, 0.1, FAKE, FAKE, 0, FAKE, FAKE, FAKE,
         FAKE, FAKE, FAKE, FAKE, FAKE, need, 0), ckv._lib.ckv_last_error_detail().decode())[1]
+
+
+def test_noalloc_entry_refuses_oversized_shapes():
+    """The fixed-scratch entry checks the shape's workspace against
+    CKV_NOALLOC_SCRATCH_BYTES before any runtime call (so also without a GPU)."""
+    lib = ckv._lib
+    big = good_shape(batch=8, num_q_heads=32, num_kv_heads=8, max_ctx=131072)
+    assert ckv.workspace_bytes(big, 4096, ckv.ENTRY_CRITICAL_KV_ATTN) > ckv.NOALLOC_SCRATCH_BYTES
+    rc = lib.ckv_critical_kv_attn_noalloc(ctypes.byref(big), FAKE, None, FAKE, FAKE, 4096, 0.1,
+                                          FAKE, FAKE, 0, None, None, None, None, FAKE, FAKE,
+                                          FAKE, 0)
+    assert rc == STATUS["EWORKSPACE"]
+    assert "fixed scratch" in lib.ckv_last_error_detail().decode()
+    # argument errors come first too
+    assert lib.ckv_critical_kv_attn_noalloc(ctypes.byref(big), FAKE, None, FAKE, FAKE, 0, 0.1,
+                                            FAKE, FAKE, 0, None, None, None, None, FAKE, FAKE,
+                                            FAKE, 0) == STATUS["ESHAPE"]
+    # the Llama-8B layer fits
+    llama = good_shape(batch=16, num_q_heads=32, num_kv_heads=8, max_ctx=32768)
+    assert ckv.workspace_bytes(llama, 2048, ckv.ENTRY_CRITICAL_KV_ATTN) <= \
+        ckv.NOALLOC_SCRATCH_BYTES
