@@ -324,6 +324,9 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
         "score": units * n * d * 2,
         # selected K and V rows once (2 k d bf16 per unit)
         "attn": units * k * 2 * d * 2,
+        # the same rows, attended by the one-launch selection and attention
+        # (its reads of the scores are implementation bytes)
+        "select_attn": units * k * 2 * d * 2,
     }
     algo_bytes = algo.get(dominant)
     achieved = algo_bytes / avg_s / 1e9 if algo_bytes else None

@@ -467,7 +467,8 @@ typedef enum ckv_kernel_id {
   CKV_K_LANDMARKS = 10, /* chunk landmarks (mean keys)                      */
   CKV_K_EXPAND = 11,  /* selected chunks -> their rows                      */
   CKV_K_RECONSTRUCT = 12, /* low-rank key rebuild (with the misses' V fetch)  */
-  CKV_K_COUNT = 13
+  CKV_K_SELECT_ATTN = 13, /* same-step selection and attention in one launch */
+  CKV_K_COUNT = 14
 } ckv_kernel_id;
 
 #define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)

@@ -46,7 +46,7 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
            "ckv_pipeline_prime",
            "ckv_decode_step")
-KERNEL_COUNT = 13
+KERNEL_COUNT = 14
 MAX_RANK = 4096
 ABI_VERSION = 5  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
@@ -319,7 +319,7 @@ def chunked_kv_attn(shape: Shape, chunk: int, q_att, q_sel, landmarks, ctx_lens,
 
 KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
               "combine": 6, "dual": 7, "gather": 8, "miss": 9, "landmarks": 10,
-              "expand": 11, "reconstruct": 12}
+              "expand": 11, "reconstruct": 12, "select_attn": 13}
 
 
 def profile_begin(kernels=None, every: int = 1) -> None:

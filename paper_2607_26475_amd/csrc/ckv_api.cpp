@@ -382,6 +382,19 @@ int select_and_merge(SelectArgs sa, const AttnArgs& at, const Dims& d, hipStream
   return CKV_OK;
 }
 
+// Shares per unit of the same-step selection and attention in one launch
+// (0: that launch does not apply and the selection, attention and merge run
+// as three kernels).  Two shares when two workgroups per unit still fit on
+// the device's CUs (then every CU has a workgroup to attend with), more when
+// a share would exceed kSelAttnMaxShare rows.
+int select_attn_splits(const Dims& d, int32_t k, const Layout& L) {
+  if (d.max_ctx > kFusedSelectMaxCtx || d.G > 8) return 0;
+  int S = (2 * (int64_t)d.U <= device_cus() && k >= 512) ? 2 : 1;
+  while ((((k + S - 1) / S + 15) & ~15) > kSelAttnMaxShare) S *= 2;
+  if (S > kSelAttnMaxSplit || S > L.chunks) return 0;
+  return S;
+}
+
 int check_chunk(int32_t chunk, int32_t k) {
   if (chunk < 1 || chunk > (1 << 20)) return fail(CKV_ESHAPE, "chunk %d outside [1, 2^20]", chunk);
   if (k % chunk) return fail(CKV_ESHAPE, "k %d is not a multiple of chunk %d", k, chunk);
@@ -632,11 +645,18 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
     if ((rc = select_and_merge(sa, at_, d, s))) return rc;
   } else {
     CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
-    if ((rc = run_select_tail(sa, d.U, s))) return rc;
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
                              d.kv_stride, k, scale, out);
-    CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
-    CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+    if (const int S = select_attn_splits(d, k, L)) {
+      // each workgroup selects its unit's set and attends over its share
+      at_.chunks = S;
+      CKV_TRY_HIP(launch_select_attn(sa, at_, d.G, S, s), "select-attention launch");
+      if (S > 1) CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+    } else {
+      if ((rc = run_select_tail(sa, d.U, s))) return rc;
+      CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
+      CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+    }
   }
   return CKV_OK;
 }

@@ -280,3 +280,227 @@ __device__ __forceinline__ void attn_chunk(const AttnArgs& a, int unit,
 }
 
 }  // namespace ckv
+
+namespace ckv {
+
+// ---- attention by a whole selection workgroup --------------------------------
+// After a kFinishThreads workgroup has selected a unit's set, its 16 waves
+// attend over its share of it: `nrows` rows whose source positions are in
+// LDS (pos[0..nrows)), read in place from the source at row stride
+// a.row_stride.  Wave w takes a contiguous run of 16-row blocks.  Per block
+// the wave's K and V rows go through its own LDS stages, so the registers
+// they were loaded into are free at once and the next block's loads are
+// issued before the current block's arithmetic: every wave keeps a block
+// (8 KiB) in flight while holding at most 128 registers (16 waves per CU).
+// Logits and the weighted V sum are the products of attn_chunk (query rows
+// in the A placement, hi + lo bf16 weight parts); the 16 waves' states are
+// merged through LDS into the workgroup's result: the normalised output when
+// the unit has one share, else the share's partial (max, weight sum,
+// weighted V sum) for k_combine.
+template <int G>
+struct WgAttnLds {
+  static constexpr int kKStage = 16 * kStageRowDwords;  // dwords per wave: 16 padded rows
+  static constexpr int kVStage = 16 * (kD / 2);         // dwords per wave: 16 rows of 256 B
+  static constexpr int kPTab = 16 * G + G + (G < 4 ? 4 - G : 0);  // weight table floats
+  static constexpr int kPerWave = kKStage + kVStage + kPTab;
+  static constexpr int kStages = (kFinishThreads / 64) * kPerWave;  // dwords
+  static constexpr int kQ = 16 * kStageRowDwords;       // query rows in the A placement
+  static constexpr int kMerge = (kFinishThreads / 64) * G * (kD + 2);  // floats, in the stages
+  static_assert(kMerge <= kStages, "the 16 waves' states fit in the stages");
+  static_assert(kPerWave % 4 == 0, "16-byte aligned stages");
+};
+
+// Output slots [lo, hi) of share `split` of `nsplit` over a set of m
+// positions: equal runs of whole 16-row blocks.
+__host__ __device__ __forceinline__ void share_range(int m, int split, int nsplit, int* lo,
+                                                     int* hi) {
+  const int per = (((m + nsplit - 1) / nsplit) + 15) & ~15;
+  *lo = min(split * per, m);
+  *hi = min(*lo + per, m);
+}
+
+// All kFinishThreads threads call this.  stages: WgAttnLds<G>::kStages
+// dwords, qlds: kQ dwords (both free on entry); pos: the share's positions.
+template <int G>
+__device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, const int32_t* pos,
+                                        int nrows, int split, int nsplit, uint32_t* stages,
+                                        uint32_t* qlds) {
+  using Lds = WgAttnLds<G>;
+  static_assert(G <= 8, "16 waves' states of at most 8 heads fit in the stages");
+  constexpr int kW = kFinishThreads / 64;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int lrow = lane >> 4, lchunk = lane & 15;
+  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+  const int nblk = (nrows + 15) >> 4;
+  const int blk0 = (wave * nblk) / kW, blk1 = ((wave + 1) * nblk) / kW;
+  uint32_t* kst = stages + wave * Lds::kPerWave;
+  uint32_t* vst = kst + Lds::kKStage;
+  float* ptab = reinterpret_cast<float*>(vst + Lds::kVStage);
+  const int64_t stride = a.row_stride;
+  const int64_t ubase = (int64_t)unit * a.max_ctx * stride + 8 * lchunk;
+
+  // the query rows first: their loads queue ahead of the first block's
+  uint4 qv_ld = make_uint4(0u, 0u, 0u, 0u);
+  const int qr = tid >> 4, qc = tid & 15;  // threads 0..255: row qr, 16-byte chunk qc
+  if (tid < 16 * 16 && qr < G)
+    qv_ld = ld16(a.q + ((int64_t)b * a.Hq + (int64_t)h * G + qr) * kD + 8 * qc);
+  // rows of block blk, clamped to the share (rows past nrows are masked)
+  auto load_block = [&](int blk, uint4* kr, uint4* vr) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int i = min(16 * blk + 4 * it + lrow, nrows - 1);
+      int p = pos[i];
+      p = p < 0 ? 0 : (p >= a.max_ctx ? a.max_ctx - 1 : p);
+      const int64_t off = ubase + (int64_t)p * stride;
+      kr[it] = ld16(a.k_rows + off);
+      vr[it] = ld16(a.v_rows + off);
+    }
+  };
+  uint4 kr[4], vr[4];
+  if (blk0 < blk1) load_block(blk0, kr, vr);
+  if (tid < 16 * 16) *reinterpret_cast<uint4*>(qlds + qr * kStageRowDwords + 4 * qc) = qv_ld;
+  lds_barrier();  // the query rows are in LDS; the first block may still be in flight
+
+  float m_i[4], l_i[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    m_i[i] = -INFINITY;
+    l_i[i] = 0.f;
+  }
+  f32x4 oacc[8];  // oacc[e][j] = O[head 4*kg + j][8*r16 + e]
+#pragma unroll
+  for (int e = 0; e < 8; ++e) oacc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int blk = blk0; blk < blk1; ++blk) {  // bounds uniform over the wave
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      *reinterpret_cast<uint4*>(kst + (4 * it + lrow) * kStageRowDwords + 4 * lchunk) = kr[it];
+      *reinterpret_cast<uint4*>(vst + (4 * it + lrow) * (kD / 2) + 4 * lchunk) = vr[it];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if (blk + 1 < blk1) load_block(blk + 1, kr, vr);
+    __builtin_amdgcn_sched_barrier(0);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const uint4 kv = *reinterpret_cast<const uint4*>(kst + r16 * kStageRowDwords + 4 * (4 * t + kg));
+      const uint4 qv = *reinterpret_cast<const uint4*>(qlds + r16 * kStageRowDwords + 4 * (4 * t + kg));
+      acc = mfma_16x16x32(as_bf16x8(qv), as_bf16x8(kv), acc);
+    }
+    const bool valid = 16 * blk + r16 < nrows;
+    float p[4], al[4];
+    bool moved = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float lg = (4 * kg + i < G && valid) ? acc[i] * a.scale : -INFINITY;
+      const float mn = fmaxf(m_i[i], row16_max(lg));
+      moved |= mn != m_i[i];
+      al[i] = m_i[i] == -INFINITY ? 0.f : __expf(m_i[i] - mn);
+      p[i] = lg == -INFINITY ? 0.f : __expf(lg - mn);
+      l_i[i] = l_i[i] * al[i] + row16_sum(p[i]);
+      m_i[i] = mn;
+    }
+    if (4 * kg < G) {
+      if (G >= 4) {
+        *reinterpret_cast<float4*>(ptab + r16 * G + 4 * kg) = make_float4(p[0], p[1], p[2], p[3]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < G; ++i) ptab[r16 * G + i] = p[i];
+      }
+    }
+    const bool rescale = __any(moved);
+    __builtin_amdgcn_wave_barrier();
+    if (rescale) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) oacc[e][j] *= al[j];
+    }
+    uint4 aw;
+    {
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float pv = r16 < G ? ptab[(4 * i + lrow) * G + r16] : 0.f;
+        const uint32_t hi = bf16_rne_bits(pv);
+        const uint32_t lo = bf16_rne_bits(pv - __uint_as_float(hi << 16));
+        w[i] = hi | (lo << 16);
+      }
+      aw = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    // this lane's own V rows back from the stage: channels [8*lchunk, +8) of
+    // rows lrow + 4i, the B operand of product e up to duplication
+    uint4 vv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      vv[i] = *reinterpret_cast<const uint4*>(vst + (4 * i + lrow) * (kD / 2) + 4 * lchunk);
+    const uint32_t* vw = reinterpret_cast<const uint32_t*>(vv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t bb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t x = vw[4 * i + (e >> 1)];
+        bb[i] = (e & 1) ? ((x >> 16) | (x & 0xffff0000u)) : ((x & 0xffffu) | (x << 16));
+      }
+      oacc[e] = mfma_16x16x32(as_bf16x8(aw), as_bf16x8(make_uint4(bb[0], bb[1], bb[2], bb[3])),
+                              oacc[e]);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // merge the 16 waves (their stages are free once every wave is here)
+  __syncthreads();
+  float* merge = reinterpret_cast<float*>(stages);
+  float* mw = merge + wave * G * (kD + 2);
+  if (4 * kg < G) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int g = 4 * kg + j;
+      if (g < G) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mw[g * (kD + 2) + 8 * r16 + e] = oacc[e][j];
+      }
+    }
+  }
+  if (lchunk == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = 4 * lrow + i;
+      if (g < G) {
+        mw[g * (kD + 2) + kD] = m_i[i];
+        mw[g * (kD + 2) + kD + 1] = l_i[i];
+      }
+    }
+  }
+  __syncthreads();
+  for (int oi = tid; oi < G * kD; oi += kFinishThreads) {
+    const int g = oi / kD, c = oi - g * kD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) M = fmaxf(M, merge[(w * G + g) * (kD + 2) + kD]);
+    float O = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) {
+      const float* mg = merge + (w * G + g) * (kD + 2);
+      const float wt = mg[kD] == -INFINITY ? 0.f : __expf(mg[kD] - M);
+      O = fmaf(wt, mg[c], O);
+      L = fmaf(wt, mg[kD + 1], L);
+    }
+    if (nsplit == 1) {
+      a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = L > 0.f ? O / L : 0.f;
+    } else {
+      float* part = a.part + (((int64_t)unit * nsplit + split) * G + g) * kPartStride;
+      part[4 + c] = O;
+      if (c == 0) {
+        part[0] = M;
+        part[1] = L;
+      }
+    }
+  }
+}
+
+}  // namespace ckv

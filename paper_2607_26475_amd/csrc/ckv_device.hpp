@@ -55,6 +55,12 @@ constexpr int kAttnRows = 4 * kWaveRows;
 constexpr int kPartStride = 132;   // floats per (chunk, head): m, l, pad, pad, o[128]
 constexpr int kMergeChunks = 8;    // partials per unit the fused selection merges
 
+// Selection and attention in one launch (same-step decode): a share of at
+// most kSelAttnMaxShare selected rows per workgroup, at most kSelAttnMaxSplit
+// shares per unit, group sizes up to 8.
+constexpr int kSelAttnMaxShare = 2048;
+constexpr int kSelAttnMaxSplit = 8;
+
 // Gather: one thread moves 16 bytes per item; items are (unit, slot, K|V, part).
 constexpr int kGatherThreads = 256;
 constexpr int kGatherUnroll = 4;

@@ -9,6 +9,8 @@
 
 namespace ckv {
 
+constexpr int kMaxDevices = 256;  // devices the per-device host tables serve
+
 // ---- workspace clearing (a kernel, not hipMemsetAsync: safe to capture) ----
 __global__ __launch_bounds__(256) void k_zero(uint4* p, int64_t n16) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -113,13 +115,16 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
   }
 }
 
-// Writes set bits of bm[0, words) as ascending positions to out[0, limit),
-// 16 waves each owning a contiguous word range (reads are lane-consecutive),
-// and returns the number of set bits.  The bitmap holds exactly m <= limit
-// bits for scores as specified; the limit only keeps other input (NaN
-// scores) inside the row.
+// Writes set bits of bm[0, words) as ascending positions to out[0, limit)
+// (when out is not null), 16 waves each owning a contiguous word range (reads
+// are lane-consecutive), and returns the number of set bits.  Output slots
+// [lo, hi) also go to share[slot - lo] when share is not null.  The bitmap
+// holds exactly m <= limit bits for scores as specified; the limit only keeps
+// other input (NaN scores) inside the row.
 __device__ __forceinline__ uint32_t emit_bitmap(const uint32_t* bm, int words, int32_t* out,
-                                                uint32_t limit, uint32_t* tmp) {
+                                                uint32_t limit, uint32_t* tmp,
+                                                int32_t* share = nullptr, uint32_t lo = 0,
+                                                uint32_t hi = 0) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr int kW = kFinishThreads / 64;
   const int per = (((words + kW - 1) / kW) + 63) & ~63;
@@ -143,7 +148,10 @@ __device__ __forceinline__ uint32_t emit_bitmap(const uint32_t* bm, int words, i
     uint32_t o = base + incl - c;
     while (bits) {
       const int bit = __ffs(bits) - 1;
-      if (o < limit) out[o] = w * 32 + bit;
+      if (o < limit) {
+        if (out) out[o] = w * 32 + bit;
+        if (share && o >= lo && o < hi) share[o - lo] = w * 32 + bit;
+      }
       ++o;
       bits &= bits - 1u;
     }
@@ -433,14 +441,34 @@ __device__ __forceinline__ void merge_partials(const SelectArgs& a, int unit, ui
   }
 }
 
-__global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
-  __shared__ uint2 cand[kCandLds];
-  __shared__ uint32_t bm[kFusedSelectMaxCtx / 32];
-  __shared__ uint32_t lhist[2048];
-  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
-  __shared__ uint32_t misc[8];
-  const int unit = blockIdx.x;
+// LDS of a one-workgroup selection (see select_unit).
+struct SelLds {
+  uint2* cand;      // [kCandLds]
+  uint32_t* bm;     // [kFusedSelectMaxCtx / 32]
+  uint32_t* lhist;  // [2048]
+  uint32_t* tmp;    // [kFinishThreads / 64 + 1]
+  uint32_t* misc;   // [8]
+};
+
+// The whole selection of one unit by one kFinishThreads workgroup, for
+// n_b <= kFusedSelectMaxCtx.  The unit's scores are read once, kSelPer per
+// thread per batch of kSelBatch positions, all loads of a batch in flight
+// together.  Positions above the first-digit bin go straight into an LDS
+// bitmap (one ballot per 64 positions, no atomics); positions inside the bin
+// become candidates (fp32 bits, position), whose slots are reserved with one
+// atomic per wave.  The threshold inside the bin is then resolved exactly,
+// the chosen candidates marked, and the bitmap written out in ascending
+// order: to idx/n_sel when `write`, and output slots [lo, hi) to share[slot -
+// lo] when share is not null.  Returns the number of positions selected.
+__device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const SelLds& L,
+                                           bool write, int32_t* share, uint32_t lo,
+                                           uint32_t hi) {
   const int tid = threadIdx.x;
+  uint2* const cand = L.cand;
+  uint32_t* const bm = L.bm;
+  uint32_t* const lhist = L.lhist;
+  uint32_t* const tmp = L.tmp;
+  uint32_t* const misc = L.misc;
   // Every read the workgroup needs first is issued before anything waits:
   // the histogram, and the first batch of scores (clamped to the row, not
   // to n_b, which is not known yet; positions at or past n_b are masked).
@@ -452,10 +480,10 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   if (a.hist_part) {
     const int64_t gu = (a.max_ctx + kStageRows - 1) / kStageRows;
     const int64_t T = gu * a.units, g0 = (int64_t)unit * gu;
-    const int64_t lo = range_owner(g0, T, a.score_nwg);
-    const int64_t hi = range_owner(g0 + gu - 1, T, a.score_nwg);
-    slots = a.hist_part + (unit + lo) * kHistBins;
-    nslots = (int)min<int64_t>(hi - lo + 1, kMaxPartials);  // the host keeps it below
+    const int64_t lo_wg = range_owner(g0, T, a.score_nwg);
+    const int64_t hi_wg = range_owner(g0 + gu - 1, T, a.score_nwg);
+    slots = a.hist_part + (unit + lo_wg) * kHistBins;
+    nslots = (int)min<int64_t>(hi_wg - lo_wg + 1, kMaxPartials);  // the host keeps it below
   }
   const int len_b = a.ctx_lens[unit / a.Hkv];
   uint2 hv[kMaxPartials];
@@ -471,56 +499,130 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   const int n = unit_len(len_b, a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   int32_t* idx = a.idx + (int64_t)unit * a.k;
-  do {  // one exit, so that the merge below appears once
-    if (m >= n) {  // uniform; every position (possibly none) is selected
-      for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
-      if (tid == 0) a.n_sel[unit] = m;
-      break;
+  if (m >= n) {  // uniform; every position (possibly none) is selected
+    for (int i = tid; i < a.k; i += kFinishThreads) {
+      if (write) idx[i] = i < n ? i : -1;
+      if (share && i < n && (uint32_t)i >= lo && (uint32_t)i < hi) share[i - lo] = i;
     }
-    store_hist_sum(hv, nslots, lhist);
-    if (tid == 64) misc[7] = 0u;
-    // the scores may still be in flight across both barriers
-    lds_barrier();
-    if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
-    lds_barrier();
-    const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
-    const uint32_t b1 = misc[4], above = misc[5];
-    const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
-    const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
-    // the last, partial batch holds NaN past n_b
-    auto pad = [&](float (&sv)[kSelPer], int j0) {
-      if (j0 + kSelBatch > n) {
+    if (write && tid == 0) a.n_sel[unit] = m;
+    return m;
+  }
+  store_hist_sum(hv, nslots, lhist);
+  if (tid == 64) misc[7] = 0u;
+  // the scores may still be in flight across both barriers
+  lds_barrier();
+  if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
+  lds_barrier();
+  const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
+  const uint32_t b1 = misc[4], above = misc[5];
+  const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
+  const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
+  // the last, partial batch holds NaN past n_b
+  auto pad = [&](float (&sv)[kSelPer], int j0) {
+    if (j0 + kSelBatch > n) {
 #pragma unroll
-        for (int u = 0; u < kSelPer; ++u)
-          if (j0 + u * kFinishThreads + tid >= n) sv[u] = __builtin_nanf("");
-      }
-    };
-    // the first batch apart, so that its compares start as its loads land
-    pad(sv0, 0);
-    classify_batch(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
-    for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {
-      float sv[kSelPer];
-      load_score_batch(srow, j0, n, sv);
-      pad(sv, j0);
-      classify_batch(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
+      for (int u = 0; u < kSelPer; ++u)
+        if (j0 + u * kFinishThreads + tid >= n) sv[u] = __builtin_nanf("");
     }
-    __syncthreads();
-    const uint32_t nc = misc[7];
-    const uint32_t need = (uint32_t)m - above;
-    const KeyedCands kc{cs};
-    uint32_t pmax;
-    const uint32_t T = refine_threshold(kc, nc, need, b1, lhist, tmp, misc, &pmax);
-    for (uint32_t i = tid; i < nc; i += kFinishThreads) {
-      const uint2 c = kc[i];
-      if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
-    }
-    __syncthreads();
-    // m positions for scores as specified (fewer only with NaN scores)
-    const int got = (int)min(emit_bitmap(bm, (n + 31) >> 5, idx, (uint32_t)a.k, tmp), (uint32_t)m);
+  };
+  // the first batch apart, so that its compares start as its loads land
+  pad(sv0, 0);
+  classify_batch(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
+  for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {
+    float sv[kSelPer];
+    load_score_batch(srow, j0, n, sv);
+    pad(sv, j0);
+    classify_batch(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
+  }
+  __syncthreads();
+  const uint32_t nc = misc[7];
+  const uint32_t need = (uint32_t)m - above;
+  const KeyedCands kc{cs};
+  uint32_t pmax;
+  const uint32_t T = refine_threshold(kc, nc, need, b1, lhist, tmp, misc, &pmax);
+  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+    const uint2 c = kc[i];
+    if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
+  }
+  __syncthreads();
+  // m positions for scores as specified (fewer only with NaN scores)
+  const int got = (int)min(emit_bitmap(bm, (n + 31) >> 5, write ? idx : nullptr,
+                                       (uint32_t)a.k, tmp, share, lo, hi),
+                           (uint32_t)m);
+  if (write) {
     for (int i = got + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
     if (tid == 0) a.n_sel[unit] = got;
-  } while (0);
+  }
+  return got;
+}
+
+__global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
+  __shared__ uint2 cand[kCandLds];
+  __shared__ uint32_t bm[kFusedSelectMaxCtx / 32];
+  __shared__ uint32_t lhist[2048];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  const int unit = blockIdx.x;
+  select_unit(a, unit, SelLds{cand, bm, lhist, tmp, misc}, true, nullptr, 0, 0);
+  // one call site, so that the merge appears once (a second inlined copy
+  // kept more of the selection's registers live)
   if (a.mpart) merge_partials(a, unit, lhist);
+}
+
+// ---- selection and attention in one launch ------------------------------------
+// Same-step decode with a set of at most kSelAttnMaxShare rows per share:
+// each workgroup selects its unit's set (select_unit; share 0 writes idx and
+// n_sel), keeps the positions of its share in LDS and attends over them with
+// all 16 waves (attn_wg).  A unit has nsplit shares, each selected in full by
+// its own workgroup, so that the attention has a workgroup on every CU.  The
+// LDS is a union: the selection's candidates, bitmap and histogram, then the
+// attention's stages and query rows; the share's positions lie past the
+// selection's area, since they are written while its bitmap is emitted.
+template <int G>
+struct SelAttnLds {
+  static constexpr int kSel = 2 * kCandLds + kFusedSelectMaxCtx / 32 + 2048;  // dwords
+  static constexpr int kQOff = WgAttnLds<G>::kStages;
+  static constexpr int kPosOff =
+      kSel > kQOff + WgAttnLds<G>::kQ ? kSel : kQOff + WgAttnLds<G>::kQ;
+  static constexpr int kDwords = kPosOff + kSelAttnMaxShare;
+};
+
+// Workgroup -> (unit, share).  Workgroups are spread over the XCDs round-robin
+// by index, so the shares of unit u take indices 8*S*(u/8) + 8*s + u%8: all
+// on the XCD of u % 8, where the second read of the unit's scores can hit
+// the L2.  Indices past the last unit have no work.
+__device__ __forceinline__ void split_block(int blk, int nsplit, int* unit, int* split) {
+  if (nsplit == 1) {
+    *unit = blk;
+    *split = 0;
+    return;
+  }
+  const int grp = blk / (8 * nsplit), r = blk - grp * 8 * nsplit;
+  *split = r >> 3;
+  *unit = grp * 8 + (r & 7);
+}
+
+template <int G>
+__global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, AttnArgs at,
+                                                                  int nsplit) {
+  using Lds = SelAttnLds<G>;
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Lds::kDwords];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  int unit, split;
+  split_block(blockIdx.x, nsplit, &unit, &split);
+  if (unit >= sa.units) return;  // uniform over the workgroup
+  const SelLds L{reinterpret_cast<uint2*>(lds), lds + 2 * kCandLds,
+                 lds + 2 * kCandLds + kFusedSelectMaxCtx / 32, tmp, misc};
+  int32_t* share = reinterpret_cast<int32_t*>(lds + Lds::kPosOff);
+  // the share of a set of m positions is known before the set is: m =
+  // min(k, n_b), and the split is by m
+  const int n = unit_len(sa.ctx_lens[unit / sa.Hkv], sa.max_ctx, sa.chunk);
+  int lo, hi;
+  share_range(min(sa.k, n), split, nsplit, &lo, &hi);
+  select_unit(sa, unit, L, split == 0, share, (uint32_t)lo, (uint32_t)hi);
+  __syncthreads();
+  attn_wg<G>(at, unit, share, hi - lo, split, nsplit, lds, lds + Lds::kQOff);
 }
 
 // ---- attention -------------------------------------------------------------
@@ -927,8 +1029,6 @@ __global__ __launch_bounds__(kGatherThreads) void k_miss_fill(GatherArgs g, Reco
 // passed to kernels.
 static __device__ __align__(256) uint8_t scratch[CKV_NOALLOC_SCRATCH_BYTES];
 
-constexpr int kMaxDevices = 256;
-
 int noalloc_scratch(void** ptr) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
@@ -996,6 +1096,22 @@ static int resident_blocks(const void* fn) {
   std::lock_guard<std::mutex> lk(mu);
   if (used < kEntries) table[used++] = Entry{fn, dev, cus * per_cu};
   return cus * per_cu;
+}
+
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  static std::mutex mu;
+  static int cus[kMaxDevices] = {};
+  std::lock_guard<std::mutex> lk(mu);
+  if (!cus[dev]) {
+    int c = 0;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c < 1)
+      c = 256;
+    cus[dev] = c;
+  }
+  return cus[dev];
 }
 
 template <int G>
@@ -1126,6 +1242,21 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
   const int attn_blocks = units * at.chunks;
   return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, nwg, s)
                  : launch_dual_i<false>(at, sc, G, attn_blocks, nwg, s);
+}
+
+hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
+                              hipStream_t s) {
+  if (nsplit < 1 || nsplit > kSelAttnMaxSplit) return hipErrorInvalidValue;
+  const int blocks = nsplit == 1 ? sa.units : (sa.units + 7) / 8 * 8 * nsplit;
+  const dim3 grid(blocks), block(kFinishThreads);
+  switch (G) {
+    case 1: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<1>, grid, block, s, sa, at, nsplit); break;
+    case 2: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<2>, grid, block, s, sa, at, nsplit); break;
+    case 4: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<4>, grid, block, s, sa, at, nsplit); break;
+    case 8: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<8>, grid, block, s, sa, at, nsplit); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s) {

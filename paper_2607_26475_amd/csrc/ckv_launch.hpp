@@ -27,6 +27,10 @@ hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_select_fused(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s);
+// same-step selection and attention in one launch, nsplit shares per unit
+// (partials [U][nsplit][G] for k_combine when nsplit > 1)
+hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
+                              hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
                        int units, int nwg, hipStream_t s);
@@ -38,6 +42,9 @@ hipError_t launch_reconstruct(const ReconArgs& a, hipStream_t s);
 hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconArgs& r,
                             hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s);
+
+// Compute units of the current device (queried once per device).
+int device_cus();
 
 // Device address of the current device's fixed scratch array
 // (CKV_NOALLOC_SCRATCH_BYTES), asked of the runtime on the first call per

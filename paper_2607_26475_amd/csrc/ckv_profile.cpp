@@ -68,7 +68,8 @@ extern "C" {
 const char* ckv_kernel_name(int id) {
   static const char* names[CKV_K_COUNT] = {"zero", "score", "hist", "filter", "finish",
                                            "attn", "combine", "dual", "gather", "miss",
-                                           "landmarks", "expand", "reconstruct"};
+                                           "landmarks", "expand", "reconstruct",
+                                           "select_attn"};
   return (id >= 0 && id < CKV_K_COUNT) ? names[id] : "";
 }
 
