@@ -93,7 +93,8 @@ typedef enum ckv_entry {
   CKV_ENTRY_SPARSE_DECODE_ATTN = 2,
   CKV_ENTRY_CRITICAL_KV_ATTN = 3,
   CKV_ENTRY_CORRECTED_ATTN = 4,
-  CKV_ENTRY_DUAL_TOKEN_ATTN = 5
+  CKV_ENTRY_DUAL_TOKEN_ATTN = 5,
+  CKV_ENTRY_DECODE_STEP = 6  /* ckv_decode_step with any kind of layer */
 } ckv_entry;
 
 typedef struct ckv_shape {
@@ -384,6 +385,19 @@ typedef struct ckv_layer {
   int32_t lr_rank;            /* > 0 (with idx_true set): misses' keys rebuilt  */
   const uint16_t* lr_u;       /* from these factors, ckv_corrected_attn_lowrank */
   const uint16_t* lr_w;       /* (u_fac, w_fac); 0/NULL otherwise               */
+  int32_t chunk;              /* > 1: a chunked layer (Sec. 2.2 chunk landmarks) */
+  const uint16_t* landmarks;  /* as ckv_chunk_landmarks writes them, [B][Hkv]    */
+                              /* [ceil(max_ctx/chunk)][d]: its selection scores */
+                              /* these with q_sel, keeps the k/chunk best chunks */
+                              /* and expands them to rows (ckv_select_chunks):  */
+                              /* idx_prev/idx_next hold rows; k_score unused.   */
+                              /* 0/1 and NULL: one score per position           */
+  const uint16_t* k_local;    /* non-NULL out_spec: two tokens (Sec. 5.2): the  */
+  const uint16_t* v_local;    /* current and the speculative token attend in   */
+  float* out_spec;            /* one launch, as ckv_dual_token_attn, with their */
+                              /* own rows k_local/v_local [B][Hkv][2][d]; the   */
+                              /* speculative token's query is q_sel and its     */
+                              /* output goes to out_spec [B][Hq][d] (G <= 8)    */
 } ckv_layer;
 
 typedef struct ckv_pipeline ckv_pipeline; /* events of one decode loop */
@@ -402,6 +416,22 @@ int ckv_pipeline_destroy(ckv_pipeline* pipe);
  * ckv_gather_kv uses (256 for pinned sources).  0 <= workgroups <= 4096,
  * else CKV_EINVAL. */
 int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups);
+
+/* For tests of the event protocol only, never for serving: breaks the
+ * loop's ordering on purpose, so that a test can show that it would see a
+ * missing wait.  CKV_PIPE_CHECK_NO_FILL_WAIT: the compute stream does not
+ * wait for a buffer's fill before attending over it (read-after-write);
+ * CKV_PIPE_CHECK_NO_RELEASE_WAIT: the copy stream does not wait for a
+ * buffer's release before refilling it (write-after-read);
+ * CKV_PIPE_CHECK_POISON: the copy stream overwrites a released buffer with
+ * NaN bits before refilling it.  Every access stays inside the buffers; a
+ * missing wait only makes an attention read rows of another layer or
+ * poison.  0 (the default) restores the normal loop; unknown bits are
+ * CKV_EINVAL. */
+#define CKV_PIPE_CHECK_NO_FILL_WAIT 1u
+#define CKV_PIPE_CHECK_NO_RELEASE_WAIT 2u
+#define CKV_PIPE_CHECK_POISON 4u
+int ckv_pipeline_set_checks(ckv_pipeline* pipe, unsigned flags);
 
 /* Starts a decode loop: gathers layer 0 (into buffer 0) and layer 1 (into
  * buffer 1) from their idx_prev/n_sel_prev on copy_stream.  Buffers are
@@ -429,7 +459,12 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
  * step's layers 0 and 1 from this step's idx_next.  Before the next step the
  * caller swaps idx_prev and idx_next.  ws is the workspace of
  * CKV_ENTRY_CRITICAL_KV_ATTN, or of CKV_ENTRY_CORRECTED_ATTN if any layer
- * has idx_true set, used on the compute stream only.
+ * has idx_true set, or of CKV_ENTRY_DECODE_STEP (which serves every layer
+ * kind) if any layer is chunked or has two tokens; it is used on the compute
+ * stream only.  A chunked or two-token layer runs the same pipelined step
+ * (one launch attends over the previous set and scores for the next one) with
+ * its selection over chunk landmarks or its second token; such a layer with
+ * idx_true set is CKV_EINVAL.
  *
  * Steps can be captured into a HIP graph on compute_stream (whole steps: the
  * copy stream joins the capture at its first wait and the caller joins it

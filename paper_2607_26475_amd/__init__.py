@@ -26,14 +26,15 @@ __all__ = [
     "MAX_RANK", "ABI_VERSION", "profile_begin", "profile_end", "abi_version",
     "Layer", "layer_array", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
-    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "EXPORTS",
+    "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "ENTRY_DECODE_STEP",
+    "EXPORTS",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
 
 SRC_DEVICE, SRC_HOST_PINNED = 0, 1
 ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
-ENTRY_CORRECTED_ATTN, ENTRY_DUAL_TOKEN_ATTN = 4, 5
+ENTRY_CORRECTED_ATTN, ENTRY_DUAL_TOKEN_ATTN, ENTRY_DECODE_STEP = 4, 5, 6
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
@@ -44,6 +45,7 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_kernel_name", "ckv_profile_begin", "ckv_profile_begin_sampled",
            "ckv_profile_end",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
+           "ckv_pipeline_set_checks",
            "ckv_pipeline_prime",
            "ckv_decode_step")
 KERNEL_COUNT = 14
@@ -68,7 +70,10 @@ class Layer(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "q_att", "q_sel", "k_score", "k_src", "v_src", "idx_prev", "n_sel_prev",
         "idx_next", "n_sel_next", "out", "idx_true", "n_true", "hits")] + [
-        ("lr_rank", ctypes.c_int32), ("lr_u", ctypes.c_void_p), ("lr_w", ctypes.c_void_p)]
+        ("lr_rank", ctypes.c_int32), ("lr_u", ctypes.c_void_p), ("lr_w", ctypes.c_void_p),
+        ("chunk", ctypes.c_int32), ("landmarks", ctypes.c_void_p),
+        ("k_local", ctypes.c_void_p), ("v_local", ctypes.c_void_p),
+        ("out_spec", ctypes.c_void_p)]
 
 
 class Shape(ctypes.Structure):
@@ -126,6 +131,7 @@ def _load() -> ctypes.CDLL:
         "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
         "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
         "ckv_pipeline_set_gather_width": (ctypes.c_int, [vp, ctypes.c_int]),
+        "ckv_pipeline_set_checks": (ctypes.c_int, [vp, ctypes.c_uint]),
         "ckv_pipeline_prime": (ctypes.c_int, [vp, sp, i32, ctypes.POINTER(Layer), ctypes.c_int,
                                               ctypes.c_int, ctypes.POINTER(vp),
                                               ctypes.POINTER(vp), vp]),
@@ -379,6 +385,13 @@ class Pipeline:
             self.close()
         except Exception:
             pass
+
+    CHECK_NO_FILL_WAIT, CHECK_NO_RELEASE_WAIT, CHECK_POISON = 1, 2, 4
+
+    def set_checks(self, flags: int) -> None:
+        """Tests of the event protocol only: skip the fill or release waits,
+        or poison released buffers (see ckv_pipeline_set_checks)."""
+        _check("ckv_pipeline_set_checks", _lib.ckv_pipeline_set_checks(self._h, flags))
 
     def set_gather_width(self, workgroups: int) -> None:
         _check("ckv_pipeline_set_gather_width",

@@ -117,6 +117,7 @@ struct Layout {
   size_t hist = 0, coarse = 0, ctrl = 0, hist2 = 0, coarse2 = 0, ctrl2 = 0, zero_end = 0;
   size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0, hist_part = 0, hist_part_bytes = 0;
   size_t slot_of = 0, miss_pos = 0, miss_slot = 0, n_miss = 0, free_slot = 0, total = 0;
+  size_t chunk_idx = 0, n_chunks = 0;  // decode step: selected chunks of a chunked layer
   int64_t bm_words = 0;
   int chunks = 0, filter_tiles = 0;
 };
@@ -127,10 +128,13 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
   size_t off = 0;
   L.filter_tiles = (d.max_ctx + kFilterTile - 1) / kFilterTile;
   L.chunks = (k + kAttnRows - 1) / kAttnRows;
-  const bool corrected = entry == CKV_ENTRY_CORRECTED_ATTN;
+  // the decode step's workspace serves every layer kind: corrected layers,
+  // two-token layers (2G head rows of partials) and chunked layers (chunk lists)
+  const bool step = entry == CKV_ENTRY_DECODE_STEP;
+  const bool corrected = entry == CKV_ENTRY_CORRECTED_ATTN || step;
   const bool select = entry == CKV_ENTRY_SELECT_TOPK || entry == CKV_ENTRY_CRITICAL_KV_ATTN ||
                       corrected;
-  const bool two_tokens = entry == CKV_ENTRY_DUAL_TOKEN_ATTN;
+  const bool two_tokens = entry == CKV_ENTRY_DUAL_TOKEN_ATTN || step;
   const bool attn = entry == CKV_ENTRY_SPARSE_DECODE_ATTN ||
                     entry == CKV_ENTRY_CRITICAL_KV_ATTN || corrected || two_tokens;
   if (select) {
@@ -187,6 +191,12 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
       L.free_slot = off;
       off += list;
     }
+  }
+  if (step) {
+    L.chunk_idx = off;
+    off += align256(U * (size_t)k * 4);
+    L.n_chunks = off;
+    off += align256(U * 4);
   }
   L.total = off;
   return L;
@@ -445,6 +455,118 @@ int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
 
 }  // namespace
 
+int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
+                         const int32_t* ctx_lens, int32_t k, float scale, void* ws,
+                         size_t ws_bytes, void* stream) {
+  Dims d;
+  int rc = check_shape(shape, &d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if ((rc = check_scale(scale))) return rc;
+  const uint16_t* q_att = p.q_att;
+  const uint16_t* q_sel = p.q_sel ? p.q_sel : p.q_att;
+  CKV_PTR(q_att);
+  CKV_PTR(q_sel);
+  CKV_PTR(ctx_lens);
+  CKV_PTR(p.idx_out);
+  CKV_PTR(p.n_sel_out);
+  CKV_PTR(p.out);
+  const bool chunked = p.chunk > 1;
+  const uint16_t* keys = chunked ? p.landmarks : p.k_score;
+  if (chunked) {
+    if ((rc = check_chunk(p.chunk, k))) return rc;
+    CKV_PTR(p.landmarks);
+  } else {
+    if (p.chunk < 0) return fail(CKV_ESHAPE, "chunk %d", p.chunk);
+    CKV_PTR(p.k_score);
+  }
+  const bool two = p.out_spec != nullptr;
+  if (two) {
+    if (d.G > 8)
+      return fail(CKV_EUNSUPPORTED, "two tokens need 2G <= 16 head rows (G = %d)", d.G);
+    CKV_PTR(p.k_local);
+    CKV_PTR(p.v_local);
+    CKV_PTR(p.out_spec);
+  }
+  const bool assembled = p.k_buf != nullptr, in_place = p.idx_in != nullptr;
+  if (assembled == in_place)
+    return fail(CKV_EINVAL, "exactly one of the assembled buffer and idx_in");
+  const uint16_t *k_src = p.k_src, *v_src = p.v_src;
+  CKV_PTR(p.n_sel_in);
+  if (assembled) {
+    CKV_PTR(p.k_buf);
+    CKV_PTR(p.v_buf);
+  } else {
+    CKV_PTR(k_src);
+    CKV_PTR(v_src);
+    if ((rc = resolve_src(p.src_kind, &k_src, &v_src))) return rc;
+  }
+  const Layout L = make_layout(d, k, CKV_ENTRY_DECODE_STEP);
+  if ((rc = check_grid(d, L))) return rc;
+  if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  if (d.U == 0) return CKV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  // the selection problem: positions, or chunks (one landmark per chunk rows,
+  // budget k / chunk), whose regions lie below the attention partials
+  Dims ds = d;
+  int32_t ks = k;
+  Layout Ls = L;
+  if (chunked) {
+    ds.max_ctx = (d.max_ctx + p.chunk - 1) / p.chunk;
+    ds.key_stride = kD;
+    ks = k / p.chunk;
+    Ls = make_layout(ds, ks, CKV_ENTRY_CRITICAL_KV_ATTN);
+    if ((rc = check_grid(ds, Ls))) return rc;
+    if (Ls.part > L.part) return fail(CKV_EWORKSPACE, "chunk selection layout overlaps");
+  }
+  int32_t* sidx = chunked ? at<int32_t>(ws, L.chunk_idx) : p.idx_out;
+  int32_t* sn = chunked ? at<int32_t>(ws, L.n_chunks) : p.n_sel_out;
+  float* scores = at<float>(ws, Ls.scores);
+  SelectArgs sa = select_args(ds, Ls, ws, scores, ctx_lens, ks, sidx, sn);
+  sa.chunk = chunked ? p.chunk : 1;
+  ScoreArgs sc = score_args(ds, Ls, q_sel, keys, ctx_lens, scale, scores, sa.hist, sa.coarse);
+  sc.chunk = sa.chunk;
+  AttnArgs at_ = assembled ? attn_args(d, L, ws, q_att, p.k_buf, p.v_buf, nullptr, p.n_sel_in,
+                                       kD, k, scale, p.out)
+                           : attn_args(d, L, ws, q_att, k_src, v_src, p.idx_in, p.n_sel_in,
+                                       d.kv_stride, k, scale, p.out);
+  if (two) {  // the speculative token attends too: its query is the selecting one
+    at_.q2 = q_sel;
+    at_.out2 = p.out_spec;
+    at_.k_local = p.k_local;
+    at_.v_local = p.v_local;
+  }
+  const ScoreKind kind = two ? (in_place ? ScoreKind::kDual2Indexed : ScoreKind::kDual2)
+                             : (in_place ? ScoreKind::kDualIndexed : ScoreKind::kDual);
+  const int nwg = score_blocks(sc, d.G, kind);
+  if (use_partials(ds, Ls, nwg))
+    set_partials(ws, Ls, nwg, &sc, &sa);
+  else
+    CKV_TRY_HIP(launch_zero(ws, Ls.zero_end, s), "zero launch");
+  CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
+  if (two) {
+    if ((rc = run_select_tail(sa, d.U, s))) return rc;
+    CKV_TRY_HIP(launch_combine(at_, 2 * d.G, d.U, s), "combine launch");
+  } else if ((rc = select_and_merge(sa, at_, d, s))) {
+    return rc;
+  }
+  if (chunked) {
+    ExpandArgs e;
+    e.chunk_idx = sidx;
+    e.n_chunks = sn;
+    e.ctx_lens = ctx_lens;
+    e.rows = p.idx_out;
+    e.n_rows = p.n_sel_out;
+    e.Hkv = d.Hkv;
+    e.max_ctx = d.max_ctx;
+    e.chunk = p.chunk;
+    e.kc = ks;
+    e.k = k;
+    CKV_TRY_HIP(launch_expand(e, d.U, s), "expand launch");
+  }
+  return CKV_OK;
+}
+
 int ckv::gather_kv_width(const ckv_shape* shape, const uint16_t* k_src, const uint16_t* v_src,
                     int src_kind, const int32_t* idx, const int32_t* n_sel, int32_t k,
                     uint16_t* k_dst, uint16_t* v_dst, int workgroups, void* stream) {
@@ -506,7 +628,7 @@ int ckv_workspace_bytes(const ckv_shape* shape, int32_t k, int entry, size_t* by
   if (!bytes) return fail(CKV_EINVAL, "bytes is NULL");
   if (entry != CKV_ENTRY_SELECT_TOPK && entry != CKV_ENTRY_SPARSE_DECODE_ATTN &&
       entry != CKV_ENTRY_CRITICAL_KV_ATTN && entry != CKV_ENTRY_CORRECTED_ATTN &&
-      entry != CKV_ENTRY_DUAL_TOKEN_ATTN)
+      entry != CKV_ENTRY_DUAL_TOKEN_ATTN && entry != CKV_ENTRY_DECODE_STEP)
     return fail(CKV_EINVAL, "unknown entry %d", entry);
   *bytes = make_layout(d, k, entry).total;
   return CKV_OK;

@@ -18,6 +18,13 @@ __global__ __launch_bounds__(256) void k_zero(uint4* p, int64_t n16) {
     p[i] = make_uint4(0u, 0u, 0u, 0u);
 }
 
+// Fills p with a 32-bit pattern (the pipeline's poison of released buffers).
+__global__ __launch_bounds__(256) void k_fill(uint4* p, int64_t n16, uint32_t pattern) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    p[i] = make_uint4(pattern, pattern, pattern, pattern);
+}
+
 // ---- scoring -------------------------------------------------------------
 template <int G, bool HIST>
 __global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a) {
@@ -654,6 +661,26 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
   }
 }
 
+// The same with two tokens (Sec. 5.2, dual-token decoding): the attention
+// role has the 2G head rows of the current and the speculative token (the
+// merge kernel adds their own rows under the causal mask), the scoring role
+// the speculative token's G heads.
+template <int G, bool INDEXED>
+__global__ __launch_bounds__(kAttnThreads) void k_dual2(AttnArgs at, ScoreArgs sc,
+                                                       int attn_blocks) {
+  constexpr int kA = AttnLds<2 * G>::kFloats;
+  constexpr int kS = kHistBins + kScoreLdsDwords;
+  __shared__ __attribute__((aligned(16))) float lds[kA > kS ? kA : kS];
+  if ((int)blockIdx.x < attn_blocks) {
+    const int unit = blockIdx.x / at.chunks;
+    attn_chunk<2 * G, INDEXED>(at, unit, blockIdx.x - unit * at.chunks, lds);
+  } else {
+    uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
+    score_range<G, true>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks,
+                         l32 + kScoreLdsDwords, l32);
+  }
+}
+
 // Merges the chunk partials of every query head into the output.  The
 // per-chunk (max, weight sum) pairs go through LDS first so that each thread's
 // loads of the weighted sums are independent of one another.  With two tokens
@@ -1065,6 +1092,14 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 == 0) return hipSuccess;
+  launch_kernel(CKV_K_ZERO, k_fill, dim3(blocks_for(n16, 256 * 4, 2048)), dim3(256), s,
+                reinterpret_cast<uint4*>(p), n16, pattern);
+  return hipGetLastError();
+}
+
 // Workgroups of a kScoreThreads kernel that fit on the device at once, per
 // (kernel, device): queried once and kept in a fixed table (no allocation on
 // the call path), so a call makes no occupancy query.  The persistent
@@ -1122,6 +1157,12 @@ static const void* score_kernel(ScoreKind kind, int chunk) {
       return chunk > 1 ? (const void*)k_score_chunks<G> : (const void*)k_score<G, true>;
     case ScoreKind::kDual: return (const void*)k_dual<G, false>;
     case ScoreKind::kDualIndexed: return (const void*)k_dual<G, true>;
+    case ScoreKind::kDual2:
+      if constexpr (G <= 8) return (const void*)k_dual2<G, false>;
+      return nullptr;
+    case ScoreKind::kDual2Indexed:
+      if constexpr (G <= 8) return (const void*)k_dual2<G, true>;
+      return nullptr;
   }
   return nullptr;
 }
@@ -1136,6 +1177,7 @@ int score_blocks(const ScoreArgs& a, int G, ScoreKind kind) {
     case 16: fn = score_kernel<16>(kind, a.chunk); break;
     default: return 0;
   }
+  if (!fn) return 0;
   const int64_t groups = (int64_t)a.units * ((a.max_ctx + kStageRows - 1) / kStageRows);
   int64_t slots = resident_blocks(fn);
   if (slots > kMaxScoreWgs) slots = kMaxScoreWgs;
@@ -1236,10 +1278,33 @@ static hipError_t launch_dual_i(const AttnArgs& at, const ScoreArgs& sc, int G,
   return hipGetLastError();
 }
 
+template <int G, bool INDEXED>
+static void launch_dual2_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks, int nwg,
+                           hipStream_t s) {
+  launch_kernel(CKV_K_DUAL, k_dual2<G, INDEXED>, dim3(attn_blocks + nwg), dim3(kAttnThreads),
+                s, at, sc, attn_blocks);
+}
+
+template <bool INDEXED>
+static hipError_t launch_dual2_i(const AttnArgs& at, const ScoreArgs& sc, int G,
+                                 int attn_blocks, int nwg, hipStream_t s) {
+  switch (G) {
+    case 1: launch_dual2_g<1, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 2: launch_dual2_g<2, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 4: launch_dual2_g<4, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    case 8: launch_dual2_g<8, INDEXED>(at, sc, attn_blocks, nwg, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
                        int units, int nwg, hipStream_t s) {
   if (nwg < 1 || nwg > kMaxScoreWgs) return hipErrorInvalidValue;
   const int attn_blocks = units * at.chunks;
+  if (at.q2)  // two tokens: 2G head rows attend, G score
+    return indexed ? launch_dual2_i<true>(at, sc, G, attn_blocks, nwg, s)
+                   : launch_dual2_i<false>(at, sc, G, attn_blocks, nwg, s);
   return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, nwg, s)
                  : launch_dual_i<false>(at, sc, G, attn_blocks, nwg, s);
 }

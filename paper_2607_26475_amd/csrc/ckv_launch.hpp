@@ -13,10 +13,12 @@ int hip_fail(hipError_t e, const char* what);
 const char* last_detail();
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s);
 // The kernel that runs a scoring pass: scores only, scores with the
 // first-digit histogram (chunk landmarks when a.chunk > 1), or the scoring
 // role of the one-launch attend-and-score kernel (buffer or rows in place).
-enum class ScoreKind { kPlain, kHist, kDual, kDualIndexed };
+// kDual2*: the same with the two tokens' 2G head rows attending (G <= 8).
+enum class ScoreKind { kPlain, kHist, kDual, kDualIndexed, kDual2, kDual2Indexed };
 // Workgroups of that scoring pass for these arguments.  A call computes it
 // once and passes the same value to the launcher and to the selection, whose
 // histogram slots depend on it.
@@ -32,6 +34,9 @@ hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStr
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
                               hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
+// The one-launch attend-and-score kernel: attention over the buffer or rows in
+// place (indexed) with G head rows, or with the 2G rows of two tokens when
+// at.q2 is set; scoring with G heads on nwg workgroups.
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
                        int units, int nwg, hipStream_t s);
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s);
@@ -50,6 +55,39 @@ int device_cus();
 // (CKV_NOALLOC_SCRATCH_BYTES), asked of the runtime on the first call per
 // device.
 int noalloc_scratch(void** ptr);
+
+// One pipelined layer of the decode loop (Sec. 4.1, Sec. 5.2-5.4): attention
+// of q_att over the set selected one step earlier (assembled in k_buf/v_buf,
+// or rows idx_in of k_src/v_src in place, n_sel_in rows) and, in the same
+// launch, the scoring of the next step's selection with q_sel (NULL: q_att):
+// of the keys k_score, or, with chunk > 1, of the chunk landmarks, whose k /
+// chunk best chunks are expanded to rows; idx_out/n_sel_out get the rows.
+// With out_spec set, the speculative token (query q_sel) attends in the same
+// launch over the same rows and the two tokens' own rows k_local/v_local
+// ([B][Hkv][2][d], causal), as ckv_dual_token_attn.  Workspace:
+// CKV_ENTRY_DECODE_STEP.
+struct PipelinedLayer {
+  const uint16_t* q_att;
+  const uint16_t* q_sel;
+  const uint16_t* k_score;
+  int32_t chunk;
+  const uint16_t* landmarks;
+  const uint16_t* k_src;
+  const uint16_t* v_src;
+  int src_kind;
+  const int32_t* idx_in;
+  const uint16_t* k_buf;
+  const uint16_t* v_buf;
+  const int32_t* n_sel_in;
+  int32_t* idx_out;
+  int32_t* n_sel_out;
+  float* out;
+  const uint16_t* k_local;
+  const uint16_t* v_local;
+  float* out_spec;
+};
+int pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p, const int32_t* ctx_lens,
+                    int32_t k, float scale, void* ws, size_t ws_bytes, void* stream);
 
 // Largest gather grid a caller may ask for.
 constexpr int kMaxGatherWgs = 4096;

@@ -13,9 +13,38 @@ struct ckv_pipeline {
   unsigned long long filled_capture[2];  // capture filled[i] was last recorded in (0: none)
   int parity;            // buffer of the next layer to compute
   int gather_wgs;        // workgroups of each refill (0: the gather's default)
+  unsigned checks;       // CKV_PIPE_CHECK_* flags (tests of the event protocol)
 };
 
 namespace {
+
+// A layer that the plain entries do not cover: chunk landmarks or two tokens.
+bool special_layer(const ckv_layer& L) { return L.chunk > 1 || L.out_spec != nullptr; }
+
+int run_special(const ckv_shape* shape, const ckv_layer& L, const int32_t* ctx_lens,
+                int32_t k, float scale, int src_kind, const uint16_t* k_buf,
+                const uint16_t* v_buf, void* ws, size_t ws_bytes, void* stream) {
+  ckv::PipelinedLayer p;
+  p.q_att = L.q_att;
+  p.q_sel = L.q_sel;
+  p.k_score = L.k_score;
+  p.chunk = L.chunk;
+  p.landmarks = L.landmarks;
+  p.k_src = L.k_src;
+  p.v_src = L.v_src;
+  p.src_kind = src_kind;
+  p.idx_in = k_buf ? nullptr : L.idx_prev;  // no buffers: rows read in place
+  p.k_buf = k_buf;
+  p.v_buf = v_buf;
+  p.n_sel_in = L.n_sel_prev;
+  p.idx_out = L.idx_next;
+  p.n_sel_out = L.n_sel_next;
+  p.out = L.out;
+  p.k_local = L.k_local;
+  p.v_local = L.v_local;
+  p.out_spec = L.out_spec;
+  return ckv::pipelined_layer(shape, p, ctx_lens, k, scale, ws, ws_bytes, stream);
+}
 
 // Id of the stream capture s takes part in, 0 if it is not capturing.
 unsigned long long capture_id(hipStream_t s) {
@@ -64,6 +93,7 @@ int ckv_pipeline_create(ckv_pipeline** pipe) {
   }
   p->parity = 0;
   p->gather_wgs = 0;
+  p->checks = 0;
   p->filled_capture[0] = p->filled_capture[1] = 0;
   *pipe = p;
   return CKV_OK;
@@ -75,6 +105,15 @@ int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups) {
     return ckv::fail(CKV_EINVAL, "gather width %d outside [0, %d]", workgroups,
                      ckv::kMaxGatherWgs);
   pipe->gather_wgs = workgroups;
+  return CKV_OK;
+}
+
+int ckv_pipeline_set_checks(ckv_pipeline* pipe, unsigned flags) {
+  if (!pipe) return ckv::fail(CKV_EINVAL, "pipe is NULL");
+  if (flags & ~(unsigned)(CKV_PIPE_CHECK_NO_FILL_WAIT | CKV_PIPE_CHECK_NO_RELEASE_WAIT |
+                          CKV_PIPE_CHECK_POISON))
+    return ckv::fail(CKV_EINVAL, "unknown check flags 0x%x", flags);
+  pipe->checks = flags;
   return CKV_OK;
 }
 
@@ -120,16 +159,23 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
         return ckv::fail(CKV_EINVAL, "layer %d: miss correction needs the two buffers", l);
     for (int l = 0; l < num_layers; ++l) {
       const ckv_layer& L = layers[l];
-      int rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
-                                    L.k_src, L.v_src, src_kind, L.idx_prev, nullptr, nullptr,
-                                    L.n_sel_prev, L.idx_next, L.n_sel_next, L.out, ws,
-                                    ws_bytes, compute_stream);
+      int rc = special_layer(L)
+                   ? run_special(shape, L, ctx_lens, k, scale, src_kind, nullptr, nullptr, ws,
+                                 ws_bytes, compute_stream)
+                   : ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k,
+                                          scale, L.k_src, L.v_src, src_kind, L.idx_prev,
+                                          nullptr, nullptr, L.n_sel_prev, L.idx_next,
+                                          L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
       if (rc) return rc;
     }
     return CKV_OK;
   }
   if (num_layers < 2 || !k_buf || !v_buf)
     return ckv::fail(CKV_EINVAL, "the two-buffer loop needs at least 2 layers and both buffers");
+  for (int l = 0; l < num_layers; ++l)
+    if (layers[l].idx_true && special_layer(layers[l]))
+      return ckv::fail(CKV_EINVAL,
+                       "layer %d: miss correction of a chunked or two-token layer", l);
   hipStream_t cs = (hipStream_t)compute_stream, xs = (hipStream_t)copy_stream;
   const unsigned long long capture = capture_id(cs);
   // A graph fixes each layer's buffer at capture time.  Over an odd number of
@@ -145,11 +191,15 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     // attention over buffer p once its gather has landed.  Under stream
     // capture a fill recorded outside this capture cannot be waited for;
     // the graph is then ordered after it by its launch.
-    if (!capture || pipe->filled_capture[p] == capture)
+    if ((!capture || pipe->filled_capture[p] == capture) &&
+        !(pipe->checks & CKV_PIPE_CHECK_NO_FILL_WAIT))
       if (hipError_t e = hipStreamWaitEvent(cs, pipe->filled[p], 0))
         return ckv::hip_fail(e, "wait for a buffer fill");
     int rc;
-    if (L.idx_true && L.lr_rank > 0) {  // misses: keys rebuilt, values fetched
+    if (special_layer(L)) {  // chunk landmarks or two tokens
+      rc = run_special(shape, L, ctx_lens, k, scale, src_kind, k_buf[p], v_buf[p], ws,
+                       ws_bytes, compute_stream);
+    } else if (L.idx_true && L.lr_rank > 0) {  // misses: keys rebuilt, values fetched
       rc = ckv_corrected_attn_lowrank(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
                                       L.k_src, L.v_src, src_kind, L.lr_rank, L.lr_u, L.lr_w,
                                       L.idx_prev, L.n_sel_prev, k_buf[p], v_buf[p],
@@ -171,8 +221,16 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     if (hipError_t e = hipEventRecord(pipe->freed[p], cs))
       return ckv::hip_fail(e, "release event record");
     // refill buffer p with the layer two ahead (into the next step at the end)
-    if (hipError_t e = hipStreamWaitEvent(xs, pipe->freed[p], 0))
-      return ckv::hip_fail(e, "wait for a buffer release");
+    if (!(pipe->checks & CKV_PIPE_CHECK_NO_RELEASE_WAIT))
+      if (hipError_t e = hipStreamWaitEvent(xs, pipe->freed[p], 0))
+        return ckv::hip_fail(e, "wait for a buffer release");
+    if (pipe->checks & CKV_PIPE_CHECK_POISON) {  // NaN bits where the refill will go
+      const size_t bytes = (size_t)shape->batch * shape->num_kv_heads * k * shape->head_dim * 2;
+      if (hipError_t e = ckv::launch_fill(k_buf[p], bytes, 0xffffffffu, xs))
+        return ckv::hip_fail(e, "poison launch");
+      if (hipError_t e = ckv::launch_fill(v_buf[p], bytes, 0xffffffffu, xs))
+        return ckv::hip_fail(e, "poison launch");
+    }
     const int j = l + 2;
     if (j < num_layers) {
       rc = gather_layer(pipe, shape, k, layers[j], layers[j].idx_prev, layers[j].n_sel_prev,

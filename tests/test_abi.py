@@ -119,6 +119,7 @@ def test_pipeline_argument_checks():
     assert lib.ckv_pipeline_create(None) == STATUS["EINVAL"]
     assert lib.ckv_pipeline_destroy(None) == STATUS["OK"]
     assert lib.ckv_pipeline_set_gather_width(None, 64) == STATUS["EINVAL"]
+    assert lib.ckv_pipeline_set_checks(None, 1) == STATUS["EINVAL"]
     layers = (ckv.Layer * 2)()
     assert lib.ckv_pipeline_prime(None, ctypes.byref(s), 16, layers, 2, 0, bufs, bufs,
                                   None) == STATUS["EINVAL"]
