@@ -230,7 +230,8 @@ def main() -> int:
     pipeline = {}
     if "long128k" in sections:
         pipeline.update(measure_pipeline(torch, ckv, synth, dev, np, host_link,
-                                         steps=args.loop_steps))
+                                         steps=args.loop_steps,
+                                         runs=("plain", "corrected", "lowrank", "chunk8")))
         log(f"pipeline long128k: {pipeline}")
         torch.cuda.empty_cache()
     if "dual64" in sections:
@@ -244,7 +245,7 @@ def main() -> int:
         # the million-token single request
         pipeline["million"] = measure_pipeline(torch, ckv, synth, dev, np, host_link, "million",
                                                n_hbm=2, n_host=2, steps=args.loop_steps,
-                                               runs=("plain",), layer_queries=True)
+                                               runs=("plain", "chunk8"), layer_queries=True)
         log(f"pipeline million: {pipeline['million']}")
     if pipeline:
         result["pipeline"] = pipeline
@@ -569,66 +570,88 @@ def measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, shape, w, scale, steps, s
     with the speculative query; the selection then picks next step's set.
     Index sets alternate between two arrays per layer by step parity.  Queries
     are step-invariant: the current one is the layer's, the speculative one
-    bf16(0.8 q + 0.6 noise)."""
+    bf16(0.8 q + 0.6 noise).  A second run co-batches the two tokens (Sec.
+    5.2): in the same launch the speculative token also attends over the set
+    and both tokens over their own new rows (causal mask)."""
     B, Hq, Hkv, d, k, L = w.batch, w.q_heads, w.kv_heads, w.head_dim, w.k, w.layers
     dev = torch.device("cuda:0")
     g = torch.Generator(device=dev)
     g.manual_seed(4321)
     qs = [(0.8 * t["q"].float() + 0.6 * torch.randn(t["q"].shape, generator=g, device=dev))
           .to(torch.bfloat16) for t in layers]
+    local = [(torch.randn((B, Hkv, 2, d), generator=g, device=dev).to(torch.bfloat16),
+              torch.randn((B, Hkv, 2, d), generator=g, device=dev).to(torch.bfloat16))
+             for _ in layers]
     i32 = dict(dtype=torch.int32, device=dev)
     idx = [[torch.empty((B, Hkv, k), **i32) for _ in range(L)] for _ in range(2)]
     nsel = [[torch.empty((B, Hkv), **i32) for _ in range(L)] for _ in range(2)]
     out = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
-    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
-    io = [ckv.layer_array([{"q_att": t["q"], "q_sel": qs[l], "k_score": kv_ptrs[l][0],
-                            "k_src": kv_ptrs[l][0], "v_src": kv_ptrs[l][1],
-                            "idx_prev": idx[c][l], "n_sel_prev": nsel[c][l],
-                            "idx_next": idx[1 - c][l], "n_sel_next": nsel[1 - c][l],
-                            "out": out[l]} for l, t in enumerate(layers)])
-          for c in range(2)]
+    out_spec = [torch.empty((B, Hq, d), device=dev) for _ in range(L)]
+    ws = ckv.workspace(shape, k, ckv.ENTRY_DECODE_STEP)
     lens = layers[0]["ctx_lens"]
     assert all(torch.equal(t["ctx_lens"], lens) for t in layers)
-    pipe = ckv.Pipeline()
-    cur = [0]
 
-    def step():
-        pipe.step(shape, io[cur[0]], lens, k, scale, ckv.SRC_DEVICE, None, None, ws, stream,
-                  None)
-        cur[0] ^= 1
+    def one_run(two):
+        io = [ckv.layer_array([{"q_att": t["q"], "q_sel": qs[l], "k_score": kv_ptrs[l][0],
+                                "k_src": kv_ptrs[l][0], "v_src": kv_ptrs[l][1],
+                                "idx_prev": idx[c][l], "n_sel_prev": nsel[c][l],
+                                "idx_next": idx[1 - c][l], "n_sel_next": nsel[1 - c][l],
+                                "out": out[l],
+                                "k_local": local[l][0] if two else None,
+                                "v_local": local[l][1] if two else None,
+                                "out_spec": out_spec[l] if two else None}
+                               for l, t in enumerate(layers)])
+              for c in range(2)]
+        pipe = ckv.Pipeline()
+        cur = [0]
 
-    # bootstrap (the pre-decoding step): same-step selection into set 0
-    for l, t in enumerate(layers):
-        kp, vp = kv_ptrs[l]
-        ckv.critical_kv_attn(shape, t["q"], qs[l], kp, t["ctx_lens"], k, scale, kp, vp,
-                             ckv.SRC_DEVICE, None, None, None, idx[0][l], nsel[0][l], out[l],
-                             ws, stream)
-    for _ in range(3):
+        def step():
+            pipe.step(shape, io[cur[0]], lens, k, scale, ckv.SRC_DEVICE, None, None, ws, stream,
+                      None)
+            cur[0] ^= 1
+
+        # bootstrap (the pre-decoding step): same-step selection into set 0
+        for l, t in enumerate(layers):
+            kp, vp = kv_ptrs[l]
+            ckv.critical_kv_attn(shape, t["q"], qs[l], kp, t["ctx_lens"], k, scale, kp, vp,
+                                 ckv.SRC_DEVICE, None, None, None, idx[0][l], nsel[0][l],
+                                 out[l], ws, stream)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        ckv.profile_begin()
         step()
-    torch.cuda.synchronize()
-    ckv.profile_begin()
-    step()
-    torch.cuda.synchronize()
-    per = {kname: round(1e3 * tot / c, 1) for kname, (c, tot, _) in ckv.profile_end().items()}
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    pipe.close()
-    ms = e0.elapsed_time(e1) / steps
-    assert all(torch.isfinite(o).all().item() for o in out[:2])
-    dual_bytes = B * Hkv * (w.max_ctx * d * 2 + k * 2 * d * 2)
-    res = {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3), "per_layer_us": per,
-           "workload": "the Llama-8B step above, pipelined through the decode loop without "
+        torch.cuda.synchronize()
+        per = {kname: round(1e3 * tot / c, 1) for kname, (c, tot, _) in ckv.profile_end().items()}
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pipe.close()
+        ms = e0.elapsed_time(e1) / steps
+        assert all(torch.isfinite(o).all().item() for o in out[:2])
+        if two:
+            assert all(torch.isfinite(o).all().item() for o in out_spec[:2])
+        dual_bytes = B * Hkv * (w.max_ctx * d * 2 + k * 2 * d * 2)
+        res = {"ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3), "per_layer_us": per}
+        if "dual" in per:
+            res["dual_bytes_per_launch"] = dual_bytes
+            res["dual_GBps"] = dual_bytes / (per["dual"] * 1e-6) / 1e9
+            res["dual_frac_of_peak"] = res["dual_GBps"] / HBM_PEAK_GBPS
+        return res
+
+    res = one_run(False)
+    res["workload"] = ("the Llama-8B step above, pipelined through the decode loop without "
                        "buffers: attention over last step's set read in place from HBM and "
-                       "scoring with the speculative query in one launch per layer"}
-    if "dual" in per:
-        res["dual_bytes_per_launch"] = dual_bytes
-        res["dual_GBps"] = dual_bytes / (per["dual"] * 1e-6) / 1e9
-        res["dual_frac_of_peak"] = res["dual_GBps"] / HBM_PEAK_GBPS
-    del qs, idx, nsel, out, ws, io
+                       "scoring with the speculative query in one launch per layer")
+    res["two_tokens"] = one_run(True)
+    res["two_tokens"]["workload"] = (
+        "the same loop with both tokens attending in that launch (2G head rows: the current "
+        "token over the set and its own row, the speculative token over the set and both "
+        "rows, causal mask), outputs for both tokens per step")
+    del qs, idx, nsel, out, out_spec, ws, local
     return res
 
 
@@ -709,16 +732,31 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
     k_buf = [torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev) for _ in range(2)]
     v_buf = [torch.empty_like(k_buf[0]) for _ in range(2)]
     shape = ckv.shape_for(B, Hq, Hkv, n, kv_row_stride=2 * d)
-    ws = ckv.workspace(shape, k, ckv.ENTRY_CORRECTED_ATTN)
+    ws = ckv.workspace(shape, k, ckv.ENTRY_DECODE_STEP)
     compute, copy = _pipeline_streams(torch)
     s1 = ckv.shape_for(B, Hq, Hkv, n)
     sc = torch.empty((B, Hkv, n), device=dev)
     wsel = ckv.workspace(s1, k, ckv.ENTRY_SELECT_TOPK)
+    wchunk = ckv.workspace(s1, k, ckv.ENTRY_CRITICAL_KV_ATTN) if any(
+        r.startswith("chunk") for r in runs) else None
+    cidx = {int(r[len("chunk"):]): torch.empty((B, Hkv, k // int(r[len("chunk"):])), **i32)
+            for r in runs if r.startswith("chunk")}
+    nch = torch.empty((B, Hkv), **i32)
 
     lr_rank = 32
     lr = []
 
-    def run(corrected, lowrank=False):
+    lms = {}  # chunk landmarks per (chunk, HBM layer), built once (prefill-time work)
+
+    def landmarks(chunk, i):
+        if (chunk, i) not in lms:
+            cmax = (n + chunk - 1) // chunk
+            lm = torch.empty((B, Hkv, cmax, d), dtype=torch.bfloat16, device=dev)
+            ckv.chunk_landmarks(s1, chunk, kscore[i], lens, lm)
+            lms[(chunk, i)] = lm
+        return lms[(chunk, i)]
+
+    def run(corrected, lowrank=False, chunk=1):
         def io(step, cur):
             return [{"q_att": q[step][l], "q_sel": qs[step][l], "k_score": kscore[l % n_hbm],
                      "k_src": hosts[l % n_host].data_ptr(),
@@ -731,12 +769,19 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
                      "hits": hits[step][l] if corrected else None,
                      "lr_rank": lr_rank if lowrank else 0,
                      "lr_u": lr[l % n_host][0] if lowrank else None,
-                     "lr_w": lr[l % n_host][1] if lowrank else None} for l in range(L)]
+                     "lr_w": lr[l % n_host][1] if lowrank else None,
+                     "chunk": chunk,
+                     "landmarks": landmarks(chunk, l % n_hbm) if chunk > 1 else None}
+                    for l in range(L)]
 
         # bootstrap selection (the pre-decoding step) into set 0
         for l in range(L):
-            ckv.score_keys(s1, q[0][l], kscore[l % n_hbm], lens, scale, sc)
-            ckv.select_topk(s1, sc, lens, k, idx[0][l], nsel[0][l], wsel)
+            if chunk > 1:
+                ckv.select_chunks(s1, chunk, q[0][l], landmarks(chunk, l % n_hbm), lens, k,
+                                  scale, cidx[chunk], nch, idx[0][l], nsel[0][l], wchunk)
+            else:
+                ckv.score_keys(s1, q[0][l], kscore[l % n_hbm], lens, scale, sc)
+                ckv.select_topk(s1, sc, lens, k, idx[0][l], nsel[0][l], wsel)
         torch.cuda.synchronize()
         pipe = ckv.Pipeline()
         if gather_width:
@@ -791,6 +836,7 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
                "kernels_ms_per_step": {kname: round(v[1] / stamped, 4)
                                        for kname, v in stats.items()},
                "overlap": (gather_ms + compute_ms) / ms,
+               "refill_GBps": B * Hkv * k * 2 * d * 2 / (gather_ms / L * 1e-3) / 1e9,
                "gather_workgroups": gather_width or ("auto: 80" if n >= 64 * k else "auto: 256")}
         if corrected:  # the misses cross the link too, on the compute stream
             found = sum(int(hits[t][l].sum()) for t in range(first, first + steps)
@@ -806,6 +852,16 @@ def measure_pipeline(torch, ckv, synth, dev, np, host_link, wl="long128k", n_hbm
         return res
 
     res = run(False)
+    for run_name in runs:
+        if run_name.startswith("chunk"):  # chunk landmarks: contiguous-block refills
+            c = int(run_name[len("chunk"):])
+            r = run(False, chunk=c)
+            r["chunk"] = c
+            refill = r["gather_ms_per_step"] / L
+            r["refill_us"] = 1e3 * refill
+            r["refill_GBps"] = B * Hkv * k * 2 * d * 2 / (refill * 1e-3) / 1e9
+            r["row_refill_GBps"] = res["refill_GBps"]
+            res[run_name] = r
     ctx = (f"context {n}" if w.ctx_min == n else f"contexts U{{{w.ctx_min}..{n}}}")
     res["workload"] = (f"{wl} decode, {L} layers: B{B}, {Hq} q / {Hkv} KV heads, head_dim {d}, "
                        f"{ctx}, k {k}; K|V rows host-pinned, scoring keys in HBM; "

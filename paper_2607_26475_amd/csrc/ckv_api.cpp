@@ -541,7 +541,7 @@ int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
   const int nwg = score_blocks(sc, d.G, kind);
   if (use_partials(ds, Ls, nwg))
     set_partials(ws, Ls, nwg, &sc, &sa);
-  else
+  else if (!p.hist_clean)
     CKV_TRY_HIP(launch_zero(ws, Ls.zero_end, s), "zero launch");
   CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
   if (two) {
@@ -715,6 +715,19 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
                          const int32_t* idx_in, const uint16_t* k_buf, const uint16_t* v_buf,
                          const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out,
                          float* out, void* ws, size_t ws_bytes, void* stream) {
+  return ckv::critical_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
+                            src_kind, idx_in, k_buf, v_buf, n_sel_in, idx_out, n_sel_out, out,
+                            ws, ws_bytes, stream, false);
+}
+
+}  // extern "C"
+
+int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                       const uint16_t* k_score, const int32_t* ctx_lens, int32_t k, float scale,
+                       const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                       const int32_t* idx_in, const uint16_t* k_buf, const uint16_t* v_buf,
+                       const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out,
+                       float* out, void* ws, size_t ws_bytes, void* stream, bool hist_clean) {
   Dims d;
   int rc = check_shape(shape, &d);
   if (rc) return rc;
@@ -754,9 +767,11 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   const bool pipelined = assembled || in_place;
   const int nwg = score_blocks(
       sc, d.G, !pipelined ? ScoreKind::kHist : in_place ? ScoreKind::kDualIndexed : ScoreKind::kDual);
+  // a pipelined call whose caller knows the histograms clear (the previous
+  // selection on this workspace left them so) skips the clearing kernel
   if (use_partials(d, L, nwg))
     set_partials(ws, L, nwg, &sc, &sa);
-  else
+  else if (!(pipelined && hist_clean))
     CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
   if (pipelined) {
     AttnArgs at_ = assembled ? attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel_in, kD,
@@ -782,6 +797,8 @@ int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
   }
   return CKV_OK;
 }
+
+extern "C" {
 
 int ckv_critical_kv_attn_noalloc(const ckv_shape* shape, const uint16_t* q_att,
                                  const uint16_t* q_sel, const uint16_t* k_score,
@@ -938,16 +955,15 @@ int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q
 
 }  // extern "C"
 
-namespace {
-
 // rank == 0: misses fetched whole; else their keys rebuilt from u_fac/w_fac
-int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
-                   const uint16_t* k_score, const int32_t* ctx_lens, int32_t k, float scale,
-                   const uint16_t* k_src, const uint16_t* v_src, int src_kind, int32_t rank,
-                   const uint16_t* u_fac, const uint16_t* w_fac, const int32_t* idx_pred,
-                   const int32_t* n_pred, uint16_t* k_buf, uint16_t* v_buf,
-                   int32_t* idx_true, int32_t* n_true, int32_t* hits, int32_t* idx_next,
-                   int32_t* n_next, float* out, void* ws, size_t ws_bytes, void* stream) {
+int ckv::corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                        const uint16_t* k_score, const int32_t* ctx_lens, int32_t k,
+                        float scale, const uint16_t* k_src, const uint16_t* v_src,
+                        int src_kind, int32_t rank, const uint16_t* u_fac,
+                        const uint16_t* w_fac, const int32_t* idx_pred, const int32_t* n_pred,
+                        uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true, int32_t* n_true,
+                        int32_t* hits, int32_t* idx_next, int32_t* n_next, float* out,
+                        void* ws, size_t ws_bytes, void* stream, bool hist_clean) {
   Dims d;
   int rc = check_shape(shape, &d);
   if (rc) return rc;
@@ -999,7 +1015,7 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
     // dual launch writes them again
     set_partials(ws, L, nwg1, &c1, &s1);
     set_partials(ws, L, nwg2, &c2, &s2);
-  } else {
+  } else if (!hist_clean) {
     CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
   }
   CKV_TRY_HIP(launch_score(c1, d.G, true, nwg1, s), "score launch");
@@ -1048,8 +1064,6 @@ int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t
   return select_and_merge(s2, at_, d, s);
 }
 
-}  // namespace
-
 extern "C" {
 
 int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
@@ -1059,9 +1073,10 @@ int ckv_corrected_attn(const ckv_shape* shape, const uint16_t* q_att, const uint
                        uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
                        int32_t* n_true, int32_t* hits, int32_t* idx_next, int32_t* n_next,
                        float* out, void* ws, size_t ws_bytes, void* stream) {
-  return corrected_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
-                        src_kind, 0, nullptr, nullptr, idx_pred, n_pred, k_buf, v_buf,
-                        idx_true, n_true, hits, idx_next, n_next, out, ws, ws_bytes, stream);
+  return ckv::corrected_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
+                             src_kind, 0, nullptr, nullptr, idx_pred, n_pred, k_buf, v_buf,
+                             idx_true, n_true, hits, idx_next, n_next, out, ws, ws_bytes,
+                             stream, false);
 }
 
 int ckv_corrected_attn_lowrank(const ckv_shape* shape, const uint16_t* q_att,
@@ -1076,9 +1091,10 @@ int ckv_corrected_attn_lowrank(const ckv_shape* shape, const uint16_t* q_att,
                                void* stream) {
   int rc = check_rank(rank);
   if (rc) return rc;
-  return corrected_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
-                        src_kind, rank, u_fac, w_fac, idx_pred, n_pred, k_buf, v_buf,
-                        idx_true, n_true, hits, idx_next, n_next, out, ws, ws_bytes, stream);
+  return ckv::corrected_impl(shape, q_att, q_sel, k_score, ctx_lens, k, scale, k_src, v_src,
+                             src_kind, rank, u_fac, w_fac, idx_pred, n_pred, k_buf, v_buf,
+                             idx_true, n_true, hits, idx_next, n_next, out, ws, ws_bytes,
+                             stream, false);
 }
 
 int ckv_reconstruct_keys(const ckv_shape* shape, int32_t rank, const uint16_t* u_fac,

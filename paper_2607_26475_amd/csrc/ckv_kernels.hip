@@ -122,6 +122,22 @@ __global__ __launch_bounds__(kFilterThreads) void k_filter(SelectArgs a) {
   }
 }
 
+// Zeroes the unit's first-digit histogram, coarse histogram and control
+// words, as the clearing kernel would, after the selection has read them for
+// the last time (all kFinishThreads threads; thread t takes bins 2t and
+// 2t + 1, the bins it loaded itself).  A selection that counted its first
+// digit into these cleared areas leaves them clear, so a caller running
+// several selections on one workspace in stream order clears it once.
+__device__ __forceinline__ void clear_unit_hist(const SelectArgs& a, int unit) {
+  static_assert(2 * kFinishThreads == kHistBins, "two bins per thread");
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's own loads of these words are back
+  __syncthreads();                // and every other thread's
+  const int t = threadIdx.x;
+  *reinterpret_cast<uint2*>(a.hist + (int64_t)unit * kHistBins + 2 * t) = make_uint2(0u, 0u);
+  if (t < kCoarseBins) a.coarse[(int64_t)unit * kCoarseBins + t] = 0u;
+  if (t < kCtrlWords) a.ctrl[(int64_t)unit * kCtrlWords + t] = 0u;
+}
+
 // Writes set bits of bm[0, words) as ascending positions to out[0, limit)
 // (when out is not null), 16 waves each owning a contiguous word range (reads
 // are lane-consecutive), and returns the number of set bits.  Output slots
@@ -240,6 +256,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
   if (m >= n) {  // uniform; every position (possibly none) is selected
     for (int i = tid; i < a.k; i += kFinishThreads) idx[i] = i < n ? i : -1;
     if (tid == 0) a.n_sel[unit] = m;
+    clear_unit_hist(a, unit);
     return;
   }
   const uint32_t* ctrl = a.ctrl + (int64_t)unit * kCtrlWords;
@@ -285,6 +302,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_finish(SelectArgs a) {
   emit_bitmap(bm, words, idx, (uint32_t)a.k, tmp);
   for (int i = m + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
   if (tid == 0) a.n_sel[unit] = m;
+  clear_unit_hist(a, unit);
 }
 
 // Whole selection of one unit in one workgroup, for n_b <= kFusedSelectMaxCtx.
@@ -466,10 +484,13 @@ struct SelLds {
 // atomic per wave.  The threshold inside the bin is then resolved exactly,
 // the chosen candidates marked, and the bitmap written out in ascending
 // order: to idx/n_sel when `write`, and output slots [lo, hi) to share[slot -
-// lo] when share is not null.  Returns the number of positions selected.
+// lo] when share is not null.  When the first digit was counted into the
+// cleared per-unit histogram (no hist_part) and `clear` is set, the unit's
+// histogram and control words are left cleared; only the unit's one reader
+// may do that.  Returns the number of positions selected.
 __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const SelLds& L,
                                            bool write, int32_t* share, uint32_t lo,
-                                           uint32_t hi) {
+                                           uint32_t hi, bool clear) {
   const int tid = threadIdx.x;
   uint2* const cand = L.cand;
   uint32_t* const bm = L.bm;
@@ -512,6 +533,7 @@ __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const 
       if (share && i < n && (uint32_t)i >= lo && (uint32_t)i < hi) share[i - lo] = i;
     }
     if (write && tid == 0) a.n_sel[unit] = m;
+    if (clear && !a.hist_part) clear_unit_hist(a, unit);
     return m;
   }
   store_hist_sum(hv, nslots, lhist);
@@ -560,6 +582,7 @@ __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const 
     for (int i = got + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
     if (tid == 0) a.n_sel[unit] = got;
   }
+  if (clear && !a.hist_part) clear_unit_hist(a, unit);
   return got;
 }
 
@@ -570,7 +593,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_fused(SelectArgs a) {
   __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
   __shared__ uint32_t misc[8];
   const int unit = blockIdx.x;
-  select_unit(a, unit, SelLds{cand, bm, lhist, tmp, misc}, true, nullptr, 0, 0);
+  select_unit(a, unit, SelLds{cand, bm, lhist, tmp, misc}, true, nullptr, 0, 0, true);
   // one call site, so that the merge appears once (a second inlined copy
   // kept more of the selection's registers live)
   if (a.mpart) merge_partials(a, unit, lhist);
@@ -627,7 +650,8 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
   const int n = unit_len(sa.ctx_lens[unit / sa.Hkv], sa.max_ctx, sa.chunk);
   int lo, hi;
   share_range(min(sa.k, n), split, nsplit, &lo, &hi);
-  select_unit(sa, unit, L, split == 0, share, (uint32_t)lo, (uint32_t)hi);
+  // the shares of a unit all read its histogram: none clears it
+  select_unit(sa, unit, L, split == 0, share, (uint32_t)lo, (uint32_t)hi, false);
   __syncthreads();
   attn_wg<G>(at, unit, share, hi - lo, split, nsplit, lds, lds + Lds::kQOff);
 }

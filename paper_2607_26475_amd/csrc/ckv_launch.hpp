@@ -85,9 +85,29 @@ struct PipelinedLayer {
   const uint16_t* k_local;
   const uint16_t* v_local;
   float* out_spec;
+  bool hist_clean;  // the workspace's selection histograms are known clear
 };
 int pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p, const int32_t* ctx_lens,
                     int32_t k, float scale, void* ws, size_t ws_bytes, void* stream);
+
+// ckv_critical_kv_attn and ckv_corrected_attn(_lowrank: rank > 0), for
+// callers that run several calls in order on one workspace: with hist_clean
+// a pipelined call skips the clearing of the selection histograms, which a
+// selection whose histograms were counted atomically leaves clear (the
+// previous call on the same workspace layout).
+int critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                  const uint16_t* k_score, const int32_t* ctx_lens, int32_t k, float scale,
+                  const uint16_t* k_src, const uint16_t* v_src, int src_kind,
+                  const int32_t* idx_in, const uint16_t* k_buf, const uint16_t* v_buf,
+                  const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out, float* out,
+                  void* ws, size_t ws_bytes, void* stream, bool hist_clean);
+int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
+                   const uint16_t* k_score, const int32_t* ctx_lens, int32_t k, float scale,
+                   const uint16_t* k_src, const uint16_t* v_src, int src_kind, int32_t rank,
+                   const uint16_t* u_fac, const uint16_t* w_fac, const int32_t* idx_pred,
+                   const int32_t* n_pred, uint16_t* k_buf, uint16_t* v_buf, int32_t* idx_true,
+                   int32_t* n_true, int32_t* hits, int32_t* idx_next, int32_t* n_next,
+                   float* out, void* ws, size_t ws_bytes, void* stream, bool hist_clean);
 
 // Largest gather grid a caller may ask for.
 constexpr int kMaxGatherWgs = 4096;

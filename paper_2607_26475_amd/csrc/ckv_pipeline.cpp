@@ -21,9 +21,19 @@ namespace {
 // A layer that the plain entries do not cover: chunk landmarks or two tokens.
 bool special_layer(const ckv_layer& L) { return L.chunk > 1 || L.out_spec != nullptr; }
 
+// Which workspace layout a layer's selections use: consecutive layers with
+// the same layout find the selection histograms as the previous layer left
+// them (clear), so only the first of them clears.
+int layout_of(const ckv_layer& L) {
+  if (L.chunk > 1) return 1000 + L.chunk;  // the chunk problem's layout
+  if (L.out_spec) return 3;                // the decode step's layout
+  return L.idx_true ? 2 : 1;               // corrected, or the fused entry's
+}
+
 int run_special(const ckv_shape* shape, const ckv_layer& L, const int32_t* ctx_lens,
                 int32_t k, float scale, int src_kind, const uint16_t* k_buf,
-                const uint16_t* v_buf, void* ws, size_t ws_bytes, void* stream) {
+                const uint16_t* v_buf, void* ws, size_t ws_bytes, void* stream,
+                bool hist_clean) {
   ckv::PipelinedLayer p;
   p.q_att = L.q_att;
   p.q_sel = L.q_sel;
@@ -43,6 +53,7 @@ int run_special(const ckv_shape* shape, const ckv_layer& L, const int32_t* ctx_l
   p.k_local = L.k_local;
   p.v_local = L.v_local;
   p.out_spec = L.out_spec;
+  p.hist_clean = hist_clean;
   return ckv::pipelined_layer(shape, p, ctx_lens, k, scale, ws, ws_bytes, stream);
 }
 
@@ -159,13 +170,14 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
         return ckv::fail(CKV_EINVAL, "layer %d: miss correction needs the two buffers", l);
     for (int l = 0; l < num_layers; ++l) {
       const ckv_layer& L = layers[l];
+      const bool clean = l > 0 && layout_of(L) == layout_of(layers[l - 1]);
       int rc = special_layer(L)
                    ? run_special(shape, L, ctx_lens, k, scale, src_kind, nullptr, nullptr, ws,
-                                 ws_bytes, compute_stream)
-                   : ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k,
-                                          scale, L.k_src, L.v_src, src_kind, L.idx_prev,
-                                          nullptr, nullptr, L.n_sel_prev, L.idx_next,
-                                          L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
+                                 ws_bytes, compute_stream, clean)
+                   : ckv::critical_impl(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
+                                        L.k_src, L.v_src, src_kind, L.idx_prev, nullptr,
+                                        nullptr, L.n_sel_prev, L.idx_next, L.n_sel_next, L.out,
+                                        ws, ws_bytes, compute_stream, clean);
       if (rc) return rc;
     }
     return CKV_OK;
@@ -195,27 +207,26 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
         !(pipe->checks & CKV_PIPE_CHECK_NO_FILL_WAIT))
       if (hipError_t e = hipStreamWaitEvent(cs, pipe->filled[p], 0))
         return ckv::hip_fail(e, "wait for a buffer fill");
+    // the previous layer of this call on the same workspace layout left the
+    // selection histograms clear
+    const bool clean = l > 0 && layout_of(L) == layout_of(layers[l - 1]);
     int rc;
     if (special_layer(L)) {  // chunk landmarks or two tokens
       rc = run_special(shape, L, ctx_lens, k, scale, src_kind, k_buf[p], v_buf[p], ws,
-                       ws_bytes, compute_stream);
-    } else if (L.idx_true && L.lr_rank > 0) {  // misses: keys rebuilt, values fetched
-      rc = ckv_corrected_attn_lowrank(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
-                                      L.k_src, L.v_src, src_kind, L.lr_rank, L.lr_u, L.lr_w,
-                                      L.idx_prev, L.n_sel_prev, k_buf[p], v_buf[p],
-                                      L.idx_true, L.n_true, L.hits, L.idx_next,
-                                      L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
-    } else if (L.idx_true) {  // the current query's own set: misses fetched into buffer p first
-      rc = ckv_corrected_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale, L.k_src,
-                              L.v_src, src_kind, L.idx_prev, L.n_sel_prev, k_buf[p],
-                              v_buf[p], L.idx_true, L.n_true, L.hits, L.idx_next,
-                              L.n_sel_next, L.out, ws, ws_bytes, compute_stream);
+                       ws_bytes, compute_stream, clean);
+    } else if (L.idx_true) {
+      // the current query's own set: misses fetched into buffer p first, their
+      // keys rebuilt from the low-rank factors if lr_rank > 0
+      rc = ckv::corrected_impl(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
+                               L.k_src, L.v_src, src_kind, L.lr_rank > 0 ? L.lr_rank : 0,
+                               L.lr_u, L.lr_w, L.idx_prev, L.n_sel_prev, k_buf[p], v_buf[p],
+                               L.idx_true, L.n_true, L.hits, L.idx_next, L.n_sel_next, L.out,
+                               ws, ws_bytes, compute_stream, clean);
     } else {
-      rc = ckv_critical_kv_attn(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
-                                nullptr, nullptr, src_kind, nullptr, k_buf[p], v_buf[p],
-                                L.n_sel_prev,
-                                L.idx_next, L.n_sel_next, L.out, ws, ws_bytes,
-                                compute_stream);
+      rc = ckv::critical_impl(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale, nullptr,
+                              nullptr, src_kind, nullptr, k_buf[p], v_buf[p], L.n_sel_prev,
+                              L.idx_next, L.n_sel_next, L.out, ws, ws_bytes, compute_stream,
+                              clean);
     }
     if (rc) return rc;
     if (hipError_t e = hipEventRecord(pipe->freed[p], cs))
