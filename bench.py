@@ -32,7 +32,7 @@ HBM_PEAK_GBPS = 8000.0
 COUNTERS = os.path.join(ROOT, "profiles", "score_llama8b_counters.txt")
 
 
-SECTIONS = ("main", "extras", "host_link", "long128k", "dual64", "million", "cpu")
+SECTIONS = ("main", "extras", "sweep", "host_link", "long128k", "dual64", "million", "cpu")
 
 
 def log(*a):
@@ -140,8 +140,9 @@ def main() -> int:
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
     scale = float(np.float32(1.0 / math.sqrt(d)))
-    need_llama = [x for x in sections if x in ("main", "extras", "cpu")]
-    n_layers = L if ("main" in sections or "extras" in sections) else (1 if need_llama else 0)
+    need_llama = [x for x in sections if x in ("main", "extras", "sweep", "cpu")]
+    n_layers = L if any(x in sections for x in ("main", "extras", "sweep")) else (
+        1 if need_llama else 0)
 
     log(f"generating {n_layers} layers of {w.name} inputs on {torch.cuda.get_device_name(0)}")
     t0 = time.time()
@@ -219,6 +220,14 @@ def main() -> int:
             f"{pipelined_hbm['per_layer_us']}")
         result.update(chunked=chunked, pipelined_hbm=pipelined_hbm, graph=graph,
                       dual_token=dual_token)
+
+    if "sweep" in sections and len(layers) == L:
+        sweep = measure_attn_sweep(torch, ckv, layers, kv_ptrs, s, w, scale, stream)
+        log("attention sweep: " + ", ".join(
+            f"k{r['k']}: select_attn {r['select_attn_us']:.1f} us, attn {r['attn_us']:.1f} us"
+            for r in sweep["points"]) + f"; fits {sweep.get('select_attn_fit')} "
+            f"{sweep.get('attn_fit')}")
+        result["attn_sweep"] = sweep
 
     host_link = None
     if "host_link" in sections:
@@ -355,6 +364,78 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
             "ms_per_step_median": median(per_step), "ms_per_step_unstamped": ms_plain,
             "hbm_algorithmic_gbps_step": step_bytes / (ms_step * 1e-3) / 1e9,
             "kernels": per_kernel, "roofline": roofline}
+
+
+def measure_attn_sweep(torch, ckv, layers, kv_ptrs, shape, w, scale, stream,
+                       budgets=(512, 1024, 2048, 4096), reps=32):
+    """The attention's time against its bytes at the Llama-8B shape (B16, 32 q
+    / 8 KV heads, n 32768): budgets k from 512 to 4096 rows per KV head, so
+    that the selected bytes grow while the grids keep their shape.  Two
+    kernels: the same-step layer's one-launch selection and attention (over
+    the 32 layers in turn, so that no call finds its rows in a cache), and the
+    standalone attention over assembled buffers (distinct buffers totalling
+    1 GiB per budget, for the same reason).  A line through the points, time
+    = fixed + bytes / rate, splits a launch into what does not grow with the
+    bytes (launch, selection, first round trip, merge, drain) and the
+    streaming rate of the selected rows.  Dispatch-stamped kernel times."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    B, Hq, Hkv, d = w.batch, w.q_heads, w.kv_heads, w.head_dim
+    L = len(layers)
+    points = []
+    i32 = dict(dtype=torch.int32, device=dev)
+    for k in budgets:
+        ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+        idx = [torch.empty((B, Hkv, k), **i32) for _ in range(L)]
+        nsel = [torch.empty((B, Hkv), **i32) for _ in range(L)]
+        out = torch.empty((B, Hq, d), device=dev)
+
+        def same_step(l):
+            kp, vp = kv_ptrs[l]
+            ckv.critical_kv_attn(shape, layers[l]["q"], None, kp, layers[l]["ctx_lens"], k,
+                                 scale, kp, vp, ckv.SRC_DEVICE, None, None, None, idx[l],
+                                 nsel[l], out, ws, stream)
+        for l in range(L):
+            same_step(l)
+        row_bytes = B * Hkv * k * 2 * d * 2
+        nbuf = max(2, min(L, (1 << 30) // row_bytes))
+        bufs = []
+        for l in range(nbuf):
+            kb = torch.empty((B, Hkv, k, d), dtype=torch.bfloat16, device=dev)
+            vb = torch.empty_like(kb)
+            ckv.gather_kv(shape, kv_ptrs[l][0], kv_ptrs[l][1], ckv.SRC_DEVICE, idx[l], nsel[l],
+                          k, kb, vb, stream)
+            bufs.append((kb, vb))
+        wsa = ckv.workspace(shape, k, ckv.ENTRY_SPARSE_DECODE_ATTN)
+        torch.cuda.synchronize()
+        ckv.profile_begin(["select_attn", "attn", "combine"])
+        for r in range(reps):
+            same_step(r % L)
+        for r in range(reps):
+            kb, vb = bufs[r % nbuf]
+            ckv.sparse_decode_attn(shape, layers[r % L]["q"], kb, vb, nsel[r % nbuf], k, scale,
+                                   out, wsa, stream)
+        st = ckv.profile_end()
+        avg = {kname: 1e3 * tot / c for kname, (c, tot, _) in st.items()}
+        points.append({"k": k, "row_bytes": row_bytes, "buffers": nbuf,
+                       "select_attn_us": avg.get("select_attn", float("nan")),
+                       "attn_us": avg.get("attn", float("nan")),
+                       "combine_launches_us": avg.get("combine", float("nan"))})
+        del ws, idx, nsel, out, bufs, wsa
+        torch.cuda.empty_cache()
+    res = {"points": points,
+           "workload": "Llama-8B shape (B16, 32 q / 8 KV heads, head_dim 128, n 32768), "
+                       f"budgets k {list(budgets)}; the same-step calls cycle over the {L} "
+                       "layers, the standalone attention over distinct buffers of 1 GiB in all"}
+    x = np.array([p["row_bytes"] for p in points], dtype=np.float64)
+    for key in ("select_attn_us", "attn_us"):
+        y = np.array([p[key] for p in points])
+        if np.all(np.isfinite(y)):
+            slope, icpt = np.polyfit(x, y, 1)
+            res[key.replace("_us", "_fit")] = {
+                "fixed_us": icpt, "marginal_GBps": 1e-3 / slope if slope > 0 else None,
+                "marginal_frac_of_peak": (1e-3 / slope) / HBM_PEAK_GBPS if slope > 0 else None}
+    return res
 
 
 def measure_host_link(torch, ckv, dev):

@@ -747,6 +747,23 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
   }
   if (a.chunks <= kMaxChunks) {
     const int nc = a.chunks;
+    // With at most kMergeChunks partials, every thread's weighted sums are
+    // loaded first, with the (max, weight sum) pairs, so the merge waits for
+    // one round trip: unconditional loads of clamped chunks and outputs,
+    // used only where valid.
+    constexpr int kPer = (G * kD + kAttnThreads - 1) / kAttnThreads;
+    const bool pre = nc <= kMergeChunks;
+    float opre[kPer][kMergeChunks];
+    if (pre) {
+#pragma unroll
+      for (int r = 0; r < kPer; ++r) {
+        const int o = min(tid + r * kAttnThreads, G * kD - 1);
+        const int g = o / kD, c = o - g * kD;
+#pragma unroll
+        for (int ch = 0; ch < kMergeChunks; ++ch)
+          opre[r][ch] = pu[(min(ch, nc - 1) * G + g) * kPartStride + 4 + c];
+      }
+    }
     for (int i = tid; i < nc * G; i += kAttnThreads) {
       const int ch = i / G, g = i - ch * G;
       s_m[g][ch] = pu[(ch * G + g) * kPartStride];
@@ -772,12 +789,20 @@ __global__ __launch_bounds__(kAttnThreads) void k_combine(AttnArgs a) {
       s_inv[g] = L > 0.f ? 1.f / L : 0.f;
     }
     __syncthreads();
-    for (int o = tid; o < G * kD; o += kAttnThreads) {
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int o = tid + r * kAttnThreads;
+      if (o >= G * kD) break;
       const int g = o / kD, c = o - g * kD;
       float O = 0.f;  // empty chunks carry weight 0 and zero sums
-#pragma unroll 8
-      for (int ch = 0; ch < nc; ++ch)
-        O = fmaf(s_m[g][ch], pu[(ch * G + g) * kPartStride + 4 + c], O);
+      if (pre) {
+#pragma unroll
+        for (int ch = 0; ch < kMergeChunks; ++ch)
+          if (ch < nc) O = fmaf(s_m[g][ch], opre[r][ch], O);
+      } else {
+        for (int ch = 0; ch < nc; ++ch)
+          O = fmaf(s_m[g][ch], pu[(ch * G + g) * kPartStride + 4 + c], O);
+      }
       if (dual)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
