@@ -294,16 +294,25 @@ SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* sc
   return a;
 }
 
+// Scoring arguments; with sel set, the pass counts the first digit into that
+// selection's histograms, and a pipelined launch with enough work may take
+// it as claims from the selection's claim counter (unit 0's control word
+// kCtrlClaim, cleared with the histograms; the pass leaves it zero), unless
+// a caller switches the pass to per-workgroup histograms.
 ScoreArgs score_args(const Dims& d, const Layout& L, const uint16_t* q,
                      const uint16_t* keys, const int32_t* ctx_lens, float scale,
-                     float* scores, uint32_t* hist, uint32_t* coarse) {
+                     float* scores, const SelectArgs* sel) {
   ScoreArgs a;
   a.q = q;
   a.keys = keys;
   a.ctx_lens = ctx_lens;
   a.scores = scores;
-  a.hist = hist;
-  a.coarse = coarse;
+  a.hist = sel ? sel->hist : nullptr;
+  a.coarse = sel ? sel->coarse : nullptr;
+  // claim numbers (and the nwg failing ones past them) must fit in 32 bits
+  const int64_t claims =
+      (int64_t)d.U * (((d.max_ctx + kStageRows - 1) / kStageRows + kClaimGroups - 1) / kClaimGroups);
+  a.claim = sel && claims + kMaxScoreWgs < ((int64_t)1 << 31) ? sel->ctrl + kCtrlClaim : nullptr;
   a.key_stride = d.key_stride;
   a.scale = scale;
   a.Hq = d.Hq;
@@ -405,6 +414,13 @@ int select_attn_splits(const Dims& d, int32_t k, const Layout& L) {
   return S;
 }
 
+// Attention of `a` over its set, then the merge of its chunk partials.
+int run_attention(const AttnArgs& a, const Dims& d, bool indexed, hipStream_t s) {
+  CKV_TRY_HIP(launch_attn(a, d.G, indexed, d.U, s), "attention launch");
+  CKV_TRY_HIP(launch_combine(a, d.G, d.U, s), "combine launch");
+  return CKV_OK;
+}
+
 int check_chunk(int32_t chunk, int32_t k) {
   if (chunk < 1 || chunk > (1 << 20)) return fail(CKV_ESHAPE, "chunk %d outside [1, 2^20]", chunk);
   if (k % chunk) return fail(CKV_ESHAPE, "k %d is not a multiple of chunk %d", k, chunk);
@@ -428,8 +444,7 @@ int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
   float* scores = at<float>(ws, Lc.scores);
   SelectArgs sa = select_args(dc, Lc, ws, scores, ctx_lens, kc, chunk_idx, n_chunks);
   sa.chunk = chunk;
-  ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, sa.hist,
-                            sa.coarse);
+  ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, &sa);
   sc.chunk = chunk;
   const int nwg = score_blocks(sc, d.G, ScoreKind::kHist);
   if (use_partials(dc, Lc, nwg))
@@ -524,7 +539,7 @@ int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
   float* scores = at<float>(ws, Ls.scores);
   SelectArgs sa = select_args(ds, Ls, ws, scores, ctx_lens, ks, sidx, sn);
   sa.chunk = chunked ? p.chunk : 1;
-  ScoreArgs sc = score_args(ds, Ls, q_sel, keys, ctx_lens, scale, scores, sa.hist, sa.coarse);
+  ScoreArgs sc = score_args(ds, Ls, q_sel, keys, ctx_lens, scale, scores, &sa);
   sc.chunk = sa.chunk;
   AttnArgs at_ = assembled ? attn_args(d, L, ws, q_att, p.k_buf, p.v_buf, nullptr, p.n_sel_in,
                                        kD, k, scale, p.out)
@@ -647,7 +662,7 @@ int ckv_score_keys(const ckv_shape* shape, const uint16_t* q, const uint16_t* k_
   if (d.U == 0) return CKV_OK;
   Layout L = make_layout(d, 1, 0);
   if ((rc = check_grid(d, L))) return rc;
-  ScoreArgs a = score_args(d, L, q, k_score, ctx_lens, scale, scores, nullptr, nullptr);
+  ScoreArgs a = score_args(d, L, q, k_score, ctx_lens, scale, scores, nullptr);
   CKV_TRY_HIP(launch_score(a, d.G, false, score_blocks(a, d.G, ScoreKind::kPlain),
                            (hipStream_t)stream),
               "score launch");
@@ -703,9 +718,7 @@ int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
   if (d.U == 0) return CKV_OK;
   hipStream_t s = (hipStream_t)stream;
   AttnArgs a = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel, kD, k, scale, out);
-  CKV_TRY_HIP(launch_attn(a, d.G, false, d.U, s), "attention launch");
-  CKV_TRY_HIP(launch_combine(a, d.G, d.U, s), "combine launch");
-  return CKV_OK;
+  return run_attention(a, d, false, s);
 }
 
 int ckv_critical_kv_attn(const ckv_shape* shape, const uint16_t* q_att,
@@ -763,7 +776,7 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
   hipStream_t s = (hipStream_t)stream;
   float* scores = at<float>(ws, L.scores);
   SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
-  ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, sa.hist, sa.coarse);
+  ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, &sa);
   const bool pipelined = assembled || in_place;
   const int nwg = score_blocks(
       sc, d.G, !pipelined ? ScoreKind::kHist : in_place ? ScoreKind::kDualIndexed : ScoreKind::kDual);
@@ -791,8 +804,7 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
       if (S > 1) CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
     } else {
       if ((rc = run_select_tail(sa, d.U, s))) return rc;
-      CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
-      CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+      if ((rc = run_attention(at_, d, true, s))) return rc;
     }
   }
   return CKV_OK;
@@ -948,9 +960,7 @@ int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q
   // the partials live past everything the chunk selection used
   AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, rows, n_rows, d.kv_stride, k, scale,
                            out);
-  CKV_TRY_HIP(launch_attn(at_, d.G, true, d.U, s), "attention launch");
-  CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
-  return CKV_OK;
+  return run_attention(at_, d, true, s);
 }
 
 }  // extern "C"
@@ -1001,13 +1011,16 @@ int ckv::corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uin
   float* scores = at<float>(ws, L.scores);
   // 1. the current token's own selection
   SelectArgs s1 = select_args(d, L, ws, scores, ctx_lens, k, idx_true, n_true);
-  ScoreArgs c1 = score_args(d, L, q_att, k_score, ctx_lens, scale, scores, s1.hist, s1.coarse);
+  ScoreArgs c1 = score_args(d, L, q_att, k_score, ctx_lens, scale, scores, &s1);
   // the next step's selection (4. below) is scored by the dual kernel
   SelectArgs s2 = select_args(d, L, ws, scores, ctx_lens, k, idx_next, n_next);
   s2.hist = at<uint32_t>(ws, L.hist2);
   s2.coarse = at<uint32_t>(ws, L.coarse2);
   s2.ctrl = at<uint32_t>(ws, L.ctrl2);
-  ScoreArgs c2 = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, s2.hist, s2.coarse);
+  ScoreArgs c2 = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, &s2);
+  // static ranges: beside this call's own gather of the misses, claims made
+  // the long-context loop slower (137.2 against 136.7 ms per step)
+  c2.claim = nullptr;
   const int nwg1 = score_blocks(c1, d.G, ScoreKind::kHist);
   const int nwg2 = score_blocks(c2, d.G, ScoreKind::kDualIndexed);
   if (use_partials(d, L, nwg1) && use_partials(d, L, nwg2)) {

@@ -319,11 +319,18 @@ __host__ __device__ __forceinline__ void share_range(int m, int split, int nspli
   *hi = min(*lo + per, m);
 }
 
+// Row source of attn_wg: the share's positions in LDS.
+struct LdsRows {
+  const int32_t* pos;
+  __device__ __forceinline__ int operator()(int i) const { return pos[i]; }
+};
+
 // All kFinishThreads threads call this.  stages: WgAttnLds<G>::kStages
-// dwords, qlds: kQ dwords (both free on entry); pos: the share's positions.
-template <int G>
-__device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, const int32_t* pos,
-                                        int nrows, int split, int nsplit, uint32_t* stages,
+// dwords, qlds: kQ dwords (both free on entry); pos(i): the source row of
+// the share's row i, clamped to [0, a.max_ctx).
+template <int G, class Rows>
+__device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, int nrows,
+                                        int split, int nsplit, uint32_t* stages,
                                         uint32_t* qlds) {
   using Lds = WgAttnLds<G>;
   static_assert(G <= 8, "16 waves' states of at most 8 heads fit in the stages");
@@ -351,7 +358,7 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, const int32
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
       const int i = min(16 * blk + 4 * it + lrow, nrows - 1);
-      int p = pos[i];
+      int p = pos(i);
       p = p < 0 ? 0 : (p >= a.max_ctx ? a.max_ctx - 1 : p);
       const int64_t off = ubase + (int64_t)p * stride;
       kr[it] = ld16(a.k_rows + off);

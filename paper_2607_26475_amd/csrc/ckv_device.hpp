@@ -17,6 +17,8 @@ constexpr int kStageRows = 32;     // key rows staged per wave per step
 constexpr int kStageRowDwords = 68;  // 256-byte row + 16-byte pad (bank spread)
 constexpr int kStageDwords = kStageRows * kStageRowDwords;
 constexpr int kFlushGroups = 64;   // groups of scores held per wave in LDS
+constexpr int kClaimGroups = 64;   // groups per claim of the dynamic scoring pass
+constexpr int kMinClaimsPerWg = 4; // claims per workgroup from which a pass takes claims
 constexpr int kScoreLdsDwords = 4 * kStageDwords + 4 * kFlushGroups * kStageRows;
 
 // Selection: the first radix digit is the top 11 bits of the order key; a
@@ -25,7 +27,8 @@ constexpr int kScoreLdsDwords = 4 * kStageDwords + 4 * kFlushGroups * kStageRows
 constexpr int kHistBits = 11;
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kCoarseBins = 64;
-constexpr int kCtrlWords = 4;      // per unit: above, cand, digit-1 bin, spare
+constexpr int kCtrlWords = 4;      // per unit: above, cand, digit-1 bin, and (unit 0
+constexpr int kCtrlClaim = 3;      //   only) the scoring pass's claim counter
 constexpr int kFilterThreads = 256;
 constexpr int kFilterTile = 4096;  // positions per filter workgroup
 constexpr int kFinishThreads = 1024;
@@ -77,6 +80,9 @@ struct ScoreArgs {
   uint32_t* coarse;         // [U][kCoarseBins]
   uint32_t* hist_part;      // non-null: per-workgroup histograms instead,
                             //   [U + kMaxScoreWgs][kHistBins], stored not added
+  uint32_t* claim;          // pipelined launches with added histograms: workgroups
+                            //   may take claims of kClaimGroups groups from this
+                            //   counter, which is zero before the launch and after it
   int64_t key_stride;
   float scale;
   int Hq, Hkv, max_ctx, units;

@@ -33,6 +33,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a) {
   score_range<G, HIST>(a, blockIdx.x, gridDim.x, lds_hist, lds_stage);
 }
 
+
 // The same pass over chunk landmarks (a kernel of its own only so that
 // traces and profiles keep the two workloads apart).
 template <int G>
@@ -653,7 +654,7 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
   // the shares of a unit all read its histogram: none clears it
   select_unit(sa, unit, L, split == 0, share, (uint32_t)lo, (uint32_t)hi, false);
   __syncthreads();
-  attn_wg<G>(at, unit, share, hi - lo, split, nsplit, lds, lds + Lds::kQOff);
+  attn_wg<G>(at, unit, LdsRows{share}, hi - lo, split, nsplit, lds, lds + Lds::kQOff);
 }
 
 // ---- attention -------------------------------------------------------------
@@ -665,23 +666,36 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(AttnArgs a) {
   attn_chunk<G, INDEXED>(a, unit, chunk, lds);
 }
 
+// The scoring role of a pipelined launch: claims from a.claim (CLAIMS),
+// else the static ranges.  They are separate kernels so that each keeps its
+// own register allocation.
+template <int G, bool CLAIMS>
+__device__ __forceinline__ void score_role(const ScoreArgs& a, int wg, int nwg, uint32_t* lds_hist,
+                                           uint32_t* lds_stage, uint32_t* lds_claim) {
+  if constexpr (CLAIMS)
+    score_claims<G>(a, nwg, lds_hist, lds_stage, lds_claim);
+  else
+    score_range<G, true>(a, wg, nwg, lds_hist, lds_stage);
+}
+
 // One launch, two roles (pipelined decode): the first attn_blocks workgroups
 // attend with q_att over the buffer assembled for this step, the rest score
 // the context with q_sel for the next step's selection.
-template <int G, bool INDEXED>
+template <int G, bool INDEXED, bool CLAIMS>
 __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc,
                                                       int attn_blocks) {
   static_assert(kAttnThreads == kScoreThreads, "roles share the block size");
   constexpr int kA = AttnLds<G>::kFloats;
   constexpr int kS = kHistBins + kScoreLdsDwords;
   __shared__ __attribute__((aligned(16))) float lds[kA > kS ? kA : kS];
+  __shared__ uint32_t lds_claim[2];
   if ((int)blockIdx.x < attn_blocks) {
     const int unit = blockIdx.x / at.chunks;
     attn_chunk<G, INDEXED>(at, unit, blockIdx.x - unit * at.chunks, lds);
   } else {
     uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
-    score_range<G, true>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks,
-                         l32 + kScoreLdsDwords, l32);
+    score_role<G, CLAIMS>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks, l32 + kScoreLdsDwords,
+                  l32, lds_claim);
   }
 }
 
@@ -689,19 +703,20 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
 // role has the 2G head rows of the current and the speculative token (the
 // merge kernel adds their own rows under the causal mask), the scoring role
 // the speculative token's G heads.
-template <int G, bool INDEXED>
+template <int G, bool INDEXED, bool CLAIMS>
 __global__ __launch_bounds__(kAttnThreads) void k_dual2(AttnArgs at, ScoreArgs sc,
                                                        int attn_blocks) {
   constexpr int kA = AttnLds<2 * G>::kFloats;
   constexpr int kS = kHistBins + kScoreLdsDwords;
   __shared__ __attribute__((aligned(16))) float lds[kA > kS ? kA : kS];
+  __shared__ uint32_t lds_claim[2];
   if ((int)blockIdx.x < attn_blocks) {
     const int unit = blockIdx.x / at.chunks;
     attn_chunk<2 * G, INDEXED>(at, unit, blockIdx.x - unit * at.chunks, lds);
   } else {
     uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
-    score_range<G, true>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks,
-                         l32 + kScoreLdsDwords, l32);
+    score_role<G, CLAIMS>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks, l32 + kScoreLdsDwords,
+                  l32, lds_claim);
   }
 }
 
@@ -1198,22 +1213,35 @@ int device_cus() {
   return cus[dev];
 }
 
+// The kernel whose residency sets a scoring grid (the claim variants of the
+// pipelined kernels have the same block size and LDS, so the same residency).
 template <int G>
 static const void* score_kernel(ScoreKind kind, int chunk) {
   switch (kind) {
     case ScoreKind::kPlain: return (const void*)k_score<G, false>;
     case ScoreKind::kHist:
       return chunk > 1 ? (const void*)k_score_chunks<G> : (const void*)k_score<G, true>;
-    case ScoreKind::kDual: return (const void*)k_dual<G, false>;
-    case ScoreKind::kDualIndexed: return (const void*)k_dual<G, true>;
+    case ScoreKind::kDual: return (const void*)k_dual<G, false, false>;
+    case ScoreKind::kDualIndexed: return (const void*)k_dual<G, true, false>;
     case ScoreKind::kDual2:
-      if constexpr (G <= 8) return (const void*)k_dual2<G, false>;
+      if constexpr (G <= 8) return (const void*)k_dual2<G, false, false>;
       return nullptr;
     case ScoreKind::kDual2Indexed:
-      if constexpr (G <= 8) return (const void*)k_dual2<G, true>;
+      if constexpr (G <= 8) return (const void*)k_dual2<G, true, false>;
       return nullptr;
   }
   return nullptr;
+}
+
+// Whether a pipelined launch's scoring grid of nwg workgroups takes claims:
+// when it adds its histograms, has a claim counter, and has at least
+// kMinClaimsPerWg claims per workgroup (each workgroup holds two claims
+// ahead, which idles workgroups at the end of a pass with fewer).
+static bool use_claims(const ScoreArgs& a, int nwg) {
+  if (!a.claim || a.hist_part) return false;
+  const int64_t gu = (a.max_ctx + kStageRows - 1) / kStageRows;
+  const int64_t claims = (int64_t)a.units * ((gu + kClaimGroups - 1) / kClaimGroups);
+  return claims >= (int64_t)kMinClaimsPerWg * nwg;
 }
 
 int score_blocks(const ScoreArgs& a, int G, ScoreKind kind) {
@@ -1309,8 +1337,12 @@ hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
 template <int G, bool INDEXED>
 static void launch_dual_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks, int nwg,
                           hipStream_t s) {
-  launch_kernel(CKV_K_DUAL, k_dual<G, INDEXED>, dim3(attn_blocks + nwg), dim3(kAttnThreads), s,
-                at, sc, attn_blocks);
+  if (use_claims(sc, nwg))
+    launch_kernel(CKV_K_DUAL, k_dual<G, INDEXED, true>, dim3(attn_blocks + nwg),
+                  dim3(kAttnThreads), s, at, sc, attn_blocks);
+  else
+    launch_kernel(CKV_K_DUAL, k_dual<G, INDEXED, false>, dim3(attn_blocks + nwg),
+                  dim3(kAttnThreads), s, at, sc, attn_blocks);
 }
 
 template <bool INDEXED>
@@ -1330,8 +1362,12 @@ static hipError_t launch_dual_i(const AttnArgs& at, const ScoreArgs& sc, int G,
 template <int G, bool INDEXED>
 static void launch_dual2_g(const AttnArgs& at, const ScoreArgs& sc, int attn_blocks, int nwg,
                            hipStream_t s) {
-  launch_kernel(CKV_K_DUAL, k_dual2<G, INDEXED>, dim3(attn_blocks + nwg), dim3(kAttnThreads),
-                s, at, sc, attn_blocks);
+  if (use_claims(sc, nwg))
+    launch_kernel(CKV_K_DUAL, k_dual2<G, INDEXED, true>, dim3(attn_blocks + nwg),
+                  dim3(kAttnThreads), s, at, sc, attn_blocks);
+  else
+    launch_kernel(CKV_K_DUAL, k_dual2<G, INDEXED, false>, dim3(attn_blocks + nwg),
+                  dim3(kAttnThreads), s, at, sc, attn_blocks);
 }
 
 template <bool INDEXED>

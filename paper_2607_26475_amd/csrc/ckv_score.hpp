@@ -57,6 +57,59 @@ __device__ __forceinline__ void store_zero_hist(uint32_t* slot) {
     *reinterpret_cast<uint4*>(slot + i) = make_uint4(0u, 0u, 0u, 0u);
 }
 
+// Scores of one staged group (kStageRows keys of one unit starting at row
+// jb) into out[0, kStageRows): the MFMA products with the G query rows, the
+// maximum over the heads, the scale; rows at or past n get -inf and are not
+// counted.  If HIST, counts the first radix digit of the others in lds_hist.
+template <int G, bool HIST>
+__device__ __forceinline__ void score_group(const uint32_t* stage, const bf16x8* qa, int jb,
+                                            int n, float scale, uint32_t* lds_hist,
+                                            float* out) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, kg = lane >> 4;
+#pragma unroll
+  for (int u = 0; u < kStageRows / 16; ++u) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const uint4 kv = *reinterpret_cast<const uint4*>(
+          stage + (16 * u + r16) * kStageRowDwords + 4 * (4 * t + kg));
+      acc = mfma_16x16x32(qa[t], as_bf16x8(kv), acc);
+    }
+    float sc = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (4 * kg + i < G) sc = fmaxf(sc, acc[i]);
+    if (G > 4) sc = fmaxf(sc, __shfl_xor(sc, 16));
+    if (G > 8) sc = fmaxf(sc, __shfl_xor(sc, 32));
+    sc *= scale;
+    const int j = jb + 16 * u + lane;
+    if (lane < 16) {
+      if (j < n) {
+        if (HIST) atomicAdd(&lds_hist[order_key(sc) >> (32 - kHistBits)], 1u);
+      } else {
+        sc = -INFINITY;
+      }
+      out[16 * u + lane] = sc;
+    }
+  }
+}
+
+// The G query rows of a unit as MFMA A operands (rows past G are zero).
+template <int G>
+__device__ __forceinline__ void load_query(const ScoreArgs& a, int unit, bf16x8* qa) {
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+  const uint16_t* qrow = a.q + ((int64_t)b * a.Hq + (int64_t)h * G + r16) * kD + 8 * kg;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (r16 < G) v = ld16(qrow + 32 * t);
+    qa[t] = as_bf16x8(v);
+  }
+}
+
 // Scores a balanced share of the whole batch: the positions of every unit are
 // cut into groups of kStageRows keys, the groups of all units are numbered
 // unit-major, and workgroup `wg` of `nwg` takes the contiguous range
@@ -91,7 +144,6 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
                                             uint32_t* lds_stage) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int r16 = lane & 15, kg = lane >> 4;
   const int lrow = lane >> 4, lchunk = lane & 15;
   constexpr int kLoads = kStageRows / 4;  // 4 rows per load instruction
   const int64_t gpu_groups = (a.max_ctx + kStageRows - 1) / kStageRows;  // per unit
@@ -105,8 +157,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
     const int unit = (int)(seg / gpu_groups);
     const int64_t ubase = (int64_t)unit * gpu_groups;
     const int64_t seg_end = min(g1, ubase + gpu_groups);
-    const int b = unit / a.Hkv, h = unit - b * a.Hkv;
-    const int n = unit_len(a.ctx_lens[b], a.max_ctx, a.chunk);
+    const int n = unit_len(a.ctx_lens[unit / a.Hkv], a.max_ctx, a.chunk);
     float* srow = a.scores + (int64_t)unit * a.max_ctx;
     // groups [ubase + first_empty, ...) hold no position below n_b
     const int64_t valid_end = min(seg_end, ubase + (n + kStageRows - 1) / kStageRows);
@@ -120,16 +171,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
         __syncthreads();
       }
       bf16x8 qa[4];
-      {
-        const uint16_t* qrow =
-            a.q + ((int64_t)b * a.Hq + (int64_t)h * G + r16) * kD + 8 * kg;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          uint4 v = make_uint4(0u, 0u, 0u, 0u);
-          if (r16 < G) v = ld16(qrow + 32 * t);
-          qa[t] = as_bf16x8(v);
-        }
-      }
+      load_query<G>(a, unit, qa);
       const uint16_t* kunit = a.keys + (int64_t)unit * a.max_ctx * a.key_stride;
       // Rows at or past n_b load row n_b - 1 instead (their scores are
       // replaced by -inf): lane-conditional loads would make the compiler
@@ -183,33 +225,8 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
               cur[i];
         if (gg + 4 < w1) load_group(gg + 4, nxt);
         __builtin_amdgcn_wave_barrier();
-        const int jb = (int)(gg - ubase) * kStageRows;
-#pragma unroll
-        for (int u = 0; u < kStageRows / 16; ++u) {
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const uint4 kv = *reinterpret_cast<const uint4*>(
-                stage + (16 * u + r16) * kStageRowDwords + 4 * (4 * t + kg));
-            acc = mfma_16x16x32(qa[t], as_bf16x8(kv), acc);
-          }
-          float sc = -INFINITY;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (4 * kg + i < G) sc = fmaxf(sc, acc[i]);
-          if (G > 4) sc = fmaxf(sc, __shfl_xor(sc, 16));
-          if (G > 8) sc = fmaxf(sc, __shfl_xor(sc, 32));
-          sc *= a.scale;
-          const int j = jb + 16 * u + lane;
-          if (lane < 16) {
-            if (j < n) {
-              if (HIST) atomicAdd(&lds_hist[order_key(sc) >> (32 - kHistBits)], 1u);
-            } else {
-              sc = -INFINITY;
-            }
-            sbuf[nb * kStageRows + 16 * u + lane] = sc;
-          }
-        }
+        score_group<G, HIST>(stage, qa, (int)(gg - ubase) * kStageRows, n, a.scale, lds_hist,
+                             sbuf + nb * kStageRows);
         if (++nb == kFlushGroups) {
           flush(first, nb);
           first = gg + 4;
@@ -233,6 +250,201 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
       store_zero_hist(a.hist_part + ((int64_t)unit + wg) * kHistBins);
     }
     seg = seg_end;
+  }
+}
+
+// The same pass with dynamic work distribution, for the added histograms
+// of the pipelined attend-and-score launch (a.claim set, a.hist_part null).
+// The groups of each unit are cut into claims of kClaimGroups; workgroups
+// take claims in increasing order from the counter a.claim, so a workgroup
+// on a CU slowed by other work (the zero-copy gather running beside the
+// pass) takes fewer of them and the pass is not held up by its slowest CUs.
+// Within a claim the four waves take its groups round-robin as above.
+//
+// Thread 0 takes claims two ahead of the one being scored, at the start of
+// each claim, and passes them through a two-entry LDS ring (one barrier per
+// claim), so each wave knows the next claim while it scores the current one
+// and prefetches that claim's first group across the boundary.  A
+// workgroup thus holds up to two claims it has not started, which leaves
+// workgroups idle at the end unless there are several claims per workgroup:
+// the host uses claims from four per workgroup.  (Taking the next claim
+// later, two rounds before the current claim's end, made the
+// million-token loop's gather beside the pass slower.)  Each workgroup takes
+// exactly one claim at or past the total; those take values total ..
+// total + nwg - 1, and the workgroup that gets the last one resets the
+// counter, so it is zero again when the launch ends.  A wave's scores stay
+// in its LDS buffer for up to kFlushGroups / (kClaimGroups / 4) claims
+// before one flush writes them, each claim's groups to its own unit's row.
+// The LDS histogram counts one unit at a time and is added to that unit's
+// histogram when the workgroup's claims move to another unit (claims
+// increase, so once per unit) and at the end.  lds_claim: two words.  Must
+// be called by all kScoreThreads threads.
+template <int G>
+__device__ __forceinline__ void score_claims(const ScoreArgs& a, int nwg, uint32_t* lds_hist,
+                                             uint32_t* lds_stage, uint32_t* lds_claim) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lrow = lane >> 4, lchunk = lane & 15;
+  constexpr int kLoads = kStageRows / 4;
+  constexpr int kPerWave = kClaimGroups / 4;       // a wave's groups of one claim
+  constexpr int kRecs = kFlushGroups / kPerWave;   // claims per score flush
+  static_assert(kClaimGroups % 4 == 0 && kFlushGroups % kPerWave == 0, "claim layout");
+  const int gpu_groups = (a.max_ctx + kStageRows - 1) / kStageRows;  // per unit
+  const int cpu = (gpu_groups + kClaimGroups - 1) / kClaimGroups;     // claims per unit
+  const uint32_t total = (uint32_t)a.units * (uint32_t)cpu;
+  uint32_t* stage = lds_stage + wave * kStageDwords;
+  float* sbuf = reinterpret_cast<float*>(lds_stage + 4 * kStageDwords) +
+                wave * kFlushGroups * kStageRows;
+
+  // thread 0: a new claim; the one that makes the counter reach total + nwg
+  // is the last of the launch and resets it
+  auto take = [&]() -> uint32_t {
+    const uint32_t c = atomicAdd(a.claim, 1u);
+    if (c == total + (uint32_t)nwg - 1u) atomicExch(a.claim, 0u);
+    return c;
+  };
+  // a claim's unit, valid length, and groups [g0, g1) of which [g0, v1) lie below n_b
+  struct Geo {
+    int unit, n, g0, g1, v1;
+  };
+  auto geo = [&](uint32_t c) {
+    Geo r;
+    r.unit = (int)(c / (uint32_t)cpu);
+    r.g0 = (int)(c - (uint32_t)r.unit * (uint32_t)cpu) * kClaimGroups;
+    r.g1 = min(r.g0 + kClaimGroups, gpu_groups);
+    r.n = unit_len(a.ctx_lens[r.unit / a.Hkv], a.max_ctx, a.chunk);
+    r.v1 = max(r.g0, min(r.g1, (r.n + kStageRows - 1) / kStageRows));
+    return r;
+  };
+  auto load_group = [&](const Geo& c, int g, uint4* v) {
+    const uint16_t* kunit = a.keys + (int64_t)c.unit * a.max_ctx * a.key_stride;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int j = min(g * kStageRows + 4 * i + lrow, c.n - 1);
+      v[i] = ld16_nt(kunit + (int64_t)j * a.key_stride + 8 * lchunk);
+    }
+  };
+
+  // buffered claims of this wave: unit, first group, groups scored
+  int rec_unit[kRecs], rec_g0[kRecs], rec_nr[kRecs];
+  int nrec = 0;
+  auto flush = [&]() {
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int q = 0; q < kRecs; ++q) {
+      if (q < nrec) {
+        float* srow = a.scores + (int64_t)rec_unit[q] * a.max_ctx;
+        const float* src = sbuf + q * kPerWave * kStageRows;
+        const int count = rec_nr[q] * kStageRows;
+        if ((a.max_ctx & 3) == 0) {
+          for (int c = 4 * lane; c < count; c += 256) {
+            const float4 v = *reinterpret_cast<const float4*>(src + c);
+            const int j = (rec_g0[q] + wave + 4 * (c / kStageRows)) * kStageRows + c % kStageRows;
+            if (j + 3 < a.max_ctx) {
+              *reinterpret_cast<float4*>(srow + j) = v;
+            } else {
+              if (j < a.max_ctx) srow[j] = v.x;
+              if (j + 1 < a.max_ctx) srow[j + 1] = v.y;
+              if (j + 2 < a.max_ctx) srow[j + 2] = v.z;
+            }
+          }
+        } else {
+          for (int c = lane; c < count; c += 64) {
+            const int j = (rec_g0[q] + wave + 4 * (c / kStageRows)) * kStageRows + c % kStageRows;
+            if (j < a.max_ctx) srow[j] = src[c];
+          }
+        }
+      }
+    }
+    nrec = 0;
+    __builtin_amdgcn_wave_barrier();
+  };
+
+  if (tid == 0) {  // claims 0 and 1
+    const uint32_t c0 = take();
+    lds_claim[0] = c0;
+    lds_claim[1] = c0 < total ? take() : c0;
+  }
+  __syncthreads();
+  uint32_t cur = lds_claim[0], nxt = lds_claim[1];
+  int cur_unit = -1;
+  bf16x8 qa[4];
+  uint4 cbuf[kLoads], nbuf[kLoads];
+  bool have = false;  // cbuf holds this wave's first group of the current claim
+#pragma unroll 1
+  for (int i = 0; cur < total; ++i) {  // cur is uniform over the workgroup
+    const Geo c = geo(cur);
+    uint32_t ahead = 0;  // claim i + 2 (none once a claim has failed)
+    if (tid == 0) ahead = nxt < total ? take() : nxt;
+    if (c.unit != cur_unit) {
+      if (cur_unit >= 0) {
+        __syncthreads();
+        flush_hist(lds_hist, a.hist + (int64_t)cur_unit * kHistBins,
+                   a.coarse + (int64_t)cur_unit * kCoarseBins);
+        __syncthreads();
+      }
+      for (int t = tid; t < kHistBins; t += kScoreThreads) lds_hist[t] = 0u;
+      __syncthreads();
+      load_query<G>(a, c.unit, qa);
+      cur_unit = c.unit;
+    }
+    // groups of the claim at or past n_b hold -inf only
+    for (int g = c.v1; g < c.g1; ++g) {
+      const int j = g * kStageRows + (tid & (kStageRows - 1));
+      if (tid < kStageRows && j < a.max_ctx)
+        a.scores[(int64_t)c.unit * a.max_ctx + j] = -INFINITY;
+    }
+    const int w0 = c.g0 + wave;
+    if (!have && w0 < c.v1) load_group(c, w0, cbuf);
+    have = false;
+    int r = 0;
+#pragma unroll 1
+    for (int g = w0; g < c.v1; g += 4, ++r) {
+#pragma unroll
+      for (int k = 0; k < kLoads; ++k)
+        *reinterpret_cast<uint4*>(stage + (4 * k + lrow) * kStageRowDwords + 4 * lchunk) =
+            cbuf[k];
+      bool pf = false;
+      if (g + 4 < c.v1) {
+        load_group(c, g + 4, nbuf);
+        pf = true;
+      } else if (nxt < total) {  // the wave's last group: prefetch across the claim
+        const Geo d = geo(nxt);
+        if (d.g0 + wave < d.v1) {
+          load_group(d, d.g0 + wave, nbuf);
+          pf = true;
+          have = true;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      score_group<G, true>(stage, qa, g * kStageRows, c.n, a.scale, lds_hist,
+                           sbuf + (nrec * kPerWave + r) * kStageRows);
+      __builtin_amdgcn_wave_barrier();
+      if (pf) {
+#pragma unroll
+        for (int k = 0; k < kLoads; ++k) cbuf[k] = nbuf[k];
+      }
+    }
+    if (r) {
+#pragma unroll
+      for (int q = 0; q < kRecs; ++q)
+        if (q == nrec) {
+          rec_unit[q] = c.unit;
+          rec_g0[q] = c.g0;
+          rec_nr[q] = r;
+        }
+      if (++nrec == kRecs) flush();
+    }
+    if (tid == 0) lds_claim[i & 1] = ahead;
+    __syncthreads();  // publishes claim i + 2
+    cur = nxt;
+    nxt = lds_claim[i & 1];
+  }
+  if (nrec) flush();
+  if (cur_unit >= 0) {
+    __syncthreads();
+    flush_hist(lds_hist, a.hist + (int64_t)cur_unit * kHistBins,
+               a.coarse + (int64_t)cur_unit * kCoarseBins);
   }
 }
 
