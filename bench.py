@@ -367,16 +367,18 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
 
 
 def measure_attn_sweep(torch, ckv, layers, kv_ptrs, shape, w, scale, stream,
-                       budgets=(512, 1024, 2048, 4096), reps=32):
+                       budgets=(512, 1024, 1536, 2048), reps=32):
     """The attention's time against its bytes at the Llama-8B shape (B16, 32 q
-    / 8 KV heads, n 32768): budgets k from 512 to 4096 rows per KV head, so
-    that the selected bytes grow while the grids keep their shape.  Two
+    / 8 KV heads, n 32768): budgets k from 512 to 2048 rows per KV head, so
+    that the selected bytes grow while the grids keep their shape (up to
+    2048 the one-launch kernel keeps one form: two workgroups per unit, each
+    over the whole set with half the heads).  Two
     kernels: the same-step layer's one-launch selection and attention (over
     the 32 layers in turn, so that no call finds its rows in a cache), and the
     standalone attention over assembled buffers (distinct buffers totalling
     1 GiB per budget, for the same reason).  A line through the points, time
     = fixed + bytes / rate, splits a launch into what does not grow with the
-    bytes (launch, selection, first round trip, merge, drain) and the
+    bytes (launch, selection, first round trip, the waves' merge, drain) and the
     streaming rate of the selected rows.  Dispatch-stamped kernel times."""
     import numpy as np
     dev = torch.device("cuda:0")

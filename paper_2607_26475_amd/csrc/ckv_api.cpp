@@ -401,14 +401,22 @@ int select_and_merge(SelectArgs sa, const AttnArgs& at, const Dims& d, hipStream
   return CKV_OK;
 }
 
-// Shares per unit of the same-step selection and attention in one launch
+// Workgroups per unit of the same-step selection and attention in one launch
 // (0: that launch does not apply and the selection, attention and merge run
-// as three kernels).  Two shares when two workgroups per unit still fit on
-// the device's CUs (then every CU has a workgroup to attend with), more when
-// a share would exceed kSelAttnMaxShare rows.
-int select_attn_splits(const Dims& d, int32_t k, const Layout& L) {
+// as three kernels).  Two when two workgroups per unit still fit on the
+// device's CUs (then every CU has a workgroup to attend with): for an even
+// group size with the whole set in one workgroup's LDS, each takes half the
+// heads (*heads = 2, no merge); else each takes a share of the rows, and more
+// shares when a share would exceed kSelAttnMaxShare rows (*heads = 1).
+int select_attn_splits(const Dims& d, int32_t k, const Layout& L, int* heads) {
+  *heads = 1;
   if (d.max_ctx > kFusedSelectMaxCtx || d.G > 8) return 0;
-  int S = (2 * (int64_t)d.U <= device_cus() && k >= 512) ? 2 : 1;
+  const bool two = 2 * (int64_t)d.U <= device_cus() && k >= 512;
+  if (two && d.G % 2 == 0 && k <= kSelAttnMaxShare) {
+    *heads = 2;
+    return 1;
+  }
+  int S = two ? 2 : 1;
   while ((((k + S - 1) / S + 15) & ~15) > kSelAttnMaxShare) S *= 2;
   if (S > kSelAttnMaxSplit || S > L.chunks) return 0;
   return S;
@@ -797,10 +805,12 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
     CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
                              d.kv_stride, k, scale, out);
-    if (const int S = select_attn_splits(d, k, L)) {
-      // each workgroup selects its unit's set and attends over its share
+    int heads;
+    if (const int S = select_attn_splits(d, k, L, &heads)) {
+      // each workgroup selects its unit's set and attends over its share of
+      // the rows, or over the whole set with its share of the heads
       at_.chunks = S;
-      CKV_TRY_HIP(launch_select_attn(sa, at_, d.G, S, s), "select-attention launch");
+      CKV_TRY_HIP(launch_select_attn(sa, at_, d.G, S, heads, s), "select-attention launch");
       if (S > 1) CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
     } else {
       if ((rc = run_select_tail(sa, d.U, s))) return rc;

@@ -327,11 +327,13 @@ struct LdsRows {
 
 // All kFinishThreads threads call this.  stages: WgAttnLds<G>::kStages
 // dwords, qlds: kQ dwords (both free on entry); pos(i): the source row of
-// the share's row i, clamped to [0, a.max_ctx).
+// the share's row i, clamped to [0, a.max_ctx).  The workgroup attends with
+// the G query heads qh0 .. qh0 + G - 1 of the unit's request (qh0 = h * G
+// for a KV head's whole group).
 template <int G, class Rows>
 __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, int nrows,
                                         int split, int nsplit, uint32_t* stages,
-                                        uint32_t* qlds) {
+                                        uint32_t* qlds, int qh0) {
   using Lds = WgAttnLds<G>;
   static_assert(G <= 8, "16 waves' states of at most 8 heads fit in the stages");
   constexpr int kW = kFinishThreads / 64;
@@ -339,7 +341,7 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
   const int lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, kg = lane >> 4;
   const int lrow = lane >> 4, lchunk = lane & 15;
-  const int b = unit / a.Hkv, h = unit - b * a.Hkv;
+  const int b = unit / a.Hkv;
   const int nblk = (nrows + 15) >> 4;
   const int blk0 = (wave * nblk) / kW, blk1 = ((wave + 1) * nblk) / kW;
   uint32_t* kst = stages + wave * Lds::kPerWave;
@@ -352,7 +354,7 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
   uint4 qv_ld = make_uint4(0u, 0u, 0u, 0u);
   const int qr = tid >> 4, qc = tid & 15;  // threads 0..255: row qr, 16-byte chunk qc
   if (tid < 16 * 16 && qr < G)
-    qv_ld = ld16(a.q + ((int64_t)b * a.Hq + (int64_t)h * G + qr) * kD + 8 * qc);
+    qv_ld = ld16(a.q + ((int64_t)b * a.Hq + qh0 + qr) * kD + 8 * qc);
   // rows of block blk, clamped to the share (rows past nrows are masked)
   auto load_block = [&](int blk, uint4* kr, uint4* vr) {
 #pragma unroll
@@ -498,7 +500,7 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
       L = fmaf(wt, mg[kD + 1], L);
     }
     if (nsplit == 1) {
-      a.out[((int64_t)b * a.Hq + (int64_t)h * G + g) * kD + c] = L > 0.f ? O / L : 0.f;
+      a.out[((int64_t)b * a.Hq + qh0 + g) * kD + c] = L > 0.f ? O / L : 0.f;
     } else {
       float* part = a.part + (((int64_t)unit * nsplit + split) * G + g) * kPartStride;
       part[4 + c] = O;

@@ -633,15 +633,23 @@ __device__ __forceinline__ void split_block(int blk, int nsplit, int* unit, int*
   *unit = grp * 8 + (r & 7);
 }
 
-template <int G>
+// HEADS == 1: the unit's set is split into nsplit shares of rows, each
+// attended by one workgroup with all G heads, and k_combine merges the
+// shares.  HEADS > 1: HEADS workgroups per unit each attend over the whole
+// set with G / HEADS of the heads and write their outputs directly (no
+// partials, no merge launch); the second workgroup's reads of each row come
+// while the first one's are recent, from the XCD's L2.
+template <int G, int HEADS>
 __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, AttnArgs at,
                                                                   int nsplit) {
-  using Lds = SelAttnLds<G>;
+  static_assert(G % HEADS == 0, "whole heads per workgroup");
+  constexpr int GA = G / HEADS;  // heads each workgroup attends with
+  using Lds = SelAttnLds<GA>;
   __shared__ __attribute__((aligned(16))) uint32_t lds[Lds::kDwords];
   __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
   __shared__ uint32_t misc[8];
   int unit, split;
-  split_block(blockIdx.x, nsplit, &unit, &split);
+  split_block(blockIdx.x, HEADS > 1 ? HEADS : nsplit, &unit, &split);
   if (unit >= sa.units) return;  // uniform over the workgroup
   const SelLds L{reinterpret_cast<uint2*>(lds), lds + 2 * kCandLds,
                  lds + 2 * kCandLds + kFusedSelectMaxCtx / 32, tmp, misc};
@@ -649,12 +657,14 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
   // the share of a set of m positions is known before the set is: m =
   // min(k, n_b), and the split is by m
   const int n = unit_len(sa.ctx_lens[unit / sa.Hkv], sa.max_ctx, sa.chunk);
-  int lo, hi;
-  share_range(min(sa.k, n), split, nsplit, &lo, &hi);
-  // the shares of a unit all read its histogram: none clears it
+  int lo = 0, hi = min(sa.k, n);
+  if (HEADS == 1) share_range(hi, split, nsplit, &lo, &hi);
+  // the workgroups of a unit all read its histogram: none clears it
   select_unit(sa, unit, L, split == 0, share, (uint32_t)lo, (uint32_t)hi, false);
   __syncthreads();
-  attn_wg<G>(at, unit, LdsRows{share}, hi - lo, split, nsplit, lds, lds + Lds::kQOff);
+  const int qh0 = (unit % sa.Hkv) * G + (HEADS > 1 ? split * GA : 0);
+  attn_wg<GA>(at, unit, LdsRows{share}, hi - lo, HEADS > 1 ? 0 : split, HEADS > 1 ? 1 : nsplit,
+              lds, lds + Lds::kQOff, qh0);
 }
 
 // ---- attention -------------------------------------------------------------
@@ -1395,17 +1405,30 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
 }
 
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
-                              hipStream_t s) {
+                              int heads, hipStream_t s) {
   if (nsplit < 1 || nsplit > kSelAttnMaxSplit) return hipErrorInvalidValue;
-  const int blocks = nsplit == 1 ? sa.units : (sa.units + 7) / 8 * 8 * nsplit;
+  if (heads != 1 && (heads != 2 || nsplit != 1 || G % 2)) return hipErrorInvalidValue;
+  const int per = heads > 1 ? heads : nsplit;  // workgroups per unit
+  const int blocks = per == 1 ? sa.units : (sa.units + 7) / 8 * 8 * per;
   const dim3 grid(blocks), block(kFinishThreads);
-  switch (G) {
-    case 1: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<1>, grid, block, s, sa, at, nsplit); break;
-    case 2: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<2>, grid, block, s, sa, at, nsplit); break;
-    case 4: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<4>, grid, block, s, sa, at, nsplit); break;
-    case 8: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<8>, grid, block, s, sa, at, nsplit); break;
-    default: return hipErrorInvalidValue;
+#define CKV_SA(g, hh) launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<g, hh>, grid, block, s, sa, at, nsplit)
+  if (heads == 1) {
+    switch (G) {
+      case 1: CKV_SA(1, 1); break;
+      case 2: CKV_SA(2, 1); break;
+      case 4: CKV_SA(4, 1); break;
+      case 8: CKV_SA(8, 1); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (G) {
+      case 2: CKV_SA(2, 2); break;
+      case 4: CKV_SA(4, 2); break;
+      case 8: CKV_SA(8, 2); break;
+      default: return hipErrorInvalidValue;
+    }
   }
+#undef CKV_SA
   return hipGetLastError();
 }
 

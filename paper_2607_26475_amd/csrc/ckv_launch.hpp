@@ -29,10 +29,12 @@ hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_select_fused(const SelectArgs& a, int units, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStream_t s);
-// same-step selection and attention in one launch, nsplit shares per unit
-// (partials [U][nsplit][G] for k_combine when nsplit > 1)
+// same-step selection and attention in one launch: heads == 1, nsplit shares
+// of rows per unit (partials [U][nsplit][G] for k_combine when nsplit > 1);
+// heads == 2 (G even, nsplit 1), two workgroups per unit attending with half
+// the heads each over the whole set, outputs written directly
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
-                              hipStream_t s);
+                              int heads, hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
 // The one-launch attend-and-score kernel: attention over the buffer or rows in
 // place (indexed) with G head rows, or with the 2G rows of two tokens when

@@ -1,11 +1,13 @@
 """Same-step decode through the one-launch selection and attention (MI355X
-only): every workgroup selects its unit's set and attends over its share of
-it; with more than one share per unit the shares' partials are merged by the
-merge kernel.  Checked against the oracle: index sets under the near-tie
-rule, outputs within 2e-3 of the oracle's attention over the GPU's own set
-(and of the oracle's whole step when the sets agree), for 1, 2 and 4 shares,
-group sizes 1, 2, 4 and 8, ragged contexts, a context shorter than k and an
-empty one.  The kernel profile confirms which launches ran.
+only): every workgroup selects its unit's set, then either attends over its
+share of the rows with all the group's heads (shares merged by the merge
+kernel when there are several) or, for an even group size with k <= 2048,
+over the whole set with half the heads, writing its outputs directly.
+Checked against the oracle: index sets under the near-tie rule, outputs
+within 2e-3 of the oracle's attention over the GPU's own set (and of the
+oracle's whole step when the sets agree), for head halves, 1, 2 and 4 row
+shares, group sizes 1, 2, 4 and 8, ragged contexts, a context shorter than k
+and an empty one.  The kernel profile confirms which launches ran.
 """
 from __future__ import annotations
 
@@ -28,14 +30,16 @@ def _log(*a):
 
 
 BASE = synth.WORKLOADS["llama8b_s"]
-# (name, workload changes, context lengths or None for the drawn ones, shares)
+# (name, workload changes, context lengths or None for the drawn ones, row
+# shares: 0 for the split by heads)
 CASES = [
-    ("k1024_2shares", dict(k=1024), None, 2),
+    ("k1024_heads", dict(k=1024), None, 0),
+    ("k2048_heads", dict(k=2048, max_ctx=8000, ctx_min=5000), None, 0),
     ("k4096_2shares", dict(k=4096, max_ctx=20000, ctx_min=15000), None, 2),
     ("k8192_4shares", dict(k=8192, max_ctx=40000, ctx_min=30000, batch=1), None, 4),
-    ("short_and_empty", dict(k=1024, batch=3), [5000, 700, 0], 2),
-    ("g8", dict(k=1024, q_heads=64), None, 2),
-    ("g2", dict(k=1024, q_heads=16), None, 2),
+    ("short_and_empty", dict(k=1024, batch=3), [5000, 700, 0], 0),
+    ("g8", dict(k=1024, q_heads=64), None, 0),
+    ("g2", dict(k=1024, q_heads=16), None, 0),
     ("g1", dict(k=1024, q_heads=8), None, 2),
     ("one_share", dict(k=256), None, 1),
 ]
