@@ -228,6 +228,11 @@ def main() -> int:
             for r in sweep["points"]) + f"; fits {sweep.get('select_attn_fit')} "
             f"{sweep.get('attn_fit')}")
         result["attn_sweep"] = sweep
+        cap = measure_read_cap(torch, ckv, layers, kv_ptrs, s, w, scale, stream)
+        log("read cap (the selected rows read with each attention form's pattern, no "
+            "arithmetic): " + ", ".join(f"{m} {r['us']:.1f} us ({r['frac_of_peak']:.2f})"
+                                        for m, r in cap["forms"].items()))
+        result["attn_read_cap"] = cap
 
     host_link = None
     if "host_link" in sections:
@@ -438,6 +443,53 @@ def measure_attn_sweep(torch, ckv, layers, kv_ptrs, shape, w, scale, stream,
                 "fixed_us": icpt, "marginal_GBps": 1e-3 / slope if slope > 0 else None,
                 "marginal_frac_of_peak": (1e-3 / slope) / HBM_PEAK_GBPS if slope > 0 else None}
     return res
+
+
+def measure_read_cap(torch, ckv, layers, kv_ptrs, shape, w, scale, stream, k=2048, reps=32):
+    """What the memory system gives the attention's access pattern at the
+    Llama-8B shape: the read-rate probe (ckv_probe_read_rows) reads the rows
+    each layer's same-step selection chose (k 2048 per KV head, 128 MiB of K
+    and V per launch) with the grid and load schedule of each attention form
+    and no arithmetic, cycling the 32 distinct layers so that no launch finds
+    its rows in a cache.  Dispatch-stamped kernel times."""
+    dev = torch.device("cuda:0")
+    B, Hq, Hkv, d = w.batch, w.q_heads, w.kv_heads, w.head_dim
+    L = len(layers)
+    i32 = dict(dtype=torch.int32, device=dev)
+    ws = ckv.workspace(shape, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    idx = [torch.empty((B, Hkv, k), **i32) for _ in range(L)]
+    nsel = torch.empty((B, Hkv), **i32)
+    out = torch.empty((B, Hq, d), device=dev)
+    for l in range(L):
+        kp, vp = kv_ptrs[l]
+        ckv.critical_kv_attn(shape, layers[l]["q"], None, kp, layers[l]["ctx_lens"], k, scale,
+                             kp, vp, ckv.SRC_DEVICE, None, None, None, idx[l], nsel, out, ws,
+                             stream)
+    row_bytes = B * Hkv * k * 2 * d * 2
+    forms = {"standalone": ckv.PROBE_STANDALONE, "row_halves": ckv.PROBE_ROW_HALVES,
+             "head_halves": ckv.PROBE_HEAD_HALVES}
+    res = {}
+    for name, mode in forms.items():
+        sink = torch.empty(ckv.probe_sink_words(shape, k, mode), **i32)
+        for l in range(4):  # warm
+            ckv.probe_read_rows(shape, kv_ptrs[l][0], kv_ptrs[l][1], idx[l], k, mode, sink, stream)
+        torch.cuda.synchronize()
+        ckv.profile_begin(["probe"])
+        for r in range(reps):
+            l = r % L
+            ckv.probe_read_rows(shape, kv_ptrs[l][0], kv_ptrs[l][1], idx[l], k, mode, sink, stream)
+        st = ckv.profile_end()
+        c, tot, mx = st["probe"]
+        us = 1e3 * tot / c
+        gbps = row_bytes / (us * 1e-6) / 1e9
+        res[name] = {"us": us, "max_us": 1e3 * mx, "launches": c, "GBps": gbps,
+                     "frac_of_peak": gbps / HBM_PEAK_GBPS}
+        del sink
+    del ws, idx
+    torch.cuda.empty_cache()
+    return {"forms": res, "bytes_per_launch": row_bytes,
+            "workload": f"Llama-8B shape (B16, 32 q / 8 KV heads, n 32768), the same-step sets "
+                        f"at k {k} of the {L} layers in turn"}
 
 
 def measure_host_link(torch, ckv, dev):

@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 5
+#define CKV_ABI_VERSION 6
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -503,7 +503,8 @@ typedef enum ckv_kernel_id {
   CKV_K_EXPAND = 11,  /* selected chunks -> their rows                      */
   CKV_K_RECONSTRUCT = 12, /* low-rank key rebuild (with the misses' V fetch)  */
   CKV_K_SELECT_ATTN = 13, /* same-step selection and attention in one launch */
-  CKV_K_COUNT = 14
+  CKV_K_PROBE = 14,   /* read-rate probe (ckv_probe_read_rows)              */
+  CKV_K_COUNT = 15
 } ckv_kernel_id;
 
 #define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)
@@ -531,6 +532,38 @@ int ckv_profile_begin_sampled(uint32_t kernel_mask, uint32_t every);
 /* Stop recording, wait for the recorded kernels to finish and write one
  * entry per ckv_kernel_id into stats[0 .. CKV_K_COUNT). */
 int ckv_profile_end(ckv_kernel_stats* stats);
+
+/* ---- read-rate probe -------------------------------------------------------
+ * For measurement, not for serving: reads the K and V rows that idx selects
+ * with the access pattern of one of the attention launches and no
+ * arithmetic, so that its duration is what the memory system gives that
+ * pattern (the attention's floor).  Per unit (request b, KV head h) it reads
+ * rows idx[b][h][0 .. k) of k_rows and v_rows (the layout of
+ * ckv_sparse_decode_attn's in-place sources: unit rows at stride
+ * shape->kv_row_stride elements, max_ctx rows per unit; entries outside
+ * [0, max_ctx), such as -1 padding, read row 0 or max_ctx - 1), 16 bytes per
+ * lane, 4 rows per load, in blocks of 16 rows with the next block in flight:
+ *   CKV_PROBE_STANDALONE: the standalone attention's grid, one 256-thread
+ *     workgroup per 256 selected rows, indices read from idx;
+ *   CKV_PROBE_ROW_HALVES: two 1024-thread workgroups per unit (each holding
+ *     the fused same-step launch's LDS, so one per CU), each over half the
+ *     set, positions staged in LDS; a unit's two go to one XCD;
+ *   CKV_PROBE_HEAD_HALVES: the same, both over the whole set (the fused
+ *     launch's head halves: the second read of each row from the L2).
+ * k: 1 .. 2^20 for the standalone grid, 1 .. 2048 for the halves
+ * (CKV_ESHAPE beyond).  sink: device, at least ckv_probe_sink_words() 32-bit
+ * words; one checksum per thread is written there so that no load is
+ * dropped.  Pointers 16-byte aligned.  Launched as kernel class CKV_K_PROBE. */
+#define CKV_PROBE_STANDALONE 0
+#define CKV_PROBE_ROW_HALVES 1
+#define CKV_PROBE_HEAD_HALVES 2
+int ckv_probe_read_rows(const ckv_shape* shape, const uint16_t* k_rows,
+                        const uint16_t* v_rows, const int32_t* idx, int32_t k, int mode,
+                        uint32_t* sink, size_t sink_words, void* stream);
+
+/* Words of sink that ckv_probe_read_rows needs for this shape, k and mode
+ * (0 for an invalid shape, k or mode). */
+size_t ckv_probe_sink_words(const ckv_shape* shape, int32_t k, int mode);
 
 #ifdef __cplusplus
 }

@@ -27,7 +27,8 @@ __all__ = [
     "Layer", "layer_array", "Pipeline", "status_str", "LIB_PATH",
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "ENTRY_DECODE_STEP",
-    "EXPORTS",
+    "EXPORTS", "probe_read_rows", "probe_sink_words", "PROBE_STANDALONE", "PROBE_ROW_HALVES",
+    "PROBE_HEAD_HALVES",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
@@ -35,6 +36,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
 SRC_DEVICE, SRC_HOST_PINNED = 0, 1
 ENTRY_SELECT_TOPK, ENTRY_SPARSE_DECODE_ATTN, ENTRY_CRITICAL_KV_ATTN = 1, 2, 3
 ENTRY_CORRECTED_ATTN, ENTRY_DUAL_TOKEN_ATTN, ENTRY_DECODE_STEP = 4, 5, 6
+PROBE_STANDALONE, PROBE_ROW_HALVES, PROBE_HEAD_HALVES = 0, 1, 2
 EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_workspace_bytes", "ckv_score_keys", "ckv_select_topk",
            "ckv_gather_kv", "ckv_sparse_decode_attn", "ckv_critical_kv_attn",
@@ -47,10 +49,10 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
            "ckv_pipeline_set_checks",
            "ckv_pipeline_prime",
-           "ckv_decode_step")
-KERNEL_COUNT = 14
+           "ckv_decode_step", "ckv_probe_read_rows", "ckv_probe_sink_words")
+KERNEL_COUNT = 15
 MAX_RANK = 4096
-ABI_VERSION = 5  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
+ABI_VERSION = 6  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -128,6 +130,8 @@ def _load() -> ctypes.CDLL:
         "ckv_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
         "ckv_profile_begin_sampled": (ctypes.c_int, [ctypes.c_uint32, ctypes.c_uint32]),
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
+        "ckv_probe_read_rows": (ctypes.c_int, [sp, vp, vp, vp, i32, ctypes.c_int, vp, sz, vp]),
+        "ckv_probe_sink_words": (sz, [sp, i32, ctypes.c_int]),
         "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
         "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
         "ckv_pipeline_set_gather_width": (ctypes.c_int, [vp, ctypes.c_int]),
@@ -325,7 +329,7 @@ def chunked_kv_attn(shape: Shape, chunk: int, q_att, q_sel, landmarks, ctx_lens,
 
 KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
               "combine": 6, "dual": 7, "gather": 8, "miss": 9, "landmarks": 10,
-              "expand": 11, "reconstruct": 12, "select_attn": 13}
+              "expand": 11, "reconstruct": 12, "select_attn": 13, "probe": 14}
 
 
 def profile_begin(kernels=None, every: int = 1) -> None:
@@ -347,6 +351,22 @@ def profile_end() -> dict:
     _check("ckv_profile_end", _lib.ckv_profile_end(arr))
     return {_lib.ckv_kernel_name(i).decode(): (arr[i].launches, arr[i].total_ms, arr[i].max_ms)
             for i in range(KERNEL_COUNT) if arr[i].launches}
+
+
+def probe_sink_words(shape: Shape, k: int, mode: int) -> int:
+    """uint32 words of sink that probe_read_rows needs (0: shape, k or mode
+    invalid)."""
+    return int(_lib.ckv_probe_sink_words(ctypes.byref(shape), k, mode))
+
+
+def probe_read_rows(shape: Shape, k_rows, v_rows, idx, k: int, mode: int, sink,
+                    stream=None) -> None:
+    """Read-rate probe (measurement only): reads the rows idx selects with the
+    access pattern of one attention launch (PROBE_*) and no arithmetic; sink
+    is a device tensor of at least probe_sink_words() int32/uint32 words."""
+    _check("ckv_probe_read_rows", _lib.ckv_probe_read_rows(
+        ctypes.byref(shape), _ptr(k_rows), _ptr(v_rows), _ptr(idx), k, mode, _ptr(sink),
+        sink.numel() if sink is not None else 0, _stream(stream)))
 
 
 def layer_array(layers) -> "ctypes.Array":

@@ -706,6 +706,64 @@ int ckv_gather_kv(const ckv_shape* shape, const uint16_t* k_src, const uint16_t*
                               stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+// The probe's shape, k and mode checks (the sink size needs all three).
+int check_probe(const ckv_shape* shape, int32_t k, int mode, Dims* d) {
+  int rc = check_shape(shape, d);
+  if (rc) return rc;
+  if ((rc = check_k(k))) return rc;
+  if (mode != CKV_PROBE_STANDALONE && mode != CKV_PROBE_ROW_HALVES &&
+      mode != CKV_PROBE_HEAD_HALVES)
+    return fail(CKV_EINVAL, "probe mode %d unknown", mode);
+  if (mode != CKV_PROBE_STANDALONE && k > kSelAttnMaxShare)
+    return fail(CKV_ESHAPE, "k %d above %d for the probe's halves", k, kSelAttnMaxShare);
+  // work-items per dispatch must stay below 2^32
+  const int64_t limit = ((int64_t)1 << 32) / kFinishThreads - 16;
+  if ((int64_t)d->U * ((k + kAttnRows - 1) / kAttnRows) > limit || (int64_t)d->U * 2 > limit)
+    return fail(CKV_EUNSUPPORTED, "grid too large for this shape");
+  return CKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ckv_probe_sink_words(const ckv_shape* shape, int32_t k, int mode) {
+  Dims d;
+  if (check_probe(shape, k, mode, &d)) return 0;
+  return ckv::probe_sink_words(d.U, k, mode);
+}
+
+int ckv_probe_read_rows(const ckv_shape* shape, const uint16_t* k_rows,
+                        const uint16_t* v_rows, const int32_t* idx, int32_t k, int mode,
+                        uint32_t* sink, size_t sink_words, void* stream) {
+  Dims d;
+  int rc = check_probe(shape, k, mode, &d);
+  if (rc) return rc;
+  CKV_PTR(k_rows);
+  CKV_PTR(v_rows);
+  CKV_PTR(idx);
+  CKV_PTR(sink);
+  const size_t need = ckv::probe_sink_words(d.U, k, mode);
+  if (sink_words < need)
+    return fail(CKV_EINVAL, "sink of %zu words, %zu needed", sink_words, need);
+  if (d.U == 0) return CKV_OK;
+  ckv::ProbeArgs a;
+  a.k_rows = k_rows;
+  a.v_rows = v_rows;
+  a.idx = idx;
+  a.sink = sink;
+  a.row_stride = d.kv_stride;
+  a.max_ctx = d.max_ctx;
+  a.k = k;
+  a.units = d.U;
+  CKV_TRY_HIP(ckv::launch_probe(a, mode, (hipStream_t)stream), "probe launch");
+  return CKV_OK;
+}
+
 int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
                            const uint16_t* k_buf, const uint16_t* v_buf,
                            const int32_t* n_sel, int32_t k, float scale, float* out,

@@ -667,6 +667,88 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
               lds, lds + Lds::kQOff, qh0);
 }
 
+// ---- read-rate probe --------------------------------------------------------
+// Reads rows pos(i0) .. pos(i1) of a unit (positions clamped to the unit's
+// rows) as the attention does: 4 rows per load instruction, K and V of a
+// block of 16 rows, the next block requested once the current one is in
+// (one block in flight per wave); a checksum stands for the arithmetic.
+template <class Rows>
+__device__ __forceinline__ uint32_t probe_rows(const ProbeArgs& a, int unit, Rows pos, int i0,
+                                               int i1) {
+  const int lane = threadIdx.x & 63;
+  const int lrow = lane >> 4, lchunk = lane & 15;
+  const int64_t ubase = (int64_t)unit * a.max_ctx * a.row_stride + 8 * lchunk;
+  uint4 kr[4], vr[4];
+  auto load = [&](int b) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      int p = pos(min(b + 4 * it + lrow, i1));
+      p = p < 0 ? 0 : (p >= a.max_ctx ? a.max_ctx - 1 : p);
+      const int64_t off = ubase + (int64_t)p * a.row_stride;
+      kr[it] = ld16(a.k_rows + off);
+      vr[it] = ld16(a.v_rows + off);
+    }
+  };
+  uint32_t acc = 0u;
+  load(i0);
+  for (int b = i0; b <= i1; b += 16) {  // bounds uniform over the wave
+#pragma unroll
+    for (int it = 0; it < 4; ++it)
+      acc ^= kr[it].x ^ kr[it].y ^ kr[it].z ^ kr[it].w ^ vr[it].x ^ vr[it].y ^ vr[it].z ^ vr[it].w;
+    if (b + 16 <= i1) load(b + 16);
+  }
+  return acc;
+}
+
+struct GlobalRows {
+  const int32_t* p;
+  __device__ __forceinline__ int operator()(int i) const { return p[i]; }
+};
+
+// MODE CKV_PROBE_STANDALONE: k_attn's grid (one kAttnThreads workgroup per
+// kAttnRows rows, kAttnRows / 4 rows per wave, indices from global memory).
+// Otherwise the fused same-step launch's: two kFinishThreads workgroups per
+// unit with its LDS (one per CU) and its workgroup -> (unit, part) mapping,
+// positions staged in LDS, each wave a contiguous run of 16-row blocks of the
+// part's rows (its half of the set, or all of it).
+template <int MODE>
+__global__ __launch_bounds__(MODE == CKV_PROBE_STANDALONE ? kAttnThreads : kFinishThreads) void
+k_probe_rows(ProbeArgs a) {
+  const int tid = threadIdx.x, wave = tid >> 6;
+  uint32_t acc = 0u;
+  if constexpr (MODE == CKV_PROBE_STANDALONE) {
+    // LDS that leaves two workgroups per CU, the attention kernel's residency
+    // (its registers allow two waves per SIMD)
+    __shared__ uint32_t lds[18 * 1024];
+    if (tid == 0) lds[blockIdx.x & 1023] = 0u;
+    const int chunks = (a.k + kAttnRows - 1) / kAttnRows;
+    const int unit = blockIdx.x / chunks, c = blockIdx.x - unit * chunks;
+    constexpr int kRowsPerWave = kAttnRows / (kAttnThreads / 64);
+    const int i0 = c * kAttnRows + wave * kRowsPerWave;
+    const int i1 = min(i0 + kRowsPerWave, a.k) - 1;
+    if (i0 <= i1) acc = probe_rows(a, unit, GlobalRows{a.idx + (int64_t)unit * a.k}, i0, i1);
+    __syncthreads();
+    if (a.k < 0) acc ^= lds[(tid + 1) & 1023];  // never (k >= 1): keeps the LDS allocated
+    a.sink[(int64_t)blockIdx.x * kAttnThreads + tid] = acc;
+  } else {
+    __shared__ __attribute__((aligned(16))) uint32_t lds[SelAttnLds<4>::kDwords];
+    int unit, part;
+    split_block(blockIdx.x, 2, &unit, &part);
+    if (unit < a.units) {  // uniform over the workgroup
+      int lo = 0, hi = a.k;
+      if (MODE == CKV_PROBE_ROW_HALVES) share_range(a.k, part, 2, &lo, &hi);
+      int32_t* pos = reinterpret_cast<int32_t*>(lds);
+      for (int i = lo + tid; i < hi; i += kFinishThreads) pos[i - lo] = a.idx[(int64_t)unit * a.k + i];
+      __syncthreads();
+      constexpr int kW = kFinishThreads / 64;
+      const int nblk = (hi - lo + 15) >> 4;
+      const int b0 = (wave * nblk) / kW, b1 = ((wave + 1) * nblk) / kW;
+      if (b0 < b1) acc = probe_rows(a, unit, LdsRows{pos}, 16 * b0, min(16 * b1, hi - lo) - 1);
+    }
+    a.sink[(int64_t)blockIdx.x * kFinishThreads + tid] = acc;
+  }
+}
+
 // ---- attention -------------------------------------------------------------
 template <int G, bool INDEXED>
 __global__ __launch_bounds__(kAttnThreads) void k_attn(AttnArgs a) {
@@ -1429,6 +1511,32 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
     }
   }
 #undef CKV_SA
+  return hipGetLastError();
+}
+
+size_t probe_sink_words(int64_t units, int k, int mode) {
+  if (mode == CKV_PROBE_STANDALONE)
+    return (size_t)units * ((k + kAttnRows - 1) / kAttnRows) * kAttnThreads;
+  return (size_t)((units + 7) / 8 * 8 * 2) * kFinishThreads;
+}
+
+hipError_t launch_probe(const ProbeArgs& a, int mode, hipStream_t s) {
+  switch (mode) {
+    case CKV_PROBE_STANDALONE:
+      launch_kernel(CKV_K_PROBE, k_probe_rows<CKV_PROBE_STANDALONE>,
+                    dim3((unsigned)(a.units * ((a.k + kAttnRows - 1) / kAttnRows))),
+                    dim3(kAttnThreads), s, a);
+      break;
+    case CKV_PROBE_ROW_HALVES:
+      launch_kernel(CKV_K_PROBE, k_probe_rows<CKV_PROBE_ROW_HALVES>,
+                    dim3((unsigned)((a.units + 7) / 8 * 8 * 2)), dim3(kFinishThreads), s, a);
+      break;
+    case CKV_PROBE_HEAD_HALVES:
+      launch_kernel(CKV_K_PROBE, k_probe_rows<CKV_PROBE_HEAD_HALVES>,
+                    dim3((unsigned)((a.units + 7) / 8 * 8 * 2)), dim3(kFinishThreads), s, a);
+      break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

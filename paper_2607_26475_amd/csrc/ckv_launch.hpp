@@ -12,6 +12,20 @@ int fail(int code, const char* fmt, ...);
 int hip_fail(hipError_t e, const char* what);
 const char* last_detail();
 
+// The read-rate probe: the rows idx[u][0 .. k) of each unit, read with the
+// access pattern of one attention launch (mode: CKV_PROBE_*) and no
+// arithmetic; sink gets one checksum per thread.
+struct ProbeArgs {
+  const uint16_t* k_rows;
+  const uint16_t* v_rows;
+  const int32_t* idx;   // [units][k]
+  uint32_t* sink;       // probe_sink_words(units, k, mode) words
+  int64_t row_stride;   // elements between a unit's rows
+  int max_ctx, k, units;
+};
+size_t probe_sink_words(int64_t units, int k, int mode);
+hipError_t launch_probe(const ProbeArgs& a, int mode, hipStream_t s);
+
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s);
 // The kernel that runs a scoring pass: scores only, scores with the

@@ -201,6 +201,28 @@ int main() {
              CKV_EWORKSPACE);  // not 256-byte aligned
     }
 
+  // the read-rate probe: sizes, refusals, and an empty batch (no launch)
+  {
+    uint32_t* const FU = reinterpret_cast<uint32_t*>(0x100000);
+    const ckv_shape s = shape(16, 32, 8, 32768);
+    if (ckv_probe_sink_words(&s, 2048, CKV_PROBE_STANDALONE) != (size_t)128 * 8 * 256) ++g_failures;
+    if (ckv_probe_sink_words(&s, 2048, CKV_PROBE_HEAD_HALVES) != (size_t)256 * 1024) ++g_failures;
+    if (ckv_probe_sink_words(&s, 4096, CKV_PROBE_ROW_HALVES) != 0) ++g_failures;
+    if (ckv_probe_sink_words(&s, 16, 3) != 0) ++g_failures;
+    EXPECT(ckv_probe_read_rows(&s, F16, F16, FI, 16, 3, FU, 1 << 20, nullptr), CKV_EINVAL);
+    EXPECT(ckv_probe_read_rows(&s, F16, F16, FI, 4096, CKV_PROBE_HEAD_HALVES, FU, 1 << 20,
+                               nullptr),
+           CKV_ESHAPE);
+    EXPECT(ckv_probe_read_rows(&s, F16, F16, FI, 2048, CKV_PROBE_STANDALONE, FU, 1000, nullptr),
+           CKV_EINVAL);  // sink too small
+    EXPECT(ckv_probe_read_rows(&s, nullptr, F16, FI, 16, CKV_PROBE_STANDALONE, FU, 1 << 20,
+                               nullptr),
+           CKV_EINVAL);
+    const ckv_shape e = shape(0, 32, 8, 32768);
+    for (int mode : {CKV_PROBE_STANDALONE, CKV_PROBE_ROW_HALVES, CKV_PROBE_HEAD_HALVES})
+      EXPECT(ckv_probe_read_rows(&e, F16, F16, FI, 2048, mode, FU, 0, nullptr), CKV_OK);
+  }
+
   // argument errors of the other entries
   {
     const ckv_shape s = shape(2, 8, 2, 64);

@@ -33,7 +33,7 @@ def test_header_functions_are_exported():
 
 
 def test_abi_version_and_status_text():
-    assert ckv.abi_version() == ckv.ABI_VERSION == 5
+    assert ckv.abi_version() == ckv.ABI_VERSION == 6
     texts = {ckv.status_str(v) for v in STATUS.values()}
     assert len(texts) == len(STATUS)
     assert ckv.status_str(99) == "unknown status"
@@ -280,3 +280,27 @@ def test_noalloc_entry_refuses_oversized_shapes():
     llama = good_shape(batch=16, num_q_heads=32, num_kv_heads=8, max_ctx=32768)
     assert ckv.workspace_bytes(llama, 2048, ckv.ENTRY_CRITICAL_KV_ATTN) <= \
         ckv.NOALLOC_SCRATCH_BYTES
+
+
+def test_probe_sizes_and_refusals():
+    s = good_shape(batch=16, num_q_heads=32, num_kv_heads=8, max_ctx=32768)
+    assert ckv.probe_sink_words(s, 2048, ckv.PROBE_STANDALONE) == 128 * 8 * 256
+    assert ckv.probe_sink_words(s, 2048, ckv.PROBE_ROW_HALVES) == 256 * 1024
+    assert ckv.probe_sink_words(s, 2048, ckv.PROBE_HEAD_HALVES) == 256 * 1024
+    assert ckv.probe_sink_words(s, 4096, ckv.PROBE_HEAD_HALVES) == 0   # halves: k <= 2048
+    assert ckv.probe_sink_words(s, 2048, 3) == 0
+    assert ckv.probe_sink_words(good_shape(batch=3, num_kv_heads=2), 256,
+                                ckv.PROBE_ROW_HALVES) == 16 * 1024  # 6 units -> 8 per XCD round
+    call = ckv._lib.ckv_probe_read_rows
+    assert call(ctypes.byref(s), FAKE, FAKE, FAKE, 2048, 3, FAKE, 1 << 20, None) == STATUS["EINVAL"]
+    assert call(ctypes.byref(s), FAKE, FAKE, FAKE, 4096, ckv.PROBE_ROW_HALVES, FAKE, 1 << 20,
+                None) == STATUS["ESHAPE"]
+    assert call(ctypes.byref(s), FAKE, FAKE, FAKE, 2048, ckv.PROBE_STANDALONE, FAKE, 1000,
+                None) == STATUS["EINVAL"]   # sink smaller than needed
+    assert call(ctypes.byref(s), None, FAKE, FAKE, 2048, ckv.PROBE_STANDALONE, FAKE, 1 << 20,
+                None) == STATUS["EINVAL"]
+    assert call(ctypes.byref(s), FAKE, FAKE, FAKE + 4, 2048, ckv.PROBE_STANDALONE, FAKE,
+                1 << 20, None) == STATUS["EINVAL"]   # misaligned
+    empty = good_shape(batch=0, num_q_heads=32, num_kv_heads=8, max_ctx=32768)
+    for mode in (ckv.PROBE_STANDALONE, ckv.PROBE_ROW_HALVES, ckv.PROBE_HEAD_HALVES):
+        assert call(ctypes.byref(empty), FAKE, FAKE, FAKE, 2048, mode, FAKE, 0, None) == 0
