@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 6
+#define CKV_ABI_VERSION 7
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -532,6 +532,23 @@ int ckv_profile_begin_sampled(uint32_t kernel_mask, uint32_t every);
 /* Stop recording, wait for the recorded kernels to finish and write one
  * entry per ckv_kernel_id into stats[0 .. CKV_K_COUNT). */
 int ckv_profile_end(ckv_kernel_stats* stats);
+
+/* ---- debug mode -----------------------------------------------------------
+ * For development, not for serving (on: nonzero; process-wide; off by default,
+ * on by default in a library built with -DCKV_DEBUG).  In debug mode every
+ * entry first checks its device-side inputs on the device and synchronises
+ * the caller's stream, returning CKV_EINVAL with the first violation in
+ * ckv_last_error_detail():
+ *   0 <= ctx_lens[b] <= max_ctx;
+ *   0 <= n_sel[u] <= k for an input count (n_sel, n_sel_in, n_pred);
+ *   entries 0 .. n_sel[u] - 1 of an input index set (idx, idx_in, idx_pred;
+ *   all k without a count) are -1 or positions below the unit's context
+ *   length (below max_ctx where the entry takes no ctx_lens).
+ * Outside debug mode these are the caller's preconditions, and kernels only
+ * clamp what they read.  Every kernel launch then also synchronises its
+ * stream, so that a failing kernel is reported by the entry that launched it
+ * (CKV_EHIP).  Debug mode synchronises, so it is not for graph capture. */
+int ckv_set_debug(int on);
 
 /* ---- read-rate probe -------------------------------------------------------
  * For measurement, not for serving: reads the K and V rows that idx selects

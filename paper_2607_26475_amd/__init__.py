@@ -28,7 +28,7 @@ __all__ = [
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "ENTRY_DECODE_STEP",
     "EXPORTS", "probe_read_rows", "probe_sink_words", "PROBE_STANDALONE", "PROBE_ROW_HALVES",
-    "PROBE_HEAD_HALVES",
+    "PROBE_HEAD_HALVES", "set_debug",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
@@ -49,10 +49,10 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
            "ckv_pipeline_set_checks",
            "ckv_pipeline_prime",
-           "ckv_decode_step", "ckv_probe_read_rows", "ckv_probe_sink_words")
+           "ckv_decode_step", "ckv_probe_read_rows", "ckv_probe_sink_words", "ckv_set_debug")
 KERNEL_COUNT = 15
 MAX_RANK = 4096
-ABI_VERSION = 6  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
+ABI_VERSION = 7  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -132,6 +132,7 @@ def _load() -> ctypes.CDLL:
         "ckv_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStats)]),
         "ckv_probe_read_rows": (ctypes.c_int, [sp, vp, vp, vp, i32, ctypes.c_int, vp, sz, vp]),
         "ckv_probe_sink_words": (sz, [sp, i32, ctypes.c_int]),
+        "ckv_set_debug": (ctypes.c_int, [ctypes.c_int]),
         "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
         "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
         "ckv_pipeline_set_gather_width": (ctypes.c_int, [vp, ctypes.c_int]),
@@ -351,6 +352,13 @@ def profile_end() -> dict:
     _check("ckv_profile_end", _lib.ckv_profile_end(arr))
     return {_lib.ckv_kernel_name(i).decode(): (arr[i].launches, arr[i].total_ms, arr[i].max_ms)
             for i in range(KERNEL_COUNT) if arr[i].launches}
+
+
+def set_debug(on: bool) -> None:
+    """Debug mode (process-wide): entries check their device-side inputs
+    (context lengths, input counts and index sets) on the device and every
+    launch synchronises; a violation raises CkvError (CKV_EINVAL)."""
+    _check("ckv_set_debug", _lib.ckv_set_debug(1 if on else 0))
 
 
 def probe_sink_words(shape: Shape, k: int, mode: int) -> int:

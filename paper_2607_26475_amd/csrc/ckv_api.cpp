@@ -5,10 +5,12 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "ckv.h"
 #include "ckv_launch.hpp"
+#include "ckv_profile.hpp"
 
 namespace ckv {
 
@@ -31,6 +33,48 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 const char* last_detail() { return g_detail.c_str(); }
+
+int debug_check(hipStream_t s, const int32_t* ctx_lens, const int32_t* idx,
+                const int32_t* n_sel, int B, int Hkv, int max_ctx, int k) {
+  if (!debug_on() || B == 0 || (!ctx_lens && !idx && !n_sel)) return CKV_OK;
+  // one 16-byte flag per device, kept until the process ends (debug mode only)
+  static std::mutex mu;
+  static unsigned long long* flags[256] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "debug check");
+  if (dev < 0 || dev >= 256) return fail(CKV_EUNSUPPORTED, "device %d", dev);
+  {
+    std::lock_guard<std::mutex> lk(mu);
+    if (!flags[dev] && (e = hipMalloc(&flags[dev], 16)) != hipSuccess)
+      return hip_fail(e, "debug check flag");
+  }
+  CheckArgs a;
+  a.ctx_lens = ctx_lens;
+  a.idx = idx;
+  a.n_sel = n_sel;
+  a.flag = flags[dev];
+  a.B = B;
+  a.Hkv = Hkv;
+  a.max_ctx = max_ctx;
+  a.k = k;
+  unsigned long long got = 0;
+  if ((e = launch_fill(a.flag, 16, 0xffffffffu, s)) != hipSuccess ||
+      (e = launch_check(a, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(&got, a.flag, 8, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return hip_fail(e, "debug check");
+  if (got == ~0ull) return CKV_OK;
+  const unsigned kind = (unsigned)(got >> 40);
+  const long long item = (long long)(got & ((1ull << 40) - 1));
+  if (kind == 1) return fail(CKV_EINVAL, "debug check: ctx_lens[%lld] outside [0, %d]", item, max_ctx);
+  if (kind == 2)
+    return fail(CKV_EINVAL, "debug check: n_sel of unit %lld outside [0, %d]", item, k);
+  return fail(CKV_EINVAL,
+              "debug check: index entry %lld of unit %lld is neither -1 nor a position below "
+              "the unit's context length",
+              item % k, item / k);
+}
 
 }  // namespace ckv
 
@@ -107,6 +151,15 @@ int check_scale(float scale) {
   do {                                                                      \
     if (!(p)) return fail(CKV_EINVAL, "%s is NULL", #p);                    \
     if (!aligned16(p)) return fail(CKV_EINVAL, "%s is not 16-byte aligned", #p); \
+  } while (0)
+
+// Debug mode: the entry's device-side inputs, checked before its launches
+// (d: the entry's Dims).
+#define CKV_DEBUG_CHECK(stream, lens, idx, nsel, kk)                                       \
+  do {                                                                                    \
+    const int rc_ = debug_check((hipStream_t)(stream), (lens), (idx), (nsel), d.B, d.Hkv,  \
+                                d.max_ctx, (kk));                                         \
+    if (rc_) return rc_;                                                                  \
   } while (0)
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -528,6 +581,7 @@ int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, assembled ? nullptr : p.idx_in, p.n_sel_in, k);
   hipStream_t s = (hipStream_t)stream;
   // the selection problem: positions, or chunks (one landmark per chunk rows,
   // budget k / chunk), whose regions lie below the attention partials
@@ -607,6 +661,7 @@ int ckv::gather_kv_width(const ckv_shape* shape, const uint16_t* k_src, const ui
     return fail(CKV_EINVAL, "gather width %d outside [0, %d]", workgroups, kMaxGatherWgs);
   if ((rc = resolve_src(src_kind, &k_src, &v_src))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, nullptr, idx, n_sel, k);
   GatherArgs a;
   a.k_src = k_src;
   a.v_src = v_src;
@@ -668,6 +723,7 @@ int ckv_score_keys(const ckv_shape* shape, const uint16_t* q, const uint16_t* k_
   CKV_PTR(ctx_lens);
   CKV_PTR(scores);
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, nullptr, nullptr, 1);
   Layout L = make_layout(d, 1, 0);
   if ((rc = check_grid(d, L))) return rc;
   ScoreArgs a = score_args(d, L, q, k_score, ctx_lens, scale, scores, nullptr);
@@ -692,6 +748,7 @@ int ckv_select_topk(const ckv_shape* shape, const float* scores, const int32_t* 
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, nullptr, nullptr, k);
   hipStream_t s = (hipStream_t)stream;
   SelectArgs a = select_args(d, L, ws, scores, ctx_lens, k, idx, n_sel);
   CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
@@ -782,6 +839,7 @@ int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, nullptr, nullptr, n_sel, k);
   hipStream_t s = (hipStream_t)stream;
   AttnArgs a = attn_args(d, L, ws, q_att, k_buf, v_buf, nullptr, n_sel, kD, k, scale, out);
   return run_attention(a, d, false, s);
@@ -839,6 +897,7 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, idx_in, n_sel_in, k);
   hipStream_t s = (hipStream_t)stream;
   float* scores = at<float>(ws, L.scores);
   SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
@@ -931,6 +990,7 @@ int ckv_dual_token_attn(const ckv_shape* shape, const uint16_t* q_cur, const uin
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, nullptr, nullptr, n_sel, k);
   hipStream_t s = (hipStream_t)stream;
   AttnArgs a = attn_args(d, L, ws, q_cur, k_buf, v_buf, nullptr, n_sel, kD, k, scale, out_cur);
   a.q2 = q_spec;
@@ -953,6 +1013,7 @@ int ckv_chunk_landmarks(const ckv_shape* shape, int32_t chunk, const uint16_t* k
   CKV_PTR(ctx_lens);
   CKV_PTR(landmarks);
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, nullptr, nullptr, 1);
   LandmarkArgs a;
   a.keys = keys;
   a.ctx_lens = ctx_lens;
@@ -987,6 +1048,7 @@ int ckv_select_chunks(const ckv_shape* shape, int32_t chunk, const uint16_t* q_s
   Layout L = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN);
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, nullptr, nullptr, k);
   return run_select_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx,
                            n_chunks, rows, n_rows, ws, (hipStream_t)stream);
 }
@@ -1021,6 +1083,7 @@ int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, nullptr, nullptr, k);
   hipStream_t s = (hipStream_t)stream;
   if ((rc = run_select_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx,
                               n_chunks, rows, n_rows, ws, s)))
@@ -1075,6 +1138,7 @@ int ckv::corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uin
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, ctx_lens, idx_pred, n_pred, k);
   hipStream_t s = (hipStream_t)stream;
   float* scores = at<float>(ws, L.scores);
   // 1. the current token's own selection
@@ -1192,6 +1256,7 @@ int ckv_reconstruct_keys(const ckv_shape* shape, int32_t rank, const uint16_t* u
   CKV_PTR(n_sel);
   CKV_PTR(k_dst);
   if (d.U == 0) return CKV_OK;
+  CKV_DEBUG_CHECK(stream, nullptr, idx, n_sel, k);
   ReconArgs r = recon_args(d, rank, u_fac, w_fac, idx, n_sel, nullptr, k, k_dst);
   CKV_TRY_HIP(launch_reconstruct(r, (hipStream_t)stream), "reconstruct launch");
   return CKV_OK;

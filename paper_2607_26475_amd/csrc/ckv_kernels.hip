@@ -5,6 +5,7 @@
 #include "ckv_score.hpp"
 #include "ckv_topk.hpp"
 
+#include <algorithm>
 #include <mutex>
 
 namespace ckv {
@@ -749,6 +750,38 @@ k_probe_rows(ProbeArgs a) {
   }
 }
 
+// ---- debug-mode input check -------------------------------------------------
+__global__ __launch_bounds__(256) void k_check(CheckArgs a) {
+  const int64_t U = (int64_t)a.B * a.Hkv;
+  const int64_t total = a.B + U + (a.idx ? U * a.k : 0);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+    unsigned long long code = ~0ull;
+    if (t < a.B) {
+      if (a.ctx_lens) {
+        const int v = a.ctx_lens[t];
+        if (v < 0 || v > a.max_ctx) code = (1ull << 40) | (unsigned long long)t;
+      }
+    } else if (t < a.B + U) {
+      const int64_t u = t - a.B;
+      if (a.n_sel) {
+        const int v = a.n_sel[u];
+        if (v < 0 || v > a.k) code = (2ull << 40) | (unsigned long long)u;
+      }
+    } else {
+      const int64_t e = t - a.B - U, u = e / a.k;
+      const int i = (int)(e - u * a.k);
+      const int count = a.n_sel ? min(max(a.n_sel[u], 0), a.k) : a.k;
+      if (i < count) {
+        const int bound = a.ctx_lens ? min(max(a.ctx_lens[u / a.Hkv], 0), a.max_ctx) : a.max_ctx;
+        const int v = a.idx[e];
+        if (v != -1 && (v < 0 || v >= bound)) code = (3ull << 40) | (unsigned long long)e;
+      }
+    }
+    if (code != ~0ull) atomicMin(a.flag, code);
+  }
+}
+
 // ---- attention -------------------------------------------------------------
 template <int G, bool INDEXED>
 __global__ __launch_bounds__(kAttnThreads) void k_attn(AttnArgs a) {
@@ -1245,7 +1278,7 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   if (n16 == 0) return hipSuccess;
   launch_kernel(CKV_K_ZERO, k_zero, dim3(blocks_for(n16, 256 * 4, 2048)), dim3(256), s,
                 reinterpret_cast<uint4*>(p), n16);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s) {
@@ -1253,7 +1286,7 @@ hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s) {
   if (n16 == 0) return hipSuccess;
   launch_kernel(CKV_K_ZERO, k_fill, dim3(blocks_for(n16, 256 * 4, 2048)), dim3(256), s,
                 reinterpret_cast<uint4*>(p), n16, pattern);
-  return hipGetLastError();
+  return launch_status();
 }
 
 // Workgroups of a kScoreThreads kernel that fit on the device at once, per
@@ -1371,27 +1404,27 @@ hipError_t launch_score(const ScoreArgs& a, int G, bool hist, int nwg, hipStream
     case 16: launch_score_g<16>(a, hist, nwg, s); break;
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_hist(const SelectArgs& a, int units, hipStream_t s) {
   launch_kernel(CKV_K_HIST, k_hist, dim3(units * a.tiles), dim3(kScoreThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_filter(const SelectArgs& a, int units, hipStream_t s) {
   launch_kernel(CKV_K_FILTER, k_filter, dim3(units * a.tiles), dim3(kFilterThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_finish(const SelectArgs& a, int units, hipStream_t s) {
   launch_kernel(CKV_K_FINISH, k_finish, dim3(units), dim3(kFinishThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_select_fused(const SelectArgs& a, int units, hipStream_t s) {
   launch_kernel(CKV_K_FINISH, k_select_fused, dim3(units), dim3(kFinishThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 template <int G>
@@ -1410,7 +1443,7 @@ hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStr
     case 16: launch_attn_g<16>(a, indexed, units, s); break;
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
@@ -1423,7 +1456,7 @@ hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s) {
     case 16: launch_kernel(CKV_K_COMBINE, k_combine<16>, grid, block, s, a); break;
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 template <int G, bool INDEXED>
@@ -1448,7 +1481,7 @@ static hipError_t launch_dual_i(const AttnArgs& at, const ScoreArgs& sc, int G,
     case 16: launch_dual_g<16, INDEXED>(at, sc, attn_blocks, nwg, s); break;
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 template <int G, bool INDEXED>
@@ -1472,7 +1505,7 @@ static hipError_t launch_dual2_i(const AttnArgs& at, const ScoreArgs& sc, int G,
     case 8: launch_dual2_g<8, INDEXED>(at, sc, attn_blocks, nwg, s); break;
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
@@ -1511,7 +1544,7 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
     }
   }
 #undef CKV_SA
-  return hipGetLastError();
+  return launch_status();
 }
 
 size_t probe_sink_words(int64_t units, int k, int mode) {
@@ -1537,19 +1570,27 @@ hipError_t launch_probe(const ProbeArgs& a, int mode, hipStream_t s) {
       break;
     default: return hipErrorInvalidValue;
   }
+  return launch_status();
+}
+
+hipError_t launch_check(const CheckArgs& a, hipStream_t s) {
+  const int64_t U = (int64_t)a.B * a.Hkv;
+  const int64_t total = a.B + U + (a.idx ? U * a.k : 0);
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_check, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s) {
   const int blocks = blocks_for(a.items, kGatherThreads, 8192);
   launch_kernel(CKV_K_LANDMARKS, k_landmarks, dim3(blocks), dim3(kGatherThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_reconstruct(const ReconArgs& a, hipStream_t s) {
   const int blocks = blocks_for(a.items, kGatherThreads, 8192);
   launch_kernel(CKV_K_RECONSTRUCT, k_reconstruct, dim3(blocks), dim3(kGatherThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconArgs& r,
@@ -1558,24 +1599,24 @@ hipError_t launch_miss_fill(const GatherArgs& g, int fetch_blocks, const ReconAr
   const int nr = blocks_for(r.items, kGatherThreads, 8192);
   launch_kernel(CKV_K_RECONSTRUCT, k_miss_fill, dim3(nf + nr), dim3(kGatherThreads), s, g, r,
                 nf);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_expand(const ExpandArgs& a, int units, hipStream_t s) {
   const dim3 grid((a.k + kGatherThreads - 1) / kGatherThreads, units);
   launch_kernel(CKV_K_EXPAND, k_expand, grid, dim3(kGatherThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s) {
   launch_kernel(CKV_K_MISS, k_miss, dim3(units), dim3(kMissThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t launch_gather(const GatherArgs& a, int max_blocks, hipStream_t s) {
   const int blocks = blocks_for(a.items, kGatherThreads * kGatherUnroll, max_blocks);
   launch_kernel(CKV_K_GATHER, k_gather, dim3(blocks), dim3(kGatherThreads), s, a);
-  return hipGetLastError();
+  return launch_status();
 }
 
 }  // namespace ckv

@@ -24,6 +24,24 @@ struct ProbeArgs {
   int max_ctx, k, units;
 };
 size_t probe_sink_words(int64_t units, int k, int mode);
+
+// Debug mode's check of an entry's device-side inputs (each may be null):
+// 0 <= ctx_lens[b] <= max_ctx; 0 <= n_sel[u] <= k; idx[u][i] for i below
+// n_sel[u] (below k without n_sel) is -1 or in [0, n_b) (n_b = max_ctx
+// without ctx_lens).  *flag: the smallest violation code, kind << 40 | item
+// (kind 1: ctx_lens[b], 2: n_sel[u], 3: idx entry u*k + i), or all ones.
+struct CheckArgs {
+  const int32_t* ctx_lens;
+  const int32_t* idx;
+  const int32_t* n_sel;
+  unsigned long long* flag;
+  int B, Hkv, max_ctx, k;
+};
+hipError_t launch_check(const CheckArgs& a, hipStream_t s);
+// In debug mode, checks those inputs on the device, synchronising `s`;
+// CKV_EINVAL names the first violation.  Otherwise returns CKV_OK at once.
+int debug_check(hipStream_t s, const int32_t* ctx_lens, const int32_t* idx,
+                const int32_t* n_sel, int B, int Hkv, int max_ctx, int k);
 hipError_t launch_probe(const ProbeArgs& a, int mode, hipStream_t s);
 
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);

@@ -61,9 +61,36 @@ bool profile_events(int id, hipEvent_t* start, hipEvent_t* stop) {
   return true;
 }
 
+#ifdef CKV_DEBUG
+std::atomic<int> g_debug{1};
+#else
+std::atomic<int> g_debug{0};
+#endif
+thread_local hipError_t g_debug_err = hipSuccess;
+
+bool debug_on() { return g_debug.load(std::memory_order_relaxed) != 0; }
+
+void debug_after_launch(hipStream_t s) {
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess && g_debug_err == hipSuccess) g_debug_err = e;
+}
+
+hipError_t launch_status() {
+  const hipError_t e = g_debug_err;
+  g_debug_err = hipSuccess;
+  const hipError_t last = hipGetLastError();
+  return e != hipSuccess ? e : last;
+}
+
 }  // namespace ckv
 
 extern "C" {
+
+int ckv_set_debug(int on) {
+  ckv::g_debug.store(on ? 1 : 0);
+  return CKV_OK;
+}
 
 const char* ckv_kernel_name(int id) {
   static const char* names[CKV_K_COUNT] = {"zero", "score", "hist", "filter", "finish",

@@ -33,7 +33,7 @@ def test_header_functions_are_exported():
 
 
 def test_abi_version_and_status_text():
-    assert ckv.abi_version() == ckv.ABI_VERSION == 6
+    assert ckv.abi_version() == ckv.ABI_VERSION == 7
     texts = {ckv.status_str(v) for v in STATUS.values()}
     assert len(texts) == len(STATUS)
     assert ckv.status_str(99) == "unknown status"
@@ -304,3 +304,16 @@ def test_probe_sizes_and_refusals():
     empty = good_shape(batch=0, num_q_heads=32, num_kv_heads=8, max_ctx=32768)
     for mode in (ckv.PROBE_STANDALONE, ckv.PROBE_ROW_HALVES, ckv.PROBE_HEAD_HALVES):
         assert call(ctypes.byref(empty), FAKE, FAKE, FAKE, 2048, mode, FAKE, 0, None) == 0
+
+
+def test_debug_mode_switch_without_a_gpu():
+    """Debug mode checks device-side inputs only when a unit exists: host-side
+    refusals are unchanged, and empty batches still return before any launch."""
+    assert ckv._lib.ckv_set_debug(1) == 0
+    try:
+        s = good_shape()
+        assert call_score(s, q=None) == STATUS["EINVAL"]
+        empty = good_shape(batch=0)
+        assert call_score(empty) == 0
+    finally:
+        assert ckv._lib.ckv_set_debug(0) == 0
