@@ -13,6 +13,7 @@ constexpr int kWave = 64;
 // Scoring: a persistent grid; each workgroup scores a balanced contiguous
 // range of kStageRows-key groups (4 waves, MFMA blocks of 16 keys).
 constexpr int kScoreThreads = 256;
+constexpr int kHistScoreWaves = 8;  // waves of the scoring kernel with histograms
 constexpr int kStageRows = 32;     // key rows staged per wave per step
 constexpr int kStageRowDwords = 68;  // 256-byte row + 16-byte pad (bank spread)
 constexpr int kStageDwords = kStageRows * kStageRowDwords;

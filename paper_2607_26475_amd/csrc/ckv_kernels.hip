@@ -27,11 +27,18 @@ __global__ __launch_bounds__(256) void k_fill(uint4* p, int64_t n16, uint32_t pa
 }
 
 // ---- scoring -------------------------------------------------------------
+// The pass with histograms runs as one workgroup of kHistScoreWaves waves per
+// CU (its LDS allows one): half as many concurrent streams of keys as two
+// four-wave workgroups, with the same loads in flight per CU, and so fewer
+// histogram slots per unit.  Measured on the Llama-8B layer in one session:
+// 159.7-163.9 us against 166.0-167.4 us; without histograms it gained nothing.
 template <int G, bool HIST>
-__global__ __launch_bounds__(kScoreThreads) void k_score(ScoreArgs a) {
+__global__ __launch_bounds__(HIST ? 64 * kHistScoreWaves : kScoreThreads) void k_score(ScoreArgs a) {
+  constexpr int kWaves = HIST ? kHistScoreWaves : kScoreThreads / 64;
   __shared__ uint32_t lds_hist[HIST ? kHistBins : 1];
-  __shared__ __attribute__((aligned(16))) uint32_t lds_stage[kScoreLdsDwords];
-  score_range<G, HIST>(a, blockIdx.x, gridDim.x, lds_hist, lds_stage);
+  __shared__ __attribute__((aligned(16)))
+  uint32_t lds_stage[kWaves * (kStageDwords + kFlushGroups * kStageRows)];
+  score_range<G, HIST, kWaves>(a, blockIdx.x, gridDim.x, lds_hist, lds_stage);
 }
 
 
@@ -1289,11 +1296,11 @@ hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s) {
   return launch_status();
 }
 
-// Workgroups of a kScoreThreads kernel that fit on the device at once, per
-// (kernel, device): queried once and kept in a fixed table (no allocation on
-// the call path), so a call makes no occupancy query.  The persistent
+// Workgroups of a kernel of `threads` threads that fit on the device at once,
+// per (kernel, device): queried once and kept in a fixed table (no allocation
+// on the call path), so a call makes no occupancy query.  The persistent
 // scoring grid is this many workgroups (or fewer if there is less work).
-static int resident_blocks(const void* fn) {
+static int resident_blocks(const void* fn, int threads = kScoreThreads) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 1024;
   struct Entry {
@@ -1313,7 +1320,7 @@ static int resident_blocks(const void* fn) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus < 1)
     cus = 256;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kScoreThreads, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, 0) !=
           hipSuccess ||
       per_cu < 1)
     per_cu = 1;
@@ -1381,7 +1388,8 @@ int score_blocks(const ScoreArgs& a, int G, ScoreKind kind) {
   }
   if (!fn) return 0;
   const int64_t groups = (int64_t)a.units * ((a.max_ctx + kStageRows - 1) / kStageRows);
-  int64_t slots = resident_blocks(fn);
+  const bool wide = kind == ScoreKind::kHist && a.chunk <= 1;  // k_score<G, true>
+  int64_t slots = resident_blocks(fn, wide ? 64 * kHistScoreWaves : kScoreThreads);
   if (slots > kMaxScoreWgs) slots = kMaxScoreWgs;
   return (int)(groups < slots ? groups : slots);
 }
@@ -1390,7 +1398,7 @@ template <int G>
 static void launch_score_g(const ScoreArgs& a, bool hist, int nwg, hipStream_t s) {
   const dim3 grid(nwg), block(kScoreThreads);
   if (a.chunk > 1) launch_kernel(CKV_K_SCORE, k_score_chunks<G>, grid, block, s, a);
-  else if (hist) launch_kernel(CKV_K_SCORE, k_score<G, true>, grid, block, s, a);
+  else if (hist) launch_kernel(CKV_K_SCORE, k_score<G, true>, grid, dim3(64 * kHistScoreWaves), s, a);
   else launch_kernel(CKV_K_SCORE, k_score<G, false>, grid, block, s, a);
 }
 

@@ -18,13 +18,13 @@
 namespace ckv {
 
 // Adds the workgroup's LDS histogram into the unit's global fine and coarse
-// histograms (kScoreThreads threads, kHistBins bins, kBinsPerThread each).
+// histograms (NT threads, kHistBins bins, kBinsPerThread each).
+template <int NT = kScoreThreads>
 __device__ __forceinline__ void flush_hist(const uint32_t* lds_hist,
                                            uint32_t* g_hist,
                                            uint32_t* g_coarse) {
-  constexpr int kBinsPerThread = kHistBins / kScoreThreads;
+  constexpr int kBinsPerThread = kHistBins / NT;
   constexpr int kThreadsPerCoarse = kHistBins / kCoarseBins / kBinsPerThread;
-  static_assert(kThreadsPerCoarse == 4, "4 threads per coarse bin");
   const int t = threadIdx.x;
   uint32_t csum = 0;
 #pragma unroll
@@ -35,14 +35,15 @@ __device__ __forceinline__ void flush_hist(const uint32_t* lds_hist,
       csum += v;
     }
   }
-  csum += __shfl_xor(csum, 1);
-  csum += __shfl_xor(csum, 2);
-  if ((t & 3) == 0 && csum) atomicAdd(&g_coarse[t >> 2], csum);
+#pragma unroll
+  for (int o = 1; o < kThreadsPerCoarse; o <<= 1) csum += __shfl_xor(csum, o);
+  if ((t % kThreadsPerCoarse) == 0 && csum) atomicAdd(&g_coarse[t / kThreadsPerCoarse], csum);
 }
 
-// Stores the workgroup's LDS histogram as its slot (kScoreThreads threads).
+// Stores the workgroup's LDS histogram as its slot (NT threads).
+template <int NT = kScoreThreads>
 __device__ __forceinline__ void store_hist(const uint32_t* lds_hist, uint32_t* slot) {
-  constexpr int kPer = kHistBins / kScoreThreads;
+  constexpr int kPer = kHistBins / NT;
   static_assert(kPer % 4 == 0, "16-byte stores");
   const int t = threadIdx.x;
 #pragma unroll
@@ -52,8 +53,9 @@ __device__ __forceinline__ void store_hist(const uint32_t* lds_hist, uint32_t* s
 }
 
 // An empty slot, for a workgroup whose groups of the unit all lie past n_b.
+template <int NT = kScoreThreads>
 __device__ __forceinline__ void store_zero_hist(uint32_t* slot) {
-  for (int i = 4 * (int)threadIdx.x; i < kHistBins; i += 4 * kScoreThreads)
+  for (int i = 4 * (int)threadIdx.x; i < kHistBins; i += 4 * NT)
     *reinterpret_cast<uint4*>(slot + i) = make_uint4(0u, 0u, 0u, 0u);
 }
 
@@ -119,10 +121,11 @@ __device__ __forceinline__ void load_query(const ScoreArgs& a, int unit, bf16x8*
 // the unit, adds the counts to the unit's histogram or stores them as its own
 // slot (hist_part; an all-zero slot when its groups of the unit all lie at or
 // past n_b).  Groups at or beyond n_b only write -inf.  Must be called by all
-// kScoreThreads threads.
+// 64 * NW threads of the workgroup; lds_stage holds NW * (kStageDwords +
+// kFlushGroups * kStageRows) dwords.
 //
-// Memory path: the four waves take the range's groups round-robin (wave w
-// the groups w, w + 4, ...), so that the workgroup streams one region at a
+// Memory path: the NW waves take the range's groups round-robin (wave w the
+// groups w, w + NW, ...), so that the workgroup streams one region at a
 // time: with a contiguous quarter per wave the scan ran 5 % slower (four
 // times as many regions in flight over the device).  A wave reads each group
 // with fully coalesced 16-byte loads (one instruction = 4 whole 256-byte
@@ -138,10 +141,11 @@ __device__ __forceinline__ void load_query(const ScoreArgs& a, int unit, bf16x8*
 // one (loads and stores share one counter), and score writes interleaved
 // with the key stream cost bandwidth even in large batches: about 10 % at
 // every 16 groups against 2 % when written once.
-template <int G, bool HIST>
+template <int G, bool HIST, int NW = 4>
 __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
                                             uint32_t* lds_hist,
                                             uint32_t* lds_stage) {
+  constexpr int NT = 64 * NW;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lrow = lane >> 4, lchunk = lane & 15;
@@ -150,7 +154,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
   const int64_t total = (int64_t)a.units * gpu_groups;
   const int64_t g0 = total * wg / nwg, g1 = total * (wg + 1) / nwg;
   uint32_t* stage = lds_stage + wave * kStageDwords;
-  float* sbuf = reinterpret_cast<float*>(lds_stage + 4 * kStageDwords) +
+  float* sbuf = reinterpret_cast<float*>(lds_stage + NW * kStageDwords) +
                 wave * kFlushGroups * kStageRows;
 
   for (int64_t seg = g0; seg < g1;) {
@@ -167,7 +171,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
     }
     if (seg < valid_end) {  // uniform over the workgroup
       if (HIST) {
-        for (int i = tid; i < kHistBins; i += kScoreThreads) lds_hist[i] = 0u;
+        for (int i = tid; i < kHistBins; i += NT) lds_hist[i] = 0u;
         __syncthreads();
       }
       bf16x8 qa[4];
@@ -193,7 +197,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
         if ((a.max_ctx & 3) == 0) {
           for (int c = 4 * lane; c < count; c += 256) {
             const float4 v = *reinterpret_cast<const float4*>(sbuf + c);
-            const int j = jb + (c / kStageRows) * 4 * kStageRows + c % kStageRows;
+            const int j = jb + (c / kStageRows) * NW * kStageRows + c % kStageRows;
             if (j + 3 < a.max_ctx) {
               *reinterpret_cast<float4*>(srow + j) = v;
             } else {
@@ -204,7 +208,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
           }
         } else {
           for (int c = lane; c < count; c += 64) {
-            const int j = jb + (c / kStageRows) * 4 * kStageRows + c % kStageRows;
+            const int j = jb + (c / kStageRows) * NW * kStageRows + c % kStageRows;
             if (j < a.max_ctx) srow[j] = sbuf[c];
           }
         }
@@ -218,18 +222,18 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
       int nb = 0;
       if (gg < w1) load_group(gg, cur);
 #pragma unroll 1
-      for (; gg < w1; gg += 4) {
+      for (; gg < w1; gg += NW) {
 #pragma unroll
         for (int i = 0; i < kLoads; ++i)
           *reinterpret_cast<uint4*>(stage + (4 * i + lrow) * kStageRowDwords + 4 * lchunk) =
               cur[i];
-        if (gg + 4 < w1) load_group(gg + 4, nxt);
+        if (gg + NW < w1) load_group(gg + NW, nxt);
         __builtin_amdgcn_wave_barrier();
         score_group<G, HIST>(stage, qa, (int)(gg - ubase) * kStageRows, n, a.scale, lds_hist,
                              sbuf + nb * kStageRows);
         if (++nb == kFlushGroups) {
           flush(first, nb);
-          first = gg + 4;
+          first = gg + NW;
           nb = 0;
         }
         __builtin_amdgcn_wave_barrier();
@@ -240,14 +244,14 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
       if (HIST) {
         __syncthreads();
         if (a.hist_part)
-          store_hist(lds_hist, a.hist_part + ((int64_t)unit + wg) * kHistBins);
+          store_hist<NT>(lds_hist, a.hist_part + ((int64_t)unit + wg) * kHistBins);
         else
-          flush_hist(lds_hist, a.hist + (int64_t)unit * kHistBins,
-                     a.coarse + (int64_t)unit * kCoarseBins);
+          flush_hist<NT>(lds_hist, a.hist + (int64_t)unit * kHistBins,
+                         a.coarse + (int64_t)unit * kCoarseBins);
         __syncthreads();
       }
     } else if (HIST && a.hist_part) {  // the unit's histogram sums this slot too
-      store_zero_hist(a.hist_part + ((int64_t)unit + wg) * kHistBins);
+      store_zero_hist<NT>(a.hist_part + ((int64_t)unit + wg) * kHistBins);
     }
     seg = seg_end;
   }
