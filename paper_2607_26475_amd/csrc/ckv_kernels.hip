@@ -799,15 +799,15 @@ __global__ __launch_bounds__(kAttnThreads) void k_attn(AttnArgs a) {
 }
 
 // The scoring role of a pipelined launch: claims from a.claim (CLAIMS),
-// else the static ranges.  They are separate kernels so that each keeps its
-// own register allocation.
+// else the static ranges, each wave with half a group in flight.  They are
+// separate kernels so that each keeps its own register allocation.
 template <int G, bool CLAIMS>
 __device__ __forceinline__ void score_role(const ScoreArgs& a, int wg, int nwg, uint32_t* lds_hist,
                                            uint32_t* lds_stage, uint32_t* lds_claim) {
   if constexpr (CLAIMS)
     score_claims<G>(a, nwg, lds_hist, lds_stage, lds_claim);
   else
-    score_range<G, true>(a, wg, nwg, lds_hist, lds_stage);
+    score_range<G, true, 4, true>(a, wg, nwg, lds_hist, lds_stage);
 }
 
 // One launch, two roles (pipelined decode): the first attn_blocks workgroups

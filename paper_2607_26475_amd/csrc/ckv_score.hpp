@@ -141,7 +141,15 @@ __device__ __forceinline__ void load_query(const ScoreArgs& a, int unit, bf16x8*
 // one (loads and stores share one counter), and score writes interleaved
 // with the key stream cost bandwidth even in large batches: about 10 % at
 // every 16 groups against 2 % when written once.
-template <int G, bool HIST, int NW = 4>
+//
+// HALVES: a wave requests the next group in two halves, the second once the
+// first has landed (after scoring the current group), so that it has 4 KiB
+// rather than 8 KiB in flight.  That suits the scoring role of the one-launch
+// attend-and-score kernels, which share the memory system with the
+// attention's random row reads: 186-188 against 189-192 us per Llama-8B
+// layer, alternated over two sessions.  The 8-wave histogram pass is slower with it (167-170 against
+// 158-165 us), as it is with 16-row groups.
+template <int G, bool HIST, int NW = 4, bool HALVES = false>
 __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
                                             uint32_t* lds_hist,
                                             uint32_t* lds_stage) {
@@ -180,14 +188,16 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
       // Rows at or past n_b load row n_b - 1 instead (their scores are
       // replaced by -inf): lane-conditional loads would make the compiler
       // wait for every outstanding load at each use.
-      auto load_group = [&](int64_t gg, uint4* v) {
+      // loads [i0, i1) of a group's kLoads
+      auto load_part = [&](int64_t gg, uint4* v, int i0, int i1) {
         const int jb = (int)(gg - ubase) * kStageRows;
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
+        for (int i = i0; i < i1; ++i) {
           const int j = min(jb + 4 * i + lrow, n - 1);
           v[i] = ld16_nt(kunit + (int64_t)j * a.key_stride + 8 * lchunk);
         }
       };
+      auto load_group = [&](int64_t gg, uint4* v) { load_part(gg, v, 0, kLoads); };
       // writes the scores of the nb buffered groups [first, first + nb): one
       // contiguous run, 16 bytes per lane when rows are 16-byte aligned
       auto flush = [&](int64_t first, int nb) {
@@ -227,10 +237,15 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
         for (int i = 0; i < kLoads; ++i)
           *reinterpret_cast<uint4*>(stage + (4 * i + lrow) * kStageRowDwords + 4 * lchunk) =
               cur[i];
-        if (gg + NW < w1) load_group(gg + NW, nxt);
+        const bool more = gg + NW < w1;
+        if (more) load_part(gg + NW, nxt, 0, HALVES ? kLoads / 2 : kLoads);
         __builtin_amdgcn_wave_barrier();
         score_group<G, HIST>(stage, qa, (int)(gg - ubase) * kStageRows, n, a.scale, lds_hist,
                              sbuf + nb * kStageRows);
+        if (HALVES && more) {
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          load_part(gg + NW, nxt, kLoads / 2, kLoads);
+        }
         if (++nb == kFlushGroups) {
           flush(first, nb);
           first = gg + NW;
