@@ -488,13 +488,14 @@ int check_chunk(int32_t chunk, int32_t k) {
   return CKV_OK;
 }
 
-// Chunk selection into caller arrays; `Lc` is the layout of the chunk problem
-// (one entry per chunk, budget k / chunk), which fits inside the layout of
-// the row problem that the caller's workspace was sized for.
-int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
-                      const uint16_t* landmarks, const int32_t* ctx_lens, int32_t k,
-                      float scale, int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
-                      int32_t* n_rows, void* ws, hipStream_t s) {
+// Scores every chunk landmark of the chunk problem (one entry per chunk,
+// budget k / chunk), whose layout fits inside the layout of the row problem
+// that the caller's workspace was sized for; sets *sa to that problem's
+// selection into chunk_idx / n_chunks and *e to the expansion of its chunks.
+int score_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
+                 const uint16_t* landmarks, const int32_t* ctx_lens, int32_t k, float scale,
+                 int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows, int32_t* n_rows,
+                 void* ws, hipStream_t s, SelectArgs* sa, ExpandArgs* e) {
   Dims dc = d;
   dc.max_ctx = (d.max_ctx + chunk - 1) / chunk;
   dc.key_stride = kD;
@@ -503,30 +504,54 @@ int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
   int rc;
   if ((rc = check_grid(dc, Lc))) return rc;
   float* scores = at<float>(ws, Lc.scores);
-  SelectArgs sa = select_args(dc, Lc, ws, scores, ctx_lens, kc, chunk_idx, n_chunks);
-  sa.chunk = chunk;
-  ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, &sa);
+  *sa = select_args(dc, Lc, ws, scores, ctx_lens, kc, chunk_idx, n_chunks);
+  sa->chunk = chunk;
+  ScoreArgs sc = score_args(dc, Lc, q_sel, landmarks, ctx_lens, scale, scores, sa);
   sc.chunk = chunk;
   const int nwg = score_blocks(sc, d.G, ScoreKind::kHist);
   if (use_partials(dc, Lc, nwg))
-    set_partials(ws, Lc, nwg, &sc, &sa);
+    set_partials(ws, Lc, nwg, &sc, sa);
   else
     CKV_TRY_HIP(launch_zero(ws, Lc.zero_end, s), "zero launch");
   CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
-  if ((rc = run_select_tail(sa, d.U, s))) return rc;
+  e->chunk_idx = chunk_idx;
+  e->n_chunks = n_chunks;
+  e->ctx_lens = ctx_lens;
+  e->rows = rows;
+  e->n_rows = n_rows;
+  e->Hkv = d.Hkv;
+  e->max_ctx = d.max_ctx;
+  e->chunk = chunk;
+  e->kc = kc;
+  e->k = k;
+  return CKV_OK;
+}
+
+// Chunk selection into caller arrays: the scoring above, the selection, and
+// the expansion to rows.
+int run_select_chunks(const Dims& d, int32_t chunk, const uint16_t* q_sel,
+                      const uint16_t* landmarks, const int32_t* ctx_lens, int32_t k,
+                      float scale, int32_t* chunk_idx, int32_t* n_chunks, int32_t* rows,
+                      int32_t* n_rows, void* ws, hipStream_t s) {
+  SelectArgs sa;
   ExpandArgs e;
-  e.chunk_idx = chunk_idx;
-  e.n_chunks = n_chunks;
-  e.ctx_lens = ctx_lens;
-  e.rows = rows;
-  e.n_rows = n_rows;
-  e.Hkv = d.Hkv;
-  e.max_ctx = d.max_ctx;
-  e.chunk = chunk;
-  e.kc = kc;
-  e.k = k;
+  int rc = score_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx, n_chunks,
+                        rows, n_rows, ws, s, &sa, &e);
+  if (rc) return rc;
+  if ((rc = run_select_tail(sa, d.U, s))) return rc;
   CKV_TRY_HIP(launch_expand(e, d.U, s), "expand launch");
   return CKV_OK;
+}
+
+// Whether the same-step chunked call selects, expands and attends in one
+// launch (k_select_attn_chunks): the conditions of the head-halves form of
+// the fused same-step launch, on the chunk problem's context, with one
+// thread per selected chunk.
+bool chunk_select_attn(const Dims& d, int32_t chunk, int32_t k) {
+  const int64_t cmax = (d.max_ctx + chunk - 1) / chunk;
+  return cmax <= kFusedSelectMaxCtx && d.G <= 8 && d.G % 2 == 0 && k >= 512 &&
+         k <= kSelAttnMaxShare && k / chunk <= kFinishThreads &&
+         2 * (int64_t)d.U <= device_cus();
 }
 
 }  // namespace
@@ -1085,12 +1110,21 @@ int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q
   if (d.U == 0) return CKV_OK;
   CKV_DEBUG_CHECK(stream, ctx_lens, nullptr, nullptr, k);
   hipStream_t s = (hipStream_t)stream;
-  if ((rc = run_select_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx,
-                              n_chunks, rows, n_rows, ws, s)))
-    return rc;
   // the partials live past everything the chunk selection used
   AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, rows, n_rows, d.kv_stride, k, scale,
                            out);
+  if (chunk > 1 && chunk_select_attn(d, chunk, k)) {
+    SelectArgs sa;
+    ExpandArgs e;
+    if ((rc = score_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx, n_chunks,
+                           rows, n_rows, ws, s, &sa, &e)))
+      return rc;
+    CKV_TRY_HIP(launch_select_attn_chunks(sa, at_, e, d.G, s), "chunk select-attention launch");
+    return CKV_OK;
+  }
+  if ((rc = run_select_chunks(d, chunk, q_sel, landmarks, ctx_lens, k, scale, chunk_idx,
+                              n_chunks, rows, n_rows, ws, s)))
+    return rc;
   return run_attention(at_, d, true, s);
 }
 

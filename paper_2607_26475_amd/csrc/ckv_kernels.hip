@@ -675,6 +675,54 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
               lds, lds + Lds::kQOff, qh0);
 }
 
+// Same-step over chunks (Sec. 2.2): sa is the chunk problem (one landmark
+// score per chunk of sa.chunk rows, budget k / chunk), at the attention over
+// rows.  Like k_select_attn with head halves, each of the unit's two
+// workgroups selects the unit's chunks, then expands them in LDS to the rows
+// below n_b and attends over all of them with half of the group's heads.
+// The first workgroup also writes the chunk list (sa.idx, sa.n_sel) and the
+// rows as k_expand does: e.rows[i] = row i of the ascending expansion, -1 at
+// or past n_b and past the last chunk, and e.n_rows.  Needs k / chunk <=
+// kFinishThreads and k <= kSelAttnMaxShare.
+template <int G>
+__global__ __launch_bounds__(kFinishThreads) void k_select_attn_chunks(SelectArgs sa,
+                                                                         AttnArgs at,
+                                                                         ExpandArgs e) {
+  constexpr int GA = G / 2;
+  using Lds = SelAttnLds<GA>;
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Lds::kDwords];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  const int tid = threadIdx.x;
+  int unit, split;
+  split_block(blockIdx.x, 2, &unit, &split);
+  if (unit >= sa.units) return;  // uniform over the workgroup
+  const SelLds L{reinterpret_cast<uint2*>(lds), lds + 2 * kCandLds,
+                 lds + 2 * kCandLds + kFusedSelectMaxCtx / 32, tmp, misc};
+  int32_t* list = reinterpret_cast<int32_t*>(lds + Lds::kPosOff);
+  const int nc = unit_len(sa.ctx_lens[unit / sa.Hkv], sa.max_ctx, sa.chunk);
+  const int m = select_unit(sa, unit, L, split == 0, list, 0u, (uint32_t)min(sa.k, nc), false);
+  __syncthreads();
+  // chunk tid's number, then its rows in place (chunk c of the list holds
+  // list slots [c * chunk, c * chunk + chunk))
+  const int C = e.chunk;
+  const int n = clamp_len(e.ctx_lens[unit / e.Hkv], e.max_ctx);
+  const int c_mine = tid < m ? list[tid] : -1;
+  const int c_last = m > 0 ? list[m - 1] : 0;
+  __syncthreads();
+  if (c_mine >= 0)
+    for (int r = 0; r < C; ++r) list[tid * C + r] = c_mine * C + r;
+  const int rows = m == 0 ? 0 : (m - 1) * C + max(0, min(C, n - c_last * C));
+  __syncthreads();
+  if (split == 0) {
+    int32_t* out_rows = e.rows + (int64_t)unit * e.k;
+    for (int i = tid; i < e.k; i += kFinishThreads) out_rows[i] = i < rows ? list[i] : -1;
+    if (tid == 0) e.n_rows[unit] = rows;
+  }
+  const int qh0 = (unit % sa.Hkv) * G + split * GA;
+  attn_wg<GA>(at, unit, LdsRows{list}, rows, 0, 1, lds, lds + Lds::kQOff, qh0);
+}
+
 // ---- read-rate probe --------------------------------------------------------
 // Reads rows pos(i0) .. pos(i1) of a unit (positions clamped to the unit's
 // rows) as the attention does: 4 rows per load instruction, K and V of a
@@ -1552,6 +1600,20 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
     }
   }
 #undef CKV_SA
+  return launch_status();
+}
+
+hipError_t launch_select_attn_chunks(const SelectArgs& sa, const AttnArgs& at,
+                                    const ExpandArgs& e, int G, hipStream_t s) {
+  if (G % 2 || sa.k > kFinishThreads || e.k > kSelAttnMaxShare || e.chunk < 2)
+    return hipErrorInvalidValue;
+  const dim3 grid((sa.units + 7) / 8 * 8 * 2), block(kFinishThreads);
+  switch (G) {
+    case 2: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn_chunks<2>, grid, block, s, sa, at, e); break;
+    case 4: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn_chunks<4>, grid, block, s, sa, at, e); break;
+    case 8: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn_chunks<8>, grid, block, s, sa, at, e); break;
+    default: return hipErrorInvalidValue;
+  }
   return launch_status();
 }
 

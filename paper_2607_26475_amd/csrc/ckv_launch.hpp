@@ -67,6 +67,10 @@ hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStr
 // the heads each over the whole set, outputs written directly
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
                               int heads, hipStream_t s);
+// the same over chunks (sa: the chunk problem, k / chunk <= kFinishThreads;
+// e: the rows written as k_expand writes them; G even, k <= kSelAttnMaxShare)
+hipError_t launch_select_attn_chunks(const SelectArgs& sa, const AttnArgs& at,
+                                    const ExpandArgs& e, int G, hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
 // The one-launch attend-and-score kernel: attention over the buffer or rows in
 // place (indexed) with G head rows, or with the 2G rows of two tokens when

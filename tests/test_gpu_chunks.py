@@ -8,6 +8,8 @@ against the oracle's attention over the GPU's rows.
 """
 from __future__ import annotations
 
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -57,8 +59,26 @@ def test_landmarks_exact(wl, chunk, interleaved):
     assert np.array_equal(lm, ref)
 
 
+# contexts of 700..1500 rows: at k 2048 every chunk of every unit is selected
+# and the last chunk is partial in most units
+EXTRA = {"short_s": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="short_s",
+                                        max_ctx=1500, ctx_min=700)}
+
+
+def _workload(wl):
+    return EXTRA[wl] if wl in EXTRA else synth.WORKLOADS[wl]
+
+
+def _fused(w, chunk, k, dev):
+    """Whether the call selects, expands and attends in one launch."""
+    G = w.q_heads // w.kv_heads
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    return (chunk > 1 and G % 2 == 0 and G <= 8 and 512 <= k <= 2048 and k // chunk <= 1024
+            and 2 * w.batch * w.kv_heads <= cus)
+
+
 def _chunk_case(wl, chunk, k, seed, dev):
-    w = synth.WORKLOADS[wl]
+    w = _workload(wl)
     t = synth.make_layer(w, seed=seed, device=dev)
     s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
     lm = _landmarks(s, chunk, t["k"], t["ctx_lens"], dev)
@@ -74,9 +94,14 @@ def _oracle_chunk_scores(w, chunk, q_sel_h, lm_h, lens_h):
 
 
 @pytest.mark.parametrize("wl,chunk,k", [
-    ("tiny", 16, 256), ("llama8b_s", 4, 256), ("llama8b_s", 7, 252), ("dual64_s", 8, 256)])
+    ("tiny", 16, 256), ("llama8b_s", 4, 256), ("llama8b_s", 7, 252), ("dual64_s", 8, 256),
+    # one launch selects, expands and attends (head halves)
+    ("llama8b_s", 8, 512), ("llama8b_s", 4, 2048), ("llama8b_s", 7, 700),
+    ("long128k_s", 16, 1024), ("short_s", 8, 2048), ("dual64_s", 2, 2048)])
 def test_chunked_kv_attn(wl, chunk, k):
-    """Same-step chunked decode: chunk set, rows and output."""
+    """Same-step chunked decode: chunk set, rows and output, through the
+    separate selection, expansion and attention kernels for small budgets and
+    through the one-launch form for the others."""
     _log("chunked", wl, chunk, k)
     dev = device()
     w, t, s, lm = _chunk_case(wl, chunk, k, 5, dev)
@@ -88,9 +113,13 @@ def test_chunked_kv_attn(wl, chunk, k):
     out = torch.full((B, Hq, d), float("nan"), device=dev)
     ws = ckv.workspace(s, k, ckv.ENTRY_CRITICAL_KV_ATTN)
     ws.fill_(0xA5)
+    ckv.profile_begin()
     ckv.chunked_kv_attn(s, chunk, t["q"], t["q_sel"], lm, t["ctx_lens"], k, SCALE, t["k"],
                         t["v"], ckv.SRC_DEVICE, cidx, nch, rows, nrows, out, ws)
+    kernels = ckv.profile_end()
     torch.cuda.synchronize()
+    fused = _fused(w, chunk, k, dev)
+    assert ("select_attn" in kernels) == fused and ("expand" in kernels) != fused, kernels
     lens_h = t["ctx_lens"].cpu().numpy()
     lm_h = lm.cpu().numpy().view(np.uint16)
     q_sel_h, q_att_h, K, V = u16(t["q_sel"]), u16(t["q"]), u16(t["k"]), u16(t["v"])
