@@ -77,9 +77,11 @@ def _fused(w, chunk, k, dev):
             and 2 * w.batch * w.kv_heads <= cus)
 
 
-def _chunk_case(wl, chunk, k, seed, dev):
+def _chunk_case(wl, chunk, k, seed, dev, lens=None):
     w = _workload(wl)
     t = synth.make_layer(w, seed=seed, device=dev)
+    if lens is not None:  # context lengths of the batch's requests, replaced
+        t["ctx_lens"] = torch.tensor(lens, dtype=torch.int32, device=dev)
     s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
     lm = _landmarks(s, chunk, t["k"], t["ctx_lens"], dev)
     return w, t, s, lm
@@ -93,18 +95,21 @@ def _oracle_chunk_scores(w, chunk, q_sel_h, lm_h, lens_h):
     return o.score_keys(sc, q_sel_h, lm_h, clens, SCALE, nthreads=8), clens
 
 
-@pytest.mark.parametrize("wl,chunk,k", [
-    ("tiny", 16, 256), ("llama8b_s", 4, 256), ("llama8b_s", 7, 252), ("dual64_s", 8, 256),
+@pytest.mark.parametrize("wl,chunk,k,lens", [
+    ("tiny", 16, 256, None), ("llama8b_s", 4, 256, None), ("llama8b_s", 7, 252, None),
+    ("dual64_s", 8, 256, None), ("llama8b_s", 8, 256, (0, 5)),
     # one launch selects, expands and attends (head halves)
-    ("llama8b_s", 8, 512), ("llama8b_s", 4, 2048), ("llama8b_s", 7, 700),
-    ("long128k_s", 16, 1024), ("short_s", 8, 2048), ("dual64_s", 2, 2048)])
-def test_chunked_kv_attn(wl, chunk, k):
+    ("llama8b_s", 8, 512, None), ("llama8b_s", 4, 2048, None), ("llama8b_s", 7, 700, None),
+    ("long128k_s", 16, 1024, None), ("short_s", 8, 2048, None), ("dual64_s", 2, 2048, None),
+    # empty contexts, one partial chunk, a partial last chunk
+    ("llama8b_s", 8, 512, (0, 5)), ("llama8b_s", 8, 512, (13, 4999))])
+def test_chunked_kv_attn(wl, chunk, k, lens):
     """Same-step chunked decode: chunk set, rows and output, through the
     separate selection, expansion and attention kernels for small budgets and
     through the one-launch form for the others."""
-    _log("chunked", wl, chunk, k)
+    _log("chunked", wl, chunk, k, lens)
     dev = device()
-    w, t, s, lm = _chunk_case(wl, chunk, k, 5, dev)
+    w, t, s, lm = _chunk_case(wl, chunk, k, 5, dev, lens)
     B, Hq, Hkv, d = w.batch, w.q_heads, w.kv_heads, w.head_dim
     kc = k // chunk
     i32 = dict(dtype=torch.int32, device=dev)
