@@ -1022,6 +1022,11 @@ int ckv_dual_token_attn(const ckv_shape* shape, const uint16_t* q_cur, const uin
   a.out2 = out_spec;
   a.k_local = k_local;
   a.v_local = v_local;
+  if (2 * (int64_t)d.U <= device_cus() && k >= 512) {
+    // a workgroup per token and unit, each over all of the unit's rows
+    CKV_TRY_HIP(launch_dual_token_wg(a, d.G, d.U, s), "dual-token attention launch");
+    return CKV_OK;
+  }
   // one launch reads each selected row once for the 2G head rows of both tokens
   CKV_TRY_HIP(launch_attn(a, 2 * d.G, false, d.U, s), "attention launch");
   CKV_TRY_HIP(launch_combine(a, 2 * d.G, d.U, s), "combine launch");

@@ -306,7 +306,7 @@ struct WgAttnLds {
   static constexpr int kStages = (kFinishThreads / 64) * kPerWave;  // dwords
   static constexpr int kQ = 16 * kStageRowDwords;       // query rows in the A placement
   static constexpr int kMerge = (kFinishThreads / 64) * G * (kD + 2);  // floats, in the stages
-  static_assert(kMerge <= kStages, "the 16 waves' states fit in the stages");
+  static_assert(kMerge + 2 * G <= kStages, "the 16 waves' states and 2 local logits per head fit in the stages");
   static_assert(kPerWave % 4 == 0, "16-byte aligned stages");
 };
 
@@ -329,11 +329,16 @@ struct LdsRows {
 // dwords, qlds: kQ dwords (both free on entry); pos(i): the source row of
 // the share's row i, clamped to [0, a.max_ctx).  The workgroup attends with
 // the G query heads qh0 .. qh0 + G - 1 of the unit's request (qh0 = h * G
-// for a KV head's whole group).
+// for a KV head's whole group).  With nloc > 0 (nsplit 1 only) the heads also
+// see the nloc rows k_loc / v_loc ([nloc][d] bf16) beside the share's rows:
+// the token's own rows in dual-token decoding (Sec. 5.2), which join the
+// final merge as one more partial per head.
 template <int G, class Rows>
 __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, int nrows,
                                         int split, int nsplit, uint32_t* stages,
-                                        uint32_t* qlds, int qh0) {
+                                        uint32_t* qlds, int qh0,
+                                        const uint16_t* k_loc = nullptr,
+                                        const uint16_t* v_loc = nullptr, int nloc = 0) {
   using Lds = WgAttnLds<G>;
   static_assert(G <= 8, "16 waves' states of at most 8 heads fit in the stages");
   constexpr int kW = kFinishThreads / 64;
@@ -485,12 +490,26 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
       }
     }
   }
+  // logits of the local rows, one wave per (head, row): lane l takes
+  // channels 2l and 2l + 1
+  float* loc = merge + kW * G * (kD + 2);  // [G][2]
+  if (wave < G * nloc) {  // uniform over the wave
+    const int g = wave / nloc, j = wave - g * nloc;
+    const uint32_t qw = qlds[g * kStageRowDwords + lane];
+    const uint32_t kw = reinterpret_cast<const uint32_t*>(k_loc + j * kD)[lane];
+    float dot = __uint_as_float(qw << 16) * __uint_as_float(kw << 16);
+    dot = fmaf(__uint_as_float(qw & 0xffff0000u), __uint_as_float(kw & 0xffff0000u), dot);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) dot += __shfl_xor(dot, o);
+    if (lane == 0) loc[g * 2 + j] = dot * a.scale;
+  }
   __syncthreads();
   for (int oi = tid; oi < G * kD; oi += kFinishThreads) {
     const int g = oi / kD, c = oi - g * kD;
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kW; ++w) M = fmaxf(M, merge[(w * G + g) * (kD + 2) + kD]);
+    for (int j = 0; j < nloc; ++j) M = fmaxf(M, loc[g * 2 + j]);
     float O = 0.f, L = 0.f;
 #pragma unroll
     for (int w = 0; w < kW; ++w) {
@@ -498,6 +517,11 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
       const float wt = mg[kD] == -INFINITY ? 0.f : __expf(mg[kD] - M);
       O = fmaf(wt, mg[c], O);
       L = fmaf(wt, mg[kD + 1], L);
+    }
+    for (int j = 0; j < nloc; ++j) {
+      const float wt = __expf(loc[g * 2 + j] - M);
+      O = fmaf(wt, __uint_as_float((uint32_t)v_loc[j * kD + c] << 16), O);
+      L += wt;
     }
     if (nsplit == 1) {
       a.out[((int64_t)b * a.Hq + qh0 + g) * kD + c] = L > 0.f ? O / L : 0.f;

@@ -723,6 +723,38 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn_chunks(SelectArg
   attn_wg<GA>(at, unit, LdsRows{list}, rows, 0, 1, lds, lds + Lds::kQOff, qh0);
 }
 
+// Co-batched dual-token attention over an assembled buffer (Sec. 5.2) when
+// two workgroups per unit fit on the CUs: the unit's first workgroup attends
+// with the current token's G heads, the second with the speculative token's,
+// each over all of the unit's rows (buffer slots 0 .. n_sel - 1; the second
+// read of a row mostly comes from the XCD's L2, both workgroups being on the
+// same XCD), and each merges its token's own rows under the causal mask
+// (current: row 0; speculative: rows 0 and 1) into its outputs.  No partials
+// and no merge launch.
+struct SlotRows {
+  __device__ __forceinline__ int operator()(int i) const { return i; }
+};
+
+template <int G>
+__global__ __launch_bounds__(kFinishThreads) void k_dual_token_wg(AttnArgs a, int units) {
+  using Lds = WgAttnLds<G>;
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Lds::kStages + Lds::kQ];
+  int unit, tok;
+  split_block(blockIdx.x, 2, &unit, &tok);
+  if (unit >= units) return;  // uniform over the workgroup
+  AttnArgs t = a;
+  t.max_ctx = a.k;  // the unit's buffer rows
+  if (tok) {
+    t.q = a.q2;
+    t.out = a.out2;
+  }
+  const int n = clamp_len(a.n_sel[unit], a.k);
+  const uint16_t* kl = a.k_local + (int64_t)unit * 2 * kD;
+  const uint16_t* vl = a.v_local + (int64_t)unit * 2 * kD;
+  attn_wg<G>(t, unit, SlotRows{}, n, 0, 1, lds, lds + Lds::kStages, (unit % a.Hkv) * G, kl, vl,
+             tok ? 2 : 1);
+}
+
 // ---- read-rate probe --------------------------------------------------------
 // Reads rows pos(i0) .. pos(i1) of a unit (positions clamped to the unit's
 // rows) as the attention does: 4 rows per load instruction, K and V of a
@@ -1612,6 +1644,18 @@ hipError_t launch_select_attn_chunks(const SelectArgs& sa, const AttnArgs& at,
     case 2: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn_chunks<2>, grid, block, s, sa, at, e); break;
     case 4: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn_chunks<4>, grid, block, s, sa, at, e); break;
     case 8: launch_kernel(CKV_K_SELECT_ATTN, k_select_attn_chunks<8>, grid, block, s, sa, at, e); break;
+    default: return hipErrorInvalidValue;
+  }
+  return launch_status();
+}
+
+hipError_t launch_dual_token_wg(const AttnArgs& a, int G, int units, hipStream_t s) {
+  const dim3 grid((units + 7) / 8 * 8 * 2), block(kFinishThreads);
+  switch (G) {
+    case 1: launch_kernel(CKV_K_ATTN, k_dual_token_wg<1>, grid, block, s, a, units); break;
+    case 2: launch_kernel(CKV_K_ATTN, k_dual_token_wg<2>, grid, block, s, a, units); break;
+    case 4: launch_kernel(CKV_K_ATTN, k_dual_token_wg<4>, grid, block, s, a, units); break;
+    case 8: launch_kernel(CKV_K_ATTN, k_dual_token_wg<8>, grid, block, s, a, units); break;
     default: return hipErrorInvalidValue;
   }
   return launch_status();

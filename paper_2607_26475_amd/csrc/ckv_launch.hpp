@@ -72,6 +72,9 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
 hipError_t launch_select_attn_chunks(const SelectArgs& sa, const AttnArgs& at,
                                     const ExpandArgs& e, int G, hipStream_t s);
 hipError_t launch_combine(const AttnArgs& a, int G, int units, hipStream_t s);
+// co-batched dual-token attention over the assembled buffer, two workgroups
+// per unit (one per token), outputs written directly (G heads per token)
+hipError_t launch_dual_token_wg(const AttnArgs& a, int G, int units, hipStream_t s);
 // The one-launch attend-and-score kernel: attention over the buffer or rows in
 // place (indexed) with G head rows, or with the 2G rows of two tokens when
 // at.q2 is set; scoring with G heads on nwg workgroups.

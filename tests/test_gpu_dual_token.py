@@ -14,8 +14,11 @@ from helpers import ATOL_OUT, SCALE, device, orc
 pytestmark = pytest.mark.gpu
 
 
+# k >= 512 (two workgroups per unit fit): a workgroup per token over all rows,
+# the own rows merged in the same launch; smaller k: 2G head rows per chunk
+# workgroup and the merge launch
 @pytest.mark.parametrize("Hq,Hkv,k", [(32, 8, 300), (8, 8, 256), (16, 8, 512), (64, 8, 2048),
-                                      (16, 2, 1000)])
+                                      (16, 2, 1000), (32, 8, 1024), (8, 8, 600)])
 def test_dual_token_attn(Hq, Hkv, k):
     print("dual token", Hq, Hkv, k, flush=True)
     dev = device()
@@ -37,9 +40,12 @@ def test_dual_token_attn(Hq, Hkv, k):
     ws = ckv.workspace(s, k, ckv.ENTRY_DUAL_TOKEN_ATTN)
     out_c = torch.full((B, Hq, d), float("nan"), device=dev)
     out_s = torch.full_like(out_c, float("nan"))
+    ckv.profile_begin()
     ckv.dual_token_attn(s, q_cur, q_spec, k_buf, v_buf, n_sel, k_loc, v_loc, k, SCALE, out_c,
                         out_s, ws)
+    kernels = ckv.profile_end()
     torch.cuda.synchronize()
+    assert ("combine" in kernels) == (k < 512), kernels
     u = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     o = orc()
     so = o.shape(B, Hq, Hkv, d, 4096)
