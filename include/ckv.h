@@ -419,7 +419,9 @@ int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups);
 
 /* For tests of the event protocol only, never for serving: breaks the
  * loop's ordering on purpose, so that a test can show that it would see a
- * missing wait.  CKV_PIPE_CHECK_NO_FILL_WAIT: the compute stream does not
+ * missing wait (CKV_PIPE_CHECK_NO_DEFER only changes where selections run:
+ * every plain layer of the loop without buffers runs its own selection, as
+ * with a smaller workspace, for comparing the two forms).  CKV_PIPE_CHECK_NO_FILL_WAIT: the compute stream does not
  * wait for a buffer's fill before attending over it (read-after-write);
  * CKV_PIPE_CHECK_NO_RELEASE_WAIT: the copy stream does not wait for a
  * buffer's release before refilling it (write-after-read);
@@ -431,6 +433,7 @@ int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups);
 #define CKV_PIPE_CHECK_NO_FILL_WAIT 1u
 #define CKV_PIPE_CHECK_NO_RELEASE_WAIT 2u
 #define CKV_PIPE_CHECK_POISON 4u
+#define CKV_PIPE_CHECK_NO_DEFER 8u
 int ckv_pipeline_set_checks(ckv_pipeline* pipe, unsigned flags);
 
 /* Starts a decode loop: gathers layer 0 (into buffer 0) and layer 1 (into
@@ -461,7 +464,13 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
  * CKV_ENTRY_CRITICAL_KV_ATTN, or of CKV_ENTRY_CORRECTED_ATTN if any layer
  * has idx_true set, or of CKV_ENTRY_DECODE_STEP (which serves every layer
  * kind) if any layer is chunked or has two tokens; it is used on the compute
- * stream only.  A chunked or two-token layer runs the same pipelined step
+ * stream only.  Without buffers and with the workspace of
+ * CKV_ENTRY_DECODE_STEP, a plain layer followed by a plain layer leaves its
+ * selection (idx_next, n_sel_next: not read before the next step) to the
+ * next layer's launch, which runs it beside that layer's attention and
+ * scoring; its own attention partials are then merged by a merge launch.
+ * The last layer's pending selection runs before the call returns, and
+ * before any chunked or two-token layer.  Results are the same either way.  A chunked or two-token layer runs the same pipelined step
  * (one launch attends over the previous set and scores for the next one) with
  * its selection over chunk landmarks or its second token; such a layer with
  * idx_true set is CKV_EINVAL.

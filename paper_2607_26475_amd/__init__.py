@@ -414,11 +414,12 @@ class Pipeline:
         except Exception:
             pass
 
-    CHECK_NO_FILL_WAIT, CHECK_NO_RELEASE_WAIT, CHECK_POISON = 1, 2, 4
+    CHECK_NO_FILL_WAIT, CHECK_NO_RELEASE_WAIT, CHECK_POISON, CHECK_NO_DEFER = 1, 2, 4, 8
 
     def set_checks(self, flags: int) -> None:
         """Tests of the event protocol only: skip the fill or release waits,
-        or poison released buffers (see ckv_pipeline_set_checks)."""
+        or poison released buffers; or run every selection in its own layer's
+        call (CHECK_NO_DEFER; see ckv_pipeline_set_checks)."""
         _check("ckv_pipeline_set_checks", _lib.ckv_pipeline_set_checks(self._h, flags))
 
     def set_gather_width(self, workgroups: int) -> None:

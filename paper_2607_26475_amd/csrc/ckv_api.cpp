@@ -171,6 +171,7 @@ struct Layout {
   size_t sel = 0, cand = 0, bitmap = 0, scores = 0, part = 0, hist_part = 0, hist_part_bytes = 0;
   size_t slot_of = 0, miss_pos = 0, miss_slot = 0, n_miss = 0, free_slot = 0, total = 0;
   size_t chunk_idx = 0, n_chunks = 0;  // decode step: selected chunks of a chunked layer
+  size_t scores_b = 0, hist_part_b = 0;  // decode step: the second scores and slots region
   int64_t bm_words = 0;
   int chunks = 0, filter_tiles = 0;
 };
@@ -250,6 +251,12 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
     off += align256(U * (size_t)k * 4);
     L.n_chunks = off;
     off += align256(U * 4);
+    // consecutive plain layers of the decode loop alternate between the
+    // scores and slots above (at the fused entry's offsets) and these
+    L.scores_b = off;
+    off = align256(off + U * (size_t)d.max_ctx * 4);
+    L.hist_part_b = off;
+    off = align256(off + L.hist_part_bytes);
   }
   L.total = off;
   return L;
@@ -889,7 +896,8 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
                        const uint16_t* k_src, const uint16_t* v_src, int src_kind,
                        const int32_t* idx_in, const uint16_t* k_buf, const uint16_t* v_buf,
                        const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out,
-                       float* out, void* ws, size_t ws_bytes, void* stream, bool hist_clean) {
+                       float* out, void* ws, size_t ws_bytes, void* stream, bool hist_clean,
+                       LoopLink* link) {
   Dims d;
   int rc = check_shape(shape, &d);
   if (rc) return rc;
@@ -921,18 +929,37 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
   Layout L = make_layout(d, k, CKV_ENTRY_CRITICAL_KV_ATTN);
   if ((rc = check_grid(d, L))) return rc;
   if ((rc = check_ws(ws, ws_bytes, L))) return rc;
+  const bool pipelined = assembled || in_place;
+  if (link && !pipelined) return fail(CKV_EINVAL, "a loop link needs a pipelined call");
+  if (link && link->alt) {  // this layer's scores and slots in the second region
+    const Layout Ls = make_layout(d, k, CKV_ENTRY_DECODE_STEP);
+    if ((rc = check_ws(ws, ws_bytes, Ls))) return rc;
+    L.scores = Ls.scores_b;
+    L.hist_part = Ls.hist_part_b;
+  }
   if (d.U == 0) return CKV_OK;
   CKV_DEBUG_CHECK(stream, ctx_lens, idx_in, n_sel_in, k);
   hipStream_t s = (hipStream_t)stream;
   float* scores = at<float>(ws, L.scores);
   SelectArgs sa = select_args(d, L, ws, scores, ctx_lens, k, idx_out, n_sel_out);
   ScoreArgs sc = score_args(d, L, q_sel, k_score, ctx_lens, scale, scores, &sa);
-  const bool pipelined = assembled || in_place;
-  const int nwg = score_blocks(
+  int nwg = score_blocks(
       sc, d.G, !pipelined ? ScoreKind::kHist : in_place ? ScoreKind::kDualIndexed : ScoreKind::kDual);
+  bool partials = use_partials(d, L, nwg);
+  // the previous layer's pending selection joins this launch when this
+  // launch is the one-token kernel with static ranges and slots
+  bool fold = false;
+  if (link && link->prev) {
+    const int nwg_sel = score_blocks(
+        sc, d.G, in_place ? ScoreKind::kDualSelIndexed : ScoreKind::kDualSel);
+    fold = partials && nwg_sel > 0 && use_partials(d, L, nwg_sel) &&
+           d.max_ctx <= kFusedSelectMaxCtx && link->prev->units == d.U;
+    if (fold) nwg = nwg_sel;
+    else CKV_TRY_HIP(launch_select_fused(*link->prev, link->prev->units, s), "select launch");
+  }
   // a pipelined call whose caller knows the histograms clear (the previous
   // selection on this workspace left them so) skips the clearing kernel
-  if (use_partials(d, L, nwg))
+  if (partials)
     set_partials(ws, L, nwg, &sc, &sa);
   else if (!(pipelined && hist_clean))
     CKV_TRY_HIP(launch_zero(ws, L.zero_end, s), "zero launch");
@@ -941,8 +968,20 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
                                          k, scale, out)
                              : attn_args(d, L, ws, q_att, k_src, v_src, idx_in, n_sel_in,
                                          d.kv_stride, k, scale, out);
-    CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
-    if ((rc = select_and_merge(sa, at_, d, s))) return rc;
+    if (fold)
+      CKV_TRY_HIP(launch_dual_sel(at_, sc, *link->prev, d.G, in_place, d.U, nwg, s),
+                  "dual launch");
+    else
+      CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
+    if (link && link->next && partials && d.max_ctx <= kFusedSelectMaxCtx) {
+      // the next layer's launch selects this layer's sets; the partials are
+      // merged now
+      CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+      *link->next = sa;
+      link->deferred = true;
+    } else if ((rc = select_and_merge(sa, at_, d, s))) {
+      return rc;
+    }
   } else {
     CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
@@ -1134,6 +1173,12 @@ int ckv_chunked_kv_attn(const ckv_shape* shape, int32_t chunk, const uint16_t* q
 }
 
 }  // extern "C"
+
+bool ckv::loop_defers(const ckv_shape* shape, int32_t k, size_t ws_bytes) {
+  Dims d;
+  if (!shape || check_shape(shape, &d) != CKV_OK || k < 1) return false;
+  return ws_bytes >= make_layout(d, k, CKV_ENTRY_DECODE_STEP).total;
+}
 
 // rank == 0: misses fetched whole; else their keys rebuilt from u_fac/w_fac
 int ckv::corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,

@@ -148,17 +148,18 @@ __device__ __forceinline__ void clear_unit_hist(const SelectArgs& a, int unit) {
 }
 
 // Writes set bits of bm[0, words) as ascending positions to out[0, limit)
-// (when out is not null), 16 waves each owning a contiguous word range (reads
+// (when out is not null), the NT / 64 waves each owning a contiguous word range (reads
 // are lane-consecutive), and returns the number of set bits.  Output slots
 // [lo, hi) also go to share[slot - lo] when share is not null.  The bitmap
 // holds exactly m <= limit bits for scores as specified; the limit only keeps
 // other input (NaN scores) inside the row.
+template <int NT = kFinishThreads>
 __device__ __forceinline__ uint32_t emit_bitmap(const uint32_t* bm, int words, int32_t* out,
                                                 uint32_t limit, uint32_t* tmp,
                                                 int32_t* share = nullptr, uint32_t lo = 0,
                                                 uint32_t hi = 0) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int kW = kFinishThreads / 64;
+  constexpr int kW = NT / 64;
   const int per = (((words + kW - 1) / kW) + 63) & ~63;
   const int w0 = wave * per, w1 = min(w0 + per, words);
   uint32_t cnt = 0;
@@ -196,9 +197,9 @@ __device__ __forceinline__ uint32_t emit_bitmap(const uint32_t* bm, int words, i
 // Radix select among candidates (order key, position) that share the first
 // digit b1: the need largest by (key descending, position ascending).
 // Returns the threshold key T; candidates with key > T are all chosen, and of
-// those equal to T the ones with position <= *pmax.  All kFinishThreads
-// threads call this; hist needs 2048 words.
-template <class Cands>
+// those equal to T the ones with position <= *pmax.  All NT threads call
+// this; hist needs 2048 words.
+template <class Cands, int NT = kFinishThreads>
 __device__ __forceinline__ uint32_t refine_threshold(const Cands& cs, uint32_t nc,
                                                      uint32_t need, uint32_t b1,
                                                      uint32_t* hist, uint32_t* tmp,
@@ -206,23 +207,23 @@ __device__ __forceinline__ uint32_t refine_threshold(const Cands& cs, uint32_t n
   const int tid = threadIdx.x;
   // Second digit: bits 20..10 of the order key (11 bits).
   static_assert(kHistBits == 11, "digits 11 + 11 + 10");
-  for (int i = tid; i < 2048; i += kFinishThreads) hist[i] = 0u;
+  for (int i = tid; i < 2048; i += NT) hist[i] = 0u;
   __syncthreads();
-  for (uint32_t i = tid; i < nc; i += kFinishThreads)
+  for (uint32_t i = tid; i < nc; i += NT)
     atomicAdd(&hist[(cs[i].x >> 10) & 2047u], 1u);
   __syncthreads();
   uint32_t need2;
-  const uint32_t b2 = find_bin_block<true>(hist, 2048, need, tmp, misc, &need2);
+  const uint32_t b2 = find_bin_block<true, NT>(hist, 2048, need, tmp, misc, &need2);
   // Third digit: bits 9..0, among candidates whose second digit is b2.
-  for (int i = tid; i < 1024; i += kFinishThreads) hist[i] = 0u;
+  for (int i = tid; i < 1024; i += NT) hist[i] = 0u;
   __syncthreads();
-  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+  for (uint32_t i = tid; i < nc; i += NT) {
     const uint32_t key = cs[i].x;
     if (((key >> 10) & 2047u) == b2) atomicAdd(&hist[key & 1023u], 1u);
   }
   __syncthreads();
   uint32_t need3;
-  const uint32_t b3 = find_bin_block<true>(hist, 1024, need2, tmp, misc, &need3);
+  const uint32_t b3 = find_bin_block<true, NT>(hist, 1024, need2, tmp, misc, &need3);
   const uint32_t T = (b1 << 21) | (b2 << 10) | b3;
   const uint32_t eq = hist[b3];  // candidates with key == T
   __syncthreads();
@@ -233,16 +234,16 @@ __device__ __forceinline__ uint32_t refine_threshold(const Cands& cs, uint32_t n
   if (eq > need3) {
     uint32_t prefix = 0u, want = need3;
     for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += kFinishThreads) hist[i] = 0u;
+      for (int i = tid; i < 256; i += NT) hist[i] = 0u;
       __syncthreads();
       const uint32_t hi_mask = shift == 24 ? 0u : (0xffffffffu << (shift + 8));
-      for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+      for (uint32_t i = tid; i < nc; i += NT) {
         const uint2 c = cs[i];
         if (c.x == T && (c.y & hi_mask) == prefix) atomicAdd(&hist[(c.y >> shift) & 255u], 1u);
       }
       __syncthreads();
       uint32_t rest;
-      const uint32_t bb = find_bin_block<false>(hist, 256, want, tmp, misc, &rest);
+      const uint32_t bb = find_bin_block<false, NT>(hist, 256, want, tmp, misc, &rest);
       prefix |= bb << shift;
       want = rest;
     }
@@ -326,6 +327,7 @@ constexpr int kSelPer = 32;
 constexpr int kSelBatch = kSelPer * kFinishThreads;
 static_assert(kFusedSelectMaxCtx % kSelBatch == 0, "whole batches");
 
+template <int NT = kFinishThreads>
 __device__ __forceinline__ void load_score_batch(const float* srow, int j0, int n,
                                                  float (&sv)[kSelPer]) {
   // unconditional loads (clamped position); 32-bit byte offsets from the
@@ -333,7 +335,7 @@ __device__ __forceinline__ void load_score_batch(const float* srow, int j0, int 
   const char* base = reinterpret_cast<const char*>(srow);
 #pragma unroll
   for (int u = 0; u < kSelPer; ++u) {
-    const uint32_t off = 4u * (uint32_t)min(j0 + u * kFinishThreads + (int)threadIdx.x, n - 1);
+    const uint32_t off = 4u * (uint32_t)min(j0 + u * NT + (int)threadIdx.x, n - 1);
     sv[u] = *reinterpret_cast<const float*>(base + off);
   }
 }
@@ -343,16 +345,17 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// Candidate slots of the fused selection: the first kCandLds in LDS, any
-// beyond (heavy ties) in the unit's global candidate area.
+// Candidate slots of the fused selection: the first CAP in LDS, any beyond
+// (heavy ties) in the unit's global candidate area.
+template <int CAP = kCandLds>
 struct SplitCands {
   uint2* lds;
   uint2* glob;
   __device__ __forceinline__ uint2 operator[](uint32_t i) const {
-    return i < (uint32_t)kCandLds ? lds[i] : glob[i];
+    return i < (uint32_t)CAP ? lds[i] : glob[i];
   }
   __device__ __forceinline__ void put(uint32_t i, uint2 v) const {
-    if (i < (uint32_t)kCandLds) lds[i] = v;
+    if (i < (uint32_t)CAP) lds[i] = v;
     else glob[i] = v;
   }
 };
@@ -362,8 +365,9 @@ struct SplitCands {
 // the LDS bitmap, one ballot per 64 positions), g_lo <= x < g_hi <=> key(x)
 // lies in it (a candidate (fp32 bits, position) appended at *ctr, one atomic
 // per wave).  Positions at or past n_b must hold NaN (then neither holds).
+template <int NT = kFinishThreads, int CAP = kCandLds>
 __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j0, float g_lo,
-                                               float g_hi, uint32_t* bm, const SplitCands& cs,
+                                               float g_hi, uint32_t* bm, const SplitCands<CAP>& cs,
                                                uint32_t* ctr) {
   static_assert(2 * kSelPer == 64, "one bitmap word per lane and batch");
   const int tid = threadIdx.x, lane = tid & 63;
@@ -381,17 +385,17 @@ __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j
         : "s"((uint32_t)hi), "n"(2 * u), "s"((uint32_t)(hi >> 32)), "n"(2 * u + 1));
     wc += (uint32_t)__popcll(ge & ~hi);
   }
-  bm[((j0 + (lane >> 1) * kFinishThreads + wave * 64) >> 5) + (lane & 1)] = word;
+  bm[((j0 + (lane >> 1) * NT + wave * 64) >> 5) + (lane & 1)] = word;
   uint32_t base = 0u;
   if (lane == 0 && wc) base = atomicAdd(ctr, wc);
   base = __builtin_amdgcn_readfirstlane(base);
-  if (base + wc <= (uint32_t)kCandLds) {  // the wave's candidates all fit in LDS
+  if (base + wc <= (uint32_t)CAP) {  // the wave's candidates all fit in LDS
 #pragma unroll
     for (int u = 0; u < kSelPer; ++u) {
       // compare again rather than keep 2 x kSelPer lane masks live
       float x = sv[u];
       asm volatile("" : "+v"(x));
-      const int j = j0 + u * kFinishThreads + tid;
+      const int j = j0 + u * NT + tid;
       // g_lo <= g_hi, so "in the bin" is the exclusive or of the two tests
       const bool ge = x >= g_lo, hi = x >= g_hi;
       const uint64_t cm = __builtin_amdgcn_ballot_w64(ge) & ~__builtin_amdgcn_ballot_w64(hi);
@@ -400,7 +404,7 @@ __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j
     }
   } else {
     for (int u = 0; u < kSelPer; ++u) {
-      const int j = j0 + u * kFinishThreads + tid;
+      const int j = j0 + u * NT + tid;
       const bool in = sv[u] >= g_lo && !(sv[u] >= g_hi);
       const uint64_t cm = __builtin_amdgcn_ballot_w64(in);
       if (in) cs.put(base + lanes_below(cm), make_uint2(__float_as_uint(sv[u]), (uint32_t)j));
@@ -411,8 +415,9 @@ __device__ __forceinline__ void classify_batch(const float (&sv)[kSelPer], int j
 
 // The candidates as (order key, position): the fused selection stores the
 // scores' fp32 bits and converts on every read.
+template <int CAP = kCandLds>
 struct KeyedCands {
-  SplitCands c;
+  SplitCands<CAP> c;
   __device__ __forceinline__ uint2 operator[](uint32_t i) const {
     const uint2 v = c[i];
     return make_uint2(order_key(__uint_as_float(v.x)), v.y);
@@ -477,16 +482,16 @@ __device__ __forceinline__ void merge_partials(const SelectArgs& a, int unit, ui
 
 // LDS of a one-workgroup selection (see select_unit).
 struct SelLds {
-  uint2* cand;      // [kCandLds]
+  uint2* cand;      // [CAP of select_unit]
   uint32_t* bm;     // [kFusedSelectMaxCtx / 32]
   uint32_t* lhist;  // [2048]
-  uint32_t* tmp;    // [kFinishThreads / 64 + 1]
+  uint32_t* tmp;    // [threads / 64 + 1]
   uint32_t* misc;   // [8]
 };
 
-// The whole selection of one unit by one kFinishThreads workgroup, for
+// The whole selection of one unit by one workgroup of NT threads, for
 // n_b <= kFusedSelectMaxCtx.  The unit's scores are read once, kSelPer per
-// thread per batch of kSelBatch positions, all loads of a batch in flight
+// thread per batch of kSelPer * NT positions, all loads of a batch in flight
 // together.  Positions above the first-digit bin go straight into an LDS
 // bitmap (one ballot per 64 positions, no atomics); positions inside the bin
 // become candidates (fp32 bits, position), whose slots are reserved with one
@@ -496,10 +501,15 @@ struct SelLds {
 // lo] when share is not null.  When the first digit was counted into the
 // cleared per-unit histogram (no hist_part) and `clear` is set, the unit's
 // histogram and control words are left cleared; only the unit's one reader
-// may do that.  Returns the number of positions selected.
+// may do that (kFinishThreads workgroups only).  Returns the number of
+// positions selected.
+template <int NT = kFinishThreads, int CAP = kCandLds>
 __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const SelLds& L,
                                            bool write, int32_t* share, uint32_t lo,
                                            uint32_t hi, bool clear) {
+  static_assert(NT >= 128 && kHistBins % NT == 0 && kFusedSelectMaxCtx % (kSelPer * NT) == 0,
+                "workgroup shape");
+  constexpr int kBatch = kSelPer * NT;
   const int tid = threadIdx.x;
   uint2* const cand = L.cand;
   uint32_t* const bm = L.bm;
@@ -523,75 +533,79 @@ __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const 
     nslots = (int)min<int64_t>(hi_wg - lo_wg + 1, kMaxPartials);  // the host keeps it below
   }
   const int len_b = a.ctx_lens[unit / a.Hkv];
-  uint2 hv[kMaxPartials];
-  load_hist_slots(slots, nslots, hv);
+  uint2 hv[kMaxPartials][kHistBins / NT / 2];
+  load_hist_slots<NT>(slots, nslots, hv);
   // every wave's histogram loads queue ahead of all score loads (a bare
   // barrier: no wait for the loads themselves)
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   const float* srow = a.scores + (int64_t)unit * a.max_ctx;
   float sv0[kSelPer];
-  load_score_batch(srow, 0, a.max_ctx, sv0);
+  load_score_batch<NT>(srow, 0, a.max_ctx, sv0);
   __builtin_amdgcn_sched_barrier(0);  // n_b is waited for only here
   const int n = unit_len(len_b, a.max_ctx, a.chunk);
   const int m = min(a.k, n);
   int32_t* idx = a.idx + (int64_t)unit * a.k;
   if (m >= n) {  // uniform; every position (possibly none) is selected
-    for (int i = tid; i < a.k; i += kFinishThreads) {
+    for (int i = tid; i < a.k; i += NT) {
       if (write) idx[i] = i < n ? i : -1;
       if (share && i < n && (uint32_t)i >= lo && (uint32_t)i < hi) share[i - lo] = i;
     }
     if (write && tid == 0) a.n_sel[unit] = m;
-    if (clear && !a.hist_part) clear_unit_hist(a, unit);
+    if constexpr (NT == kFinishThreads) {
+      if (clear && !a.hist_part) clear_unit_hist(a, unit);
+    }
     return m;
   }
-  store_hist_sum(hv, nslots, lhist);
+  store_hist_sum<NT>(hv, nslots, lhist);
   if (tid == 64) misc[7] = 0u;
   // the scores may still be in flight across both barriers
   lds_barrier();
   if (tid < 64) find_first_bin_lds(lhist, (uint32_t)m, misc + 4);
   lds_barrier();
-  const SplitCands cs{cand, a.cand + (int64_t)unit * a.max_ctx};
+  const SplitCands<CAP> cs{cand, a.cand + (int64_t)unit * a.max_ctx};
   const uint32_t b1 = misc[4], above = misc[5];
   const float g_lo = __uint_as_float(key_floor_bits((uint64_t)b1 << (32 - kHistBits)));
   const float g_hi = __uint_as_float(key_floor_bits((uint64_t)(b1 + 1u) << (32 - kHistBits)));
   // the last, partial batch holds NaN past n_b
   auto pad = [&](float (&sv)[kSelPer], int j0) {
-    if (j0 + kSelBatch > n) {
+    if (j0 + kBatch > n) {
 #pragma unroll
       for (int u = 0; u < kSelPer; ++u)
-        if (j0 + u * kFinishThreads + tid >= n) sv[u] = __builtin_nanf("");
+        if (j0 + u * NT + tid >= n) sv[u] = __builtin_nanf("");
     }
   };
   // the first batch apart, so that its compares start as its loads land
   pad(sv0, 0);
-  classify_batch(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
-  for (int j0 = kSelBatch; j0 < n; j0 += kSelBatch) {
+  classify_batch<NT, CAP>(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
+  for (int j0 = kBatch; j0 < n; j0 += kBatch) {
     float sv[kSelPer];
-    load_score_batch(srow, j0, n, sv);
+    load_score_batch<NT>(srow, j0, n, sv);
     pad(sv, j0);
-    classify_batch(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
+    classify_batch<NT, CAP>(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
   }
   __syncthreads();
   const uint32_t nc = misc[7];
   const uint32_t need = (uint32_t)m - above;
-  const KeyedCands kc{cs};
+  const KeyedCands<CAP> kc{cs};
   uint32_t pmax;
-  const uint32_t T = refine_threshold(kc, nc, need, b1, lhist, tmp, misc, &pmax);
-  for (uint32_t i = tid; i < nc; i += kFinishThreads) {
+  const uint32_t T = refine_threshold<KeyedCands<CAP>, NT>(kc, nc, need, b1, lhist, tmp, misc, &pmax);
+  for (uint32_t i = tid; i < nc; i += NT) {
     const uint2 c = kc[i];
     if (c.x > T || (c.x == T && c.y <= pmax)) atomicOr(&bm[c.y >> 5], 1u << (c.y & 31));
   }
   __syncthreads();
   // m positions for scores as specified (fewer only with NaN scores)
-  const int got = (int)min(emit_bitmap(bm, (n + 31) >> 5, write ? idx : nullptr,
+  const int got = (int)min(emit_bitmap<NT>(bm, (n + 31) >> 5, write ? idx : nullptr,
                                        (uint32_t)a.k, tmp, share, lo, hi),
                            (uint32_t)m);
   if (write) {
-    for (int i = got + tid; i < a.k; i += kFinishThreads) idx[i] = -1;
+    for (int i = got + tid; i < a.k; i += NT) idx[i] = -1;
     if (tid == 0) a.n_sel[unit] = got;
   }
-  if (clear && !a.hist_part) clear_unit_hist(a, unit);
+  if constexpr (NT == kFinishThreads) {
+      if (clear && !a.hist_part) clear_unit_hist(a, unit);
+    }
   return got;
 }
 
@@ -908,6 +922,44 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
     uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
     score_role<G, CLAIMS>(sc, blockIdx.x - attn_blocks, gridDim.x - attn_blocks, l32 + kScoreLdsDwords,
                   l32, lds_claim);
+  }
+}
+
+// The same with a third role for the decode loop: the first sel_blocks
+// workgroups select the previous layer's sets for the next step (sel: that
+// layer's selection over the scores and per-workgroup histogram slots its
+// own launch left), as the fused selection does but with kAttnThreads
+// threads and the first kDualSelCands candidates in LDS.  Those sets are not
+// needed before the next step, so the selection's latency-bound work runs
+// beside this layer's streams instead of as a launch between layers.
+constexpr int kDualSelCands = 7168;
+template <int G, bool INDEXED>
+__global__ __launch_bounds__(kAttnThreads) void k_dual_sel(AttnArgs at, ScoreArgs sc,
+                                                          SelectArgs sel, int attn_blocks,
+                                                          int sel_blocks) {
+  constexpr int kA = AttnLds<G>::kFloats;
+  constexpr int kS = kHistBins + kScoreLdsDwords;
+  constexpr int kL = kA > kS ? kA : kS;
+  static_assert(2 * kDualSelCands + kFusedSelectMaxCtx / 32 + 2048 <= kL,
+                "the selection role's candidates, bitmap and histogram fit");
+  __shared__ __attribute__((aligned(16))) float lds[kL];
+  __shared__ uint32_t tmp[kAttnThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
+  int blk = blockIdx.x;
+  if (blk < sel_blocks) {
+    const SelLds L{reinterpret_cast<uint2*>(l32), l32 + 2 * kDualSelCands,
+                   l32 + 2 * kDualSelCands + kFusedSelectMaxCtx / 32, tmp, misc};
+    select_unit<kAttnThreads, kDualSelCands>(sel, blk, L, true, nullptr, 0, 0, false);
+    return;
+  }
+  blk -= sel_blocks;
+  if (blk < attn_blocks) {
+    const int unit = blk / at.chunks;
+    attn_chunk<G, INDEXED>(at, unit, blk - unit * at.chunks, lds);
+  } else {
+    score_range<G, true, 4, true>(sc, blk - attn_blocks, gridDim.x - sel_blocks - attn_blocks,
+                                  l32 + kScoreLdsDwords, l32);
   }
 }
 
@@ -1441,6 +1493,8 @@ static const void* score_kernel(ScoreKind kind, int chunk) {
     case ScoreKind::kDual2Indexed:
       if constexpr (G <= 8) return (const void*)k_dual2<G, true, false>;
       return nullptr;
+    case ScoreKind::kDualSel: return (const void*)k_dual_sel<G, false>;
+    case ScoreKind::kDualSelIndexed: return (const void*)k_dual_sel<G, true>;
   }
   return nullptr;
 }
@@ -1605,6 +1659,33 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
                    : launch_dual2_i<false>(at, sc, G, attn_blocks, nwg, s);
   return indexed ? launch_dual_i<true>(at, sc, G, attn_blocks, nwg, s)
                  : launch_dual_i<false>(at, sc, G, attn_blocks, nwg, s);
+}
+
+template <bool INDEXED>
+static hipError_t launch_dual_sel_i(const AttnArgs& at, const ScoreArgs& sc,
+                                    const SelectArgs& sel, int G, int attn_blocks,
+                                    int sel_blocks, int nwg, hipStream_t s) {
+  const dim3 grid(sel_blocks + attn_blocks + nwg), block(kAttnThreads);
+#define CKV_DS(g) launch_kernel(CKV_K_DUAL, k_dual_sel<g, INDEXED>, grid, block, s, at, sc, sel, attn_blocks, sel_blocks)
+  switch (G) {
+    case 1: CKV_DS(1); break;
+    case 2: CKV_DS(2); break;
+    case 4: CKV_DS(4); break;
+    case 8: CKV_DS(8); break;
+    case 16: CKV_DS(16); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef CKV_DS
+  return launch_status();
+}
+
+hipError_t launch_dual_sel(const AttnArgs& at, const ScoreArgs& sc, const SelectArgs& sel,
+                           int G, bool indexed, int units, int nwg, hipStream_t s) {
+  if (nwg < 1 || nwg > kMaxScoreWgs || !sc.hist_part || !sel.hist_part ||
+      sel.max_ctx > kFusedSelectMaxCtx || at.q2)
+    return hipErrorInvalidValue;
+  return indexed ? launch_dual_sel_i<true>(at, sc, sel, G, units * at.chunks, sel.units, nwg, s)
+                 : launch_dual_sel_i<false>(at, sc, sel, G, units * at.chunks, sel.units, nwg, s);
 }
 
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,

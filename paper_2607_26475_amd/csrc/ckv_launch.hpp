@@ -50,7 +50,9 @@ hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s);
 // first-digit histogram (chunk landmarks when a.chunk > 1), or the scoring
 // role of the one-launch attend-and-score kernel (buffer or rows in place).
 // kDual2*: the same with the two tokens' 2G head rows attending (G <= 8).
-enum class ScoreKind { kPlain, kHist, kDual, kDualIndexed, kDual2, kDual2Indexed };
+enum class ScoreKind {
+  kPlain, kHist, kDual, kDualIndexed, kDual2, kDual2Indexed, kDualSel, kDualSelIndexed
+};
 // Workgroups of that scoring pass for these arguments.  A call computes it
 // once and passes the same value to the launcher and to the selection, whose
 // histogram slots depend on it.
@@ -80,6 +82,12 @@ hipError_t launch_dual_token_wg(const AttnArgs& a, int G, int units, hipStream_t
 // at.q2 is set; scoring with G heads on nwg workgroups.
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
                        int units, int nwg, hipStream_t s);
+// The same (one token, static scoring ranges with per-workgroup histogram
+// slots) with the previous layer's selection `sel` (its own slots, n_b <=
+// kFusedSelectMaxCtx) as a third role: sel.units workgroups first; nwg from
+// score_blocks with ScoreKind::kDualSel(Indexed).
+hipError_t launch_dual_sel(const AttnArgs& at, const ScoreArgs& sc, const SelectArgs& sel,
+                           int G, bool indexed, int units, int nwg, hipStream_t s);
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s);
 hipError_t launch_landmarks(const LandmarkArgs& a, hipStream_t s);
 hipError_t launch_expand(const ExpandArgs& a, int units, hipStream_t s);
@@ -131,6 +139,26 @@ struct PipelinedLayer {
 int pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p, const int32_t* ctx_lens,
                     int32_t k, float scale, void* ws, size_t ws_bytes, void* stream);
 
+// Plain pipelined layers of the decode loop without buffers: a layer may leave
+// its selection (its sets for the next step) to the next layer's launch,
+// which runs it as a third role.  alt: this layer's scores and histogram
+// slots go to the decode step layout's second region (consecutive layers
+// alternate, so the previous layer's stay intact); prev: the previous
+// layer's pending selection, run by this call (in its launch when it can);
+// next (may be null): where this layer leaves its own selection if it
+// defers it (then *deferred is set and its attention partials are merged by
+// a merge launch instead).  The caller runs a pending selection itself
+// (launch_select_fused) before anything else uses the workspace.
+struct LoopLink {
+  bool alt = false;
+  const SelectArgs* prev = nullptr;
+  SelectArgs* next = nullptr;
+  bool deferred = false;
+};
+// Whether a workspace of ws_bytes holds the second region (the decode step
+// layout's), so that the loop may defer selections.
+bool loop_defers(const ckv_shape* shape, int32_t k, size_t ws_bytes);
+
 // ckv_critical_kv_attn and ckv_corrected_attn(_lowrank: rank > 0), for
 // callers that run several calls in order on one workspace: with hist_clean
 // a pipelined call skips the clearing of the selection histograms, which a
@@ -141,7 +169,8 @@ int critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t*
                   const uint16_t* k_src, const uint16_t* v_src, int src_kind,
                   const int32_t* idx_in, const uint16_t* k_buf, const uint16_t* v_buf,
                   const int32_t* n_sel_in, int32_t* idx_out, int32_t* n_sel_out, float* out,
-                  void* ws, size_t ws_bytes, void* stream, bool hist_clean);
+                  void* ws, size_t ws_bytes, void* stream, bool hist_clean,
+                  LoopLink* link = nullptr);
 int corrected_impl(const ckv_shape* shape, const uint16_t* q_att, const uint16_t* q_sel,
                    const uint16_t* k_score, const int32_t* ctx_lens, int32_t k, float scale,
                    const uint16_t* k_src, const uint16_t* v_src, int src_kind, int32_t rank,

@@ -122,7 +122,7 @@ int ckv_pipeline_set_gather_width(ckv_pipeline* pipe, int workgroups) {
 int ckv_pipeline_set_checks(ckv_pipeline* pipe, unsigned flags) {
   if (!pipe) return ckv::fail(CKV_EINVAL, "pipe is NULL");
   if (flags & ~(unsigned)(CKV_PIPE_CHECK_NO_FILL_WAIT | CKV_PIPE_CHECK_NO_RELEASE_WAIT |
-                          CKV_PIPE_CHECK_POISON))
+                          CKV_PIPE_CHECK_POISON | CKV_PIPE_CHECK_NO_DEFER))
     return ckv::fail(CKV_EINVAL, "unknown check flags 0x%x", flags);
   pipe->checks = flags;
   return CKV_OK;
@@ -168,19 +168,48 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
     for (int l = 0; l < num_layers; ++l)
       if (layers[l].idx_true)
         return ckv::fail(CKV_EINVAL, "layer %d: miss correction needs the two buffers", l);
+    // With the decode step's workspace, a plain layer followed by a plain
+    // layer leaves its selection (the sets for the next step, not needed
+    // before then) to the next layer's launch; consecutive plain layers
+    // alternate between two regions of scores and histogram slots.  A
+    // pending selection runs on its own before a special layer and after the
+    // last layer.
+    const bool defers =
+        ckv::loop_defers(shape, k, ws_bytes) && !(pipe->checks & CKV_PIPE_CHECK_NO_DEFER);
+    hipStream_t cs = (hipStream_t)compute_stream;
+    ckv::SelectArgs pend, mine;
+    bool have = false;
+    auto flush = [&]() -> int {
+      if (!have) return CKV_OK;
+      have = false;
+      if (hipError_t e = ckv::launch_select_fused(pend, pend.units, cs))
+        return ckv::hip_fail(e, "select launch");
+      return CKV_OK;
+    };
     for (int l = 0; l < num_layers; ++l) {
       const ckv_layer& L = layers[l];
       const bool clean = l > 0 && layout_of(L) == layout_of(layers[l - 1]);
-      int rc = special_layer(L)
-                   ? run_special(shape, L, ctx_lens, k, scale, src_kind, nullptr, nullptr, ws,
-                                 ws_bytes, compute_stream, clean)
-                   : ckv::critical_impl(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale,
-                                        L.k_src, L.v_src, src_kind, L.idx_prev, nullptr,
-                                        nullptr, L.n_sel_prev, L.idx_next, L.n_sel_next, L.out,
-                                        ws, ws_bytes, compute_stream, clean);
+      int rc;
+      if (special_layer(L)) {
+        if ((rc = flush())) return rc;
+        rc = run_special(shape, L, ctx_lens, k, scale, src_kind, nullptr, nullptr, ws, ws_bytes,
+                         compute_stream, clean);
+      } else {
+        const bool next_plain = l + 1 < num_layers && !special_layer(layers[l + 1]);
+        ckv::LoopLink link;
+        link.alt = (l & 1) != 0;
+        link.prev = have ? &pend : nullptr;
+        link.next = next_plain ? &mine : nullptr;
+        rc = ckv::critical_impl(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale, L.k_src,
+                                L.v_src, src_kind, L.idx_prev, nullptr, nullptr, L.n_sel_prev,
+                                L.idx_next, L.n_sel_next, L.out, ws, ws_bytes, compute_stream,
+                                clean, defers ? &link : nullptr);
+        have = link.deferred;
+        if (have) pend = mine;
+      }
       if (rc) return rc;
     }
-    return CKV_OK;
+    return flush();
   }
   if (num_layers < 2 || !k_buf || !v_buf)
     return ckv::fail(CKV_EINVAL, "the two-buffer loop needs at least 2 layers and both buffers");

@@ -70,32 +70,41 @@ __device__ __forceinline__ void walk_first_bin(const uint32_t* stage, uint32_t c
   }
 }
 
-// All kFinishThreads threads: the first-digit histogram is the sum of nslots
-// (1 .. kMaxPartials) consecutive slots of kHistBins counts.  Every thread
-// loads its two bins of every slot at once (one round trip; slots past nslots
-// repeat slot 0 and are not added) ...
+// All NT threads: the first-digit histogram is the sum of nslots (1 ..
+// kMaxPartials) consecutive slots of kHistBins counts.  Every thread loads
+// its kHistBins / NT consecutive bins of every slot at once (one round trip;
+// slots past nslots repeat slot 0 and are not added) ...
+template <int NT = kFinishThreads>
 __device__ __forceinline__ void load_hist_slots(const uint32_t* hist, int nslots,
-                                                uint2 (&v)[kMaxPartials]) {
-  static_assert(2 * kFinishThreads == kHistBins, "two bins per thread");
+                                                uint2 (&v)[kMaxPartials][kHistBins / NT / 2]) {
+  constexpr int kPairs = kHistBins / NT / 2;
+  static_assert(kPairs >= 1, "two bins per thread at least");
   const int t = threadIdx.x;
 #pragma unroll
   for (int p = 0; p < kMaxPartials; ++p)
-    v[p] = *reinterpret_cast<const uint2*>(hist + (int64_t)(p < nslots ? p : 0) * kHistBins +
-                                           2 * t);
+#pragma unroll
+    for (int q = 0; q < kPairs; ++q)
+      v[p][q] = *reinterpret_cast<const uint2*>(
+          hist + (int64_t)(p < nslots ? p : 0) * kHistBins + 2 * (kPairs * t + q));
 }
 
 // ... and stores the sums to lhist (LDS); the caller synchronises before
 // reading it.
-__device__ __forceinline__ void store_hist_sum(const uint2 (&v)[kMaxPartials], int nslots,
-                                               uint32_t* lhist) {
-  uint2 acc = make_uint2(0u, 0u);
+template <int NT = kFinishThreads>
+__device__ __forceinline__ void store_hist_sum(const uint2 (&v)[kMaxPartials][kHistBins / NT / 2],
+                                               int nslots, uint32_t* lhist) {
+  constexpr int kPairs = kHistBins / NT / 2;
 #pragma unroll
-  for (int p = 0; p < kMaxPartials; ++p)
-    if (p < nslots) {
-      acc.x += v[p].x;
-      acc.y += v[p].y;
-    }
-  *reinterpret_cast<uint2*>(lhist + 2 * threadIdx.x) = acc;
+  for (int q = 0; q < kPairs; ++q) {
+    uint2 acc = make_uint2(0u, 0u);
+#pragma unroll
+    for (int p = 0; p < kMaxPartials; ++p)
+      if (p < nslots) {
+        acc.x += v[p][q].x;
+        acc.y += v[p][q].y;
+      }
+    *reinterpret_cast<uint2*>(lhist + 2 * (kPairs * threadIdx.x + q)) = acc;
+  }
 }
 
 // Wave 0 only: the bin holding the m-th largest key, from the histogram in
@@ -114,12 +123,12 @@ __device__ __forceinline__ void find_first_bin_lds(const uint32_t* lhist, uint32
   walk_first_bin(lhist, c, m, out);
 }
 
-// All threads of a kFinishThreads workgroup: given a histogram of nb bins in
-// LDS (nb a multiple of kFinishThreads or at most kFinishThreads), find the
+// All threads of an NT-thread workgroup: given a histogram of nb bins in
+// LDS (nb a multiple of NT or at most NT), find the
 // bin where the running count (from the top bin down when DESC, else from
 // bin 0 up) first reaches `need`.  Returns the bin and sets *rest to the
 // number still needed inside that bin.
-template <bool DESC>
+template <bool DESC, int NT = kFinishThreads>
 __device__ __forceinline__ uint32_t find_bin_block(const uint32_t* hist, int nb,
                                                    uint32_t need, uint32_t* tmp,
                                                    uint32_t* misc,
@@ -129,14 +138,14 @@ __device__ __forceinline__ uint32_t find_bin_block(const uint32_t* hist, int nb,
     misc[0] = 0u;
     misc[1] = 0u;
   }
-  const int per = nb > kFinishThreads ? nb / kFinishThreads : 1;
+  const int per = nb > NT ? nb / NT : 1;
   // thread t owns scan positions [t*per, t*per + per)
   auto bin_at = [&](int pos) { return DESC ? nb - 1 - pos : pos; };
   uint32_t v = 0u;
   if (t * per < nb)
     for (int i = 0; i < per; ++i) v += hist[bin_at(t * per + i)];
   uint32_t total;
-  const uint32_t incl = block_incl_scan<kFinishThreads / 64>(v, tmp, &total);
+  const uint32_t incl = block_incl_scan<NT / 64>(v, tmp, &total);
   if (t * per < nb && incl >= need && incl - v < need) {
     uint32_t run = incl - v;
     for (int i = 0; i < per; ++i) {

@@ -1,0 +1,93 @@
+"""Deferred selections in the decode loop without buffers (MI355X only).
+
+With the decode step's workspace, a plain layer followed by a plain layer
+leaves its selection (its sets for the next step) to the next layer's
+attend-and-score launch, which runs it as a third role with 256-thread
+workgroups; the layer's attention partials are merged by the merge launch.
+The selection is exact and the merge takes the same order of operations
+either way, so every index set, count and output must equal, bit for bit,
+those of the same loop with every selection in its own layer's call
+(CHECK_NO_DEFER).  Cases: all layers plain (the selection of layers 0 .. L-2
+deferred, the last one's run at the end of the call), a chunked layer in the
+middle (the pending selection runs before it), a single layer, ragged
+contexts; two steps each, and the first step also against the oracle.
+Deferral needs the per-workgroup histogram slots (at most 8 per unit, so at
+least about 74 units beside 512 scoring workgroups): the batches here have
+80 and 96 units.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+import paper_2607_26475_amd as ckv
+import synth
+from helpers import ATOL_OUT, SCALE, check_index_sets, device, oracle_attn_over, orc, u16
+from test_gpu_pipeline import Loop
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(*a):
+    print(*a, flush=True)
+
+
+def _run(w, layers, chunk_layers, no_defer, dev, steps=2):
+    lp = Loop(w, layers, steps=steps, seed=17, dev=dev)
+    lp.in_place = True
+    if chunk_layers:
+        lp.chunk_layers = set(chunk_layers)
+        lp.set_chunked(8)
+    lp.bootstrap()
+    boot = ([i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]])
+    pipe = ckv.Pipeline()
+    if no_defer:
+        pipe.set_checks(ckv.Pipeline.CHECK_NO_DEFER)
+    ckv.profile_begin()
+    hist = lp.run(steps, pipe)
+    kernels = ckv.profile_end()
+    pipe.close()
+    return lp, boot, hist, kernels
+
+
+WL = {"llama80": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="llama80", batch=10),
+      "dual96": dataclasses.replace(synth.WORKLOADS["dual64_s"], name="dual96", batch=12)}
+
+
+@pytest.mark.parametrize("wl,layers,chunk_layers", [
+    ("llama80", 4, None), ("llama80", 4, (2,)), ("llama80", 1, None), ("dual96", 3, None)])
+def test_deferred_selection_matches_undeferred(wl, layers, chunk_layers):
+    _log("deferred", wl, layers, chunk_layers)
+    dev = device()
+    w = WL[wl]
+    lp, boot, hist, kernels = _run(w, layers, chunk_layers, False, dev)
+    _, _, ref, ref_kernels = _run(w, layers, chunk_layers, True, dev)
+    _log("  kernels", {k: v[0] for k, v in kernels.items()},
+         "undeferred", {k: v[0] for k, v in ref_kernels.items()})
+    plain = [l for l in range(layers) if not chunk_layers or l not in chunk_layers]
+    # layers whose successor is plain defer their selection: one merge launch each
+    deferred = [l for l in plain if l + 1 < layers and l + 1 in plain]
+    assert "zero" not in kernels, kernels  # per-workgroup histogram slots
+    assert kernels.get("combine", (0,))[0] == 2 * len(deferred), kernels
+    assert ref_kernels.get("combine", (0,))[0] == 0, ref_kernels
+    for st in range(2):
+        for part in range(3):  # idx, n_sel, outputs of every layer
+            for l in range(layers):
+                np.testing.assert_array_equal(hist[st][part][l], ref[st][part][l],
+                                              err_msg=f"step {st + 1} layer {l} part {part}")
+    # the first step's plain layers against the oracle
+    o = orc()
+    lens = lp.lens.cpu().numpy()
+    so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
+    g_idx, g_nsel, g_out = hist[0][:3]
+    for l in plain:
+        K, V = u16(lp.t[l]["k"]), u16(lp.t[l]["v"])
+        S = o.score_keys(so, u16(lp.q_sel[1][l]), K, lens, SCALE, nthreads=8)
+        r_idx, r_nsel = o.select_topk(so, S, lens, w.k, nthreads=8)
+        swaps = check_index_sets(g_idx[l], g_nsel[l], r_idx, r_nsel, S, lens)
+        att = oracle_attn_over(so, u16(lp.q_att[1][l]), K, V, boot[0][l], boot[1][l], w.k)
+        err = np.abs(g_out[l] - att).max()
+        _log(f"  layer {l}: swaps {swaps}, max abs err {err:.2e}")
+        assert err <= ATOL_OUT

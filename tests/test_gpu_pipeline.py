@@ -69,6 +69,7 @@ class Loop:
         self.shape = ckv.shape_for(B, Hq, Hkv, w.max_ctx, kv_row_stride=2 * d)
         self.ws = ckv.workspace(self.shape, k, ckv.ENTRY_DECODE_STEP)
         self.chunk, self.lms = 1, None      # chunked layers: set_chunked()
+        self.chunk_layers = None            # the chunked layers (None: all of them)
         self.two, self.local = False, None  # two-token layers: set_two_tokens()
         self.out_spec = [torch.full((B, Hq, d), float("nan"), device=dev) for _ in range(layers)]
         self.in_place = False               # rows read from the device caches, no buffers
@@ -90,12 +91,15 @@ class Loop:
                  "lr_rank": self.lowrank[l][0] if l in self.lowrank else 0,
                  "lr_u": self.lowrank[l][1] if l in self.lowrank else None,
                  "lr_w": self.lowrank[l][2] if l in self.lowrank else None,
-                 "chunk": self.chunk,
-                 "landmarks": self.lms[l] if self.chunk > 1 else None,
+                 "chunk": self.chunk if self.chunked(l) else 1,
+                 "landmarks": self.lms[l] if self.chunked(l) else None,
                  "k_local": self.local[step][l][0] if self.two else None,
                  "v_local": self.local[step][l][1] if self.two else None,
                  "out_spec": self.out_spec[l] if self.two else None}
                 for l in range(self.L)]
+
+    def chunked(self, l):
+        return self.chunk > 1 and (self.chunk_layers is None or l in self.chunk_layers)
 
     def set_chunked(self, chunk):
         """Chunked layers: landmarks of `chunk` rows of every layer's keys."""
