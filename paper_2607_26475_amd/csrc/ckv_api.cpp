@@ -565,7 +565,7 @@ bool chunk_select_attn(const Dims& d, int32_t chunk, int32_t k) {
 
 int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
                          const int32_t* ctx_lens, int32_t k, float scale, void* ws,
-                         size_t ws_bytes, void* stream) {
+                         size_t ws_bytes, void* stream, LoopLink* link) {
   Dims d;
   int rc = check_shape(shape, &d);
   if (rc) return rc;
@@ -589,6 +589,8 @@ int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
     CKV_PTR(p.k_score);
   }
   const bool two = p.out_spec != nullptr;
+  if (link && (!two || chunked || p.k_buf))
+    return fail(CKV_EINVAL, "a loop link needs a two-token layer read in place");
   if (two) {
     if (d.G > 8)
       return fail(CKV_EUNSUPPORTED, "two tokens need 2G <= 16 head rows (G = %d)", d.G);
@@ -628,6 +630,10 @@ int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
     if ((rc = check_grid(ds, Ls))) return rc;
     if (Ls.part > L.part) return fail(CKV_EWORKSPACE, "chunk selection layout overlaps");
   }
+  if (link && link->alt) {  // this layer's scores and slots in the second region
+    Ls.scores = L.scores_b;
+    Ls.hist_part = L.hist_part_b;
+  }
   int32_t* sidx = chunked ? at<int32_t>(ws, L.chunk_idx) : p.idx_out;
   int32_t* sn = chunked ? at<int32_t>(ws, L.n_chunks) : p.n_sel_out;
   float* scores = at<float>(ws, Ls.scores);
@@ -647,14 +653,34 @@ int ckv::pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p,
   }
   const ScoreKind kind = two ? (in_place ? ScoreKind::kDual2Indexed : ScoreKind::kDual2)
                              : (in_place ? ScoreKind::kDualIndexed : ScoreKind::kDual);
-  const int nwg = score_blocks(sc, d.G, kind);
-  if (use_partials(ds, Ls, nwg))
+  int nwg = score_blocks(sc, d.G, kind);
+  const bool partials = use_partials(ds, Ls, nwg);
+  // the previous two-token layer's pending selection joins this launch
+  bool fold = false;
+  if (link && link->prev) {
+    const int nwg_sel = score_blocks(
+        sc, d.G, in_place ? ScoreKind::kDual2SelIndexed : ScoreKind::kDual2Sel);
+    fold = partials && nwg_sel > 0 && use_partials(ds, Ls, nwg_sel) &&
+           d.max_ctx <= kFusedSelectMaxCtx && link->prev->units == d.U;
+    if (fold) nwg = nwg_sel;
+    else CKV_TRY_HIP(launch_select_fused(*link->prev, link->prev->units, s), "select launch");
+  }
+  if (partials)
     set_partials(ws, Ls, nwg, &sc, &sa);
   else if (!p.hist_clean)
     CKV_TRY_HIP(launch_zero(ws, Ls.zero_end, s), "zero launch");
-  CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
+  if (fold)
+    CKV_TRY_HIP(launch_dual_sel(at_, sc, *link->prev, d.G, in_place, d.U, nwg, s),
+                "dual launch");
+  else
+    CKV_TRY_HIP(launch_dual(at_, sc, d.G, in_place, d.U, nwg, s), "dual launch");
   if (two) {
-    if ((rc = run_select_tail(sa, d.U, s))) return rc;
+    if (link && link->next && partials && d.max_ctx <= kFusedSelectMaxCtx) {
+      *link->next = sa;  // the next two-token layer's launch selects
+      link->deferred = true;
+    } else if ((rc = run_select_tail(sa, d.U, s))) {
+      return rc;
+    }
     CKV_TRY_HIP(launch_combine(at_, 2 * d.G, d.U, s), "combine launch");
   } else if ((rc = select_and_merge(sa, at_, d, s))) {
     return rc;

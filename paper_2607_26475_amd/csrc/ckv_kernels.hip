@@ -931,13 +931,15 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual(AttnArgs at, ScoreArgs sc
 // own launch left), as the fused selection does but with kAttnThreads
 // threads and the first kDualSelCands candidates in LDS.  Those sets are not
 // needed before the next step, so the selection's latency-bound work runs
-// beside this layer's streams instead of as a launch between layers.
+// beside this layer's streams instead of as a launch between layers.  TWO:
+// the attention role has the 2G head rows of two tokens, as in k_dual2.
 constexpr int kDualSelCands = 7168;
-template <int G, bool INDEXED>
+template <int G, bool INDEXED, bool TWO = false>
 __global__ __launch_bounds__(kAttnThreads) void k_dual_sel(AttnArgs at, ScoreArgs sc,
                                                           SelectArgs sel, int attn_blocks,
                                                           int sel_blocks) {
-  constexpr int kA = AttnLds<G>::kFloats;
+  constexpr int GA = TWO ? 2 * G : G;  // attention head rows
+  constexpr int kA = AttnLds<GA>::kFloats;
   constexpr int kS = kHistBins + kScoreLdsDwords;
   constexpr int kL = kA > kS ? kA : kS;
   static_assert(2 * kDualSelCands + kFusedSelectMaxCtx / 32 + 2048 <= kL,
@@ -956,7 +958,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_dual_sel(AttnArgs at, ScoreArg
   blk -= sel_blocks;
   if (blk < attn_blocks) {
     const int unit = blk / at.chunks;
-    attn_chunk<G, INDEXED>(at, unit, blk - unit * at.chunks, lds);
+    attn_chunk<GA, INDEXED>(at, unit, blk - unit * at.chunks, lds);
   } else {
     score_range<G, true, 4, true>(sc, blk - attn_blocks, gridDim.x - sel_blocks - attn_blocks,
                                   l32 + kScoreLdsDwords, l32);
@@ -1495,6 +1497,12 @@ static const void* score_kernel(ScoreKind kind, int chunk) {
       return nullptr;
     case ScoreKind::kDualSel: return (const void*)k_dual_sel<G, false>;
     case ScoreKind::kDualSelIndexed: return (const void*)k_dual_sel<G, true>;
+    case ScoreKind::kDual2Sel:
+      if constexpr (G <= 8) return (const void*)k_dual_sel<G, false, true>;
+      return nullptr;
+    case ScoreKind::kDual2SelIndexed:
+      if constexpr (G <= 8) return (const void*)k_dual_sel<G, true, true>;
+      return nullptr;
   }
   return nullptr;
 }
@@ -1661,18 +1669,23 @@ hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool inde
                  : launch_dual_i<false>(at, sc, G, attn_blocks, nwg, s);
 }
 
-template <bool INDEXED>
+template <bool INDEXED, bool TWO>
 static hipError_t launch_dual_sel_i(const AttnArgs& at, const ScoreArgs& sc,
                                     const SelectArgs& sel, int G, int attn_blocks,
                                     int sel_blocks, int nwg, hipStream_t s) {
   const dim3 grid(sel_blocks + attn_blocks + nwg), block(kAttnThreads);
-#define CKV_DS(g) launch_kernel(CKV_K_DUAL, k_dual_sel<g, INDEXED>, grid, block, s, at, sc, sel, attn_blocks, sel_blocks)
+#define CKV_DS(g) launch_kernel(CKV_K_DUAL, k_dual_sel<g, INDEXED, TWO>, grid, block, s, at, sc, sel, attn_blocks, sel_blocks)
   switch (G) {
     case 1: CKV_DS(1); break;
     case 2: CKV_DS(2); break;
     case 4: CKV_DS(4); break;
     case 8: CKV_DS(8); break;
-    case 16: CKV_DS(16); break;
+    case 16:
+      if constexpr (!TWO) {
+        CKV_DS(16);
+        break;
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 #undef CKV_DS
@@ -1682,10 +1695,14 @@ static hipError_t launch_dual_sel_i(const AttnArgs& at, const ScoreArgs& sc,
 hipError_t launch_dual_sel(const AttnArgs& at, const ScoreArgs& sc, const SelectArgs& sel,
                            int G, bool indexed, int units, int nwg, hipStream_t s) {
   if (nwg < 1 || nwg > kMaxScoreWgs || !sc.hist_part || !sel.hist_part ||
-      sel.max_ctx > kFusedSelectMaxCtx || at.q2)
+      sel.max_ctx > kFusedSelectMaxCtx)
     return hipErrorInvalidValue;
-  return indexed ? launch_dual_sel_i<true>(at, sc, sel, G, units * at.chunks, sel.units, nwg, s)
-                 : launch_dual_sel_i<false>(at, sc, sel, G, units * at.chunks, sel.units, nwg, s);
+  const int ab = units * at.chunks, sb = sel.units;
+  if (at.q2)  // two tokens: 2G head rows attend, G score
+    return indexed ? launch_dual_sel_i<true, true>(at, sc, sel, G, ab, sb, nwg, s)
+                   : launch_dual_sel_i<false, true>(at, sc, sel, G, ab, sb, nwg, s);
+  return indexed ? launch_dual_sel_i<true, false>(at, sc, sel, G, ab, sb, nwg, s)
+                 : launch_dual_sel_i<false, false>(at, sc, sel, G, ab, sb, nwg, s);
 }
 
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,

@@ -51,7 +51,8 @@ hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s);
 // role of the one-launch attend-and-score kernel (buffer or rows in place).
 // kDual2*: the same with the two tokens' 2G head rows attending (G <= 8).
 enum class ScoreKind {
-  kPlain, kHist, kDual, kDualIndexed, kDual2, kDual2Indexed, kDualSel, kDualSelIndexed
+  kPlain, kHist, kDual, kDualIndexed, kDual2, kDual2Indexed, kDualSel, kDualSelIndexed,
+  kDual2Sel, kDual2SelIndexed
 };
 // Workgroups of that scoring pass for these arguments.  A call computes it
 // once and passes the same value to the launcher and to the selection, whose
@@ -82,10 +83,10 @@ hipError_t launch_dual_token_wg(const AttnArgs& a, int G, int units, hipStream_t
 // at.q2 is set; scoring with G heads on nwg workgroups.
 hipError_t launch_dual(const AttnArgs& at, const ScoreArgs& sc, int G, bool indexed,
                        int units, int nwg, hipStream_t s);
-// The same (one token, static scoring ranges with per-workgroup histogram
-// slots) with the previous layer's selection `sel` (its own slots, n_b <=
-// kFusedSelectMaxCtx) as a third role: sel.units workgroups first; nwg from
-// score_blocks with ScoreKind::kDualSel(Indexed).
+// The same (static scoring ranges with per-workgroup histogram slots; one
+// token, or two when at.q2 is set) with the previous layer's selection `sel`
+// (its own slots, n_b <= kFusedSelectMaxCtx) as a third role: sel.units
+// workgroups first; nwg from score_blocks with ScoreKind::kDual(2)Sel(Indexed).
 hipError_t launch_dual_sel(const AttnArgs& at, const ScoreArgs& sc, const SelectArgs& sel,
                            int G, bool indexed, int units, int nwg, hipStream_t s);
 hipError_t launch_miss(const MissArgs& a, int units, hipStream_t s);
@@ -136,8 +137,14 @@ struct PipelinedLayer {
   float* out_spec;
   bool hist_clean;  // the workspace's selection histograms are known clear
 };
+struct LoopLink;
+// link (two-token layers of the loop without buffers; see LoopLink): this
+// layer's scores and slots in the decode step layout's second region when
+// link->alt, the previous two-token layer's pending selection folded into
+// this launch, this layer's selection left to the next one.
 int pipelined_layer(const ckv_shape* shape, const PipelinedLayer& p, const int32_t* ctx_lens,
-                    int32_t k, float scale, void* ws, size_t ws_bytes, void* stream);
+                    int32_t k, float scale, void* ws, size_t ws_bytes, void* stream,
+                    LoopLink* link = nullptr);
 
 // Plain pipelined layers of the decode loop without buffers: a layer may leave
 // its selection (its sets for the next step) to the next layer's launch,

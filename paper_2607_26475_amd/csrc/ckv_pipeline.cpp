@@ -33,7 +33,7 @@ int layout_of(const ckv_layer& L) {
 int run_special(const ckv_shape* shape, const ckv_layer& L, const int32_t* ctx_lens,
                 int32_t k, float scale, int src_kind, const uint16_t* k_buf,
                 const uint16_t* v_buf, void* ws, size_t ws_bytes, void* stream,
-                bool hist_clean) {
+                bool hist_clean, ckv::LoopLink* link = nullptr) {
   ckv::PipelinedLayer p;
   p.q_att = L.q_att;
   p.q_sel = L.q_sel;
@@ -54,7 +54,7 @@ int run_special(const ckv_shape* shape, const ckv_layer& L, const int32_t* ctx_l
   p.v_local = L.v_local;
   p.out_spec = L.out_spec;
   p.hist_clean = hist_clean;
-  return ckv::pipelined_layer(shape, p, ctx_lens, k, scale, ws, ws_bytes, stream);
+  return ckv::pipelined_layer(shape, p, ctx_lens, k, scale, ws, ws_bytes, stream, link);
 }
 
 // Id of the stream capture s takes part in, 0 if it is not capturing.
@@ -169,11 +169,11 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
       if (layers[l].idx_true)
         return ckv::fail(CKV_EINVAL, "layer %d: miss correction needs the two buffers", l);
     // With the decode step's workspace, a plain layer followed by a plain
-    // layer leaves its selection (the sets for the next step, not needed
-    // before then) to the next layer's launch; consecutive plain layers
-    // alternate between two regions of scores and histogram slots.  A
-    // pending selection runs on its own before a special layer and after the
-    // last layer.
+    // layer, or a two-token layer followed by a two-token layer, leaves its
+    // selection (the sets for the next step, not needed before then) to the
+    // next layer's launch; consecutive layers of a kind alternate between two
+    // regions of scores and histogram slots.  A pending selection runs on its
+    // own before a layer of another kind and after the last layer.
     const bool defers =
         ckv::loop_defers(shape, k, ws_bytes) && !(pipe->checks & CKV_PIPE_CHECK_NO_DEFER);
     hipStream_t cs = (hipStream_t)compute_stream;
@@ -186,28 +186,35 @@ int ckv_decode_step(ckv_pipeline* pipe, const ckv_shape* shape, int num_layers,
         return ckv::hip_fail(e, "select launch");
       return CKV_OK;
     };
+    // 0: plain, 1: two tokens, 2: chunked (never deferred)
+    auto kind_of = [](const ckv_layer& L) { return L.chunk > 1 ? 2 : L.out_spec ? 1 : 0; };
+    int pend_kind = -1;
     for (int l = 0; l < num_layers; ++l) {
       const ckv_layer& L = layers[l];
+      const int kind = kind_of(L);
       const bool clean = l > 0 && layout_of(L) == layout_of(layers[l - 1]);
       int rc;
-      if (special_layer(L)) {
+      if (have && pend_kind != kind)
         if ((rc = flush())) return rc;
+      ckv::LoopLink link;
+      link.alt = (l & 1) != 0;
+      link.prev = have ? &pend : nullptr;
+      link.next = l + 1 < num_layers && kind_of(layers[l + 1]) == kind ? &mine : nullptr;
+      ckv::LoopLink* lk = defers && kind != 2 ? &link : nullptr;
+      if (kind != 0)
         rc = run_special(shape, L, ctx_lens, k, scale, src_kind, nullptr, nullptr, ws, ws_bytes,
-                         compute_stream, clean);
-      } else {
-        const bool next_plain = l + 1 < num_layers && !special_layer(layers[l + 1]);
-        ckv::LoopLink link;
-        link.alt = (l & 1) != 0;
-        link.prev = have ? &pend : nullptr;
-        link.next = next_plain ? &mine : nullptr;
+                         compute_stream, clean, lk);
+      else
         rc = ckv::critical_impl(shape, L.q_att, L.q_sel, L.k_score, ctx_lens, k, scale, L.k_src,
                                 L.v_src, src_kind, L.idx_prev, nullptr, nullptr, L.n_sel_prev,
                                 L.idx_next, L.n_sel_next, L.out, ws, ws_bytes, compute_stream,
-                                clean, defers ? &link : nullptr);
-        have = link.deferred;
-        if (have) pend = mine;
-      }
+                                clean, lk);
       if (rc) return rc;
+      have = lk && link.deferred;
+      if (have) {
+        pend = mine;
+        pend_kind = kind;
+      }
     }
     return flush();
   }

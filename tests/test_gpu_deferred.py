@@ -1,16 +1,19 @@
 """Deferred selections in the decode loop without buffers (MI355X only).
 
-With the decode step's workspace, a plain layer followed by a plain layer
-leaves its selection (its sets for the next step) to the next layer's
-attend-and-score launch, which runs it as a third role with 256-thread
-workgroups; the layer's attention partials are merged by the merge launch.
+With the decode step's workspace, a plain layer followed by a plain layer,
+or a two-token layer followed by a two-token layer, leaves its selection
+(its sets for the next step) to the next layer's attend-and-score launch,
+which runs it as a third role with 256-thread workgroups; the layer's
+attention partials are merged by the merge launch.
 The selection is exact and the merge takes the same order of operations
 either way, so every index set, count and output must equal, bit for bit,
 those of the same loop with every selection in its own layer's call
 (CHECK_NO_DEFER).  Cases: all layers plain (the selection of layers 0 .. L-2
 deferred, the last one's run at the end of the call), a chunked layer in the
-middle (the pending selection runs before it), a single layer, ragged
-contexts; two steps each, and the first step also against the oracle.
+middle (the pending selection runs before it), all layers two-token, plain
+and two-token layers mixed (a pending selection runs when the kind changes),
+a single layer, ragged contexts; two steps each, and the first step's plain
+layers also against the oracle.
 Deferral needs the per-workgroup histogram slots (at most 8 per unit, so at
 least about 74 units beside 512 scoring workgroups): the batches here have
 80 and 96 units.
@@ -34,12 +37,15 @@ def _log(*a):
     print(*a, flush=True)
 
 
-def _run(w, layers, chunk_layers, no_defer, dev, steps=2):
+def _run(w, layers, chunk_layers, two_layers, no_defer, dev, steps=2):
     lp = Loop(w, layers, steps=steps, seed=17, dev=dev)
     lp.in_place = True
     if chunk_layers:
         lp.chunk_layers = set(chunk_layers)
         lp.set_chunked(8)
+    if two_layers:
+        lp.two_layers = None if two_layers == "all" else set(two_layers)
+        lp.set_two_tokens(steps)
     lp.bootstrap()
     boot = ([i.cpu().numpy() for i in lp.idx[0]], [n.cpu().numpy() for n in lp.nsel[0]])
     pipe = ckv.Pipeline()
@@ -56,24 +62,33 @@ WL = {"llama80": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="llama80
       "dual96": dataclasses.replace(synth.WORKLOADS["dual64_s"], name="dual96", batch=12)}
 
 
-@pytest.mark.parametrize("wl,layers,chunk_layers", [
-    ("llama80", 4, None), ("llama80", 4, (2,)), ("llama80", 1, None), ("dual96", 3, None)])
-def test_deferred_selection_matches_undeferred(wl, layers, chunk_layers):
-    _log("deferred", wl, layers, chunk_layers)
+@pytest.mark.parametrize("wl,layers,chunk_layers,two_layers", [
+    ("llama80", 4, None, None), ("llama80", 4, (2,), None), ("llama80", 1, None, None),
+    ("dual96", 3, None, None), ("llama80", 4, None, "all"), ("llama80", 5, None, (1, 2, 4))])
+def test_deferred_selection_matches_undeferred(wl, layers, chunk_layers, two_layers):
+    _log("deferred", wl, layers, chunk_layers, two_layers)
     dev = device()
     w = WL[wl]
-    lp, boot, hist, kernels = _run(w, layers, chunk_layers, False, dev)
-    _, _, ref, ref_kernels = _run(w, layers, chunk_layers, True, dev)
+    lp, boot, hist, kernels = _run(w, layers, chunk_layers, two_layers, False, dev)
+    _, _, ref, ref_kernels = _run(w, layers, chunk_layers, two_layers, True, dev)
     _log("  kernels", {k: v[0] for k, v in kernels.items()},
          "undeferred", {k: v[0] for k, v in ref_kernels.items()})
-    plain = [l for l in range(layers) if not chunk_layers or l not in chunk_layers]
-    # layers whose successor is plain defer their selection: one merge launch each
-    deferred = [l for l in plain if l + 1 < layers and l + 1 in plain]
+    def kind(l):
+        if chunk_layers and l in chunk_layers:
+            return 2
+        return 1 if two_layers and (two_layers == "all" or l in two_layers) else 0
+
+    plain = [l for l in range(layers) if kind(l) == 0]
+    # layers followed by a layer of their kind (plain or two-token) defer their
+    # selection; plain ones merge their partials in a merge launch instead
+    deferred = [l for l in range(layers)
+                if kind(l) != 2 and l + 1 < layers and kind(l + 1) == kind(l)]
+    merges = [l for l in deferred if kind(l) == 0] + [l for l in range(layers) if kind(l) == 1]
     assert "zero" not in kernels, kernels  # per-workgroup histogram slots
-    assert kernels.get("combine", (0,))[0] == 2 * len(deferred), kernels
-    assert ref_kernels.get("combine", (0,))[0] == 0, ref_kernels
+    assert kernels.get("combine", (0,))[0] == 2 * len(merges), kernels
+    assert kernels["finish"][0] == ref_kernels["finish"][0] - 2 * len(deferred), kernels
     for st in range(2):
-        for part in range(3):  # idx, n_sel, outputs of every layer
+        for part in (0, 1, 2, 6):  # idx, n_sel, outputs, speculative outputs of every layer
             for l in range(layers):
                 np.testing.assert_array_equal(hist[st][part][l], ref[st][part][l],
                                               err_msg=f"step {st + 1} layer {l} part {part}")

@@ -71,6 +71,7 @@ class Loop:
         self.chunk, self.lms = 1, None      # chunked layers: set_chunked()
         self.chunk_layers = None            # the chunked layers (None: all of them)
         self.two, self.local = False, None  # two-token layers: set_two_tokens()
+        self.two_layers = None              # the two-token layers (None: all of them)
         self.out_spec = [torch.full((B, Hq, d), float("nan"), device=dev) for _ in range(layers)]
         self.in_place = False               # rows read from the device caches, no buffers
         self.copy = torch.cuda.Stream(device=dev)
@@ -93,10 +94,13 @@ class Loop:
                  "lr_w": self.lowrank[l][2] if l in self.lowrank else None,
                  "chunk": self.chunk if self.chunked(l) else 1,
                  "landmarks": self.lms[l] if self.chunked(l) else None,
-                 "k_local": self.local[step][l][0] if self.two else None,
-                 "v_local": self.local[step][l][1] if self.two else None,
-                 "out_spec": self.out_spec[l] if self.two else None}
+                 "k_local": self.local[step][l][0] if self.two_token(l) else None,
+                 "v_local": self.local[step][l][1] if self.two_token(l) else None,
+                 "out_spec": self.out_spec[l] if self.two_token(l) else None}
                 for l in range(self.L)]
+
+    def two_token(self, l):
+        return self.two and (self.two_layers is None or l in self.two_layers)
 
     def chunked(self, l):
         return self.chunk > 1 and (self.chunk_layers is None or l in self.chunk_layers)
