@@ -465,12 +465,13 @@ int ckv_pipeline_prime(ckv_pipeline* pipe, const ckv_shape* shape, int32_t k,
  * has idx_true set, or of CKV_ENTRY_DECODE_STEP (which serves every layer
  * kind) if any layer is chunked or has two tokens; it is used on the compute
  * stream only.  Without buffers and with the workspace of
- * CKV_ENTRY_DECODE_STEP, a plain layer followed by a plain layer leaves its
- * selection (idx_next, n_sel_next: not read before the next step) to the
- * next layer's launch, which runs it beside that layer's attention and
- * scoring; its own attention partials are then merged by a merge launch.
- * The last layer's pending selection runs before the call returns, and
- * before any chunked or two-token layer.  Results are the same either way.  A chunked or two-token layer runs the same pipelined step
+ * CKV_ENTRY_DECODE_STEP, a plain layer followed by a plain layer, or a
+ * two-token layer followed by a two-token layer, leaves its selection
+ * (idx_next, n_sel_next: not read before the next step) to the next layer's
+ * launch, which runs it beside that layer's attention and scoring; a plain
+ * layer's own attention partials are then merged by a merge launch.  A
+ * pending selection runs before the call returns and before a layer of
+ * another kind.  Results are the same either way.  A chunked or two-token layer runs the same pipelined step
  * (one launch attends over the previous set and scores for the next one) with
  * its selection over chunk landmarks or its second token; such a layer with
  * idx_true set is CKV_EINVAL.
