@@ -62,7 +62,10 @@ def test_landmarks_exact(wl, chunk, interleaved):
 # contexts of 700..1500 rows: at k 2048 every chunk of every unit is selected
 # and the last chunk is partial in most units
 EXTRA = {"short_s": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="short_s",
-                                        max_ctx=1500, ctx_min=700)}
+                                        max_ctx=1500, ctx_min=700),
+         # group sizes 8 and 2
+         "g8_s": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="g8_s", q_heads=64),
+         "g2_s": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="g2_s", q_heads=16)}
 
 
 def _workload(wl):
@@ -102,7 +105,8 @@ def _oracle_chunk_scores(w, chunk, q_sel_h, lm_h, lens_h):
     ("llama8b_s", 8, 512, None), ("llama8b_s", 4, 2048, None), ("llama8b_s", 7, 700, None),
     ("long128k_s", 16, 1024, None), ("short_s", 8, 2048, None), ("dual64_s", 2, 2048, None),
     # empty contexts, one partial chunk, a partial last chunk
-    ("llama8b_s", 8, 512, (0, 5)), ("llama8b_s", 8, 512, (13, 4999))])
+    ("llama8b_s", 8, 512, (0, 5)), ("llama8b_s", 8, 512, (13, 4999)),
+    ("g8_s", 8, 1024, None), ("g2_s", 4, 1024, None)])
 def test_chunked_kv_attn(wl, chunk, k, lens):
     """Same-step chunked decode: chunk set, rows and output, through the
     separate selection, expansion and attention kernels for small budgets and

@@ -59,12 +59,16 @@ def _run(w, layers, chunk_layers, two_layers, no_defer, dev, steps=2):
 
 
 WL = {"llama80": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="llama80", batch=10),
-      "dual96": dataclasses.replace(synth.WORKLOADS["dual64_s"], name="dual96", batch=12)}
+      "dual96": dataclasses.replace(synth.WORKLOADS["dual64_s"], name="dual96", batch=12),
+      # group sizes 8 and 2 (the 2G = 16 head rows of two tokens at G = 8)
+      "g8": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="g8", batch=10, q_heads=64),
+      "g2": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="g2", batch=10, q_heads=16)}
 
 
 @pytest.mark.parametrize("wl,layers,chunk_layers,two_layers", [
     ("llama80", 4, None, None), ("llama80", 4, (2,), None), ("llama80", 1, None, None),
-    ("dual96", 3, None, None), ("llama80", 4, None, "all"), ("llama80", 5, None, (1, 2, 4))])
+    ("dual96", 3, None, None), ("llama80", 4, None, "all"), ("llama80", 5, None, (1, 2, 4)),
+    ("g8", 3, None, None), ("g8", 3, None, "all"), ("g2", 3, None, (1, 2))])
 def test_deferred_selection_matches_undeferred(wl, layers, chunk_layers, two_layers):
     _log("deferred", wl, layers, chunk_layers, two_layers)
     dev = device()
