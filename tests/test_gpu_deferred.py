@@ -24,6 +24,7 @@ import dataclasses
 
 import numpy as np
 import pytest
+import torch
 
 import paper_2607_26475_amd as ckv
 import synth
@@ -110,3 +111,67 @@ def test_deferred_selection_matches_undeferred(wl, layers, chunk_layers, two_lay
         err = np.abs(g_out[l] - att).max()
         _log(f"  layer {l}: swaps {swaps}, max abs err {err:.2e}")
         assert err <= ATOL_OUT
+
+
+def test_full_llama8b_decode_step_deferred():
+    """Three full-size Llama-8B-shaped layers (B16, 32 / 8 heads, n 32768, k
+    2048) through one decode step without buffers, with the deferred
+    selections (five histogram slots per unit) and without: every set, count
+    and output bit for bit, and two sampled units of the middle layer's new
+    set against the oracle's selection."""
+    _log("full llama8b decode step, deferred")
+    dev = device()
+    w = synth.WORKLOADS["llama8b"]
+    L, G, k = 3, w.group, w.k
+    ts = [synth.make_layer(w, seed=0, layer=l, device=dev) for l in range(L)]
+    lens = ts[0]["ctx_lens"]
+    shape = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
+    i32 = dict(dtype=torch.int32, device=dev)
+    B, Hq, Hkv, d = w.batch, w.q_heads, w.kv_heads, w.head_dim
+    spec = []
+    for l, t in enumerate(ts):
+        g = synth.generator(w.name, 0, l, "spec", dev)
+        spec.append((0.8 * t["q"].float() + 0.6 * torch.randn(t["q"].shape, generator=g,
+                                                               device=dev)).to(torch.bfloat16))
+    ws = ckv.workspace(shape, k, ckv.ENTRY_DECODE_STEP)
+    idx0 = [torch.empty((B, Hkv, k), **i32) for _ in range(L)]
+    n0 = [torch.empty((B, Hkv), **i32) for _ in range(L)]
+    boot_out = torch.empty((B, Hq, d), device=dev)
+    for l, t in enumerate(ts):  # the pre-decoding selection
+        ckv.critical_kv_attn(shape, t["q"], spec[l], t["k"], lens, k, SCALE, t["k"], t["v"],
+                             ckv.SRC_DEVICE, None, None, None, idx0[l], n0[l], boot_out, ws)
+    res = []
+    for no_defer in (False, True):
+        idx1 = [torch.full((B, Hkv, k), -9, **i32) for _ in range(L)]
+        n1 = [torch.full((B, Hkv), -9, **i32) for _ in range(L)]
+        out = [torch.full((B, Hq, d), float("nan"), device=dev) for _ in range(L)]
+        io = [{"q_att": t["q"], "q_sel": spec[l], "k_score": t["k"], "k_src": t["k"],
+               "v_src": t["v"], "idx_prev": idx0[l], "n_sel_prev": n0[l], "idx_next": idx1[l],
+               "n_sel_next": n1[l], "out": out[l]} for l, t in enumerate(ts)]
+        pipe = ckv.Pipeline()
+        if no_defer:
+            pipe.set_checks(ckv.Pipeline.CHECK_NO_DEFER)
+        ckv.profile_begin()
+        pipe.step(shape, io, lens, k, SCALE, ckv.SRC_DEVICE, None, None, ws, None, None)
+        kernels = ckv.profile_end()
+        torch.cuda.synchronize()
+        pipe.close()
+        _log("  no_defer", no_defer, {n: v[0] for n, v in kernels.items()})
+        res.append(([i.cpu().numpy() for i in idx1], [n.cpu().numpy() for n in n1],
+                    [o.cpu().numpy() for o in out], kernels))
+    assert res[0][3]["finish"][0] == 1 and res[1][3]["finish"][0] == L, (res[0][3], res[1][3])
+    for part in range(3):
+        for l in range(L):
+            np.testing.assert_array_equal(res[0][part][l], res[1][part][l],
+                                          err_msg=f"layer {l} part {part}")
+    o = orc()
+    lens_h = lens.cpu().numpy()
+    q_sel = u16(spec[1])
+    for b, h in ((3, 5), (11, 2)):
+        n = int(lens_h[b])
+        S = o.unit_scores(q_sel[b, h * G:(h + 1) * G], u16(ts[1]["k"][b, h, :n]), SCALE)
+        r_idx, m = o.unit_select(S, k)
+        Sfull = np.full((1, 1, n), np.nan)
+        Sfull[0, 0] = S
+        check_index_sets(res[0][0][1][b:b + 1, h:h + 1], res[0][1][1][b:b + 1, h:h + 1],
+                         r_idx[None, None], np.array([[m]]), Sfull, np.array([n]))
