@@ -32,7 +32,8 @@ HBM_PEAK_GBPS = 8000.0
 COUNTERS = os.path.join(ROOT, "profiles", "score_llama8b_counters.txt")
 
 
-SECTIONS = ("main", "extras", "sweep", "host_link", "long128k", "dual64", "million", "cpu")
+SECTIONS = ("main", "extras", "pipelined", "sweep", "host_link", "long128k", "dual64", "million",
+            "cpu")
 
 
 def log(*a):
@@ -97,7 +98,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-host-link", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the dual-token, chunked, graph and pipelined-HBM sections "
+                    help="skip the dual-token, chunked and graph sections "
                          "(the main step alone, e.g. for its kernel profile)")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the pipelined long-context measurement")
@@ -140,8 +141,8 @@ def main() -> int:
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
     scale = float(np.float32(1.0 / math.sqrt(d)))
-    need_llama = [x for x in sections if x in ("main", "extras", "sweep", "cpu")]
-    n_layers = L if any(x in sections for x in ("main", "extras", "sweep")) else (
+    need_llama = [x for x in sections if x in ("main", "extras", "pipelined", "sweep", "cpu")]
+    n_layers = L if any(x in sections for x in ("main", "extras", "pipelined", "sweep")) else (
         1 if need_llama else 0)
 
     log(f"generating {n_layers} layers of {w.name} inputs on {torch.cuda.get_device_name(0)}")
@@ -213,13 +214,14 @@ def main() -> int:
         log(f"graph replay: {graph['ms_per_step']:.3f} ms/step, {graph['tokens_per_s']:.0f} "
             f"tokens/s, bit-identical {graph['bit_identical_to_eager']}")
         del idx, nsel, out, ws
+        result.update(chunked=chunked, graph=graph, dual_token=dual_token)
+    if "pipelined" in sections:
         pipelined_hbm = measure_pipelined_hbm(torch, ckv, layers, kv_ptrs, s, w, scale,
                                               args.steps, stream)
         log(f"pipelined, HBM: {pipelined_hbm['ms_per_step']:.3f} ms/step, "
             f"{pipelined_hbm['tokens_per_s']:.0f} tokens/s, per layer "
             f"{pipelined_hbm['per_layer_us']}")
-        result.update(chunked=chunked, pipelined_hbm=pipelined_hbm, graph=graph,
-                      dual_token=dual_token)
+        result.update(pipelined_hbm=pipelined_hbm)
 
     if "sweep" in sections and len(layers) == L:
         sweep = measure_attn_sweep(torch, ckv, layers, kv_ptrs, s, w, scale, stream)
