@@ -12,8 +12,9 @@ those of the same loop with every selection in its own layer's call
 deferred, the last one's run at the end of the call), a chunked layer in the
 middle (the pending selection runs before it), all layers two-token, plain
 and two-token layers mixed (a pending selection runs when the kind changes),
-a single layer, ragged contexts; two steps each, and the first step's plain
-layers also against the oracle.
+a single layer, ragged contexts, three seeded random sequences of the three
+kinds; two steps each, and the first step's plain layers also against the
+oracle.
 Deferral needs the per-workgroup histogram slots (at most 8 per unit, so at
 least about 74 units beside 512 scoring workgroups): the batches here have
 80 and 96 units.
@@ -66,10 +67,22 @@ WL = {"llama80": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="llama80
       "g2": dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="g2", batch=10, q_heads=16)}
 
 
+def _random_kinds(count=3, layers=6, seed=0):
+    """Seeded sequences of plain, two-token and chunked layers."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        kinds = rng.integers(0, 3, size=layers)
+        chunk = tuple(int(l) for l in np.nonzero(kinds == 2)[0]) or None
+        two = tuple(int(l) for l in np.nonzero(kinds == 1)[0]) or None
+        out.append(("llama80", layers, chunk, two))
+    return out
+
+
 @pytest.mark.parametrize("wl,layers,chunk_layers,two_layers", [
     ("llama80", 4, None, None), ("llama80", 4, (2,), None), ("llama80", 1, None, None),
     ("dual96", 3, None, None), ("llama80", 4, None, "all"), ("llama80", 5, None, (1, 2, 4)),
-    ("g8", 3, None, None), ("g8", 3, None, "all"), ("g2", 3, None, (1, 2))])
+    ("g8", 3, None, None), ("g8", 3, None, "all"), ("g2", 3, None, (1, 2))] + _random_kinds())
 def test_deferred_selection_matches_undeferred(wl, layers, chunk_layers, two_layers):
     _log("deferred", wl, layers, chunk_layers, two_layers)
     dev = device()
