@@ -10,7 +10,9 @@ path, and the many-workgroup selection.  Each case checks the same-step call
 (Sec. 2.2 selection, Sec. 5.3-5.4 attention).  Its index sets are compared
 with the oracle's under the near-tie rule, and its output with the oracle's
 attention over the GPU's set.  Then the case checks the pipelined call that
-attends over that set in place and selects with a second query.
+attends over that set in place and selects with a second query.  The same
+holds for co-batched dual-token attention (random per-unit counts) and the
+same-step chunked call (random chunk sizes, budgets whole multiples of them).
 """
 from __future__ import annotations
 
@@ -84,4 +86,121 @@ def test_random_shape_fused_entry(name, B, Hq, Hkv, n, k, lens, dual, keys):
     swaps = check_index_sets(s_idx, s_nsel, r_idx, r_nsel, S_sel, lens_h)
     err = np.abs(s_out - oracle_attn_over(so, q_att, K, V, f_idx, f_nsel, k)).max()
     print(f"  pipelined in place: tolerated swaps {swaps}, max abs err {err:.2e}", flush=True)
+    assert err <= ATOL_OUT
+
+
+def _dual_cases(count=16, seed=20261203):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.choice([1, 2, 4, 8]))  # 2G head rows fill at most the 16 MFMA rows
+        b = int(rng.integers(1, 8))
+        k = int(rng.integers(1, 3001))
+        cases.append((f"d{i:02d}_b{b}_h{hkv}x{g}_k{k}", b, g * hkv, hkv, k, int(rng.integers(1 << 30))))
+    return cases
+
+
+DUAL = _dual_cases()
+
+
+@pytest.mark.parametrize("name,B,Hq,Hkv,k,seed", DUAL, ids=[c[0] for c in DUAL])
+def test_random_shape_dual_token(name, B, Hq, Hkv, k, seed):
+    """Co-batched dual-token attention (Sec. 5.2) over buffers with random
+    per-unit counts in [0, k], both tokens against the oracle."""
+    print("random dual token", name, flush=True)
+    dev = device()
+    rng = np.random.default_rng(seed)
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    d = 128
+    bf = lambda *shape, sc=1.0: (torch.randn(shape, generator=g, device=dev) * sc).to(
+        torch.bfloat16)
+    q_cur = bf(B, Hq, d)
+    q_spec = (0.8 * q_cur.float() + 0.6 * torch.randn((B, Hq, d), generator=g, device=dev)).to(
+        torch.bfloat16)
+    k_buf, v_buf = bf(B, Hkv, k, d), bf(B, Hkv, k, d)
+    k_loc, v_loc = bf(B, Hkv, 2, d, sc=2.0), bf(B, Hkv, 2, d)
+    ns = rng.integers(0, k + 1, size=(B, Hkv)).astype(np.int32)
+    ns.flat[0] = k  # one full buffer
+    n_sel = torch.from_numpy(ns).to(dev)
+    s = ckv.shape_for(B, Hq, Hkv, 4096)
+    ws = ckv.workspace(s, k, ckv.ENTRY_DUAL_TOKEN_ATTN)
+    out_c = torch.full((B, Hq, d), float("nan"), device=dev)
+    out_s = torch.full_like(out_c, float("nan"))
+    ckv.dual_token_attn(s, q_cur, q_spec, k_buf, v_buf, n_sel, k_loc, v_loc, k, SCALE, out_c,
+                        out_s, ws)
+    torch.cuda.synchronize()
+    o = orc()
+    so = o.shape(B, Hq, Hkv, d, 4096)
+    rc, rs = o.dual_token_attn(so, u16(q_cur), u16(q_spec), u16(k_buf), u16(v_buf), ns,
+                               u16(k_loc), u16(v_loc), k, SCALE, nthreads=8)
+    ec = np.abs(out_c.cpu().numpy() - rc).max()
+    es = np.abs(out_s.cpu().numpy() - rs).max()
+    print(f"  max abs err current {ec:.2e}, speculative {es:.2e}", flush=True)
+    assert ec <= ATOL_OUT and es <= ATOL_OUT
+
+
+def _chunk_cases(count=16, seed=20261204):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.choice([1, 2, 4, 8, 16]))
+        b = int(rng.integers(1, 8))
+        chunk = int(rng.choice([1, 2, 3, 4, 7, 8, 16, 33, 64]))
+        n = int(rng.integers(chunk, 30001))
+        k = chunk * int(rng.integers(1, max(2, min(2048, n + 64) // chunk) + 1))
+        lens = rng.integers(0, n + 1, size=b)
+        if i % 3 == 0:
+            lens[0] = n
+        if i % 4 == 1:
+            lens[-1] = 0
+        cases.append((f"c{i:02d}_b{b}_h{hkv}x{g}_C{chunk}_n{n}_k{k}", b, g * hkv, hkv, chunk, n,
+                      k, [int(x) for x in lens]))
+    return cases
+
+
+CHUNK = _chunk_cases()
+
+
+@pytest.mark.parametrize("name,B,Hq,Hkv,chunk,n,k,lens", CHUNK, ids=[c[0] for c in CHUNK])
+def test_random_shape_chunked(name, B, Hq, Hkv, chunk, n, k, lens):
+    """Same-step chunked decode (Sec. 2.2 chunk landmarks): the chunk sets
+    under the near-tie rule on the oracle's chunk scores, the rows as the
+    exact expansion of the GPU's chunks, the output against the oracle's
+    attention over those rows."""
+    from test_gpu_chunks import _landmarks, _oracle_chunk_scores
+    print("random chunked", name, "lens", lens, flush=True)
+    dev = device()
+    w = synth.Workload(name, B, Hq, Hkv, 128, n, n, k, 1, "hbm", False, "normal")
+    t = synth.make_layer(w, seed=13, device=dev)
+    t["ctx_lens"] = torch.tensor(lens, dtype=torch.int32, device=dev)
+    s = ckv.shape_for(B, Hq, Hkv, n)
+    lm = _landmarks(s, chunk, t["k"], t["ctx_lens"], dev)
+    kc = k // chunk
+    i32 = dict(dtype=torch.int32, device=dev)
+    cidx, rows = torch.full((B, Hkv, kc), -9, **i32), torch.full((B, Hkv, k), -9, **i32)
+    nch, nrows = torch.full((B, Hkv), -9, **i32), torch.full((B, Hkv), -9, **i32)
+    out = torch.full((B, Hq, 128), float("nan"), device=dev)
+    ws = ckv.workspace(s, k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    ckv.chunked_kv_attn(s, chunk, t["q"], t["q_sel"], lm, t["ctx_lens"], k, SCALE, t["k"],
+                        t["v"], ckv.SRC_DEVICE, cidx, nch, rows, nrows, out, ws)
+    torch.cuda.synchronize()
+    lens_h = np.array(lens, dtype=np.int32)
+    lm_h = lm.cpu().numpy().view(np.uint16)
+    q_sel_h, q_att_h, K, V = u16(t["q_sel"]), u16(t["q"]), u16(t["k"]), u16(t["v"])
+    S, clens = _oracle_chunk_scores(w, chunk, q_sel_h, lm_h, lens_h)
+    o = orc()
+    so = o.shape(B, Hq, Hkv, 128, n)
+    r_c, r_nc, _, _ = o.select_chunks(so, chunk, q_sel_h, lm_h, lens_h, k, SCALE, nthreads=8)
+    g_c, g_nc = cidx.cpu().numpy(), nch.cpu().numpy()
+    g_r, g_nr = rows.cpu().numpy(), nrows.cpu().numpy()
+    swaps = check_index_sets(g_c, g_nc, r_c, r_nc, S, clens)
+    for b in range(B):
+        for h in range(Hkv):
+            want, nr = o.expand_chunks(chunk, g_c[b, h, :g_nc[b, h]], int(lens_h[b]), k)
+            assert g_nr[b, h] == nr and np.array_equal(g_r[b, h], want), (b, h)
+    err = np.abs(out.cpu().numpy() - oracle_attn_over(so, q_att_h, K, V, g_r, g_nr, k)).max()
+    print(f"  tolerated swaps {swaps}, max abs err {err:.2e}", flush=True)
     assert err <= ATOL_OUT
