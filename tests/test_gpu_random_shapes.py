@@ -12,7 +12,9 @@ with the oracle's under the near-tie rule, and its output with the oracle's
 attention over the GPU's set.  Then the case checks the pipelined call that
 attends over that set in place and selects with a second query.  The same
 holds for co-batched dual-token attention (random per-unit counts) and the
-same-step chunked call (random chunk sizes, budgets whole multiples of them).
+same-step chunked call (random chunk sizes, budgets whole multiples of them),
+and for two steps of the decode loop, host-pinned behind the two buffers or
+in place.
 """
 from __future__ import annotations
 
@@ -204,3 +206,62 @@ def test_random_shape_chunked(name, B, Hq, Hkv, chunk, n, k, lens):
     err = np.abs(out.cpu().numpy() - oracle_attn_over(so, q_att_h, K, V, g_r, g_nr, k)).max()
     print(f"  tolerated swaps {swaps}, max abs err {err:.2e}", flush=True)
     assert err <= ATOL_OUT
+
+
+def _loop_cases(count=10, seed=20261205):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.choice([1, 2, 4, 8, 16]))
+        b = int(rng.integers(1, 8))
+        n = int(rng.integers(16, 20001))
+        nmin = int(rng.integers(0, n + 1))
+        k = int(rng.integers(1, min(2048, n + 64) + 1))
+        layers = int(rng.integers(2, 5))
+        in_place = bool(i % 2)
+        cases.append((f"p{i:02d}_b{b}_h{hkv}x{g}_n{nmin}-{n}_k{k}_L{layers}_"
+                       + ("inplace" if in_place else "buffers"), b, g * hkv, hkv, n, nmin, k,
+                       layers, in_place))
+    return cases
+
+
+LOOP = _loop_cases()
+
+
+@pytest.mark.parametrize("name,B,Hq,Hkv,n,nmin,k,layers,in_place", LOOP,
+                         ids=[c[0] for c in LOOP])
+def test_random_shape_decode_loop(name, B, Hq, Hkv, n, nmin, k, layers, in_place):
+    """The decode loop (Sec. 5.3-5.4) over two steps, with the caches
+    host-pinned behind the two buffers or in HBM read in place: every layer's
+    new set against the oracle's selection from that step's speculative
+    query, and its output against the oracle's attention over the set chosen
+    one step earlier."""
+    from test_gpu_pipeline import Loop
+    print("random loop", name, flush=True)
+    dev = device()
+    w = synth.Workload(name, B, Hq, Hkv, 128, n, nmin, k, layers,
+                       "hbm" if in_place else "host", True, "normal")
+    lp = Loop(w, layers, steps=2, seed=23, dev=dev)
+    lp.in_place = in_place
+    lp.bootstrap()
+    boot = ([i.cpu().numpy() for i in lp.idx[0]], [x.cpu().numpy() for x in lp.nsel[0]])
+    pipe = ckv.Pipeline()
+    hist = lp.run(2, pipe)
+    pipe.close()
+    o = orc()
+    lens = lp.lens.cpu().numpy()
+    so = o.shape(B, Hq, Hkv, 128, n)
+    prev = boot
+    for st in (1, 2):
+        g_idx, g_nsel, g_out = hist[st - 1][:3]
+        for l in range(layers):
+            K, V = u16(lp.t[l]["k"]), u16(lp.t[l]["v"])
+            S = o.score_keys(so, u16(lp.q_sel[st][l]), K, lens, SCALE, nthreads=8)
+            r_idx, r_nsel = o.select_topk(so, S, lens, k, nthreads=8)
+            swaps = check_index_sets(g_idx[l], g_nsel[l], r_idx, r_nsel, S, lens)
+            ref = oracle_attn_over(so, u16(lp.q_att[st][l]), K, V, prev[0][l], prev[1][l], k)
+            err = np.abs(g_out[l] - ref).max()
+            print(f"  step {st} layer {l}: swaps {swaps}, max abs err {err:.2e}", flush=True)
+            assert err <= ATOL_OUT
+        prev = (g_idx, g_nsel)
