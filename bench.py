@@ -29,7 +29,7 @@ if ROOT not in sys.path:
 METRIC = ("decode-step attention tokens/s at batch×context; "
           "achieved HBM GB/s + host GB/s")
 HBM_PEAK_GBPS = 8000.0
-COUNTERS = os.path.join(ROOT, "profiles", "score_llama8b_counters.txt")
+COUNTERS = os.path.join(ROOT, "profiles", "critical_llama8b_counters.txt")
 
 
 SECTIONS = ("main", "extras", "pipelined", "sweep", "host_link", "long128k", "dual64", "million",
@@ -46,23 +46,25 @@ def median(xs):
     return xs[n // 2] if n % 2 else 0.5 * (xs[n // 2 - 1] + xs[n // 2])
 
 
-SCORE_SOURCES = ("ckv_score.hpp", "ckv_device.hpp")
+KERNEL_SOURCES = ("ckv_score.hpp", "ckv_device.hpp", "ckv_topk.hpp", "ckv_attn.hpp",
+                  "ckv_kernels.hip")
 
 
 def source_digest() -> str:
-    """sha256 over the sources of the scoring kernel (counters taken on other
+    """sha256 over the sources of the step's kernels (counters taken on other
     sources are stale)."""
     h = hashlib.sha256()
-    for name in SCORE_SOURCES:
+    for name in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2607_26475_amd", "csrc", name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()
 
 
-def read_counters():
-    """HBM bytes per launch of the scoring kernel from the committed rocprofv3
-    counter summary, or None if absent or taken on other sources."""
+def read_counters(kernel):
+    """HBM bytes per launch of the step's dominant kernel from the committed
+    rocprofv3 counter summary, or None if absent, taken on other sources or
+    for another kernel."""
     if not os.path.exists(COUNTERS):
         return None
     vals = {}
@@ -70,7 +72,7 @@ def read_counters():
         if ":" in line:
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("source_sha256") != source_digest():
+    if vals.get("source_sha256") != source_digest() or vals.get("kernel") != kernel:
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -326,8 +328,15 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
     ms_step, per_step = timed(args.steps)
     dstats = ckv.profile_end()
     ms_plain, _ = timed(args.steps)  # same steps with no stamps at all (overhead check)
+    # the same steps with the scoring launch and the selection and attention
+    # launch apart (the two-launch form of the same results), for comparison
+    ckv.set_one_launch_same_step(False)
+    try:
+        ms_two, _ = timed(args.steps)
+    finally:
+        ckv.set_one_launch_same_step(True)
     log(f"  {ms_step:.3f} ms/step, median {median(per_step):.3f} ({ms_plain:.3f} ms/step "
-        f"unstamped)")
+        f"unstamped, {ms_two:.3f} with the layer as two launches)")
     log("  per layer: " + ", ".join(f"{kname} {v['avg_us']:.1f} us"
                                    for kname, v in per_kernel.items()))
     assert all(torch.isfinite(o).all().item() for o in out[:2])
@@ -344,10 +353,12 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
         # the same rows, attended by the one-launch selection and attention
         # (its reads of the scores are implementation bytes)
         "select_attn": units * k * 2 * d * 2,
+        # the layer in one launch: the key scan and the selected rows
+        "critical": units * n * d * 2 + units * k * 2 * d * 2,
     }
     algo_bytes = algo.get(dominant)
     achieved = algo_bytes / avg_s / 1e9 if algo_bytes else None
-    traffic = read_counters() if dominant == "score" else None
+    traffic = read_counters(dominant)
     roofline = {
         "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
         "frac": achieved / HBM_PEAK_GBPS if achieved else None, "traffic": traffic,
@@ -369,6 +380,7 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
     del idx, nsel, out, ws
     return {"value": tokens_per_s, "ms_per_step": ms_step,
             "ms_per_step_median": median(per_step), "ms_per_step_unstamped": ms_plain,
+            "ms_per_step_two_launches": ms_two,
             "hbm_algorithmic_gbps_step": step_bytes / (ms_step * 1e-3) / 1e9,
             "kernels": per_kernel, "roofline": roofline}
 
@@ -386,7 +398,17 @@ def measure_attn_sweep(torch, ckv, layers, kv_ptrs, shape, w, scale, stream,
     1 GiB per budget, for the same reason).  A line through the points, time
     = fixed + bytes / rate, splits a launch into what does not grow with the
     bytes (launch, selection, first round trip, the waves' merge, drain) and the
-    streaming rate of the selected rows.  Dispatch-stamped kernel times."""
+    streaming rate of the selected rows.  Dispatch-stamped kernel times.  The
+    same-step calls run in the two-launch form here, so that the selection
+    and attention launch is timed apart from the scoring."""
+    ckv.set_one_launch_same_step(False)
+    try:
+        return _attn_sweep(torch, ckv, layers, kv_ptrs, shape, w, scale, stream, budgets, reps)
+    finally:
+        ckv.set_one_launch_same_step(True)
+
+
+def _attn_sweep(torch, ckv, layers, kv_ptrs, shape, w, scale, stream, budgets, reps):
     import numpy as np
     dev = torch.device("cuda:0")
     B, Hq, Hkv, d = w.batch, w.q_heads, w.kv_heads, w.head_dim

@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 7
+#define CKV_ABI_VERSION 8
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -514,7 +514,8 @@ typedef enum ckv_kernel_id {
   CKV_K_RECONSTRUCT = 12, /* low-rank key rebuild (with the misses' V fetch)  */
   CKV_K_SELECT_ATTN = 13, /* same-step selection and attention in one launch */
   CKV_K_PROBE = 14,   /* read-rate probe (ckv_probe_read_rows)              */
-  CKV_K_COUNT = 15
+  CKV_K_CRITICAL = 15, /* same-step scoring, selection and attention in one launch */
+  CKV_K_COUNT = 16
 } ckv_kernel_id;
 
 #define CKV_K_ALL ((1u << CKV_K_COUNT) - 1u)
@@ -559,6 +560,23 @@ int ckv_profile_end(ckv_kernel_stats* stats);
  * stream, so that a failing kernel is reported by the entry that launched it
  * (CKV_EHIP).  Debug mode synchronises, so it is not for graph capture. */
 int ckv_set_debug(int on);
+
+/* ---- the same-step layer in one launch ---------------------------------------
+ * Where it applies, a same-step call of ckv_critical_kv_attn (or of
+ * ckv_critical_kv_attn_noalloc) scores, selects and attends in one launch:
+ * the group size is 2, 4 or 8, the batch has a multiple of 8 units with two
+ * workgroups per unit fitting on the device, 512 <= k <= 2048, max_ctx <=
+ * 65536, and the per-workgroup histogram slots apply (at least about 40
+ * units).  Each unit's selection
+ * and attention then start as soon as that unit's scores are complete (Sec. 2.2
+ * selection inside the step, with the attention of Sec. 5.3-5.4), not after
+ * the whole scoring pass.  The launch hands each unit's scores over through
+ * flags in the workspace, which are zero again when it ends.  Otherwise, or
+ * with this setting off, the call runs the scoring launch, then the
+ * selection and attention launch.  Both forms give the same bits.  The
+ * setting (on: nonzero; process-wide; on by default) is for comparing the
+ * two; calls already launched keep their form. */
+int ckv_set_one_launch_same_step(int on);
 
 /* ---- read-rate probe -------------------------------------------------------
  * For measurement, not for serving: reads the K and V rows that idx selects

@@ -28,7 +28,7 @@ __all__ = [
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "ENTRY_DECODE_STEP",
     "EXPORTS", "probe_read_rows", "probe_sink_words", "PROBE_STANDALONE", "PROBE_ROW_HALVES",
-    "PROBE_HEAD_HALVES", "set_debug",
+    "PROBE_HEAD_HALVES", "set_debug", "set_one_launch_same_step",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
@@ -49,10 +49,11 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_pipeline_create", "ckv_pipeline_destroy", "ckv_pipeline_set_gather_width",
            "ckv_pipeline_set_checks",
            "ckv_pipeline_prime",
-           "ckv_decode_step", "ckv_probe_read_rows", "ckv_probe_sink_words", "ckv_set_debug")
-KERNEL_COUNT = 15
+           "ckv_decode_step", "ckv_probe_read_rows", "ckv_probe_sink_words", "ckv_set_debug",
+           "ckv_set_one_launch_same_step")
+KERNEL_COUNT = 16
 MAX_RANK = 4096
-ABI_VERSION = 7  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
+ABI_VERSION = 8  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -133,6 +134,7 @@ def _load() -> ctypes.CDLL:
         "ckv_probe_read_rows": (ctypes.c_int, [sp, vp, vp, vp, i32, ctypes.c_int, vp, sz, vp]),
         "ckv_probe_sink_words": (sz, [sp, i32, ctypes.c_int]),
         "ckv_set_debug": (ctypes.c_int, [ctypes.c_int]),
+        "ckv_set_one_launch_same_step": (ctypes.c_int, [ctypes.c_int]),
         "ckv_pipeline_create": (ctypes.c_int, [ctypes.POINTER(vp)]),
         "ckv_pipeline_destroy": (ctypes.c_int, [vp]),
         "ckv_pipeline_set_gather_width": (ctypes.c_int, [vp, ctypes.c_int]),
@@ -330,7 +332,8 @@ def chunked_kv_attn(shape: Shape, chunk: int, q_att, q_sel, landmarks, ctx_lens,
 
 KERNEL_IDS = {"zero": 0, "score": 1, "hist": 2, "filter": 3, "finish": 4, "attn": 5,
               "combine": 6, "dual": 7, "gather": 8, "miss": 9, "landmarks": 10,
-              "expand": 11, "reconstruct": 12, "select_attn": 13, "probe": 14}
+              "expand": 11, "reconstruct": 12, "select_attn": 13, "probe": 14,
+              "critical": 15}
 
 
 def profile_begin(kernels=None, every: int = 1) -> None:
@@ -359,6 +362,13 @@ def set_debug(on: bool) -> None:
     (context lengths, input counts and index sets) on the device and every
     launch synchronises; a violation raises CkvError (CKV_EINVAL)."""
     _check("ckv_set_debug", _lib.ckv_set_debug(1 if on else 0))
+
+
+def set_one_launch_same_step(on: bool) -> None:
+    """Whether same-step calls run as one launch where that form applies
+    (process-wide, on by default); off, as the scoring launch then the
+    selection and attention launch.  Both forms give the same bits."""
+    _check("ckv_set_one_launch_same_step", _lib.ckv_set_one_launch_same_step(1 if on else 0))
 
 
 def probe_sink_words(shape: Shape, k: int, mode: int) -> int:

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -93,6 +94,19 @@ struct Dims {
   int64_t key_stride, kv_stride;
 };
 
+// ckv_set_one_launch_same_step
+std::atomic<int> g_one_launch{1};
+
+// A tag for one launch of the one-launch same-step kernel: a 32-bit value
+// that is never zero in the high half and its complement in the low half.
+uint64_t next_fused_tag() {
+  static std::atomic<uint32_t> counter{0};
+  uint32_t t = counter.fetch_add(1u, std::memory_order_relaxed) + 1u;
+  t *= 2654435761u;  // spread consecutive calls over the 32 bits
+  t |= 1u;
+  return ((uint64_t)t << 32) | (uint32_t)~t;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 int check_shape(const ckv_shape* s, Dims* d) {
@@ -172,6 +186,7 @@ struct Layout {
   size_t slot_of = 0, miss_pos = 0, miss_slot = 0, n_miss = 0, free_slot = 0, total = 0;
   size_t chunk_idx = 0, n_chunks = 0;  // decode step: selected chunks of a chunked layer
   size_t scores_b = 0, hist_part_b = 0;  // decode step: the second scores and slots region
+  size_t flags = 0;  // the same-step layer in one launch: hand-over flags per slot
   int64_t bm_words = 0;
   int chunks = 0, filter_tiles = 0;
 };
@@ -226,6 +241,10 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
     L.hist_part = off;
     L.hist_part_bytes = (U + (size_t)std::min<int64_t>(groups, kMaxScoreWgs)) * kHistBins * 4;
     off = align256(off + L.hist_part_bytes);
+    if (entry == CKV_ENTRY_CRITICAL_KV_ATTN) {  // two 64-bit flags per slot
+      L.flags = off;
+      off = align256(off + (U + (size_t)std::min<int64_t>(groups, kMaxScoreWgs)) * 16);
+    }
   }
   if (attn) {
     L.part = off;
@@ -351,6 +370,7 @@ SelectArgs select_args(const Dims& d, const Layout& L, void* ws, const float* sc
   a.mpart = nullptr;
   a.mout = nullptr;
   a.mchunks = a.mG = a.mHq = 0;
+  a.affine = 0;
   return a;
 }
 
@@ -1009,11 +1029,20 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
       return rc;
     }
   } else {
-    CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
                              d.kv_stride, k, scale, out);
     int heads;
-    if (const int S = select_attn_splits(d, k, L, &heads)) {
+    const int S = select_attn_splits(d, k, L, &heads);
+    if (S == 1 && heads == 2 && partials && L.flags && g_one_launch.load() &&
+        critical_blocks(d.G, d.U, nwg)) {
+      // scoring, selection and attention in one launch, XCD-affine slots
+      sa.affine = 1;
+      const FusedSync fs{at<uint64_t>(ws, L.flags), next_fused_tag()};
+      CKV_TRY_HIP(launch_critical(sc, sa, at_, fs, d.G, nwg, s), "same-step launch");
+      return CKV_OK;
+    }
+    CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
+    if (S) {
       // each workgroup selects its unit's set and attends over its share of
       // the rows, or over the whole set with its share of the heads
       at_.chunks = S;
@@ -1028,6 +1057,11 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
 }
 
 extern "C" {
+
+int ckv_set_one_launch_same_step(int on) {
+  g_one_launch.store(on ? 1 : 0);
+  return CKV_OK;
+}
 
 int ckv_critical_kv_attn_noalloc(const ckv_shape* shape, const uint16_t* q_att,
                                  const uint16_t* q_sel, const uint16_t* k_score,

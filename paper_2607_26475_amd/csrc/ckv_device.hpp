@@ -114,6 +114,22 @@ struct SelectArgs {
   const float* mpart;       // [U][mchunks][mG][kPartStride]
   float* mout;              // [B][mHq][d]
   int mchunks, mG, mHq;
+  // Non-zero: the slots come from the XCD-affine ranges of the one-launch
+  // same-step kernel (xcd_slot0), not from ranges in plain unit order.
+  int affine;
+};
+
+
+// The one-launch same-step kernel's hand-over from scoring to selection:
+// once a scoring workgroup's scores and histogram slot of a unit are stored
+// (device-coherent stores, waited for), it sets that slot's two flags, one for
+// each of the unit's two attending workgroups, to the launch's tag; each of
+// those waits for its flags of all the unit's slots and then clears them, so
+// that they are zero again after the launch.  The tag's halves are each
+// other's complement, so no stale word and no zero matches it.
+struct FusedSync {
+  uint64_t* flags;  // [U + kMaxScoreWgs][2]
+  uint64_t tag;
 };
 
 struct AttnArgs {
@@ -217,6 +233,27 @@ __device__ __forceinline__ int clamp_len(int n, int hi) {
 // [wg*T/nwg, (wg+1)*T/nwg)) that holds group g.
 __host__ __device__ __forceinline__ int64_t range_owner(int64_t g, int64_t T, int64_t nwg) {
   return ((g + 1) * nwg - 1) / T;
+}
+
+// The one-launch same-step kernel's scoring ranges: its scoring workgroups
+// are spread over the 8 XCDs round-robin by index, and the workgroups
+// x, x + 8, x + 16, ... (XCD x) score the units x, x + 8, x + 16, ... in
+// balanced contiguous ranges of those units' groups.  A unit's scores are
+// then written on the XCD where its selection and attention run (the same
+// index map, split_block), and the units of an XCD are complete as soon as
+// that XCD's ranges are.  Needs U and nwg multiples of 8.  The slot of (unit,
+// workgroup) is unique within XCD x's block of U/8 + nwg/8 slots, as in plain
+// unit order.  xcd_slot0 returns the first slot of `unit` and the number of
+// consecutive slots that hold its histogram.
+__host__ __device__ __forceinline__ int64_t xcd_slot0(int unit, int units, int nwg,
+                                                      int64_t gu, int* nslots) {
+  const int x = unit & 7, v = unit >> 3;
+  const int ux = units >> 3, nx = nwg >> 3;
+  const int64_t T = (int64_t)ux * gu;
+  const int64_t lo = range_owner((int64_t)v * gu, T, nx);
+  const int64_t hi = range_owner((int64_t)v * gu + gu - 1, T, nx);
+  *nslots = (int)(hi - lo + 1);
+  return (int64_t)x * (ux + nx) + v + lo;
 }
 
 // Monotone map from fp32 to uint32: a < b as floats <=> key(a) < key(b);

@@ -327,7 +327,7 @@ constexpr int kSelPer = 32;
 constexpr int kSelBatch = kSelPer * kFinishThreads;
 static_assert(kFusedSelectMaxCtx % kSelBatch == 0, "whole batches");
 
-template <int NT = kFinishThreads>
+template <int NT = kFinishThreads, bool COH = false>
 __device__ __forceinline__ void load_score_batch(const float* srow, int j0, int n,
                                                  float (&sv)[kSelPer]) {
   // unconditional loads (clamped position); 32-bit byte offsets from the
@@ -336,7 +336,11 @@ __device__ __forceinline__ void load_score_batch(const float* srow, int j0, int 
 #pragma unroll
   for (int u = 0; u < kSelPer; ++u) {
     const uint32_t off = 4u * (uint32_t)min(j0 + u * NT + (int)threadIdx.x, n - 1);
-    sv[u] = *reinterpret_cast<const float*>(base + off);
+    if constexpr (COH)  // stored by other workgroups of the same launch
+      sv[u] = __hip_atomic_load(reinterpret_cast<const float*>(base + off), __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
+    else
+      sv[u] = *reinterpret_cast<const float*>(base + off);
   }
 }
 
@@ -503,7 +507,7 @@ struct SelLds {
 // histogram and control words are left cleared; only the unit's one reader
 // may do that (kFinishThreads workgroups only).  Returns the number of
 // positions selected.
-template <int NT = kFinishThreads, int CAP = kCandLds>
+template <int NT = kFinishThreads, int CAP = kCandLds, bool COH = false>
 __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const SelLds& L,
                                            bool write, int32_t* share, uint32_t lo,
                                            uint32_t hi, bool clear) {
@@ -526,22 +530,27 @@ __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const 
   int nslots = 1;
   if (a.hist_part) {
     const int64_t gu = (a.max_ctx + kStageRows - 1) / kStageRows;
-    const int64_t T = gu * a.units, g0 = (int64_t)unit * gu;
-    const int64_t lo_wg = range_owner(g0, T, a.score_nwg);
-    const int64_t hi_wg = range_owner(g0 + gu - 1, T, a.score_nwg);
-    slots = a.hist_part + (unit + lo_wg) * kHistBins;
-    nslots = (int)min<int64_t>(hi_wg - lo_wg + 1, kMaxPartials);  // the host keeps it below
+    if (a.affine) {
+      slots = a.hist_part + xcd_slot0(unit, a.units, a.score_nwg, gu, &nslots) * kHistBins;
+      nslots = min(nslots, kMaxPartials);  // the host keeps it below
+    } else {
+      const int64_t T = gu * a.units, g0 = (int64_t)unit * gu;
+      const int64_t lo_wg = range_owner(g0, T, a.score_nwg);
+      const int64_t hi_wg = range_owner(g0 + gu - 1, T, a.score_nwg);
+      slots = a.hist_part + (unit + lo_wg) * kHistBins;
+      nslots = (int)min<int64_t>(hi_wg - lo_wg + 1, kMaxPartials);  // the host keeps it below
+    }
   }
   const int len_b = a.ctx_lens[unit / a.Hkv];
   uint2 hv[kMaxPartials][kHistBins / NT / 2];
-  load_hist_slots<NT>(slots, nslots, hv);
+  load_hist_slots<NT, COH>(slots, nslots, hv);
   // every wave's histogram loads queue ahead of all score loads (a bare
   // barrier: no wait for the loads themselves)
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   const float* srow = a.scores + (int64_t)unit * a.max_ctx;
   float sv0[kSelPer];
-  load_score_batch<NT>(srow, 0, a.max_ctx, sv0);
+  load_score_batch<NT, COH>(srow, 0, a.max_ctx, sv0);
   __builtin_amdgcn_sched_barrier(0);  // n_b is waited for only here
   const int n = unit_len(len_b, a.max_ctx, a.chunk);
   const int m = min(a.k, n);
@@ -580,7 +589,7 @@ __device__ __forceinline__ int select_unit(const SelectArgs& a, int unit, const 
   classify_batch<NT, CAP>(sv0, 0, g_lo, g_hi, bm, cs, &misc[7]);
   for (int j0 = kBatch; j0 < n; j0 += kBatch) {
     float sv[kSelPer];
-    load_score_batch<NT>(srow, j0, n, sv);
+    load_score_batch<NT, COH>(srow, j0, n, sv);
     pad(sv, j0);
     classify_batch<NT, CAP>(sv, j0, g_lo, g_hi, bm, cs, &misc[7]);
   }
@@ -661,18 +670,17 @@ __device__ __forceinline__ void split_block(int blk, int nsplit, int* unit, int*
 // set with G / HEADS of the heads and write their outputs directly (no
 // partials, no merge launch); the second workgroup's reads of each row come
 // while the first one's are recent, from the XCD's L2.
-template <int G, int HEADS>
-__global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, AttnArgs at,
-                                                                  int nsplit) {
+// One workgroup's part of k_select_attn: the selection of `unit`, then the
+// attention over its share of the rows or with its share of the heads.
+// COH: the scores and slots were stored by other workgroups of the same launch.
+template <int G, int HEADS, bool COH = false>
+__device__ __forceinline__ void select_attn_part(const SelectArgs& sa, const AttnArgs& at,
+                                                 int unit, int split, int nsplit,
+                                                 uint32_t* lds, uint32_t* tmp,
+                                                 uint32_t* misc) {
   static_assert(G % HEADS == 0, "whole heads per workgroup");
   constexpr int GA = G / HEADS;  // heads each workgroup attends with
   using Lds = SelAttnLds<GA>;
-  __shared__ __attribute__((aligned(16))) uint32_t lds[Lds::kDwords];
-  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
-  __shared__ uint32_t misc[8];
-  int unit, split;
-  split_block(blockIdx.x, HEADS > 1 ? HEADS : nsplit, &unit, &split);
-  if (unit >= sa.units) return;  // uniform over the workgroup
   const SelLds L{reinterpret_cast<uint2*>(lds), lds + 2 * kCandLds,
                  lds + 2 * kCandLds + kFusedSelectMaxCtx / 32, tmp, misc};
   int32_t* share = reinterpret_cast<int32_t*>(lds + Lds::kPosOff);
@@ -682,11 +690,74 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
   int lo = 0, hi = min(sa.k, n);
   if (HEADS == 1) share_range(hi, split, nsplit, &lo, &hi);
   // the workgroups of a unit all read its histogram: none clears it
-  select_unit(sa, unit, L, split == 0, share, (uint32_t)lo, (uint32_t)hi, false);
+  select_unit<kFinishThreads, kCandLds, COH>(sa, unit, L, split == 0, share, (uint32_t)lo,
+                                             (uint32_t)hi, false);
   __syncthreads();
   const int qh0 = (unit % sa.Hkv) * G + (HEADS > 1 ? split * GA : 0);
   attn_wg<GA>(at, unit, LdsRows{share}, hi - lo, HEADS > 1 ? 0 : split, HEADS > 1 ? 1 : nsplit,
               lds, lds + Lds::kQOff, qh0);
+}
+
+template <int G, int HEADS>
+__global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, AttnArgs at,
+                                                                  int nsplit) {
+  __shared__ __attribute__((aligned(16))) uint32_t lds[SelAttnLds<G / HEADS>::kDwords];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  int unit, split;
+  split_block(blockIdx.x, HEADS > 1 ? HEADS : nsplit, &unit, &split);
+  if (unit >= sa.units) return;  // uniform over the workgroup
+  select_attn_part<G, HEADS>(sa, at, unit, split, nsplit, lds, tmp, misc);
+}
+
+// ---- the same-step layer in one launch ------------------------------------
+// Scoring, selection and attention of a same-step call in one launch, for
+// the head-halves form at U and grid multiples of 8.  The first nS
+// workgroups (one per CU, dispatched first) score with XCD-affine ranges
+// (xcd_slot0): the units of XCD x are complete as soon as its ranges are.
+// The XCDs stream at different rates, so the units of the faster ones select
+// and attend while the slower ones still score, and no unit waits for a
+// launch boundary.  The 2U workgroups after them are k_select_attn's head
+// halves, placed by the same index map on the XCD that scored their unit.
+// Each waits for the hand-over flags of its unit's slots (FusedSync), then
+// reads the scores and slots with device-coherent loads, so nothing rests on
+// where the workgroups run.  Only higher-indexed workgroups wait, and only
+// for lower-indexed ones that never wait.  The wait is bounded all the same
+// (kFusedSpinLimit polls): a broken hand-over leaves the outputs undefined
+// but cannot hang the launch.
+constexpr uint32_t kFusedSpinLimit = 1u << 20;
+template <int G>
+__global__ __launch_bounds__(kFinishThreads) void k_critical(ScoreArgs sc, SelectArgs sa,
+                                                             AttnArgs at, FusedSync fs, int nS) {
+  using Lds = SelAttnLds<G / 2>;
+  static_assert(kHistBins + kHistScoreWaves * (kStageDwords + kFlushGroups * kStageRows) <=
+                    Lds::kDwords,
+                "the scoring role's histogram, stages and score buffers fit");
+  __shared__ __attribute__((aligned(16))) uint32_t lds[Lds::kDwords];
+  __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
+  __shared__ uint32_t misc[8];
+  if ((int)blockIdx.x < nS) {
+    score_range<G, true, kHistScoreWaves, false, true>(sc, blockIdx.x, nS, lds,
+                                                       lds + kHistBins, fs);
+    return;
+  }
+  int unit, half;
+  split_block(blockIdx.x - nS, 2, &unit, &half);
+  if (unit >= sa.units) return;  // uniform over the workgroup
+  int nslots;
+  const int64_t s0 = xcd_slot0(unit, sa.units, sa.score_nwg,
+                               (sa.max_ctx + kStageRows - 1) / kStageRows, &nslots);
+  if ((int)threadIdx.x < nslots) {
+    uint64_t* f = fs.flags + 2 * (s0 + threadIdx.x) + half;
+    for (uint32_t spin = 0;
+         __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != fs.tag &&
+         spin < kFusedSpinLimit;
+         ++spin)
+      __builtin_amdgcn_s_sleep(2);
+    __hip_atomic_store(f, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  select_attn_part<G, 2, true>(sa, at, unit, half, 1, lds, tmp, misc);
 }
 
 // Same-step over chunks (Sec. 2.2): sa is the chunk problem (one landmark
@@ -1730,6 +1801,35 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
     }
   }
 #undef CKV_SA
+  return launch_status();
+}
+
+template <int G>
+static const void* critical_kernel() {
+  return (const void*)k_critical<G>;
+}
+
+int critical_blocks(int G, int units, int nwg) {
+  if (units < 8 || units % 8 || nwg < 8 || nwg % 8) return 0;
+  const void* fn = G == 2 ? critical_kernel<2>() : G == 4 ? critical_kernel<4>()
+                 : G == 8 ? critical_kernel<8>() : nullptr;
+  // every scoring workgroup resident at once, so that none waits for a
+  // workgroup that waits for it
+  if (!fn || nwg > resident_blocks(fn, kFinishThreads)) return 0;
+  return nwg + 2 * units;
+}
+
+hipError_t launch_critical(const ScoreArgs& sc, const SelectArgs& sa, const AttnArgs& at,
+                           const FusedSync& fs, int G, int nwg, hipStream_t s) {
+  const int blocks = critical_blocks(G, sa.units, nwg);
+  if (!blocks || !sa.affine || sa.score_nwg != nwg || !sc.hist_part) return hipErrorInvalidValue;
+  const dim3 grid(blocks), block(kFinishThreads);
+  switch (G) {
+    case 2: launch_kernel(CKV_K_CRITICAL, k_critical<2>, grid, block, s, sc, sa, at, fs, nwg); break;
+    case 4: launch_kernel(CKV_K_CRITICAL, k_critical<4>, grid, block, s, sc, sa, at, fs, nwg); break;
+    case 8: launch_kernel(CKV_K_CRITICAL, k_critical<8>, grid, block, s, sc, sa, at, fs, nwg); break;
+    default: return hipErrorInvalidValue;
+  }
   return launch_status();
 }
 

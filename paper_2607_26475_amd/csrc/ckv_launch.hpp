@@ -70,6 +70,14 @@ hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStr
 // the heads each over the whole set, outputs written directly
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
                               int heads, hipStream_t s);
+// the same-step layer in one launch (k_critical): scoring on nwg workgroups
+// with XCD-affine ranges and slots (sa.affine set, sa.score_nwg = nwg), then
+// the head-halves selection and attention; 0 workgroups when the launch does
+// not apply (G odd or above 8, U or nwg not multiples of 8, or more scoring
+// workgroups than fit on the device at once).
+int critical_blocks(int G, int units, int nwg);
+hipError_t launch_critical(const ScoreArgs& sc, const SelectArgs& sa, const AttnArgs& at,
+                           const FusedSync& fs, int G, int nwg, hipStream_t s);
 // the same over chunks (sa: the chunk problem, k / chunk <= kFinishThreads;
 // e: the rows written as k_expand writes them; G even, k <= kSelAttnMaxShare)
 hipError_t launch_select_attn_chunks(const SelectArgs& sa, const AttnArgs& at,

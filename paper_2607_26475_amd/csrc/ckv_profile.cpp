@@ -96,7 +96,7 @@ const char* ckv_kernel_name(int id) {
   static const char* names[CKV_K_COUNT] = {"zero", "score", "hist", "filter", "finish",
                                            "attn", "combine", "dual", "gather", "miss",
                                            "landmarks", "expand", "reconstruct",
-                                           "select_attn", "probe"};
+                                           "select_attn", "probe", "critical"};
   return (id >= 0 && id < CKV_K_COUNT) ? names[id] : "";
 }
 

@@ -59,6 +59,34 @@ __device__ __forceinline__ void store_zero_hist(uint32_t* slot) {
     *reinterpret_cast<uint4*>(slot + i) = make_uint4(0u, 0u, 0u, 0u);
 }
 
+// The workgroup's LDS histogram (or zeros, lds_hist null) as its slot,
+// device-coherent, 8 bytes per lane with consecutive lanes on consecutive
+// words (NT threads).
+template <int NT>
+__device__ __forceinline__ void store_hist_coherent(const uint32_t* lds_hist, uint32_t* slot) {
+  constexpr int kPairs = kHistBins / NT / 2;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < kPairs; ++q) {
+    const int i = 2 * (t + NT * q);
+    const uint64_t w = lds_hist ? ((uint64_t)lds_hist[i] | ((uint64_t)lds_hist[i + 1] << 32))
+                                : 0ull;
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(slot + i), w, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// After a fused scoring workgroup's stores of a (unit, slot): every thread
+// waits for its own stores, the barrier then covers the workgroup's, and the
+// slot's two flags take the launch's tag.
+__device__ __forceinline__ void hand_over(const FusedSync& fs, int64_t slot) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x < 2)
+    __hip_atomic_store(fs.flags + 2 * slot + threadIdx.x, fs.tag, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Scores of one staged group (kStageRows keys of one unit starting at row
 // jb) into out[0, kStageRows): the MFMA products with the G query rows, the
 // maximum over the heads, the scale; rows at or past n get -inf and are not
@@ -149,25 +177,40 @@ __device__ __forceinline__ void load_query(const ScoreArgs& a, int unit, bf16x8*
 // attention's random row reads: 186-188 against 189-192 us per Llama-8B
 // layer, alternated over two sessions.  The 8-wave histogram pass is slower with it (167-170 against
 // 158-165 us), as it is with 16-row groups.
-template <int G, bool HIST, int NW = 4, bool HALVES = false>
+//
+// FUSED (the scoring role of the one-launch same-step kernel, HIST with
+// per-workgroup slots): the ranges are XCD-affine (xcd_slot0); the workgroup
+// may have more than NW waves, the others only join its barriers; scores and
+// slots are stored device-coherent, 8 bytes per lane over whole lines, and
+// each finished (unit, slot) is handed over through fs (FusedSync).
+template <int G, bool HIST, int NW = 4, bool HALVES = false, bool FUSED = false>
 __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
                                             uint32_t* lds_hist,
-                                            uint32_t* lds_stage) {
+                                            uint32_t* lds_stage, FusedSync fs = FusedSync{}) {
+  static_assert(!FUSED || (HIST && !HALVES), "the fused scoring role counts histograms");
   constexpr int NT = 64 * NW;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int lrow = lane >> 4, lchunk = lane & 15;
+  const bool active = !FUSED || wave < NW;  // uniform over the wave
   constexpr int kLoads = kStageRows / 4;  // 4 rows per load instruction
   const int64_t gpu_groups = (a.max_ctx + kStageRows - 1) / kStageRows;  // per unit
-  const int64_t total = (int64_t)a.units * gpu_groups;
-  const int64_t g0 = total * wg / nwg, g1 = total * (wg + 1) / nwg;
-  uint32_t* stage = lds_stage + wave * kStageDwords;
+  // FUSED: XCD x = wg % 8 scores units x, x + 8, ... with its nwg / 8 workgroups
+  const int xcd = FUSED ? (wg & 7) : 0;
+  const int wr = FUSED ? (wg >> 3) : wg, nwr = FUSED ? (nwg >> 3) : nwg;
+  const int64_t units_r = FUSED ? (a.units >> 3) : a.units;
+  const int64_t total = units_r * gpu_groups;
+  const int64_t g0 = total * wr / nwr, g1 = total * (wr + 1) / nwr;
+  uint32_t* stage = lds_stage + (active ? wave : 0) * kStageDwords;
   float* sbuf = reinterpret_cast<float*>(lds_stage + NW * kStageDwords) +
-                wave * kFlushGroups * kStageRows;
+                (active ? wave : 0) * kFlushGroups * kStageRows;
 
   for (int64_t seg = g0; seg < g1;) {
-    const int unit = (int)(seg / gpu_groups);
-    const int64_t ubase = (int64_t)unit * gpu_groups;
+    const int vunit = (int)(seg / gpu_groups);
+    const int unit = FUSED ? 8 * vunit + xcd : vunit;
+    const int64_t slot = FUSED ? (int64_t)xcd * (units_r + nwr) + vunit + wr
+                               : (int64_t)unit + wg;
+    const int64_t ubase = (int64_t)vunit * gpu_groups;
     const int64_t seg_end = min(g1, ubase + gpu_groups);
     const int n = unit_len(a.ctx_lens[unit / a.Hkv], a.max_ctx, a.chunk);
     float* srow = a.scores + (int64_t)unit * a.max_ctx;
@@ -179,7 +222,8 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
     }
     if (seg < valid_end) {  // uniform over the workgroup
       if (HIST) {
-        for (int i = tid; i < kHistBins; i += NT) lds_hist[i] = 0u;
+        if (!FUSED || tid < NT)
+          for (int i = tid; i < kHistBins; i += NT) lds_hist[i] = 0u;
         __syncthreads();
       }
       bf16x8 qa[4];
@@ -204,7 +248,26 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
         __builtin_amdgcn_wave_barrier();
         const int jb = (int)(first - ubase) * kStageRows;
         const int count = nb * kStageRows;
-        if ((a.max_ctx & 3) == 0) {
+        if constexpr (FUSED) {
+          // 8 bytes per lane, consecutive lanes on consecutive pairs: each
+          // instruction covers whole 128-byte lines of four groups
+          for (int c = 2 * lane; c < count; c += 128) {
+            const int j = jb + (c / kStageRows) * NW * kStageRows + c % kStageRows;
+            const float2 v = *reinterpret_cast<const float2*>(sbuf + c);
+            if ((a.max_ctx & 1) == 0 && j + 1 < a.max_ctx) {
+              const uint64_t w = (uint64_t)__float_as_uint(v.x) |
+                                 ((uint64_t)__float_as_uint(v.y) << 32);
+              __hip_atomic_store(reinterpret_cast<uint64_t*>(srow + j), w, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+              if (j < a.max_ctx)
+                __hip_atomic_store(srow + j, v.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              if (j + 1 < a.max_ctx)
+                __hip_atomic_store(srow + j + 1, v.y, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            }
+          }
+        } else if ((a.max_ctx & 3) == 0) {
           for (int c = 4 * lane; c < count; c += 256) {
             const float4 v = *reinterpret_cast<const float4*>(sbuf + c);
             const int j = jb + (c / kStageRows) * NW * kStageRows + c % kStageRows;
@@ -224,8 +287,9 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
         }
         __builtin_amdgcn_wave_barrier();
       };
-      // this wave's groups of the segment below n_b: every fourth one
-      const int64_t w0 = seg + wave, w1 = valid_end;
+      // this wave's groups of the segment below n_b: every NW-th one (none
+      // for the waves past NW of the fused role)
+      const int64_t w1 = valid_end, w0 = active ? seg + wave : w1;
       uint4 cur[kLoads], nxt[kLoads];
       int64_t gg = w0;
       int64_t first = gg;
@@ -258,15 +322,24 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
       if (nb) flush(first, nb);
       if (HIST) {
         __syncthreads();
-        if (a.hist_part)
-          store_hist<NT>(lds_hist, a.hist_part + ((int64_t)unit + wg) * kHistBins);
-        else
+        if constexpr (FUSED) {
+          if (tid < NT) store_hist_coherent<NT>(lds_hist, a.hist_part + slot * kHistBins);
+        } else if (a.hist_part) {
+          store_hist<NT>(lds_hist, a.hist_part + slot * kHistBins);
+        } else {
           flush_hist<NT>(lds_hist, a.hist + (int64_t)unit * kHistBins,
                          a.coarse + (int64_t)unit * kCoarseBins);
-        __syncthreads();
+        }
+        if constexpr (FUSED) hand_over(fs, slot);
+        else __syncthreads();
       }
     } else if (HIST && a.hist_part) {  // the unit's histogram sums this slot too
-      store_zero_hist<NT>(a.hist_part + ((int64_t)unit + wg) * kHistBins);
+      if constexpr (FUSED) {
+        if (tid < NT) store_hist_coherent<NT>(nullptr, a.hist_part + slot * kHistBins);
+        hand_over(fs, slot);
+      } else {
+        store_zero_hist<NT>(a.hist_part + slot * kHistBins);
+      }
     }
     seg = seg_end;
   }

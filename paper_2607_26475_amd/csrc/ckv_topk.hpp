@@ -74,7 +74,7 @@ __device__ __forceinline__ void walk_first_bin(const uint32_t* stage, uint32_t c
 // kMaxPartials) consecutive slots of kHistBins counts.  Every thread loads
 // its kHistBins / NT consecutive bins of every slot at once (one round trip;
 // slots past nslots repeat slot 0 and are not added) ...
-template <int NT = kFinishThreads>
+template <int NT = kFinishThreads, bool COH = false>
 __device__ __forceinline__ void load_hist_slots(const uint32_t* hist, int nslots,
                                                 uint2 (&v)[kMaxPartials][kHistBins / NT / 2]) {
   constexpr int kPairs = kHistBins / NT / 2;
@@ -83,9 +83,17 @@ __device__ __forceinline__ void load_hist_slots(const uint32_t* hist, int nslots
 #pragma unroll
   for (int p = 0; p < kMaxPartials; ++p)
 #pragma unroll
-    for (int q = 0; q < kPairs; ++q)
-      v[p][q] = *reinterpret_cast<const uint2*>(
-          hist + (int64_t)(p < nslots ? p : 0) * kHistBins + 2 * (kPairs * t + q));
+    for (int q = 0; q < kPairs; ++q) {
+      const uint32_t* src =
+          hist + (int64_t)(p < nslots ? p : 0) * kHistBins + 2 * (kPairs * t + q);
+      if constexpr (COH) {  // stored by other workgroups of the same launch
+        const uint64_t w = __hip_atomic_load(reinterpret_cast<const uint64_t*>(src),
+                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        v[p][q] = make_uint2((uint32_t)w, (uint32_t)(w >> 32));
+      } else {
+        v[p][q] = *reinterpret_cast<const uint2*>(src);
+      }
+    }
 }
 
 // ... and stores the sums to lhist (LDS); the caller synchronises before
