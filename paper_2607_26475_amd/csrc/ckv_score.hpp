@@ -76,14 +76,14 @@ __device__ __forceinline__ void store_hist_coherent(const uint32_t* lds_hist, ui
   }
 }
 
-// After a fused scoring workgroup's stores of a (unit, slot): every thread
-// waits for its own stores, the barrier then covers the workgroup's, and the
-// slot's two flags take the launch's tag.
-__device__ __forceinline__ void hand_over(const FusedSync& fs, int64_t slot) {
+// After a fused scoring workgroup's stores of the consecutive slots [slot0,
+// slot0 + count): every thread waits for its own stores, the barrier then
+// covers the workgroup's, and each slot's two flags take the launch's tag.
+__device__ __forceinline__ void hand_over(const FusedSync& fs, int64_t slot0, int count) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if (threadIdx.x < 2)
-    __hip_atomic_store(fs.flags + 2 * slot + threadIdx.x, fs.tag, __ATOMIC_RELAXED,
+  for (int t = threadIdx.x; t < 2 * count; t += blockDim.x)
+    __hip_atomic_store(fs.flags + 2 * slot0 + t, fs.tag, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -208,8 +208,7 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
   for (int64_t seg = g0; seg < g1;) {
     const int vunit = (int)(seg / gpu_groups);
     const int unit = FUSED ? 8 * vunit + xcd : vunit;
-    const int64_t slot = FUSED ? (int64_t)xcd * (units_r + nwr) + vunit + wr
-                               : (int64_t)unit + wg;
+    const int64_t slot = FUSED ? xcd * (units_r + nwr) + vunit + wr : (int64_t)unit + wg;
     const int64_t ubase = (int64_t)vunit * gpu_groups;
     const int64_t seg_end = min(g1, ubase + gpu_groups);
     const int n = unit_len(a.ctx_lens[unit / a.Hkv], a.max_ctx, a.chunk);
@@ -330,18 +329,24 @@ __device__ __forceinline__ void score_range(const ScoreArgs& a, int wg, int nwg,
           flush_hist<NT>(lds_hist, a.hist + (int64_t)unit * kHistBins,
                          a.coarse + (int64_t)unit * kCoarseBins);
         }
-        if constexpr (FUSED) hand_over(fs, slot);
-        else __syncthreads();
+        __syncthreads();
       }
     } else if (HIST && a.hist_part) {  // the unit's histogram sums this slot too
       if constexpr (FUSED) {
         if (tid < NT) store_hist_coherent<NT>(nullptr, a.hist_part + slot * kHistBins);
-        hand_over(fs, slot);
       } else {
         store_zero_hist<NT>(a.hist_part + slot * kHistBins);
       }
     }
     seg = seg_end;
+  }
+  if constexpr (FUSED) {
+    // every slot of the range handed over at its end, after one wait for all
+    // its stores (a wait between units would stall the key stream)
+    if (g0 < g1) {
+      const int v0 = (int)(g0 / gpu_groups), v1 = (int)((g1 - 1) / gpu_groups);
+      hand_over(fs, xcd * (units_r + nwr) + v0 + wr, v1 - v0 + 1);
+    }
   }
 }
 
