@@ -2,13 +2,16 @@
 per-device scratch) against ckv_critical_kv_attn with a caller workspace, on
 the same inputs (MI355X only).
 
-Two calls in a row go through the fixed scratch, the second on a smaller
-shape, so the second finds the first call's contents in the scratch; a
-third call runs the pipelined form (rows read in place) on a third shape.
+Calls in a row go through the fixed scratch: a batch whose same-step layer
+runs as one launch (its hand-over flags in the scratch) twice, then two
+smaller shapes, each finding the previous call's contents in the scratch;
+a last call runs the pipelined form (rows read in place) on another shape.
 Both entries run the same kernels, so index sets, counts and outputs must be
 bit-identical.  A shape whose workspace exceeds the scratch is refused.
 """
 from __future__ import annotations
+
+import dataclasses
 
 import numpy as np
 import pytest
@@ -37,8 +40,13 @@ def _same(a, b, what):
         assert torch.equal(x, y), (what, name)
 
 
+# 40 units: the same-step call runs as one launch, its hand-over flags in the scratch
+ONE_LAUNCH = dataclasses.replace(synth.WORKLOADS["llama8b_s"], name="u40", batch=5, max_ctx=5000,
+                                 ctx_min=3000, k=1024)
+
+
 def _same_step_pair(wl, seed, dev):
-    w = synth.WORKLOADS[wl]
+    w = wl if isinstance(wl, synth.Workload) else synth.WORKLOADS[wl]
     t = synth.make_layer(w, seed=seed, device=dev)
     s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
     assert ckv.workspace_bytes(s, w.k, ckv.ENTRY_CRITICAL_KV_ATTN) <= ckv.NOALLOC_SCRATCH_BYTES
@@ -46,18 +54,24 @@ def _same_step_pair(wl, seed, dev):
     ref, got = _outputs(w, dev), _outputs(w, dev)
     ckv.critical_kv_attn(s, t["q"], t["q_sel"], t["k"], t["ctx_lens"], w.k, SCALE, t["k"],
                          t["v"], ckv.SRC_DEVICE, None, None, None, *ref, ws)
+    ckv.profile_begin()
     ckv.critical_kv_attn_noalloc(s, t["q"], t["q_sel"], t["k"], t["ctx_lens"], w.k, SCALE,
                                  t["k"], t["v"], ckv.SRC_DEVICE, None, None, None, *got)
+    kernels = ckv.profile_end()
     torch.cuda.synchronize()
     assert torch.isfinite(got[2]).all()
-    _same(ref, got, wl)
+    _same(ref, got, w.name)
+    assert ("critical" in kernels) == (w is ONE_LAUNCH), kernels
     return w, t, got
 
 
 def test_noalloc_matches_workspace_entry():
     dev = device()
-    # 1. a larger shape, then 2. a smaller one on the same (now stale) scratch
-    _log("no-alloc: same-step llama8b_s, then tiny")
+    # 1. the layer in one launch (hand-over flags in the scratch), twice, then
+    # 2. a smaller shape and 3. a smaller one again on the same (now stale) scratch
+    _log("no-alloc: same-step u40 (one launch) twice, llama8b_s, then tiny")
+    _same_step_pair(ONE_LAUNCH, 20, dev)
+    _same_step_pair(ONE_LAUNCH, 19, dev)
     _same_step_pair("llama8b_s", 21, dev)
     _same_step_pair("tiny", 22, dev)
     # 3. the pipelined form over rows read in place, selected one step earlier
