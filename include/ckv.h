@@ -173,6 +173,8 @@ int ckv_sparse_decode_attn(const ckv_shape* shape, const uint16_t* q_att,
  *   Same-step mode (idx_in == NULL, k_buf == NULL): out = attention of q_att
  *     over the rows idx_out of k_src / v_src (read in place, src_kind says
  *     where), i.e. ckv_sparse_decode_attn applied to ckv_gather_kv(idx_out).
+ *     Where it applies, the scoring, the selection and the attention run as
+ *     one launch (see ckv_set_one_launch_same_step), with the same results.
  *   Pipelined modes (Sec. 4.1: the set attended at step t was selected at
  *   step t-1 from the speculative token's query): out = attention of q_att
  *   over the set selected one step earlier, and in the same launch the
