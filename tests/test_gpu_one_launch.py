@@ -167,3 +167,22 @@ def test_one_launch_graph_replays():
         eager = _call(w, t, lens, ws, False, True)
         for a, b in zip(eager[:3], ref[:3]):
             assert torch.equal(a, b), rep
+
+
+def test_one_launch_full_size_repeated():
+    """Four Llama-8B layers (B16, 32 q / 8 KV heads, n 32768, k 2048) called
+    in turn 25 times through one workspace: every call bit-identical to the
+    two-launch form of the same layer."""
+    dev = device()
+    w = dataclasses.replace(synth.WORKLOADS["llama8b"], layers=4)
+    s = ckv.shape_for(w.batch, w.q_heads, w.kv_heads, w.max_ctx)
+    ws = ckv.workspace(s, w.k, ckv.ENTRY_CRITICAL_KV_ATTN)
+    layers = [synth.make_layer(w, seed=0, layer=l, device=dev) for l in range(w.layers)]
+    ref = [_call(w, t, t["ctx_lens"], ws, False, False)[:3] for t in layers]
+    for it in range(25):
+        for l, t in enumerate(layers):
+            got = _call(w, t, t["ctx_lens"], ws, False, True)
+            assert set(got[3]) == {"critical"}, got[3]
+            for a, b in zip(got[:3], ref[l]):
+                assert torch.equal(a, b), (it, l)
+    print("  100 one-launch calls bit-identical to the two-launch form", flush=True)
