@@ -275,14 +275,15 @@ def main() -> int:
     return 0
 
 
-def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_every=8):
+def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_every=31):
     """The headline: the Llama-8B same-step decode step, K steps timed by
     events on the compute stream (one more event after each step gives the
     per-step times and their median).  Inside the timed steps one launch in
     `stamp_every` of the dominant kernel carries dispatch-stamped events: its
     average duration there gives the roofline.  A stamped dispatch costs a few
-    microseconds more than a plain one, so only a sample is stamped; the same
-    steps are timed once more with no stamp at all."""
+    microseconds more than a plain one, so only a sample is stamped (one launch
+    in 31: prime to the 32 layers, so the stamps move through all of them);
+    the same steps are timed once more with no stamp at all."""
     B, Hq, Hkv, d, n, k, L = (w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx, w.k,
                               w.layers)
     dev = torch.device("cuda:0")
@@ -329,7 +330,8 @@ def measure_main(torch, ckv, layers, kv_ptrs, s, w, scale, args, stream, stamp_e
     dstats = ckv.profile_end()
     ms_plain, _ = timed(args.steps)  # same steps with no stamps at all (overhead check)
     # the same steps with the scoring launch and the selection and attention
-    # launch apart (the two-launch form of the same results), for comparison
+    # launch apart (the two-launch form: the same index sets, the outputs
+    # within fp32 rounding), for comparison
     ckv.set_one_launch_same_step(False)
     try:
         ms_two, _ = timed(args.steps)

@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define CKV_ABI_VERSION 8
+#define CKV_ABI_VERSION 9
 
 typedef enum ckv_status {
   CKV_OK = 0,
@@ -573,11 +573,22 @@ int ckv_set_debug(int on);
  * and attention then start as soon as that unit's scores are complete (Sec. 2.2
  * selection inside the step, with the attention of Sec. 5.3-5.4), not after
  * the whole scoring pass.  The launch hands each unit's scores over through
- * flags in the workspace, which are zero again when it ends.  Otherwise, or
- * with this setting off, the call runs the scoring launch, then the
- * selection and attention launch.  Both forms give the same bits.  The
- * setting (on: nonzero; process-wide; on by default) is for comparing the
- * two; calls already launched keep their form. */
+ * flags in the workspace, which are zero again when it ends.  Each of a
+ * unit's two workgroups selects the unit's set; by default each then attends
+ * over half of the set's rows with all of the group's heads, and the second
+ * merges the first's partial (handed over through a per-unit flag) into the
+ * output.  Otherwise, or with this setting off, the call runs the scoring
+ * launch, then the selection and attention launch, whose two workgroups per
+ * unit attend over the whole set with half the heads each.
+ *   on = CKV_ONE_LAUNCH_OFF: two launches.
+ *   on = CKV_ONE_LAUNCH_HEAD_HALVES: one launch with that head-halves
+ *        attention; the same bits as two launches.
+ *   any other value: one launch with row halves (the default).  The index
+ *        sets and counts are those of the other forms bit for bit; the
+ *        outputs add the same terms in another order (fp32 rounding only).
+ * The setting is process-wide and for comparing the forms; calls already
+ * launched keep their form. */
+enum { CKV_ONE_LAUNCH_OFF = 0, CKV_ONE_LAUNCH_ROW_HALVES = 1, CKV_ONE_LAUNCH_HEAD_HALVES = 2 };
 int ckv_set_one_launch_same_step(int on);
 
 /* ---- read-rate probe -------------------------------------------------------

@@ -28,7 +28,8 @@ __all__ = [
     "SRC_DEVICE", "SRC_HOST_PINNED", "ENTRY_SELECT_TOPK",
     "ENTRY_SPARSE_DECODE_ATTN", "ENTRY_CRITICAL_KV_ATTN", "ENTRY_CORRECTED_ATTN", "ENTRY_DUAL_TOKEN_ATTN", "ENTRY_DECODE_STEP",
     "EXPORTS", "probe_read_rows", "probe_sink_words", "PROBE_STANDALONE", "PROBE_ROW_HALVES",
-    "PROBE_HEAD_HALVES", "set_debug", "set_one_launch_same_step",
+    "PROBE_HEAD_HALVES", "set_debug", "set_one_launch_same_step", "ONE_LAUNCH_OFF",
+    "ONE_LAUNCH_ROW_HALVES", "ONE_LAUNCH_HEAD_HALVES",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libckv.so")
@@ -53,7 +54,7 @@ EXPORTS = ("ckv_abi_version", "ckv_status_str", "ckv_last_error_detail",
            "ckv_set_one_launch_same_step")
 KERNEL_COUNT = 16
 MAX_RANK = 4096
-ABI_VERSION = 8  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
+ABI_VERSION = 9  # CKV_ABI_VERSION of include/ckv.h that this binding marshals for
 
 
 class CkvError(RuntimeError):
@@ -364,11 +365,18 @@ def set_debug(on: bool) -> None:
     _check("ckv_set_debug", _lib.ckv_set_debug(1 if on else 0))
 
 
-def set_one_launch_same_step(on: bool) -> None:
+ONE_LAUNCH_OFF, ONE_LAUNCH_ROW_HALVES, ONE_LAUNCH_HEAD_HALVES = 0, 1, 2
+
+
+def set_one_launch_same_step(on) -> None:
     """Whether same-step calls run as one launch where that form applies
-    (process-wide, on by default); off, as the scoring launch then the
-    selection and attention launch.  Both forms give the same bits."""
-    _check("ckv_set_one_launch_same_step", _lib.ckv_set_one_launch_same_step(1 if on else 0))
+    (process-wide).  False / ONE_LAUNCH_OFF: the scoring launch, then the
+    selection and attention launch with head halves.  ONE_LAUNCH_HEAD_HALVES:
+    one launch with that attention, the same bits as two launches.  True /
+    ONE_LAUNCH_ROW_HALVES (the default): one launch whose two workgroups per
+    unit attend over half the rows each and merge in the launch; the same
+    index sets, outputs within fp32 rounding of the other forms."""
+    _check("ckv_set_one_launch_same_step", _lib.ckv_set_one_launch_same_step(int(on)))
 
 
 def probe_sink_words(shape: Shape, k: int, mode: int) -> int:

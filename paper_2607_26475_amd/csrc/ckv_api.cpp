@@ -95,7 +95,7 @@ struct Dims {
 };
 
 // ckv_set_one_launch_same_step
-std::atomic<int> g_one_launch{1};
+std::atomic<int> g_one_launch{CKV_ONE_LAUNCH_ROW_HALVES};
 
 // A tag for one launch of the one-launch same-step kernel: a 32-bit value
 // that is never zero in the high half and its complement in the low half.
@@ -187,6 +187,7 @@ struct Layout {
   size_t chunk_idx = 0, n_chunks = 0;  // decode step: selected chunks of a chunked layer
   size_t scores_b = 0, hist_part_b = 0;  // decode step: the second scores and slots region
   size_t flags = 0;  // the same-step layer in one launch: hand-over flags per slot
+  size_t merge = 0;  // and its row halves' merge flags per unit
   int64_t bm_words = 0;
   int chunks = 0, filter_tiles = 0;
 };
@@ -241,9 +242,11 @@ Layout make_layout(const Dims& d, int32_t k, int entry) {
     L.hist_part = off;
     L.hist_part_bytes = (U + (size_t)std::min<int64_t>(groups, kMaxScoreWgs)) * kHistBins * 4;
     off = align256(off + L.hist_part_bytes);
-    if (entry == CKV_ENTRY_CRITICAL_KV_ATTN) {  // two 64-bit flags per slot
+    if (entry == CKV_ENTRY_CRITICAL_KV_ATTN) {  // two 64-bit flags per slot, one per unit
       L.flags = off;
       off = align256(off + (U + (size_t)std::min<int64_t>(groups, kMaxScoreWgs)) * 16);
+      L.merge = off;
+      off = align256(off + U * 8);
     }
   }
   if (attn) {
@@ -1033,12 +1036,15 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
                              d.kv_stride, k, scale, out);
     int heads;
     const int S = select_attn_splits(d, k, L, &heads);
-    if (S == 1 && heads == 2 && partials && L.flags && g_one_launch.load() &&
-        critical_blocks(d.G, d.U, nwg)) {
+    const int one = g_one_launch.load();
+    // row halves need a partial per half in the attention partials
+    const bool rows = one == CKV_ONE_LAUNCH_ROW_HALVES && L.chunks >= 2;
+    if (S == 1 && heads == 2 && partials && L.flags && one &&
+        critical_blocks(d.G, d.U, nwg, rows)) {
       // scoring, selection and attention in one launch, XCD-affine slots
       sa.affine = 1;
-      const FusedSync fs{at<uint64_t>(ws, L.flags), next_fused_tag()};
-      CKV_TRY_HIP(launch_critical(sc, sa, at_, fs, d.G, nwg, s), "same-step launch");
+      const FusedSync fs{at<uint64_t>(ws, L.flags), at<uint64_t>(ws, L.merge), next_fused_tag()};
+      CKV_TRY_HIP(launch_critical(sc, sa, at_, fs, d.G, nwg, rows, s), "same-step launch");
       return CKV_OK;
     }
     CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
@@ -1059,7 +1065,9 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
 extern "C" {
 
 int ckv_set_one_launch_same_step(int on) {
-  g_one_launch.store(on ? 1 : 0);
+  g_one_launch.store(on == CKV_ONE_LAUNCH_HEAD_HALVES ? CKV_ONE_LAUNCH_HEAD_HALVES
+                     : on                             ? CKV_ONE_LAUNCH_ROW_HALVES
+                                                      : CKV_ONE_LAUNCH_OFF);
   return CKV_OK;
 }
 

@@ -332,13 +332,19 @@ struct LdsRows {
 // for a KV head's whole group).  With nloc > 0 (nsplit 1 only) the heads also
 // see the nloc rows k_loc / v_loc ([nloc][d] bf16) beside the share's rows:
 // the token's own rows in dual-token decoding (Sec. 5.2), which join the
-// final merge as one more partial per head.
-template <int G, class Rows>
+// final merge as one more partial per head.  MERGE2 (nsplit 2, no local
+// rows): the two shares' workgroups merge in the launch instead of k_combine.
+// Share 0 stores its partial with device-coherent stores and, once they have
+// completed, sets *mflag to tag; share 1 waits for the flag (bounded), clears
+// it, and merges both partials into the output in k_combine's order of
+// operations, so the outputs equal those of the two-launch form bit for bit.
+template <int G, class Rows, bool MERGE2 = false>
 __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, int nrows,
                                         int split, int nsplit, uint32_t* stages,
                                         uint32_t* qlds, int qh0,
                                         const uint16_t* k_loc = nullptr,
-                                        const uint16_t* v_loc = nullptr, int nloc = 0) {
+                                        const uint16_t* v_loc = nullptr, int nloc = 0,
+                                        uint64_t* mflag = nullptr, uint64_t tag = 0) {
   using Lds = WgAttnLds<G>;
   static_assert(G <= 8, "16 waves' states of at most 8 heads fit in the stages");
   constexpr int kW = kFinishThreads / 64;
@@ -504,6 +510,7 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
     if (lane == 0) loc[g * 2 + j] = dot * a.scale;
   }
   __syncthreads();
+  float mine[3];  // MERGE2, share 1: this thread's (M, L, O)
   for (int oi = tid; oi < G * kD; oi += kFinishThreads) {
     const int g = oi / kD, c = oi - g * kD;
     float M = -INFINITY;
@@ -523,7 +530,20 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
       O = fmaf(wt, __uint_as_float((uint32_t)v_loc[j * kD + c] << 16), O);
       L += wt;
     }
-    if (nsplit == 1) {
+    if constexpr (MERGE2) {
+      float* part = a.part + (((int64_t)unit * 2) * G + g) * kPartStride;  // share 0's
+      if (split == 0) {
+        __hip_atomic_store(part + 4 + c, O, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (c == 0) {
+          __hip_atomic_store(part, M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(part + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      } else {
+        mine[0] = M;
+        mine[1] = L;
+        mine[2] = O;
+      }
+    } else if (nsplit == 1) {
       a.out[((int64_t)b * a.Hq + qh0 + g) * kD + c] = L > 0.f ? O / L : 0.f;
     } else {
       float* part = a.part + (((int64_t)unit * nsplit + split) * G + g) * kPartStride;
@@ -532,6 +552,46 @@ __device__ __forceinline__ void attn_wg(const AttnArgs& a, int unit, Rows pos, i
         part[0] = M;
         part[1] = L;
       }
+    }
+  }
+  if constexpr (MERGE2) {
+    static_assert(G * kD <= kFinishThreads, "one output per thread");
+    if (split == 0) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (tid == 0) __hip_atomic_store(mflag, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    if (tid == 0) {
+      for (uint32_t spin = 0;
+           __hip_atomic_load(mflag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != tag &&
+           spin < kFusedSpinLimit;
+           ++spin)
+        __builtin_amdgcn_s_sleep(2);
+      __hip_atomic_store(mflag, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (tid < G * kD) {
+      const int g = tid / kD, c = tid - g * kD;
+      const float* p0 = a.part + (((int64_t)unit * 2) * G + g) * kPartStride;
+      const float m0 = __hip_atomic_load(p0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float l0 = __hip_atomic_load(p0 + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float o0 = __hip_atomic_load(p0 + 4 + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // k_combine with two chunks and no local rows, step by step
+      float M = fmaxf(-INFINITY, -INFINITY);
+      M = fmaxf(M, m0);
+      M = fmaxf(M, mine[0]);
+      const float w0 = m0 == -INFINITY ? 0.f : __expf(m0 - M);
+      float L = fmaf(w0, l0, 0.f);
+      const float w1 = mine[0] == -INFINITY ? 0.f : __expf(mine[0] - M);
+      L = fmaf(w1, mine[1], L);
+      L += 0.f;
+      L += 0.f;
+      const float inv = L > 0.f ? 1.f / L : 0.f;
+      float O = 0.f;
+      O = fmaf(w0, o0, O);
+      O = fmaf(w1, mine[2], O);
+      a.out[((int64_t)b * a.Hq + qh0 + g) * kD + c] = O * inv;
     }
   }
 }

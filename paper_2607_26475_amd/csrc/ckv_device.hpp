@@ -126,11 +126,17 @@ struct SelectArgs {
 // each of the unit's two attending workgroups, to the launch's tag; each of
 // those waits for its flags of all the unit's slots and then clears them, so
 // that they are zero again after the launch.  The tag's halves are each
-// other's complement, so no stale word and no zero matches it.
+// other's complement, so no stale word and no zero matches it.  With row
+// halves the unit's first workgroup hands its attention partial to the
+// second the same way, through the unit's merge flag.
 struct FusedSync {
   uint64_t* flags;  // [U + kMaxScoreWgs][2]
+  uint64_t* merge;  // [U], row halves only
   uint64_t tag;
 };
+// Every wait on these flags gives up after this many polls (about a second):
+// a broken hand-over leaves outputs undefined but cannot hang a launch.
+constexpr uint32_t kFusedSpinLimit = 1u << 20;
 
 struct AttnArgs {
   const uint16_t* q;        // [B][Hq][d]

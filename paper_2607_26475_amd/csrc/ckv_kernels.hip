@@ -673,11 +673,14 @@ __device__ __forceinline__ void split_block(int blk, int nsplit, int* unit, int*
 // One workgroup's part of k_select_attn: the selection of `unit`, then the
 // attention over its share of the rows or with its share of the heads.
 // COH: the scores and slots were stored by other workgroups of the same launch.
-template <int G, int HEADS, bool COH = false>
+// MERGE2 (HEADS 1, nsplit 2): the two shares merge through fs (attn_wg).
+template <int G, int HEADS, bool COH = false, bool MERGE2 = false>
 __device__ __forceinline__ void select_attn_part(const SelectArgs& sa, const AttnArgs& at,
                                                  int unit, int split, int nsplit,
                                                  uint32_t* lds, uint32_t* tmp,
-                                                 uint32_t* misc) {
+                                                 uint32_t* misc,
+                                                 const FusedSync* fs = nullptr) {
+  static_assert(!MERGE2 || HEADS == 1, "the merge joins row shares");
   static_assert(G % HEADS == 0, "whole heads per workgroup");
   constexpr int GA = G / HEADS;  // heads each workgroup attends with
   using Lds = SelAttnLds<GA>;
@@ -694,8 +697,13 @@ __device__ __forceinline__ void select_attn_part(const SelectArgs& sa, const Att
                                              (uint32_t)hi, false);
   __syncthreads();
   const int qh0 = (unit % sa.Hkv) * G + (HEADS > 1 ? split * GA : 0);
-  attn_wg<GA>(at, unit, LdsRows{share}, hi - lo, HEADS > 1 ? 0 : split, HEADS > 1 ? 1 : nsplit,
-              lds, lds + Lds::kQOff, qh0);
+  if constexpr (MERGE2)
+    attn_wg<GA, LdsRows, true>(at, unit, LdsRows{share}, hi - lo, split, 2, lds,
+                               lds + Lds::kQOff, qh0, nullptr, nullptr, 0, fs->merge + unit,
+                               fs->tag);
+  else
+    attn_wg<GA>(at, unit, LdsRows{share}, hi - lo, HEADS > 1 ? 0 : split,
+                HEADS > 1 ? 1 : nsplit, lds, lds + Lds::kQOff, qh0);
 }
 
 template <int G, int HEADS>
@@ -725,11 +733,10 @@ __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, A
 // for lower-indexed ones that never wait.  The wait is bounded all the same
 // (kFusedSpinLimit polls): a broken hand-over leaves the outputs undefined
 // but cannot hang the launch.
-constexpr uint32_t kFusedSpinLimit = 1u << 20;
-template <int G>
+template <int G, bool ROWS>
 __global__ __launch_bounds__(kFinishThreads) void k_critical(ScoreArgs sc, SelectArgs sa,
                                                              AttnArgs at, FusedSync fs, int nS) {
-  using Lds = SelAttnLds<G / 2>;
+  using Lds = SelAttnLds<ROWS ? G : G / 2>;
   static_assert(kHistBins + kHistScoreWaves * (kStageDwords + kFlushGroups * kStageRows) <=
                     Lds::kDwords,
                 "the scoring role's histogram, stages and score buffers fit");
@@ -757,7 +764,10 @@ __global__ __launch_bounds__(kFinishThreads) void k_critical(ScoreArgs sc, Selec
     __hip_atomic_store(f, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
-  select_attn_part<G, 2, true>(sa, at, unit, half, 1, lds, tmp, misc);
+  if constexpr (ROWS)
+    select_attn_part<G, 1, true, true>(sa, at, unit, half, 2, lds, tmp, misc, &fs);
+  else
+    select_attn_part<G, 2, true>(sa, at, unit, half, 1, lds, tmp, misc);
 }
 
 // Same-step over chunks (Sec. 2.2): sa is the chunk problem (one landmark
@@ -1805,14 +1815,14 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
 }
 
 template <int G>
-static const void* critical_kernel() {
-  return (const void*)k_critical<G>;
+static const void* critical_kernel(bool rows) {
+  return rows ? (const void*)k_critical<G, true> : (const void*)k_critical<G, false>;
 }
 
-int critical_blocks(int G, int units, int nwg) {
+int critical_blocks(int G, int units, int nwg, bool rows) {
   if (units < 8 || units % 8 || nwg < 8 || nwg % 8) return 0;
-  const void* fn = G == 2 ? critical_kernel<2>() : G == 4 ? critical_kernel<4>()
-                 : G == 8 ? critical_kernel<8>() : nullptr;
+  const void* fn = G == 2 ? critical_kernel<2>(rows) : G == 4 ? critical_kernel<4>(rows)
+                 : G == 8 ? critical_kernel<8>(rows) : nullptr;
   // every scoring workgroup resident at once, so that none waits for a
   // workgroup that waits for it
   if (!fn || nwg > resident_blocks(fn, kFinishThreads)) return 0;
@@ -1820,16 +1830,22 @@ int critical_blocks(int G, int units, int nwg) {
 }
 
 hipError_t launch_critical(const ScoreArgs& sc, const SelectArgs& sa, const AttnArgs& at,
-                           const FusedSync& fs, int G, int nwg, hipStream_t s) {
-  const int blocks = critical_blocks(G, sa.units, nwg);
-  if (!blocks || !sa.affine || sa.score_nwg != nwg || !sc.hist_part) return hipErrorInvalidValue;
+                           const FusedSync& fs, int G, int nwg, bool rows, hipStream_t s) {
+  const int blocks = critical_blocks(G, sa.units, nwg, rows);
+  if (!blocks || !sa.affine || sa.score_nwg != nwg || !sc.hist_part || (rows && !fs.merge) ||
+      (rows && !at.part))
+    return hipErrorInvalidValue;
   const dim3 grid(blocks), block(kFinishThreads);
+#define CKV_CRITICAL(GG)                                                                        \
+  rows ? launch_kernel(CKV_K_CRITICAL, k_critical<GG, true>, grid, block, s, sc, sa, at, fs, nwg) \
+       : launch_kernel(CKV_K_CRITICAL, k_critical<GG, false>, grid, block, s, sc, sa, at, fs, nwg)
   switch (G) {
-    case 2: launch_kernel(CKV_K_CRITICAL, k_critical<2>, grid, block, s, sc, sa, at, fs, nwg); break;
-    case 4: launch_kernel(CKV_K_CRITICAL, k_critical<4>, grid, block, s, sc, sa, at, fs, nwg); break;
-    case 8: launch_kernel(CKV_K_CRITICAL, k_critical<8>, grid, block, s, sc, sa, at, fs, nwg); break;
+    case 2: CKV_CRITICAL(2); break;
+    case 4: CKV_CRITICAL(4); break;
+    case 8: CKV_CRITICAL(8); break;
     default: return hipErrorInvalidValue;
   }
+#undef CKV_CRITICAL
   return launch_status();
 }
 

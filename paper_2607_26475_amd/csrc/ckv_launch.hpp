@@ -72,12 +72,14 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
                               int heads, hipStream_t s);
 // the same-step layer in one launch (k_critical): scoring on nwg workgroups
 // with XCD-affine ranges and slots (sa.affine set, sa.score_nwg = nwg), then
-// the head-halves selection and attention; 0 workgroups when the launch does
-// not apply (G odd or above 8, U or nwg not multiples of 8, or more scoring
-// workgroups than fit on the device at once).
-int critical_blocks(int G, int units, int nwg);
+// the selection and attention by two workgroups per unit, with half the
+// heads each or (rows) with half the rows each, merged in the launch through
+// fs.merge and at.part; 0 workgroups when the launch does not apply (G odd or
+// above 8, U or nwg not multiples of 8, or more scoring workgroups than fit on
+// the device at once).
+int critical_blocks(int G, int units, int nwg, bool rows);
 hipError_t launch_critical(const ScoreArgs& sc, const SelectArgs& sa, const AttnArgs& at,
-                           const FusedSync& fs, int G, int nwg, hipStream_t s);
+                           const FusedSync& fs, int G, int nwg, bool rows, hipStream_t s);
 // the same over chunks (sa: the chunk problem, k / chunk <= kFinishThreads;
 // e: the rows written as k_expand writes them; G even, k <= kSelAttnMaxShare)
 hipError_t launch_select_attn_chunks(const SelectArgs& sa, const AttnArgs& at,

@@ -33,7 +33,7 @@ def test_header_functions_are_exported():
 
 
 def test_abi_version_and_status_text():
-    assert ckv.abi_version() == ckv.ABI_VERSION == 8
+    assert ckv.abi_version() == ckv.ABI_VERSION == 9
     texts = {ckv.status_str(v) for v in STATUS.values()}
     assert len(texts) == len(STATUS)
     assert ckv.status_str(99) == "unknown status"
