@@ -317,3 +317,19 @@ def test_debug_mode_switch_without_a_gpu():
         assert call_score(empty) == 0
     finally:
         assert ckv._lib.ckv_set_debug(0) == 0
+
+
+def test_one_launch_modes_match_the_header():
+    """The one-launch setting's modes: the binding's constants are the
+    header's enum values, and every mode (and any other nonzero value, which
+    means row halves) is accepted without a GPU."""
+    text = open(os.path.join(os.path.dirname(__file__), "..", "include", "ckv.h")).read()
+    vals = dict(re.findall(r"(CKV_ONE_LAUNCH_\w+) = (\d+)", text))
+    assert vals == {"CKV_ONE_LAUNCH_OFF": "0", "CKV_ONE_LAUNCH_ROW_HALVES": "1",
+                    "CKV_ONE_LAUNCH_HEAD_HALVES": "2"}, vals
+    assert (ckv.ONE_LAUNCH_OFF, ckv.ONE_LAUNCH_ROW_HALVES, ckv.ONE_LAUNCH_HEAD_HALVES) == (0, 1, 2)
+    try:
+        for mode in (ckv.ONE_LAUNCH_OFF, ckv.ONE_LAUNCH_HEAD_HALVES, 7, False, True):
+            ckv.set_one_launch_same_step(mode)
+    finally:
+        ckv.set_one_launch_same_step(ckv.ONE_LAUNCH_ROW_HALVES)
