@@ -60,6 +60,7 @@ def _lens(w, seed):
     lens[0] = w.max_ctx
     lens[1] = 0
     lens[2] = min(w.k - 1, w.max_ctx)  # every position selected
+    lens[3] = 10  # row halves: the first takes all 10 rows, the second none
     return torch.tensor(lens, dtype=torch.int32)
 
 
