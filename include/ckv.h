@@ -579,13 +579,14 @@ int ckv_set_debug(int on);
  * merges the first's partial (handed over through a per-unit flag) into the
  * output.  Otherwise, or with this setting off, the call runs the scoring
  * launch, then the selection and attention launch, whose two workgroups per
- * unit attend over the whole set with half the heads each.
- *   on = CKV_ONE_LAUNCH_OFF: two launches.
- *   on = CKV_ONE_LAUNCH_HEAD_HALVES: one launch with that head-halves
- *        attention; the same bits as two launches.
- *   any other value: one launch with row halves (the default).  The index
- *        sets and counts are those of the other forms bit for bit; the
- *        outputs add the same terms in another order (fp32 rounding only).
+ * unit attend and merge the same way.
+ *   on = CKV_ONE_LAUNCH_OFF: two launches; the same bits as one launch.
+ *   on = CKV_ONE_LAUNCH_HEAD_HALVES: one launch (or, where it does not
+ *        apply, two) whose two workgroups per unit attend over the whole set
+ *        with half of the heads each.  The index sets and counts are those
+ *        of the other forms bit for bit; the outputs add the same terms in
+ *        another order (fp32 rounding only).
+ *   any other value: one launch with row halves (the default).
  * The setting is process-wide and for comparing the forms; calls already
  * launched keep their form. */
 enum { CKV_ONE_LAUNCH_OFF = 0, CKV_ONE_LAUNCH_ROW_HALVES = 1, CKV_ONE_LAUNCH_HEAD_HALVES = 2 };

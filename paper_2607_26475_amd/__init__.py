@@ -370,11 +370,12 @@ ONE_LAUNCH_OFF, ONE_LAUNCH_ROW_HALVES, ONE_LAUNCH_HEAD_HALVES = 0, 1, 2
 
 def set_one_launch_same_step(on) -> None:
     """Whether same-step calls run as one launch where that form applies
-    (process-wide).  False / ONE_LAUNCH_OFF: the scoring launch, then the
-    selection and attention launch with head halves.  ONE_LAUNCH_HEAD_HALVES:
-    one launch with that attention, the same bits as two launches.  True /
-    ONE_LAUNCH_ROW_HALVES (the default): one launch whose two workgroups per
-    unit attend over half the rows each and merge in the launch; the same
+    (process-wide).  True / ONE_LAUNCH_ROW_HALVES (the default): one launch
+    whose two workgroups per unit attend over half the rows each and merge in
+    the launch.  False / ONE_LAUNCH_OFF: the scoring launch, then the
+    selection and attention launch, attending the same way (the same bits).
+    ONE_LAUNCH_HEAD_HALVES: two workgroups per unit attending over the whole
+    set with half the heads each, in one launch where that applies; the same
     index sets, outputs within fp32 rounding of the other forms."""
     _check("ckv_set_one_launch_same_step", _lib.ckv_set_one_launch_same_step(int(on)))
 

@@ -1035,7 +1035,7 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
     AttnArgs at_ = attn_args(d, L, ws, q_att, k_src, v_src, idx_out, n_sel_out,
                              d.kv_stride, k, scale, out);
     int heads;
-    const int S = select_attn_splits(d, k, L, &heads);
+    int S = select_attn_splits(d, k, L, &heads);
     const int one = g_one_launch.load();
     // row halves need a partial per half in the attention partials
     const bool rows = one == CKV_ONE_LAUNCH_ROW_HALVES && L.chunks >= 2;
@@ -1050,10 +1050,21 @@ int ckv::critical_impl(const ckv_shape* shape, const uint16_t* q_att, const uint
     CKV_TRY_HIP(launch_score(sc, d.G, true, nwg, s), "score launch");
     if (S) {
       // each workgroup selects its unit's set and attends over its share of
-      // the rows, or over the whole set with its share of the heads
+      // the rows, or over the whole set with its share of the heads.  Two
+      // workgroups per unit attend over half of the rows each and merge in
+      // the launch, unless head halves are asked for (where they apply) or
+      // the layout has no merge flags.
+      const bool merge2 = (S == 2 || (S == 1 && heads == 2 && one != CKV_ONE_LAUNCH_HEAD_HALVES)) &&
+                          L.merge > 0 && L.chunks >= 2;
+      if (merge2) {
+        S = 2;
+        heads = 1;
+      }
       at_.chunks = S;
-      CKV_TRY_HIP(launch_select_attn(sa, at_, d.G, S, heads, s), "select-attention launch");
-      if (S > 1) CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
+      const FusedSync fs{nullptr, merge2 ? at<uint64_t>(ws, L.merge) : nullptr, next_fused_tag()};
+      CKV_TRY_HIP(launch_select_attn(sa, at_, d.G, S, heads, merge2 ? &fs : nullptr, s),
+                  "select-attention launch");
+      if (S > 1 && !merge2) CKV_TRY_HIP(launch_combine(at_, d.G, d.U, s), "combine launch");
     } else {
       if ((rc = run_select_tail(sa, d.U, s))) return rc;
       if ((rc = run_attention(at_, d, true, s))) return rc;

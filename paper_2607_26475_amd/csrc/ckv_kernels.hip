@@ -706,16 +706,17 @@ __device__ __forceinline__ void select_attn_part(const SelectArgs& sa, const Att
                 HEADS > 1 ? 1 : nsplit, lds, lds + Lds::kQOff, qh0);
 }
 
-template <int G, int HEADS>
+// MERGE2: two row shares that merge in the launch through fs (attn_wg).
+template <int G, int HEADS, bool MERGE2 = false>
 __global__ __launch_bounds__(kFinishThreads) void k_select_attn(SelectArgs sa, AttnArgs at,
-                                                                  int nsplit) {
+                                                                  int nsplit, FusedSync fs) {
   __shared__ __attribute__((aligned(16))) uint32_t lds[SelAttnLds<G / HEADS>::kDwords];
   __shared__ uint32_t tmp[kFinishThreads / 64 + 1];
   __shared__ uint32_t misc[8];
   int unit, split;
   split_block(blockIdx.x, HEADS > 1 ? HEADS : nsplit, &unit, &split);
   if (unit >= sa.units) return;  // uniform over the workgroup
-  select_attn_part<G, HEADS>(sa, at, unit, split, nsplit, lds, tmp, misc);
+  select_attn_part<G, HEADS, false, MERGE2>(sa, at, unit, split, nsplit, lds, tmp, misc, &fs);
 }
 
 // ---- the same-step layer in one launch ------------------------------------
@@ -1787,14 +1788,26 @@ hipError_t launch_dual_sel(const AttnArgs& at, const ScoreArgs& sc, const Select
 }
 
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
-                              int heads, hipStream_t s) {
+                              int heads, const FusedSync* merge, hipStream_t s) {
   if (nsplit < 1 || nsplit > kSelAttnMaxSplit) return hipErrorInvalidValue;
   if (heads != 1 && (heads != 2 || nsplit != 1 || G % 2)) return hipErrorInvalidValue;
+  if (merge && (heads != 1 || nsplit != 2 || !merge->merge || !at.part))
+    return hipErrorInvalidValue;
   const int per = heads > 1 ? heads : nsplit;  // workgroups per unit
   const int blocks = per == 1 ? sa.units : (sa.units + 7) / 8 * 8 * per;
   const dim3 grid(blocks), block(kFinishThreads);
-#define CKV_SA(g, hh) launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<g, hh>, grid, block, s, sa, at, nsplit)
-  if (heads == 1) {
+  const FusedSync fs = merge ? *merge : FusedSync{nullptr, nullptr, 0};
+#define CKV_SA(g, hh) launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<g, hh>, grid, block, s, sa, at, nsplit, fs)
+#define CKV_SAM(g) launch_kernel(CKV_K_SELECT_ATTN, k_select_attn<g, 1, true>, grid, block, s, sa, at, nsplit, fs)
+  if (merge) {
+    switch (G) {
+      case 1: CKV_SAM(1); break;
+      case 2: CKV_SAM(2); break;
+      case 4: CKV_SAM(4); break;
+      case 8: CKV_SAM(8); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else if (heads == 1) {
     switch (G) {
       case 1: CKV_SA(1, 1); break;
       case 2: CKV_SA(2, 1); break;
@@ -1811,6 +1824,7 @@ hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, i
     }
   }
 #undef CKV_SA
+#undef CKV_SAM
   return launch_status();
 }
 

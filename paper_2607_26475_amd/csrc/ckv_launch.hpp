@@ -67,9 +67,11 @@ hipError_t launch_attn(const AttnArgs& a, int G, bool indexed, int units, hipStr
 // same-step selection and attention in one launch: heads == 1, nsplit shares
 // of rows per unit (partials [U][nsplit][G] for k_combine when nsplit > 1);
 // heads == 2 (G even, nsplit 1), two workgroups per unit attending with half
-// the heads each over the whole set, outputs written directly
+// the heads each over the whole set, outputs written directly.  merge (heads
+// 1, nsplit 2 only): the two row shares merge in the launch through
+// merge->merge and at.part, written directly too (no k_combine)
 hipError_t launch_select_attn(const SelectArgs& sa, const AttnArgs& at, int G, int nsplit,
-                              int heads, hipStream_t s);
+                              int heads, const FusedSync* merge, hipStream_t s);
 // the same-step layer in one launch (k_critical): scoring on nwg workgroups
 // with XCD-affine ranges and slots (sa.affine set, sa.score_nwg = nwg), then
 // the selection and attention by two workgroups per unit, with half the

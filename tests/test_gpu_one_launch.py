@@ -6,12 +6,13 @@ k <= 2048), a same-step call scores, selects and attends in one launch, each
 unit's selection starting once its scores are handed over.  The selection
 is exact, so every index set and count must equal, bit for bit, those of the
 same call in two launches (scoring launch, then the selection and attention
-launch); the kernel profile shows which form ran.  With head halves the
-attention code is the two-launch form's, so the outputs must be equal too.
-With row halves (the default) each of a unit's two workgroups attends over
-half the rows with all heads and the second merges the first's partial in
-the launch: the same terms added in another order, so the outputs must agree
-within fp32 rounding (FORM_TOL) and repeat bit for bit.  The one-launch
+launch); the kernel profile shows which form ran.  By default both forms
+attend with row halves (each of a unit's two workgroups over half the rows
+with all heads, the second merging the first's partial inside the launch)
+in the same code, so the outputs must be equal too.  With head halves asked
+for, the one launch attends over the whole set with half the heads per
+workgroup: the same terms added in another order, so its outputs must agree
+with the row halves' within fp32 rounding (FORM_TOL) and repeat bit for bit.  The one-launch
 results are also checked against the oracle (Sec. 2.2 selection, Sec.
 5.3-5.4 attention).  The hand-over flags live in the workspace: a workspace
 filled with garbage, calls of other shapes in between, and graph replays
@@ -123,14 +124,14 @@ def test_one_launch_matches_two_launches_and_oracle(name, interleaved):
           {k: v[0] for k, v in two[3].items()}, flush=True)
     assert set(one[3]) == {"critical"}, one[3]
     assert set(heads[3]) == {"critical"}, heads[3]
-    assert "critical" not in two[3] and "select_attn" in two[3], two[3]
-    for a, b in zip(heads[:3], two[:3]):
+    assert "critical" not in two[3] and "select_attn" in two[3] and "combine" not in two[3], two[3]
+    for a, b in zip(one[:3], two[:3]):
         assert torch.equal(a, b)
-    diff = _same_sets_close_outputs(one, two)
+    diff = _same_sets_close_outputs(heads, two)
     again = _call(w, t, lens, ws, interleaved, ROWS)  # the flags were left clear
     for a, b in zip(one[:3], again[:3]):
         assert torch.equal(a, b)
-    print(f"  row halves against two launches: sets equal, outputs within {diff:.2e}", flush=True)
+    print(f"  head halves against row halves: sets equal, outputs within {diff:.2e}", flush=True)
     o = orc()
     so = o.shape(w.batch, w.q_heads, w.kv_heads, w.head_dim, w.max_ctx)
     lens_h = lens.cpu().numpy()
@@ -194,8 +195,8 @@ def test_one_launch_graph_replays():
 
 def test_one_launch_full_size_repeated():
     """Four Llama-8B layers (B16, 32 q / 8 KV heads, n 32768, k 2048) called
-    in turn 25 times through one workspace in each one-launch form: the head
-    halves bit-identical to the two-launch form of the same layer, the row
+    in turn 25 times through one workspace in each one-launch form: the row
+    halves bit-identical to the two-launch form of the same layer, the head
     halves with its index sets and within FORM_TOL of its outputs, and every
     repeat bit-identical to the form's first call."""
     dev = device()
@@ -204,12 +205,12 @@ def test_one_launch_full_size_repeated():
     ws = ckv.workspace(s, w.k, ckv.ENTRY_CRITICAL_KV_ATTN)
     layers = [synth.make_layer(w, seed=0, layer=l, device=dev) for l in range(w.layers)]
     ref = [_call(w, t, t["ctx_lens"], ws, False, OFF)[:3] for t in layers]
-    first = [_call(w, t, t["ctx_lens"], ws, False, ROWS)[:3] for t in layers]
+    first = [_call(w, t, t["ctx_lens"], ws, False, HEADS)[:3] for t in layers]
     for l in range(w.layers):
         _same_sets_close_outputs(first[l], ref[l])
     for it in range(25):
         for l, t in enumerate(layers):
-            for mode, want in ((ROWS, first[l]), (HEADS, ref[l])):
+            for mode, want in ((ROWS, ref[l]), (HEADS, first[l])):
                 got = _call(w, t, t["ctx_lens"], ws, False, mode)
                 assert set(got[3]) == {"critical"}, got[3]
                 for a, b in zip(got[:3], want):

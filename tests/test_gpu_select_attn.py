@@ -1,8 +1,10 @@
 """Same-step decode through the one-launch selection and attention (MI355X
 only): every workgroup selects its unit's set, then either attends over its
-share of the rows with all the group's heads (shares merged by the merge
-kernel when there are several) or, for an even group size with k <= 2048,
-over the whole set with half the heads, writing its outputs directly.
+share of the rows with all the group's heads, or, for an even group size with
+k <= 2048 when head halves are asked for, over the whole set with half the
+heads, writing its outputs directly.  Two shares (two workgroups per unit,
+the default wherever head halves would apply) merge inside the launch; more
+shares are merged by the merge kernel.
 Checked against the oracle: index sets under the near-tie rule, outputs
 within 2e-3 of the oracle's attention over the GPU's own set (and of the
 oracle's whole step when the sets agree), for head halves, 1, 2 and 4 row
@@ -31,22 +33,27 @@ def _log(*a):
 
 BASE = synth.WORKLOADS["llama8b_s"]
 # (name, workload changes, context lengths or None for the drawn ones, row
-# shares: 0 for the split by heads)
+# shares: 0 for the split by heads, whether head halves are asked for)
 CASES = [
-    ("k1024_heads", dict(k=1024), None, 0),
-    ("k2048_heads", dict(k=2048, max_ctx=8000, ctx_min=5000), None, 0),
-    ("k4096_2shares", dict(k=4096, max_ctx=20000, ctx_min=15000), None, 2),
-    ("k8192_4shares", dict(k=8192, max_ctx=40000, ctx_min=30000, batch=1), None, 4),
-    ("short_and_empty", dict(k=1024, batch=3), [5000, 700, 0], 0),
-    ("g8", dict(k=1024, q_heads=64), None, 0),
-    ("g2", dict(k=1024, q_heads=16), None, 0),
-    ("g1", dict(k=1024, q_heads=8), None, 2),
-    ("one_share", dict(k=256), None, 1),
+    ("k1024_rows", dict(k=1024), None, 2, False),
+    ("k1024_heads", dict(k=1024), None, 0, True),
+    ("k2048_rows", dict(k=2048, max_ctx=8000, ctx_min=5000), None, 2, False),
+    ("k2048_heads", dict(k=2048, max_ctx=8000, ctx_min=5000), None, 0, True),
+    ("k4096_2shares", dict(k=4096, max_ctx=20000, ctx_min=15000), None, 2, False),
+    ("k8192_4shares", dict(k=8192, max_ctx=40000, ctx_min=30000, batch=1), None, 4, False),
+    ("short_and_empty", dict(k=1024, batch=3), [5000, 700, 0], 2, False),
+    ("short_and_empty_heads", dict(k=1024, batch=3), [5000, 700, 0], 0, True),
+    ("tiny_share", dict(k=1024, batch=3), [5000, 10, 0], 2, False),
+    ("g8", dict(k=1024, q_heads=64), None, 2, False),
+    ("g8_heads", dict(k=1024, q_heads=64), None, 0, True),
+    ("g2", dict(k=1024, q_heads=16), None, 2, False),
+    ("g1", dict(k=1024, q_heads=8), None, 2, False),
+    ("one_share", dict(k=256), None, 1, False),
 ]
 
 
-@pytest.mark.parametrize("name,changes,lens,shares", CASES, ids=[c[0] for c in CASES])
-def test_select_attn_matches_oracle(name, changes, lens, shares):
+@pytest.mark.parametrize("name,changes,lens,shares,heads", CASES, ids=[c[0] for c in CASES])
+def test_select_attn_matches_oracle(name, changes, lens, shares, heads):
     _log("select+attention", name)
     dev = device()
     w = dataclasses.replace(BASE, name=f"selattn_{name}", **changes)
@@ -54,11 +61,15 @@ def test_select_attn_matches_oracle(name, changes, lens, shares):
     if lens is not None:
         t["ctx_lens"] = torch.tensor(lens, dtype=torch.int32, device=dev)
     run = Run(w, t["ctx_lens"], dev)
-    ckv.profile_begin()
-    run.same_step(t["q"], t["q_sel"], t["k"], t["k"], t["v"], ckv.SRC_DEVICE)
-    kernels = ckv.profile_end()
+    ckv.set_one_launch_same_step(ckv.ONE_LAUNCH_HEAD_HALVES if heads else ckv.ONE_LAUNCH_ROW_HALVES)
+    try:
+        ckv.profile_begin()
+        run.same_step(t["q"], t["q_sel"], t["k"], t["k"], t["v"], ckv.SRC_DEVICE)
+        kernels = ckv.profile_end()
+    finally:
+        ckv.set_one_launch_same_step(ckv.ONE_LAUNCH_ROW_HALVES)
     assert "select_attn" in kernels and "attn" not in kernels, kernels
-    assert ("combine" in kernels) == (shares > 1), kernels
+    assert ("combine" in kernels) == (shares > 2), kernels
     g_idx, g_nsel, g_out = run.host()
     lens_np = t["ctx_lens"].cpu().numpy()
     q_att, q_sel, K, V = u16(t["q"]), u16(t["q_sel"]), u16(t["k"]), u16(t["v"])
